@@ -1,0 +1,21 @@
+"""fp64 CPU oracle for the LoGo attention layer forward (test infrastructure).
+
+Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
+leg use this package.  The HIP library never loads it and shares no code
+with it.  The arithmetic lives in ``logo_oracle.c`` (plain C, fp64, OpenMP);
+this module only builds that file with gcc and marshals numpy arrays.
+"""
+from .oracle import (  # noqa: F401
+    SEL_RATIO,
+    SEL_THRESHOLD,
+    attn_rows,
+    build,
+    contextnorm,
+    fuse,
+    library_path,
+    logo_fwd,
+    num_threads,
+    select,
+    set_num_threads,
+    thresholds,
+)

@@ -1,0 +1,332 @@
+/*
+ * logo_oracle.c -- plain fp64 CPU oracle for the forward pass of one LoGo
+ * attention layer (LoGo: Token-Level Dynamic Local-Global Attention).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the definition the GPU path is
+ * checked against.  It shares no code with the HIP library: it is compiled by
+ * gcc into its own shared object and is called only by the tests, by the
+ * package smoke check and by the benchmark's CPU-baseline leg.  Nothing on
+ * the product path may load it.
+ *
+ * Every function writes out a plain definition from the paper, in double
+ * precision, without tiling, online rescaling or any reordering beyond what
+ * the definition states:
+ *
+ *   - softmax attention over a context set C_t           (Sec. 3.1, Eq. attention)
+ *   - global context {1..t}, local context {max(1,t-w+1)..t}
+ *                                                         (Sec. 3.1, below Eq. attention)
+ *   - hard routing z_t = [p_t > b_th], strict, shared by all heads
+ *                                                         (Sec. 3.2, Eq. gate-routing;
+ *                                                          Sec. 3.1, Eq. token-routing)
+ *   - query-sparse global branch: global rows only for selected tokens,
+ *     keys/values dense                                   (Sec. 3.2, Eq. query-sparse-global)
+ *   - ContextNorm: head-wise RMSNorm of each branch       (Sec. 3.2, Eq. contextnorm)
+ *   - output fusion (1-p) oL + p oG for selected tokens,
+ *     oL otherwise                                        (Sec. 3.2, Eq. output-fusion)
+ *
+ * Readings where the paper is silent (each also listed in the design notes):
+ *   - positions are 0-based: key j is visible to query i iff j <= i (global)
+ *     or i-w < j <= i (local); the local context holds exactly min(i+1, w)
+ *     keys, the query itself included.
+ *   - a target ratio rho becomes a per-sequence threshold: k = floor(rho*T)
+ *     in IEEE double; thr = -inf if k == T, else the (k+1)-th largest gate
+ *     value of the sequence (an input value, no interpolation).  A zero
+ *     threshold is reported as +0.0.
+ *   - GQA: query head h reads key/value head floor(h / (Hq/Hkv)).
+ *   - ContextNorm: o / sqrt(mean_c o_c^2 + eps) * g per (token, head), with a
+ *     per-branch gain g[Hq][d] (1 when absent).
+ *   - the fusion weight is the fp32 gate value p, widened to double.
+ *
+ * Inputs: bf16 tensors are raw uint16 bit patterns, widened exactly.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_SEL_THRESHOLD 0
+#define ORACLE_SEL_RATIO 1
+
+static double bf16_to_double(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* Sequence that owns packed token t: largest b with cu[b] <= t < cu[b+1]. */
+static int owner_sequence(const int32_t *cu, int B, int64_t t)
+{
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) / 2;
+        if ((int64_t)cu[mid] <= t)
+            lo = mid;
+        else
+            hi = mid - 1;
+    }
+    /* skip empty sequences that start at the same offset */
+    while (lo + 1 < B && (int64_t)cu[lo + 1] <= t)
+        lo++;
+    return lo;
+}
+
+static int cmp_float_ascending(const void *a, const void *b)
+{
+    float x = *(const float *)a, y = *(const float *)b;
+    return (x < y) ? -1 : (x > y) ? 1 : 0;
+}
+
+/*
+ * Per-sequence threshold b_th (Sec. 3.2, Eq. gate-routing).
+ * Threshold mode: every sequence uses `threshold`.
+ * Ratio mode: the order statistic described in the header.
+ */
+void oracle_thresholds(const float *gate, const int32_t *cu, int B, int mode,
+                       float threshold, double ratio, float *thr_out)
+{
+    for (int b = 0; b < B; b++) {
+        if (mode == ORACLE_SEL_THRESHOLD) {
+            thr_out[b] = threshold;
+            continue;
+        }
+        int64_t T = (int64_t)cu[b + 1] - cu[b];
+        int64_t k = (int64_t)floor(ratio * (double)T);
+        if (k >= T) {
+            thr_out[b] = -INFINITY;
+            continue;
+        }
+        float *s = (float *)malloc((size_t)T * sizeof(float));
+        memcpy(s, gate + cu[b], (size_t)T * sizeof(float));
+        qsort(s, (size_t)T, sizeof(float), cmp_float_ascending);
+        float thr = s[T - k - 1];
+        if (thr == 0.0f)
+            thr = 0.0f; /* -0.0 -> +0.0 */
+        thr_out[b] = thr;
+        free(s);
+    }
+}
+
+/*
+ * Hard routing (Sec. 3.2, Eq. gate-routing): z_t = [p_t > thr_b], compared in
+ * fp32, selected tokens kept in ascending order.  Writes sel_idx (packed
+ * token index), cu_sel[B+1] (selections before each sequence), tok2sel[N]
+ * (rank or -1).  Returns the number of selected tokens.
+ */
+int64_t oracle_select(const float *gate, const int32_t *cu, int B, const float *thr,
+                      int32_t *sel_idx, int32_t *cu_sel, int32_t *tok2sel)
+{
+    int64_t n = 0;
+    for (int b = 0; b < B; b++) {
+        cu_sel[b] = (int32_t)n;
+        for (int64_t t = cu[b]; t < cu[b + 1]; t++) {
+            if (gate[t] > thr[b]) {
+                if (sel_idx)
+                    sel_idx[n] = (int32_t)t;
+                if (tok2sel)
+                    tok2sel[t] = (int32_t)n;
+                n++;
+            } else if (tok2sel) {
+                tok2sel[t] = -1;
+            }
+        }
+    }
+    cu_sel[B] = (int32_t)n;
+    return n;
+}
+
+/*
+ * Softmax attention for a list of query rows (Sec. 3.1, Eq. attention).
+ * rows[r] is a packed token index; out is [n_rows][Hq][d].
+ * window <= 0 : global context, keys 0..pos
+ * window >= 1 : local context, keys max(0, pos-window+1)..pos
+ * Two passes per (row, head): scores and their maximum, then the weighted
+ * sum of values divided by the sum of weights.
+ */
+void oracle_attn_rows(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                      int Hq, int Hkv, int d, const int32_t *cu, int B,
+                      const int32_t *rows, int64_t n_rows, int window, double scale,
+                      double *out)
+{
+    const int G = Hq / Hkv;
+    int64_t max_T = 0;
+    for (int b = 0; b < B; b++)
+        if ((int64_t)cu[b + 1] - cu[b] > max_T)
+            max_T = (int64_t)cu[b + 1] - cu[b];
+
+#pragma omp parallel
+    {
+        double *s = (double *)malloc((size_t)(max_T > 0 ? max_T : 1) * sizeof(double));
+        double *qd = (double *)malloc((size_t)d * sizeof(double));
+        double *acc = (double *)malloc((size_t)d * sizeof(double));
+#pragma omp for schedule(dynamic, 4)
+        for (int64_t job = 0; job < n_rows * Hq; job++) {
+            int64_t r = job / Hq;
+            int h = (int)(job % Hq);
+            int hk = h / G;
+            int64_t t = rows[r];
+            int b = owner_sequence(cu, B, t);
+            int64_t base = cu[b];
+            int64_t pos = t - base;
+            int64_t lo = (window >= 1) ? (pos - window + 1 > 0 ? pos - window + 1 : 0) : 0;
+            int64_t nk = pos - lo + 1;
+
+            for (int c = 0; c < d; c++)
+                qd[c] = bf16_to_double(q[(t * Hq + h) * (int64_t)d + c]);
+
+            double m = -INFINITY;
+            for (int64_t j = 0; j < nk; j++) {
+                const uint16_t *kr = k + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                double dot = 0.0;
+                for (int c = 0; c < d; c++)
+                    dot += qd[c] * bf16_to_double(kr[c]);
+                s[j] = scale * dot;
+                if (s[j] > m)
+                    m = s[j];
+            }
+
+            double den = 0.0;
+            for (int c = 0; c < d; c++)
+                acc[c] = 0.0;
+            for (int64_t j = 0; j < nk; j++) {
+                double e = exp(s[j] - m);
+                const uint16_t *vr = v + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                den += e;
+                for (int c = 0; c < d; c++)
+                    acc[c] += e * bf16_to_double(vr[c]);
+            }
+            double *o = out + (r * Hq + h) * (int64_t)d;
+            for (int c = 0; c < d; c++)
+                o[c] = acc[c] / den;
+        }
+        free(s);
+        free(qd);
+        free(acc);
+    }
+}
+
+/*
+ * ContextNorm (Sec. 3.2, Eq. contextnorm): head-wise RMSNorm, in place on
+ * o[n_rows][Hq][d].  gain is [Hq][d] (NULL means 1).
+ */
+void oracle_contextnorm(double *o, int64_t n_rows, int Hq, int d, const float *gain,
+                        double eps)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t job = 0; job < n_rows * Hq; job++) {
+        int h = (int)(job % Hq);
+        double *row = o + job * (int64_t)d;
+        double ss = 0.0;
+        for (int c = 0; c < d; c++)
+            ss += row[c] * row[c];
+        double inv = 1.0 / sqrt(ss / (double)d + eps);
+        for (int c = 0; c < d; c++) {
+            double g = gain ? (double)gain[h * d + c] : 1.0;
+            row[c] = row[c] * inv * g;
+        }
+    }
+}
+
+/*
+ * Output fusion (Sec. 3.2, Eq. output-fusion).  ol is [N][Hq][d] (all
+ * tokens), og is [n_sel][Hq][d] (compact, rank order); out is [N][Hq][d].
+ */
+void oracle_fuse(const double *ol, const double *og, const float *gate,
+                 const int32_t *tok2sel, int64_t N, int Hq, int d, double *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < N; t++) {
+        const int64_t row = (int64_t)Hq * d;
+        const double *l = ol + t * row;
+        double *o = out + t * row;
+        int32_t r = tok2sel[t];
+        if (r < 0) {
+            for (int64_t e = 0; e < row; e++)
+                o[e] = l[e];
+        } else {
+            double p = (double)gate[t];
+            const double *g = og + (int64_t)r * row;
+            for (int64_t e = 0; e < row; e++)
+                o[e] = (1.0 - p) * l[e] + p * g[e];
+        }
+    }
+}
+
+/*
+ * The whole layer.  q_g/k_g/v_g may be NULL (identity branch transform:
+ * the global branch reads the local tensors, Sec. 3.2, Eq. branch-transform
+ * at initialisation).  apply_norm = 0 skips ContextNorm (raw fusion, a
+ * diagnostic).  Outputs (all caller-allocated):
+ *   thr_out[B], sel_idx[N], cu_sel[B+1], tok2sel[N],
+ *   o_local[N][Hq][d]  (raw local branch),
+ *   o_global[N][Hq][d] (raw global branch, compact: first n_sel rows used),
+ *   out[N][Hq][d]      (fused output).
+ * Returns n_sel.
+ */
+int64_t oracle_logo_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        const uint16_t *q_g, const uint16_t *k_g, const uint16_t *v_g,
+                        const float *gate, const int32_t *cu, int B, int Hq, int Hkv,
+                        int d, int window, double scale, int mode, float threshold,
+                        double ratio, const float *gain_local, const float *gain_global,
+                        double eps, int apply_norm, float *thr_out, int32_t *sel_idx,
+                        int32_t *cu_sel, int32_t *tok2sel, double *o_local,
+                        double *o_global, double *out)
+{
+    const int64_t N = cu[B];
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    if (!q_g)
+        q_g = q;
+    if (!k_g)
+        k_g = k;
+    if (!v_g)
+        v_g = v;
+
+    oracle_thresholds(gate, cu, B, mode, threshold, ratio, thr_out);
+    int64_t n_sel = oracle_select(gate, cu, B, thr_out, sel_idx, cu_sel, tok2sel);
+
+    int32_t *all = (int32_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int32_t));
+    for (int64_t t = 0; t < N; t++)
+        all[t] = (int32_t)t;
+    oracle_attn_rows(q, k, v, Hq, Hkv, d, cu, B, all, N, window, scale, o_local);
+    free(all);
+    oracle_attn_rows(q_g, k_g, v_g, Hq, Hkv, d, cu, B, sel_idx, n_sel, 0, scale, o_global);
+
+    const int64_t row = (int64_t)Hq * d;
+    double *nl = (double *)malloc((size_t)(N > 0 ? N : 1) * row * sizeof(double));
+    double *ng = (double *)malloc((size_t)(n_sel > 0 ? n_sel : 1) * row * sizeof(double));
+    memcpy(nl, o_local, (size_t)N * row * sizeof(double));
+    memcpy(ng, o_global, (size_t)n_sel * row * sizeof(double));
+    if (apply_norm) {
+        oracle_contextnorm(nl, N, Hq, d, gain_local, eps);
+        oracle_contextnorm(ng, n_sel, Hq, d, gain_global, eps);
+    }
+    oracle_fuse(nl, ng, gate, tok2sel, N, Hq, d, out);
+    free(nl);
+    free(ng);
+    return n_sel;
+}

@@ -1,0 +1,166 @@
+"""ctypes marshalling for the C oracle (``logo_oracle.c``).
+
+Test infrastructure: see the package docstring.  Every function here converts
+numpy arguments and calls one C function; none does arithmetic of its own.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Dict, Optional
+
+import numpy as np
+
+SEL_THRESHOLD = 0
+SEL_RATIO = 1
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "logo_oracle.c")
+_LIB = os.path.join(_HERE, "liblogo_oracle.so")
+_lib = None
+
+
+def library_path() -> str:
+    return _LIB
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, IEEE semantics, no FMA contraction)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp"
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+               "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    override = os.environ.get("LOGO_ORACLE_LIB")  # mutation tests load a planted variant
+    if override:
+        lib = ctypes.CDLL(override)
+    else:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32, i64, f32, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+    lib.oracle_num_threads.restype = i32
+    lib.oracle_set_num_threads.argtypes = [i32]
+    lib.oracle_thresholds.argtypes = [P, P, i32, i32, f32, f64, P]
+    lib.oracle_select.argtypes = [P, P, i32, P, P, P, P]
+    lib.oracle_select.restype = i64
+    lib.oracle_attn_rows.argtypes = [P, P, P, i32, i32, i32, P, i32, P, i64, i32, f64, P]
+    lib.oracle_contextnorm.argtypes = [P, i64, i32, i32, P, f64]
+    lib.oracle_fuse.argtypes = [P, P, P, P, i64, i32, i32, P]
+    lib.oracle_logo_fwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64,
+                                    i32, f32, f64, P, P, f64, i32, P, P, P, P, P, P, P]
+    lib.oracle_logo_fwd.restype = i64
+    _lib = lib
+    return lib
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    _load().oracle_set_num_threads(int(n))
+
+
+def thresholds(gate, cu_seqlens, mode: int, threshold: float = 0.0, ratio: float = 0.0):
+    gate, cu = _c(gate, np.float32), _c(cu_seqlens, np.int32)
+    B = cu.size - 1
+    thr = np.empty(B, dtype=np.float32)
+    _load().oracle_thresholds(_ptr(gate), _ptr(cu), B, mode, threshold, ratio, _ptr(thr))
+    return thr
+
+
+def select(gate, cu_seqlens, thr):
+    gate, cu, thr = _c(gate, np.float32), _c(cu_seqlens, np.int32), _c(thr, np.float32)
+    B = cu.size - 1
+    N = int(cu[-1])
+    sel = np.empty(max(N, 1), dtype=np.int32)
+    cu_sel = np.empty(B + 1, dtype=np.int32)
+    tok2sel = np.empty(max(N, 1), dtype=np.int32)
+    n = _load().oracle_select(_ptr(gate), _ptr(cu), B, _ptr(thr), _ptr(sel), _ptr(cu_sel),
+                              _ptr(tok2sel))
+    return sel[:n].copy(), cu_sel, tok2sel[:N].copy()
+
+
+def attn_rows(q, k, v, cu_seqlens, rows, window: int, scale: float = 0.0):
+    """fp64 attention rows: [len(rows), Hq, d].  window <= 0 means global."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    cu, rows = _c(cu_seqlens, np.int32), _c(rows, np.int32)
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    if scale <= 0:
+        scale = 1.0 / np.sqrt(d)
+    out = np.empty((rows.size, Hq, d), dtype=np.float64)
+    _load().oracle_attn_rows(_ptr(q), _ptr(k), _ptr(v), Hq, Hkv, d, _ptr(cu), cu.size - 1,
+                             _ptr(rows), rows.size, int(window), float(scale), _ptr(out))
+    return out
+
+
+def contextnorm(o, gain=None, eps: float = 1e-6):
+    o = np.array(o, dtype=np.float64, copy=True, order="C")
+    n, Hq, d = o.shape
+    _load().oracle_contextnorm(_ptr(o), n, Hq, d, _ptr(_c(gain, np.float32)), eps)
+    return o
+
+
+def fuse(ol, og, gate, tok2sel):
+    ol, og = _c(ol, np.float64), _c(og, np.float64)
+    gate, tok2sel = _c(gate, np.float32), _c(tok2sel, np.int32)
+    N, Hq, d = ol.shape
+    if og.size == 0:
+        og = np.zeros((1, Hq, d))
+    out = np.empty_like(ol)
+    _load().oracle_fuse(_ptr(ol), _ptr(og), _ptr(gate), _ptr(tok2sel), N, Hq, d, _ptr(out))
+    return out
+
+
+def logo_fwd(q, k, v, gate, cu_seqlens, window: int, *, ratio: Optional[float] = None,
+             threshold: Optional[float] = None, q_g=None, k_g=None, v_g=None,
+             gain_local=None, gain_global=None, eps: float = 1e-6, apply_norm: bool = True,
+             scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """The whole layer in fp64.  Exactly one of ``ratio``/``threshold`` is given."""
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    q_g, k_g, v_g = _c(q_g, np.uint16), _c(k_g, np.uint16), _c(v_g, np.uint16)
+    gate, cu = _c(gate, np.float32), _c(cu_seqlens, np.int32)
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    B = cu.size - 1
+    mode = SEL_RATIO if ratio is not None else SEL_THRESHOLD
+    thr = np.empty(B, dtype=np.float32)
+    sel = np.empty(max(N, 1), dtype=np.int32)
+    cu_sel = np.empty(B + 1, dtype=np.int32)
+    tok2sel = np.empty(max(N, 1), dtype=np.int32)
+    ol = np.empty((max(N, 1), Hq, d), dtype=np.float64)
+    og = np.empty((max(N, 1), Hq, d), dtype=np.float64)
+    out = np.empty((max(N, 1), Hq, d), dtype=np.float64)
+    n = _load().oracle_logo_fwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g), _ptr(gate), _ptr(cu), B,
+        Hq, Hkv, d, int(window), float(scale), mode,
+        float(threshold if threshold is not None else 0.0),
+        float(ratio if ratio is not None else 0.0),
+        _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)), float(eps),
+        1 if apply_norm else 0, _ptr(thr), _ptr(sel), _ptr(cu_sel), _ptr(tok2sel), _ptr(ol),
+        _ptr(og), _ptr(out))
+    return dict(thr=thr, sel_idx=sel[:n].copy(), cu_sel=cu_sel, tok2sel=tok2sel[:N].copy(),
+                o_local=ol[:N], o_global=og[:n].copy(), out=out[:N], n_sel=int(n))

@@ -1,0 +1,60 @@
+"""Planted mistakes in the oracle must fail its pins (CPU only).
+
+Each mutation below is a plausible slip in the C oracle (an off-by-one, a
+wrong index, a swapped weight, a dropped term).  The test compiles a mutated
+copy of ``oracle/logo_oracle.c`` into a temporary library, runs the pin suite
+against it in a subprocess and requires that suite to fail.  The real oracle
+is never modified.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "logo_oracle.c")
+
+MUTATIONS = {
+    "window_w_plus_1_keys": ("pos - window + 1 > 0 ? pos - window + 1 : 0",
+                             "pos - window > 0 ? pos - window : 0"),
+    "gate_ge_instead_of_gt": ("if (gate[t] > thr[b])", "if (gate[t] >= thr[b])"),
+    "threshold_index_off_by_one": ("float thr = s[T - k - 1];", "float thr = s[T - k];"),
+    "ratio_ceil": ("(int64_t)floor(ratio * (double)T)", "(int64_t)ceil(ratio * (double)T)"),
+    "gqa_modulo_mapping": ("int hk = h / G;", "int hk = h % Hkv;"),
+    "scale_dropped": ("s[j] = scale * dot;", "s[j] = dot;"),
+    "values_read_from_keys": ("const uint16_t *vr = v + ", "const uint16_t *vr = k + "),
+    "softmax_not_normalised": ("o[c] = acc[c] / den;", "o[c] = acc[c] / (double)nk;"),
+    "norm_eps_outside_sqrt": ("1.0 / sqrt(ss / (double)d + eps)", "1.0 / (sqrt(ss / (double)d) + eps)"),
+    "norm_sum_not_mean": ("1.0 / sqrt(ss / (double)d + eps)", "1.0 / sqrt(ss + eps)"),
+    "norm_gain_ignores_head": ("gain[h * d + c]", "gain[c]"),
+    "fusion_weights_swapped": ("o[e] = (1.0 - p) * l[e] + p * g[e];",
+                               "o[e] = p * l[e] + (1.0 - p) * g[e];"),
+    "unselected_not_normalised": ("oracle_contextnorm(nl, N, Hq, d, gain_local, eps);", ""),
+    "global_branch_reads_local_tensors": (
+        "oracle_attn_rows(q_g, k_g, v_g, Hq, Hkv, d, cu, B, sel_idx",
+        "oracle_attn_rows(q, k, v, Hq, Hkv, d, cu, B, sel_idx"),
+    "global_branch_windowed": ("sel_idx, n_sel, 0, scale, o_global", "sel_idx, n_sel, window, scale, o_global"),
+    "varlen_leak_into_previous_sequence": (
+        "int64_t lo = (window >= 1) ? (pos - window + 1 > 0 ? pos - window + 1 : 0) : 0;",
+        "int64_t lo = (window >= 1) ? (pos - window + 1 > 0 ? pos - window + 1 : 0) : -base;"),
+    "tok2sel_rank_off_by_one": ("tok2sel[t] = (int32_t)n;", "tok2sel[t] = (int32_t)n + 1;"),
+    "cu_sel_not_prefix": ("cu_sel[b] = (int32_t)n;", "cu_sel[b] = 0;"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_fails_pins(name, tmp_path):
+    old, new = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique/present: {old!r}"
+    mutated = tmp_path / "mut.c"
+    mutated.write_text(src.replace(old, new))
+    lib = tmp_path / "libmut.so"
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+                    "-ffp-contract=off", "-o", str(lib), str(mutated), "-lm"], check=True)
+    env = dict(os.environ, LOGO_ORACLE_LIB=str(lib), OMP_NUM_THREADS="2")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       env=env, cwd=ROOT, capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"pins did not catch mutation {name}:\n{r.stdout[-2000:]}"

@@ -1,0 +1,357 @@
+"""Pins for the fp64 oracle (CPU only).
+
+The oracle is the definition the GPU path is checked against, so it is pinned
+here to things other than itself: a hand-derived example (tests/golden),
+closed forms, invariants the paper states, and an independent numpy brute
+force on tiny inputs that builds the full score matrix with explicit masks.
+Each test names the passage it follows.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def bf16(x):
+    """Exact bf16 bits for values that are representable (asserted)."""
+    x = np.asarray(x, dtype=np.float32)
+    b = synth.bf16_bits_from_f32(x).reshape(x.shape)
+    assert np.array_equal(synth.f32_from_bf16_bits(b).reshape(x.shape), x), "not bf16-exact"
+    return b
+
+
+def wide(b):
+    return synth.f32_from_bf16_bits(b).reshape(b.shape).astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Independent brute force (numpy, full T x T score matrix, explicit masks).
+# ---------------------------------------------------------------------------
+def brute_layer(q, k, v, gate, seqlens, window, *, ratio=None, threshold=None,
+                q_g=None, k_g=None, v_g=None, gain_l=None, gain_g=None, eps=1e-6,
+                scale=None):
+    qf, kf, vf = wide(q), wide(k), wide(v)
+    qg = wide(q_g) if q_g is not None else qf
+    kg = wide(k_g) if k_g is not None else kf
+    vg = wide(v_g) if v_g is not None else vf
+    N, Hq, d = qf.shape
+    Hkv = kf.shape[1]
+    G = Hq // Hkv
+    sc = 1.0 / math.sqrt(d) if scale is None else scale
+    heads = np.arange(Hq) // G
+    ol = np.zeros((N, Hq, d))
+    og_full = np.zeros((N, Hq, d))
+    selected = np.zeros(N, dtype=bool)
+    thr_list = []
+    start = 0
+    for T in seqlens:
+        sl = slice(start, start + T)
+        p = gate[sl]
+        if ratio is not None:
+            kk = math.floor(ratio * T)
+            thr = -np.inf if kk >= T else np.sort(p)[T - kk - 1]
+        else:
+            thr = threshold
+        thr_list.append(thr)
+        if T == 0:
+            continue
+        selected[sl] = np.array([p[i] > np.float32(thr) for i in range(T)], dtype=bool)
+        i = np.arange(T)[:, None]
+        j = np.arange(T)[None, :]
+        causal = j <= i
+        local = causal & (j > i - window)
+        for h in range(Hq):
+            for (Q, K, V, mask, dst) in ((qf, kf, vf, local, ol), (qg, kg, vg, causal, og_full)):
+                S = sc * (Q[sl, h, :] @ K[sl, heads[h], :].T)
+                S = np.where(mask, S, -np.inf)
+                W = np.exp(S - S.max(axis=1, keepdims=True))
+                W = W / W.sum(axis=1, keepdims=True)
+                dst[sl, h, :] = W @ V[sl, heads[h], :]
+        start += T
+
+    def rms(o, g):
+        r = np.sqrt((o ** 2).mean(axis=-1, keepdims=True) + eps)
+        return o / r * (1.0 if g is None else g.astype(np.float64)[None])
+
+    nl, ng = rms(ol, gain_l), rms(og_full, gain_g)
+    pw = gate.astype(np.float64)[:, None, None]
+    out = np.where(selected[:, None, None], (1 - pw) * nl + pw * ng, nl)
+    sel_idx = np.nonzero(selected)[0]
+    return dict(o_local=ol, o_global=og_full[sel_idx], out=out, sel_idx=sel_idx,
+                thr=np.array(thr_list, dtype=np.float32), selected=selected)
+
+
+def test_hand_example_threshold(oracle_lib):
+    """Hand-derived T=3 example (tests/golden/hand_t3_d4.json), threshold mode."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_t3_d4.json")))
+    inp = g["inputs"]
+    q = bf16(np.array(inp["q"], np.float32)[:, None, :])
+    k = bf16(np.array(inp["k"], np.float32)[:, None, :])
+    v = bf16(np.array(inp["v"], np.float32)[:, None, :])
+    gate = np.array(inp["gate"], np.float32)
+    cu = np.array([0, 3], np.int32)
+    r = oracle_lib.logo_fwd(q, k, v, gate, cu, inp["window"], threshold=0.5, eps=inp["eps"])
+    e = g["threshold_0.5"]
+    assert r["sel_idx"].tolist() == e["sel_idx"]
+    assert r["cu_sel"].tolist() == e["cu_sel"]
+    assert r["tok2sel"].tolist() == e["tok2sel"]
+    np.testing.assert_allclose(r["o_local"][:, 0, :], e["o_local"], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(r["o_global"][:, 0, :], e["o_global"], rtol=0, atol=1e-14)
+    np.testing.assert_allclose(r["out"][:, 0, :], e["out"], rtol=0, atol=1e-14)
+
+
+def test_hand_example_ratio(oracle_lib):
+    """Same example in ratio mode: strict '>' leaves the tie at the threshold out."""
+    g = json.load(open(os.path.join(GOLDEN, "hand_t3_d4.json")))
+    inp = g["inputs"]
+    q = bf16(np.array(inp["q"], np.float32)[:, None, :])
+    k = bf16(np.array(inp["k"], np.float32)[:, None, :])
+    v = bf16(np.array(inp["v"], np.float32)[:, None, :])
+    gate = np.array(inp["gate"], np.float32)
+    cu = np.array([0, 3], np.int32)
+    r = oracle_lib.logo_fwd(q, k, v, gate, cu, inp["window"], ratio=0.5, eps=inp["eps"])
+    e = g["ratio_0.5"]
+    assert float(r["thr"][0]) == e["thr"]
+    assert r["sel_idx"].tolist() == e["sel_idx"]
+    assert r["cu_sel"].tolist() == e["cu_sel"]
+    assert r["tok2sel"].tolist() == e["tok2sel"]
+    np.testing.assert_allclose(r["out"][:, 0, :], e["out"], rtol=0, atol=1e-14)
+
+
+def test_contextnorm_hand(oracle_lib):
+    """Eq. contextnorm: (3,4) has rms sqrt(12.5), so it maps to (3,4)/sqrt(12.5)."""
+    o = np.array([[[3.0, 4.0]]])
+    r = oracle_lib.contextnorm(o, eps=0.0)
+    np.testing.assert_allclose(r[0, 0], [0.848528137423857, 1.131370849898476], atol=1e-15)
+    gain = np.array([[2.0, -0.5]], np.float32)
+    r = oracle_lib.contextnorm(o, gain=gain, eps=0.0)
+    np.testing.assert_allclose(r[0, 0], [1.697056274847714, -0.565685424949238], atol=1e-15)
+    # eps is added to the mean square, not to the rms
+    r = oracle_lib.contextnorm(np.array([[[1.0, 1.0]]]), eps=3.0)
+    np.testing.assert_allclose(r[0, 0], [0.5, 0.5], atol=1e-15)
+
+
+CASES = [
+    # seqlens, Hq, Hkv, d, window, mode, value
+    ((16,), 2, 2, 8, 4, "ratio", 0.25),
+    ((5, 11), 4, 2, 8, 3, "ratio", 0.5),
+    ((9, 0, 7), 4, 1, 16, 1, "threshold", 0.4),
+    ((13,), 2, 1, 4, 16, "ratio", 1.0),
+    ((12, 4), 2, 2, 8, 6, "threshold", 0.7),
+    ((1, 15), 6, 3, 8, 2, "ratio", 0.34),
+]
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_bruteforce_tiny(oracle_lib, case):
+    """Whole layer on T <= 16 against the numpy brute force (Sec. 3.1-3.2)."""
+    seqlens, Hq, Hkv, d, w, mode, val = CASES[case]
+    wl = synth.small_workload(seqlens, Hq, Hkv, d, w, val if mode == "ratio" else 0.0,
+                              seed=700 + case)
+    x = synth.make_inputs(wl, distinct_global=(case % 2 == 1))
+    rng = np.random.default_rng(case)
+    gain_l = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if case % 3 == 0 else None
+    gain_g = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if case % 3 == 0 else None
+    kw = dict(ratio=val) if mode == "ratio" else dict(threshold=val)
+    extra = {}
+    if case % 2 == 1:
+        extra = dict(q_g=x["q_g"], k_g=x["k_g"], v_g=x["v_g"])
+    r = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w,
+                            gain_local=gain_l, gain_global=gain_g, **kw, **extra)
+    b = brute_layer(x["q"], x["k"], x["v"], x["gate"], seqlens, w, gain_l=gain_l,
+                    gain_g=gain_g, **kw, **extra)
+    assert r["sel_idx"].tolist() == b["sel_idx"].tolist()
+    assert np.array_equal(r["thr"], b["thr"])
+    exp_cu = np.concatenate([[0], np.cumsum([b["selected"][s:s + T].sum() for s, T in
+                                             zip(np.cumsum((0,) + seqlens[:-1]), seqlens)])])
+    assert r["cu_sel"].tolist() == exp_cu.tolist()
+    exp_t2s = np.full(sum(seqlens), -1)
+    exp_t2s[b["sel_idx"]] = np.arange(b["sel_idx"].size)
+    assert r["tok2sel"].tolist() == exp_t2s.tolist()
+    np.testing.assert_allclose(r["o_local"], b["o_local"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["o_global"], b["o_global"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(r["out"], b["out"], rtol=0, atol=1e-12)
+
+
+def _rows(N):
+    return np.arange(N, dtype=np.int32)
+
+
+def test_window_one_is_value(oracle_lib):
+    """w = 1: the local context is the token itself, so O^L_t = v_t (Sec. 3.1)."""
+    wl = synth.small_workload((37, 20), 4, 2, 16, 1, 0.0, seed=11)
+    x = synth.make_inputs(wl)
+    o = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(57), window=1)
+    vv = np.repeat(wide(x["v"]), 2, axis=1)
+    np.testing.assert_allclose(o, vv, rtol=0, atol=1e-15)
+
+
+def test_zero_query_is_window_mean(oracle_lib):
+    """q = 0: all scores are equal, so the output is the mean of the context values.
+
+    Local: mean of v over the last min(t, w) tokens (exactly w keys with self).
+    Global: mean over the whole prefix.
+    """
+    wl = synth.small_workload((50, 31), 2, 1, 8, 7, 0.0, seed=12)
+    x = synth.make_inputs(wl)
+    q = np.zeros_like(x["q"])
+    vv = wide(x["v"])[:, 0, :]
+    for window in (7, 0):
+        o = oracle_lib.attn_rows(q, x["k"], x["v"], x["cu_seqlens"], _rows(81), window=window)
+        for t in range(81):
+            base = 0 if t < 50 else 50
+            pos = t - base
+            lo = base + (max(0, pos - window + 1) if window > 0 else 0)
+            ref = vv[lo:t + 1].mean(axis=0)
+            for h in range(2):
+                np.testing.assert_allclose(o[t, h], ref, rtol=0, atol=1e-14)
+
+
+def test_window_ge_T_is_dense(oracle_lib):
+    """w >= T: the local context is the whole causal prefix (Sec. 3.1)."""
+    wl = synth.small_workload((40,), 4, 2, 16, 40, 0.0, seed=13)
+    x = synth.make_inputs(wl)
+    for w in (40, 41, 1000):
+        a = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(40), window=w)
+        g = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(40), window=0)
+        np.testing.assert_array_equal(a, g)
+    a = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(40), window=39)
+    assert not np.array_equal(a[39:], g[39:])
+
+
+def test_ratio_one_is_dense_and_ratio_zero_is_local(oracle_lib):
+    """rho = 1 selects every token, so O^G is dense causal attention on all rows;
+    rho = 0 selects none, so the output is Norm^L(O^L) (Sec. 3.2, Eq. output-fusion)."""
+    wl = synth.small_workload((64, 33), 4, 2, 16, 8, 1.0, seed=14)
+    x = synth.make_inputs(wl)
+    r1 = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 8, ratio=1.0)
+    assert r1["n_sel"] == 97 and r1["sel_idx"].tolist() == list(range(97))
+    assert np.all(np.isneginf(r1["thr"]))
+    dense = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(97), window=0)
+    np.testing.assert_array_equal(r1["o_global"], dense)
+    r0 = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 8, ratio=0.0)
+    assert r0["n_sel"] == 0 and np.all(r0["tok2sel"] == -1)
+    np.testing.assert_array_equal(r0["out"], oracle_lib.contextnorm(r0["o_local"]))
+
+
+def test_shift_invariance(oracle_lib):
+    """Adding one vector c to every key of a head shifts each query's scores by
+    q.c, which the softmax cancels (Eq. attention).  Values are chosen so the
+    shifted keys stay bf16-exact."""
+    rng = np.random.default_rng(5)
+    N, H, d = 30, 2, 8
+    q = bf16(rng.integers(-4, 5, (N, H, d)) / 4.0)
+    k = bf16(rng.integers(-8, 9, (N, H, d)) / 8.0)
+    v = synth.bf16_bits_from_f32(rng.standard_normal((N, H, d)).astype(np.float32))
+    v = v.reshape(N, H, d)
+    c = rng.integers(-8, 9, (1, H, d)) / 8.0
+    k2 = bf16(wide(k) + c)
+    cu = np.array([0, N], np.int32)
+    for w in (5, 0):
+        a = oracle_lib.attn_rows(q, k, v, cu, _rows(N), window=w)
+        b = oracle_lib.attn_rows(q, k2, v, cu, _rows(N), window=w)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_gqa_equals_repeated_mha(oracle_lib):
+    """Query head h reads kv head floor(h/G): repeating each kv head G times
+    (contiguous grouping) gives the MHA result."""
+    wl = synth.small_workload((45,), 8, 2, 16, 9, 0.0, seed=15)
+    x = synth.make_inputs(wl)
+    krep = np.repeat(x["k"], 4, axis=1)
+    vrep = np.repeat(x["v"], 4, axis=1)
+    for w in (9, 0):
+        a = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(45), window=w)
+        b = oracle_lib.attn_rows(x["q"], krep, vrep, x["cu_seqlens"], _rows(45), window=w)
+        np.testing.assert_array_equal(a, b)
+
+
+def test_head_permutation(oracle_lib):
+    """Permuting heads (MHA) permutes the outputs of both branches and the fusion."""
+    wl = synth.small_workload((33,), 4, 4, 8, 5, 0.25, seed=16)
+    x = synth.make_inputs(wl)
+    perm = np.array([2, 0, 3, 1])
+    a = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 5, ratio=0.25)
+    b = oracle_lib.logo_fwd(x["q"][:, perm], x["k"][:, perm], x["v"][:, perm], x["gate"],
+                            x["cu_seqlens"], 5, ratio=0.25)
+    np.testing.assert_array_equal(a["out"][:, perm], b["out"])
+
+
+def test_varlen_is_separate_runs(oracle_lib):
+    """Packed sequences do not see each other: packing = running each alone."""
+    wl = synth.small_workload((19, 26, 7), 2, 1, 8, 6, 0.3, seed=17)
+    x = synth.make_inputs(wl)
+    r = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 6, ratio=0.3)
+    cu = x["cu_seqlens"]
+    for b in range(3):
+        s, e = cu[b], cu[b + 1]
+        rb = oracle_lib.logo_fwd(x["q"][s:e], x["k"][s:e], x["v"][s:e], x["gate"][s:e],
+                                 np.array([0, e - s], np.int32), 6, ratio=0.3)
+        np.testing.assert_array_equal(r["out"][s:e], rb["out"])
+        assert (r["sel_idx"][r["cu_sel"][b]:r["cu_sel"][b + 1]] - s).tolist() == \
+            rb["sel_idx"].tolist()
+
+
+def test_selection_order_statistic_and_ties(oracle_lib):
+    """Ratio mode keeps the k = floor(rho T) largest gates when they are distinct;
+    with ties at the threshold the strict '>' keeps fewer (Eq. gate-routing)."""
+    rng = np.random.default_rng(3)
+    for T, rho in ((100, 0.25), (64, 1 / 8), (7, 0.5), (10, 0.99), (1, 0.5), (2, 1.0)):
+        g = rng.permutation(T).astype(np.float32) / T
+        cu = np.array([0, T], np.int32)
+        thr = oracle_lib.thresholds(g, cu, oracle_lib.SEL_RATIO, ratio=rho)
+        sel, cu_sel, t2s = oracle_lib.select(g, cu, thr)
+        kk = math.floor(rho * T)
+        assert sel.size == kk
+        assert sorted(sel.tolist()) == sorted(np.argsort(-g, kind="stable")[:kk].tolist())
+        assert sel.tolist() == sorted(sel.tolist())
+    g = np.array([0.1, 0.5, 0.5, 0.5, 0.9, 0.2], np.float32)
+    cu = np.array([0, 6], np.int32)
+    thr = oracle_lib.thresholds(g, cu, oracle_lib.SEL_RATIO, ratio=0.5)  # k = 3
+    assert thr[0] == np.float32(0.5)
+    sel, _, _ = oracle_lib.select(g, cu, thr)
+    assert sel.tolist() == [4]
+    # threshold mode: +inf selects nothing, -inf selects every finite gate
+    for t, n in ((np.inf, 0), (-np.inf, 6), (0.5, 1), (0.1, 5), (0.2, 4)):
+        thr = oracle_lib.thresholds(g, cu, oracle_lib.SEL_THRESHOLD, threshold=t)
+        sel, _, _ = oracle_lib.select(g, cu, thr)
+        assert sel.size == n
+
+
+def test_fusion_weights(oracle_lib):
+    """Eq. output-fusion: a selected token with p = 1 takes Norm^G, one with p
+    just above a threshold of 0 takes (1-p) Norm^L + p Norm^G; unselected
+    tokens take Norm^L."""
+    wl = synth.small_workload((24,), 2, 2, 8, 3, 0.0, seed=18)
+    x = synth.make_inputs(wl)
+    gate = np.where(np.arange(24) % 3 == 0, 1.0, 0.0).astype(np.float32)
+    gate[5] = np.float32(0.125)
+    r = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], gate, x["cu_seqlens"], 3, threshold=0.0)
+    nl = oracle_lib.contextnorm(r["o_local"])
+    ng = oracle_lib.contextnorm(r["o_global"])
+    for t in range(24):
+        if t % 3 == 0:
+            np.testing.assert_allclose(r["out"][t], ng[r["tok2sel"][t]], atol=1e-15)
+        elif t == 5:
+            np.testing.assert_allclose(
+                r["out"][t], 0.875 * nl[t] + 0.125 * ng[r["tok2sel"][t]], atol=1e-15)
+        else:
+            assert r["tok2sel"][t] == -1
+            np.testing.assert_array_equal(r["out"][t], nl[t])
+
+
+def test_scale_argument(oracle_lib):
+    """Doubling q (exact in bf16) equals doubling the softmax scale."""
+    wl = synth.small_workload((20,), 2, 2, 8, 0, 0.0, seed=19)
+    x = synth.make_inputs(wl)
+    q2 = bf16(2.0 * wide(x["q"]))
+    a = oracle_lib.attn_rows(q2, x["k"], x["v"], x["cu_seqlens"], _rows(20), 0)
+    b = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(20), 0,
+                             scale=2.0 / math.sqrt(8))
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
