@@ -1,0 +1,219 @@
+/*
+ * logo.h -- C ABI of liblogo: the forward pass of one LoGo attention layer
+ * (LoGo: Token-Level Dynamic Local-Global Attention) on AMD MI355X (gfx950).
+ *
+ * The layer (Sec. 3.2):
+ *   O^L = SoftmaxAttn_w(Q, K, V)             for every token   (Eq. branch-attention)
+ *   z_t = [p_t > b_th]                        per token, all heads share it
+ *                                             (Eq. gate-routing, Eq. token-routing)
+ *   O^G_I = SoftmaxAttn_inf(Q^G_I, K^G, V^G)  for selected tokens only, K/V dense
+ *                                             (Eq. query-sparse-global)
+ *   out_t = (1-p_t) Norm^L(O^L_t) + p_t Norm^G(O^G_t)  if z_t = 1
+ *         = Norm^L(O^L_t)                               otherwise
+ *                                             (Eq. contextnorm, Eq. output-fusion)
+ *
+ * Conventions for every entry point
+ *   - Tensors are DEVICE pointers, row-major and contiguous, in packed varlen
+ *     layout: Q [N][Hq][d], K and V [N][Hkv][d], gate [N], with sequence b
+ *     occupying tokens cu_seqlens[b] .. cu_seqlens[b+1]-1.
+ *   - bf16 tensors are passed as raw 16-bit patterns (logo_bf16).
+ *   - Positions are 0-based within a sequence.  Key j is visible to query i
+ *     iff j <= i (global) or i-w < j <= i (local: exactly min(i+1, w) keys,
+ *     the query included; the paper's 1-based context {max(1,t-w+1)..t}).
+ *   - GQA: query head h reads key/value head h / (Hq/Hkv).
+ *   - The caller owns every buffer.  The library never allocates or frees
+ *     device memory, keeps no pointer after a call returns, and never
+ *     synchronises: every call only enqueues work on `stream` (NULL = the
+ *     default stream) and returns.  Device-side faults surface at the
+ *     caller's next synchronisation.
+ *   - Arguments are validated on the host before anything is enqueued: on
+ *     any error status nothing has been launched.  No C++ exception crosses
+ *     this interface.
+ *   - Calls are thread-safe.  Two calls that share output or workspace
+ *     buffers must be ordered by the caller (same stream or events).
+ */
+#ifndef LOGO_H
+#define LOGO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t logo_bf16;      /* raw bfloat16 bits                              */
+typedef void *logo_stream;       /* a hipStream_t; NULL selects the default stream */
+
+typedef enum {
+    LOGO_OK = 0,
+    LOGO_ERR_NULL = 1,        /* a required pointer is NULL                        */
+    LOGO_ERR_SHAPE = 2,       /* inconsistent sizes (heads, tokens, capacity)      */
+    LOGO_ERR_UNSUPPORTED = 3, /* a valid but unimplemented case (head_dim)         */
+    LOGO_ERR_ARG = 4,         /* an argument out of its domain (ratio, window...)  */
+    LOGO_ERR_WORKSPACE = 5,   /* workspace missing, misaligned or too small        */
+    LOGO_ERR_HIP = 6          /* the HIP runtime refused a launch                  */
+} logo_status;
+
+typedef enum {
+    LOGO_SEL_THRESHOLD = 0,   /* one scalar threshold b_th for every sequence      */
+    LOGO_SEL_RATIO = 1        /* per-sequence threshold from a target ratio rho    */
+} logo_sel_mode;
+
+/* Which entry point logo_workspace_bytes() sizes. */
+typedef enum {
+    LOGO_ENTRY_SELECT = 0,
+    LOGO_ENTRY_LOCAL = 1,
+    LOGO_ENTRY_GLOBAL = 2,
+    LOGO_ENTRY_COMBINE = 3,
+    LOGO_ENTRY_FWD = 4,
+    LOGO_ENTRY_DENSE = 5
+} logo_entry;
+
+/* Problem description (a host struct; only cu_seqlens is a device pointer). */
+typedef struct {
+    int32_t num_seqs;               /* B >= 1                                            */
+    int32_t total_tokens;           /* N = cu_seqlens[B] >= 0                            */
+    int32_t max_seqlen;             /* >= every T_b; bounds the launch grids             */
+    const int32_t *cu_seqlens;      /* device [B+1]: 0 = cu[0] <= cu[1] <= ... = N       */
+    const int32_t *cu_seqlens_host; /* optional host copy of cu_seqlens (NULL allowed);
+                                       when given it is checked against N / max_seqlen
+                                       and sizes the ratio-mode selection bound          */
+    int32_t num_q_heads;            /* Hq >= 1                                           */
+    int32_t num_kv_heads;           /* Hkv >= 1, Hq % Hkv == 0                            */
+    int32_t head_dim;               /* d in {64, 128}                                    */
+    int32_t window;                 /* w >= 1 (local span, Sec. 3.1); w >= max_seqlen
+                                       makes the local branch full causal attention      */
+    float softmax_scale;            /* <= 0 selects 1/sqrt(d) (Eq. attention)            */
+} logo_problem;
+
+/*
+ * logo_select -- hard routing and stream compaction (Eq. gate-routing;
+ * Sec. 3.3 and App. B: selected queries in ascending order with their
+ * original positions and compacted cu_seqlens).
+ *
+ *   gate       device [N] fp32: the preference p_t (already through the
+ *              sigmoid of Eq. gate-routing).  A NaN gate is never selected.
+ *   mode       LOGO_SEL_THRESHOLD: thr_b = threshold for every b (NaN is
+ *              rejected; -inf selects every non-NaN gate, +inf none).
+ *              LOGO_SEL_RATIO: k_b = floor(ratio * T_b) in IEEE double,
+ *              thr_b = -inf if k_b == T_b, else the (k_b+1)-th largest gate
+ *              of sequence b (an input value, -0 reported as +0).  Gates
+ *              must be finite in this mode.  0 <= ratio <= 1.
+ *   Selection: z_t = gate[t] > thr_b, strict, compared in fp32.
+ *   sel_idx    device [sel_capacity] int32: packed token indices of the
+ *              selected tokens, strictly ascending (sequence-major).
+ *   cu_sel     device [B+1] int32: cu_sel[b] = number of selected tokens in
+ *              sequences 0..b-1; cu_sel[B] = n_sel (the realized ratio of
+ *              Eq. realized-ratio is n_sel / N).
+ *   tok2sel    device [N] int32 or NULL: rank of token t in sel_idx, or -1.
+ *   thr_out    device [B] fp32 or NULL: the thresholds used.
+ *   Capacity:  in ratio mode sel_capacity must be >= sum_b floor(ratio*T_b)
+ *              (checked when cu_seqlens_host is given, else it must be >= N).
+ *              In threshold mode any sel_capacity >= 0 is accepted; if more
+ *              tokens pass, sel_idx keeps the first sel_capacity of them,
+ *              tok2sel marks the rest -1, and cu_sel still counts all of
+ *              them, so cu_sel[B] > sel_capacity reports the overflow.
+ *   ws         device workspace of >= logo_workspace_bytes(p, LOGO_ENTRY_SELECT, 0)
+ *              bytes, 256-byte aligned.
+ */
+logo_status logo_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
+                        float threshold, double ratio, int32_t *sel_idx, int32_t sel_capacity,
+                        int32_t *cu_sel, int32_t *tok2sel, float *thr_out, void *ws,
+                        size_t ws_bytes, logo_stream stream);
+
+/*
+ * logo_local_attn -- the local branch O^L = SoftmaxAttn_w(Q, K, V) for every
+ * token and query head (Eq. branch-attention; local context of Sec. 3.1).
+ *   q [N][Hq][d], k/v [N][Hkv][d] bf16; o_local [N][Hq][d] fp32 (raw
+ *   attention output, not normalised).  No workspace.
+ */
+logo_status logo_local_attn(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                            const logo_bf16 *v, float *o_local, logo_stream stream);
+
+/*
+ * logo_global_attn_sparse_q -- the query-sparse global branch
+ * O^G_I = SoftmaxAttn_inf(Q_I, K, V) (Eq. query-sparse-global): full causal
+ * attention for the selected rows only, keys and values dense.
+ *   sel_idx/cu_sel as produced by logo_select (only the first
+ *   min(cu_sel[B], sel_capacity) rows are computed).
+ *   o_global [sel_capacity][Hq][d] fp32, compact in rank order (row r is
+ *   token sel_idx[r]); rows at or past n_sel are left untouched.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_GLOBAL, sel_capacity) bytes,
+ *   256-byte aligned (tile table and work-queue counters).
+ */
+logo_status logo_global_attn_sparse_q(const logo_problem *p, const logo_bf16 *q,
+                                      const logo_bf16 *k, const logo_bf16 *v,
+                                      const int32_t *sel_idx, const int32_t *cu_sel,
+                                      int32_t sel_capacity, float *o_global, void *ws,
+                                      size_t ws_bytes, logo_stream stream);
+
+/*
+ * logo_combine -- ContextNorm and output fusion, scattered back to token
+ * order (Eq. contextnorm, Eq. output-fusion).
+ *   Norm(o) = o / sqrt(mean_c o_c^2 + eps) * g[h][c] per (token, head).
+ *   out_t = (1-p_t) Norm^L(O^L_t) + p_t Norm^G(O^G_{tok2sel[t]}) if tok2sel[t] >= 0,
+ *         = Norm^L(O^L_t) otherwise;  with apply_norm == 0 Norm is the identity.
+ *   o_local [N][Hq][d] fp32, o_global [*][Hq][d] fp32 compact (may be NULL
+ *   when no token is selected), gate [N] fp32, tok2sel [N] int32,
+ *   gain_local / gain_global [Hq][d] fp32 or NULL (= 1), eps >= 0,
+ *   out [N][Hq][d] bf16 (round to nearest even, once).  No workspace.
+ */
+logo_status logo_combine(const logo_problem *p, const float *o_local, const float *o_global,
+                         const float *gate, const int32_t *tok2sel, const float *gain_local,
+                         const float *gain_global, float eps, int apply_norm, logo_bf16 *out,
+                         logo_stream stream);
+
+/*
+ * logo_attn_fwd -- the whole layer: select, local branch, query-sparse
+ * global branch, ContextNorm and fusion, in one stream-ordered sequence with
+ * no host synchronisation (Sec. 3.2-3.3).
+ *   q_g/k_g/v_g: global-branch tensors of the same shapes as q/k/v, or NULL
+ *   to use q/k/v (the identity branch transform of Eq. branch-transform).
+ *   sel_idx [sel_capacity], cu_sel [B+1], tok2sel [N], thr_out [B]: outputs
+ *   as for logo_select; each may be NULL, in which case it lives in the
+ *   workspace (sel_idx NULL requires sel_capacity = 0, meaning "size it for
+ *   the worst case of the mode").  out [N][Hq][d] bf16.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD, sel_capacity) bytes.
+ */
+logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                          const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                          const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                          float threshold, double ratio, const float *gain_local,
+                          const float *gain_global, float eps, logo_bf16 *out,
+                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                          int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                          logo_stream stream);
+
+/*
+ * logo_dense_causal_attn -- dense causal softmax attention for every token
+ * (Eq. attention with the global context), bf16 output [N][Hq][d].  This is
+ * the dense baseline the query-sparse layer is measured against; it uses
+ * the same kernel template as the global branch.  No workspace.
+ */
+logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
+                                   const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
+                                   logo_stream stream);
+
+/*
+ * Workspace size in bytes for `entry` (a logo_entry value); sel_capacity is
+ * used by LOGO_ENTRY_GLOBAL and LOGO_ENTRY_FWD (0 = worst case of the
+ * problem: N).  Returns 0 for an invalid problem.
+ */
+size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capacity);
+
+/* Selection bound used by the ratio-mode capacity check: sum_b floor(ratio*T_b)
+ * computed from cu_seqlens_host, or N when that is NULL.  -1 on bad input. */
+int64_t logo_ratio_capacity(const logo_problem *p, double ratio);
+
+/* Static string naming a status. */
+const char *logo_status_str(logo_status s);
+
+/* Library version, "MAJOR.MINOR.PATCH". */
+const char *logo_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOGO_H */

@@ -1,0 +1,34 @@
+"""MI355X-native forward pass of one LoGo attention layer.
+
+A thin ctypes binding over ``liblogo.so`` (HIP kernels for gfx950, C ABI in
+``include/logo.h``).  Every function here only checks tensors and marshals
+pointers and the current torch stream into the C call of the same name; all
+computation happens in the HIP kernels.  Importing the package does not load
+the library; the first call does, and raises if it is missing (build it with
+``paper_2608_29539_amd.build.build_library()``).
+"""
+from .binding import (  # noqa: F401
+    LOGO_ENTRY_COMBINE,
+    LOGO_ENTRY_DENSE,
+    LOGO_ENTRY_FWD,
+    LOGO_ENTRY_GLOBAL,
+    LOGO_ENTRY_LOCAL,
+    LOGO_ENTRY_SELECT,
+    LOGO_SEL_RATIO,
+    LOGO_SEL_THRESHOLD,
+    LogoError,
+    Problem,
+    exported_symbols,
+    library,
+    library_path,
+    logo_attn_fwd,
+    logo_combine,
+    logo_dense_causal_attn,
+    logo_global_attn_sparse_q,
+    logo_local_attn,
+    logo_ratio_capacity,
+    logo_select,
+    logo_status_str,
+    logo_version,
+    logo_workspace_bytes,
+)

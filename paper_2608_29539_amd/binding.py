@@ -1,0 +1,345 @@
+"""ctypes binding for liblogo.so (argument marshalling only).
+
+Each ``logo_*`` function takes torch tensors on the current CUDA/HIP device,
+checks dtype / shape / contiguity, allocates outputs and workspace with torch
+when the caller does not pass them, and calls the C entry point of the same
+name on ``torch.cuda.current_stream()``.  No arithmetic of the layer happens
+here.  A failing status raises ``LogoError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(HERE, "liblogo.so")
+
+LOGO_SEL_THRESHOLD = 0
+LOGO_SEL_RATIO = 1
+LOGO_ENTRY_SELECT = 0
+LOGO_ENTRY_LOCAL = 1
+LOGO_ENTRY_GLOBAL = 2
+LOGO_ENTRY_COMBINE = 3
+LOGO_ENTRY_FWD = 4
+LOGO_ENTRY_DENSE = 5
+
+#: every symbol include/logo.h declares
+EXPORTS = (
+    "logo_select", "logo_local_attn", "logo_global_attn_sparse_q", "logo_combine",
+    "logo_attn_fwd", "logo_dense_causal_attn", "logo_workspace_bytes",
+    "logo_ratio_capacity", "logo_status_str", "logo_version",
+)
+
+_lib = None
+
+
+class LogoError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {logo_status_str(status)} ({status})")
+        self.status = status
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("total_tokens", ctypes.c_int32),
+        ("max_seqlen", ctypes.c_int32),
+        ("cu_seqlens", ctypes.c_void_p),
+        ("cu_seqlens_host", ctypes.c_void_p),
+        ("num_q_heads", ctypes.c_int32),
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("window", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float),
+    ]
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def library():
+    """Load liblogo.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(
+            f"{_LIB_PATH} is missing: build it with "
+            "`python -m paper_2608_29539_amd.build` (hipcc, gfx950)")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, i32, i64, f32, f64, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                 ctypes.c_float, ctypes.c_double, ctypes.c_size_t)
+    PP = ctypes.POINTER(_Problem)
+    sigs = {
+        "logo_select": [PP, P, i32, f32, f64, P, i32, P, P, P, P, sz, P],
+        "logo_local_attn": [PP, P, P, P, P, P],
+        "logo_global_attn_sparse_q": [PP, P, P, P, P, P, i32, P, P, sz, P],
+        "logo_combine": [PP, P, P, P, P, P, P, f32, ctypes.c_int, P, P],
+        "logo_attn_fwd": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P, P,
+                          P, P, sz, P],
+        "logo_dense_causal_attn": [PP, P, P, P, P, P],
+    }
+    for name, args in sigs.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.logo_workspace_bytes.argtypes = [PP, ctypes.c_int, i32]
+    lib.logo_workspace_bytes.restype = sz
+    lib.logo_ratio_capacity.argtypes = [PP, f64]
+    lib.logo_ratio_capacity.restype = i64
+    lib.logo_status_str.argtypes = [ctypes.c_int]
+    lib.logo_status_str.restype = ctypes.c_char_p
+    lib.logo_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def exported_symbols() -> dict:
+    """Which declared symbols the built library exports (name -> bool)."""
+    lib = library()
+    return {name: hasattr(lib, name) for name in EXPORTS}
+
+
+def logo_status_str(status: int) -> str:
+    return library().logo_status_str(int(status)).decode()
+
+
+def logo_version() -> str:
+    return library().logo_version().decode()
+
+
+class Problem:
+    """Host description of a packed varlen problem (mirrors ``logo_problem``).
+
+    ``cu_seqlens`` is an int32 device tensor; ``cu_seqlens_host`` an optional
+    host copy (a list or CPU tensor) used for validation and the ratio-mode
+    selection bound.
+    """
+
+    def __init__(self, cu_seqlens, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                 window: int, *, total_tokens: Optional[int] = None,
+                 max_seqlen: Optional[int] = None, cu_seqlens_host: Optional[Sequence[int]] = None,
+                 softmax_scale: float = 0.0):
+        import numpy as np
+        self.cu_seqlens = cu_seqlens
+        host = None
+        if cu_seqlens_host is not None:
+            host = np.ascontiguousarray(np.asarray(
+                cu_seqlens_host.cpu() if hasattr(cu_seqlens_host, "cpu") else cu_seqlens_host),
+                dtype=np.int32)
+        self._host = host
+        B = int(cu_seqlens.numel()) - 1
+        if total_tokens is None or max_seqlen is None:
+            if host is None:
+                raise ValueError("give total_tokens and max_seqlen, or cu_seqlens_host")
+            total_tokens = int(host[-1]) if total_tokens is None else total_tokens
+            max_seqlen = int(np.max(np.diff(host))) if max_seqlen is None and B > 0 else max_seqlen
+        self.num_seqs = B
+        self.total_tokens = int(total_tokens)
+        self.max_seqlen = int(max_seqlen)
+        self.num_q_heads, self.num_kv_heads, self.head_dim = num_q_heads, num_kv_heads, head_dim
+        self.window = int(window)
+        self.softmax_scale = float(softmax_scale)
+        self._c = _Problem(B, self.total_tokens, self.max_seqlen,
+                           ctypes.c_void_p(cu_seqlens.data_ptr()),
+                           None if host is None else host.ctypes.data_as(ctypes.c_void_p),
+                           num_q_heads, num_kv_heads, head_dim, self.window, self.softmax_scale)
+
+    @property
+    def c(self):
+        return ctypes.byref(self._c)
+
+
+def _stream():
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t) -> Optional[ctypes.c_void_p]:
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(t, dtype, shape, name):
+    import torch
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    return t
+
+
+def _ws(prob: Problem, entry: int, cap: int, ws):
+    import torch
+    need = library().logo_workspace_bytes(prob.c, entry, cap)
+    if need == 0:
+        return None, 0
+    if ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=prob.cu_seqlens.device)
+    return ws, int(ws.numel())
+
+
+def _call(name: str, *args):
+    st = getattr(library(), name)(*args)
+    if st != 0:
+        raise LogoError(name, st)
+
+
+def logo_workspace_bytes(prob: Problem, entry: int, sel_capacity: int = 0) -> int:
+    return int(library().logo_workspace_bytes(prob.c, entry, sel_capacity))
+
+
+def logo_ratio_capacity(prob: Problem, ratio: float) -> int:
+    return int(library().logo_ratio_capacity(prob.c, ratio))
+
+
+def logo_select(prob: Problem, gate, *, ratio: Optional[float] = None,
+                threshold: Optional[float] = None, sel_capacity: Optional[int] = None,
+                sel_idx=None, cu_sel=None, tok2sel=None, thr_out=None, ws=None):
+    """Hard routing + compaction.  Returns (sel_idx, cu_sel, tok2sel, thr_out)."""
+    import torch
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    N, B = prob.total_tokens, prob.num_seqs
+    dev = prob.cu_seqlens.device
+    _check(gate, torch.float32, (N,), "gate")
+    mode = LOGO_SEL_RATIO if ratio is not None else LOGO_SEL_THRESHOLD
+    if sel_capacity is None:
+        sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
+    if sel_idx is None:
+        sel_idx = torch.empty(max(sel_capacity, 1), dtype=torch.int32, device=dev)
+    if cu_sel is None:
+        cu_sel = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if tok2sel is None:
+        tok2sel = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    if thr_out is None:
+        thr_out = torch.empty(B, dtype=torch.float32, device=dev)
+    ws, nbytes = _ws(prob, LOGO_ENTRY_SELECT, 0, ws)
+    _call("logo_select", prob.c, _ptr(gate), mode,
+          float(threshold if threshold is not None else 0.0),
+          float(ratio if ratio is not None else 0.0), _ptr(sel_idx), int(sel_capacity),
+          _ptr(cu_sel), _ptr(tok2sel), _ptr(thr_out), _ptr(ws), nbytes, _stream())
+    return sel_idx, cu_sel, tok2sel, thr_out
+
+
+def logo_local_attn(prob: Problem, q, k, v, o_local=None):
+    """Local branch, raw fp32 output [N, Hq, d]."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    if o_local is None:
+        o_local = torch.empty((N, Hq, d), dtype=torch.float32, device=q.device)
+    _check(o_local, torch.float32, (N, Hq, d), "o_local")
+    _call("logo_local_attn", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(o_local), _stream())
+    return o_local
+
+
+def logo_global_attn_sparse_q(prob: Problem, q, k, v, sel_idx, cu_sel, sel_capacity: int,
+                              o_global=None, ws=None):
+    """Query-sparse global branch, compact fp32 output [sel_capacity, Hq, d]."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    _check(cu_sel, torch.int32, (prob.num_seqs + 1,), "cu_sel")
+    _check(sel_idx, torch.int32, None, "sel_idx")
+    if sel_idx.numel() < sel_capacity:
+        raise ValueError("sel_idx is smaller than sel_capacity")
+    if o_global is None:
+        o_global = torch.empty((max(sel_capacity, 1), Hq, d), dtype=torch.float32, device=q.device)
+    _check(o_global, torch.float32, None, "o_global")
+    if o_global.numel() < sel_capacity * Hq * d:
+        raise ValueError("o_global is smaller than sel_capacity rows")
+    ws, nbytes = _ws(prob, LOGO_ENTRY_GLOBAL, max(sel_capacity, 1), ws)
+    _call("logo_global_attn_sparse_q", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(sel_idx),
+          _ptr(cu_sel), int(sel_capacity), _ptr(o_global), _ptr(ws), nbytes, _stream())
+    return o_global
+
+
+def logo_combine(prob: Problem, o_local, o_global, gate, tok2sel, *, gain_local=None,
+                 gain_global=None, eps: float = 1e-6, apply_norm: bool = True, out=None):
+    """ContextNorm + fusion, bf16 output [N, Hq, d]."""
+    import torch
+    N, Hq, d = prob.total_tokens, prob.num_q_heads, prob.head_dim
+    _check(o_local, torch.float32, (N, Hq, d), "o_local")
+    _check(gate, torch.float32, (N,), "gate")
+    _check(tok2sel, torch.int32, None, "tok2sel")
+    if o_global is not None:
+        _check(o_global, torch.float32, None, "o_global")
+    for g, nm in ((gain_local, "gain_local"), (gain_global, "gain_global")):
+        if g is not None:
+            _check(g, torch.float32, (Hq, d), nm)
+    if out is None:
+        out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=o_local.device)
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    _call("logo_combine", prob.c, _ptr(o_local), _ptr(o_global), _ptr(gate), _ptr(tok2sel),
+          _ptr(gain_local), _ptr(gain_global), float(eps), 1 if apply_norm else 0, _ptr(out),
+          _stream())
+    return out
+
+
+def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None,
+                  threshold: Optional[float] = None, q_g=None, k_g=None, v_g=None,
+                  gain_local=None, gain_global=None, eps: float = 1e-6, out=None,
+                  sel_capacity: Optional[int] = None, sel_idx=None, cu_sel=None, tok2sel=None,
+                  thr_out=None, ws=None):
+    """The whole layer.  Returns (out, sel_idx, cu_sel, tok2sel, thr_out)."""
+    import torch
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
+                        prob.num_seqs)
+    dev = q.device
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    for t, nm, shp in ((q_g, "q_g", (N, Hq, d)), (k_g, "k_g", (N, Hkv, d)),
+                       (v_g, "v_g", (N, Hkv, d))):
+        if t is not None:
+            _check(t, torch.bfloat16, shp, nm)
+    _check(gate, torch.float32, (N,), "gate")
+    mode = LOGO_SEL_RATIO if ratio is not None else LOGO_SEL_THRESHOLD
+    if sel_capacity is None:
+        sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
+    if sel_idx is None:
+        sel_idx = torch.empty(max(sel_capacity, 1), dtype=torch.int32, device=dev)
+    if cu_sel is None:
+        cu_sel = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if tok2sel is None:
+        tok2sel = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    if thr_out is None:
+        thr_out = torch.empty(B, dtype=torch.float32, device=dev)
+    if out is None:
+        out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=dev)
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    ws, nbytes = _ws(prob, LOGO_ENTRY_FWD, max(sel_capacity, 1), ws)
+    _call("logo_attn_fwd", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g),
+          _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
+          float(ratio if ratio is not None else 0.0), _ptr(gain_local), _ptr(gain_global),
+          float(eps), _ptr(out), _ptr(sel_idx), int(max(sel_capacity, 1)), _ptr(cu_sel),
+          _ptr(tok2sel), _ptr(thr_out), _ptr(ws), nbytes, _stream())
+    return out, sel_idx, cu_sel, tok2sel, thr_out
+
+
+def logo_dense_causal_attn(prob: Problem, q, k, v, out=None):
+    """Dense causal attention for every token (the baseline), bf16 [N, Hq, d]."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    if out is None:
+        out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=q.device)
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    _call("logo_dense_causal_attn", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream())
+    return out

@@ -1,0 +1,398 @@
+// attention.hip -- softmax attention kernels for gfx950 (bf16 MFMA, fp32
+// online softmax).  One template serves the three row sets of the layer:
+//
+//   kModeLocal  : every token, keys max(0, i-w+1)..i       (local branch,
+//                 Sec. 3.1 local context; Eq. branch-attention)
+//   kModeGlobal : selected tokens only, keys 0..i          (query-sparse global
+//                 branch, Eq. query-sparse-global; App. B forward traversal)
+//   kModeDense  : every token, keys 0..i                   (dense causal
+//                 baseline, Eq. attention with the global context)
+//
+// Work decomposition.  A workgroup has 4 waves; each wave owns 32 query rows
+// of one query head, and all 4 waves read the same key/value head, so a
+// staged K/V tile in LDS serves 128 rows.  With GQA group size G the waves
+// take gcd(G,4) heads of one KV group, which keeps the tile's token span --
+// and so its causal-diagonal band -- short.
+//
+// MFMA formulation (v_mfma_f32_32x32x16_bf16, lane l: column l%32, rows
+// 8*(i/4) + 4*(l/32) + i%4 of the 32x32 accumulator).  The kernel computes
+// S^T = K Q^T, so each lane's accumulator column is ONE query: row max and
+// row sum need only the lane and its partner l^32.  The same registers,
+// rounded to bf16, are directly the B operand of O^T = V^T P^T when the key
+// order of the V^T tile in LDS is permuted to match (see store_tile).  O^T
+// again has one query per lane column, so the online-softmax rescale is a
+// per-lane multiply.
+//
+// Causal handling (App. B): per KV tile a wave classifies itself as fully
+// visible (no predicate), beyond its last row (skipped) or on the diagonal /
+// window edge (real-position mask on each score).
+#include "logo_internal.h"
+
+namespace logo {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kNegInf = -__builtin_inff();
+
+template <int D>
+struct alignas(16) Smem {
+    uint16_t k[kBlockN][D + 8];       // K tile, natural key order, +16 B pad per row
+    uint16_t vt[D][kBlockN + 8];      // V^T tile, permuted key order, +16 B pad per row
+};
+
+// Value of the partner lane (l ^ 32) and own value, combined.
+__device__ __forceinline__ float pair_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+template <int D>
+struct Stage {
+    static constexpr int kChunksK = kBlockN * D / 8 / kThreads;   // 16-byte chunks per thread
+    u32x4 k[kChunksK];
+    u32x4 v[4];                                                  // 4 keys x 8 values
+};
+
+// Global -> registers: keys [k0, k0+64) of one sequence.  Keys at or past
+// the sequence end load as zeros (they are masked, and zero values keep
+// masked-out products finite).
+template <int D>
+__device__ __forceinline__ void load_tile(Stage<D> &st, const uint16_t *__restrict__ K,
+                                          const uint16_t *__restrict__ V, int64_t base,
+                                          int T, int k0, int hkv, int kvh, int tid) {
+    const int64_t rs = (int64_t)hkv * D;
+#pragma unroll
+    for (int i = 0; i < Stage<D>::kChunksK; i++) {
+        const int c = tid + i * kThreads;
+        const int r = c / (D / 8), cc = c % (D / 8);
+        const int key = k0 + r;
+        if (key < T)
+            st.k[i] = *(const u32x4 *)(K + (base + key) * rs + (int64_t)kvh * D + cc * 8);
+        else
+            st.k[i] = u32x4{0, 0, 0, 0};
+    }
+    const int dc = tid >> 4, kg = tid & 15;
+    if (dc < D / 8) {
+#pragma unroll
+        for (int r = 0; r < 4; r++) {
+            const int key = k0 + kg * 4 + r;
+            if (key < T)
+                st.v[r] = *(const u32x4 *)(V + (base + key) * rs + (int64_t)kvh * D + dc * 8);
+            else
+                st.v[r] = u32x4{0, 0, 0, 0};
+        }
+    }
+}
+
+// Registers -> LDS.  K is copied as is.  V is transposed: thread (dc, kg)
+// holds keys 4kg..4kg+3 x values 8dc..8dc+7 and writes, for each value
+// column, the 4 keys as one 8-byte run of row (8dc + j) of V^T.  Within each
+// 32-key half, 4-key group q (0..7) goes to slot 16*(q/4) + 8*(q%2) + 4*((q%4)/2):
+// the 8 keys an MFMA lane group contracts over in one 16-key slice are then
+// contiguous, in exactly the order the S^T accumulator holds them.
+template <int D>
+__device__ __forceinline__ void store_tile(Smem<D> &sm, const Stage<D> &st, int tid) {
+#pragma unroll
+    for (int i = 0; i < Stage<D>::kChunksK; i++) {
+        const int c = tid + i * kThreads;
+        const int r = c / (D / 8), cc = c % (D / 8);
+        *(u32x4 *)&sm.k[r][cc * 8] = st.k[i];
+    }
+    const int dc = tid >> 4, kg = tid & 15;
+    if (dc < D / 8) {
+        const int q4 = kg & 7;
+        const int slot = (kg >> 3) * 32 + (q4 >> 2) * 16 + (q4 & 1) * 8 + ((q4 & 3) >> 1) * 4;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint32_t a0 = st.v[0][j], a1 = st.v[1][j], a2 = st.v[2][j], a3 = st.v[3][j];
+            u32x2 lo, hi;
+            lo.x = (a0 & 0xFFFFu) | (a1 << 16);
+            lo.y = (a2 & 0xFFFFu) | (a3 << 16);
+            hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
+            hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
+            *(u32x2 *)&sm.vt[dc * 8 + 2 * j][slot] = lo;
+            *(u32x2 *)&sm.vt[dc * 8 + 2 * j + 1][slot] = hi;
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    __bf16 x = (__bf16)a, y = (__bf16)b;   // round to nearest even
+    return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+}
+
+// Attention for one work item: a tile of rows x the heads of one head group.
+//   Local / dense: tile jt of sequence b, rows = tokens jt*tpw ...
+//   Global: rows = sel_idx[first .. first+nrows), all in sequence b.
+template <int D, int MODE>
+__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int b, int hg,
+                                            int jt, SparseTile tile) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int g = lane >> 5, m = lane & 31;
+    const int64_t base = a.cu_seqlens[b];
+    const int T = a.cu_seqlens[b + 1] - (int)base;
+    const int hw = wave % a.hpw, tb = wave / a.hpw;
+    const int head = hg * a.hpw + hw;
+    const int kvh = (hg * a.hpw) / a.group;
+
+    int nvalid, wg_pmin, wg_pmax;
+    if (MODE == kModeGlobal) {
+        nvalid = tile.nrows;
+        wg_pmax = tile.pos_max;
+        wg_pmin = a.sel_idx[tile.first] - (int)base;
+    } else {
+        const int p0 = jt * a.tpw;
+        nvalid = min(a.tpw, T - p0);
+        wg_pmin = p0;
+        wg_pmax = p0 + nvalid - 1;
+    }
+    // This lane's query row; rows past the tile end repeat the last row and
+    // are never stored.
+    const int ri = tb * kRowsPerWave + m;
+    const bool row_valid = ri < nvalid;
+    const int ric = row_valid ? ri : nvalid - 1;
+    int pos;
+    int64_t orow;
+    if (MODE == kModeGlobal) {
+        const int rank = tile.first + ric;
+        pos = a.sel_idx[rank] - (int)base;
+        orow = rank;
+    } else {
+        pos = wg_pmin + ric;
+        orow = base + pos;
+    }
+    const int64_t qtok = base + pos;
+    const bool wave_valid = tb * kRowsPerWave < nvalid;
+    const int wpmin = __builtin_amdgcn_readfirstlane(pos);
+    const int wpmax = __builtin_amdgcn_readlane(pos, 31);
+
+    bf16x8 qf[D / 16];
+    {
+        const uint16_t *qp = a.q + (qtok * a.hq + head) * (int64_t)D + g * 8;
+#pragma unroll
+        for (int s = 0; s < D / 16; s++)
+            qf[s] = *(const bf16x8 *)(qp + s * 16);
+    }
+
+    const int w = a.window;
+    const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
+    const int kb_lo = lo / kBlockN, kb_hi = wg_pmax / kBlockN;
+    const float c = a.scale_log2;
+
+    f32x16 acc[D / 32];
+#pragma unroll
+    for (int cb = 0; cb < D / 32; cb++)
+        acc[cb] = f32x16{};
+    float m_run = kNegInf, l_run = 0.f;
+
+    Stage<D> st;
+    load_tile<D>(st, a.k, a.v, base, T, kb_lo * kBlockN, a.hkv, kvh, tid);
+
+    for (int kb = kb_lo; kb <= kb_hi; kb++) {
+        __syncthreads();                     // previous tile fully consumed
+        store_tile<D>(sm, st, tid);
+        __syncthreads();                     // tile visible to all waves
+        if (kb < kb_hi)
+            load_tile<D>(st, a.k, a.v, base, T, (kb + 1) * kBlockN, a.hkv, kvh, tid);
+
+        const int k0 = kb * kBlockN;
+        bool active = wave_valid && k0 <= wpmax;
+        if (MODE == kModeLocal)
+            active = active && (k0 + kBlockN - 1 >= wpmin - w + 1);
+        if (!active)
+            continue;
+
+        // S^T = K Q^T for two 32-key halves.
+        f32x16 s[2];
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++) {
+            s[sb] = f32x16{};
+#pragma unroll
+            for (int ss = 0; ss < D / 16; ss++) {
+                const bf16x8 kf = *(const bf16x8 *)&sm.k[sb * 32 + m][ss * 16 + g * 8];
+                s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
+            }
+        }
+
+        bool need_mask = (k0 + kBlockN - 1 > wpmin);
+        if (MODE == kModeLocal)
+            need_mask = need_mask || (k0 < wpmax - w + 1);
+        if (need_mask) {
+#pragma unroll
+            for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+                for (int i = 0; i < 16; i++) {
+                    const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+                    bool ok = key <= pos;
+                    if (MODE == kModeLocal)
+                        ok = ok && (key > pos - w);
+                    if (!ok)
+                        s[sb][i] = kNegInf;
+                }
+        }
+
+        float mx = kNegInf;
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+            for (int i = 0; i < 16; i++)
+                mx = fmaxf(mx, s[sb][i]);
+        mx = pair_max(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float mc = (m_new == kNegInf) ? 0.f : m_new * c;
+        const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+
+        float psum = 0.f;
+        uint32_t pw[2][8];
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
+                psum += p0 + p1;
+                pw[sb][i >> 1] = pack_bf16x2(p0, p1);
+            }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+            for (int cb = 0; cb < D / 32; cb++)
+                acc[cb] *= alpha;
+        }
+
+        // O^T += V^T P^T over four 16-key slices.
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+            for (int ss = 0; ss < 2; ss++) {
+                u32x4 pu = {pw[sb][ss * 4 + 0], pw[sb][ss * 4 + 1], pw[sb][ss * 4 + 2],
+                            pw[sb][ss * 4 + 3]};
+                const bf16x8 pf = __builtin_bit_cast(bf16x8, pu);
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++) {
+                    const bf16x8 vf =
+                        *(const bf16x8 *)&sm.vt[cb * 32 + m][sb * 32 + ss * 16 + g * 8];
+                    acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
+                }
+            }
+    }
+
+    const float l_tot = pair_sum(l_run);
+    if (!(wave_valid && row_valid))
+        return;
+    const float inv = 1.f / l_tot;
+    if (MODE == kModeDense) {
+        uint16_t *op = (uint16_t *)a.out + (orow * a.hq + head) * (int64_t)D + g * 4;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int qd = 0; qd < 4; qd++) {
+                u32x2 v;
+                v.x = pack_bf16x2(acc[cb][qd * 4 + 0] * inv, acc[cb][qd * 4 + 1] * inv);
+                v.y = pack_bf16x2(acc[cb][qd * 4 + 2] * inv, acc[cb][qd * 4 + 3] * inv);
+                *(u32x2 *)(op + cb * 32 + qd * 8) = v;
+            }
+    } else {
+        float *op = (float *)a.out + (orow * a.hq + head) * (int64_t)D + g * 4;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int qd = 0; qd < 4; qd++) {
+                f32x4 v = {acc[cb][qd * 4 + 0] * inv, acc[cb][qd * 4 + 1] * inv,
+                           acc[cb][qd * 4 + 2] * inv, acc[cb][qd * 4 + 3] * inv};
+                *(f32x4 *)(op + cb * 32 + qd * 8) = v;
+            }
+    }
+}
+
+template <int D, int MODE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_kernel(const AttnArgs a) {
+    __shared__ Smem<D> sm;
+    if (MODE == kModeGlobal) {
+        // Persistent workgroups pull (tile, head group) items from the queue
+        // of their XCD (workgroups are dispatched round-robin over the 8
+        // XCDs): queue x holds items x, x+8, x+16, ...  Items are in
+        // longest-first order, and items that share a KV head tend to share
+        // an XCD and its L2.
+        __shared__ int s_item;
+        const int x = blockIdx.x % kQueues;
+        const int n_items = a.queue[0] * a.n_hg;
+        for (;;) {
+            if (threadIdx.x == 0)
+                s_item = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
+            __syncthreads();
+            const int item = s_item;
+            __syncthreads();
+            if (item >= n_items)
+                break;
+            const SparseTile t = a.tiles[item / a.n_hg];
+            attend_item<D, MODE>(a, sm, t.seq, item % a.n_hg, 0, t);
+        }
+    } else {
+        const int hg = blockIdx.x % a.n_hg;
+        const int rest = blockIdx.x / a.n_hg;
+        const int b = rest % a.num_seqs;
+        int jt = rest / a.num_seqs;
+        if (MODE == kModeDense)
+            jt = a.ntile_max - 1 - jt;       // longest rows first
+        const int T = a.cu_seqlens[b + 1] - a.cu_seqlens[b];
+        if (jt * a.tpw >= T)
+            return;
+        attend_item<D, MODE>(a, sm, b, hg, jt, SparseTile{0, 0, 0, 0});
+    }
+}
+
+template <int D, int MODE>
+hipError_t launch_one(const AttnArgs &a, int grid, hipStream_t s) {
+    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(grid), dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int D, int MODE>
+int blocks_per_cu_one() {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE>, kThreads, 0) !=
+        hipSuccess)
+        return 1;
+    return n > 0 ? n : 1;
+}
+
+}  // namespace
+
+hipError_t launch_attention(int mode, int head_dim, const AttnArgs &a, int grid, hipStream_t s) {
+    if (grid <= 0)
+        return hipSuccess;
+    if (head_dim == 128) {
+        if (mode == kModeLocal) return launch_one<128, kModeLocal>(a, grid, s);
+        if (mode == kModeGlobal) return launch_one<128, kModeGlobal>(a, grid, s);
+        return launch_one<128, kModeDense>(a, grid, s);
+    }
+    if (mode == kModeLocal) return launch_one<64, kModeLocal>(a, grid, s);
+    if (mode == kModeGlobal) return launch_one<64, kModeGlobal>(a, grid, s);
+    return launch_one<64, kModeDense>(a, grid, s);
+}
+
+int attention_blocks_per_cu(int mode, int head_dim) {
+    if (head_dim == 128) {
+        if (mode == kModeLocal) return blocks_per_cu_one<128, kModeLocal>();
+        if (mode == kModeGlobal) return blocks_per_cu_one<128, kModeGlobal>();
+        return blocks_per_cu_one<128, kModeDense>();
+    }
+    if (mode == kModeLocal) return blocks_per_cu_one<64, kModeLocal>();
+    if (mode == kModeGlobal) return blocks_per_cu_one<64, kModeGlobal>();
+    return blocks_per_cu_one<64, kModeDense>();
+}
+
+}  // namespace logo

@@ -1,0 +1,446 @@
+// logo_api.cpp -- the C ABI of liblogo (include/logo.h): argument validation,
+// workspace carving and stream-ordered kernel launches.  Every argument is
+// checked on the host before the first launch, so an error status means that
+// nothing was enqueued.  The library holds no device memory and never
+// synchronises (unless LOGO_DEBUG_SYNC=1 is set, which synchronises the
+// stream after each launch to localise device faults).
+#include "../../include/logo.h"
+#include "logo_internal.h"
+
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+
+using namespace logo;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+bool debug_sync() {
+    static const bool on = [] {
+        const char *e = std::getenv("LOGO_DEBUG_SYNC");
+        return e && e[0] == '1';
+    }();
+    return on;
+}
+
+logo_status hip_status(hipError_t e, hipStream_t s) {
+    if (e != hipSuccess)
+        return LOGO_ERR_HIP;
+    if (debug_sync() && hipStreamSynchronize(s) != hipSuccess)
+        return LOGO_ERR_HIP;
+    return LOGO_OK;
+}
+
+logo_status check_problem(const logo_problem *p) {
+    if (!p || !p->cu_seqlens)
+        return LOGO_ERR_NULL;
+    if (p->num_seqs < 1 || p->total_tokens < 0 || p->max_seqlen < 0)
+        return LOGO_ERR_SHAPE;
+    if (p->total_tokens > 0 && p->max_seqlen < 1)
+        return LOGO_ERR_SHAPE;
+    if (p->num_q_heads < 1 || p->num_kv_heads < 1 || p->num_q_heads % p->num_kv_heads != 0)
+        return LOGO_ERR_SHAPE;
+    if (p->head_dim != 64 && p->head_dim != 128)
+        return LOGO_ERR_UNSUPPORTED;
+    if (p->window < 1)
+        return LOGO_ERR_ARG;
+    if (std::isnan(p->softmax_scale) || std::isinf(p->softmax_scale))
+        return LOGO_ERR_ARG;
+    // element offsets are 64-bit in the kernels; token and row indices are 32-bit
+    if ((long long)p->total_tokens * p->num_q_heads >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    if (p->cu_seqlens_host) {
+        const int32_t *cu = p->cu_seqlens_host;
+        if (cu[0] != 0 || cu[p->num_seqs] != p->total_tokens)
+            return LOGO_ERR_SHAPE;
+        for (int b = 0; b < p->num_seqs; b++) {
+            const long long T = (long long)cu[b + 1] - cu[b];
+            if (T < 0 || T > p->max_seqlen)
+                return LOGO_ERR_SHAPE;
+        }
+    }
+    return LOGO_OK;
+}
+
+float scale_log2(const logo_problem *p) {
+    const double s = p->softmax_scale > 0.f ? (double)p->softmax_scale
+                                            : 1.0 / std::sqrt((double)p->head_dim);
+    return (float)(s * 1.4426950408889634);   // log2(e)
+}
+
+AttnArgs make_args(const logo_problem *p, const TilePlan &tp) {
+    AttnArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.cu_seqlens = p->cu_seqlens;
+    a.num_seqs = p->num_seqs;
+    a.hq = p->num_q_heads;
+    a.hkv = p->num_kv_heads;
+    a.group = p->num_q_heads / p->num_kv_heads;
+    a.hpw = tp.hpw;
+    a.tpw = tp.tpw;
+    a.n_hg = tp.n_hg;
+    a.window = p->window;
+    a.ntile_max = (p->max_seqlen + tp.tpw - 1) / tp.tpw;
+    a.scale_log2 = scale_log2(p);
+    return a;
+}
+
+// --- workspace layouts ------------------------------------------------------
+struct SelectWs {
+    size_t thr, counts, total;
+};
+SelectWs select_ws(const logo_problem *p) {
+    SelectWs w;
+    size_t off = 0;
+    w.thr = off;
+    off += align_up(sizeof(float) * (size_t)p->num_seqs);
+    w.counts = off;
+    off += align_up(sizeof(int32_t) * (size_t)select_chunks(p->total_tokens));
+    w.total = off;
+    return w;
+}
+
+struct GlobalWs {
+    size_t tiles, prefix, queue, total;
+};
+GlobalWs global_ws(const logo_problem *p, int32_t cap) {
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const size_t max_tiles = (size_t)(cap + tp.tpw - 1) / tp.tpw + (size_t)p->num_seqs;
+    GlobalWs w;
+    size_t off = 0;
+    w.tiles = off;
+    off += align_up(sizeof(SparseTile) * max_tiles);
+    w.prefix = off;
+    off += align_up(sizeof(int32_t) * ((size_t)p->num_seqs + 1));
+    w.queue = off;
+    off += align_up(sizeof(int32_t) * (1 + kQueues));
+    w.total = off;
+    return w;
+}
+
+struct FwdWs {
+    size_t sel, sel_ws, glob_ws, o_local, o_global, sel_idx, cu_sel, tok2sel, thr, total;
+};
+FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
+    const size_t row = (size_t)p->num_q_heads * p->head_dim * sizeof(float);
+    FwdWs w;
+    size_t off = 0;
+    w.sel_ws = off;
+    off += align_up(select_ws(p).total);
+    w.glob_ws = off;
+    off += align_up(global_ws(p, cap).total);
+    w.o_local = off;
+    off += align_up(row * (size_t)p->total_tokens);
+    w.o_global = off;
+    off += align_up(row * (size_t)cap);
+    w.sel_idx = off;
+    off += align_up(sizeof(int32_t) * (size_t)cap);
+    w.cu_sel = off;
+    off += align_up(sizeof(int32_t) * ((size_t)p->num_seqs + 1));
+    w.tok2sel = off;
+    off += align_up(sizeof(int32_t) * (size_t)p->total_tokens);
+    w.thr = off;
+    off += align_up(sizeof(float) * (size_t)p->num_seqs);
+    w.total = off;
+    w.sel = 0;
+    return w;
+}
+
+logo_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+    if (need == 0)
+        return LOGO_OK;
+    if (!ws || ((uintptr_t)ws % kAlign) != 0 || ws_bytes < need)
+        return LOGO_ERR_WORKSPACE;
+    return LOGO_OK;
+}
+
+int64_t ratio_capacity(const logo_problem *p, double ratio) {
+    if (!p->cu_seqlens_host)
+        return p->total_tokens;
+    int64_t s = 0;
+    for (int b = 0; b < p->num_seqs; b++) {
+        const int64_t T = (int64_t)p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b];
+        int64_t k = (int64_t)std::floor(ratio * (double)T);
+        s += k < T ? k : T;
+    }
+    return s;
+}
+
+logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel_mode mode,
+                              float threshold, double ratio, const int32_t *sel_idx,
+                              int32_t cap, const int32_t *cu_sel) {
+    if (!gate || !cu_sel)
+        return LOGO_ERR_NULL;
+    if (cap < 0)
+        return LOGO_ERR_SHAPE;
+    if (cap > 0 && !sel_idx)
+        return LOGO_ERR_NULL;
+    if (mode == LOGO_SEL_THRESHOLD) {
+        if (std::isnan(threshold))
+            return LOGO_ERR_ARG;
+    } else if (mode == LOGO_SEL_RATIO) {
+        if (!(ratio >= 0.0 && ratio <= 1.0))
+            return LOGO_ERR_ARG;
+        if ((int64_t)cap < ratio_capacity(p, ratio))
+            return LOGO_ERR_SHAPE;
+    } else {
+        return LOGO_ERR_ARG;
+    }
+    return LOGO_OK;
+}
+
+logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
+                       float threshold, double ratio, int32_t *sel_idx, int32_t cap,
+                       int32_t *cu_sel, int32_t *tok2sel, float *thr_out, char *ws,
+                       hipStream_t s) {
+    const SelectWs w = select_ws(p);
+    float *thr = thr_out ? thr_out : (float *)(ws + w.thr);
+    return hip_status(launch_select(p->cu_seqlens, p->num_seqs, p->total_tokens, gate,
+                                    (int)mode, threshold, ratio, sel_idx, cap, cu_sel, tok2sel,
+                                    thr, (int32_t *)(ws + w.counts), s),
+                      s);
+}
+
+logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                      const logo_bf16 *v, float *o, hipStream_t s) {
+    if (p->total_tokens == 0)
+        return LOGO_OK;
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    AttnArgs a = make_args(p, tp);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = o;
+    const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max;
+    if (grid >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    return hip_status(launch_attention(kModeLocal, p->head_dim, a, (int)grid, s), s);
+}
+
+logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                       const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
+                       int32_t cap, float *o, char *ws, hipStream_t s) {
+    if (p->total_tokens == 0 || cap == 0)
+        return LOGO_OK;
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const GlobalWs w = global_ws(p, cap);
+    SparseTile *tiles = (SparseTile *)(ws + w.tiles);
+    int32_t *prefix = (int32_t *)(ws + w.prefix);
+    int32_t *queue = (int32_t *)(ws + w.queue);
+    logo_status st = hip_status(launch_sparse_plan(p->cu_seqlens, cu_sel, sel_idx, p->num_seqs,
+                                                   tp.tpw, cap, p->max_seqlen, tiles, prefix,
+                                                   queue, s),
+                                s);
+    if (st != LOGO_OK)
+        return st;
+    AttnArgs a = make_args(p, tp);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = o;
+    a.sel_idx = sel_idx;
+    a.tiles = tiles;
+    a.queue = queue;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return LOGO_ERR_HIP;
+    const int per_cu = attention_blocks_per_cu(kModeGlobal, p->head_dim);
+    int grid = cus * per_cu;
+    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    return hip_status(launch_attention(kModeGlobal, p->head_dim, a, grid, s), s);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *logo_status_str(logo_status s) {
+    switch (s) {
+    case LOGO_OK: return "LOGO_OK";
+    case LOGO_ERR_NULL: return "LOGO_ERR_NULL";
+    case LOGO_ERR_SHAPE: return "LOGO_ERR_SHAPE";
+    case LOGO_ERR_UNSUPPORTED: return "LOGO_ERR_UNSUPPORTED";
+    case LOGO_ERR_ARG: return "LOGO_ERR_ARG";
+    case LOGO_ERR_WORKSPACE: return "LOGO_ERR_WORKSPACE";
+    case LOGO_ERR_HIP: return "LOGO_ERR_HIP";
+    }
+    return "LOGO_ERR_UNKNOWN";
+}
+
+const char *logo_version(void) { return "0.1.0"; }
+
+int64_t logo_ratio_capacity(const logo_problem *p, double ratio) {
+    if (check_problem(p) != LOGO_OK || !(ratio >= 0.0 && ratio <= 1.0))
+        return -1;
+    return ratio_capacity(p, ratio);
+}
+
+size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capacity) {
+    if (check_problem(p) != LOGO_OK || sel_capacity < 0)
+        return 0;
+    const int32_t cap = sel_capacity > 0 ? sel_capacity : p->total_tokens;
+    switch (entry) {
+    case LOGO_ENTRY_SELECT: return select_ws(p).total;
+    case LOGO_ENTRY_GLOBAL: return global_ws(p, cap).total;
+    case LOGO_ENTRY_FWD: return fwd_ws(p, cap).total;
+    case LOGO_ENTRY_LOCAL:
+    case LOGO_ENTRY_COMBINE:
+    case LOGO_ENTRY_DENSE: return 0;
+    }
+    return 0;
+}
+
+logo_status logo_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
+                        float threshold, double ratio, int32_t *sel_idx, int32_t sel_capacity,
+                        int32_t *cu_sel, int32_t *tok2sel, float *thr_out, void *ws,
+                        size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    st = check_select_args(p, gate, mode, threshold, ratio, sel_idx, sel_capacity, cu_sel);
+    if (st != LOGO_OK)
+        return st;
+    st = check_ws(ws, ws_bytes, select_ws(p).total);
+    if (st != LOGO_OK)
+        return st;
+    return run_select(p, gate, mode, threshold, ratio, sel_idx, sel_capacity, cu_sel, tok2sel,
+                      thr_out, (char *)ws, (hipStream_t)stream);
+}
+
+logo_status logo_local_attn(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                            const logo_bf16 *v, float *o_local, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (p->total_tokens > 0 && (!q || !k || !v || !o_local))
+        return LOGO_ERR_NULL;
+    return run_local(p, q, k, v, o_local, (hipStream_t)stream);
+}
+
+logo_status logo_global_attn_sparse_q(const logo_problem *p, const logo_bf16 *q,
+                                      const logo_bf16 *k, const logo_bf16 *v,
+                                      const int32_t *sel_idx, const int32_t *cu_sel,
+                                      int32_t sel_capacity, float *o_global, void *ws,
+                                      size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    if (!cu_sel)
+        return LOGO_ERR_NULL;
+    if (sel_capacity > 0 && p->total_tokens > 0 && (!q || !k || !v || !sel_idx || !o_global))
+        return LOGO_ERR_NULL;
+    if (sel_capacity > 0 && p->total_tokens > 0) {
+        st = check_ws(ws, ws_bytes, global_ws(p, sel_capacity).total);
+        if (st != LOGO_OK)
+            return st;
+    }
+    return run_global(p, q, k, v, sel_idx, cu_sel, sel_capacity, o_global, (char *)ws,
+                      (hipStream_t)stream);
+}
+
+logo_status logo_combine(const logo_problem *p, const float *o_local, const float *o_global,
+                         const float *gate, const int32_t *tok2sel, const float *gain_local,
+                         const float *gain_global, float eps, int apply_norm, logo_bf16 *out,
+                         logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (p->total_tokens > 0 && (!o_local || !gate || !tok2sel || !out))
+        return LOGO_ERR_NULL;
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    return hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, o_local,
+                                     o_global, gate, tok2sel, gain_local, gain_global, eps,
+                                     apply_norm ? 1 : 0, out, s),
+                      s);
+}
+
+logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                          const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                          const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                          float threshold, double ratio, const float *gain_local,
+                          const float *gain_global, float eps, logo_bf16 *out,
+                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                          int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                          logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (p->total_tokens > 0 && (!q || !k || !v || !gate || !out))
+        return LOGO_ERR_NULL;
+    if (!gate)
+        return LOGO_ERR_NULL;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    if (sel_idx && sel_capacity == 0 && p->total_tokens > 0)
+        return LOGO_ERR_SHAPE;
+    int32_t cap = sel_capacity;
+    if (!sel_idx && cap == 0)
+        cap = mode == LOGO_SEL_RATIO && ratio >= 0.0 && ratio <= 1.0
+                  ? (int32_t)ratio_capacity(p, ratio)
+                  : p->total_tokens;
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    const FwdWs w = fwd_ws(p, cap);
+    st = check_ws(ws, ws_bytes, w.total);
+    if (st != LOGO_OK)
+        return st;
+    char *base = (char *)ws;
+    int32_t *sel = sel_idx ? sel_idx : (int32_t *)(base + w.sel_idx);
+    int32_t *cus = cu_sel ? cu_sel : (int32_t *)(base + w.cu_sel);
+    int32_t *t2s = tok2sel ? tok2sel : (int32_t *)(base + w.tok2sel);
+    float *thr = thr_out ? thr_out : (float *)(base + w.thr);
+    st = check_select_args(p, gate, mode, threshold, ratio, sel, cap, cus);
+    if (st != LOGO_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    float *ol = (float *)(base + w.o_local);
+    float *og = (float *)(base + w.o_global);
+
+    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
+    if (st != LOGO_OK)
+        return st;
+    st = run_local(p, q, k, v, ol, s);
+    if (st != LOGO_OK)
+        return st;
+    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, og,
+                    base + w.glob_ws, s);
+    if (st != LOGO_OK)
+        return st;
+    return hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, ol, og, gate,
+                                     t2s, gain_local, gain_global, eps, 1, out, s),
+                      s);
+}
+
+logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
+                                   const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
+                                   logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (p->total_tokens == 0)
+        return LOGO_OK;
+    if (!q || !k || !v || !out)
+        return LOGO_ERR_NULL;
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    AttnArgs a = make_args(p, tp);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.out = out;
+    const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max;
+    if (grid >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    hipStream_t s = (hipStream_t)stream;
+    return hip_status(launch_attention(kModeDense, p->head_dim, a, (int)grid, s), s);
+}
+
+}  // extern "C"

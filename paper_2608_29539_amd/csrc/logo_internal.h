@@ -1,0 +1,88 @@
+// logo_internal.h -- launch plans and kernel launchers shared by the host
+// entry points (logo_api.cpp) and the HIP kernel files.  Not installed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace logo {
+
+// ---------------------------------------------------------------------------
+// Attention tiling.  One workgroup = 4 waves of 64 lanes.  Each wave owns 32
+// query rows of one query head; the 4 waves share one key/value head, so the
+// K/V tile a workgroup stages in LDS serves 4 x 32 rows.  With GQA group
+// size G the 4 waves cover HPW = gcd(G, 4) heads x (4 / HPW) blocks of 32
+// tokens: a tile is TPW = 32 * 4 / HPW tokens x HPW heads.
+// ---------------------------------------------------------------------------
+constexpr int kWaves = 4;
+constexpr int kRowsPerWave = 32;
+constexpr int kBlockN = 64;   // keys per K/V tile
+constexpr int kThreads = kWaves * 64;
+constexpr int kQueues = 8;    // one work queue per XCD
+
+struct TilePlan {
+    int hpw;      // heads per workgroup (1, 2 or 4)
+    int tpw;      // tokens per workgroup
+    int n_hg;     // head groups = Hq / hpw
+};
+
+inline TilePlan make_tile_plan(int hq, int hkv) {
+    const int g = hq / hkv;
+    TilePlan t;
+    t.hpw = (g % 4 == 0) ? 4 : (g % 2 == 0) ? 2 : 1;
+    t.tpw = kRowsPerWave * (kWaves / t.hpw);
+    t.n_hg = hq / t.hpw;
+    return t;
+}
+
+// One entry of the query-sparse tile table (written on the device).
+struct SparseTile {
+    int32_t first;    // index of the tile's first row in sel_idx
+    int32_t nrows;    // rows in the tile (1..tpw)
+    int32_t seq;      // sequence b
+    int32_t pos_max;  // position of the tile's last row (work ~ pos_max + 1)
+};
+
+enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
+
+struct AttnArgs {
+    const uint16_t *q;
+    const uint16_t *k;
+    const uint16_t *v;
+    void *out;                 // fp32 [rows][Hq][d] or bf16 for dense
+    const int32_t *cu_seqlens;
+    const int32_t *sel_idx;    // global mode
+    const SparseTile *tiles;   // global mode
+    int32_t *queue;            // global mode: [0] = n_tiles, [1 + x] = queue x counter
+    int32_t num_seqs;
+    int32_t hq, hkv, group;    // group = hq / hkv
+    int32_t hpw, tpw, n_hg;
+    int32_t window;
+    int32_t ntile_max;         // local/dense: ceil(max_seqlen / tpw)
+    float scale_log2;          // softmax_scale * log2(e)
+};
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_attention(int mode, int head_dim, const AttnArgs &a, int grid,
+                            hipStream_t s);
+int attention_blocks_per_cu(int mode, int head_dim);
+
+hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
+                              const int32_t *sel_idx, int num_seqs, int tpw,
+                              int sel_capacity, int max_seqlen, SparseTile *tiles,
+                              int32_t *tile_prefix, int32_t *queue, hipStream_t s);
+
+hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
+                         const float *gate, int mode, float threshold, double ratio,
+                         int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                         int32_t *tok2sel, float *thr, int32_t *chunk_counts,
+                         hipStream_t s);
+int select_chunks(int n_tokens);
+
+hipError_t launch_combine(int n_tokens, int hq, int head_dim, const float *o_local,
+                          const float *o_global, const float *gate,
+                          const int32_t *tok2sel, const float *gain_local,
+                          const float *gain_global, float eps, int apply_norm,
+                          uint16_t *out, hipStream_t s);
+
+}  // namespace logo

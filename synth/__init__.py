@@ -11,6 +11,7 @@ from .logo_inputs import (  # noqa: F401
     Workload,
     bf16_bits_from_f32,
     f32_from_bf16_bits,
+    make_gate_only,
     make_inputs,
     small_workload,
     markov_burst_gate,

@@ -169,6 +169,19 @@ def make_inputs(w: Workload, *, distinct_global: bool = False) -> Dict[str, np.n
     return out
 
 
+def make_gate_only(w: Workload) -> Dict[str, np.ndarray]:
+    """The gate and cu_seqlens of a workload, without drawing Q/K/V.
+
+    The gate uses its own spawned stream, so these are the same bytes as the
+    ``gate`` returned by ``make_inputs``.
+    """
+    ss = np.random.SeedSequence(w.seed).spawn(4)
+    rg = np.random.Generator(np.random.PCG64(ss[3]))
+    cu = np.zeros(len(w.seqlens) + 1, dtype=np.int32)
+    cu[1:] = np.cumsum(np.asarray(w.seqlens, dtype=np.int64)).astype(np.int32)
+    return dict(gate=make_gate(rg, w.seqlens, w.gate), cu_seqlens=cu)
+
+
 def small_workload(seqlens: Sequence[int], hq: int, hkv: int, d: int, window: int,
                    ratio: float, seed: int, gate: str = "uniform",
                    qkv_scale: Optional[float] = None) -> Workload:

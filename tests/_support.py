@@ -1,0 +1,105 @@
+"""Helpers shared by the GPU tests: moving synthetic inputs to the device,
+oracle evaluation on a subset of rows, and the error metrics used by the
+parity bar.  Expected values always come from ``oracle`` (never from the HIP
+path)."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+import synth
+
+
+def bf16_to_torch(a: np.ndarray, device):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def to_device(x: dict, device="cuda"):
+    import torch
+    out = {}
+    for k, v in x.items():
+        if v.dtype == np.uint16:
+            out[k] = bf16_to_torch(v, device)
+        else:
+            out[k] = torch.from_numpy(np.ascontiguousarray(v)).to(device)
+    return out
+
+
+def torch_bf16_to_f64(t) -> np.ndarray:
+    import torch
+    return t.detach().to(torch.float32).cpu().numpy().astype(np.float64)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """fp64 -> nearest-even bf16 (via fp32), widened back: the output format's floor."""
+    b = synth.bf16_bits_from_f32(np.asarray(x, np.float64).astype(np.float32))
+    return synth.f32_from_bf16_bits(b).reshape(np.shape(x)).astype(np.float64)
+
+
+def oracle_layer_rows(x: dict, window: int, rows: np.ndarray, *, ratio=None, threshold=None,
+                      gain_local=None, gain_global=None, eps=1e-6):
+    """Oracle layer output for the packed token indices ``rows`` only.
+
+    Threshold and selection are computed over the whole sequences (as the
+    layer does); attention, ContextNorm and fusion only for ``rows``.
+    """
+    mode = oracle.SEL_RATIO if ratio is not None else oracle.SEL_THRESHOLD
+    thr = oracle.thresholds(x["gate"], x["cu_seqlens"], mode,
+                            threshold=threshold if threshold is not None else 0.0,
+                            ratio=ratio if ratio is not None else 0.0)
+    sel_idx, cu_sel, tok2sel = oracle.select(x["gate"], x["cu_seqlens"], thr)
+    rows = np.asarray(rows, dtype=np.int32)
+    qg, kg, vg = x.get("q_g", x["q"]), x.get("k_g", x["k"]), x.get("v_g", x["v"])
+    ol = oracle.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], rows, window)
+    selected_rows = rows[tok2sel[rows] >= 0]
+    og = oracle.attn_rows(qg, kg, vg, x["cu_seqlens"], selected_rows, 0)
+    sub_t2s = np.full(rows.size, -1, np.int32)
+    sub_t2s[tok2sel[rows] >= 0] = np.arange(selected_rows.size, dtype=np.int32)
+    nl = oracle.contextnorm(ol, gain_local, eps)
+    ng = oracle.contextnorm(og, gain_global, eps) if og.size else og
+    out = oracle.fuse(nl, ng, x["gate"][rows], sub_t2s)
+    return dict(out=out, o_local=ol, o_global=og, selected_rows=selected_rows, thr=thr,
+                sel_idx=sel_idx, cu_sel=cu_sel, tok2sel=tok2sel)
+
+
+def err_stats(got: np.ndarray, ref: np.ndarray) -> dict:
+    e = np.abs(np.asarray(got, np.float64) - np.asarray(ref, np.float64))
+    floor = np.abs(bf16_round(ref) - ref)
+    return dict(max_abs=float(e.max()) if e.size else 0.0,
+                mean_abs=float(e.mean()) if e.size else 0.0,
+                n_over=int((e > 2e-2).sum()),
+                floor_max=float(floor.max()) if floor.size else 0.0,
+                floor_mean=float(floor.mean()) if floor.size else 0.0)
+
+
+def rel_rms_err(got: np.ndarray, ref: np.ndarray) -> dict:
+    """Error of raw attention rows measured in units of each (row, head) RMS."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    rms = np.sqrt((ref ** 2).mean(axis=-1, keepdims=True))
+    e = np.abs(got - ref) / rms
+    return dict(max_rel=float(e.max()) if e.size else 0.0,
+                mean_rel=float(e.mean()) if e.size else 0.0)
+
+
+def sample_rows(cu: np.ndarray, tok2sel: np.ndarray, n_sel_rows: int, n_other: int,
+                seed: int) -> np.ndarray:
+    """A spread of token rows: selected and unselected, including each
+    sequence's first and last tokens and the latest selected tokens (the
+    longest global rows)."""
+    rng = np.random.default_rng(seed)
+    N = int(cu[-1])
+    sel = np.nonzero(tok2sel >= 0)[0]
+    uns = np.nonzero(tok2sel < 0)[0]
+    picks = []
+    if sel.size:
+        picks.append(rng.choice(sel, size=min(n_sel_rows, sel.size), replace=False))
+        picks.append(sel[-min(8, sel.size):])
+    if uns.size:
+        picks.append(rng.choice(uns, size=min(n_other, uns.size), replace=False))
+    for b in range(cu.size - 1):
+        if cu[b + 1] > cu[b]:
+            picks.append(np.array([cu[b], cu[b + 1] - 1, min(cu[b] + 63, cu[b + 1] - 1)]))
+    r = np.unique(np.concatenate(picks)) if picks else np.zeros(0, np.int64)
+    return r[(r >= 0) & (r < N)].astype(np.int32)

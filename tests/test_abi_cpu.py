@@ -1,0 +1,171 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects every invalid argument with its documented
+status before launching anything (no call here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "logo.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(7)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2608_29539_amd as pk
+    if not os.path.exists(pk.library_path()):
+        from paper_2608_29539_amd.build import build_library
+        build_library()
+    return pk.library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(logo_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert "logo_attn_fwd" in names and len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), f"liblogo.so does not export {n}"
+
+
+def test_status_strings_and_version(lib):
+    import paper_2608_29539_amd as pk
+    assert pk.logo_status_str(0) == "LOGO_OK"
+    assert pk.logo_status_str(5) == "LOGO_ERR_WORKSPACE"
+    assert pk.logo_version().count(".") == 2
+
+
+class Prob:
+    """A logo_problem whose cu_seqlens points at HOST memory: validation never
+    dereferences the device pointer, so this is safe for argument checks."""
+
+    def __init__(self, seqlens=(100, 50), hq=8, hkv=2, d=128, window=16, scale=0.0,
+                 host=True, max_seqlen=None):
+        import paper_2608_29539_amd.binding as b
+        cu = np.zeros(len(seqlens) + 1, np.int32)
+        cu[1:] = np.cumsum(seqlens)
+        self.cu = cu
+        self.s = b._Problem(len(seqlens), int(cu[-1]),
+                            int(max(seqlens)) if max_seqlen is None else max_seqlen,
+                            cu.ctypes.data_as(ctypes.c_void_p),
+                            cu.ctypes.data_as(ctypes.c_void_p) if host else None,
+                            hq, hkv, d, window, scale)
+
+    @property
+    def c(self):
+        return ctypes.byref(self.s)
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+def test_problem_validation(lib):
+    def local(p):
+        return lib.logo_local_attn(p.c, FAKE, FAKE, FAKE, FAKE, None)
+
+    assert lib.logo_local_attn(None, FAKE, FAKE, FAKE, FAKE, None) == ERR_NULL
+    p = Prob()
+    p.s.cu_seqlens = None
+    assert local(p) == ERR_NULL
+    assert local(Prob(hq=6, hkv=4)) == ERR_SHAPE
+    assert local(Prob(hq=0)) == ERR_SHAPE
+    assert local(Prob(d=96)) == ERR_UNSUPPORTED
+    assert local(Prob(d=256)) == ERR_UNSUPPORTED
+    assert local(Prob(window=0)) == ERR_ARG
+    assert local(Prob(scale=float("nan"))) == ERR_ARG
+    assert local(Prob(max_seqlen=60)) == ERR_SHAPE          # host copy shows T = 100
+    p = Prob()
+    p.s.total_tokens = 149                                  # cu[B] = 150
+    assert local(p) == ERR_SHAPE
+    p = Prob()
+    p.s.num_seqs = 0
+    assert local(p) == ERR_SHAPE
+    p = Prob()
+    assert lib.logo_local_attn(p.c, None, FAKE, FAKE, FAKE, None) == ERR_NULL
+
+
+def test_select_validation(lib):
+    p = Prob()
+    ws_need = lib.logo_workspace_bytes(p.c, 0, 0)
+    assert ws_need > 0
+
+    def sel(mode=1, thr=0.0, ratio=0.25, sel_idx=FAKE, cap=150, cu_sel=FAKE, ws=FAKE,
+            ws_bytes=None, gate=FAKE):
+        return lib.logo_select(p.c, gate, mode, thr, ratio, sel_idx, cap, cu_sel, None, None, ws,
+                               ws_need if ws_bytes is None else ws_bytes, None)
+
+    assert sel(gate=None) == ERR_NULL
+    assert sel(cu_sel=None) == ERR_NULL
+    assert sel(sel_idx=None) == ERR_NULL
+    assert sel(ratio=-0.1) == ERR_ARG
+    assert sel(ratio=1.5) == ERR_ARG
+    assert sel(ratio=float("nan")) == ERR_ARG
+    assert sel(mode=0, thr=float("nan")) == ERR_ARG
+    assert sel(mode=7) == ERR_ARG
+    assert sel(cap=-1) == ERR_SHAPE
+    # ratio 0.25 of (100, 50) needs floor(25) + floor(12.5) = 37 rows
+    assert lib.logo_ratio_capacity(p.c, 0.25) == 37
+    assert sel(cap=36) == ERR_SHAPE
+    assert sel(ws=None) == ERR_WORKSPACE
+    assert sel(ws_bytes=ws_need - 1) == ERR_WORKSPACE
+    assert sel(ws=ctypes.c_void_p(0x1008)) == ERR_WORKSPACE   # misaligned
+    # without a host copy the bound is N
+    q = Prob(host=False)
+    assert lib.logo_ratio_capacity(q.c, 0.25) == 150
+    assert lib.logo_select(q.c, FAKE, 1, 0.0, 0.25, FAKE, 149, FAKE, None, None, FAKE,
+                           ws_need, None) == ERR_SHAPE
+
+
+def test_global_combine_fwd_validation(lib):
+    p = Prob()
+    need = lib.logo_workspace_bytes(p.c, 2, 64)
+    assert need > 0
+    g = lib.logo_global_attn_sparse_q
+    assert g(p.c, FAKE, FAKE, FAKE, FAKE, FAKE, -1, FAKE, FAKE, need, None) == ERR_SHAPE
+    assert g(p.c, FAKE, FAKE, FAKE, FAKE, None, 64, FAKE, FAKE, need, None) == ERR_NULL
+    assert g(p.c, FAKE, FAKE, FAKE, None, FAKE, 64, FAKE, FAKE, need, None) == ERR_NULL
+    assert g(p.c, FAKE, FAKE, FAKE, FAKE, FAKE, 64, FAKE, FAKE, need - 1, None) == ERR_WORKSPACE
+    c = lib.logo_combine
+    assert c(p.c, FAKE, FAKE, FAKE, FAKE, None, None, ctypes.c_float(-1.0), 1, FAKE,
+             None) == ERR_ARG
+    assert c(p.c, None, FAKE, FAKE, FAKE, None, None, ctypes.c_float(1e-6), 1, FAKE,
+             None) == ERR_NULL
+    f = lib.logo_attn_fwd
+    need_f = lib.logo_workspace_bytes(p.c, 4, 150)
+    args = [p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 1, 0.0, 0.25, None, None, 1e-6, FAKE,
+            FAKE, 150, FAKE, FAKE, FAKE, FAKE, need_f, None]
+    bad = list(args)
+    bad[1] = None
+    assert f(*bad) == ERR_NULL
+    bad = list(args)
+    bad[10] = 2.0
+    assert f(*bad) == ERR_ARG
+    bad = list(args)
+    bad[21] = need_f - 1
+    assert f(*bad) == ERR_WORKSPACE
+    bad = list(args)
+    bad[13] = float("inf")
+    assert f(*bad) == ERR_ARG
+    d = lib.logo_dense_causal_attn
+    assert d(Prob(d=32).c, FAKE, FAKE, FAKE, FAKE, None) == ERR_UNSUPPORTED
+    assert d(p.c, FAKE, None, FAKE, FAKE, None) == ERR_NULL
+
+
+def test_workspace_sizes(lib):
+    p = Prob(seqlens=(32768,), hq=32, hkv=8, d=128, window=1024)
+    fwd = lib.logo_workspace_bytes(p.c, 4, 4096)
+    # fp32 O^L (N x Hq x d) + compact fp32 O^G (cap x Hq x d) dominate
+    assert fwd >= 32768 * 32 * 128 * 4 + 4096 * 32 * 128 * 4
+    assert lib.logo_workspace_bytes(p.c, 1, 0) == 0
+    assert lib.logo_workspace_bytes(p.c, 5, 0) == 0
+    assert lib.logo_workspace_bytes(p.c, 2, 4096) % 256 == 0
+    bad = Prob(d=48)
+    assert lib.logo_workspace_bytes(bad.c, 4, 10) == 0

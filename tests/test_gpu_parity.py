@@ -1,0 +1,330 @@
+"""GPU parity: the HIP path (called through the C ABI) against the fp64 oracle.
+
+Bars (fixed here, not tuned per run):
+  * selection (sel_idx, cu_sel, tok2sel, thresholds): bit-exact;
+  * raw branch outputs O^L / O^G / dense (fp32): error relative to each
+    (row, head) RMS, max <= 2e-2 and mean <= 2e-3 -- the layer bar expressed
+    before ContextNorm (which divides by that RMS);
+  * layer output (bf16): max-abs <= 2e-2 and mean-abs <= 2e-3 against the
+    fp64 oracle;
+  * combine on identical fp32 inputs: within one bf16 rounding of the oracle.
+Small cases compare every element; full-size workloads compare a spread of
+sampled rows that the oracle computes one by one.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _support import (bf16_round, err_stats, oracle_layer_rows, rel_rms_err, sample_rows,
+                      to_device, torch_bf16_to_f64)
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS = 2e-2, 2e-3
+
+
+@pytest.fixture(scope="module")
+def pk():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible: the gpu tests need an MI355X")
+    import paper_2608_29539_amd as pk
+    pk.library()   # raises if liblogo.so is missing
+    oracle.build(force=False)
+    return pk
+
+
+def problem(pk, x, dev, w: synth.Workload, window=None, scale=0.0):
+    return pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim,
+                      w.window if window is None else window,
+                      cu_seqlens_host=x["cu_seqlens"], softmax_scale=scale)
+
+
+def report(tag, st):
+    print(f"[{tag}] " + " ".join(f"{k}={v:.3g}" if isinstance(v, float) else f"{k}={v}"
+                                 for k, v in st.items()), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# selection
+# ---------------------------------------------------------------------------
+SELECT_CASES = [
+    # (name, seqlens, gate kind, mode, value)
+    ("T1k-ratio", (1024,), "uniform", "ratio", 0.25),
+    ("ragged-ratio", (0, 1, 63, 64, 65, 5000, 0), "uniform", "ratio", 0.3),
+    ("ragged-kT-1", (7, 100, 4097), "uniform", "ratio", 0.999),
+    ("ratio0", (300, 700), "uniform", "ratio", 0.0),
+    ("ratio1", (300, 700), "uniform", "ratio", 1.0),
+    ("thr-half", (513, 2048, 1), "uniform", "threshold", 0.5),
+    ("thr-neginf", (513, 100), "uniform", "threshold", -math.inf),
+    ("thr-posinf", (513, 100), "uniform", "threshold", math.inf),
+    ("burst-ratio", (20000,), "markov_burst", "ratio", 1 / 8),
+    ("many-seqs", tuple(range(0, 3000, 7)), "uniform", "ratio", 0.125),
+]
+
+
+def _select_and_compare(pk, gate, cu, mode, val, tag):
+    import torch
+    dev_gate = torch.from_numpy(gate).cuda()
+    dev_cu = torch.from_numpy(cu).cuda()
+    prob = pk.Problem(dev_cu, 4, 4, 64, 16, cu_seqlens_host=cu)
+    kw = dict(ratio=val) if mode == "ratio" else dict(threshold=val)
+    sel, cu_sel, t2s, thr = pk.logo_select(prob, dev_gate, **kw)
+    torch.cuda.synchronize()
+    omode = oracle.SEL_RATIO if mode == "ratio" else oracle.SEL_THRESHOLD
+    ethr = oracle.thresholds(gate, cu, omode, threshold=val if mode != "ratio" else 0.0,
+                             ratio=val if mode == "ratio" else 0.0)
+    esel, ecu, et2s = oracle.select(gate, cu, ethr)
+    n = int(ecu[-1])
+    assert np.array_equal(thr.cpu().numpy().view(np.uint32), ethr.view(np.uint32)), tag
+    assert cu_sel.cpu().numpy().tolist() == ecu.tolist(), tag
+    assert sel.cpu().numpy()[:n].tolist() == esel.tolist(), tag
+    N = int(cu[-1])
+    assert t2s.cpu().numpy()[:N].tolist() == et2s.tolist(), tag
+    print(f"[select {tag}] n_sel={n} N={N}", flush=True)
+
+
+@pytest.mark.parametrize("ci", range(len(SELECT_CASES)), ids=[c[0] for c in SELECT_CASES])
+def test_select_bit_exact(pk, ci):
+    name, seqlens, kind, mode, val = SELECT_CASES[ci]
+    w = synth.small_workload(seqlens, 4, 4, 64, 16, val if mode == "ratio" else 0.0,
+                             seed=900 + ci, gate=kind)
+    x = synth.make_gate_only(w)
+    _select_and_compare(pk, x["gate"], x["cu_seqlens"], mode, val, name)
+
+
+def test_select_ties_and_nan(pk):
+    rng = np.random.default_rng(4)
+    cu = np.array([0, 4000, 4000, 9000], np.int32)
+    gate = (rng.integers(0, 16, 9000) / 16.0).astype(np.float32)   # heavy ties
+    for r in (0.1, 0.5, 0.9):
+        _select_and_compare(pk, gate, cu, "ratio", r, f"ties-{r}")
+    g2 = gate.copy()
+    g2[::97] = np.nan
+    g2[5] = -0.0
+    g2[6] = 0.0
+    _select_and_compare(pk, g2, cu, "threshold", 0.4375, "nan-thr")
+    _select_and_compare(pk, g2, cu, "threshold", -0.0, "zero-thr")
+    g3 = (rng.standard_normal(9000) * 3).astype(np.float32)         # negative values too
+    g3[10:20] = -0.0
+    g3[20:30] = 0.0
+    for r in (0.05, 0.5, 0.97):
+        _select_and_compare(pk, g3, cu, "ratio", r, f"signed-{r}")
+
+
+@pytest.mark.parametrize("name", ["T1k-tiny", "T8k-b2", "T32k-gqa", "T128k-gqa",
+                                  "varlen-4seq-r0", "varlen-4seq-r0.03125", "varlen-4seq-r0.125",
+                                  "varlen-4seq-r0.5", "varlen-4seq-r1"])
+def test_select_workloads(pk, name):
+    w = synth.WORKLOADS[name]
+    x = synth.make_gate_only(w)
+    _select_and_compare(pk, x["gate"], x["cu_seqlens"], "ratio", w.ratio, name)
+
+
+def test_select_overflow_threshold_mode(pk):
+    """Threshold mode with a small capacity: the first sel_capacity selections
+    are kept, the rest are marked -1, and cu_sel still counts them all."""
+    import torch
+    rng = np.random.default_rng(8)
+    cu = np.array([0, 1000, 2500], np.int32)
+    gate = rng.random(2500, dtype=np.float32)
+    prob = pk.Problem(torch.from_numpy(cu).cuda(), 4, 4, 64, 16, cu_seqlens_host=cu)
+    cap = 300
+    sel, cu_sel, t2s, _ = pk.logo_select(prob, torch.from_numpy(gate).cuda(), threshold=0.5,
+                                         sel_capacity=cap)
+    ethr = oracle.thresholds(gate, cu, oracle.SEL_THRESHOLD, threshold=0.5)
+    esel, ecu, et2s = oracle.select(gate, cu, ethr)
+    assert cu_sel.cpu().numpy().tolist() == ecu.tolist()
+    assert sel.cpu().numpy()[:cap].tolist() == esel[:cap].tolist()
+    exp = np.where(et2s < cap, et2s, -1)
+    assert t2s.cpu().numpy().tolist() == exp.tolist()
+
+
+# ---------------------------------------------------------------------------
+# branches (raw fp32 outputs), every element
+# ---------------------------------------------------------------------------
+BRANCH_CASES = [
+    # (seqlens, Hq, Hkv, d, window)
+    ((1000,), 4, 4, 64, 128),
+    ((1023, 65), 8, 2, 128, 63),
+    ((777,), 8, 1, 128, 64),
+    ((700, 1, 129), 2, 1, 64, 65),
+    ((513,), 4, 2, 128, 1),
+    ((600,), 4, 4, 128, 600),
+    ((450, 300), 16, 2, 128, 5000),
+    ((2100,), 8, 8, 64, 256),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(BRANCH_CASES)))
+def test_local_branch(pk, ci):
+    seqlens, hq, hkv, d, win = BRANCH_CASES[ci]
+    w = synth.small_workload(seqlens, hq, hkv, d, win, 0.25, seed=1200 + ci)
+    x = synth.make_inputs(w)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    o = pk.logo_local_attn(prob, dev["q"], dev["k"], dev["v"]).cpu().numpy()
+    ref = oracle.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"],
+                           np.arange(w.total_tokens, dtype=np.int32), win)
+    st = rel_rms_err(o, ref)
+    report(f"local {ci}", st)
+    assert st["max_rel"] <= MAX_ABS and st["mean_rel"] <= MEAN_ABS
+
+
+@pytest.mark.parametrize("ci", range(len(BRANCH_CASES)))
+def test_global_branch(pk, ci):
+    import torch
+    seqlens, hq, hkv, d, win = BRANCH_CASES[ci]
+    ratio = (0.25, 0.5, 0.125, 1.0, 0.05, 0.3, 0.75, 0.2)[ci]
+    w = synth.small_workload(seqlens, hq, hkv, d, win, ratio, seed=1300 + ci)
+    x = synth.make_inputs(w)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    sel, cu_sel, t2s, thr = pk.logo_select(prob, dev["gate"], ratio=ratio)
+    cap = pk.logo_ratio_capacity(prob, ratio)
+    og = pk.logo_global_attn_sparse_q(prob, dev["q"], dev["k"], dev["v"], sel, cu_sel, cap)
+    torch.cuda.synchronize()
+    ethr = oracle.thresholds(x["gate"], x["cu_seqlens"], oracle.SEL_RATIO, ratio=ratio)
+    esel, ecu, _ = oracle.select(x["gate"], x["cu_seqlens"], ethr)
+    n = int(ecu[-1])
+    assert int(cu_sel[-1]) == n
+    ref = oracle.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], esel, 0)
+    got = og.cpu().numpy()[:n]
+    st = rel_rms_err(got, ref)
+    report(f"global {ci} n={n}", st)
+    assert st["max_rel"] <= MAX_ABS and st["mean_rel"] <= MEAN_ABS
+
+
+@pytest.mark.parametrize("ci", [0, 1, 2, 3, 7])
+def test_dense_causal(pk, ci):
+    seqlens, hq, hkv, d, win = BRANCH_CASES[ci]
+    w = synth.small_workload(seqlens, hq, hkv, d, win, 0.0, seed=1400 + ci)
+    x = synth.make_inputs(w)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    o = torch_bf16_to_f64(pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"]))
+    ref = oracle.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"],
+                           np.arange(w.total_tokens, dtype=np.int32), 0)
+    st = rel_rms_err(o, ref)
+    report(f"dense {ci}", st)
+    # bf16 output: add one bf16 rounding (2^-9 relative) to the raw-branch bar
+    assert st["max_rel"] <= MAX_ABS + 2 ** -8 and st["mean_rel"] <= MEAN_ABS + 2 ** -9
+
+
+def test_combine_on_identical_inputs(pk):
+    """logo_combine fed the oracle's branch outputs (rounded to fp32) against
+    the oracle's ContextNorm + fusion of those same fp32 values."""
+    import torch
+    rng = np.random.default_rng(21)
+    N, hq, d = 700, 6, 128
+    cu = np.array([0, 300, 700], np.int32)
+    ol = rng.standard_normal((N, hq, d)).astype(np.float32) * rng.uniform(0.1, 3, (N, hq, 1)).astype(np.float32)
+    t2s = np.full(N, -1, np.int32)
+    selected = np.sort(rng.choice(N, 200, replace=False))
+    t2s[selected] = np.arange(200)
+    og = rng.standard_normal((200, hq, d)).astype(np.float32)
+    gate = rng.random(N, dtype=np.float32)
+    gl = rng.uniform(0.5, 1.5, (hq, d)).astype(np.float32)
+    gg = rng.uniform(0.5, 1.5, (hq, d)).astype(np.float32)
+    prob = pk.Problem(torch.from_numpy(cu).cuda(), hq, hq, d, 16, cu_seqlens_host=cu)
+    T = lambda a: torch.from_numpy(a).cuda()
+    for norm, gains in ((True, False), (True, True), (False, False)):
+        out = pk.logo_combine(prob, T(ol), T(og), T(gate), T(t2s),
+                              gain_local=T(gl) if gains else None,
+                              gain_global=T(gg) if gains else None, apply_norm=norm)
+        got = torch_bf16_to_f64(out)
+        nl = oracle.contextnorm(ol, gl if gains else None) if norm else ol.astype(np.float64)
+        ng = oracle.contextnorm(og, gg if gains else None) if norm else og.astype(np.float64)
+        ref = oracle.fuse(nl, ng, gate, t2s)
+        # one bf16 rounding (<= 2^-9 relative) plus fp32 evaluation error
+        assert np.all(np.abs(got - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-6), (norm, gains)
+        assert np.mean(got == bf16_round(ref)) > 0.99, (norm, gains)
+
+
+# ---------------------------------------------------------------------------
+# whole layer
+# ---------------------------------------------------------------------------
+def _layer(pk, w: synth.Workload, x=None, n_sel_rows=96, n_other=96, full=False, **kw):
+    import torch
+    x = synth.make_inputs(w) if x is None else x
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    extra = {k: dev[k] for k in ("q_g", "k_g", "v_g") if k in dev}
+    out, sel, cu_sel, t2s, thr = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                                  ratio=w.ratio, **extra, **kw)
+    torch.cuda.synchronize()
+    ethr = oracle.thresholds(x["gate"], x["cu_seqlens"], oracle.SEL_RATIO, ratio=w.ratio)
+    esel, ecu, et2s = oracle.select(x["gate"], x["cu_seqlens"], ethr)
+    n = int(ecu[-1])
+    assert cu_sel.cpu().numpy().tolist() == ecu.tolist()
+    assert sel.cpu().numpy()[:n].tolist() == esel.tolist()
+    assert t2s.cpu().numpy()[:w.total_tokens].tolist() == et2s.tolist()
+    rows = (np.arange(w.total_tokens, dtype=np.int32) if full else
+            sample_rows(x["cu_seqlens"], et2s, n_sel_rows, n_other, seed=w.seed))
+    ref = oracle_layer_rows(x, w.window, rows, ratio=w.ratio)
+    got = torch_bf16_to_f64(out[torch.from_numpy(rows).long().cuda()])
+    st = err_stats(got, ref["out"])
+    report(f"layer {w.name} rows={rows.size} n_sel={n}", st)
+    assert st["max_abs"] <= MAX_ABS and st["mean_abs"] <= MEAN_ABS
+    return out
+
+
+def test_layer_tiny_full(pk):
+    _layer(pk, synth.WORKLOADS["T1k-tiny"], full=True)
+
+
+@pytest.mark.parametrize("name", ["T8k-b2", "T32k-gqa", "varlen-4seq-r0", "varlen-4seq-r0.03125",
+                                  "varlen-4seq-r0.125", "varlen-4seq-r0.5", "varlen-4seq-r1"])
+def test_layer_workloads_sampled(pk, name):
+    _layer(pk, synth.WORKLOADS[name])
+
+
+def test_layer_longest_sampled(pk):
+    _layer(pk, synth.WORKLOADS["T128k-gqa"], n_sel_rows=40, n_other=64)
+
+
+@pytest.mark.parametrize("ci", range(4))
+def test_layer_small_full(pk, ci):
+    cases = [((1000, 23, 1), 8, 2, 128, 100, 0.3), ((513,), 4, 4, 64, 1, 0.9),
+             ((640, 0, 300), 8, 8, 128, 2000, 0.5), ((129, 257), 16, 2, 64, 64, 1.0)]
+    seqlens, hq, hkv, d, win, r = cases[ci]
+    w = synth.small_workload(seqlens, hq, hkv, d, win, r, seed=1500 + ci)
+    _layer(pk, w, full=True)
+
+
+def test_layer_distinct_global_tensors(pk):
+    w = synth.small_workload((900, 400), 8, 2, 128, 96, 0.4, seed=1600)
+    x = synth.make_inputs(w, distinct_global=True)
+    _layer(pk, w, x=x, full=True)
+
+
+def test_single_selected_at_position_zero(pk):
+    import torch
+    w = synth.small_workload((300,), 4, 2, 128, 32, 0.0, seed=1700)
+    x = synth.make_inputs(w)
+    x["gate"][:] = 0.1
+    x["gate"][0] = 0.9
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    out, sel, cu_sel, t2s, _ = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                                threshold=0.5)
+    assert cu_sel.cpu().tolist() == [0, 1] and int(sel[0]) == 0
+    ref = oracle.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 32, threshold=0.5)
+    st = err_stats(torch_bf16_to_f64(out), ref["out"])
+    report("single-at-0", st)
+    assert st["max_abs"] <= MAX_ABS and st["mean_abs"] <= MEAN_ABS
+
+
+def test_determinism(pk):
+    import torch
+    w = synth.small_workload((3000, 1500), 8, 2, 128, 256, 0.25, seed=1800)
+    x = synth.make_inputs(w)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    a = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=0.25)[0].clone()
+    b = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=0.25)[0].clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
