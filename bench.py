@@ -1,0 +1,255 @@
+#!/usr/bin/env python3
+"""Benchmark: forward pass of one LoGo attention layer on one MI355X.
+
+A step is one ``logo_attn_fwd`` call (selection, local branch, query-sparse
+global branch, ContextNorm + fusion) over one batch of synthetic inputs that
+are already resident in HBM.  The default workload is "T32k-gqa" (B=1,
+T=32768, 32 query heads / 8 KV heads, d=128, window 1024, ratio 1/8, bursty
+gate).
+
+Reported (one JSON line on stdout):
+  value          effective TFLOP/s = 4 d Hq (P_local + P_global) / t_step,
+                 P_local = sum_i min(pos_i+1, w), P_global = sum_{i selected} (pos_i+1)
+                 (causally valid (query, key) pairs only, realized selection)
+  speedup_vs_dense   t_dense / t_step, t_dense = best in-repo dense causal kernel
+  roofline       the query-sparse global kernel (the dominant one) against the
+                 dense bf16 MFMA peak, its duration taken from HIP events
+                 recorded on its own stream inside the timed steps
+  cpu_baseline   the fp64 oracle on a bounded sample of the same workload
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LoGo attn fwd effective TFLOP/s + speedup vs dense causal at T=32K, ratio 1/8"
+PEAK_BF16_TFLOPS = 2500.0        # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def pair_counts(cu: np.ndarray, window: int, sel_idx: np.ndarray):
+    """(P_local, P_global, P_dense) over the realized selection."""
+    p_local = 0
+    p_dense = 0
+    for b in range(cu.size - 1):
+        T = int(cu[b + 1] - cu[b])
+        pos = np.arange(T, dtype=np.int64)
+        p_local += int(np.minimum(pos + 1, window).sum())
+        p_dense += T * (T + 1) // 2
+    seq = np.searchsorted(cu, sel_idx, side="right") - 1
+    pos_sel = sel_idx.astype(np.int64) - cu[seq]
+    p_global = int((pos_sel + 1).sum())
+    return p_local, p_global, p_dense
+
+
+def cpu_baseline(x, w, stride: int, log_fn=log):
+    """Time the fp64 oracle on every stride-th token row (and every stride-th
+    selected row) of the workload; return a cpu_baseline record."""
+    import oracle
+    oracle.build(force=False)
+    thr = oracle.thresholds(x["gate"], x["cu_seqlens"], oracle.SEL_RATIO, ratio=w.ratio)
+    _, _, tok2sel = oracle.select(x["gate"], x["cu_seqlens"], thr)
+    N = w.total_tokens
+    uns = np.nonzero(tok2sel < 0)[0][::stride]
+    sel = np.nonzero(tok2sel >= 0)[0][::stride]
+    rows = np.sort(np.concatenate([uns, sel])).astype(np.int32)
+    cu = x["cu_seqlens"]
+    seq = np.searchsorted(cu, rows, side="right") - 1
+    pos = rows.astype(np.int64) - cu[seq]
+    is_sel = tok2sel[rows] >= 0
+    pairs = int(np.minimum(pos + 1, w.window).sum() + (pos[is_sel] + 1).sum())
+    flops = 4.0 * w.head_dim * w.num_q_heads * pairs
+    t0 = time.perf_counter()
+    oracle.logo_rows(x, w.window, rows, ratio=w.ratio)
+    dt = time.perf_counter() - t0
+    log_fn(f"cpu oracle: {rows.size} rows ({int(is_sel.sum())} selected) in {dt:.2f}s")
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": (f"{w.name}: every {stride}th unselected and every {stride}th selected "
+                       f"token row ({rows.size} of {N} rows, all {w.num_q_heads} heads), "
+                       f"selection over the full sequence; {dt:.1f}s fp64")}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="T32k-gqa")
+    ap.add_argument("--dense-steps", type=int, default=5)
+    ap.add_argument("--cpu-stride", type=int, default=0,
+                    help="oracle sample stride (0 = pick one for ~10-30 s of CPU work)")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense baseline")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the layer's "
+              "multi-GPU sharding is described in DESIGN.md but not built.", file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    import paper_2608_29539_amd as pk
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    pk.library()
+    w = synth.WORKLOADS[args.workload]
+    log(f"workload {w.name}: seqlens={list(w.seqlens)} Hq={w.num_q_heads} Hkv={w.num_kv_heads} "
+        f"d={w.head_dim} w={w.window} ratio={w.ratio}")
+    t0 = time.perf_counter()
+    x = synth.make_inputs(w)
+    log(f"inputs drawn in {time.perf_counter() - t0:.1f}s")
+    dev = {}
+    for k_, v_ in x.items():
+        t = torch.from_numpy(np.ascontiguousarray(v_.view(np.int16) if v_.dtype == np.uint16
+                                                  else v_)).cuda()
+        dev[k_] = t.view(torch.bfloat16) if v_.dtype == np.uint16 else t
+    prob = pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
+                      cu_seqlens_host=x["cu_seqlens"])
+    N, Hq, d, B = w.total_tokens, w.num_q_heads, w.head_dim, len(w.seqlens)
+    cap = max(pk.logo_ratio_capacity(prob, w.ratio), 1)
+    out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device="cuda")
+    sel_idx = torch.empty(cap, dtype=torch.int32, device="cuda")
+    cu_sel = torch.empty(B + 1, dtype=torch.int32, device="cuda")
+    tok2sel = torch.empty(N, dtype=torch.int32, device="cuda")
+    thr = torch.empty(B, dtype=torch.float32, device="cuda")
+    ws = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_FWD, cap), dtype=torch.uint8,
+                     device="cuda")
+
+    n_ev = args.steps + args.warmup
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(n_ev)]
+    for row in evs:
+        for e in row:
+            e.record()                      # materialise the HIP events
+    torch.cuda.synchronize()
+
+    def step(i):
+        pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=w.ratio,
+                         out=out, sel_capacity=cap, sel_idx=sel_idx, cu_sel=cu_sel,
+                         tok2sel=tok2sel, thr_out=thr, ws=ws, events=evs[i])
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    start.record()
+    for i in range(args.warmup, n_ev):
+        step(i)
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = start.elapsed_time(end) / args.steps
+    stage_names = ("select", "local", "global", "combine")
+    stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1])
+                                  for i in range(args.warmup, n_ev)]))
+                for j, n in enumerate(stage_names)}
+    log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); stages "
+        + " ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
+
+    sel_np = sel_idx[: int(cu_sel[-1])].cpu().numpy()
+    p_local, p_global, p_dense = pair_counts(x["cu_seqlens"], w.window, sel_np)
+    fl = 4.0 * d * Hq
+    value = fl * (p_local + p_global) / (ms_step * 1e-3) / 1e12
+    ideal = p_dense / (p_local + p_global)
+    global_tflops = fl * p_global / (stage_ms["global"] * 1e-3) / 1e12 if p_global else 0.0
+    local_tflops = fl * p_local / (stage_ms["local"] * 1e-3) / 1e12
+
+    # dense causal baseline: the DENSE kernel and the query-sparse kernel with every row selected
+    dense = {}
+    if not args.no_dense:
+        o2 = torch.empty((N, Hq, d), dtype=torch.bfloat16, device="cuda")
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"], out=o2)
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(args.dense_steps):
+            pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"], out=o2)
+        s1.record()
+        torch.cuda.synchronize()
+        dense["dense_kernel_ms"] = s0.elapsed_time(s1) / args.dense_steps
+        all_idx = torch.arange(N, dtype=torch.int32, device="cuda")
+        og = torch.empty((N, Hq, d), dtype=torch.float32, device="cuda")
+        gws = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_GLOBAL, N),
+                          dtype=torch.uint8, device="cuda")
+        cu_all = dev["cu_seqlens"].clone()
+        pk.logo_global_attn_sparse_q(prob, dev["q"], dev["k"], dev["v"], all_idx, cu_all, N,
+                                     o_global=og, ws=gws)
+        torch.cuda.synchronize()
+        s0.record()
+        for _ in range(args.dense_steps):
+            pk.logo_global_attn_sparse_q(prob, dev["q"], dev["k"], dev["v"], all_idx, cu_all, N,
+                                         o_global=og, ws=gws)
+        s1.record()
+        torch.cuda.synchronize()
+        dense["sparse_q_all_rows_ms"] = s0.elapsed_time(s1) / args.dense_steps
+        del o2, og, gws
+        t_dense = min(dense.values())
+        dense["t_dense_ms"] = t_dense
+        dense["dense_tflops"] = fl * p_dense / (t_dense * 1e-3) / 1e12
+        log("dense: " + " ".join(f"{k}={v:.3f}" for k, v in dense.items()))
+
+    roofline = {"bound": "mfma", "kernel": "attn_kernel<128, global> (query-sparse global branch)",
+                "achieved": round(global_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "flops_per_launch": fl * p_global,
+                "duration_ms": round(stage_ms["global"], 4)}
+
+    cpu = None
+    if not args.no_cpu:
+        stride = args.cpu_stride
+        if not stride:
+            # calibrate on a tiny sample, then size the sample for ~15 s of oracle time
+            probe = cpu_baseline(x, w, 512, log_fn=lambda *a: None)
+            rate = probe["value"] * 1e12
+            stride = max(1, int(np.ceil(fl * (p_local + p_global) / (rate * 15.0))))
+        cpu = cpu_baseline(x, w, stride)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": B, "seqlens": list(w.seqlens),
+                   "q_heads": Hq, "kv_heads": w.num_kv_heads, "head_dim": d,
+                   "window": w.window, "ratio": w.ratio, "gate": w.gate,
+                   "n_sel": int(sel_np.size)},
+        "speedup_vs_dense": round(dense["t_dense_ms"] / ms_step, 3) if dense else None,
+        "ideal_speedup_pairs": round(ideal, 3),
+        "ideal_speedup_paper": round(1.0 / (w.ratio + w.window / w.max_seqlen), 3),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "local_tflops": round(local_tflops, 2),
+        "global_tflops": round(global_tflops, 2),
+        "dense": {k: round(v, 4) for k, v in dense.items()} if dense else None,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -186,6 +186,25 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
                           logo_stream stream);
 
 /*
+ * logo_attn_fwd_profiled -- logo_attn_fwd that additionally records five
+ * caller-created HIP events (hipEvent_t, passed as void*) on `stream`:
+ *   events[0] before the selection kernels, events[1] after them,
+ *   events[2] after the local branch, events[3] after the global branch
+ *   (tile plan + query-sparse attention), events[4] after ContextNorm and
+ *   fusion.  Elapsed times between consecutive events are the stage times.
+ *   `events` must not be NULL; everything else is as for logo_attn_fwd.
+ */
+logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
+                                   const logo_bf16 *k, const logo_bf16 *v,
+                                   const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                   const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                   float threshold, double ratio, const float *gain_local,
+                                   const float *gain_global, float eps, logo_bf16 *out,
+                                   int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                                   int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                                   logo_stream stream, void *const *events);
+
+/*
  * logo_dense_causal_attn -- dense causal softmax attention for every token
  * (Eq. attention with the global context), bf16 output [N][Hq][d].  This is
  * the dense baseline the query-sparse layer is measured against; it uses

@@ -14,6 +14,7 @@ from .oracle import (  # noqa: F401
     fuse,
     library_path,
     logo_fwd,
+    logo_rows,
     num_threads,
     select,
     set_num_threads,

@@ -164,3 +164,35 @@ def logo_fwd(q, k, v, gate, cu_seqlens, window: int, *, ratio: Optional[float] =
         _ptr(og), _ptr(out))
     return dict(thr=thr, sel_idx=sel[:n].copy(), cu_sel=cu_sel, tok2sel=tok2sel[:N].copy(),
                 o_local=ol[:N], o_global=og[:n].copy(), out=out[:N], n_sel=int(n))
+
+
+def logo_rows(x: Dict[str, np.ndarray], window: int, rows, *, ratio: Optional[float] = None,
+              threshold: Optional[float] = None, gain_local=None, gain_global=None,
+              eps: float = 1e-6) -> Dict[str, np.ndarray]:
+    """The layer output for the packed token indices ``rows`` only.
+
+    Thresholds and selection are computed over the whole sequences (as the
+    layer does); attention, ContextNorm and fusion only for ``rows``.  ``x``
+    holds q, k, v (and optionally q_g, k_g, v_g), gate and cu_seqlens.  The
+    result equals ``logo_fwd(...)["out"][rows]``; this composition of the C
+    functions only avoids computing the other rows.
+    """
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    mode = SEL_RATIO if ratio is not None else SEL_THRESHOLD
+    thr = thresholds(x["gate"], x["cu_seqlens"], mode,
+                     threshold=threshold if threshold is not None else 0.0,
+                     ratio=ratio if ratio is not None else 0.0)
+    sel_idx, cu_sel, tok2sel = select(x["gate"], x["cu_seqlens"], thr)
+    rows = np.asarray(rows, dtype=np.int32)
+    qg, kg, vg = x.get("q_g", x["q"]), x.get("k_g", x["k"]), x.get("v_g", x["v"])
+    ol = attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], rows, window)
+    selected_rows = rows[tok2sel[rows] >= 0]
+    og = attn_rows(qg, kg, vg, x["cu_seqlens"], selected_rows, 0)
+    sub_t2s = np.full(rows.size, -1, np.int32)
+    sub_t2s[tok2sel[rows] >= 0] = np.arange(selected_rows.size, dtype=np.int32)
+    nl = contextnorm(ol, gain_local, eps)
+    ng = contextnorm(og, gain_global, eps) if og.size else og
+    out = fuse(nl, ng, x["gate"][rows], sub_t2s)
+    return dict(out=out, o_local=ol, o_global=og, selected_rows=selected_rows, thr=thr,
+                sel_idx=sel_idx, cu_sel=cu_sel, tok2sel=tok2sel)

@@ -27,7 +27,7 @@ LOGO_ENTRY_DENSE = 5
 #: every symbol include/logo.h declares
 EXPORTS = (
     "logo_select", "logo_local_attn", "logo_global_attn_sparse_q", "logo_combine",
-    "logo_attn_fwd", "logo_dense_causal_attn", "logo_workspace_bytes",
+    "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
     "logo_ratio_capacity", "logo_status_str", "logo_version",
 )
 
@@ -79,6 +79,8 @@ def library():
         "logo_combine": [PP, P, P, P, P, P, P, f32, ctypes.c_int, P, P],
         "logo_attn_fwd": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P, P,
                           P, P, sz, P],
+        "logo_attn_fwd_profiled": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32,
+                                   P, P, P, P, sz, P, P],
         "logo_dense_causal_attn": [PP, P, P, P, P, P],
     }
     for name, args in sigs.items():
@@ -292,8 +294,13 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
                   threshold: Optional[float] = None, q_g=None, k_g=None, v_g=None,
                   gain_local=None, gain_global=None, eps: float = 1e-6, out=None,
                   sel_capacity: Optional[int] = None, sel_idx=None, cu_sel=None, tok2sel=None,
-                  thr_out=None, ws=None):
-    """The whole layer.  Returns (out, sel_idx, cu_sel, tok2sel, thr_out)."""
+                  thr_out=None, ws=None, events=None):
+    """The whole layer.  Returns (out, sel_idx, cu_sel, tok2sel, thr_out).
+
+    ``events``: optional sequence of five recorded-once ``torch.cuda.Event``
+    objects; when given, ``logo_attn_fwd_profiled`` records them at the stage
+    boundaries (see include/logo.h).
+    """
     import torch
     if (ratio is None) == (threshold is None):
         raise ValueError("give exactly one of ratio / threshold")
@@ -323,11 +330,18 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
         out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=dev)
     _check(out, torch.bfloat16, (N, Hq, d), "out")
     ws, nbytes = _ws(prob, LOGO_ENTRY_FWD, max(sel_capacity, 1), ws)
-    _call("logo_attn_fwd", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g),
-          _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
-          float(ratio if ratio is not None else 0.0), _ptr(gain_local), _ptr(gain_global),
-          float(eps), _ptr(out), _ptr(sel_idx), int(max(sel_capacity, 1)), _ptr(cu_sel),
-          _ptr(tok2sel), _ptr(thr_out), _ptr(ws), nbytes, _stream())
+    args = [prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g), _ptr(gate), mode,
+            float(threshold if threshold is not None else 0.0),
+            float(ratio if ratio is not None else 0.0), _ptr(gain_local), _ptr(gain_global),
+            float(eps), _ptr(out), _ptr(sel_idx), int(max(sel_capacity, 1)), _ptr(cu_sel),
+            _ptr(tok2sel), _ptr(thr_out), _ptr(ws), nbytes, _stream()]
+    if events is None:
+        _call("logo_attn_fwd", *args)
+    else:
+        if len(events) != 5:
+            raise ValueError("events: five torch.cuda.Event objects")
+        handles = (ctypes.c_void_p * 5)(*[ctypes.c_void_p(e.cuda_event) for e in events])
+        _call("logo_attn_fwd_profiled", *args, handles)
     return out, sel_idx, cu_sel, tok2sel, thr_out
 
 

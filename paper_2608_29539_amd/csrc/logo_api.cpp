@@ -255,6 +255,72 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     return hip_status(launch_attention(kModeGlobal, p->head_dim, a, grid, s), s);
 }
 
+logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                     const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                     const logo_bf16 *v_g, const float *gate, logo_sel_mode mode, float threshold,
+                     double ratio, const float *gain_local, const float *gain_global, float eps,
+                     logo_bf16 *out, int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                     int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                     logo_stream stream, void *const *events) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (p->total_tokens > 0 && (!q || !k || !v || !gate || !out))
+        return LOGO_ERR_NULL;
+    if (!gate)
+        return LOGO_ERR_NULL;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    if (sel_idx && sel_capacity == 0 && p->total_tokens > 0)
+        return LOGO_ERR_SHAPE;
+    int32_t cap = sel_capacity;
+    if (!sel_idx && cap == 0)
+        cap = mode == LOGO_SEL_RATIO && ratio >= 0.0 && ratio <= 1.0
+                  ? (int32_t)ratio_capacity(p, ratio)
+                  : p->total_tokens;
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    const FwdWs w = fwd_ws(p, cap);
+    st = check_ws(ws, ws_bytes, w.total);
+    if (st != LOGO_OK)
+        return st;
+    char *base = (char *)ws;
+    int32_t *sel = sel_idx ? sel_idx : (int32_t *)(base + w.sel_idx);
+    int32_t *cus = cu_sel ? cu_sel : (int32_t *)(base + w.cu_sel);
+    int32_t *t2s = tok2sel ? tok2sel : (int32_t *)(base + w.tok2sel);
+    float *thr = thr_out ? thr_out : (float *)(base + w.thr);
+    st = check_select_args(p, gate, mode, threshold, ratio, sel, cap, cus);
+    if (st != LOGO_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    float *ol = (float *)(base + w.o_local);
+    float *og = (float *)(base + w.o_global);
+    auto mark = [&](int i) -> logo_status {
+        if (events && hipEventRecord((hipEvent_t)events[i], s) != hipSuccess)
+            return LOGO_ERR_HIP;
+        return LOGO_OK;
+    };
+
+    if ((st = mark(0)) != LOGO_OK)
+        return st;
+    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
+    if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
+        return st;
+    st = run_local(p, q, k, v, ol, s);
+    if (st != LOGO_OK || (st = mark(2)) != LOGO_OK)
+        return st;
+    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, og,
+                    base + w.glob_ws, s);
+    if (st != LOGO_OK || (st = mark(3)) != LOGO_OK)
+        return st;
+    st = hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, ol, og, gate,
+                                   t2s, gain_local, gain_global, eps, 1, out, s),
+                    s);
+    if (st != LOGO_OK)
+        return st;
+    return mark(4);
+}
+
 }  // namespace
 
 extern "C" {
@@ -371,53 +437,28 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
                           int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
                           int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
                           logo_stream stream) {
-    logo_status st = check_problem(p);
-    if (st != LOGO_OK)
-        return st;
-    if (p->total_tokens > 0 && (!q || !k || !v || !gate || !out))
-        return LOGO_ERR_NULL;
-    if (!gate)
-        return LOGO_ERR_NULL;
-    if (sel_capacity < 0)
-        return LOGO_ERR_SHAPE;
-    if (sel_idx && sel_capacity == 0 && p->total_tokens > 0)
-        return LOGO_ERR_SHAPE;
-    int32_t cap = sel_capacity;
-    if (!sel_idx && cap == 0)
-        cap = mode == LOGO_SEL_RATIO && ratio >= 0.0 && ratio <= 1.0
-                  ? (int32_t)ratio_capacity(p, ratio)
-                  : p->total_tokens;
-    if (!(eps >= 0.f) || std::isinf(eps))
-        return LOGO_ERR_ARG;
-    const FwdWs w = fwd_ws(p, cap);
-    st = check_ws(ws, ws_bytes, w.total);
-    if (st != LOGO_OK)
-        return st;
-    char *base = (char *)ws;
-    int32_t *sel = sel_idx ? sel_idx : (int32_t *)(base + w.sel_idx);
-    int32_t *cus = cu_sel ? cu_sel : (int32_t *)(base + w.cu_sel);
-    int32_t *t2s = tok2sel ? tok2sel : (int32_t *)(base + w.tok2sel);
-    float *thr = thr_out ? thr_out : (float *)(base + w.thr);
-    st = check_select_args(p, gate, mode, threshold, ratio, sel, cap, cus);
-    if (st != LOGO_OK)
-        return st;
-    hipStream_t s = (hipStream_t)stream;
-    float *ol = (float *)(base + w.o_local);
-    float *og = (float *)(base + w.o_global);
+    return fwd_impl(p, q, k, v, q_g, k_g, v_g, gate, mode, threshold, ratio, gain_local,
+                    gain_global, eps, out, sel_idx, sel_capacity, cu_sel, tok2sel, thr_out, ws,
+                    ws_bytes, stream, nullptr);
+}
 
-    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
-    if (st != LOGO_OK)
-        return st;
-    st = run_local(p, q, k, v, ol, s);
-    if (st != LOGO_OK)
-        return st;
-    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, og,
-                    base + w.glob_ws, s);
-    if (st != LOGO_OK)
-        return st;
-    return hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, ol, og, gate,
-                                     t2s, gain_local, gain_global, eps, 1, out, s),
-                      s);
+logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
+                                   const logo_bf16 *k, const logo_bf16 *v,
+                                   const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                   const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                   float threshold, double ratio, const float *gain_local,
+                                   const float *gain_global, float eps, logo_bf16 *out,
+                                   int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                                   int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                                   logo_stream stream, void *const *events) {
+    if (!events)
+        return LOGO_ERR_NULL;
+    for (int i = 0; i < 5; i++)
+        if (!events[i])
+            return LOGO_ERR_NULL;
+    return fwd_impl(p, q, k, v, q_g, k_g, v_g, gate, mode, threshold, ratio, gain_local,
+                    gain_global, eps, out, sel_idx, sel_capacity, cu_sel, tok2sel, thr_out, ws,
+                    ws_bytes, stream, events);
 }
 
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,

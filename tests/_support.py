@@ -37,30 +37,9 @@ def bf16_round(x: np.ndarray) -> np.ndarray:
     return synth.f32_from_bf16_bits(b).reshape(np.shape(x)).astype(np.float64)
 
 
-def oracle_layer_rows(x: dict, window: int, rows: np.ndarray, *, ratio=None, threshold=None,
-                      gain_local=None, gain_global=None, eps=1e-6):
-    """Oracle layer output for the packed token indices ``rows`` only.
-
-    Threshold and selection are computed over the whole sequences (as the
-    layer does); attention, ContextNorm and fusion only for ``rows``.
-    """
-    mode = oracle.SEL_RATIO if ratio is not None else oracle.SEL_THRESHOLD
-    thr = oracle.thresholds(x["gate"], x["cu_seqlens"], mode,
-                            threshold=threshold if threshold is not None else 0.0,
-                            ratio=ratio if ratio is not None else 0.0)
-    sel_idx, cu_sel, tok2sel = oracle.select(x["gate"], x["cu_seqlens"], thr)
-    rows = np.asarray(rows, dtype=np.int32)
-    qg, kg, vg = x.get("q_g", x["q"]), x.get("k_g", x["k"]), x.get("v_g", x["v"])
-    ol = oracle.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], rows, window)
-    selected_rows = rows[tok2sel[rows] >= 0]
-    og = oracle.attn_rows(qg, kg, vg, x["cu_seqlens"], selected_rows, 0)
-    sub_t2s = np.full(rows.size, -1, np.int32)
-    sub_t2s[tok2sel[rows] >= 0] = np.arange(selected_rows.size, dtype=np.int32)
-    nl = oracle.contextnorm(ol, gain_local, eps)
-    ng = oracle.contextnorm(og, gain_global, eps) if og.size else og
-    out = oracle.fuse(nl, ng, x["gate"][rows], sub_t2s)
-    return dict(out=out, o_local=ol, o_global=og, selected_rows=selected_rows, thr=thr,
-                sel_idx=sel_idx, cu_sel=cu_sel, tok2sel=tok2sel)
+def oracle_layer_rows(x: dict, window: int, rows: np.ndarray, **kw):
+    """Oracle layer output for the token rows ``rows`` (see ``oracle.logo_rows``)."""
+    return oracle.logo_rows(x, window, rows, **kw)
 
 
 def err_stats(got: np.ndarray, ref: np.ndarray) -> dict:

@@ -355,3 +355,14 @@ def test_scale_argument(oracle_lib):
     b = oracle_lib.attn_rows(x["q"], x["k"], x["v"], x["cu_seqlens"], _rows(20), 0,
                              scale=2.0 / math.sqrt(8))
     np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
+
+
+def test_logo_rows_matches_whole_layer(oracle_lib):
+    """The row-subset composition used for large workloads equals the whole
+    layer on those rows."""
+    wl = synth.small_workload((200, 57), 4, 2, 16, 9, 0.3, seed=20)
+    x = synth.make_inputs(wl)
+    full = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], 9, ratio=0.3)
+    rows = np.array([0, 5, 17, 199, 200, 201, 256, 120], np.int32)
+    sub = oracle_lib.logo_rows(x, 9, rows, ratio=0.3)
+    np.testing.assert_allclose(sub["out"], full["out"][rows], rtol=0, atol=1e-15)
