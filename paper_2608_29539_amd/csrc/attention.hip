@@ -36,13 +36,21 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
 
+// LDS tiles, both in natural [key][d] order.  K rows are padded by 16 B so
+// that the 16-byte fragment reads of 8 consecutive rows hit distinct banks;
+// V rows by 64 B so that the transpose reads (4 rows x 32 B per 16 lanes,
+// two 16-lane groups 32 B apart) do.
+constexpr int kKPad = 8;
+constexpr int kVPad = 32;
 template <int D>
 struct alignas(16) Smem {
-    uint16_t k[kBlockN][D + 8];       // K tile, natural key order, +16 B pad per row
-    uint16_t vt[D][kBlockN + 8];      // V^T tile, permuted key order, +16 B pad per row
+    uint16_t k[kBlockN][D + kKPad];
+    uint16_t v[kBlockN][D + kVPad];
 };
 
 // Value of the partner lane (l ^ 32) and own value, combined.
@@ -57,9 +65,9 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 template <int D>
 struct Stage {
-    static constexpr int kChunksK = kBlockN * D / 8 / kThreads;   // 16-byte chunks per thread
-    u32x4 k[kChunksK];
-    u32x4 v[4];                                                  // 4 keys x 8 values
+    static constexpr int kChunks = kBlockN * D / 8 / kThreads;   // 16-byte chunks per thread
+    u32x4 k[kChunks];
+    u32x4 v[kChunks];
 };
 
 // Global -> registers: keys [k0, k0+64) of one sequence.  Keys at or past
@@ -71,70 +79,64 @@ __device__ __forceinline__ void load_tile(Stage<D> &st, const uint16_t *__restri
                                           int T, int k0, int hkv, int kvh, int tid) {
     const int64_t rs = (int64_t)hkv * D;
 #pragma unroll
-    for (int i = 0; i < Stage<D>::kChunksK; i++) {
+    for (int i = 0; i < Stage<D>::kChunks; i++) {
         const int c = tid + i * kThreads;
         const int r = c / (D / 8), cc = c % (D / 8);
         const int key = k0 + r;
-        if (key < T)
-            st.k[i] = *(const u32x4 *)(K + (base + key) * rs + (int64_t)kvh * D + cc * 8);
-        else
+        if (key < T) {
+            const int64_t off = (base + key) * rs + (int64_t)kvh * D + cc * 8;
+            st.k[i] = *(const u32x4 *)(K + off);
+            st.v[i] = *(const u32x4 *)(V + off);
+        } else {
             st.k[i] = u32x4{0, 0, 0, 0};
-    }
-    const int dc = tid >> 4, kg = tid & 15;
-    if (dc < D / 8) {
-#pragma unroll
-        for (int r = 0; r < 4; r++) {
-            const int key = k0 + kg * 4 + r;
-            if (key < T)
-                st.v[r] = *(const u32x4 *)(V + (base + key) * rs + (int64_t)kvh * D + dc * 8);
-            else
-                st.v[r] = u32x4{0, 0, 0, 0};
+            st.v[i] = u32x4{0, 0, 0, 0};
         }
     }
 }
 
-// Registers -> LDS.  K is copied as is.  V is transposed: thread (dc, kg)
-// holds keys 4kg..4kg+3 x values 8dc..8dc+7 and writes, for each value
-// column, the 4 keys as one 8-byte run of row (8dc + j) of V^T.  Within each
-// 32-key half, 4-key group q (0..7) goes to slot 16*(q/4) + 8*(q%2) + 4*((q%4)/2):
-// the 8 keys an MFMA lane group contracts over in one 16-key slice are then
-// contiguous, in exactly the order the S^T accumulator holds them.
+// Registers -> LDS, a plain row-major copy of both tiles.
 template <int D>
 __device__ __forceinline__ void store_tile(Smem<D> &sm, const Stage<D> &st, int tid) {
 #pragma unroll
-    for (int i = 0; i < Stage<D>::kChunksK; i++) {
+    for (int i = 0; i < Stage<D>::kChunks; i++) {
         const int c = tid + i * kThreads;
         const int r = c / (D / 8), cc = c % (D / 8);
         *(u32x4 *)&sm.k[r][cc * 8] = st.k[i];
-    }
-    const int dc = tid >> 4, kg = tid & 15;
-    if (dc < D / 8) {
-        const int q4 = kg & 7;
-        const int slot = (kg >> 3) * 32 + (q4 >> 2) * 16 + (q4 & 1) * 8 + ((q4 & 3) >> 1) * 4;
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const uint32_t a0 = st.v[0][j], a1 = st.v[1][j], a2 = st.v[2][j], a3 = st.v[3][j];
-            u32x2 lo, hi;
-            lo.x = (a0 & 0xFFFFu) | (a1 << 16);
-            lo.y = (a2 & 0xFFFFu) | (a3 << 16);
-            hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
-            hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
-            *(u32x2 *)&sm.vt[dc * 8 + 2 * j][slot] = lo;
-            *(u32x2 *)&sm.vt[dc * 8 + 2 * j + 1][slot] = hi;
-        }
+        *(u32x4 *)&sm.v[r][cc * 8] = st.v[i];
     }
 }
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// V^T operand of the O^T MFMA straight from the row-major V tile with the
+// gfx950 LDS transpose read: within each 16-lane group, lane 4b+e receives
+// element e of the 4-element rows addressed by lanes b, b+4, b+8, b+12.
+// Lane i of group q addresses row (key0 + 4*(q/2) + i/4), columns
+// (c0 + 16*(q%2) + 4*(i%4)) .. +3, so lane l ends up holding column c0 + l%32
+// for keys key0 + 4*(l/32) + 0..3 (first read) and, 8 rows further, + 8..11
+// (second read): the 8 keys of its MFMA k-slice, in the order the S^T
+// accumulator (and so P^T) holds them.
+__device__ __forceinline__ bf16x8 read_vt_frag(const uint16_t *vrow_lane, int row_stride) {
+    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)vrow_lane);
+    const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vrow_lane + 8 * row_stride));
+    const s16x4 ab[2] = {a, b};
+    return __builtin_bit_cast(bf16x8, ab);
+}
+
+// Two fp32 -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ bf16x2 cvt_bf16x2(float a, float b) {
+    return __builtin_convertvector(f32x2{a, b}, bf16x2);
+}
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    __bf16 x = (__bf16)a, y = (__bf16)b;   // round to nearest even
-    return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+    return __builtin_bit_cast(uint32_t, cvt_bf16x2(a, b));
 }
 
 // Attention for one work item: a tile of rows x the heads of one head group.
 //   Local / dense: tile jt of sequence b, rows = tokens jt*tpw ...
 //   Global: rows = sel_idx[first .. first+nrows), all in sequence b.
 template <int D, int MODE>
-__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int b, int hg,
+__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int b, int hg,
                                             int jt, SparseTile tile) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
     const int g = lane >> 5, m = lane & 31;
@@ -183,10 +185,15 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
             qf[s] = *(const bf16x8 *)(qp + s * 16);
     }
 
+    // lane's row / column inside a V tile for the transpose reads
+    const int vt_row = 4 * g + ((lane & 15) >> 2);
+    const int vt_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
     const int w = a.window;
     const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
     const int kb_lo = lo / kBlockN, kb_hi = wg_pmax / kBlockN;
     const float c = a.scale_log2;
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
     f32x16 acc[D / 32];
 #pragma unroll
@@ -194,100 +201,111 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         acc[cb] = f32x16{};
     float m_run = kNegInf, l_run = 0.f;
 
+    // Double-buffered K/V tiles: tile kb is computed from buffer (kb-kb_lo)&1
+    // while tile kb+1 travels global -> registers -> the other buffer; one
+    // barrier per tile separates the two.
     Stage<D> st;
     load_tile<D>(st, a.k, a.v, base, T, kb_lo * kBlockN, a.hkv, kvh, tid);
+    __syncthreads();                         // the previous item's last tile is consumed
+    store_tile<D>(sm[0], st, tid);
+    __syncthreads();
 
     for (int kb = kb_lo; kb <= kb_hi; kb++) {
-        __syncthreads();                     // previous tile fully consumed
-        store_tile<D>(sm, st, tid);
-        __syncthreads();                     // tile visible to all waves
-        if (kb < kb_hi)
+        const Smem<D> &cur = sm[(kb - kb_lo) & 1];
+        const bool more = kb < kb_hi;
+        if (more)
             load_tile<D>(st, a.k, a.v, base, T, (kb + 1) * kBlockN, a.hkv, kvh, tid);
 
         const int k0 = kb * kBlockN;
         bool active = wave_valid && k0 <= wpmax;
         if (MODE == kModeLocal)
             active = active && (k0 + kBlockN - 1 >= wpmin - w + 1);
-        if (!active)
-            continue;
-
-        // S^T = K Q^T for two 32-key halves.
-        f32x16 s[2];
+        if (active) {
+            // S^T = K Q^T for two 32-key halves.
+            f32x16 s[2];
 #pragma unroll
-        for (int sb = 0; sb < 2; sb++) {
-            s[sb] = f32x16{};
+            for (int sb = 0; sb < 2; sb++) {
+                s[sb] = f32x16{};
 #pragma unroll
-            for (int ss = 0; ss < D / 16; ss++) {
-                const bf16x8 kf = *(const bf16x8 *)&sm.k[sb * 32 + m][ss * 16 + g * 8];
-                s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
+                for (int ss = 0; ss < D / 16; ss++) {
+                    const bf16x8 kf = *(const bf16x8 *)&cur.k[sb * 32 + m][ss * 16 + g * 8];
+                    s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
+                }
             }
-        }
 
-        bool need_mask = (k0 + kBlockN - 1 > wpmin);
-        if (MODE == kModeLocal)
-            need_mask = need_mask || (k0 < wpmax - w + 1);
-        if (need_mask) {
+            bool need_mask = (k0 + kBlockN - 1 > wpmin);
+            if (MODE == kModeLocal)
+                need_mask = need_mask || (k0 < wpmax - w + 1);
+            if (need_mask) {
+#pragma unroll
+                for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+                    for (int i = 0; i < 16; i++) {
+                        const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+                        bool ok = key <= pos;
+                        if (MODE == kModeLocal)
+                            ok = ok && (key > pos - w);
+                        if (!ok)
+                            s[sb][i] = kNegInf;
+                    }
+            }
+
+            float mx = kNegInf;
 #pragma unroll
             for (int sb = 0; sb < 2; sb++)
 #pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
-                    bool ok = key <= pos;
-                    if (MODE == kModeLocal)
-                        ok = ok && (key > pos - w);
-                    if (!ok)
-                        s[sb][i] = kNegInf;
+                for (int i = 0; i < 16; i++)
+                    mx = fmaxf(mx, s[sb][i]);
+            mx = pair_max(mx);
+            const float m_new = fmaxf(m_run, mx);
+            const float mc = (m_new == kNegInf) ? 0.f : m_new * c;
+            const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+
+            // P = exp2(s*c - m*c), rounded to bf16 for the PV product; the row
+            // sum accumulates the same rounded values (v_dot2 with ones).
+            float psum = 0.f;
+            bf16x2 pw[2][8];
+#pragma unroll
+            for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+                for (int i = 0; i < 16; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
+                    pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
+                    psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
+                }
+            l_run = l_run * alpha + psum;
+            m_run = m_new;
+
+            if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+                    acc[cb] *= alpha;
+            }
+
+            // O^T += V^T P^T over four 16-key slices.
+#pragma unroll
+            for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+                for (int ss = 0; ss < 2; ss++) {
+                    bf16x8 pf;
+#pragma unroll
+                    for (int j = 0; j < 4; j++) {
+                        pf[2 * j] = pw[sb][ss * 4 + j][0];
+                        pf[2 * j + 1] = pw[sb][ss * 4 + j][1];
+                    }
+#pragma unroll
+                    for (int cb = 0; cb < D / 32; cb++) {
+                        const bf16x8 vf = read_vt_frag(
+                            &cur.v[sb * 32 + ss * 16 + vt_row][cb * 32 + vt_col], D + kVPad);
+                        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
+                    }
                 }
         }
-
-        float mx = kNegInf;
-#pragma unroll
-        for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-            for (int i = 0; i < 16; i++)
-                mx = fmaxf(mx, s[sb][i]);
-        mx = pair_max(mx);
-        const float m_new = fmaxf(m_run, mx);
-        const float mc = (m_new == kNegInf) ? 0.f : m_new * c;
-        const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
-
-        float psum = 0.f;
-        uint32_t pw[2][8];
-#pragma unroll
-        for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
-                psum += p0 + p1;
-                pw[sb][i >> 1] = pack_bf16x2(p0, p1);
-            }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-
-        if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-            for (int cb = 0; cb < D / 32; cb++)
-                acc[cb] *= alpha;
-        }
-
-        // O^T += V^T P^T over four 16-key slices.
-#pragma unroll
-        for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-            for (int ss = 0; ss < 2; ss++) {
-                u32x4 pu = {pw[sb][ss * 4 + 0], pw[sb][ss * 4 + 1], pw[sb][ss * 4 + 2],
-                            pw[sb][ss * 4 + 3]};
-                const bf16x8 pf = __builtin_bit_cast(bf16x8, pu);
-#pragma unroll
-                for (int cb = 0; cb < D / 32; cb++) {
-                    const bf16x8 vf =
-                        *(const bf16x8 *)&sm.vt[cb * 32 + m][sb * 32 + ss * 16 + g * 8];
-                    acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
-                }
-            }
+        if (more)
+            store_tile<D>(sm[(kb + 1 - kb_lo) & 1], st, tid);
+        __syncthreads();
     }
-
     const float l_tot = pair_sum(l_run);
     if (!(wave_valid && row_valid))
         return;
@@ -319,7 +337,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
 template <int D, int MODE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
-    __shared__ Smem<D> sm;
+    __shared__ Smem<D> sm[2];
     if (MODE == kModeGlobal) {
         // Persistent workgroups pull (tile, head group) items from the queue
         // of their XCD (workgroups are dispatched round-robin over the 8
