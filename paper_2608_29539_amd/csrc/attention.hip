@@ -70,27 +70,29 @@ struct Stage {
     u32x4 v[kChunks];
 };
 
-// Global -> registers: keys [k0, k0+64) of one sequence.  Keys at or past
-// the sequence end load as zeros (they are masked, and zero values keep
-// masked-out products finite).
+// Buffer resource word 3 for raw (untyped, stride 0) buffer loads.
+constexpr int kRawBufferFlags = 0x00020000;
+
+// Global -> registers: keys [k0, k0+64) of one sequence through buffer loads.
+// The resource descriptor is rebuilt per tile on the scalar unit: its base is
+// the tile's first key row of this KV head and its size covers exactly the
+// rows that exist, so rows at or past the sequence end read as zeros (the
+// hardware range check) -- masked keys with zero values keep the masked-out
+// products finite.  Each thread's byte offset inside a tile is fixed.
 template <int D>
-__device__ __forceinline__ void load_tile(Stage<D> &st, const uint16_t *__restrict__ K,
-                                          const uint16_t *__restrict__ V, int64_t base,
-                                          int T, int k0, int hkv, int kvh, int tid) {
-    const int64_t rs = (int64_t)hkv * D;
+__device__ __forceinline__ void load_tile(Stage<D> &st, const uint16_t *kv_k, const uint16_t *kv_v,
+                                          int T, int k0, int row_bytes, const int *voff) {
+    const int rows = min(kBlockN, T - k0);
+    const int nbytes = rows > 0 ? rows * row_bytes : 0;
+    const long long shift = (long long)k0 * row_bytes;
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)kv_k + shift), (short)0, nbytes, kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)kv_v + shift), (short)0, nbytes, kRawBufferFlags);
 #pragma unroll
     for (int i = 0; i < Stage<D>::kChunks; i++) {
-        const int c = tid + i * kThreads;
-        const int r = c / (D / 8), cc = c % (D / 8);
-        const int key = k0 + r;
-        if (key < T) {
-            const int64_t off = (base + key) * rs + (int64_t)kvh * D + cc * 8;
-            st.k[i] = *(const u32x4 *)(K + off);
-            st.v[i] = *(const u32x4 *)(V + off);
-        } else {
-            st.k[i] = u32x4{0, 0, 0, 0};
-            st.v[i] = u32x4{0, 0, 0, 0};
-        }
+        st.k[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff[i], 0, 0));
+        st.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff[i], 0, 0));
     }
 }
 
@@ -135,22 +137,36 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 // Attention for one work item: a tile of rows x the heads of one head group.
 //   Local / dense: tile jt of sequence b, rows = tokens jt*tpw ...
 //   Global: rows = sel_idx[first .. first+nrows), all in sequence b.
+//
+// Online softmax with a lazily moved reference max: a row's reference m_ref
+// only moves (rescaling O and l) when a tile's max exceeds it by more than
+// 2^kLazy in the exp2 domain, so probabilities stay <= 2^kLazy and most tiles
+// skip the rescale.  The result is the same softmax after the final O / l.
+constexpr float kLazy = 8.f;
+
+// Wave-uniform value, made explicit so the compiler keeps it in SGPRs.
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
 template <int D, int MODE>
 __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int b, int hg,
                                             int jt, SparseTile tile) {
-    const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uni(tid >> 6);
     const int g = lane >> 5, m = lane & 31;
-    const int64_t base = a.cu_seqlens[b];
-    const int T = a.cu_seqlens[b + 1] - (int)base;
+    b = uni(b);
+    hg = uni(hg);
+    const int64_t base = uni(a.cu_seqlens[b]);
+    const int T = uni(a.cu_seqlens[b + 1] - (int)base);
     const int hw = wave % a.hpw, tb = wave / a.hpw;
     const int head = hg * a.hpw + hw;
     const int kvh = (hg * a.hpw) / a.group;
 
     int nvalid, wg_pmin, wg_pmax;
     if (MODE == kModeGlobal) {
-        nvalid = tile.nrows;
-        wg_pmax = tile.pos_max;
-        wg_pmin = a.sel_idx[tile.first] - (int)base;
+        tile.first = uni(tile.first);
+        nvalid = uni(tile.nrows);
+        wg_pmax = uni(tile.pos_max);
+        wg_pmin = uni(a.sel_idx[tile.first] - (int)base);
     } else {
         const int p0 = jt * a.tpw;
         nvalid = min(a.tpw, T - p0);
@@ -185,42 +201,59 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
             qf[s] = *(const bf16x8 *)(qp + s * 16);
     }
 
-    // lane's row / column inside a V tile for the transpose reads
+    // Lane's row / column inside a V tile for the transpose reads.
     const int vt_row = 4 * g + ((lane & 15) >> 2);
     const int vt_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
     const int w = a.window;
     const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
     const int kb_lo = lo / kBlockN, kb_hi = wg_pmax / kBlockN;
+    // Tiles this wave computes: a contiguous, wave-uniform sub-range.
+    int kb_first = kb_lo, kb_last = wpmax / kBlockN;
+    if (MODE == kModeLocal)
+        kb_first = max(kb_lo, max(0, wpmin - w + 1) / kBlockN);
+    if (!wave_valid) {
+        kb_first = kb_hi + 1;
+        kb_last = kb_hi;
+    }
     const float c = a.scale_log2;
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+
+    // K/V base of this sequence and KV head, and this thread's fixed byte
+    // offsets inside a tile.
+    const int row_bytes = a.hkv * D * 2;
+    const uint16_t *kv_k = a.k + (base * a.hkv + kvh) * (int64_t)D;
+    const uint16_t *kv_v = a.v + (base * a.hkv + kvh) * (int64_t)D;
+    int voff[Stage<D>::kChunks];
+#pragma unroll
+    for (int i = 0; i < Stage<D>::kChunks; i++) {
+        const int cidx = tid + i * kThreads;
+        voff[i] = (cidx / (D / 8)) * row_bytes + (cidx % (D / 8)) * 16;
+    }
 
     f32x16 acc[D / 32];
 #pragma unroll
     for (int cb = 0; cb < D / 32; cb++)
         acc[cb] = f32x16{};
-    float m_run = kNegInf, l_run = 0.f;
+    float m_ref = kNegInf, l_run = 0.f;
 
     // Double-buffered K/V tiles: tile kb is computed from buffer (kb-kb_lo)&1
     // while tile kb+1 travels global -> registers -> the other buffer; one
     // barrier per tile separates the two.
     Stage<D> st;
-    load_tile<D>(st, a.k, a.v, base, T, kb_lo * kBlockN, a.hkv, kvh, tid);
+    load_tile<D>(st, kv_k, kv_v, T, kb_lo * kBlockN, row_bytes, voff);
     __syncthreads();                         // the previous item's last tile is consumed
     store_tile<D>(sm[0], st, tid);
     __syncthreads();
 
-    for (int kb = kb_lo; kb <= kb_hi; kb++) {
+    // One KV tile: stage the next tile around the (optional) compute.
+    auto step = [&](int kb, bool compute) {
         const Smem<D> &cur = sm[(kb - kb_lo) & 1];
         const bool more = kb < kb_hi;
         if (more)
-            load_tile<D>(st, a.k, a.v, base, T, (kb + 1) * kBlockN, a.hkv, kvh, tid);
-
-        const int k0 = kb * kBlockN;
-        bool active = wave_valid && k0 <= wpmax;
-        if (MODE == kModeLocal)
-            active = active && (k0 + kBlockN - 1 >= wpmin - w + 1);
-        if (active) {
+            load_tile<D>(st, kv_k, kv_v, T, (kb + 1) * kBlockN, row_bytes, voff);
+        if (compute) {
+            const int k0 = kb * kBlockN;
             // S^T = K Q^T for two 32-key halves.
             f32x16 s[2];
 #pragma unroll
@@ -232,7 +265,6 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
                     s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
                 }
             }
-
             bool need_mask = (k0 + kBlockN - 1 > wpmin);
             if (MODE == kModeLocal)
                 need_mask = need_mask || (k0 < wpmax - w + 1);
@@ -249,21 +281,30 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
                             s[sb][i] = kNegInf;
                     }
             }
-
             float mx = kNegInf;
 #pragma unroll
             for (int sb = 0; sb < 2; sb++)
 #pragma unroll
                 for (int i = 0; i < 16; i++)
                     mx = fmaxf(mx, s[sb][i]);
-            mx = pair_max(mx);
-            const float m_new = fmaxf(m_run, mx);
-            const float mc = (m_new == kNegInf) ? 0.f : m_new * c;
-            const float alpha = __builtin_amdgcn_exp2f(fmaf(m_run, c, -mc));
+            mx = pair_max(mx) * c;           // tile max in the exp2 domain
+            // Move the reference only when the new max is far above it.
+            const bool move = mx > m_ref + kLazy;
+            if (__builtin_amdgcn_ballot_w64(move)) {
+                // lanes that keep their reference scale by exactly 1 (a lane
+                // whose rows are still fully masked has m_ref = -inf)
+                const float m_new = move ? mx : m_ref;
+                const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+                    acc[cb] *= alpha;
+                l_run *= alpha;
+                m_ref = m_new;
+            }
+            const float mc = (m_ref == kNegInf) ? 0.f : m_ref;
 
-            // P = exp2(s*c - m*c), rounded to bf16 for the PV product; the row
-            // sum accumulates the same rounded values (v_dot2 with ones).
-            float psum = 0.f;
+            // P = exp2(s*c - m_ref), rounded to bf16 for the PV product; the
+            // row sum accumulates the same rounded values (v_dot2 with ones).
             bf16x2 pw[2][8];
 #pragma unroll
             for (int sb = 0; sb < 2; sb++)
@@ -272,16 +313,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
                     const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
                     const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
                     pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
-                    psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
+                    l_run = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, l_run, false);
                 }
-            l_run = l_run * alpha + psum;
-            m_run = m_new;
-
-            if (__builtin_amdgcn_ballot_w64(alpha != 1.f)) {
-#pragma unroll
-                for (int cb = 0; cb < D / 32; cb++)
-                    acc[cb] *= alpha;
-            }
 
             // O^T += V^T P^T over four 16-key slices.
 #pragma unroll
@@ -305,7 +338,18 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         if (more)
             store_tile<D>(sm[(kb + 1 - kb_lo) & 1], st, tid);
         __syncthreads();
-    }
+    };
+
+    // Every wave walks all tiles of the workgroup's range (they share the
+    // staging and the barriers) but computes only its own sub-range.
+    int kb = kb_lo;
+    for (; kb < kb_first && kb <= kb_hi; kb++)
+        step(kb, false);
+    for (; kb <= kb_last; kb++)
+        step(kb, true);
+    for (; kb <= kb_hi; kb++)
+        step(kb, false);
+
     const float l_tot = pair_sum(l_run);
     if (!(wave_valid && row_valid))
         return;
@@ -351,7 +395,7 @@ void attn_kernel(const AttnArgs a) {
             if (threadIdx.x == 0)
                 s_item = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
             __syncthreads();
-            const int item = s_item;
+            const int item = __builtin_amdgcn_readfirstlane(s_item);
             __syncthreads();
             if (item >= n_items)
                 break;
