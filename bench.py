@@ -54,6 +54,31 @@ def pair_counts(cu: np.ndarray, window: int, sel_idx: np.ndarray):
     return p_local, p_global, p_dense
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_global_T32k-gqa_traffic.md")
+KERNEL_SRC = os.path.join(ROOT, "paper_2608_29539_amd", "csrc", "attention.hip")
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per launch of the global kernel from the committed counter
+    summary, or None when the summary is missing, is for another workload, or
+    was taken on a different kernel source than the one built now."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    fields = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.startswith("- "):
+            k, v = line[2:].split(":", 1)
+            fields[k.strip()] = v.strip().strip("`")
+    src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    if fields.get("workload") != workload or fields.get("kernel_source_sha256") != src_hash:
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(x, w, stride: int, log_fn=log):
     """Time the fp64 oracle on every stride-th token row (and every stride-th
     selected row) of the workload; return a cpu_baseline record."""
@@ -93,6 +118,9 @@ def main(argv=None):
                     help="oracle sample stride (0 = pick one for ~10-30 s of CPU work)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense baseline")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before timing, run one plain device-to-device copy of MIB MiB "
+                         "(the reference kernel for scaling FETCH_SIZE / WRITE_SIZE)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -130,6 +158,16 @@ def main(argv=None):
     thr = torch.empty(B, dtype=torch.float32, device="cuda")
     ws = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_FWD, cap), dtype=torch.uint8,
                      device="cuda")
+
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: {nbytes} bytes copied")
+        del src, dst
 
     n_ev = args.steps + args.warmup
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(n_ev)]
@@ -206,7 +244,8 @@ def main(argv=None):
 
     roofline = {"bound": "mfma", "kernel": "attn_kernel<128, global> (query-sparse global branch)",
                 "achieved": round(global_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4),
+                "traffic": committed_traffic(w.name),
                 "flops_per_launch": fl * p_global,
                 "duration_ms": round(stage_ms["global"], 4)}
 
