@@ -167,14 +167,23 @@ logo_status logo_combine(const logo_problem *p, const float *o_local, const floa
 /*
  * logo_attn_fwd -- the whole layer: select, local branch, query-sparse
  * global branch, ContextNorm and fusion, in one stream-ordered sequence with
- * no host synchronisation (Sec. 3.2-3.3).
+ * no host synchronisation (Sec. 3.2-3.3).  ContextNorm and the fusion run in
+ * the epilogues of the two attention kernels: the local kernel writes
+ * Norm^L(O^L) (bf16) for unselected tokens and keeps (1-p) Norm^L(O^L) (fp32,
+ * workspace) for selected ones, which the global kernel completes.
  *   q_g/k_g/v_g: global-branch tensors of the same shapes as q/k/v, or NULL
  *   to use q/k/v (the identity branch transform of Eq. branch-transform).
+ *   gain_local / gain_global [Hq][d] fp32 or NULL (= 1); eps >= 0.
  *   sel_idx [sel_capacity], cu_sel [B+1], tok2sel [N], thr_out [B]: outputs
  *   as for logo_select; each may be NULL, in which case it lives in the
- *   workspace (sel_idx NULL requires sel_capacity = 0, meaning "size it for
- *   the worst case of the mode").  out [N][Hq][d] bf16.
- *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD, sel_capacity) bytes.
+ *   workspace.  sel_capacity bounds the selection as for logo_select; with
+ *   sel_idx NULL, 0 selects the mode's bound (ratio mode: the ratio bound,
+ *   threshold mode: N).  In threshold mode, tokens past the capacity are
+ *   fused as unselected (cu_sel[B] > sel_capacity reports it).
+ *   out [N][Hq][d] bf16.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD, sel_capacity) bytes,
+ *   256-byte aligned (selection scratch, tile table, queue counters and the
+ *   compact fp32 buffer of the selected rows).
  */
 logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                           const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
@@ -189,9 +198,12 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
  * logo_attn_fwd_profiled -- logo_attn_fwd that additionally records five
  * caller-created HIP events (hipEvent_t, passed as void*) on `stream`:
  *   events[0] before the selection kernels, events[1] after them,
- *   events[2] after the local branch, events[3] after the global branch
- *   (tile plan + query-sparse attention), events[4] after ContextNorm and
- *   fusion.  Elapsed times between consecutive events are the stage times.
+ *   events[2] after the local branch (which also applies Norm^L and writes
+ *   the unselected rows of `out`), events[3] after the global branch (tile
+ *   plan + query-sparse attention, which applies Norm^G and the fusion for
+ *   the selected rows), events[4] at the end (ContextNorm and fusion run
+ *   inside the two attention kernels, so events[3] and events[4] bracket no
+ *   work).  Elapsed times between consecutive events are the stage times.
  *   `events` must not be NULL; everything else is as for logo_attn_fwd.
  */
 logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,

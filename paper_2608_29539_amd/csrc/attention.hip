@@ -147,7 +147,7 @@ constexpr float kLazy = 8.f;
 // Wave-uniform value, made explicit so the compiler keeps it in SGPRs.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-template <int D, int MODE>
+template <int D, int MODE, int EPI>
 __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int b, int hg,
                                             int jt, SparseTile tile) {
     const int tid = threadIdx.x, lane = tid & 63;
@@ -351,9 +351,69 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         step(kb, false);
 
     const float l_tot = pair_sum(l_run);
+    const float inv = 1.f / l_tot;
+    if (EPI == kEpiFused && MODE != kModeDense) {
+        // ContextNorm over the row's d values: this lane holds d/2 of them,
+        // its partner l^32 the other half.
+        float ss = 0.f;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int i = 0; i < 16; i++) {
+                const float o = acc[cb][i] * inv;
+                acc[cb][i] = o;
+                ss = fmaf(o, o, ss);
+            }
+        ss = pair_sum(ss);
+        if (!(wave_valid && row_valid))
+            return;
+        const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
+        const int64_t tok = qtok;
+        const float p = a.gate[tok];
+        const int r = (MODE == kModeGlobal) ? (int)orow : a.tok2sel[tok];
+        const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
+        uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
+        if (MODE == kModeLocal && r >= 0) {
+            // selected token: keep (1-p) Norm^L in fp32 for the global kernel
+            float *lp = a.lc + ((int64_t)r * a.hq + head) * D + g * 4;
+            const float wgt = (1.f - p) * rn;
+#pragma unroll
+            for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+                for (int qd = 0; qd < 4; qd++) {
+                    f32x4 gn = {1.f, 1.f, 1.f, 1.f};
+                    if (gp)
+                        gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
+                    f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
+                               acc[cb][qd * 4 + 3]};
+                    *(f32x4 *)(lp + cb * 32 + qd * 8) = v * gn * wgt;
+                }
+            return;
+        }
+        const float *lp = (MODE == kModeGlobal)
+                              ? a.lc + ((int64_t)r * a.hq + head) * D + g * 4 : nullptr;
+        const float wgt = (MODE == kModeGlobal) ? p * rn : rn;
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int qd = 0; qd < 4; qd++) {
+                f32x4 gn = {1.f, 1.f, 1.f, 1.f};
+                if (gp)
+                    gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
+                f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
+                           acc[cb][qd * 4 + 3]};
+                v = v * gn * wgt;
+                if (MODE == kModeGlobal)
+                    v += *(const f32x4 *)(lp + cb * 32 + qd * 8);
+                u32x2 o;
+                o.x = pack_bf16x2(v.x, v.y);
+                o.y = pack_bf16x2(v.z, v.w);
+                *(u32x2 *)(op + cb * 32 + qd * 8) = o;
+            }
+        return;
+    }
     if (!(wave_valid && row_valid))
         return;
-    const float inv = 1.f / l_tot;
     if (MODE == kModeDense) {
         uint16_t *op = (uint16_t *)a.out + (orow * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
@@ -378,7 +438,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     }
 }
 
-template <int D, int MODE>
+template <int D, int MODE, int EPI>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
     __shared__ Smem<D> sm[2];
@@ -400,7 +460,7 @@ void attn_kernel(const AttnArgs a) {
             if (item >= n_items)
                 break;
             const SparseTile t = a.tiles[item / a.n_hg];
-            attend_item<D, MODE>(a, sm, t.seq, item % a.n_hg, 0, t);
+            attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
         }
     } else {
         const int hg = blockIdx.x % a.n_hg;
@@ -412,38 +472,44 @@ void attn_kernel(const AttnArgs a) {
         const int T = a.cu_seqlens[b + 1] - a.cu_seqlens[b];
         if (jt * a.tpw >= T)
             return;
-        attend_item<D, MODE>(a, sm, b, hg, jt, SparseTile{0, 0, 0, 0});
+        attend_item<D, MODE, EPI>(a, sm, b, hg, jt, SparseTile{0, 0, 0, 0});
     }
 }
 
-template <int D, int MODE>
+template <int D, int MODE, int EPI>
 hipError_t launch_one(const AttnArgs &a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<D, MODE, EPI>), dim3(grid), dim3(kThreads), 0, s, a);
     return hipGetLastError();
 }
 
 template <int D, int MODE>
 int blocks_per_cu_one() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE>, kThreads, 0) !=
-        hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE, kEpiRaw>, kThreads,
+                                                     0) != hipSuccess)
         return 1;
     return n > 0 ? n : 1;
 }
 
+template <int D>
+hipError_t launch_d(int mode, int epi, const AttnArgs &a, int grid, hipStream_t s) {
+    if (mode == kModeLocal)
+        return epi == kEpiFused ? launch_one<D, kModeLocal, kEpiFused>(a, grid, s)
+                                : launch_one<D, kModeLocal, kEpiRaw>(a, grid, s);
+    if (mode == kModeGlobal)
+        return epi == kEpiFused ? launch_one<D, kModeGlobal, kEpiFused>(a, grid, s)
+                                : launch_one<D, kModeGlobal, kEpiRaw>(a, grid, s);
+    return launch_one<D, kModeDense, kEpiRaw>(a, grid, s);
+}
+
 }  // namespace
 
-hipError_t launch_attention(int mode, int head_dim, const AttnArgs &a, int grid, hipStream_t s) {
+hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, int grid,
+                            hipStream_t s) {
     if (grid <= 0)
         return hipSuccess;
-    if (head_dim == 128) {
-        if (mode == kModeLocal) return launch_one<128, kModeLocal>(a, grid, s);
-        if (mode == kModeGlobal) return launch_one<128, kModeGlobal>(a, grid, s);
-        return launch_one<128, kModeDense>(a, grid, s);
-    }
-    if (mode == kModeLocal) return launch_one<64, kModeLocal>(a, grid, s);
-    if (mode == kModeGlobal) return launch_one<64, kModeGlobal>(a, grid, s);
-    return launch_one<64, kModeDense>(a, grid, s);
+    return head_dim == 128 ? launch_d<128>(mode, epi, a, grid, s)
+                           : launch_d<64>(mode, epi, a, grid, s);
 }
 
 int attention_blocks_per_cu(int mode, int head_dim) {

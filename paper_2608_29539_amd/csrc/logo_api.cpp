@@ -122,8 +122,10 @@ GlobalWs global_ws(const logo_problem *p, int32_t cap) {
     return w;
 }
 
+// logo_attn_fwd runs the fused epilogues, so its only large buffer is the
+// compact fp32 (1-p) Norm^L of the selected rows.
 struct FwdWs {
-    size_t sel, sel_ws, glob_ws, o_local, o_global, sel_idx, cu_sel, tok2sel, thr, total;
+    size_t sel_ws, glob_ws, lc, sel_idx, cu_sel, tok2sel, thr, total;
 };
 FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
     const size_t row = (size_t)p->num_q_heads * p->head_dim * sizeof(float);
@@ -133,9 +135,7 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
     off += align_up(select_ws(p).total);
     w.glob_ws = off;
     off += align_up(global_ws(p, cap).total);
-    w.o_local = off;
-    off += align_up(row * (size_t)p->total_tokens);
-    w.o_global = off;
+    w.lc = off;
     off += align_up(row * (size_t)cap);
     w.sel_idx = off;
     off += align_up(sizeof(int32_t) * (size_t)cap);
@@ -146,7 +146,6 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
     w.thr = off;
     off += align_up(sizeof(float) * (size_t)p->num_seqs);
     w.total = off;
-    w.sel = 0;
     return w;
 }
 
@@ -205,8 +204,29 @@ logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode m
                       s);
 }
 
+// Fused-epilogue inputs (logo_attn_fwd only).
+struct FusedEpi {
+    const int32_t *tok2sel;
+    const float *gate;
+    const float *gain;
+    float eps;
+    float *lc;
+    logo_bf16 *out;
+};
+
+void set_fused(AttnArgs &a, const FusedEpi *f, const float *gain) {
+    a.tok2sel = f->tok2sel;
+    a.gate = f->gate;
+    a.gain = gain;
+    a.eps = f->eps;
+    a.lc = f->lc;
+    a.out_bf16 = f->out;
+}
+
+// o: raw fp32 O^L (f == NULL) or the fused epilogue (f != NULL).
 logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
-                      const logo_bf16 *v, float *o, hipStream_t s) {
+                      const logo_bf16 *v, float *o, const FusedEpi *f, const float *gain,
+                      hipStream_t s) {
     if (p->total_tokens == 0)
         return LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
@@ -215,15 +235,19 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
     a.k = k;
     a.v = v;
     a.out = o;
+    if (f)
+        set_fused(a, f, gain);
     const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max;
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
-    return hip_status(launch_attention(kModeLocal, p->head_dim, a, (int)grid, s), s);
+    return hip_status(
+        launch_attention(kModeLocal, f ? kEpiFused : kEpiRaw, p->head_dim, a, (int)grid, s), s);
 }
 
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                        const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
-                       int32_t cap, float *o, char *ws, hipStream_t s) {
+                       int32_t cap, float *o, const FusedEpi *f, const float *gain, char *ws,
+                       hipStream_t s) {
     if (p->total_tokens == 0 || cap == 0)
         return LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
@@ -245,6 +269,8 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     a.sel_idx = sel_idx;
     a.tiles = tiles;
     a.queue = queue;
+    if (f)
+        set_fused(a, f, gain);
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -252,7 +278,8 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     const int per_cu = attention_blocks_per_cu(kModeGlobal, p->head_dim);
     int grid = cus * per_cu;
     grid = ((grid + kQueues - 1) / kQueues) * kQueues;
-    return hip_status(launch_attention(kModeGlobal, p->head_dim, a, grid, s), s);
+    return hip_status(
+        launch_attention(kModeGlobal, f ? kEpiFused : kEpiRaw, p->head_dim, a, grid, s), s);
 }
 
 logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
@@ -293,8 +320,7 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     if (st != LOGO_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
-    float *ol = (float *)(base + w.o_local);
-    float *og = (float *)(base + w.o_global);
+    const FusedEpi fe{t2s, gate, nullptr, eps, (float *)(base + w.lc), out};
     auto mark = [&](int i) -> logo_status {
         if (events && hipEventRecord((hipEvent_t)events[i], s) != hipSuccess)
             return LOGO_ERR_HIP;
@@ -306,17 +332,15 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
     if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
         return st;
-    st = run_local(p, q, k, v, ol, s);
+    // Local branch with the fused epilogue: Norm^L(O^L) straight to `out`
+    // for unselected tokens, (1-p) Norm^L(O^L) to the compact buffer for
+    // selected ones.  Then the global branch finishes the selected rows.
+    st = run_local(p, q, k, v, nullptr, &fe, gain_local, s);
     if (st != LOGO_OK || (st = mark(2)) != LOGO_OK)
         return st;
-    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, og,
-                    base + w.glob_ws, s);
+    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, nullptr, &fe,
+                    gain_global, base + w.glob_ws, s);
     if (st != LOGO_OK || (st = mark(3)) != LOGO_OK)
-        return st;
-    st = hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, ol, og, gate,
-                                   t2s, gain_local, gain_global, eps, 1, out, s),
-                    s);
-    if (st != LOGO_OK)
         return st;
     return mark(4);
 }
@@ -385,7 +409,7 @@ logo_status logo_local_attn(const logo_problem *p, const logo_bf16 *q, const log
         return st;
     if (p->total_tokens > 0 && (!q || !k || !v || !o_local))
         return LOGO_ERR_NULL;
-    return run_local(p, q, k, v, o_local, (hipStream_t)stream);
+    return run_local(p, q, k, v, o_local, nullptr, nullptr, (hipStream_t)stream);
 }
 
 logo_status logo_global_attn_sparse_q(const logo_problem *p, const logo_bf16 *q,
@@ -407,8 +431,8 @@ logo_status logo_global_attn_sparse_q(const logo_problem *p, const logo_bf16 *q,
         if (st != LOGO_OK)
             return st;
     }
-    return run_global(p, q, k, v, sel_idx, cu_sel, sel_capacity, o_global, (char *)ws,
-                      (hipStream_t)stream);
+    return run_global(p, q, k, v, sel_idx, cu_sel, sel_capacity, o_global, nullptr, nullptr,
+                      (char *)ws, (hipStream_t)stream);
 }
 
 logo_status logo_combine(const logo_problem *p, const float *o_local, const float *o_global,
@@ -481,7 +505,7 @@ logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
     hipStream_t s = (hipStream_t)stream;
-    return hip_status(launch_attention(kModeDense, p->head_dim, a, (int)grid, s), s);
+    return hip_status(launch_attention(kModeDense, kEpiRaw, p->head_dim, a, (int)grid, s), s);
 }
 
 }  // extern "C"

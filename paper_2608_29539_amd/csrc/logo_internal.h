@@ -45,6 +45,15 @@ struct SparseTile {
 
 enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
 
+// Epilogue of the local / global modes.
+//   kEpiRaw   : write the branch output O (fp32) -- logo_local_attn and
+//               logo_global_attn_sparse_q.
+//   kEpiFused : ContextNorm + output fusion in place (logo_attn_fwd): the local
+//               kernel writes bf16 Norm^L(O^L) to `out` for unselected tokens and
+//               (1-p) Norm^L(O^L) (fp32) to the compact buffer `lc` for selected
+//               ones; the global kernel then writes bf16 lc + p Norm^G(O^G).
+enum AttnEpi { kEpiRaw = 0, kEpiFused = 1 };
+
 struct AttnArgs {
     const uint16_t *q;
     const uint16_t *k;
@@ -60,10 +69,17 @@ struct AttnArgs {
     int32_t window;
     int32_t ntile_max;         // local/dense: ceil(max_seqlen / tpw)
     float scale_log2;          // softmax_scale * log2(e)
+    // fused epilogue only
+    const int32_t *tok2sel;    // [N] rank or -1
+    const float *gate;         // [N]
+    const float *gain;         // [Hq][d] of this branch, or NULL (= 1)
+    float eps;
+    float *lc;                 // [capacity][Hq][d] fp32: (1-p) Norm^L of selected rows
+    uint16_t *out_bf16;        // [N][Hq][d]
 };
 
 // Launchers (return hipSuccess or the launch error).
-hipError_t launch_attention(int mode, int head_dim, const AttnArgs &a, int grid,
+hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, int grid,
                             hipStream_t s);
 int attention_blocks_per_cu(int mode, int head_dim);
 

@@ -162,8 +162,9 @@ def test_global_combine_fwd_validation(lib):
 def test_workspace_sizes(lib):
     p = Prob(seqlens=(32768,), hq=32, hkv=8, d=128, window=1024)
     fwd = lib.logo_workspace_bytes(p.c, 4, 4096)
-    # fp32 O^L (N x Hq x d) + compact fp32 O^G (cap x Hq x d) dominate
-    assert fwd >= 32768 * 32 * 128 * 4 + 4096 * 32 * 128 * 4
+    # the compact fp32 (1-p) Norm^L rows of the selected tokens dominate;
+    # no full-size fp32 branch buffer is needed by the fused path
+    assert 4096 * 32 * 128 * 4 <= fwd < 32768 * 32 * 128 * 4
     assert lib.logo_workspace_bytes(p.c, 1, 0) == 0
     assert lib.logo_workspace_bytes(p.c, 5, 0) == 0
     assert lib.logo_workspace_bytes(p.c, 2, 4096) % 256 == 0
