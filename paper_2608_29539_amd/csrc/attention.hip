@@ -18,8 +18,8 @@
 // 8*(i/4) + 4*(l/32) + i%4 of the 32x32 accumulator).  The kernel computes
 // S^T = K Q^T, so each lane's accumulator column is ONE query: row max and
 // row sum need only the lane and its partner l^32.  The same registers,
-// rounded to bf16, are directly the B operand of O^T = V^T P^T when the key
-// order of the V^T tile in LDS is permuted to match (see store_tile).  O^T
+// rounded to bf16, are directly the B operand of O^T = V^T P^T when the V^T
+// operand is read from LDS in the matching key order (see read_vt_frag).  O^T
 // again has one query per lane column, so the online-softmax rescale is a
 // per-lane multiply.
 //
@@ -27,6 +27,8 @@
 // visible (no predicate), beyond its last row (skipped) or on the diagonal /
 // window edge (real-position mask on each score).
 #include "logo_internal.h"
+
+#include <type_traits>
 
 namespace logo {
 namespace {
@@ -63,49 +65,89 @@ __device__ __forceinline__ float pair_sum(float x) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D>
-struct Stage {
-    static constexpr int kChunks = kBlockN * D / 8 / kThreads;   // 16-byte chunks per thread
-    u32x4 k[kChunks];
-    u32x4 v[kChunks];
-};
-
 // Buffer resource word 3 for raw (untyped, stride 0) buffer loads.
 constexpr int kRawBufferFlags = 0x00020000;
 
-// Global -> registers: keys [k0, k0+64) of one sequence through buffer loads.
-// The resource descriptor is rebuilt per tile on the scalar unit: its base is
-// the tile's first key row of this KV head and its size covers exactly the
-// rows that exist, so rows at or past the sequence end read as zeros (the
-// hardware range check) -- masked keys with zero values keep the masked-out
-// products finite.  Each thread's byte offset inside a tile is fixed.
+// K/V tiles go global -> LDS directly (buffer_load_dwordx4 ... lds): each
+// wave-instruction writes 64 consecutive 16-byte LDS slots (lane i at
+// M0 + 16 i), so a padded tile is filled as a sequence of 1 KB slot runs; a
+// lane whose slot is row padding re-loads the row's last chunk (never read).
+// The per-lane byte offsets inside a tile are fixed and computed once.
 template <int D>
-__device__ __forceinline__ void load_tile(Stage<D> &st, const uint16_t *kv_k, const uint16_t *kv_v,
-                                          int T, int k0, int row_bytes, const int *voff) {
-    const int rows = min(kBlockN, T - k0);
-    const int nbytes = rows > 0 ? rows * row_bytes : 0;
-    const long long shift = (long long)k0 * row_bytes;
-    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)kv_k + shift), (short)0, nbytes, kRawBufferFlags);
-    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)kv_v + shift), (short)0, nbytes, kRawBufferFlags);
+struct Dma {
+    static constexpr int kSlotsK = (D + kKPad) * 2 / 16;     // 16-byte slots per K row
+    static constexpr int kSlotsV = (D + kVPad) * 2 / 16;
+    static constexpr int kInstK = kSlotsK;                   // 64 rows x slots / 64 lanes
+    static constexpr int kInstV = kSlotsV;
+    static constexpr int kPerWaveK = (kInstK + kWaves - 1) / kWaves;
+    static constexpr int kPerWaveV = (kInstV + kWaves - 1) / kWaves;
+    int voff_k[kPerWaveK];
+    int voff_v[kPerWaveV];
+};
+
+template <int D>
+__device__ __forceinline__ void dma_plan(Dma<D> &d, int wave, int lane, int row_bytes) {
 #pragma unroll
-    for (int i = 0; i < Stage<D>::kChunks; i++) {
-        st.k[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, voff[i], 0, 0));
-        st.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff[i], 0, 0));
+    for (int i = 0; i < Dma<D>::kPerWaveK; i++) {
+        const int slot = (i * kWaves + wave) * 64 + lane;
+        const int row = slot / Dma<D>::kSlotsK, col = min(slot % Dma<D>::kSlotsK, D / 8 - 1);
+        d.voff_k[i] = row * row_bytes + col * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < Dma<D>::kPerWaveV; i++) {
+        const int slot = (i * kWaves + wave) * 64 + lane;
+        const int row = slot / Dma<D>::kSlotsV, col = min(slot % Dma<D>::kSlotsV, D / 8 - 1);
+        d.voff_v[i] = row * row_bytes + col * 16;
     }
 }
 
-// Registers -> LDS, a plain row-major copy of both tiles.
+// Descriptor of one tile: base = its first key row of this KV head, size =
+// the rows that exist, so rows at or past the sequence end read as zeros
+// (masked keys with zero values keep masked-out products finite).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t *kv, int T, int k0,
+                                                            int row_bytes) {
+    const int rows = min(kBlockN, T - k0);
+    const int nbytes = rows > 0 ? rows * row_bytes : 0;
+    return __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)kv + (long long)k0 * row_bytes), (short)0, nbytes,
+        kRawBufferFlags);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One 16-byte-per-lane global -> LDS load (non-template wrapper: the host
+// compilation pass rejects this builtin inside templates).
+__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, void *lds, int voffset) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, voffset, 0, 0, 0);
+}
+
 template <int D>
-__device__ __forceinline__ void store_tile(Smem<D> &sm, const Stage<D> &st, int tid) {
+__device__ __forceinline__ void dma_k(Smem<D> &buf, const Dma<D> &d, const uint16_t *kv_k, int T,
+                                      int k0, int row_bytes, int wave) {
+    const __amdgpu_buffer_rsrc_t r = tile_rsrc(kv_k, T, k0, row_bytes);
 #pragma unroll
-    for (int i = 0; i < Stage<D>::kChunks; i++) {
-        const int c = tid + i * kThreads;
-        const int r = c / (D / 8), cc = c % (D / 8);
-        *(u32x4 *)&sm.k[r][cc * 8] = st.k[i];
-        *(u32x4 *)&sm.v[r][cc * 8] = st.v[i];
+    for (int i = 0; i < Dma<D>::kPerWaveK; i++) {
+        const int inst = i * kWaves + wave;
+        if (inst < Dma<D>::kInstK)
+            lds_load16(r, (char *)&buf.k[0][0] + inst * 1024, d.voff_k[i]);
     }
+}
+template <int D>
+__device__ __forceinline__ void dma_v(Smem<D> &buf, const Dma<D> &d, const uint16_t *kv_v, int T,
+                                      int k0, int row_bytes, int wave) {
+    const __amdgpu_buffer_rsrc_t r = tile_rsrc(kv_v, T, k0, row_bytes);
+#pragma unroll
+    for (int i = 0; i < Dma<D>::kPerWaveV; i++) {
+        const int inst = i * kWaves + wave;
+        if (inst < Dma<D>::kInstV)
+            lds_load16(r, (char *)&buf.v[0][0] + inst * 1024, d.voff_v[i]);
+    }
+}
+
+// Completion of this wave's LDS-bound loads, then the workgroup barrier.
+__device__ __forceinline__ void dma_wait_barrier() {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
 }
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -146,6 +188,69 @@ constexpr float kLazy = 8.f;
 
 // Wave-uniform value, made explicit so the compiler keeps it in SGPRs.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// Split-KV partials of the global branch.  Every entry of a split tile
+// stores its unnormalised O (relative to its reference m, exp2 domain), m
+// and l per lane, releases them, and counts itself done; the entry that
+// counts last acquires the others and folds all of them in split order, so
+// the result does not depend on which entry finished last.  Returns false
+// for the entries that are not last (nothing more to do).
+template <int D>
+__device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile &t, int hg,
+                                            int wave, int lane, f32x16 (&acc)[D / 32], float m,
+                                            float &l) {
+    __shared__ int s_last;
+    constexpr int kAccFloats = kWaves * 64 * (D / 2);
+    const int sid = uni(t.sid), split = uni(t.split), ns = uni(t.nsplit);
+    const int li = wave * 64 + lane;
+    float *base = a.partial + (int64_t)sid * a.n_hg * partial_floats(D);
+    const int64_t slot_stride = (int64_t)a.n_hg * partial_floats(D);
+    float *mine = base + split * slot_stride + (int64_t)hg * partial_floats(D);
+#pragma unroll
+    for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+        for (int qd = 0; qd < 4; qd++) {
+            f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
+                       acc[cb][qd * 4 + 3]};
+            *(f32x4 *)(mine + ((cb * 4 + qd) * (kWaves * 64) + li) * 4) = v;
+        }
+    mine[kAccFloats + li] = m;
+    mine[kAccFloats + kWaves * 64 + li] = l;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (threadIdx.x == 0)
+        s_last = atomicAdd(&a.split_cnt[sid * a.n_hg + hg], 1) == ns - 1;
+    __syncthreads();
+    const bool last = s_last;
+    if (!last)
+        return false;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    float M = kNegInf, L = 0.f;
+#pragma unroll
+    for (int cb = 0; cb < D / 32; cb++)
+        acc[cb] = f32x16{};
+    for (int j = 0; j < ns; j++) {
+        const float *pj = base + j * slot_stride + (int64_t)hg * partial_floats(D);
+        const float mj = pj[kAccFloats + li];
+        const float lj = pj[kAccFloats + kWaves * 64 + li];
+        const float mn = fmaxf(M, mj);
+        const float mc = (mn == kNegInf) ? 0.f : mn;
+        const float ra = __builtin_amdgcn_exp2f(M - mc), rb = __builtin_amdgcn_exp2f(mj - mc);
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int qd = 0; qd < 4; qd++) {
+                const f32x4 v = *(const f32x4 *)(pj + ((cb * 4 + qd) * (kWaves * 64) + li) * 4);
+#pragma unroll
+                for (int e = 0; e < 4; e++)
+                    acc[cb][qd * 4 + e] = fmaf(acc[cb][qd * 4 + e], ra, v[e] * rb);
+            }
+        L = fmaf(L, ra, lj * rb);
+        M = mn;
+    }
+    l = L;
+    return true;
+}
 
 template <int D, int MODE, int EPI>
 __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int b, int hg,
@@ -207,9 +312,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
 
     const int w = a.window;
     const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
-    const int kb_lo = lo / kBlockN, kb_hi = wg_pmax / kBlockN;
+    // KV blocks of this item: a global entry covers its own KV range
+    const int kb_lo = (MODE == kModeGlobal) ? uni(tile.kb_begin) : lo / kBlockN;
+    const int kb_hi = (MODE == kModeGlobal) ? uni(tile.kb_end) : wg_pmax / kBlockN;
     // Tiles this wave computes: a contiguous, wave-uniform sub-range.
-    int kb_first = kb_lo, kb_last = wpmax / kBlockN;
+    int kb_first = kb_lo, kb_last = min(wpmax / kBlockN, kb_hi);
     if (MODE == kModeLocal)
         kb_first = max(kb_lo, max(0, wpmin - w + 1) / kBlockN);
     if (!wave_valid) {
@@ -224,12 +331,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     const int row_bytes = a.hkv * D * 2;
     const uint16_t *kv_k = a.k + (base * a.hkv + kvh) * (int64_t)D;
     const uint16_t *kv_v = a.v + (base * a.hkv + kvh) * (int64_t)D;
-    int voff[Stage<D>::kChunks];
-#pragma unroll
-    for (int i = 0; i < Stage<D>::kChunks; i++) {
-        const int cidx = tid + i * kThreads;
-        voff[i] = (cidx / (D / 8)) * row_bytes + (cidx % (D / 8)) * 16;
-    }
+    Dma<D> dma;
+    dma_plan<D>(dma, wave, lane, row_bytes);
 
     f32x16 acc[D / 32];
 #pragma unroll
@@ -237,24 +340,68 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         acc[cb] = f32x16{};
     float m_ref = kNegInf, l_run = 0.f;
 
-    // Double-buffered K/V tiles: tile kb is computed from buffer (kb-kb_lo)&1
-    // while tile kb+1 travels global -> registers -> the other buffer; one
-    // barrier per tile separates the two.
-    Stage<D> st;
-    load_tile<D>(st, kv_k, kv_v, T, kb_lo * kBlockN, row_bytes, voff);
+    // Software-pipelined KV loop.  Iteration kb issues S(kb) = K(kb) Q^T and
+    // then PV(kb-1) (the previous tile's rounded P, kept in registers), so the
+    // softmax of tile kb overlaps the PV MFMAs of tile kb-1.  K(kb+1) and V(kb)
+    // are staged during iteration kb (V one tile later than K, because it is
+    // consumed one iteration later); two buffers each, one barrier per tile.
+    bf16x2 pw[2][8];                          // P of the last softmax-ed tile
     __syncthreads();                         // the previous item's last tile is consumed
-    store_tile<D>(sm[0], st, tid);
-    __syncthreads();
+    dma_k<D>(sm[0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
+    dma_wait_barrier();
 
-    // One KV tile: stage the next tile around the (optional) compute.
-    auto step = [&](int kb, bool compute) {
-        const Smem<D> &cur = sm[(kb - kb_lo) & 1];
-        const bool more = kb < kb_hi;
-        if (more)
-            load_tile<D>(st, kv_k, kv_v, T, (kb + 1) * kBlockN, row_bytes, voff);
-        if (compute) {
-            const int k0 = kb * kBlockN;
-            // S^T = K Q^T for two 32-key halves.
+    // PV of the tile whose P is in pw, V read from buffer vb, for one 16-key
+    // slice q (0..3) of the 64-key tile.
+    auto pv_slice = [&](const Smem<D> &vb, int q) {
+        const int sb = q >> 1, ss = q & 1;
+        bf16x8 pf;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            pf[2 * j] = pw[sb][ss * 4 + j][0];
+            pf[2 * j + 1] = pw[sb][ss * 4 + j][1];
+        }
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++) {
+            const bf16x8 vf = read_vt_frag(&vb.v[sb * 32 + ss * 16 + vt_row][cb * 32 + vt_col],
+                                           D + kVPad);
+            acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
+        }
+    };
+    auto pv = [&](const Smem<D> &vb) {
+#pragma unroll
+        for (int q = 0; q < 4; q++)
+            pv_slice(vb, q);
+    };
+    // Rescale of O decided by the previous softmax, applied before the next
+    // PV accumulates into O (deferred so that no branch separates a tile's
+    // exps from the PV MFMAs they are interleaved with).
+    bool resc_pend = false;
+    float alpha_pend = 1.f;
+    auto apply_rescale = [&]() {
+        if (resc_pend) {
+#pragma unroll
+            for (int cb = 0; cb < D / 32; cb++)
+                acc[cb] *= alpha_pend;
+            resc_pend = false;
+        }
+    };
+
+    // One KV tile.  do_s: compute S(kb) and its softmax into pw.  do_pv:
+    // also accumulate PV of the previous tile (V from the other buffer), one
+    // 16-key slice at a time, each slice's 4 MFMAs followed by the 8 exps that
+    // overwrite that slice of pw with tile kb's P.  masked: apply the
+    // real-position mask (diagonal / window-edge tiles only).
+    auto step = [&](int kb, auto do_s, auto do_pv, auto masked) {
+        const int cb_ = (kb - kb_lo) & 1;
+        // K(kb+1) into the other K buffer, V(kb) into this tile's V buffer:
+        // both were last read before the previous barrier.
+        if (kb < kb_hi)
+            dma_k<D>(sm[cb_ ^ 1], dma, kv_k, T, (kb + 1) * kBlockN, row_bytes, wave);
+        dma_v<D>(sm[cb_], dma, kv_v, T, kb * kBlockN, row_bytes, wave);
+        if constexpr (decltype(do_pv)::value)
+            apply_rescale();
+        if constexpr (decltype(do_s)::value) {
+            const Smem<D> &cur = sm[cb_];
             f32x16 s[2];
 #pragma unroll
             for (int sb = 0; sb < 2; sb++) {
@@ -265,10 +412,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
                     s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
                 }
             }
-            bool need_mask = (k0 + kBlockN - 1 > wpmin);
-            if (MODE == kModeLocal)
-                need_mask = need_mask || (k0 < wpmax - w + 1);
-            if (need_mask) {
+            if constexpr (decltype(masked)::value) {
+                const int k0 = kb * kBlockN;
 #pragma unroll
                 for (int sb = 0; sb < 2; sb++)
 #pragma unroll
@@ -288,69 +433,92 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
                 for (int i = 0; i < 16; i++)
                     mx = fmaxf(mx, s[sb][i]);
             mx = pair_max(mx) * c;           // tile max in the exp2 domain
-            // Move the reference only when the new max is far above it.
+            // The reference moves only when the new max is far above it; a
+            // lane whose rows are still fully masked keeps m_ref = -inf.
             const bool move = mx > m_ref + kLazy;
-            if (__builtin_amdgcn_ballot_w64(move)) {
-                // lanes that keep their reference scale by exactly 1 (a lane
-                // whose rows are still fully masked has m_ref = -inf)
-                const float m_new = move ? mx : m_ref;
-                const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
-#pragma unroll
-                for (int cb = 0; cb < D / 32; cb++)
-                    acc[cb] *= alpha;
-                l_run *= alpha;
-                m_ref = m_new;
-            }
-            const float mc = (m_ref == kNegInf) ? 0.f : m_ref;
-
-            // P = exp2(s*c - m_ref), rounded to bf16 for the PV product; the
+            const float m_new = move ? mx : m_ref;
+            const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
+            const float mc = (m_new == kNegInf) ? 0.f : m_new;
+            // P = exp2(s*c - m_new), rounded to bf16 for the PV product; the
             // row sum accumulates the same rounded values (v_dot2 with ones).
-            bf16x2 pw[2][8];
+            float psum = 0.f;
 #pragma unroll
-            for (int sb = 0; sb < 2; sb++)
+            for (int q = 0; q < 4; q++) {
+                if constexpr (decltype(do_pv)::value)
+                    pv_slice(sm[cb_ ^ 1], q);
+                const int sb = q >> 1, i0 = (q & 1) * 8;
 #pragma unroll
-                for (int i = 0; i < 16; i += 2) {
+                for (int i = i0; i < i0 + 8; i += 2) {
                     const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
                     const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
                     pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
-                    l_run = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, l_run, false);
+                    psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
                 }
-
-            // O^T += V^T P^T over four 16-key slices.
-#pragma unroll
-            for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-                for (int ss = 0; ss < 2; ss++) {
-                    bf16x8 pf;
-#pragma unroll
-                    for (int j = 0; j < 4; j++) {
-                        pf[2 * j] = pw[sb][ss * 4 + j][0];
-                        pf[2 * j + 1] = pw[sb][ss * 4 + j][1];
-                    }
-#pragma unroll
-                    for (int cb = 0; cb < D / 32; cb++) {
-                        const bf16x8 vf = read_vt_frag(
-                            &cur.v[sb * 32 + ss * 16 + vt_row][cb * 32 + vt_col], D + kVPad);
-                        acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
-                    }
-                }
+            }
+            l_run = fmaf(l_run, alpha, psum);
+            m_ref = m_new;
+            resc_pend = __builtin_amdgcn_ballot_w64(move) != 0;
+            alpha_pend = alpha;
+        } else if constexpr (decltype(do_pv)::value) {
+            pv(sm[cb_ ^ 1]);
         }
-        if (more)
-            store_tile<D>(sm[(kb + 1 - kb_lo) & 1], st, tid);
-        __syncthreads();
+        dma_wait_barrier();
     };
+
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    // Tiles needing the real-position mask: the diagonal tail (some key past
+    // the wave's first row) and, for the local branch, the window's left edge.
+    int kb_um_lo = kb_first, kb_um_hi = min(kb_last, (wpmin + 1) / kBlockN - 1);
+    if (MODE == kModeLocal) {
+        const int edge = wpmax - w + 1;            // keys below this are out for the last row
+        if (edge > 0)
+            kb_um_lo = max(kb_um_lo, (edge + kBlockN - 1) / kBlockN);
+    }
+    auto unmasked = [&](int kb_) { return kb_ >= kb_um_lo && kb_ <= kb_um_hi; };
 
     // Every wave walks all tiles of the workgroup's range (they share the
     // staging and the barriers) but computes only its own sub-range.
     int kb = kb_lo;
     for (; kb < kb_first && kb <= kb_hi; kb++)
-        step(kb, false);
-    for (; kb <= kb_last; kb++)
-        step(kb, true);
+        step(kb, F_{}, F_{}, F_{});
+    bool pending = false;
+    if (kb <= kb_last) {
+        // first computed tile (no PV yet), then three loops of a single kind
+        // each -- masked window edge, unmasked middle, masked diagonal -- so
+        // that no loop body switches between instantiations
+        if (unmasked(kb))
+            step(kb, T_{}, F_{}, F_{});
+        else
+            step(kb, T_{}, F_{}, T_{});
+        kb++;
+        for (const int e = min(kb_last, kb_um_lo - 1); kb <= e; kb++)
+            step(kb, T_{}, T_{}, T_{});
+        for (const int e = min(kb_last, kb_um_hi); kb <= e; kb++)
+            step(kb, T_{}, T_{}, F_{});
+        for (; kb <= kb_last; kb++)
+            step(kb, T_{}, T_{}, T_{});
+        pending = true;
+    }
+    if (pending && kb <= kb_hi) {
+        step(kb, F_{}, T_{}, F_{});
+        pending = false;
+        kb++;
+    }
     for (; kb <= kb_hi; kb++)
-        step(kb, false);
+        step(kb, F_{}, F_{}, F_{});
+    if (pending) {
+        apply_rescale();
+        pv(sm[(kb_hi - kb_lo) & 1]);        // V(kb_hi) was staged by the last step
+    }
 
-    const float l_tot = pair_sum(l_run);
+    float l_tot = pair_sum(l_run);
+    if constexpr (MODE == kModeGlobal) {
+        // a split entry: publish the partial, and the last of the tile's
+        // entries to finish merges all of them and runs the epilogue
+        if (uni(tile.nsplit) > 1 && !merge_split<D>(a, tile, hg, wave, lane, acc, m_ref, l_tot))
+            return;
+    }
     const float inv = 1.f / l_tot;
     if (EPI == kEpiFused && MODE != kModeDense) {
         // ContextNorm over the row's d values: this lane holds d/2 of them,
@@ -447,20 +615,26 @@ void attn_kernel(const AttnArgs a) {
         // of their XCD (workgroups are dispatched round-robin over the 8
         // XCDs): queue x holds items x, x+8, x+16, ...  Items are in
         // longest-first order, and items that share a KV head tend to share
-        // an XCD and its L2.
+        // an XCD and its L2.  Every workgroup exits after all 8 queues have
+        // returned an index past the end.
         __shared__ int s_item;
-        const int x = blockIdx.x % kQueues;
+        const int x0 = blockIdx.x % kQueues;
         const int n_items = a.queue[0] * a.n_hg;
-        for (;;) {
-            if (threadIdx.x == 0)
-                s_item = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
-            __syncthreads();
-            const int item = __builtin_amdgcn_readfirstlane(s_item);
-            __syncthreads();
-            if (item >= n_items)
-                break;
-            const SparseTile t = a.tiles[item / a.n_hg];
-            attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
+        // Own XCD's queue first; once it is empty, take what is left in the
+        // other queues (in XCD order), so no XCD idles while another has work.
+        for (int qi = 0; qi < kQueues; qi++) {
+            const int x = (x0 + qi) % kQueues;
+            for (;;) {
+                if (threadIdx.x == 0)
+                    s_item = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
+                __syncthreads();
+                const int item = __builtin_amdgcn_readfirstlane(s_item);
+                __syncthreads();
+                if (item >= n_items)
+                    break;
+                const SparseTile t = a.tiles[item / a.n_hg];
+                attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
+            }
         }
     } else {
         const int hg = blockIdx.x % a.n_hg;

@@ -105,19 +105,29 @@ SelectWs select_ws(const logo_problem *p) {
 }
 
 struct GlobalWs {
-    size_t tiles, prefix, queue, total;
+    size_t tiles, tiles_tmp, scratch, queue, split_cnt, partial, total;
+    int max_tiles, slots, stride;
 };
 GlobalWs global_ws(const logo_problem *p, int32_t cap) {
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
-    const size_t max_tiles = (size_t)(cap + tp.tpw - 1) / tp.tpw + (size_t)p->num_seqs;
     GlobalWs w;
+    w.max_tiles = (int)((cap + tp.tpw - 1) / tp.tpw + p->num_seqs);
+    w.slots = split_slots(w.max_tiles, tp.n_hg);
+    w.stride = (w.max_tiles > p->num_seqs ? w.max_tiles : p->num_seqs) + 1;
+    const size_t entries = (size_t)w.max_tiles + (size_t)w.slots;
     size_t off = 0;
     w.tiles = off;
-    off += align_up(sizeof(SparseTile) * max_tiles);
-    w.prefix = off;
-    off += align_up(sizeof(int32_t) * ((size_t)p->num_seqs + 1));
+    off += align_up(sizeof(SparseTile) * entries);
+    w.tiles_tmp = off;
+    off += align_up(sizeof(SparseTile) * entries);
+    w.scratch = off;
+    off += align_up(sizeof(int32_t) * 2 * (size_t)w.stride);
     w.queue = off;
     off += align_up(sizeof(int32_t) * (1 + kQueues));
+    w.split_cnt = off;
+    off += align_up(sizeof(int32_t) * (size_t)w.slots * tp.n_hg);
+    w.partial = off;
+    off += align_up(sizeof(float) * partial_floats(p->head_dim) * (size_t)w.slots * tp.n_hg);
     w.total = off;
     return w;
 }
@@ -253,12 +263,21 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
     const GlobalWs w = global_ws(p, cap);
     SparseTile *tiles = (SparseTile *)(ws + w.tiles);
-    int32_t *prefix = (int32_t *)(ws + w.prefix);
     int32_t *queue = (int32_t *)(ws + w.queue);
-    logo_status st = hip_status(launch_sparse_plan(p->cu_seqlens, cu_sel, sel_idx, p->num_seqs,
-                                                   tp.tpw, cap, p->max_seqlen, tiles, prefix,
-                                                   queue, s),
-                                s);
+    int32_t *split_cnt = (int32_t *)(ws + w.split_cnt);
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return LOGO_ERR_HIP;
+    const int per_cu = attention_blocks_per_cu(kModeGlobal, p->head_dim);
+    int grid = cus * per_cu;
+    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    logo_status st = hip_status(
+        launch_sparse_plan(p->cu_seqlens, cu_sel, sel_idx, p->num_seqs, tp.tpw, cap,
+                           p->max_seqlen, tp.n_hg, grid, w.slots, w.stride,
+                           (SparseTile *)(ws + w.tiles_tmp), tiles, (int32_t *)(ws + w.scratch),
+                           queue, split_cnt, s),
+        s);
     if (st != LOGO_OK)
         return st;
     AttnArgs a = make_args(p, tp);
@@ -269,15 +288,10 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     a.sel_idx = sel_idx;
     a.tiles = tiles;
     a.queue = queue;
+    a.split_cnt = split_cnt;
+    a.partial = (float *)(ws + w.partial);
     if (f)
         set_fused(a, f, gain);
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return LOGO_ERR_HIP;
-    const int per_cu = attention_blocks_per_cu(kModeGlobal, p->head_dim);
-    int grid = cus * per_cu;
-    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
     return hip_status(
         launch_attention(kModeGlobal, f ? kEpiFused : kEpiRaw, p->head_dim, a, grid, s), s);
 }

@@ -35,13 +35,43 @@ inline TilePlan make_tile_plan(int hq, int hkv) {
     return t;
 }
 
-// One entry of the query-sparse tile table (written on the device).
+// One work entry of the query-sparse global branch (written on the device):
+// a tile of selected rows and the range of 64-key KV blocks it covers.  A
+// long tile is split into nsplit entries over consecutive KV ranges; each
+// writes a partial (O, m, l) and the one that finishes last merges them in
+// split order (attention.hip).
 struct SparseTile {
-    int32_t first;    // index of the tile's first row in sel_idx
-    int32_t nrows;    // rows in the tile (1..tpw)
-    int32_t seq;      // sequence b
-    int32_t pos_max;  // position of the tile's last row (work ~ pos_max + 1)
+    int32_t first;     // index of the tile's first row in sel_idx
+    int32_t nrows;     // rows in the tile (1..tpw)
+    int32_t seq;       // sequence b
+    int32_t pos_max;   // position of the tile's last row
+    int32_t kb_begin;  // first KV block of this entry
+    int32_t kb_end;    // last KV block of this entry (inclusive)
+    int32_t split;     // 0 .. nsplit-1
+    int32_t nsplit;    // 1 = whole tile
+    int32_t sid;       // first partial slot of a split tile (also its counter), -1 if whole
+    int32_t pad[3];
 };
+constexpr int kMaxSplit = 4;          // KV ranges per tile at most
+constexpr int kSplitDiv = 1;          // split tiles longer than 1/kSplitDiv of a workgroup's mean load
+constexpr int kMinSplitBlocks = 16;   // never split tiles of 16 KV blocks or fewer
+constexpr int kSplitGridRef = 512;    // persistent workgroups the split slots are sized for
+
+// Partial result of one split entry for one head group, lane-major: the
+// 4 waves x 64 lanes each hold d/2 fp32 outputs, then m (exp2 domain) and l
+// of every lane.
+__host__ __device__ constexpr size_t partial_floats(int head_dim) {
+    return (size_t)kWaves * 64 * (head_dim / 2 + 2);
+}
+// Partial slots (per head group) for a problem with max_tiles tiles: split
+// tiles have more than W / (kSplitDiv grid n_hg) blocks for a total of W
+// (blocks x head groups), so their ceil(blocks / target) add up to at most
+// 2 kSplitDiv grid / n_hg.
+inline int split_slots(int max_tiles, int n_hg) {
+    const long long a = (long long)max_tiles * kMaxSplit;
+    const long long b = 2LL * kSplitDiv * kSplitGridRef / n_hg + kMaxSplit;
+    return (int)(a < b ? a : b);
+}
 
 enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
 
@@ -61,8 +91,10 @@ struct AttnArgs {
     void *out;                 // fp32 [rows][Hq][d] or bf16 for dense
     const int32_t *cu_seqlens;
     const int32_t *sel_idx;    // global mode
-    const SparseTile *tiles;   // global mode
-    int32_t *queue;            // global mode: [0] = n_tiles, [1 + x] = queue x counter
+    const SparseTile *tiles;   // global mode: work entries, longest first
+    int32_t *queue;            // global mode: [0] = n_entries, [1 + x] = queue x counter
+    int32_t *split_cnt;        // global mode: [sid * n_hg + hg] entries of a split tile done
+    float *partial;            // global mode: [(sid + split) * n_hg + hg] partial results
     int32_t num_seqs;
     int32_t hq, hkv, group;    // group = hq / hkv
     int32_t hpw, tpw, n_hg;
@@ -83,10 +115,15 @@ hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, 
                             hipStream_t s);
 int attention_blocks_per_cu(int mode, int head_dim);
 
+// Tile plan of the global branch.  tiles_tmp and tiles each hold
+// max_tiles + split_slots entries; scratch holds 2 * stride ints with
+// stride >= max(B, max_tiles) + 1; split_cnt holds split_slots * n_hg ints.
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
                               const int32_t *sel_idx, int num_seqs, int tpw,
-                              int sel_capacity, int max_seqlen, SparseTile *tiles,
-                              int32_t *tile_prefix, int32_t *queue, hipStream_t s);
+                              int sel_capacity, int max_seqlen, int n_hg, int grid_wgs,
+                              int split_slots, int stride, SparseTile *tiles_tmp,
+                              SparseTile *tiles, int32_t *scratch, int32_t *queue,
+                              int32_t *split_cnt, hipStream_t s);
 
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,

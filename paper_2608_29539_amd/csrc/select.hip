@@ -13,8 +13,11 @@
 //                     writes sel_idx, tok2sel and cu_sel.
 //   sparse_plan_kernel
 //                     cuts each sequence's selected rows into tiles of tpw
-//                     rows and orders the tiles longest-first (bucketed by the
-//                     position of their last row), then resets the work queues.
+//                     rows, splits the longest tiles into KV ranges so that no
+//                     work entry exceeds a fraction of one persistent
+//                     workgroup's mean load, orders the entries longest-first
+//                     (bucketed by KV length), then resets the work queues and
+//                     the split counters.
 #include "logo_internal.h"
 
 namespace logo {
@@ -245,74 +248,170 @@ __global__ __launch_bounds__(kSelThreads) void write_kernel(const int32_t *cu, i
     }
 }
 
-__global__ __launch_bounds__(1024) void sparse_plan_kernel(const int32_t *cu, const int32_t *cu_sel,
-                                                           const int32_t *sel_idx, int B, int tpw,
-                                                           int cap, int max_seqlen,
-                                                           SparseTile *tiles, int32_t *tprefix,
-                                                           int32_t *queue) {
-    constexpr int kBuckets = 1024;
-    __shared__ int s_wave[16];
-    __shared__ int s_carry;
-    __shared__ int hist[kBuckets];
+// Exclusive prefix sum, in place, of n ints in global memory by one
+// 1024-thread workgroup (chunks of 1024 with a carry); returns the total.
+__device__ int block_exclusive_scan_array(int32_t *v, int n, int *s_wave, int *s_carry) {
     const int tid = threadIdx.x;
     if (tid == 0)
-        s_carry = 0;
+        *s_carry = 0;
     __syncthreads();
-    // 1. tiles per sequence -> exclusive prefix tprefix[0..B]
-    for (int c0 = 0; c0 < B; c0 += 1024) {
-        const int b = c0 + tid;
-        int cnt = 0;
-        if (b < B) {
-            const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
-            cnt = (s1 - s0 + tpw - 1) / tpw;
-        }
-        const int carry = s_carry;
-        const int incl = block_inclusive_scan(cnt, s_wave);
-        if (b < B)
-            tprefix[b] = carry + incl - cnt;
+    for (int c0 = 0; c0 < n; c0 += 1024) {
+        const int i = c0 + tid;
+        const int x = i < n ? v[i] : 0;
+        const int carry = *s_carry;
+        const int incl = block_inclusive_scan(x, s_wave);
+        if (i < n)
+            v[i] = carry + incl - x;
         __syncthreads();
         if (tid == 1023)
-            s_carry = carry + incl;
+            *s_carry = carry + incl;
         __syncthreads();
     }
-    const int n_tiles = s_carry;
-    if (tid == 0)
-        tprefix[B] = n_tiles;
-    for (int i = tid; i < kBuckets; i += 1024)
-        hist[i] = 0;
-    __syncthreads();   // tprefix (global) and hist visible block-wide
+    const int total = *s_carry;
+    __syncthreads();
+    return total;
+}
 
-    // 2. bucket histogram of tile lengths (longest first)
-    const long long ms = max_seqlen > 0 ? max_seqlen : 1;
-    for (int u = tid; u < n_tiles; u += 1024) {
-        const int b = owner_seq(tprefix, B, u);
-        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
-        const int first = s0 + (u - tprefix[b]) * tpw;
-        const int nrows = min(tpw, s1 - first);
-        const int pmax = sel_idx[first + nrows - 1] - cu[b];
-        long long bk = ((ms - 1 - pmax) * kBuckets) / ms;
-        bk = bk < 0 ? 0 : (bk >= kBuckets ? kBuckets - 1 : bk);
-        atomicAdd(&hist[bk], 1);
-    }
+constexpr int kBuckets = 1024;
+
+__device__ __forceinline__ int entry_blocks(const SparseTile &t) { return t.kb_end - t.kb_begin + 1; }
+
+// Longest-first bucket sort of n entries of src into dst by their number of
+// KV blocks (in [1, max_blocks]); the order inside a bucket is arbitrary and
+// no result depends on it.
+__device__ void bucket_sort_desc(const SparseTile *src, SparseTile *dst, int n, int max_blocks,
+                                 int *hist, int *s_wave) {
+    const int tid = threadIdx.x;
+    const long long mw = max_blocks > 0 ? max_blocks : 1;
+    auto bucket = [&](const SparseTile &t) {
+        long long bk = ((mw - entry_blocks(t)) * kBuckets) / mw;
+        return (int)(bk < 0 ? 0 : (bk >= kBuckets ? kBuckets - 1 : bk));
+    };
+    hist[tid] = 0;
+    __syncthreads();
+    for (int u = tid; u < n; u += 1024)
+        atomicAdd(&hist[bucket(src[u])], 1);
     __syncthreads();
     const int hv = hist[tid];
     const int incl = block_inclusive_scan(hv, s_wave);
-    hist[tid] = incl - hv;   // exclusive offsets
+    hist[tid] = incl - hv;
     __syncthreads();
-    // 3. scatter (order inside a bucket is arbitrary; results do not depend on it)
-    for (int u = tid; u < n_tiles; u += 1024) {
-        const int b = owner_seq(tprefix, B, u);
+    for (int u = tid; u < n; u += 1024) {
+        const SparseTile t = src[u];
+        dst[atomicAdd(&hist[bucket(t)], 1)] = t;
+    }
+    __syncthreads();
+}
+
+// One workgroup of 1024 threads.  scratch holds 2 * (stride) ints with
+// stride >= max(B, max_tiles) + 1.
+__global__ __launch_bounds__(1024) void sparse_plan_kernel(
+    const int32_t *cu, const int32_t *cu_sel, const int32_t *sel_idx, int B, int tpw, int cap,
+    int max_seqlen, int n_hg, int grid_wgs, int split_slots, int stride, SparseTile *tmp,
+    SparseTile *out, int32_t *scratch, int32_t *queue, int32_t *split_cnt) {
+    __shared__ int s_wave[16];
+    __shared__ int s_carry;
+    __shared__ int hist[kBuckets];
+    __shared__ unsigned long long s_total_blocks;
+    const int tid = threadIdx.x;
+    int32_t *sa = scratch, *sb = scratch + stride;
+
+    // 1. tiles per sequence -> exclusive prefix
+    for (int b = tid; b < B; b += 1024) {
         const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
-        const int first = s0 + (u - tprefix[b]) * tpw;
+        sa[b] = (s1 - s0 + tpw - 1) / tpw;
+    }
+    __syncthreads();
+    const int n_tiles = block_exclusive_scan_array(sa, B, s_wave, &s_carry);
+    if (tid == 0) {
+        sa[B] = n_tiles;
+        s_total_blocks = 0;
+    }
+    __syncthreads();
+
+    // 2. the whole tiles (unsorted) into tmp, and their total KV blocks
+    unsigned long long my_blocks = 0;
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int b = owner_seq(sa, B, u);
+        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
+        const int first = s0 + (u - sa[b]) * tpw;
         const int nrows = min(tpw, s1 - first);
         const int pmax = sel_idx[first + nrows - 1] - cu[b];
-        long long bk = ((ms - 1 - pmax) * kBuckets) / ms;
-        bk = bk < 0 ? 0 : (bk >= kBuckets ? kBuckets - 1 : bk);
-        const int slot = atomicAdd(&hist[bk], 1);
-        tiles[slot] = SparseTile{first, nrows, b, pmax};
+        SparseTile t;
+        t.first = first;
+        t.nrows = nrows;
+        t.seq = b;
+        t.pos_max = pmax;
+        t.kb_begin = 0;
+        t.kb_end = pmax / kBlockN;
+        t.split = 0;
+        t.nsplit = 1;
+        t.sid = -1;
+        t.pad[0] = t.pad[1] = t.pad[2] = 0;
+        tmp[u] = t;
+        my_blocks += (unsigned long long)(t.kb_end + 1);
     }
+    atomicAdd(&s_total_blocks, my_blocks);
+    __syncthreads();
+    const int max_blocks = (max_seqlen + kBlockN - 1) / kBlockN;
+    // 3. longest first
+    bucket_sort_desc(tmp, out, n_tiles, max_blocks, hist, s_wave);
+
+    // 4. KV split: a tile longer than `target` blocks (a 1/kSplitDiv share of
+    //    the mean load of one persistent workgroup) becomes ns = ceil(blocks /
+    //    target) entries (at most kMaxSplit) over consecutive KV ranges, while
+    //    partial slots last (longest tiles first).
+    const unsigned long long work = s_total_blocks * (unsigned long long)n_hg;
+    const unsigned long long div = (unsigned long long)kSplitDiv * (unsigned long long)grid_wgs;
+    long long target = (long long)((work + div - 1) / div);
+    if (target < kMinSplitBlocks)
+        target = kMinSplitBlocks;
+    auto nsplit_of = [&](const SparseTile &t) {
+        const long long nb = entry_blocks(t);
+        if (nb <= target)
+            return 1;
+        const long long ns = (nb + target - 1) / target;
+        return (int)(ns < kMaxSplit ? ns : kMaxSplit);
+    };
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int ns = nsplit_of(out[u]);
+        sa[u] = ns > 1 ? ns : 0;
+    }
+    __syncthreads();
+    block_exclusive_scan_array(sa, n_tiles, s_wave, &s_carry);   // slot base
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int ns = nsplit_of(out[u]);
+        sb[u] = (ns > 1 && sa[u] + ns <= split_slots) ? ns : 1;
+    }
+    __syncthreads();
+    // sb[u] = entries of tile u; keep a copy of the counts in tmp's pad
+    for (int u = tid; u < n_tiles; u += 1024)
+        out[u].pad[0] = sb[u];
+    __syncthreads();
+    const int n_entries = block_exclusive_scan_array(sb, n_tiles, s_wave, &s_carry);
+    for (int u = tid; u < n_tiles; u += 1024) {
+        SparseTile t = out[u];
+        const int ns = t.pad[0];
+        t.pad[0] = 0;
+        const int nb = t.kb_end + 1;
+        const int e0 = sb[u];
+        for (int s = 0; s < ns; s++) {
+            SparseTile h = t;
+            h.kb_begin = (int)(((long long)s * nb) / ns);
+            h.kb_end = (int)(((long long)(s + 1) * nb) / ns) - 1;
+            h.split = s;
+            h.nsplit = ns;
+            h.sid = ns > 1 ? sa[u] : -1;
+            tmp[e0 + s] = h;
+        }
+    }
+    __syncthreads();
+    // 5. entries longest first
+    bucket_sort_desc(tmp, out, n_entries, max_blocks, hist, s_wave);
+    for (int i = tid; i < split_slots * n_hg; i += 1024)
+        split_cnt[i] = 0;
     if (tid == 0) {
-        queue[0] = n_tiles;
+        queue[0] = n_entries;
         for (int x = 0; x < kQueues; x++)
             queue[1 + x] = 0;
     }
@@ -353,10 +452,13 @@ hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
 
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
                               const int32_t *sel_idx, int num_seqs, int tpw, int sel_capacity,
-                              int max_seqlen, SparseTile *tiles, int32_t *tile_prefix,
-                              int32_t *queue, hipStream_t s) {
+                              int max_seqlen, int n_hg, int grid_wgs, int split_slots,
+                              int stride, SparseTile *tiles_tmp, SparseTile *tiles,
+                              int32_t *scratch, int32_t *queue, int32_t *split_cnt,
+                              hipStream_t s) {
     hipLaunchKernelGGL(sparse_plan_kernel, dim3(1), dim3(1024), 0, s, cu_seqlens, cu_sel, sel_idx,
-                       num_seqs, tpw, sel_capacity, max_seqlen, tiles, tile_prefix, queue);
+                       num_seqs, tpw, sel_capacity, max_seqlen, n_hg, grid_wgs, split_slots,
+                       stride, tiles_tmp, tiles, scratch, queue, split_cnt);
     return hipGetLastError();
 }
 
