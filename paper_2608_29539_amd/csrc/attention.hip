@@ -73,80 +73,102 @@ constexpr int kRawBufferFlags = 0x00020000;
 // M0 + 16 i), so a padded tile is filled as a sequence of 1 KB slot runs; a
 // lane whose slot is row padding re-loads the row's last chunk (never read).
 // The per-lane byte offsets inside a tile are fixed and computed once.
-template <int D>
+template <int D, int W>
 struct Dma {
     static constexpr int kSlotsK = (D + kKPad) * 2 / 16;     // 16-byte slots per K row
     static constexpr int kSlotsV = (D + kVPad) * 2 / 16;
     static constexpr int kInstK = kSlotsK;                   // 64 rows x slots / 64 lanes
     static constexpr int kInstV = kSlotsV;
-    static constexpr int kPerWaveK = (kInstK + kWaves - 1) / kWaves;
-    static constexpr int kPerWaveV = (kInstV + kWaves - 1) / kWaves;
+    static constexpr int kPerWaveK = (kInstK + W - 1) / W;
+    static constexpr int kPerWaveV = (kInstV + W - 1) / W;
     int voff_k[kPerWaveK];
     int voff_v[kPerWaveV];
 };
 
-template <int D>
-__device__ __forceinline__ void dma_plan(Dma<D> &d, int wave, int lane, int row_bytes) {
+template <int D, int W>
+__device__ __forceinline__ void dma_plan(Dma<D, W> &d, int wave, int lane, int row_bytes) {
 #pragma unroll
-    for (int i = 0; i < Dma<D>::kPerWaveK; i++) {
-        const int slot = (i * kWaves + wave) * 64 + lane;
-        const int row = slot / Dma<D>::kSlotsK, col = min(slot % Dma<D>::kSlotsK, D / 8 - 1);
+    for (int i = 0; i < Dma<D, W>::kPerWaveK; i++) {
+        const int slot = (i * W + wave) * 64 + lane;
+        const int row = slot / Dma<D, W>::kSlotsK, col = min(slot % Dma<D, W>::kSlotsK, D / 8 - 1);
         d.voff_k[i] = row * row_bytes + col * 16;
     }
 #pragma unroll
-    for (int i = 0; i < Dma<D>::kPerWaveV; i++) {
-        const int slot = (i * kWaves + wave) * 64 + lane;
-        const int row = slot / Dma<D>::kSlotsV, col = min(slot % Dma<D>::kSlotsV, D / 8 - 1);
+    for (int i = 0; i < Dma<D, W>::kPerWaveV; i++) {
+        const int slot = (i * W + wave) * 64 + lane;
+        const int row = slot / Dma<D, W>::kSlotsV, col = min(slot % Dma<D, W>::kSlotsV, D / 8 - 1);
         d.voff_v[i] = row * row_bytes + col * 16;
     }
 }
 
 // Descriptor of one tile: base = its first key row of this KV head, size =
 // the rows that exist, so rows at or past the sequence end read as zeros
-// (masked keys with zero values keep masked-out products finite).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const uint16_t *kv, int T, int k0,
-                                                            int row_bytes) {
+// (masked keys with zero values keep masked-out products finite).  Raw
+// buffer descriptor words: base address (48 bits, stride 0), size in bytes,
+// flags.
+__device__ __forceinline__ u32x4 tile_rsrc(const uint16_t *kv, int T, int k0, int row_bytes) {
     const int rows = min(kBlockN, T - k0);
     const int nbytes = rows > 0 ? rows * row_bytes : 0;
-    return __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)kv + (long long)k0 * row_bytes), (short)0, nbytes,
-        kRawBufferFlags);
+    const uint64_t p = (uint64_t)((const char *)kv + (long long)k0 * row_bytes);
+    u32x4 r;
+    r[0] = __builtin_amdgcn_readfirstlane((uint32_t)p);
+    r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) & 0xFFFFu;
+    r[2] = __builtin_amdgcn_readfirstlane(nbytes);
+    r[3] = kRawBufferFlags;
+    return r;
 }
 
-typedef __attribute__((address_space(3))) void lds_void;
-
-// One 16-byte-per-lane global -> LDS load (non-template wrapper: the host
-// compilation pass rejects this builtin inside templates).
-__device__ __forceinline__ void lds_load16(__amdgpu_buffer_rsrc_t r, void *lds, int voffset) {
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void *)lds, 16, voffset, 0, 0, 0);
+// One 16-byte-per-lane global -> LDS load.  Issued as inline assembly so that
+// the compiler does not make every later LDS read wait for it: the tile it
+// fills is only read after the wait + barrier that ends the pipeline step,
+// while the reads in between go to the other buffer.  M0 (the LDS base of
+// the load) is saved and restored around it.
+__device__ __forceinline__ void lds_load16(u32x4 r, const void *lds, int voffset) {
+    const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds);
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %1\n\t"
+        "s_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "s"(lds_addr), "v"(voffset), "s"(r)
+        : "memory");
 }
 
-template <int D>
-__device__ __forceinline__ void dma_k(Smem<D> &buf, const Dma<D> &d, const uint16_t *kv_k, int T,
-                                      int k0, int row_bytes, int wave) {
-    const __amdgpu_buffer_rsrc_t r = tile_rsrc(kv_k, T, k0, row_bytes);
+template <int D, int W>
+__device__ __forceinline__ void dma_k(Smem<D> &buf, const Dma<D, W> &d, const uint16_t *kv_k,
+                                      int T, int k0, int row_bytes, int wave) {
+    const u32x4 r = tile_rsrc(kv_k, T, k0, row_bytes);
 #pragma unroll
-    for (int i = 0; i < Dma<D>::kPerWaveK; i++) {
-        const int inst = i * kWaves + wave;
-        if (inst < Dma<D>::kInstK)
+    for (int i = 0; i < Dma<D, W>::kPerWaveK; i++) {
+        const int inst = i * W + wave;
+        if (inst < Dma<D, W>::kInstK)
             lds_load16(r, (char *)&buf.k[0][0] + inst * 1024, d.voff_k[i]);
     }
 }
-template <int D>
-__device__ __forceinline__ void dma_v(Smem<D> &buf, const Dma<D> &d, const uint16_t *kv_v, int T,
-                                      int k0, int row_bytes, int wave) {
-    const __amdgpu_buffer_rsrc_t r = tile_rsrc(kv_v, T, k0, row_bytes);
+template <int D, int W>
+__device__ __forceinline__ void dma_v(Smem<D> &buf, const Dma<D, W> &d, const uint16_t *kv_v,
+                                      int T, int k0, int row_bytes, int wave) {
+    const u32x4 r = tile_rsrc(kv_v, T, k0, row_bytes);
 #pragma unroll
-    for (int i = 0; i < Dma<D>::kPerWaveV; i++) {
-        const int inst = i * kWaves + wave;
-        if (inst < Dma<D>::kInstV)
+    for (int i = 0; i < Dma<D, W>::kPerWaveV; i++) {
+        const int inst = i * W + wave;
+        if (inst < Dma<D, W>::kInstV)
             lds_load16(r, (char *)&buf.v[0][0] + inst * 1024, d.voff_v[i]);
     }
 }
 
+// s_waitcnt operand that waits for vmcnt = 0 only (lgkmcnt and expcnt at
+// their maximum).  Issued through the builtin so the compiler knows that no
+// vector-memory load is outstanding afterwards.
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 // Completion of this wave's LDS-bound loads, then the workgroup barrier.
 __device__ __forceinline__ void dma_wait_barrier() {
-    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     __syncthreads();
 }
 
@@ -200,7 +222,8 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
                                             int wave, int lane, f32x16 (&acc)[D / 32], float m,
                                             float &l) {
     __shared__ int s_last;
-    constexpr int kAccFloats = kWaves * 64 * (D / 2);
+    constexpr int kLanes = kWavesGlobal * 64;
+    constexpr int kAccFloats = kLanes * (D / 2);
     const int sid = uni(t.sid), split = uni(t.split), ns = uni(t.nsplit);
     const int li = wave * 64 + lane;
     float *base = a.partial + (int64_t)sid * a.n_hg * partial_floats(D);
@@ -212,10 +235,10 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
         for (int qd = 0; qd < 4; qd++) {
             f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
                        acc[cb][qd * 4 + 3]};
-            *(f32x4 *)(mine + ((cb * 4 + qd) * (kWaves * 64) + li) * 4) = v;
+            *(f32x4 *)(mine + ((cb * 4 + qd) * kLanes + li) * 4) = v;
         }
     mine[kAccFloats + li] = m;
-    mine[kAccFloats + kWaves * 64 + li] = l;
+    mine[kAccFloats + kLanes + li] = l;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (threadIdx.x == 0)
@@ -232,7 +255,7 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
     for (int j = 0; j < ns; j++) {
         const float *pj = base + j * slot_stride + (int64_t)hg * partial_floats(D);
         const float mj = pj[kAccFloats + li];
-        const float lj = pj[kAccFloats + kWaves * 64 + li];
+        const float lj = pj[kAccFloats + kLanes + li];
         const float mn = fmaxf(M, mj);
         const float mc = (mn == kNegInf) ? 0.f : mn;
         const float ra = __builtin_amdgcn_exp2f(M - mc), rb = __builtin_amdgcn_exp2f(mj - mc);
@@ -240,7 +263,7 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
         for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
             for (int qd = 0; qd < 4; qd++) {
-                const f32x4 v = *(const f32x4 *)(pj + ((cb * 4 + qd) * (kWaves * 64) + li) * 4);
+                const f32x4 v = *(const f32x4 *)(pj + ((cb * 4 + qd) * kLanes + li) * 4);
 #pragma unroll
                 for (int e = 0; e < 4; e++)
                     acc[cb][qd * 4 + e] = fmaf(acc[cb][qd * 4 + e], ra, v[e] * rb);
@@ -304,6 +327,10 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
 #pragma unroll
         for (int s = 0; s < D / 16; s++)
             qf[s] = *(const bf16x8 *)(qp + s * 16);
+        // Q is in registers before the KV loop starts: inside the loop the
+        // only vector-memory loads in flight are the K/V tile loads, which the
+        // compiler does not track.
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     }
 
     // Lane's row / column inside a V tile for the transpose reads.
@@ -331,8 +358,9 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     const int row_bytes = a.hkv * D * 2;
     const uint16_t *kv_k = a.k + (base * a.hkv + kvh) * (int64_t)D;
     const uint16_t *kv_v = a.v + (base * a.hkv + kvh) * (int64_t)D;
-    Dma<D> dma;
-    dma_plan<D>(dma, wave, lane, row_bytes);
+    constexpr int W = waves_of(MODE);
+    Dma<D, W> dma;
+    dma_plan<D, W>(dma, wave, lane, row_bytes);
 
     f32x16 acc[D / 32];
 #pragma unroll
@@ -347,7 +375,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     // consumed one iteration later); two buffers each, one barrier per tile.
     bf16x2 pw[2][8];                          // P of the last softmax-ed tile
     __syncthreads();                         // the previous item's last tile is consumed
-    dma_k<D>(sm[0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
+    dma_k<D, W>(sm[0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
     dma_wait_barrier();
 
     // PV of the tile whose P is in pw, V read from buffer vb, for one 16-key
@@ -396,8 +424,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         // K(kb+1) into the other K buffer, V(kb) into this tile's V buffer:
         // both were last read before the previous barrier.
         if (kb < kb_hi)
-            dma_k<D>(sm[cb_ ^ 1], dma, kv_k, T, (kb + 1) * kBlockN, row_bytes, wave);
-        dma_v<D>(sm[cb_], dma, kv_v, T, kb * kBlockN, row_bytes, wave);
+            dma_k<D, W>(sm[cb_ ^ 1], dma, kv_k, T, (kb + 1) * kBlockN, row_bytes, wave);
+        dma_v<D, W>(sm[cb_], dma, kv_v, T, kb * kBlockN, row_bytes, wave);
         if constexpr (decltype(do_pv)::value)
             apply_rescale();
         if constexpr (decltype(do_s)::value) {
@@ -607,7 +635,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
 }
 
 template <int D, int MODE, int EPI>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(waves_of(MODE) * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
     __shared__ Smem<D> sm[2];
     if (MODE == kModeGlobal) {
@@ -652,14 +680,15 @@ void attn_kernel(const AttnArgs a) {
 
 template <int D, int MODE, int EPI>
 hipError_t launch_one(const AttnArgs &a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((attn_kernel<D, MODE, EPI>), dim3(grid), dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<D, MODE, EPI>), dim3(grid), dim3(waves_of(MODE) * 64), 0, s, a);
     return hipGetLastError();
 }
 
 template <int D, int MODE>
 int blocks_per_cu_one() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE, kEpiRaw>, kThreads,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE, kEpiRaw>,
+                                                     waves_of(MODE) * 64,
                                                      0) != hipSuccess)
         return 1;
     return n > 0 ? n : 1;

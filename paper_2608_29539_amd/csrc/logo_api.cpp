@@ -109,7 +109,7 @@ struct GlobalWs {
     int max_tiles, slots, stride;
 };
 GlobalWs global_ws(const logo_problem *p, int32_t cap) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
     GlobalWs w;
     w.max_tiles = (int)((cap + tp.tpw - 1) / tp.tpw + p->num_seqs);
     w.slots = split_slots(w.max_tiles, tp.n_hg);
@@ -239,7 +239,7 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
                       hipStream_t s) {
     if (p->total_tokens == 0)
         return LOGO_OK;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;
@@ -260,7 +260,7 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
                        hipStream_t s) {
     if (p->total_tokens == 0 || cap == 0)
         return LOGO_OK;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
     const GlobalWs w = global_ws(p, cap);
     SparseTile *tiles = (SparseTile *)(ws + w.tiles);
     int32_t *queue = (int32_t *)(ws + w.queue);
@@ -509,7 +509,7 @@ logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
         return LOGO_OK;
     if (!q || !k || !v || !out)
         return LOGO_ERR_NULL;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeDense);
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;

@@ -8,17 +8,26 @@
 namespace logo {
 
 // ---------------------------------------------------------------------------
-// Attention tiling.  One workgroup = 4 waves of 64 lanes.  Each wave owns 32
-// query rows of one query head; the 4 waves share one key/value head, so the
-// K/V tile a workgroup stages in LDS serves 4 x 32 rows.  With GQA group
-// size G the 4 waves cover HPW = gcd(G, 4) heads x (4 / HPW) blocks of 32
-// tokens: a tile is TPW = 32 * 4 / HPW tokens x HPW heads.
+// Attention tiling.  A workgroup has W waves of 64 lanes; each wave owns 32
+// query rows of one query head, and all W waves read the same key/value head,
+// so a K/V tile staged in LDS serves 32 W rows.  With GQA group size G the
+// waves cover HPW = gcd(G, 4) heads x (W / HPW) blocks of 32 tokens: a tile
+// is TPW = 32 W / HPW tokens x HPW heads.  The local branch uses W = 4 (two
+// workgroups per CU: its items are short, and a second workgroup hides one's
+// start and end); the global and dense modes use W = 8 (one workgroup per CU:
+// each staged tile serves twice the rows).
 // ---------------------------------------------------------------------------
-constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
 constexpr int kBlockN = 64;   // keys per K/V tile
-constexpr int kThreads = kWaves * 64;
 constexpr int kQueues = 8;    // one work queue per XCD
+constexpr int kWavesLocal = 4;
+constexpr int kWavesGlobal = 8;
+
+enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
+
+__host__ __device__ constexpr int waves_of(int mode) {
+    return mode == kModeLocal ? kWavesLocal : kWavesGlobal;
+}
 
 struct TilePlan {
     int hpw;      // heads per workgroup (1, 2 or 4)
@@ -26,11 +35,11 @@ struct TilePlan {
     int n_hg;     // head groups = Hq / hpw
 };
 
-inline TilePlan make_tile_plan(int hq, int hkv) {
+inline TilePlan make_tile_plan(int hq, int hkv, int mode) {
     const int g = hq / hkv;
     TilePlan t;
     t.hpw = (g % 4 == 0) ? 4 : (g % 2 == 0) ? 2 : 1;
-    t.tpw = kRowsPerWave * (kWaves / t.hpw);
+    t.tpw = kRowsPerWave * (waves_of(mode) / t.hpw);
     t.n_hg = hq / t.hpw;
     return t;
 }
@@ -58,10 +67,10 @@ constexpr int kMinSplitBlocks = 16;   // never split tiles of 16 KV blocks or fe
 constexpr int kSplitGridRef = 512;    // persistent workgroups the split slots are sized for
 
 // Partial result of one split entry for one head group, lane-major: the
-// 4 waves x 64 lanes each hold d/2 fp32 outputs, then m (exp2 domain) and l
-// of every lane.
+// lanes of the global mode's waves each hold d/2 fp32 outputs, then m (exp2
+// domain) and l of every lane.
 __host__ __device__ constexpr size_t partial_floats(int head_dim) {
-    return (size_t)kWaves * 64 * (head_dim / 2 + 2);
+    return (size_t)kWavesGlobal * 64 * (head_dim / 2 + 2);
 }
 // Partial slots (per head group) for a problem with max_tiles tiles: split
 // tiles have more than W / (kSplitDiv grid n_hg) blocks for a total of W
@@ -72,8 +81,6 @@ inline int split_slots(int max_tiles, int n_hg) {
     const long long b = 2LL * kSplitDiv * kSplitGridRef / n_hg + kMaxSplit;
     return (int)(a < b ? a : b);
 }
-
-enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
 
 // Epilogue of the local / global modes.
 //   kEpiRaw   : write the branch output O (fp32) -- logo_local_attn and
