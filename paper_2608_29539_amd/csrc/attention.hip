@@ -43,17 +43,23 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
 
-// LDS tiles, both in natural [key][d] order.  K rows are padded by 16 B so
-// that the 16-byte fragment reads of 8 consecutive rows hit distinct banks;
-// V rows by 64 B so that the transpose reads (4 rows x 32 B per 16 lanes,
-// two 16-lane groups 32 B apart) do.
+// LDS tiles, both [key][d].  K rows are padded by 16 B so that the 16-byte
+// fragment reads of 8 consecutive rows hit distinct banks.  V rows are not
+// padded; instead the 64-byte segments of a row are permuted (segment j of
+// row r is stored at j ^ vswz(r)) so that the transpose reads, which take
+// one 64-byte segment from each of 4 consecutive rows per half-wave, hit 4
+// distinct 64-byte bank groups of the 256-byte bank window.
 constexpr int kKPad = 8;
-constexpr int kVPad = 32;
 template <int D>
 struct alignas(16) Smem {
     uint16_t k[kBlockN][D + kKPad];
-    uint16_t v[kBlockN][D + kVPad];
+    uint16_t v[kBlockN][D];
 };
+template <int D>
+__device__ __forceinline__ constexpr int vswz(int r) {
+    // rows per 256-byte bank window: 128 / D; segments per row: D / 32
+    return (r / (128 / D)) % (D / 32);
+}
 
 // Value of the partner lane (l ^ 32) and own value, combined.
 __device__ __forceinline__ float pair_max(float x) {
@@ -76,7 +82,7 @@ constexpr int kRawBufferFlags = 0x00020000;
 template <int D, int W>
 struct Dma {
     static constexpr int kSlotsK = (D + kKPad) * 2 / 16;     // 16-byte slots per K row
-    static constexpr int kSlotsV = (D + kVPad) * 2 / 16;
+    static constexpr int kSlotsV = D * 2 / 16;
     static constexpr int kInstK = kSlotsK;                   // 64 rows x slots / 64 lanes
     static constexpr int kInstV = kSlotsV;
     static constexpr int kPerWaveK = (kInstK + W - 1) / W;
@@ -95,8 +101,10 @@ __device__ __forceinline__ void dma_plan(Dma<D, W> &d, int wave, int lane, int r
     }
 #pragma unroll
     for (int i = 0; i < Dma<D, W>::kPerWaveV; i++) {
+        // LDS slot (row, chunk p) receives the chunk whose segment maps to p's
         const int slot = (i * W + wave) * 64 + lane;
-        const int row = slot / Dma<D, W>::kSlotsV, col = min(slot % Dma<D, W>::kSlotsV, D / 8 - 1);
+        const int row = slot / Dma<D, W>::kSlotsV, p = slot % Dma<D, W>::kSlotsV;
+        const int col = ((p >> 2) ^ vswz<D>(row)) * 4 + (p & 3);
         d.voff_v[i] = row * row_bytes + col * 16;
     }
 }
@@ -336,6 +344,12 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     // Lane's row / column inside a V tile for the transpose reads.
     const int vt_row = 4 * g + ((lane & 15) >> 2);
     const int vt_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    // Stored column of this lane's read in 32-column block cb (the rows it
+    // reads differ from vt_row by multiples of 8, which keep vswz).
+    int vt_scol[D / 32];
+#pragma unroll
+    for (int cb = 0; cb < D / 32; cb++)
+        vt_scol[cb] = (cb ^ vswz<D>(vt_row)) * 32 + vt_col;
 
     const int w = a.window;
     const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
@@ -390,8 +404,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         }
 #pragma unroll
         for (int cb = 0; cb < D / 32; cb++) {
-            const bf16x8 vf = read_vt_frag(&vb.v[sb * 32 + ss * 16 + vt_row][cb * 32 + vt_col],
-                                           D + kVPad);
+            const bf16x8 vf = read_vt_frag(&vb.v[sb * 32 + ss * 16 + vt_row][vt_scol[cb]], D);
             acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
         }
     };
