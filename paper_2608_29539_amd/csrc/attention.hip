@@ -335,10 +335,14 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
 #pragma unroll
         for (int s = 0; s < D / 16; s++)
             qf[s] = *(const bf16x8 *)(qp + s * 16);
-        // Q is in registers before the KV loop starts: inside the loop the
-        // only vector-memory loads in flight are the K/V tile loads, which the
-        // compiler does not track.
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    }
+    // Inputs of the fused epilogue, fetched now so that their latency overlaps
+    // the KV loop.
+    float ep_gate = 0.f;
+    int ep_rank = -1;
+    if (EPI == kEpiFused && MODE != kModeDense) {
+        ep_gate = a.gate[qtok];
+        ep_rank = (MODE == kModeGlobal) ? (int)orow : a.tok2sel[qtok];
     }
 
     // Lane's row / column inside a V tile for the transpose reads.
@@ -390,6 +394,9 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     bf16x2 pw[2][8];                          // P of the last softmax-ed tile
     __syncthreads();                         // the previous item's last tile is consumed
     dma_k<D, W>(sm[0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
+    // This wait also covers the Q (and epilogue input) loads: inside the loop
+    // the only vector-memory loads in flight are the K/V tile loads, which
+    // the compiler does not track.
     dma_wait_barrier();
 
     // PV of the tile whose P is in pw, V read from buffer vb, for one 16-key
@@ -578,8 +585,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
             return;
         const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
         const int64_t tok = qtok;
-        const float p = a.gate[tok];
-        const int r = (MODE == kModeGlobal) ? (int)orow : a.tok2sel[tok];
+        const float p = ep_gate;
+        const int r = ep_rank;
         const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
         uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
         if (MODE == kModeLocal && r >= 0) {
