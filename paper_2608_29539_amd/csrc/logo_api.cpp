@@ -99,7 +99,7 @@ SelectWs select_ws(const logo_problem *p) {
     w.thr = off;
     off += align_up(sizeof(float) * (size_t)p->num_seqs);
     w.counts = off;
-    off += align_up(sizeof(int32_t) * (size_t)select_chunks(p->total_tokens));
+    off += align_up(sizeof(int32_t) * (size_t)p->num_seqs);
     w.total = off;
     return w;
 }

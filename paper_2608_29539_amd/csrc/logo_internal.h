@@ -132,12 +132,12 @@ hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
                               SparseTile *tiles, int32_t *scratch, int32_t *queue,
                               int32_t *split_cnt, hipStream_t s);
 
+// Selection: thresholds, ranks and compaction.  seq_counts holds num_seqs
+// ints (per-sequence selected counts when num_seqs > 1).
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *chunk_counts,
-                         hipStream_t s);
-int select_chunks(int n_tokens);
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s);
 
 hipError_t launch_combine(int n_tokens, int hq, int head_dim, const float *o_local,
                           const float *o_global, const float *gate,

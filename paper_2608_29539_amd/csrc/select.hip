@@ -3,14 +3,18 @@
 // original positions and compacted sequence offsets), plus the tile plan
 // of the query-sparse global branch.
 //
-//   threshold_kernel  ratio mode: per sequence, k = floor(ratio*T) in IEEE
-//                     double; the threshold is the (k+1)-th largest gate, found
-//                     by a three-pass radix select (12 + 12 + 8 bits) over
-//                     order-preserving uint32 keys with LDS histograms.
-//   count_kernel      z_t = gate[t] > thr[b(t)] (strict, fp32); per-chunk counts
-//                     from wave ballots.
-//   write_kernel      exclusive ranks (chunk offset + ballot/mbcnt prefix),
-//                     writes sel_idx, tok2sel and cu_sel.
+//   select_seq_kernel one 1024-thread workgroup per sequence.  Threshold:
+//                     ratio mode takes k = floor(ratio*T) in IEEE double and
+//                     the (k+1)-th largest gate, found by a three-pass radix
+//                     select (12 + 12 + 8 bits) over order-preserving uint32
+//                     keys with LDS histograms; threshold mode takes the given
+//                     value.  Then z_t = gate[t] > thr (strict, fp32, done on
+//                     the keys) is counted and, with the sequence's offset
+//                     known, compacted: ranks from wave ballots, mbcnt and a
+//                     workgroup scan; writes sel_idx, tok2sel and cu_sel.  One
+//                     sequence: a single launch does all of it.  Several: a
+//                     first launch finds the thresholds and counts, a second
+//                     one compacts with offset = sum of the earlier counts.
 //   sparse_plan_kernel
 //                     cuts each sequence's selected rows into tiles of tpw
 //                     rows, splits the longest tiles into KV ranges so that no
@@ -23,10 +27,10 @@
 namespace logo {
 namespace {
 
-constexpr int kSelThreads = 256;
-constexpr int kSelPerThread = 16;
-constexpr int kSelChunk = kSelThreads * kSelPerThread;   // tokens per workgroup
-constexpr int kRadixThreads = 1024;
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kKeysPerThread = 32;                      // gate keys per thread per chunk
+constexpr int kSelChunk = kKeysPerThread * kSelThreads;  // tokens per chunk (32768)
 
 // Order-preserving map from fp32 to uint32 (-0 is folded onto +0 first).
 __device__ __forceinline__ uint32_t float_key(float f) {
@@ -39,11 +43,12 @@ __device__ __forceinline__ float key_float(uint32_t k) {
     const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
     return __uint_as_float(u);
 }
+// Keys above this one are positive NaNs, which never compare greater.
+constexpr uint32_t kPosInfKey = 0xFF800000u;
 
 // Block-wide inclusive scan of one int per thread (blockDim.x <= 1024).
 __device__ __forceinline__ int block_inclusive_scan(int v, int *s_wave) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int nwaves = (blockDim.x + 63) >> 6;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
         const int t = __shfl_up(v, d, 64);
@@ -56,77 +61,23 @@ __device__ __forceinline__ int block_inclusive_scan(int v, int *s_wave) {
     int before = 0;
     for (int i = 0; i < wave; i++)
         before += s_wave[i];
-    (void)nwaves;
     __syncthreads();
     return v + before;
 }
 
-__global__ __launch_bounds__(kRadixThreads) void threshold_kernel(const int32_t *cu,
-                                                                  const float *gate,
-                                                                  double ratio, float *thr) {
-    __shared__ int hist[4096];
-    __shared__ int s_wave[16];
-    __shared__ uint32_t s_bin;
-    __shared__ int s_rank;
-    const int b = blockIdx.x, tid = threadIdx.x;
-    const int base = cu[b];
-    const int T = cu[b + 1] - base;
-    const long long k = (long long)floor(ratio * (double)T);
-    if (k >= T) {
-        if (tid == 0)
-            thr[b] = -__builtin_inff();
-        return;
-    }
-    int rank = (int)(T - k - 1);      // ascending rank of the threshold value
-    uint32_t prefix = 0, pmask = 0;
-    const int shifts[3] = {20, 8, 0};
-    const int widths[3] = {12, 12, 8};
-    for (int pass = 0; pass < 3; pass++) {
-        const int sh = shifts[pass], nb = 1 << widths[pass];
-        for (int i = tid; i < 4096; i += kRadixThreads)
-            hist[i] = 0;
-        __syncthreads();
-        for (int t = tid; t < T; t += kRadixThreads) {
-            const uint32_t key = float_key(gate[base + t]);
-            if ((key & pmask) == prefix)
-                atomicAdd(&hist[(key >> sh) & (nb - 1)], 1);
-        }
-        __syncthreads();
-        // Each thread owns 4 consecutive bins (nb <= 4096).
-        int own = 0;
-        int cnt[4];
+// Block-wide sum (every thread gets it).
+__device__ __forceinline__ int block_sum(int v, int *s_wave) {
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-            const int bin = tid * 4 + j;
-            cnt[j] = bin < nb ? hist[bin] : 0;
-            own += cnt[j];
-        }
-        const int incl = block_inclusive_scan(own, s_wave);
-        int run = incl - own;
-#pragma unroll
-        for (int j = 0; j < 4; j++) {
-            if (cnt[j] > 0 && rank >= run && rank < run + cnt[j]) {
-                s_bin = (uint32_t)(tid * 4 + j);
-                s_rank = rank - run;
-            }
-            run += cnt[j];
-        }
-        __syncthreads();
-        prefix |= s_bin << sh;
-        pmask |= (uint32_t)(nb - 1) << sh;
-        rank = s_rank;
-        __syncthreads();
-    }
-    if (tid == 0) {
-        float f = key_float(prefix);
-        thr[b] = f;
-    }
-}
-
-__global__ void fill_threshold_kernel(int num_seqs, float value, float *thr) {
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b < num_seqs)
-        thr[b] = value;
+    for (int d = 32; d > 0; d >>= 1)
+        v += __shfl_xor(v, d, 64);
+    if ((threadIdx.x & 63) == 0)
+        s_wave[threadIdx.x >> 6] = v;
+    __syncthreads();
+    int sum = 0;
+    for (int i = 0; i < (int)(blockDim.x >> 6); i++)
+        sum += s_wave[i];
+    __syncthreads();
+    return sum;
 }
 
 // Largest b in [0, B-1] with cu[b] <= t (the owner of token t).
@@ -142,109 +93,193 @@ __device__ __forceinline__ int owner_seq(const int32_t *cu, int B, int t) {
     return lo;
 }
 
-__global__ __launch_bounds__(kSelThreads) void count_kernel(const int32_t *cu, int B, int N,
-                                                             const float *gate, const float *thr,
-                                                             int32_t *chunk_counts) {
-    __shared__ int s_cnt[kSelThreads / 64];
-    const int c0 = blockIdx.x * kSelChunk;
-    const int tid = threadIdx.x;
-    int b = -1, b_end = 0;
-    int count = 0;
-    for (int i = 0; i < kSelPerThread; i++) {
-        const int t = c0 + i * kSelThreads + tid;
-        bool z = false;
-        if (t < N) {
-            if (b < 0 || t >= b_end) {
-                b = owner_seq(cu, B, t);
-                b_end = cu[b + 1];
-            }
-            z = gate[t] > thr[b];
-        }
-        count += __popcll(__ballot(z));
-    }
-    if ((tid & 63) == 0)
-        s_cnt[tid >> 6] = count;
-    __syncthreads();
-    if (tid == 0) {
-        int s = 0;
-        for (int w = 0; w < kSelThreads / 64; w++)
-            s += s_cnt[w];
-        chunk_counts[blockIdx.x] = s;
-    }
-}
+// kThreshold: find thr[b] (ratio mode) or take `fixed` (threshold mode), and
+// write thr[b]; otherwise read thr[b].  kWrite: compact (offset = sum of
+// cnt[b'] over b' < b, or 0 for a single sequence); otherwise write cnt[b].
+template <bool kThreshold, bool kWrite>
+__global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
+    const int32_t *__restrict__ cu, int B, const float *__restrict__ gate, int mode, float fixed,
+    double ratio, float *__restrict__ thr, int32_t *__restrict__ cnt, int32_t *__restrict__ sel_idx,
+    int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel) {
+    __shared__ int hist[4096];
+    __shared__ int s_wave[kSelWaves];
+    __shared__ uint32_t s_bin;
+    __shared__ int s_rank, s_bincnt;
+    __shared__ int s_cnt[kKeysPerThread * kSelWaves];   // selected per (round, wave)
+    __shared__ int s_total;
+    const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t base = cu[b];
+    const int T = cu[b + 1] - (int)base;
 
-__global__ __launch_bounds__(kSelThreads) void write_kernel(const int32_t *cu, int B, int N,
-                                                             const float *gate, const float *thr,
-                                                             const int32_t *chunk_counts,
-                                                             int32_t *sel_idx, int32_t cap,
-                                                             int32_t *cu_sel, int32_t *tok2sel) {
-    __shared__ int s_red[kSelThreads / 64];
-    __shared__ int s_off;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // Offset of this chunk = sum of the counts of all earlier chunks.
-    int part = 0;
-    for (int i = tid; i < (int)blockIdx.x; i += kSelThreads)
-        part += chunk_counts[i];
+    // Keys of one chunk of kSelChunk tokens (token c0 + j * 1024 + tid in
+    // key[j]), loaded with all loads in flight at once; a sequence that fits
+    // in one chunk is loaded once.
+    const bool resident = T <= kSelChunk;
+    uint32_t key[kKeysPerThread];
+    auto load_chunk = [&](int c0) {
 #pragma unroll
-    for (int d = 32; d > 0; d >>= 1)
-        part += __shfl_xor(part, d, 64);
-    if (lane == 0)
-        s_red[wave] = part;
-    __syncthreads();
-    if (tid == 0) {
-        int s = 0;
-        for (int w = 0; w < kSelThreads / 64; w++)
-            s += s_red[w];
-        s_off = s;
-    }
-    __syncthreads();
-    int offset = s_off;
-    __syncthreads();
+        for (int j = 0; j < kKeysPerThread; j++) {
+            const int t = c0 + j * kSelThreads + tid;
+            key[j] = t < T ? float_key(gate[base + t]) : 0u;
+        }
+    };
+    if (resident)
+        load_chunk(0);
 
-    const int c0 = blockIdx.x * kSelChunk;
-    int b = -1, b_end = 0;
-    for (int i = 0; i < kSelPerThread; i++) {
-        const int t = c0 + i * kSelThreads + tid;
-        bool z = false;
-        if (t < N) {
-            if (b < 0 || t >= b_end) {
-                b = owner_seq(cu, B, t);
-                b_end = cu[b + 1];
+    uint32_t thr_key;
+    if constexpr (kThreshold) {
+        const long long k = mode == 1 ? (long long)floor(ratio * (double)T) : 0;
+        if (mode != 1) {
+            thr_key = float_key(fixed);
+        } else if (k >= T) {
+            thr_key = float_key(-__builtin_inff());
+        } else {
+            int rank = (int)(T - k - 1);      // ascending rank of the threshold value
+            uint32_t prefix = 0, pmask = 0;
+            for (int pass = 0; pass < 3; pass++) {
+                const int sh = pass == 0 ? 20 : (pass == 1 ? 8 : 0);
+                const int nb = pass == 2 ? 256 : 4096;
+                for (int i = tid; i < 4096; i += kSelThreads)
+                    hist[i] = 0;
+                __syncthreads();
+                for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+                    if (!resident)
+                        load_chunk(c0);
+                    // Runs of equal digits are counted in a register and added
+                    // in one atomic (concentrated gate distributions put most
+                    // keys of a pass into a few bins).
+                    int cur = -1, run_len = 0;
+#pragma unroll
+                    for (int j = 0; j < kKeysPerThread; j++) {
+                        const int t = c0 + j * kSelThreads + tid;
+                        if (t < T && (key[j] & pmask) == prefix) {
+                            const int d = (int)((key[j] >> sh) & (uint32_t)(nb - 1));
+                            if (d != cur) {
+                                if (run_len > 0)
+                                    atomicAdd(&hist[cur], run_len);
+                                cur = d;
+                                run_len = 0;
+                            }
+                            run_len++;
+                        }
+                    }
+                    if (run_len > 0)
+                        atomicAdd(&hist[cur], run_len);
+                }
+                __syncthreads();
+                // Each thread owns 4 consecutive bins.
+                int own = 0;
+                int c4[4];
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    const int bin = tid * 4 + j;
+                    c4[j] = bin < nb ? hist[bin] : 0;
+                    own += c4[j];
+                }
+                const int incl = block_inclusive_scan(own, s_wave);
+                int run = incl - own;
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    if (c4[j] > 0 && rank >= run && rank < run + c4[j]) {
+                        s_bin = (uint32_t)(tid * 4 + j);
+                        s_rank = rank - run;
+                        s_bincnt = c4[j];
+                    }
+                    run += c4[j];
+                }
+                __syncthreads();
+                prefix |= s_bin << sh;
+                pmask |= (uint32_t)(nb - 1) << sh;
+                rank = s_rank;
+                const bool unique = s_bincnt == 1;
+                __syncthreads();
+                if (pass < 2 && unique && resident) {
+                    // one key left in the bin: it is the threshold
+#pragma unroll
+                    for (int j = 0; j < kKeysPerThread; j++) {
+                        const int t = j * kSelThreads + tid;
+                        if (t < T && (key[j] & pmask) == prefix)
+                            s_bin = key[j];
+                    }
+                    __syncthreads();
+                    prefix = s_bin;
+                    break;
+                }
             }
-            z = gate[t] > thr[b];
+            thr_key = prefix;
         }
-        const unsigned long long mask = __ballot(z);
-        const int lane_prefix = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-        if (lane == 0)
-            s_red[wave] = __popcll(mask);
-        __syncthreads();
-        int before = 0, total = 0;
-        for (int w = 0; w < kSelThreads / 64; w++) {
-            const int cw = s_red[w];
-            if (w < wave)
-                before += cw;
-            total += cw;
-        }
-        __syncthreads();
-        const int rank = offset + before + lane_prefix;   // exclusive rank of token t
-        if (t < N) {
-            if (z && rank < cap)
-                sel_idx[rank] = t;
-            if (tok2sel)
-                tok2sel[t] = (z && rank < cap) ? rank : -1;
-            // cu_sel[b'] for every sequence b' that starts at token t
-            if (cu[b] == t) {
-                for (int bb = b; bb >= 0 && cu[bb] == t; bb--)
-                    cu_sel[bb] = rank;
-            }
-        }
-        offset += total;
+        if (tid == 0)
+            thr[b] = mode == 1 ? key_float(thr_key) : fixed;
+    } else {
+        thr_key = float_key(thr[b]);
     }
-    // Sequences that start at N (the end), including cu_sel[B] = n_sel.
-    if (blockIdx.x == gridDim.x - 1 && tid == 0) {
-        for (int bb = B; bb >= 0 && cu[bb] == N; bb--)
-            cu_sel[bb] = offset;
+    // z = gate > thr on the keys: -0 and +0 share a key, and NaN gates (keys
+    // above +inf, or below -inf) never pass.
+    auto pass_z = [&](uint32_t kj, int t) { return t < T && kj > thr_key && kj <= kPosInfKey; };
+
+    if constexpr (!kWrite) {
+        int mine = 0;
+        for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+            if (!resident)
+                load_chunk(c0);
+#pragma unroll
+            for (int j = 0; j < kKeysPerThread; j++)
+                mine += pass_z(key[j], c0 + j * kSelThreads + tid) ? 1 : 0;
+        }
+        const int total = block_sum(mine, s_wave);
+        if (tid == 0)
+            cnt[b] = total;
+    } else {
+        int offset = 0;
+        if (B > 1) {
+            int part = 0;
+            for (int i = tid; i < b; i += kSelThreads)
+                part += cnt[i];
+            offset = block_sum(part, s_wave);
+        }
+        if (tid == 0)
+            cu_sel[b] = offset;
+        int running = offset;
+        for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+            if (!resident)
+                load_chunk(c0);
+            uint64_t mask[kKeysPerThread];
+#pragma unroll
+            for (int j = 0; j < kKeysPerThread; j++) {
+                mask[j] = __ballot(pass_z(key[j], c0 + j * kSelThreads + tid));
+                if (lane == 0)
+                    s_cnt[j * kSelWaves + wave] = (int)__popcll(mask[j]);
+            }
+            __syncthreads();
+            // exclusive scan of the (round, wave) counts in token order
+            const int n_cnt = kKeysPerThread * kSelWaves;   // 512 <= 1024
+            const int v = tid < n_cnt ? s_cnt[tid] : 0;
+            const int incl = block_inclusive_scan(v, s_wave);
+            if (tid < n_cnt)
+                s_cnt[tid] = incl - v;
+            if (tid == kSelThreads - 1)
+                s_total = incl;
+            __syncthreads();
+#pragma unroll
+            for (int j = 0; j < kKeysPerThread; j++) {
+                const int t = c0 + j * kSelThreads + tid;
+                if (t < T) {
+                    const uint64_t m = mask[j];
+                    const bool z = (m >> lane) & 1ull;
+                    const int r = running + s_cnt[j * kSelWaves + wave] +
+                                  (int)__builtin_amdgcn_mbcnt_hi(
+                                      (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+                    if (z && r < cap)
+                        sel_idx[r] = (int32_t)(base + t);
+                    if (tok2sel)
+                        tok2sel[base + t] = (z && r < cap) ? r : -1;
+                }
+            }
+            running += s_total;
+            __syncthreads();
+        }
+        if (b == B - 1 && tid == 0)
+            cu_sel[B] = running;
     }
 }
 
@@ -419,33 +454,25 @@ __global__ __launch_bounds__(1024) void sparse_plan_kernel(
 
 }  // namespace
 
-int select_chunks(int n_tokens) {
-    const int c = (n_tokens + kSelChunk - 1) / kSelChunk;
-    return c > 0 ? c : 1;
-}
-
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *chunk_counts, hipStream_t s) {
-    if (mode == 1) {
-        hipLaunchKernelGGL(threshold_kernel, dim3(num_seqs), dim3(kRadixThreads), 0, s,
-                           cu_seqlens, gate, ratio, thr);
-    } else {
-        hipLaunchKernelGGL(fill_threshold_kernel, dim3((num_seqs + 255) / 256), dim3(256), 0, s,
-                           num_seqs, threshold, thr);
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s) {
+    (void)n_tokens;
+    if (num_seqs == 1) {
+        hipLaunchKernelGGL((select_seq_kernel<true, true>), dim3(1), dim3(kSelThreads), 0, s,
+                           cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
+                           sel_capacity, cu_sel, tok2sel);
+        return hipGetLastError();
     }
+    hipLaunchKernelGGL((select_seq_kernel<true, false>), dim3(num_seqs), dim3(kSelThreads), 0, s,
+                       cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
+                       sel_capacity, cu_sel, tok2sel);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    const int chunks = select_chunks(n_tokens);
-    hipLaunchKernelGGL(count_kernel, dim3(chunks), dim3(kSelThreads), 0, s, cu_seqlens, num_seqs,
-                       n_tokens, gate, (const float *)thr, chunk_counts);
-    e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
-    hipLaunchKernelGGL(write_kernel, dim3(chunks), dim3(kSelThreads), 0, s, cu_seqlens, num_seqs,
-                       n_tokens, gate, (const float *)thr, (const int32_t *)chunk_counts, sel_idx,
+    hipLaunchKernelGGL((select_seq_kernel<false, true>), dim3(num_seqs), dim3(kSelThreads), 0, s,
+                       cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
                        sel_capacity, cu_sel, tok2sel);
     return hipGetLastError();
 }
