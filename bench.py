@@ -55,14 +55,24 @@ def pair_counts(cu: np.ndarray, window: int, sel_idx: np.ndarray):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_global_T32k-gqa_traffic.md")
-KERNEL_SRC = os.path.join(ROOT, "paper_2608_29539_amd", "csrc", "attention.hip")
+# Sources whose change invalidates the committed counter figures: the global
+# kernel, its tiling constants and the tile plan that orders its work.
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_29539_amd", "csrc", f)
+               for f in ("attention.hip", "logo_internal.h", "select.hip")]
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()
 
 
 def committed_traffic(workload: str):
     """HBM bytes per launch of the global kernel from the committed counter
     summary, or None when the summary is missing, is for another workload, or
     was taken on a different kernel source than the one built now."""
-    import hashlib
     if not os.path.exists(TRAFFIC_FILE):
         return None
     fields = {}
@@ -70,7 +80,7 @@ def committed_traffic(workload: str):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    src_hash = hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    src_hash = kernel_source_hash()
     if fields.get("workload") != workload or fields.get("kernel_source_sha256") != src_hash:
         return None
     try:
@@ -193,7 +203,7 @@ def main(argv=None):
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     ms_step = start.elapsed_time(end) / args.steps
-    stage_names = ("select", "local", "global", "combine")
+    stage_names = ("select", "local", "plan", "global")
     stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1])
                                   for i in range(args.warmup, n_ev)]))
                 for j, n in enumerate(stage_names)}

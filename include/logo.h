@@ -197,14 +197,14 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
 /*
  * logo_attn_fwd_profiled -- logo_attn_fwd that additionally records five
  * caller-created HIP events (hipEvent_t, passed as void*) on `stream`:
- *   events[0] before the selection kernels, events[1] after them,
+ *   events[0] before the selection kernel(s), events[1] after them,
  *   events[2] after the local branch (which also applies Norm^L and writes
- *   the unselected rows of `out`), events[3] after the global branch (tile
- *   plan + query-sparse attention, which applies Norm^G and the fusion for
- *   the selected rows), events[4] at the end (ContextNorm and fusion run
- *   inside the two attention kernels, so events[3] and events[4] bracket no
- *   work).  Elapsed times between consecutive events are the stage times.
- *   `events` must not be NULL; everything else is as for logo_attn_fwd.
+ *   the unselected rows of `out`), events[3] after the tile plan of the
+ *   global branch, events[4] after the query-sparse attention kernel (which
+ *   applies Norm^G and the fusion for the selected rows).  Elapsed times
+ *   between consecutive events are the stage times (select, local, plan,
+ *   global).  `events` must not be NULL; everything else is as for
+ *   logo_attn_fwd.
  */
 logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v,

@@ -257,9 +257,9 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                        const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
                        int32_t cap, float *o, const FusedEpi *f, const float *gain, char *ws,
-                       hipStream_t s) {
+                       hipStream_t s, hipEvent_t after_plan = nullptr) {
     if (p->total_tokens == 0 || cap == 0)
-        return LOGO_OK;
+        return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
     const GlobalWs w = global_ws(p, cap);
     SparseTile *tiles = (SparseTile *)(ws + w.tiles);
@@ -280,6 +280,8 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
         s);
     if (st != LOGO_OK)
         return st;
+    if (after_plan && hipEventRecord(after_plan, s) != hipSuccess)
+        return LOGO_ERR_HIP;
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;
@@ -353,8 +355,8 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     if (st != LOGO_OK || (st = mark(2)) != LOGO_OK)
         return st;
     st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, nullptr, &fe,
-                    gain_global, base + w.glob_ws, s);
-    if (st != LOGO_OK || (st = mark(3)) != LOGO_OK)
+                    gain_global, base + w.glob_ws, s, events ? (hipEvent_t)events[3] : nullptr);
+    if (st != LOGO_OK)
         return st;
     return mark(4);
 }
