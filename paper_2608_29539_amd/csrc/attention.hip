@@ -52,8 +52,8 @@ constexpr float kNegInf = -__builtin_inff();
 constexpr int kKPad = 8;
 template <int D>
 struct alignas(16) Smem {
-    uint16_t k[kBlockN][D + kKPad];
-    uint16_t v[kBlockN][D];
+    uint16_t k[2][kBlockN][D + kKPad];
+    uint16_t v[2][kBlockN][D];
 };
 template <int D>
 __device__ __forceinline__ constexpr int vswz(int r) {
@@ -147,25 +147,25 @@ __device__ __forceinline__ void lds_load16(u32x4 r, const void *lds, int voffset
 }
 
 template <int D, int W>
-__device__ __forceinline__ void dma_k(Smem<D> &buf, const Dma<D, W> &d, const uint16_t *kv_k,
+__device__ __forceinline__ void dma_k(uint16_t *dst, const Dma<D, W> &d, const uint16_t *kv_k,
                                       int T, int k0, int row_bytes, int wave) {
     const u32x4 r = tile_rsrc(kv_k, T, k0, row_bytes);
 #pragma unroll
     for (int i = 0; i < Dma<D, W>::kPerWaveK; i++) {
         const int inst = i * W + wave;
         if (inst < Dma<D, W>::kInstK)
-            lds_load16(r, (char *)&buf.k[0][0] + inst * 1024, d.voff_k[i]);
+            lds_load16(r, (char *)dst + inst * 1024, d.voff_k[i]);
     }
 }
 template <int D, int W>
-__device__ __forceinline__ void dma_v(Smem<D> &buf, const Dma<D, W> &d, const uint16_t *kv_v,
+__device__ __forceinline__ void dma_v(uint16_t *dst, const Dma<D, W> &d, const uint16_t *kv_v,
                                       int T, int k0, int row_bytes, int wave) {
     const u32x4 r = tile_rsrc(kv_v, T, k0, row_bytes);
 #pragma unroll
     for (int i = 0; i < Dma<D, W>::kPerWaveV; i++) {
         const int inst = i * W + wave;
         if (inst < Dma<D, W>::kInstV)
-            lds_load16(r, (char *)&buf.v[0][0] + inst * 1024, d.voff_v[i]);
+            lds_load16(r, (char *)dst + inst * 1024, d.voff_v[i]);
     }
 }
 
@@ -284,7 +284,7 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
 }
 
 template <int D, int MODE, int EPI>
-__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int b, int hg,
+__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int b, int hg,
                                             int jt, SparseTile tile) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);
@@ -386,22 +386,47 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         acc[cb] = f32x16{};
     float m_ref = kNegInf, l_run = 0.f;
 
-    // Software-pipelined KV loop.  Iteration kb issues S(kb) = K(kb) Q^T and
-    // then PV(kb-1) (the previous tile's rounded P, kept in registers), so the
-    // softmax of tile kb overlaps the PV MFMAs of tile kb-1.  K(kb+1) and V(kb)
-    // are staged during iteration kb (V one tile later than K, because it is
-    // consumed one iteration later); two buffers each, one barrier per tile.
+    // Software-pipelined KV loop.  Step kb (between two barriers) stages
+    // K(kb+1) and V(kb), computes S(kb) = K(kb) Q^T, then interleaves the
+    // softmax of tile kb, 16 keys at a time, with the PV MFMAs of tile kb-1
+    // (its rounded P kept in registers), so the exps of one tile overlap the
+    // PV MFMAs of the previous one.  V is consumed one step after K; two
+    // buffers each, and every buffer is rewritten only after the barrier that
+    // ends its last read.
     bf16x2 pw[2][8];                          // P of the last softmax-ed tile
+    f32x16 s[2];                              // S of the tile being softmax-ed
+    auto kidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
+    auto vidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
     __syncthreads();                         // the previous item's last tile is consumed
-    dma_k<D, W>(sm[0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
+    dma_k<D, W>(&sm.k[0][0][0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
     // This wait also covers the Q (and epilogue input) loads: inside the loop
     // the only vector-memory loads in flight are the K/V tile loads, which
     // the compiler does not track.
     dma_wait_barrier();
 
-    // PV of the tile whose P is in pw, V read from buffer vb, for one 16-key
-    // slice q (0..3) of the 64-key tile.
-    auto pv_slice = [&](const Smem<D> &vb, int q) {
+    // Loads of step kb: K(kb+1) and V(kb).
+    auto stage = [&](int kb_) {
+        if (kb_ < kb_hi)
+            dma_k<D, W>(&sm.k[kidx(kb_ + 1)][0][0], dma, kv_k, T, (kb_ + 1) * kBlockN, row_bytes,
+                        wave);
+        dma_v<D, W>(&sm.v[vidx(kb_)][0][0], dma, kv_v, T, kb_ * kBlockN, row_bytes, wave);
+    };
+    // S(kb) = K(kb) Q^T into s.
+    auto op_s = [&](int kb_) {
+        const uint16_t(*kt)[D + kKPad] = sm.k[kidx(kb_)];
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++) {
+            s[sb] = f32x16{};
+#pragma unroll
+            for (int ss = 0; ss < D / 16; ss++) {
+                const bf16x8 kf = *(const bf16x8 *)&kt[sb * 32 + m][ss * 16 + g * 8];
+                s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
+            }
+        }
+    };
+    // PV of the tile whose P is in pw, V from buffer vi, for one 16-key slice
+    // q (0..3) of the 64-key tile.
+    auto pv_slice = [&](int vi, int q) {
         const int sb = q >> 1, ss = q & 1;
         bf16x8 pf;
 #pragma unroll
@@ -411,14 +436,14 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         }
 #pragma unroll
         for (int cb = 0; cb < D / 32; cb++) {
-            const bf16x8 vf = read_vt_frag(&vb.v[sb * 32 + ss * 16 + vt_row][vt_scol[cb]], D);
+            const bf16x8 vf = read_vt_frag(&sm.v[vi][sb * 32 + ss * 16 + vt_row][vt_scol[cb]], D);
             acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
         }
     };
-    auto pv = [&](const Smem<D> &vb) {
+    auto pv = [&](int vi) {
 #pragma unroll
         for (int q = 0; q < 4; q++)
-            pv_slice(vb, q);
+            pv_slice(vi, q);
     };
     // Rescale of O decided by the previous softmax, applied before the next
     // PV accumulates into O (deferred so that no branch separates a tile's
@@ -433,88 +458,76 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
             resc_pend = false;
         }
     };
-
-    // One KV tile.  do_s: compute S(kb) and its softmax into pw.  do_pv:
-    // also accumulate PV of the previous tile (V from the other buffer), one
-    // 16-key slice at a time, each slice's 4 MFMAs followed by the 8 exps that
-    // overwrite that slice of pw with tile kb's P.  masked: apply the
-    // real-position mask (diagonal / window-edge tiles only).
-    auto step = [&](int kb, auto do_s, auto do_pv, auto masked) {
-        const int cb_ = (kb - kb_lo) & 1;
-        // K(kb+1) into the other K buffer, V(kb) into this tile's V buffer:
-        // both were last read before the previous barrier.
-        if (kb < kb_hi)
-            dma_k<D, W>(sm[cb_ ^ 1], dma, kv_k, T, (kb + 1) * kBlockN, row_bytes, wave);
-        dma_v<D, W>(sm[cb_], dma, kv_v, T, kb * kBlockN, row_bytes, wave);
-        if constexpr (decltype(do_pv)::value)
-            apply_rescale();
-        if constexpr (decltype(do_s)::value) {
-            const Smem<D> &cur = sm[cb_];
-            f32x16 s[2];
-#pragma unroll
-            for (int sb = 0; sb < 2; sb++) {
-                s[sb] = f32x16{};
-#pragma unroll
-                for (int ss = 0; ss < D / 16; ss++) {
-                    const bf16x8 kf = *(const bf16x8 *)&cur.k[sb * 32 + m][ss * 16 + g * 8];
-                    s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
-                }
-            }
-            if constexpr (decltype(masked)::value) {
-                const int k0 = kb * kBlockN;
-#pragma unroll
-                for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-                    for (int i = 0; i < 16; i++) {
-                        const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
-                        bool ok = key <= pos;
-                        if (MODE == kModeLocal)
-                            ok = ok && (key > pos - w);
-                        if (!ok)
-                            s[sb][i] = kNegInf;
-                    }
-            }
-            float mx = kNegInf;
+    // Softmax of tile kb (s -> pw); with do_pv, each 16-key slice's exps are
+    // preceded by that slice's PV MFMAs of tile kb-1 (V(kb-1)), which read
+    // the old pw before the exps overwrite it.  masked: the real-position
+    // mask (diagonal / window-edge tiles only).
+    auto op_sm = [&](int kb_, auto do_pv, auto masked) {
+        if constexpr (decltype(masked)::value) {
+            const int k0 = kb_ * kBlockN;
 #pragma unroll
             for (int sb = 0; sb < 2; sb++)
 #pragma unroll
-                for (int i = 0; i < 16; i++)
-                    mx = fmaxf(mx, s[sb][i]);
-            mx = pair_max(mx) * c;           // tile max in the exp2 domain
-            // The reference moves only when the new max is far above it; a
-            // lane whose rows are still fully masked keeps m_ref = -inf.
-            const bool move = mx > m_ref + kLazy;
-            const float m_new = move ? mx : m_ref;
-            const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
-            const float mc = (m_new == kNegInf) ? 0.f : m_new;
-            // P = exp2(s*c - m_new), rounded to bf16 for the PV product; the
-            // row sum accumulates the same rounded values (v_dot2 with ones).
-            float psum = 0.f;
-#pragma unroll
-            for (int q = 0; q < 4; q++) {
-                if constexpr (decltype(do_pv)::value)
-                    pv_slice(sm[cb_ ^ 1], q);
-                const int sb = q >> 1, i0 = (q & 1) * 8;
-#pragma unroll
-                for (int i = i0; i < i0 + 8; i += 2) {
-                    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
-                    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
-                    pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
-                    psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
+                for (int i = 0; i < 16; i++) {
+                    const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+                    bool ok = key <= pos;
+                    if (MODE == kModeLocal)
+                        ok = ok && (key > pos - w);
+                    if (!ok)
+                        s[sb][i] = kNegInf;
                 }
-            }
-            l_run = fmaf(l_run, alpha, psum);
-            m_ref = m_new;
-            resc_pend = __builtin_amdgcn_ballot_w64(move) != 0;
-            alpha_pend = alpha;
-        } else if constexpr (decltype(do_pv)::value) {
-            pv(sm[cb_ ^ 1]);
         }
-        dma_wait_barrier();
+        float mx = kNegInf;
+#pragma unroll
+        for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+            for (int i = 0; i < 16; i++)
+                mx = fmaxf(mx, s[sb][i]);
+        mx = pair_max(mx) * c;               // tile max in the exp2 domain
+        // The reference moves only when the new max is far above it; a lane
+        // whose rows are still fully masked keeps m_ref = -inf.
+        const bool move = mx > m_ref + kLazy;
+        const float m_new = move ? mx : m_ref;
+        const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
+        const float mc = (m_new == kNegInf) ? 0.f : m_new;
+        // P = exp2(s*c - m_new), rounded to bf16 for the PV product; the row
+        // sum accumulates the same rounded values (v_dot2 with ones).
+        float psum = 0.f;
+        const int vprev = vidx(kb_ - 1);
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            if constexpr (decltype(do_pv)::value)
+                pv_slice(vprev, q);
+            const int sb = q >> 1, i0 = (q & 1) * 8;
+#pragma unroll
+            for (int i = i0; i < i0 + 8; i += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
+                pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
+                psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
+            }
+        }
+        l_run = fmaf(l_run, alpha, psum);
+        m_ref = m_new;
+        resc_pend = __builtin_amdgcn_ballot_w64(move) != 0;
+        alpha_pend = alpha;
     };
 
     using T_ = std::true_type;
     using F_ = std::false_type;
+    // One step: S(kb) + softmax(kb) [x PV(kb-1)], or PV(kb-1) alone.
+    auto step = [&](int kb_, auto do_s, auto do_pv, auto masked) {
+        stage(kb_);
+        if constexpr (decltype(do_pv)::value)
+            apply_rescale();
+        if constexpr (decltype(do_s)::value) {
+            op_s(kb_);
+            op_sm(kb_, do_pv, masked);
+        } else if constexpr (decltype(do_pv)::value) {
+            pv(vidx(kb_ - 1));
+        }
+        dma_wait_barrier();
+    };
     // Tiles needing the real-position mask: the diagonal tail (some key past
     // the wave's first row) and, for the local branch, the window's left edge.
     int kb_um_lo = kb_first, kb_um_hi = min(kb_last, (wpmin + 1) / kBlockN - 1);
@@ -526,15 +539,15 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
     auto unmasked = [&](int kb_) { return kb_ >= kb_um_lo && kb_ <= kb_um_hi; };
 
     // Every wave walks all tiles of the workgroup's range (they share the
-    // staging and the barriers) but computes only its own sub-range.
+    // staging and the barriers) but computes only its own sub-range
+    // kb_first..kb_last, in loops of a single kind each -- masked window
+    // edge, unmasked middle, masked diagonal -- so that no loop body switches
+    // between instantiations.
     int kb = kb_lo;
+    bool pending = false;
     for (; kb < kb_first && kb <= kb_hi; kb++)
         step(kb, F_{}, F_{}, F_{});
-    bool pending = false;
-    if (kb <= kb_last) {
-        // first computed tile (no PV yet), then three loops of a single kind
-        // each -- masked window edge, unmasked middle, masked diagonal -- so
-        // that no loop body switches between instantiations
+    if (kb_first <= kb_last) {
         if (unmasked(kb))
             step(kb, T_{}, F_{}, F_{});
         else
@@ -557,7 +570,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
         step(kb, F_{}, F_{}, F_{});
     if (pending) {
         apply_rescale();
-        pv(sm[(kb_hi - kb_lo) & 1]);        // V(kb_hi) was staged by the last step
+        pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step
     }
 
     float l_tot = pair_sum(l_run);
@@ -657,7 +670,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> *sm, int 
 template <int D, int MODE, int EPI>
 __global__ __launch_bounds__(waves_of(MODE) * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
-    __shared__ Smem<D> sm[2];
+    __shared__ Smem<D> sm;
     if (MODE == kModeGlobal) {
         // Persistent workgroups pull (tile, head group) items from the queue
         // of their XCD (workgroups are dispatched round-robin over the 8
