@@ -414,15 +414,24 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     // S(kb) = K(kb) Q^T into s.
     auto op_s = [&](int kb_) {
         const uint16_t(*kt)[D + kKPad] = sm.k[kidx(kb_)];
+        s[0] = f32x16{};
+        s[1] = f32x16{};
 #pragma unroll
-        for (int sb = 0; sb < 2; sb++) {
-            s[sb] = f32x16{};
+        for (int ss = 0; ss < D / 16; ss++)
 #pragma unroll
-            for (int ss = 0; ss < D / 16; ss++) {
+            for (int sb = 0; sb < 2; sb++) {
                 const bf16x8 kf = *(const bf16x8 *)&kt[sb * 32 + m][ss * 16 + g * 8];
                 s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
             }
+        // Schedule: four K-fragment reads ahead, then one MFMA per read, so
+        // LDS latency hides behind the MFMAs of the two S blocks.
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // DS reads
+#pragma unroll
+        for (int i = 0; i < D / 8 - 4; i++) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         }
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     };
     // PV of the tile whose P is in pw, V from buffer vi, for one 16-key slice
     // q (0..3) of the 64-key tile.
