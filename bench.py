@@ -89,6 +89,39 @@ def committed_traffic(workload: str):
         return None
 
 
+def gpu_info(torch, busy=None):
+    """Device name and the clock the peaks assume; the shader clock rocm-smi
+    reports while `busy` (a callable that enqueues about a second of layer
+    steps) keeps the GPU loaded, when the tool is available (best effort)."""
+    import subprocess
+    props = torch.cuda.get_device_properties(0)
+    info = {"name": props.name, "arch": getattr(props, "gcnArchName", None),
+            "compute_units": props.multi_processor_count, "peak_sclk_mhz_assumed": 2400}
+    if busy is not None:
+        busy()
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                           timeout=20)
+        for line in r.stdout.splitlines():
+            if "sclk" in line:
+                info["sclk_reported"] = line.split(":", 1)[-1].strip()
+                break
+    except Exception:                       # the tool is optional
+        pass
+    torch.cuda.synchronize()
+    return info
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(x, w, stride: int, log_fn=log):
     """Time the fp64 oracle on every stride-th token row (and every stride-th
     selected row) of the workload; return a cpu_baseline record."""
@@ -111,7 +144,7 @@ def cpu_baseline(x, w, stride: int, log_fn=log):
     dt = time.perf_counter() - t0
     log_fn(f"cpu oracle: {rows.size} rows ({int(is_sel.sum())} selected) in {dt:.2f}s")
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
             "sample": (f"{w.name}: every {stride}th unselected and every {stride}th selected "
                        f"token row ({rows.size} of {N} rows, all {w.num_q_heads} heads), "
                        f"selection over the full sequence; {dt:.1f}s fp64")}
@@ -128,6 +161,8 @@ def main(argv=None):
                     help="oracle sample stride (0 = pick one for ~10-30 s of CPU work)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU-oracle baseline")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense baseline")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the threshold-mode run and the clock query")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of MIB MiB "
                          "(the reference kernel for scaling FETCH_SIZE / WRITE_SIZE)")
@@ -252,6 +287,43 @@ def main(argv=None):
         dense["dense_tflops"] = fl * p_dense / (t_dense * 1e-3) / 1e12
         log("dense: " + " ".join(f"{k}={v:.3f}" for k, v in dense.items()))
 
+    # Threshold mode on the same inputs (the Markov "on" set itself, b_th = 0.5)
+    thr_mode = None
+    if not args.no_extra:
+        cap_t = N
+        sel_t = torch.empty(cap_t, dtype=torch.int32, device="cuda")
+        ws_t = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_FWD, cap_t),
+                           dtype=torch.uint8, device="cuda")
+
+        def step_t():
+            pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], threshold=0.5,
+                             out=out, sel_capacity=cap_t, sel_idx=sel_t, cu_sel=cu_sel,
+                             tok2sel=tok2sel, thr_out=thr, ws=ws_t)
+        for _ in range(2):
+            step_t()
+        torch.cuda.synchronize()
+        n_t = 10
+        start.record()
+        for _ in range(n_t):
+            step_t()
+        end.record()
+        torch.cuda.synchronize()
+        ms_t = start.elapsed_time(end) / n_t
+        sel_t_np = sel_t[: int(cu_sel[-1])].cpu().numpy()
+        pl_t, pg_t, _ = pair_counts(x["cu_seqlens"], w.window, sel_t_np)
+        thr_mode = {"threshold": 0.5, "n_sel": int(sel_t_np.size),
+                    "realized_ratio": round(sel_t_np.size / N, 5), "ms_per_step": round(ms_t, 4),
+                    "tflops": round(fl * (pl_t + pg_t) / (ms_t * 1e-3) / 1e12, 2),
+                    "speedup_vs_dense": round(dense["t_dense_ms"] / ms_t, 3) if dense else None}
+        log(f"threshold mode: {thr_mode}")
+        del sel_t, ws_t
+
+    # selection stage against its HBM roofline: gate read, tok2sel write, sel_idx write
+    sel_bytes = 4.0 * N + 4.0 * N + 4.0 * sel_np.size
+    select_hbm = {"bytes": sel_bytes, "ms": round(stage_ms["select"], 4),
+                  "GB_s": round(sel_bytes / (stage_ms["select"] * 1e-3) / 1e9, 1),
+                  "peak_GB_s": PEAK_HBM_GBS}
+
     roofline = {"bound": "mfma", "kernel": "attn_kernel<128, global> (query-sparse global branch)",
                 "achieved": round(global_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4),
@@ -295,6 +367,10 @@ def main(argv=None):
         "dense": {k: round(v, 4) for k, v in dense.items()} if dense else None,
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "select_hbm": select_hbm,
+        "threshold_mode": thr_mode,
+        "gpu": gpu_info(torch, busy=lambda: [step(0) for _ in range(600)])
+               if not args.no_extra else None,
     }
     print(json.dumps(rec), flush=True)
     return 0
