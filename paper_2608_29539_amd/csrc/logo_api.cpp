@@ -202,16 +202,46 @@ logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel
     return LOGO_OK;
 }
 
+// plan != NULL: the selection launch(es) also build the global tile plan.
 logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
                        float threshold, double ratio, int32_t *sel_idx, int32_t cap,
                        int32_t *cu_sel, int32_t *tok2sel, float *thr_out, char *ws,
-                       hipStream_t s) {
+                       hipStream_t s, const PlanArgs *plan = nullptr) {
     const SelectWs w = select_ws(p);
     float *thr = thr_out ? thr_out : (float *)(ws + w.thr);
     return hip_status(launch_select(p->cu_seqlens, p->num_seqs, p->total_tokens, gate,
                                     (int)mode, threshold, ratio, sel_idx, cap, cu_sel, tok2sel,
-                                    thr, (int32_t *)(ws + w.counts), s),
+                                    thr, (int32_t *)(ws + w.counts), plan, s),
                       s);
+}
+
+// Persistent grid of the global kernel and the arguments of its tile plan
+// (work table in the global workspace `ws`).
+logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int32_t *cu_sel,
+                        int32_t cap, char *ws, PlanArgs &pa, int &grid) {
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
+    const GlobalWs w = global_ws(p, cap);
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return LOGO_ERR_HIP;
+    grid = cus * attention_blocks_per_cu(kModeGlobal, p->head_dim);
+    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    pa.cu_sel = cu_sel;
+    pa.sel_idx = sel_idx;
+    pa.tpw = tp.tpw;
+    pa.cap = cap;
+    pa.max_seqlen = p->max_seqlen;
+    pa.n_hg = tp.n_hg;
+    pa.grid_wgs = grid;
+    pa.split_slots = w.slots;
+    pa.stride = w.stride;
+    pa.tmp = (SparseTile *)(ws + w.tiles_tmp);
+    pa.out = (SparseTile *)(ws + w.tiles);
+    pa.scratch = (int32_t *)(ws + w.scratch);
+    pa.queue = (int32_t *)(ws + w.queue);
+    pa.split_cnt = (int32_t *)(ws + w.split_cnt);
+    return LOGO_OK;
 }
 
 // Fused-epilogue inputs (logo_attn_fwd only).
@@ -257,29 +287,21 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                        const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
                        int32_t cap, float *o, const FusedEpi *f, const float *gain, char *ws,
-                       hipStream_t s, hipEvent_t after_plan = nullptr) {
+                       hipStream_t s, hipEvent_t after_plan = nullptr, bool plan_done = false) {
     if (p->total_tokens == 0 || cap == 0)
         return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
     const GlobalWs w = global_ws(p, cap);
-    SparseTile *tiles = (SparseTile *)(ws + w.tiles);
-    int32_t *queue = (int32_t *)(ws + w.queue);
-    int32_t *split_cnt = (int32_t *)(ws + w.split_cnt);
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return LOGO_ERR_HIP;
-    const int per_cu = attention_blocks_per_cu(kModeGlobal, p->head_dim);
-    int grid = cus * per_cu;
-    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
-    logo_status st = hip_status(
-        launch_sparse_plan(p->cu_seqlens, cu_sel, sel_idx, p->num_seqs, tp.tpw, cap,
-                           p->max_seqlen, tp.n_hg, grid, w.slots, w.stride,
-                           (SparseTile *)(ws + w.tiles_tmp), tiles, (int32_t *)(ws + w.scratch),
-                           queue, split_cnt, s),
-        s);
+    PlanArgs pa;
+    int grid = 0;
+    logo_status st = global_plan(p, sel_idx, cu_sel, cap, ws, pa, grid);
     if (st != LOGO_OK)
         return st;
+    if (!plan_done) {
+        st = hip_status(launch_sparse_plan(p->cu_seqlens, p->num_seqs, pa, s), s);
+        if (st != LOGO_OK)
+            return st;
+    }
     if (after_plan && hipEventRecord(after_plan, s) != hipSuccess)
         return LOGO_ERR_HIP;
     AttnArgs a = make_args(p, tp);
@@ -288,9 +310,9 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     a.v = v;
     a.out = o;
     a.sel_idx = sel_idx;
-    a.tiles = tiles;
-    a.queue = queue;
-    a.split_cnt = split_cnt;
+    a.tiles = pa.out;
+    a.queue = pa.queue;
+    a.split_cnt = pa.split_cnt;
     a.partial = (float *)(ws + w.partial);
     if (f)
         set_fused(a, f, gain);
@@ -345,7 +367,14 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
 
     if ((st = mark(0)) != LOGO_OK)
         return st;
-    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
+    // The selection launch also builds the global branch's tile plan.
+    PlanArgs plan;
+    int grid_g = 0;
+    const bool with_plan = p->total_tokens > 0 && cap > 0;
+    if (with_plan && (st = global_plan(p, sel, cus, cap, base + w.glob_ws, plan, grid_g)) != LOGO_OK)
+        return st;
+    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s,
+                    with_plan ? &plan : nullptr);
     if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
         return st;
     // Local branch with the fused epilogue: Norm^L(O^L) straight to `out`
@@ -355,7 +384,8 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     if (st != LOGO_OK || (st = mark(2)) != LOGO_OK)
         return st;
     st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, nullptr, &fe,
-                    gain_global, base + w.glob_ws, s, events ? (hipEvent_t)events[3] : nullptr);
+                    gain_global, base + w.glob_ws, s, events ? (hipEvent_t)events[3] : nullptr,
+                    /*plan_done=*/true);
     if (st != LOGO_OK)
         return st;
     return mark(4);

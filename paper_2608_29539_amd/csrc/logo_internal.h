@@ -122,22 +122,28 @@ hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, 
                             hipStream_t s);
 int attention_blocks_per_cu(int mode, int head_dim);
 
-// Tile plan of the global branch.  tiles_tmp and tiles each hold
-// max_tiles + split_slots entries; scratch holds 2 * stride ints with
+// Tile plan of the global branch (device-built work table).  tmp and out each
+// hold max_tiles + split_slots entries; scratch holds 2 * stride ints with
 // stride >= max(B, max_tiles) + 1; split_cnt holds split_slots * n_hg ints.
-hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
-                              const int32_t *sel_idx, int num_seqs, int tpw,
-                              int sel_capacity, int max_seqlen, int n_hg, int grid_wgs,
-                              int split_slots, int stride, SparseTile *tiles_tmp,
-                              SparseTile *tiles, int32_t *scratch, int32_t *queue,
-                              int32_t *split_cnt, hipStream_t s);
+struct PlanArgs {
+    const int32_t *cu_sel;     // [B+1] compacted sequence offsets
+    const int32_t *sel_idx;    // [cap] selected token indices
+    int32_t tpw, cap, max_seqlen, n_hg, grid_wgs, split_slots, stride;
+    SparseTile *tmp, *out;
+    int32_t *scratch, *queue, *split_cnt;
+};
+hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
+                              hipStream_t s);
 
 // Selection: thresholds, ranks and compaction.  seq_counts holds num_seqs
-// ints (per-sequence selected counts when num_seqs > 1).
+// ints (per-sequence selected counts when num_seqs > 1).  With a non-null
+// plan the global tile plan is built too (inside the selection launch for
+// one sequence, as a separate launch otherwise).
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s);
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts,
+                         const PlanArgs *plan, hipStream_t s);
 
 hipError_t launch_combine(int n_tokens, int hq, int head_dim, const float *o_local,
                           const float *o_global, const float *gate,

@@ -93,14 +93,202 @@ __device__ __forceinline__ int owner_seq(const int32_t *cu, int B, int t) {
     return lo;
 }
 
+// Exclusive prefix sum, in place, of n ints in global memory by one
+// 1024-thread workgroup (chunks of 1024 with a carry); returns the total.
+__device__ int block_exclusive_scan_array(int32_t *v, int n, int *s_wave, int *s_carry) {
+    const int tid = threadIdx.x;
+    if (tid == 0)
+        *s_carry = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < n; c0 += 1024) {
+        const int i = c0 + tid;
+        const int x = i < n ? v[i] : 0;
+        const int carry = *s_carry;
+        const int incl = block_inclusive_scan(x, s_wave);
+        if (i < n)
+            v[i] = carry + incl - x;
+        __syncthreads();
+        if (tid == 1023)
+            *s_carry = carry + incl;
+        __syncthreads();
+    }
+    const int total = *s_carry;
+    __syncthreads();
+    return total;
+}
+
+constexpr int kBuckets = 1024;
+
+__device__ __forceinline__ int entry_blocks(const SparseTile &t) { return t.kb_end - t.kb_begin + 1; }
+
+// Longest-first bucket sort of n entries of src into dst by their number of
+// KV blocks (in [1, max_blocks]); the order inside a bucket is arbitrary and
+// no result depends on it.
+__device__ void bucket_sort_desc(const SparseTile *src, SparseTile *dst, int n, int max_blocks,
+                                 int *hist, int *s_wave) {
+    const int tid = threadIdx.x;
+    const long long mw = max_blocks > 0 ? max_blocks : 1;
+    auto bucket = [&](const SparseTile &t) {
+        long long bk = ((mw - entry_blocks(t)) * kBuckets) / mw;
+        return (int)(bk < 0 ? 0 : (bk >= kBuckets ? kBuckets - 1 : bk));
+    };
+    hist[tid] = 0;
+    __syncthreads();
+    for (int u = tid; u < n; u += 1024)
+        atomicAdd(&hist[bucket(src[u])], 1);
+    __syncthreads();
+    const int hv = hist[tid];
+    const int incl = block_inclusive_scan(hv, s_wave);
+    hist[tid] = incl - hv;
+    __syncthreads();
+    for (int u = tid; u < n; u += 1024) {
+        const SparseTile t = src[u];
+        dst[atomicAdd(&hist[bucket(t)], 1)] = t;
+    }
+    __syncthreads();
+}
+
+// Work tables that fit are built in LDS and copied out once at the end (the
+// plan's phases are short, so global-memory round trips would dominate).
+constexpr int kPlanLdsEntries = 640;
+constexpr int kPlanLdsInts = 1280;
+
+// The tile plan, run by one workgroup of 1024 threads (see PlanArgs).
+__device__ void plan_body(const int32_t *cu, int B, const PlanArgs &p) {
+    const int32_t *cu_sel = p.cu_sel, *sel_idx = p.sel_idx;
+    const int tpw = p.tpw, cap = p.cap, max_seqlen = p.max_seqlen, n_hg = p.n_hg;
+    const int grid_wgs = p.grid_wgs, split_slots = p.split_slots, stride = p.stride;
+    __shared__ SparseTile l_tmp[kPlanLdsEntries], l_out[kPlanLdsEntries];
+    __shared__ int32_t l_scratch[kPlanLdsInts];
+    const bool in_lds = stride + split_slots <= kPlanLdsEntries && 2 * stride <= kPlanLdsInts;
+    SparseTile *tmp = in_lds ? l_tmp : p.tmp, *out = in_lds ? l_out : p.out;
+    int32_t *scratch = in_lds ? l_scratch : p.scratch;
+    int32_t *queue = p.queue, *split_cnt = p.split_cnt;
+    __shared__ int s_wave[16];
+    __shared__ int s_carry;
+    __shared__ int hist[kBuckets];
+    __shared__ unsigned long long s_total_blocks;
+    const int tid = threadIdx.x;
+    int32_t *sa = scratch, *sb = scratch + stride;
+
+    // 1. tiles per sequence -> exclusive prefix
+    for (int b = tid; b < B; b += 1024) {
+        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
+        sa[b] = (s1 - s0 + tpw - 1) / tpw;
+    }
+    __syncthreads();
+    const int n_tiles = block_exclusive_scan_array(sa, B, s_wave, &s_carry);
+    if (tid == 0) {
+        sa[B] = n_tiles;
+        s_total_blocks = 0;
+    }
+    __syncthreads();
+
+    // 2. the whole tiles (unsorted) into tmp, and their total KV blocks
+    unsigned long long my_blocks = 0;
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int b = owner_seq(sa, B, u);
+        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
+        const int first = s0 + (u - sa[b]) * tpw;
+        const int nrows = min(tpw, s1 - first);
+        const int pmax = sel_idx[first + nrows - 1] - cu[b];
+        SparseTile t;
+        t.first = first;
+        t.nrows = nrows;
+        t.seq = b;
+        t.pos_max = pmax;
+        t.kb_begin = 0;
+        t.kb_end = pmax / kBlockN;
+        t.split = 0;
+        t.nsplit = 1;
+        t.sid = -1;
+        t.pad[0] = t.pad[1] = t.pad[2] = 0;
+        tmp[u] = t;
+        my_blocks += (unsigned long long)(t.kb_end + 1);
+    }
+    atomicAdd(&s_total_blocks, my_blocks);
+    __syncthreads();
+    const int max_blocks = (max_seqlen + kBlockN - 1) / kBlockN;
+    // 3. longest first
+    bucket_sort_desc(tmp, out, n_tiles, max_blocks, hist, s_wave);
+
+    // 4. KV split: a tile longer than `target` blocks (a 1/kSplitDiv share of
+    //    the mean load of one persistent workgroup) becomes ns = ceil(blocks /
+    //    target) entries (at most kMaxSplit) over consecutive KV ranges, while
+    //    partial slots last (longest tiles first).
+    const unsigned long long work = s_total_blocks * (unsigned long long)n_hg;
+    const unsigned long long div = (unsigned long long)kSplitDiv * (unsigned long long)grid_wgs;
+    long long target = (long long)((work + div - 1) / div);
+    if (target < kMinSplitBlocks)
+        target = kMinSplitBlocks;
+    auto nsplit_of = [&](const SparseTile &t) {
+        const long long nb = entry_blocks(t);
+        if (nb <= target)
+            return 1;
+        const long long ns = (nb + target - 1) / target;
+        return (int)(ns < kMaxSplit ? ns : kMaxSplit);
+    };
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int ns = nsplit_of(out[u]);
+        sa[u] = ns > 1 ? ns : 0;
+    }
+    __syncthreads();
+    block_exclusive_scan_array(sa, n_tiles, s_wave, &s_carry);   // slot base
+    for (int u = tid; u < n_tiles; u += 1024) {
+        const int ns = nsplit_of(out[u]);
+        sb[u] = (ns > 1 && sa[u] + ns <= split_slots) ? ns : 1;
+    }
+    __syncthreads();
+    // sb[u] = entries of tile u; keep a copy of the counts in tmp's pad
+    for (int u = tid; u < n_tiles; u += 1024)
+        out[u].pad[0] = sb[u];
+    __syncthreads();
+    const int n_entries = block_exclusive_scan_array(sb, n_tiles, s_wave, &s_carry);
+    for (int u = tid; u < n_tiles; u += 1024) {
+        SparseTile t = out[u];
+        const int ns = t.pad[0];
+        t.pad[0] = 0;
+        const int nb = t.kb_end + 1;
+        const int e0 = sb[u];
+        for (int s = 0; s < ns; s++) {
+            SparseTile h = t;
+            h.kb_begin = (int)(((long long)s * nb) / ns);
+            h.kb_end = (int)(((long long)(s + 1) * nb) / ns) - 1;
+            h.split = s;
+            h.nsplit = ns;
+            h.sid = ns > 1 ? sa[u] : -1;
+            tmp[e0 + s] = h;
+        }
+    }
+    __syncthreads();
+    // 5. entries longest first
+    bucket_sort_desc(tmp, out, n_entries, max_blocks, hist, s_wave);
+    if (in_lds) {
+        for (int u = tid; u < n_entries; u += 1024)
+            p.out[u] = out[u];
+    }
+    for (int i = tid; i < split_slots * n_hg; i += 1024)
+        split_cnt[i] = 0;
+    if (tid == 0) {
+        queue[0] = n_entries;
+        for (int x = 0; x < kQueues; x++)
+            queue[1 + x] = 0;
+    }
+}
+
+__global__ __launch_bounds__(1024) void sparse_plan_kernel(const int32_t *cu, int B, PlanArgs p) {
+    plan_body(cu, B, p);
+}
+
 // kThreshold: find thr[b] (ratio mode) or take `fixed` (threshold mode), and
 // write thr[b]; otherwise read thr[b].  kWrite: compact (offset = sum of
 // cnt[b'] over b' < b, or 0 for a single sequence); otherwise write cnt[b].
-template <bool kThreshold, bool kWrite>
+// kPlan (one sequence only): then build the global tile plan.
+template <bool kThreshold, bool kWrite, bool kPlan>
 __global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
     const int32_t *__restrict__ cu, int B, const float *__restrict__ gate, int mode, float fixed,
     double ratio, float *__restrict__ thr, int32_t *__restrict__ cnt, int32_t *__restrict__ sel_idx,
-    int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel) {
+    int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel, PlanArgs plan) {
     __shared__ int hist[4096];
     __shared__ int s_wave[kSelWaves];
     __shared__ uint32_t s_bin;
@@ -280,175 +468,11 @@ __global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
         }
         if (b == B - 1 && tid == 0)
             cu_sel[B] = running;
-    }
-}
-
-// Exclusive prefix sum, in place, of n ints in global memory by one
-// 1024-thread workgroup (chunks of 1024 with a carry); returns the total.
-__device__ int block_exclusive_scan_array(int32_t *v, int n, int *s_wave, int *s_carry) {
-    const int tid = threadIdx.x;
-    if (tid == 0)
-        *s_carry = 0;
-    __syncthreads();
-    for (int c0 = 0; c0 < n; c0 += 1024) {
-        const int i = c0 + tid;
-        const int x = i < n ? v[i] : 0;
-        const int carry = *s_carry;
-        const int incl = block_inclusive_scan(x, s_wave);
-        if (i < n)
-            v[i] = carry + incl - x;
-        __syncthreads();
-        if (tid == 1023)
-            *s_carry = carry + incl;
-        __syncthreads();
-    }
-    const int total = *s_carry;
-    __syncthreads();
-    return total;
-}
-
-constexpr int kBuckets = 1024;
-
-__device__ __forceinline__ int entry_blocks(const SparseTile &t) { return t.kb_end - t.kb_begin + 1; }
-
-// Longest-first bucket sort of n entries of src into dst by their number of
-// KV blocks (in [1, max_blocks]); the order inside a bucket is arbitrary and
-// no result depends on it.
-__device__ void bucket_sort_desc(const SparseTile *src, SparseTile *dst, int n, int max_blocks,
-                                 int *hist, int *s_wave) {
-    const int tid = threadIdx.x;
-    const long long mw = max_blocks > 0 ? max_blocks : 1;
-    auto bucket = [&](const SparseTile &t) {
-        long long bk = ((mw - entry_blocks(t)) * kBuckets) / mw;
-        return (int)(bk < 0 ? 0 : (bk >= kBuckets ? kBuckets - 1 : bk));
-    };
-    hist[tid] = 0;
-    __syncthreads();
-    for (int u = tid; u < n; u += 1024)
-        atomicAdd(&hist[bucket(src[u])], 1);
-    __syncthreads();
-    const int hv = hist[tid];
-    const int incl = block_inclusive_scan(hv, s_wave);
-    hist[tid] = incl - hv;
-    __syncthreads();
-    for (int u = tid; u < n; u += 1024) {
-        const SparseTile t = src[u];
-        dst[atomicAdd(&hist[bucket(t)], 1)] = t;
-    }
-    __syncthreads();
-}
-
-// One workgroup of 1024 threads.  scratch holds 2 * (stride) ints with
-// stride >= max(B, max_tiles) + 1.
-__global__ __launch_bounds__(1024) void sparse_plan_kernel(
-    const int32_t *cu, const int32_t *cu_sel, const int32_t *sel_idx, int B, int tpw, int cap,
-    int max_seqlen, int n_hg, int grid_wgs, int split_slots, int stride, SparseTile *tmp,
-    SparseTile *out, int32_t *scratch, int32_t *queue, int32_t *split_cnt) {
-    __shared__ int s_wave[16];
-    __shared__ int s_carry;
-    __shared__ int hist[kBuckets];
-    __shared__ unsigned long long s_total_blocks;
-    const int tid = threadIdx.x;
-    int32_t *sa = scratch, *sb = scratch + stride;
-
-    // 1. tiles per sequence -> exclusive prefix
-    for (int b = tid; b < B; b += 1024) {
-        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
-        sa[b] = (s1 - s0 + tpw - 1) / tpw;
-    }
-    __syncthreads();
-    const int n_tiles = block_exclusive_scan_array(sa, B, s_wave, &s_carry);
-    if (tid == 0) {
-        sa[B] = n_tiles;
-        s_total_blocks = 0;
-    }
-    __syncthreads();
-
-    // 2. the whole tiles (unsorted) into tmp, and their total KV blocks
-    unsigned long long my_blocks = 0;
-    for (int u = tid; u < n_tiles; u += 1024) {
-        const int b = owner_seq(sa, B, u);
-        const int s0 = min(cu_sel[b], cap), s1 = min(cu_sel[b + 1], cap);
-        const int first = s0 + (u - sa[b]) * tpw;
-        const int nrows = min(tpw, s1 - first);
-        const int pmax = sel_idx[first + nrows - 1] - cu[b];
-        SparseTile t;
-        t.first = first;
-        t.nrows = nrows;
-        t.seq = b;
-        t.pos_max = pmax;
-        t.kb_begin = 0;
-        t.kb_end = pmax / kBlockN;
-        t.split = 0;
-        t.nsplit = 1;
-        t.sid = -1;
-        t.pad[0] = t.pad[1] = t.pad[2] = 0;
-        tmp[u] = t;
-        my_blocks += (unsigned long long)(t.kb_end + 1);
-    }
-    atomicAdd(&s_total_blocks, my_blocks);
-    __syncthreads();
-    const int max_blocks = (max_seqlen + kBlockN - 1) / kBlockN;
-    // 3. longest first
-    bucket_sort_desc(tmp, out, n_tiles, max_blocks, hist, s_wave);
-
-    // 4. KV split: a tile longer than `target` blocks (a 1/kSplitDiv share of
-    //    the mean load of one persistent workgroup) becomes ns = ceil(blocks /
-    //    target) entries (at most kMaxSplit) over consecutive KV ranges, while
-    //    partial slots last (longest tiles first).
-    const unsigned long long work = s_total_blocks * (unsigned long long)n_hg;
-    const unsigned long long div = (unsigned long long)kSplitDiv * (unsigned long long)grid_wgs;
-    long long target = (long long)((work + div - 1) / div);
-    if (target < kMinSplitBlocks)
-        target = kMinSplitBlocks;
-    auto nsplit_of = [&](const SparseTile &t) {
-        const long long nb = entry_blocks(t);
-        if (nb <= target)
-            return 1;
-        const long long ns = (nb + target - 1) / target;
-        return (int)(ns < kMaxSplit ? ns : kMaxSplit);
-    };
-    for (int u = tid; u < n_tiles; u += 1024) {
-        const int ns = nsplit_of(out[u]);
-        sa[u] = ns > 1 ? ns : 0;
-    }
-    __syncthreads();
-    block_exclusive_scan_array(sa, n_tiles, s_wave, &s_carry);   // slot base
-    for (int u = tid; u < n_tiles; u += 1024) {
-        const int ns = nsplit_of(out[u]);
-        sb[u] = (ns > 1 && sa[u] + ns <= split_slots) ? ns : 1;
-    }
-    __syncthreads();
-    // sb[u] = entries of tile u; keep a copy of the counts in tmp's pad
-    for (int u = tid; u < n_tiles; u += 1024)
-        out[u].pad[0] = sb[u];
-    __syncthreads();
-    const int n_entries = block_exclusive_scan_array(sb, n_tiles, s_wave, &s_carry);
-    for (int u = tid; u < n_tiles; u += 1024) {
-        SparseTile t = out[u];
-        const int ns = t.pad[0];
-        t.pad[0] = 0;
-        const int nb = t.kb_end + 1;
-        const int e0 = sb[u];
-        for (int s = 0; s < ns; s++) {
-            SparseTile h = t;
-            h.kb_begin = (int)(((long long)s * nb) / ns);
-            h.kb_end = (int)(((long long)(s + 1) * nb) / ns) - 1;
-            h.split = s;
-            h.nsplit = ns;
-            h.sid = ns > 1 ? sa[u] : -1;
-            tmp[e0 + s] = h;
+        if constexpr (kPlan) {
+            // one sequence: this workgroup wrote all of sel_idx and cu_sel
+            __syncthreads();
+            plan_body(cu, B, plan);
         }
-    }
-    __syncthreads();
-    // 5. entries longest first
-    bucket_sort_desc(tmp, out, n_entries, max_blocks, hist, s_wave);
-    for (int i = tid; i < split_slots * n_hg; i += 1024)
-        split_cnt[i] = 0;
-    if (tid == 0) {
-        queue[0] = n_entries;
-        for (int x = 0; x < kQueues; x++)
-            queue[1 + x] = 0;
     }
 }
 
@@ -457,35 +481,39 @@ __global__ __launch_bounds__(1024) void sparse_plan_kernel(
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s) {
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts,
+                         const PlanArgs *plan, hipStream_t s) {
     (void)n_tokens;
+    const PlanArgs none{};
     if (num_seqs == 1) {
-        hipLaunchKernelGGL((select_seq_kernel<true, true>), dim3(1), dim3(kSelThreads), 0, s,
-                           cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
-                           sel_capacity, cu_sel, tok2sel);
+        if (plan)
+            hipLaunchKernelGGL((select_seq_kernel<true, true, true>), dim3(1), dim3(kSelThreads), 0,
+                               s, cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts,
+                               sel_idx, sel_capacity, cu_sel, tok2sel, *plan);
+        else
+            hipLaunchKernelGGL((select_seq_kernel<true, true, false>), dim3(1), dim3(kSelThreads),
+                               0, s, cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts,
+                               sel_idx, sel_capacity, cu_sel, tok2sel, none);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((select_seq_kernel<true, false>), dim3(num_seqs), dim3(kSelThreads), 0, s,
-                       cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
-                       sel_capacity, cu_sel, tok2sel);
+    hipLaunchKernelGGL((select_seq_kernel<true, false, false>), dim3(num_seqs), dim3(kSelThreads),
+                       0, s, cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts,
+                       sel_idx, sel_capacity, cu_sel, tok2sel, none);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((select_seq_kernel<false, true>), dim3(num_seqs), dim3(kSelThreads), 0, s,
-                       cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
-                       sel_capacity, cu_sel, tok2sel);
-    return hipGetLastError();
+    hipLaunchKernelGGL((select_seq_kernel<false, true, false>), dim3(num_seqs), dim3(kSelThreads),
+                       0, s, cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts,
+                       sel_idx, sel_capacity, cu_sel, tok2sel, none);
+    e = hipGetLastError();
+    if (e != hipSuccess || !plan)
+        return e;
+    return launch_sparse_plan(cu_seqlens, num_seqs, *plan, s);
 }
 
-hipError_t launch_sparse_plan(const int32_t *cu_seqlens, const int32_t *cu_sel,
-                              const int32_t *sel_idx, int num_seqs, int tpw, int sel_capacity,
-                              int max_seqlen, int n_hg, int grid_wgs, int split_slots,
-                              int stride, SparseTile *tiles_tmp, SparseTile *tiles,
-                              int32_t *scratch, int32_t *queue, int32_t *split_cnt,
+hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
                               hipStream_t s) {
-    hipLaunchKernelGGL(sparse_plan_kernel, dim3(1), dim3(1024), 0, s, cu_seqlens, cu_sel, sel_idx,
-                       num_seqs, tpw, sel_capacity, max_seqlen, n_hg, grid_wgs, split_slots,
-                       stride, tiles_tmp, tiles, scratch, queue, split_cnt);
+    hipLaunchKernelGGL(sparse_plan_kernel, dim3(1), dim3(1024), 0, s, cu_seqlens, num_seqs, plan);
     return hipGetLastError();
 }
 
