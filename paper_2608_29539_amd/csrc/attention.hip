@@ -215,6 +215,9 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 // 2^kLazy in the exp2 domain, so probabilities stay <= 2^kLazy and most tiles
 // skip the rescale.  The result is the same softmax after the final O / l.
 constexpr float kLazy = 8.f;
+// 32-row MFMA column blocks per wave: each K / V^T fragment read from LDS
+// feeds one MFMA per row group.
+constexpr int RG = kRowsPerWave / 32;
 
 // Wave-uniform value, made explicit so the compiler keeps it in SGPRs.
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
@@ -227,26 +230,30 @@ __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlan
 // for the entries that are not last (nothing more to do).
 template <int D>
 __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile &t, int hg,
-                                            int wave, int lane, f32x16 (&acc)[D / 32], float m,
-                                            float &l) {
+                                            int wave, int lane, f32x16 (&acc)[RG][D / 32],
+                                            const float (&m)[RG], float (&l)[RG]) {
     __shared__ int s_last;
     constexpr int kLanes = kWavesGlobal * 64;
-    constexpr int kAccFloats = kLanes * (D / 2);
+    constexpr int kAccFloats = kLanes * RG * (D / 2);
     const int sid = uni(t.sid), split = uni(t.split), ns = uni(t.nsplit);
     const int li = wave * 64 + lane;
-    float *base = a.partial + (int64_t)sid * a.n_hg * partial_floats(D);
-    const int64_t slot_stride = (int64_t)a.n_hg * partial_floats(D);
-    float *mine = base + split * slot_stride + (int64_t)hg * partial_floats(D);
+    const int64_t pf = (int64_t)partial_floats(D);
+    float *base = a.partial + (int64_t)sid * a.n_hg * pf;
+    const int64_t slot_stride = (int64_t)a.n_hg * pf;
+    float *mine = base + split * slot_stride + (int64_t)hg * pf;
 #pragma unroll
-    for (int cb = 0; cb < D / 32; cb++)
+    for (int rg = 0; rg < RG; rg++) {
 #pragma unroll
-        for (int qd = 0; qd < 4; qd++) {
-            f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
-                       acc[cb][qd * 4 + 3]};
-            *(f32x4 *)(mine + ((cb * 4 + qd) * kLanes + li) * 4) = v;
-        }
-    mine[kAccFloats + li] = m;
-    mine[kAccFloats + kLanes + li] = l;
+        for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+            for (int qd = 0; qd < 4; qd++) {
+                const f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
+                                 acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
+                *(f32x4 *)(mine + (((rg * (D / 32) + cb) * 4 + qd) * kLanes + li) * 4) = v;
+            }
+        mine[kAccFloats + rg * kLanes + li] = m[rg];
+        mine[kAccFloats + (RG + rg) * kLanes + li] = l[rg];
+    }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
     if (threadIdx.x == 0)
@@ -256,30 +263,34 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
     if (!last)
         return false;
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    float M = kNegInf, L = 0.f;
 #pragma unroll
-    for (int cb = 0; cb < D / 32; cb++)
-        acc[cb] = f32x16{};
-    for (int j = 0; j < ns; j++) {
-        const float *pj = base + j * slot_stride + (int64_t)hg * partial_floats(D);
-        const float mj = pj[kAccFloats + li];
-        const float lj = pj[kAccFloats + kLanes + li];
-        const float mn = fmaxf(M, mj);
-        const float mc = (mn == kNegInf) ? 0.f : mn;
-        const float ra = __builtin_amdgcn_exp2f(M - mc), rb = __builtin_amdgcn_exp2f(mj - mc);
+    for (int rg = 0; rg < RG; rg++) {
+        float M = kNegInf, L = 0.f;
 #pragma unroll
         for (int cb = 0; cb < D / 32; cb++)
+            acc[rg][cb] = f32x16{};
+        for (int j = 0; j < ns; j++) {
+            const float *pj = base + j * slot_stride + (int64_t)hg * pf;
+            const float mj = pj[kAccFloats + rg * kLanes + li];
+            const float lj = pj[kAccFloats + (RG + rg) * kLanes + li];
+            const float mn = fmaxf(M, mj);
+            const float mc = (mn == kNegInf) ? 0.f : mn;
+            const float ra = __builtin_amdgcn_exp2f(M - mc), rb = __builtin_amdgcn_exp2f(mj - mc);
 #pragma unroll
-            for (int qd = 0; qd < 4; qd++) {
-                const f32x4 v = *(const f32x4 *)(pj + ((cb * 4 + qd) * kLanes + li) * 4);
+            for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
-                for (int e = 0; e < 4; e++)
-                    acc[cb][qd * 4 + e] = fmaf(acc[cb][qd * 4 + e], ra, v[e] * rb);
-            }
-        L = fmaf(L, ra, lj * rb);
-        M = mn;
+                for (int qd = 0; qd < 4; qd++) {
+                    const f32x4 v = *(const f32x4 *)(
+                        pj + (((rg * (D / 32) + cb) * 4 + qd) * kLanes + li) * 4);
+#pragma unroll
+                    for (int e = 0; e < 4; e++)
+                        acc[rg][cb][qd * 4 + e] = fmaf(acc[rg][cb][qd * 4 + e], ra, v[e] * rb);
+                }
+            L = fmaf(L, ra, lj * rb);
+            M = mn;
+        }
+        l[rg] = L;
     }
-    l = L;
     return true;
 }
 
@@ -309,40 +320,50 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         wg_pmin = p0;
         wg_pmax = p0 + nvalid - 1;
     }
-    // This lane's query row; rows past the tile end repeat the last row and
-    // are never stored.
-    const int ri = tb * kRowsPerWave + m;
-    const bool row_valid = ri < nvalid;
-    const int ric = row_valid ? ri : nvalid - 1;
-    int pos;
-    int64_t orow;
-    if (MODE == kModeGlobal) {
-        const int rank = tile.first + ric;
-        pos = a.sel_idx[rank] - (int)base;
-        orow = rank;
-    } else {
-        pos = wg_pmin + ric;
-        orow = base + pos;
+    // This lane's query rows (one per row group); rows past the tile end
+    // repeat the last row and are never stored.
+    int pos[RG];
+    int64_t orow[RG], qtok[RG];
+    bool row_valid[RG];
+#pragma unroll
+    for (int rg = 0; rg < RG; rg++) {
+        const int ri = tb * kRowsPerWave + rg * 32 + m;
+        row_valid[rg] = ri < nvalid;
+        const int ric = row_valid[rg] ? ri : nvalid - 1;
+        if (MODE == kModeGlobal) {
+            const int rank = tile.first + ric;
+            pos[rg] = a.sel_idx[rank] - (int)base;
+            orow[rg] = rank;
+        } else {
+            pos[rg] = wg_pmin + ric;
+            orow[rg] = base + pos[rg];
+        }
+        qtok[rg] = base + pos[rg];
     }
-    const int64_t qtok = base + pos;
     const bool wave_valid = tb * kRowsPerWave < nvalid;
-    const int wpmin = __builtin_amdgcn_readfirstlane(pos);
-    const int wpmax = __builtin_amdgcn_readlane(pos, 31);
+    const int wpmin = __builtin_amdgcn_readfirstlane(pos[0]);
+    const int wpmax = __builtin_amdgcn_readlane(pos[RG - 1], 31);
 
-    bf16x8 qf[D / 16];
-    {
-        const uint16_t *qp = a.q + (qtok * a.hq + head) * (int64_t)D + g * 8;
+    bf16x8 qf[RG][D / 16];
+#pragma unroll
+    for (int rg = 0; rg < RG; rg++) {
+        const uint16_t *qp = a.q + (qtok[rg] * a.hq + head) * (int64_t)D + g * 8;
 #pragma unroll
         for (int s = 0; s < D / 16; s++)
-            qf[s] = *(const bf16x8 *)(qp + s * 16);
+            qf[rg][s] = *(const bf16x8 *)(qp + s * 16);
     }
     // Inputs of the fused epilogue, fetched now so that their latency overlaps
     // the KV loop.
-    float ep_gate = 0.f;
-    int ep_rank = -1;
-    if (EPI == kEpiFused && MODE != kModeDense) {
-        ep_gate = a.gate[qtok];
-        ep_rank = (MODE == kModeGlobal) ? (int)orow : a.tok2sel[qtok];
+    float ep_gate[RG];
+    int ep_rank[RG];
+#pragma unroll
+    for (int rg = 0; rg < RG; rg++) {
+        ep_gate[rg] = 0.f;
+        ep_rank[rg] = -1;
+        if (EPI == kEpiFused && MODE != kModeDense) {
+            ep_gate[rg] = a.gate[qtok[rg]];
+            ep_rank[rg] = (MODE == kModeGlobal) ? (int)orow[rg] : a.tok2sel[qtok[rg]];
+        }
     }
 
     // Lane's row / column inside a V tile for the transpose reads.
@@ -380,11 +401,16 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     Dma<D, W> dma;
     dma_plan<D, W>(dma, wave, lane, row_bytes);
 
-    f32x16 acc[D / 32];
+    f32x16 acc[RG][D / 32];
+    float m_ref[RG], l_run[RG];
 #pragma unroll
-    for (int cb = 0; cb < D / 32; cb++)
-        acc[cb] = f32x16{};
-    float m_ref = kNegInf, l_run = 0.f;
+    for (int rg = 0; rg < RG; rg++) {
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++)
+            acc[rg][cb] = f32x16{};
+        m_ref[rg] = kNegInf;
+        l_run[rg] = 0.f;
+    }
 
     // Software-pipelined KV loop.  Step kb (between two barriers) stages
     // K(kb+1) and V(kb), computes S(kb) = K(kb) Q^T, then interleaves the
@@ -393,8 +419,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     // PV MFMAs of the previous one.  V is consumed one step after K; two
     // buffers each, and every buffer is rewritten only after the barrier that
     // ends its last read.
-    bf16x2 pw[2][8];                          // P of the last softmax-ed tile
-    f32x16 s[2];                              // S of the tile being softmax-ed
+    bf16x2 pw[RG][2][8];                      // P of the last softmax-ed tile
+    f32x16 s[RG][2];                          // S of the tile being softmax-ed
     auto kidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
     auto vidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
     __syncthreads();                         // the previous item's last tile is consumed
@@ -414,39 +440,48 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     // S(kb) = K(kb) Q^T into s.
     auto op_s = [&](int kb_) {
         const uint16_t(*kt)[D + kKPad] = sm.k[kidx(kb_)];
-        s[0] = f32x16{};
-        s[1] = f32x16{};
+#pragma unroll
+        for (int rg = 0; rg < RG; rg++)
+            s[rg][0] = s[rg][1] = f32x16{};
 #pragma unroll
         for (int ss = 0; ss < D / 16; ss++)
 #pragma unroll
             for (int sb = 0; sb < 2; sb++) {
                 const bf16x8 kf = *(const bf16x8 *)&kt[sb * 32 + m][ss * 16 + g * 8];
-                s[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ss], s[sb], 0, 0, 0);
+#pragma unroll
+                for (int rg = 0; rg < RG; rg++)
+                    s[rg][sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[rg][ss],
+                                                                        s[rg][sb], 0, 0, 0);
             }
-        // Schedule: four K-fragment reads ahead, then one MFMA per read, so
-        // LDS latency hides behind the MFMAs of the two S blocks.
+        // Schedule: four K-fragment reads ahead, then the MFMAs of one read
+        // per read, so LDS latency hides behind the MFMAs of the S blocks.
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // DS reads
 #pragma unroll
         for (int i = 0; i < D / 8 - 4; i++) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x008, RG, 0); // MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         }
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * RG, 0);
     };
     // PV of the tile whose P is in pw, V from buffer vi, for one 16-key slice
     // q (0..3) of the 64-key tile.
     auto pv_slice = [&](int vi, int q) {
         const int sb = q >> 1, ss = q & 1;
-        bf16x8 pf;
+        bf16x8 pf[RG];
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-            pf[2 * j] = pw[sb][ss * 4 + j][0];
-            pf[2 * j + 1] = pw[sb][ss * 4 + j][1];
-        }
+        for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+            for (int j = 0; j < 4; j++) {
+                pf[rg][2 * j] = pw[rg][sb][ss * 4 + j][0];
+                pf[rg][2 * j + 1] = pw[rg][sb][ss * 4 + j][1];
+            }
 #pragma unroll
         for (int cb = 0; cb < D / 32; cb++) {
             const bf16x8 vf = read_vt_frag(&sm.v[vi][sb * 32 + ss * 16 + vt_row][vt_scol[cb]], D);
-            acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[cb], 0, 0, 0);
+#pragma unroll
+            for (int rg = 0; rg < RG; rg++)
+                acc[rg][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[rg], acc[rg][cb], 0, 0,
+                                                                      0);
         }
     };
     auto pv = [&](int vi) {
@@ -458,12 +493,17 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     // PV accumulates into O (deferred so that no branch separates a tile's
     // exps from the PV MFMAs they are interleaved with).
     bool resc_pend = false;
-    float alpha_pend = 1.f;
+    float alpha_pend[RG];
+#pragma unroll
+    for (int rg = 0; rg < RG; rg++)
+        alpha_pend[rg] = 1.f;
     auto apply_rescale = [&]() {
         if (resc_pend) {
 #pragma unroll
-            for (int cb = 0; cb < D / 32; cb++)
-                acc[cb] *= alpha_pend;
+            for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+                    acc[rg][cb] *= alpha_pend[rg];
             resc_pend = false;
         }
     };
@@ -475,33 +515,42 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         if constexpr (decltype(masked)::value) {
             const int k0 = kb_ * kBlockN;
 #pragma unroll
+            for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                for (int sb = 0; sb < 2; sb++)
+#pragma unroll
+                    for (int i = 0; i < 16; i++) {
+                        const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+                        bool ok = key <= pos[rg];
+                        if (MODE == kModeLocal)
+                            ok = ok && (key > pos[rg] - w);
+                        if (!ok)
+                            s[rg][sb][i] = kNegInf;
+                    }
+        }
+        float alpha[RG], mc[RG], psum[RG];
+        bool any_move = false;
+#pragma unroll
+        for (int rg = 0; rg < RG; rg++) {
+            float mx = kNegInf;
+#pragma unroll
             for (int sb = 0; sb < 2; sb++)
 #pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
-                    bool ok = key <= pos;
-                    if (MODE == kModeLocal)
-                        ok = ok && (key > pos - w);
-                    if (!ok)
-                        s[sb][i] = kNegInf;
-                }
+                for (int i = 0; i < 16; i++)
+                    mx = fmaxf(mx, s[rg][sb][i]);
+            mx = pair_max(mx) * c;           // tile max in the exp2 domain
+            // The reference moves only when the new max is far above it; a
+            // lane whose rows are still fully masked keeps m_ref = -inf.
+            const bool move = mx > m_ref[rg] + kLazy;
+            const float m_new = move ? mx : m_ref[rg];
+            alpha[rg] = move ? __builtin_amdgcn_exp2f(m_ref[rg] - m_new) : 1.f;
+            mc[rg] = (m_new == kNegInf) ? 0.f : m_new;
+            m_ref[rg] = m_new;
+            any_move = any_move || move;
+            psum[rg] = 0.f;
         }
-        float mx = kNegInf;
-#pragma unroll
-        for (int sb = 0; sb < 2; sb++)
-#pragma unroll
-            for (int i = 0; i < 16; i++)
-                mx = fmaxf(mx, s[sb][i]);
-        mx = pair_max(mx) * c;               // tile max in the exp2 domain
-        // The reference moves only when the new max is far above it; a lane
-        // whose rows are still fully masked keeps m_ref = -inf.
-        const bool move = mx > m_ref + kLazy;
-        const float m_new = move ? mx : m_ref;
-        const float alpha = move ? __builtin_amdgcn_exp2f(m_ref - m_new) : 1.f;
-        const float mc = (m_new == kNegInf) ? 0.f : m_new;
-        // P = exp2(s*c - m_new), rounded to bf16 for the PV product; the row
-        // sum accumulates the same rounded values (v_dot2 with ones).
-        float psum = 0.f;
+        // P = exp2(s*c - m), rounded to bf16 for the PV product; the row sum
+        // accumulates the same rounded values (v_dot2 with ones).
         const int vprev = vidx(kb_ - 1);
 #pragma unroll
         for (int q = 0; q < 4; q++) {
@@ -509,17 +558,22 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
                 pv_slice(vprev, q);
             const int sb = q >> 1, i0 = (q & 1) * 8;
 #pragma unroll
-            for (int i = i0; i < i0 + 8; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(s[sb][i], c, -mc));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(s[sb][i + 1], c, -mc));
-                pw[sb][i >> 1] = cvt_bf16x2(p0, p1);
-                psum = __builtin_amdgcn_fdot2_f32_bf16(pw[sb][i >> 1], ones, psum, false);
-            }
+            for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                for (int i = i0; i < i0 + 8; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[rg][sb][i], c, -mc[rg]));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[rg][sb][i + 1], c, -mc[rg]));
+                    pw[rg][sb][i >> 1] = cvt_bf16x2(p0, p1);
+                    psum[rg] = __builtin_amdgcn_fdot2_f32_bf16(pw[rg][sb][i >> 1], ones, psum[rg],
+                                                               false);
+                }
         }
-        l_run = fmaf(l_run, alpha, psum);
-        m_ref = m_new;
-        resc_pend = __builtin_amdgcn_ballot_w64(move) != 0;
-        alpha_pend = alpha;
+#pragma unroll
+        for (int rg = 0; rg < RG; rg++) {
+            l_run[rg] = fmaf(l_run[rg], alpha[rg], psum[rg]);
+            alpha_pend[rg] = alpha[rg];
+        }
+        resc_pend = __builtin_amdgcn_ballot_w64(any_move) != 0;
     };
 
     using T_ = std::true_type;
@@ -582,39 +636,60 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step
     }
 
-    float l_tot = pair_sum(l_run);
+    float l_tot[RG];
+#pragma unroll
+    for (int rg = 0; rg < RG; rg++)
+        l_tot[rg] = pair_sum(l_run[rg]);
     if constexpr (MODE == kModeGlobal) {
         // a split entry: publish the partial, and the last of the tile's
         // entries to finish merges all of them and runs the epilogue
         if (uni(tile.nsplit) > 1 && !merge_split<D>(a, tile, hg, wave, lane, acc, m_ref, l_tot))
             return;
     }
-    const float inv = 1.f / l_tot;
-    if (EPI == kEpiFused && MODE != kModeDense) {
-        // ContextNorm over the row's d values: this lane holds d/2 of them,
-        // its partner l^32 the other half.
-        float ss = 0.f;
 #pragma unroll
-        for (int cb = 0; cb < D / 32; cb++)
+    for (int rg = 0; rg < RG; rg++) {
+        const float inv = 1.f / l_tot[rg];
+        if (EPI == kEpiFused && MODE != kModeDense) {
+            // ContextNorm over the row's d values: this lane holds d/2 of
+            // them, its partner l^32 the other half.
+            float ss = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; i++) {
-                const float o = acc[cb][i] * inv;
-                acc[cb][i] = o;
-                ss = fmaf(o, o, ss);
+            for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+                for (int i = 0; i < 16; i++) {
+                    const float o = acc[rg][cb][i] * inv;
+                    acc[rg][cb][i] = o;
+                    ss = fmaf(o, o, ss);
+                }
+            ss = pair_sum(ss);
+            if (!(wave_valid && row_valid[rg]))
+                continue;
+            const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
+            const int64_t tok = qtok[rg];
+            const float p = ep_gate[rg];
+            const int r = ep_rank[rg];
+            const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
+            uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
+            if (MODE == kModeLocal && r >= 0) {
+                // selected token: keep (1-p) Norm^L in fp32 for the global kernel
+                float *lp = a.lc + ((int64_t)r * a.hq + head) * D + g * 4;
+                const float wgt = (1.f - p) * rn;
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+                    for (int qd = 0; qd < 4; qd++) {
+                        f32x4 gn = {1.f, 1.f, 1.f, 1.f};
+                        if (gp)
+                            gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
+                        f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
+                                   acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
+                        *(f32x4 *)(lp + cb * 32 + qd * 8) = v * gn * wgt;
+                    }
+                continue;
             }
-        ss = pair_sum(ss);
-        if (!(wave_valid && row_valid))
-            return;
-        const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
-        const int64_t tok = qtok;
-        const float p = ep_gate;
-        const int r = ep_rank;
-        const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
-        uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
-        if (MODE == kModeLocal && r >= 0) {
-            // selected token: keep (1-p) Norm^L in fp32 for the global kernel
-            float *lp = a.lc + ((int64_t)r * a.hq + head) * D + g * 4;
-            const float wgt = (1.f - p) * rn;
+            const float *lp = (MODE == kModeGlobal)
+                                  ? a.lc + ((int64_t)r * a.hq + head) * D + g * 4 : nullptr;
+            const float wgt = (MODE == kModeGlobal) ? p * rn : rn;
 #pragma unroll
             for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
@@ -622,57 +697,42 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
                     f32x4 gn = {1.f, 1.f, 1.f, 1.f};
                     if (gp)
                         gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
-                    f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
-                               acc[cb][qd * 4 + 3]};
-                    *(f32x4 *)(lp + cb * 32 + qd * 8) = v * gn * wgt;
+                    f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
+                               acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
+                    v = v * gn * wgt;
+                    if (MODE == kModeGlobal)
+                        v += *(const f32x4 *)(lp + cb * 32 + qd * 8);
+                    u32x2 o;
+                    o.x = pack_bf16x2(v.x, v.y);
+                    o.y = pack_bf16x2(v.z, v.w);
+                    *(u32x2 *)(op + cb * 32 + qd * 8) = o;
                 }
-            return;
+            continue;
         }
-        const float *lp = (MODE == kModeGlobal)
-                              ? a.lc + ((int64_t)r * a.hq + head) * D + g * 4 : nullptr;
-        const float wgt = (MODE == kModeGlobal) ? p * rn : rn;
+        if (!(wave_valid && row_valid[rg]))
+            continue;
+        if (MODE == kModeDense) {
+            uint16_t *op = (uint16_t *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
-        for (int cb = 0; cb < D / 32; cb++)
+            for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
-            for (int qd = 0; qd < 4; qd++) {
-                f32x4 gn = {1.f, 1.f, 1.f, 1.f};
-                if (gp)
-                    gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
-                f32x4 v = {acc[cb][qd * 4 + 0], acc[cb][qd * 4 + 1], acc[cb][qd * 4 + 2],
-                           acc[cb][qd * 4 + 3]};
-                v = v * gn * wgt;
-                if (MODE == kModeGlobal)
-                    v += *(const f32x4 *)(lp + cb * 32 + qd * 8);
-                u32x2 o;
-                o.x = pack_bf16x2(v.x, v.y);
-                o.y = pack_bf16x2(v.z, v.w);
-                *(u32x2 *)(op + cb * 32 + qd * 8) = o;
-            }
-        return;
-    }
-    if (!(wave_valid && row_valid))
-        return;
-    if (MODE == kModeDense) {
-        uint16_t *op = (uint16_t *)a.out + (orow * a.hq + head) * (int64_t)D + g * 4;
+                for (int qd = 0; qd < 4; qd++) {
+                    u32x2 v;
+                    v.x = pack_bf16x2(acc[rg][cb][qd * 4 + 0] * inv, acc[rg][cb][qd * 4 + 1] * inv);
+                    v.y = pack_bf16x2(acc[rg][cb][qd * 4 + 2] * inv, acc[rg][cb][qd * 4 + 3] * inv);
+                    *(u32x2 *)(op + cb * 32 + qd * 8) = v;
+                }
+        } else {
+            float *op = (float *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
-        for (int cb = 0; cb < D / 32; cb++)
+            for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
-            for (int qd = 0; qd < 4; qd++) {
-                u32x2 v;
-                v.x = pack_bf16x2(acc[cb][qd * 4 + 0] * inv, acc[cb][qd * 4 + 1] * inv);
-                v.y = pack_bf16x2(acc[cb][qd * 4 + 2] * inv, acc[cb][qd * 4 + 3] * inv);
-                *(u32x2 *)(op + cb * 32 + qd * 8) = v;
-            }
-    } else {
-        float *op = (float *)a.out + (orow * a.hq + head) * (int64_t)D + g * 4;
-#pragma unroll
-        for (int cb = 0; cb < D / 32; cb++)
-#pragma unroll
-            for (int qd = 0; qd < 4; qd++) {
-                f32x4 v = {acc[cb][qd * 4 + 0] * inv, acc[cb][qd * 4 + 1] * inv,
-                           acc[cb][qd * 4 + 2] * inv, acc[cb][qd * 4 + 3] * inv};
-                *(f32x4 *)(op + cb * 32 + qd * 8) = v;
-            }
+                for (int qd = 0; qd < 4; qd++) {
+                    f32x4 v = {acc[rg][cb][qd * 4 + 0] * inv, acc[rg][cb][qd * 4 + 1] * inv,
+                               acc[rg][cb][qd * 4 + 2] * inv, acc[rg][cb][qd * 4 + 3] * inv};
+                    *(f32x4 *)(op + cb * 32 + qd * 8) = v;
+                }
+        }
     }
 }
 

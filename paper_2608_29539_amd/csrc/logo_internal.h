@@ -70,7 +70,7 @@ constexpr int kSplitGridRef = 512;    // persistent workgroups the split slots a
 // lanes of the global mode's waves each hold d/2 fp32 outputs, then m (exp2
 // domain) and l of every lane.
 __host__ __device__ constexpr size_t partial_floats(int head_dim) {
-    return (size_t)kWavesGlobal * 64 * (head_dim / 2 + 2);
+    return (size_t)kWavesGlobal * 64 * (kRowsPerWave / 32) * (head_dim / 2 + 2);
 }
 // Partial slots (per head group) for a problem with max_tiles tiles: split
 // tiles have more than W / (kSplitDiv grid n_hg) blocks for a total of W
