@@ -9,6 +9,7 @@ from .oracle import (  # noqa: F401
     SEL_RATIO,
     SEL_THRESHOLD,
     attn_rows,
+    budget_update,
     build,
     contextnorm,
     fuse,
@@ -16,6 +17,8 @@ from .oracle import (  # noqa: F401
     logo_fwd,
     logo_rows,
     num_threads,
+    pmask_initial_threshold,
+    realized_ratio,
     select,
     set_num_threads,
     thresholds,

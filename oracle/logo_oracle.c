@@ -23,6 +23,11 @@
  *   - ContextNorm: head-wise RMSNorm of each branch       (Sec. 3.2, Eq. contextnorm)
  *   - output fusion (1-p) oL + p oG for selected tokens,
  *     oL otherwise                                        (Sec. 3.2, Eq. output-fusion)
+ *   - realized ratio F = (selected tokens) / (valid tokens)
+ *                                                         (Sec. 3.1, Eq. realized-ratio)
+ *   - budget controller b_th <- b_th + gamma sign(F - rho) and the P-mask
+ *     starting threshold                                  (Sec. 3.2, Eq. threshold-update
+ *                                                          and the P-mask paragraph)
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *   - positions are 0-based: key j is visible to query i iff j <= i (global)
@@ -99,6 +104,49 @@ static int cmp_float_ascending(const void *a, const void *b)
 {
     float x = *(const float *)a, y = *(const float *)b;
     return (x < y) ? -1 : (x > y) ? 1 : 0;
+}
+
+/*
+ * Realized global ratio of one routing pass (Sec. 3.1, Eq. realized-ratio):
+ * the fraction of the n_valid token positions whose z is 1, in double.
+ */
+double oracle_realized_ratio(int64_t n_selected, int64_t n_valid)
+{
+    return n_valid > 0 ? (double)n_selected / (double)n_valid : 0.0;
+}
+
+/*
+ * One budget-controller step (Sec. 3.2, Eq. threshold-update):
+ *   b_th <- b_th + gamma * sign(F - rho)
+ * with sign(0) = 0: the threshold rises when more tokens than the target
+ * went global (fewer pass next time) and falls when fewer did.  F is the
+ * realized ratio above and is compared with rho in double; the update itself
+ * is one fp32 multiply-free add of +-gamma (or nothing).  No valid tokens:
+ * no update.
+ */
+float oracle_budget_update(float b_th, int64_t n_selected, int64_t n_valid, double rho,
+                           float gamma)
+{
+    if (n_valid <= 0)
+        return b_th;
+    double f = oracle_realized_ratio(n_selected, n_valid);
+    if (f > rho)
+        return b_th + gamma;
+    if (f < rho)
+        return b_th - gamma;
+    return b_th;
+}
+
+/*
+ * P-mask starting threshold (Sec. 3.2, progressive masking): chosen so that
+ * pmask_steps controller steps of +gamma (every token is selected while the
+ * threshold is below every gate, so F = 1 > rho) bring b_th to the initial
+ * gate centre 0.5: b_th,0 = 0.5 - gamma * pmask_steps, evaluated in double
+ * and rounded once to fp32.
+ */
+float oracle_pmask_initial_threshold(float gamma, int64_t pmask_steps)
+{
+    return (float)(0.5 - (double)gamma * (double)pmask_steps);
 }
 
 /*

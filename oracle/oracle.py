@@ -61,6 +61,12 @@ def _load():
     lib.oracle_logo_fwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64,
                                     i32, f32, f64, P, P, f64, i32, P, P, P, P, P, P, P]
     lib.oracle_logo_fwd.restype = i64
+    lib.oracle_realized_ratio.argtypes = [i64, i64]
+    lib.oracle_realized_ratio.restype = f64
+    lib.oracle_budget_update.argtypes = [f32, i64, i64, f64, f32]
+    lib.oracle_budget_update.restype = f32
+    lib.oracle_pmask_initial_threshold.argtypes = [f32, i64]
+    lib.oracle_pmask_initial_threshold.restype = f32
     _lib = lib
     return lib
 
@@ -131,6 +137,22 @@ def fuse(ol, og, gate, tok2sel):
     out = np.empty_like(ol)
     _load().oracle_fuse(_ptr(ol), _ptr(og), _ptr(gate), _ptr(tok2sel), N, Hq, d, _ptr(out))
     return out
+
+
+def realized_ratio(n_selected: int, n_valid: int) -> float:
+    """F of Eq. realized-ratio (Sec. 3.1)."""
+    return float(_load().oracle_realized_ratio(int(n_selected), int(n_valid)))
+
+
+def budget_update(b_th: float, n_selected: int, n_valid: int, rho: float, gamma: float) -> float:
+    """One step of Eq. threshold-update (Sec. 3.2); fp32 result."""
+    return float(_load().oracle_budget_update(float(b_th), int(n_selected), int(n_valid),
+                                              float(rho), float(gamma)))
+
+
+def pmask_initial_threshold(gamma: float, pmask_steps: int) -> float:
+    """Starting threshold of the P-mask schedule (Sec. 3.2); fp32 result."""
+    return float(_load().oracle_pmask_initial_threshold(float(gamma), int(pmask_steps)))
 
 
 def logo_fwd(q, k, v, gate, cu_seqlens, window: int, *, ratio: Optional[float] = None,

@@ -40,6 +40,13 @@ MUTATIONS = {
         "int64_t lo = (window >= 1) ? (pos - window + 1 > 0 ? pos - window + 1 : 0) : -base;"),
     "tok2sel_rank_off_by_one": ("tok2sel[t] = (int32_t)n;", "tok2sel[t] = (int32_t)n + 1;"),
     "cu_sel_not_prefix": ("cu_sel[b] = (int32_t)n;", "cu_sel[b] = 0;"),
+    "controller_sign_flipped": ("        return b_th + gamma;\n    if (f < rho)\n        return b_th - gamma;",
+                                "        return b_th - gamma;\n    if (f < rho)\n        return b_th + gamma;"),
+    "controller_moves_on_equality": ("    if (f > rho)\n        return b_th + gamma;",
+                                     "    if (f >= rho)\n        return b_th + gamma;"),
+    "realized_ratio_inverted": ("(double)n_selected / (double)n_valid", "(double)n_valid / (double)n_selected"),
+    "pmask_start_sign": ("(float)(0.5 - (double)gamma * (double)pmask_steps)",
+                         "(float)(0.5 + (double)gamma * (double)pmask_steps)"),
 }
 
 

@@ -366,3 +366,64 @@ def test_logo_rows_matches_whole_layer(oracle_lib):
     rows = np.array([0, 5, 17, 199, 200, 201, 256, 120], np.int32)
     sub = oracle_lib.logo_rows(x, 9, rows, ratio=0.3)
     np.testing.assert_allclose(sub["out"], full["out"][rows], rtol=0, atol=1e-15)
+
+
+# ---------------------------------------------------------------------------
+# budget controller (Sec. 3.2, Eq. threshold-update; Sec. 3.1, Eq.
+# realized-ratio; P-mask paragraph).  Dyadic values keep every fp32 step exact.
+# ---------------------------------------------------------------------------
+def test_realized_ratio_hand(oracle_lib):
+    assert oracle_lib.realized_ratio(3, 8) == 0.375
+    assert oracle_lib.realized_ratio(0, 5) == 0.0
+    assert oracle_lib.realized_ratio(7, 7) == 1.0
+
+
+def test_budget_update_sign_cases(oracle_lib):
+    # F = 3/8 > rho = 1/4: too many global tokens, the threshold rises
+    assert oracle_lib.budget_update(0.25, 3, 8, 0.25, 0.125) == 0.375
+    # F = 1/8 < rho: it falls
+    assert oracle_lib.budget_update(0.25, 1, 8, 0.25, 0.125) == 0.125
+    # F == rho exactly: sign(0) = 0, no change
+    assert oracle_lib.budget_update(0.25, 2, 8, 0.25, 0.125) == 0.25
+    # no valid token: no change
+    assert oracle_lib.budget_update(0.25, 0, 0, 0.25, 0.125) == 0.25
+
+
+def test_pmask_reaches_gate_centre(oracle_lib):
+    # gamma = 2^-10, 1024 P-mask steps: b0 = 0.5 - 1 = -0.5; while b_th < every
+    # gate in (0,1) all tokens are selected (F = 1 > rho), each step adds gamma,
+    # and after exactly 1024 steps the threshold sits at 0.5
+    gamma, S = 2.0 ** -10, 1024
+    b = oracle_lib.pmask_initial_threshold(gamma, S)
+    assert b == -0.5
+    rng = np.random.default_rng(5)
+    gate = rng.uniform(0.0, 1.0, 4096).astype(np.float32)
+    cu = np.array([0, gate.size], np.int32)
+    for step in range(S):
+        thr = oracle_lib.thresholds(gate, cu, oracle_lib.SEL_THRESHOLD, threshold=b)
+        _, cu_sel, _ = oracle_lib.select(gate, cu, thr)
+        if b < 0:
+            assert int(cu_sel[-1]) == gate.size        # P-mask: everything global
+        b = oracle_lib.budget_update(b, int(cu_sel[-1]), gate.size, 0.25, gamma)
+        if b > 0.0:
+            break
+    # the first 512 steps (b from -0.5 up to 0) select everything
+    assert step >= 511
+
+
+def test_controller_settles_at_target_quantile(oracle_lib):
+    # gates on the grid (i + 0.5)/N: the fraction above t is 1 - t, so with
+    # rho = 1/4 the controller must settle within gamma of t = 0.75 and then
+    # keep F within the mass of one gamma-band of rho
+    N, rho, gamma = 4096, 0.25, 2.0 ** -6
+    gate = ((np.arange(N) + 0.5) / N).astype(np.float32)
+    cu = np.array([0, N], np.int32)
+    b = 0.0
+    for _ in range(200):
+        thr = oracle_lib.thresholds(gate, cu, oracle_lib.SEL_THRESHOLD, threshold=b)
+        _, cu_sel, _ = oracle_lib.select(gate, cu, thr)
+        b = oracle_lib.budget_update(b, int(cu_sel[-1]), N, rho, gamma)
+    assert abs(b - 0.75) <= gamma
+    thr = oracle_lib.thresholds(gate, cu, oracle_lib.SEL_THRESHOLD, threshold=b)
+    _, cu_sel, _ = oracle_lib.select(gate, cu, thr)
+    assert abs(int(cu_sel[-1]) / N - rho) <= gamma
