@@ -57,7 +57,8 @@ typedef enum {
 
 typedef enum {
     LOGO_SEL_THRESHOLD = 0,   /* one scalar threshold b_th for every sequence      */
-    LOGO_SEL_RATIO = 1        /* per-sequence threshold from a target ratio rho    */
+    LOGO_SEL_RATIO = 1,       /* per-sequence threshold from a target ratio rho    */
+    LOGO_SEL_THRESHOLD_DEVICE = 2  /* b_th read on the device from thr_out[0]      */
 } logo_sel_mode;
 
 /* Which entry point logo_workspace_bytes() sizes. */
@@ -100,6 +101,12 @@ typedef struct {
  *              thr_b = -inf if k_b == T_b, else the (k_b+1)-th largest gate
  *              of sequence b (an input value, -0 reported as +0).  Gates
  *              must be finite in this mode.  0 <= ratio <= 1.
+ *              LOGO_SEL_THRESHOLD_DEVICE: thr_b = b_th for every b, where
+ *              b_th is read on the device from thr_out[0] when the
+ *              selection runs (the threshold the budget controller keeps on
+ *              the device, see logo_budget_update); thr_out must not be
+ *              NULL and every thr_out[b] is set to b_th.  A NaN b_th
+ *              selects nothing.
  *   Selection: z_t = gate[t] > thr_b, strict, compared in fp32.
  *   sel_idx    device [sel_capacity] int32: packed token indices of the
  *              selected tokens, strictly ascending (sequence-major).
@@ -110,7 +117,7 @@ typedef struct {
  *   thr_out    device [B] fp32 or NULL: the thresholds used.
  *   Capacity:  in ratio mode sel_capacity must be >= sum_b floor(ratio*T_b)
  *              (checked when cu_seqlens_host is given, else it must be >= N).
- *              In threshold mode any sel_capacity >= 0 is accepted; if more
+ *              In the threshold modes any sel_capacity >= 0 is accepted; if more
  *              tokens pass, sel_idx keeps the first sel_capacity of them,
  *              tok2sel marks the rest -1, and cu_sel still counts all of
  *              them, so cu_sel[B] > sel_capacity reports the overflow.
@@ -225,6 +232,35 @@ logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
                                    logo_stream stream);
+
+/*
+ * logo_budget_update -- one step of the global-budget controller
+ * (Sec. 3.2, Eq. threshold-update) on the device, without a host sync:
+ *   F    = cu_sel[B] / N, the realized global ratio of the last selection
+ *          (Sec. 3.1, Eq. realized-ratio; N = total_tokens, the valid tokens)
+ *   b_th <- b_th + gamma * sign(F - rho), sign(0) = 0
+ * F and rho are compared in double; the update is one fp32 add of +-gamma.
+ * With N == 0 nothing changes.
+ *   cu_sel    device [B+1] int32, as written by logo_select / logo_attn_fwd
+ *   rho       target ratio, 0 <= rho <= 1
+ *   gamma     update rate, finite and >= 0
+ *   b_th      device fp32 scalar, updated in place (the value a
+ *             LOGO_SEL_THRESHOLD_DEVICE selection reads from thr_out[0])
+ *   realized  device fp32 scalar or NULL: receives F rounded to fp32
+ * Errors: LOGO_ERR_NULL (problem, cu_sel or b_th NULL), LOGO_ERR_ARG (rho or
+ * gamma out of range), LOGO_ERR_HIP.  One single-thread launch.
+ */
+logo_status logo_budget_update(const logo_problem *p, const int32_t *cu_sel, double rho,
+                               float gamma, float *b_th, float *realized, logo_stream stream);
+
+/*
+ * Starting threshold of the progressive-masking (P-mask) schedule (Sec. 3.2):
+ * b_th,0 = 0.5 - gamma * pmask_steps (double, rounded once to fp32), so that
+ * pmask_steps controller steps of +gamma -- every token is selected while
+ * b_th is below every gate p in (0,1), so F = 1 > rho -- bring b_th to the
+ * initial gate centre 0.5.  Host function, no device work.
+ */
+float logo_pmask_initial_threshold(float gamma, int64_t pmask_steps);
 
 /*
  * Workspace size in bytes for `entry` (a logo_entry value); sel_capacity is

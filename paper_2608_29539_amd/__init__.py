@@ -16,16 +16,19 @@ from .binding import (  # noqa: F401
     LOGO_ENTRY_SELECT,
     LOGO_SEL_RATIO,
     LOGO_SEL_THRESHOLD,
+    LOGO_SEL_THRESHOLD_DEVICE,
     LogoError,
     Problem,
     exported_symbols,
     library,
     library_path,
     logo_attn_fwd,
+    logo_budget_update,
     logo_combine,
     logo_dense_causal_attn,
     logo_global_attn_sparse_q,
     logo_local_attn,
+    logo_pmask_initial_threshold,
     logo_ratio_capacity,
     logo_select,
     logo_status_str,

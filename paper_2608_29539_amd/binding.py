@@ -17,6 +17,7 @@ _LIB_PATH = os.path.join(HERE, "liblogo.so")
 
 LOGO_SEL_THRESHOLD = 0
 LOGO_SEL_RATIO = 1
+LOGO_SEL_THRESHOLD_DEVICE = 2
 LOGO_ENTRY_SELECT = 0
 LOGO_ENTRY_LOCAL = 1
 LOGO_ENTRY_GLOBAL = 2
@@ -28,7 +29,8 @@ LOGO_ENTRY_DENSE = 5
 EXPORTS = (
     "logo_select", "logo_local_attn", "logo_global_attn_sparse_q", "logo_combine",
     "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
-    "logo_ratio_capacity", "logo_status_str", "logo_version",
+    "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
+    "logo_pmask_initial_threshold",
 )
 
 _lib = None
@@ -82,6 +84,7 @@ def library():
         "logo_attn_fwd_profiled": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32,
                                    P, P, P, P, sz, P, P],
         "logo_dense_causal_attn": [PP, P, P, P, P, P],
+        "logo_budget_update": [PP, P, f64, f32, P, P, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -94,6 +97,8 @@ def library():
     lib.logo_status_str.argtypes = [ctypes.c_int]
     lib.logo_status_str.restype = ctypes.c_char_p
     lib.logo_version.restype = ctypes.c_char_p
+    lib.logo_pmask_initial_threshold.argtypes = [f32, i64]
+    lib.logo_pmask_initial_threshold.restype = f32
     _lib = lib
     return lib
 
@@ -202,17 +207,33 @@ def logo_ratio_capacity(prob: Problem, ratio: float) -> int:
     return int(library().logo_ratio_capacity(prob.c, ratio))
 
 
+def _sel_mode(ratio, threshold, threshold_device, B):
+    """(mode, thr_out override) for exactly one of ratio / threshold /
+    threshold_device (a device fp32 tensor of >= B elements holding b_th in
+    element 0; it also receives the thresholds used)."""
+    import torch
+    if sum(x is not None for x in (ratio, threshold, threshold_device)) != 1:
+        raise ValueError("give exactly one of ratio / threshold / threshold_device")
+    if threshold_device is not None:
+        if (threshold_device.dtype != torch.float32 or not threshold_device.is_cuda
+                or threshold_device.numel() < B or not threshold_device.is_contiguous()):
+            raise ValueError("threshold_device: contiguous device float32 tensor of >= B values")
+        return LOGO_SEL_THRESHOLD_DEVICE, threshold_device
+    return (LOGO_SEL_RATIO if ratio is not None else LOGO_SEL_THRESHOLD), None
+
+
 def logo_select(prob: Problem, gate, *, ratio: Optional[float] = None,
-                threshold: Optional[float] = None, sel_capacity: Optional[int] = None,
-                sel_idx=None, cu_sel=None, tok2sel=None, thr_out=None, ws=None):
+                threshold: Optional[float] = None, threshold_device=None,
+                sel_capacity: Optional[int] = None, sel_idx=None, cu_sel=None, tok2sel=None,
+                thr_out=None, ws=None):
     """Hard routing + compaction.  Returns (sel_idx, cu_sel, tok2sel, thr_out)."""
     import torch
-    if (ratio is None) == (threshold is None):
-        raise ValueError("give exactly one of ratio / threshold")
     N, B = prob.total_tokens, prob.num_seqs
+    mode, thr_dev = _sel_mode(ratio, threshold, threshold_device, B)
+    if thr_dev is not None:
+        thr_out = thr_dev
     dev = prob.cu_seqlens.device
     _check(gate, torch.float32, (N,), "gate")
-    mode = LOGO_SEL_RATIO if ratio is not None else LOGO_SEL_THRESHOLD
     if sel_capacity is None:
         sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
     if sel_idx is None:
@@ -291,7 +312,8 @@ def logo_combine(prob: Problem, o_local, o_global, gate, tok2sel, *, gain_local=
 
 
 def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None,
-                  threshold: Optional[float] = None, q_g=None, k_g=None, v_g=None,
+                  threshold: Optional[float] = None, threshold_device=None, q_g=None, k_g=None,
+                  v_g=None,
                   gain_local=None, gain_global=None, eps: float = 1e-6, out=None,
                   sel_capacity: Optional[int] = None, sel_idx=None, cu_sel=None, tok2sel=None,
                   thr_out=None, ws=None, events=None):
@@ -302,10 +324,11 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
     boundaries (see include/logo.h).
     """
     import torch
-    if (ratio is None) == (threshold is None):
-        raise ValueError("give exactly one of ratio / threshold")
     N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
                         prob.num_seqs)
+    mode, thr_dev = _sel_mode(ratio, threshold, threshold_device, B)
+    if thr_dev is not None:
+        thr_out = thr_dev
     dev = q.device
     _check(q, torch.bfloat16, (N, Hq, d), "q")
     _check(k, torch.bfloat16, (N, Hkv, d), "k")
@@ -315,7 +338,6 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
         if t is not None:
             _check(t, torch.bfloat16, shp, nm)
     _check(gate, torch.float32, (N,), "gate")
-    mode = LOGO_SEL_RATIO if ratio is not None else LOGO_SEL_THRESHOLD
     if sel_capacity is None:
         sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
     if sel_idx is None:
@@ -357,3 +379,22 @@ def logo_dense_causal_attn(prob: Problem, q, k, v, out=None):
     _check(out, torch.bfloat16, (N, Hq, d), "out")
     _call("logo_dense_causal_attn", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream())
     return out
+
+
+def logo_budget_update(prob: Problem, cu_sel, rho: float, gamma: float, b_th, realized=None):
+    """One controller step b_th <- b_th + gamma sign(F - rho), F = cu_sel[B] / N,
+    on the device (b_th: device fp32 tensor, element 0 updated in place)."""
+    import torch
+    _check(cu_sel, torch.int32, (prob.num_seqs + 1,), "cu_sel")
+    if b_th.dtype != torch.float32 or not b_th.is_cuda or b_th.numel() < 1:
+        raise ValueError("b_th: device float32 tensor")
+    if realized is not None and (realized.dtype != torch.float32 or not realized.is_cuda):
+        raise ValueError("realized: device float32 tensor")
+    _call("logo_budget_update", prob.c, _ptr(cu_sel), float(rho), float(gamma), _ptr(b_th),
+          _ptr(realized), _stream())
+    return b_th
+
+
+def logo_pmask_initial_threshold(gamma: float, pmask_steps: int) -> float:
+    """Starting threshold of the P-mask schedule (host value)."""
+    return float(library().logo_pmask_initial_threshold(float(gamma), int(pmask_steps)))

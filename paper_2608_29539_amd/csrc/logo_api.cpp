@@ -181,7 +181,7 @@ int64_t ratio_capacity(const logo_problem *p, double ratio) {
 
 logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel_mode mode,
                               float threshold, double ratio, const int32_t *sel_idx,
-                              int32_t cap, const int32_t *cu_sel) {
+                              int32_t cap, const int32_t *cu_sel, const float *thr_out) {
     if (!gate || !cu_sel)
         return LOGO_ERR_NULL;
     if (cap < 0)
@@ -191,6 +191,9 @@ logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel
     if (mode == LOGO_SEL_THRESHOLD) {
         if (std::isnan(threshold))
             return LOGO_ERR_ARG;
+    } else if (mode == LOGO_SEL_THRESHOLD_DEVICE) {
+        if (!thr_out)
+            return LOGO_ERR_NULL;
     } else if (mode == LOGO_SEL_RATIO) {
         if (!(ratio >= 0.0 && ratio <= 1.0))
             return LOGO_ERR_ARG;
@@ -354,7 +357,7 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     int32_t *cus = cu_sel ? cu_sel : (int32_t *)(base + w.cu_sel);
     int32_t *t2s = tok2sel ? tok2sel : (int32_t *)(base + w.tok2sel);
     float *thr = thr_out ? thr_out : (float *)(base + w.thr);
-    st = check_select_args(p, gate, mode, threshold, ratio, sel, cap, cus);
+    st = check_select_args(p, gate, mode, threshold, ratio, sel, cap, cus, thr_out);
     if (st != LOGO_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
@@ -416,6 +419,27 @@ int64_t logo_ratio_capacity(const logo_problem *p, double ratio) {
     return ratio_capacity(p, ratio);
 }
 
+logo_status logo_budget_update(const logo_problem *p, const int32_t *cu_sel, double rho,
+                               float gamma, float *b_th, float *realized, logo_stream stream) {
+    if (!p)
+        return LOGO_ERR_NULL;
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (!cu_sel || !b_th)
+        return LOGO_ERR_NULL;
+    if (!(rho >= 0.0 && rho <= 1.0) || !(gamma >= 0.f) || std::isinf(gamma))
+        return LOGO_ERR_ARG;
+    hipStream_t s = (hipStream_t)stream;
+    return hip_status(launch_budget_update(cu_sel, p->num_seqs, p->total_tokens, rho, gamma,
+                                           b_th, realized, s),
+                      s);
+}
+
+float logo_pmask_initial_threshold(float gamma, int64_t pmask_steps) {
+    return (float)(0.5 - (double)gamma * (double)pmask_steps);
+}
+
 size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capacity) {
     if (check_problem(p) != LOGO_OK || sel_capacity < 0)
         return 0;
@@ -438,7 +462,8 @@ logo_status logo_select(const logo_problem *p, const float *gate, logo_sel_mode 
     logo_status st = check_problem(p);
     if (st != LOGO_OK)
         return st;
-    st = check_select_args(p, gate, mode, threshold, ratio, sel_idx, sel_capacity, cu_sel);
+    st = check_select_args(p, gate, mode, threshold, ratio, sel_idx, sel_capacity, cu_sel,
+                           thr_out);
     if (st != LOGO_OK)
         return st;
     st = check_ws(ws, ws_bytes, select_ws(p).total);

@@ -145,6 +145,10 @@ hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          int32_t *tok2sel, float *thr, int32_t *seq_counts,
                          const PlanArgs *plan, hipStream_t s);
 
+// One budget-controller step on the device (b_th += gamma sign(F - rho)).
+hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,
+                                float gamma, float *b_th, float *realized, hipStream_t s);
+
 hipError_t launch_combine(int n_tokens, int hq, int head_dim, const float *o_local,
                           const float *o_global, const float *gate,
                           const int32_t *tok2sel, const float *gain_local,

@@ -15,6 +15,8 @@
 //                     sequence: a single launch does all of it.  Several: a
 //                     first launch finds the thresholds and counts, a second
 //                     one compacts with offset = sum of the earlier counts.
+//   budget_kernel     one step of the global-budget controller (Sec. 3.2, Eq.
+//                     threshold-update) from the realized ratio cu_sel[B] / N.
 //   sparse_plan_kernel
 //                     cuts each sequence's selected rows into tiles of tpw
 //                     rows, splits the longest tiles into KV ranges so that no
@@ -317,8 +319,11 @@ __global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
     uint32_t thr_key;
     if constexpr (kThreshold) {
         const long long k = mode == 1 ? (long long)floor(ratio * (double)T) : 0;
+        if (mode == 2)
+            fixed = thr[0];                   // the device-held threshold
         if (mode != 1) {
-            thr_key = float_key(fixed);
+            // a NaN threshold (device mode) selects nothing, as gate > NaN
+            thr_key = fixed == fixed ? float_key(fixed) : 0xFFFFFFFFu;
         } else if (k >= T) {
             thr_key = float_key(-__builtin_inff());
         } else {
@@ -399,7 +404,8 @@ __global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
         if (tid == 0)
             thr[b] = mode == 1 ? key_float(thr_key) : fixed;
     } else {
-        thr_key = float_key(thr[b]);
+        const float v = thr[b];
+        thr_key = v == v ? float_key(v) : 0xFFFFFFFFu;   // NaN: nothing passes
     }
     // z = gate > thr on the keys: -0 and +0 share a key, and NaN gates (keys
     // above +inf, or below -inf) never pass.
@@ -476,7 +482,32 @@ __global__ __launch_bounds__(kSelThreads) void select_seq_kernel(
     }
 }
 
+// F = cu_sel[B] / N (Eq. realized-ratio), compared with rho in double;
+// b_th <- b_th + gamma sign(F - rho) in fp32 (Eq. threshold-update).
+__global__ void budget_kernel(const int32_t *cu_sel, int B, int N, double rho, float gamma,
+                              float *b_th, float *realized) {
+    if (threadIdx.x != 0)
+        return;
+    if (N <= 0) {
+        if (realized)
+            *realized = 0.f;
+        return;
+    }
+    const double f = (double)cu_sel[B] / (double)N;
+    const float b = *b_th;
+    *b_th = f > rho ? b + gamma : (f < rho ? b - gamma : b);
+    if (realized)
+        *realized = (float)f;
+}
+
 }  // namespace
+
+hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,
+                                float gamma, float *b_th, float *realized, hipStream_t s) {
+    hipLaunchKernelGGL(budget_kernel, dim3(1), dim3(64), 0, s, cu_sel, num_seqs, n_tokens, rho,
+                       gamma, b_th, realized);
+    return hipGetLastError();
+}
 
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
                          const float *gate, int mode, float threshold, double ratio,

@@ -170,3 +170,25 @@ def test_workspace_sizes(lib):
     assert lib.logo_workspace_bytes(p.c, 2, 4096) % 256 == 0
     bad = Prob(d=48)
     assert lib.logo_workspace_bytes(bad.c, 4, 10) == 0
+
+
+def test_budget_controller_validation(lib):
+    p = Prob()
+    f = lib.logo_budget_update          # argument types set by the binding
+    assert f(None, FAKE, 0.5, 0.1, FAKE, None, None) == ERR_NULL
+    assert f(p.c, None, 0.5, 0.1, FAKE, None, None) == ERR_NULL
+    assert f(p.c, FAKE, 0.5, 0.1, None, None, None) == ERR_NULL
+    assert f(p.c, FAKE, 1.5, 0.1, FAKE, None, None) == ERR_ARG
+    assert f(p.c, FAKE, float("nan"), 0.1, FAKE, None, None) == ERR_ARG
+    assert f(p.c, FAKE, 0.5, -0.1, FAKE, None, None) == ERR_ARG
+    assert f(p.c, FAKE, 0.5, float("inf"), FAKE, None, None) == ERR_ARG
+    g = lib.logo_pmask_initial_threshold
+    assert g(2.0 ** -10, 1024) == -0.5
+    assert g(0.25, 0) == 0.5
+
+
+def test_device_threshold_mode_needs_thr_out(lib):
+    p = Prob()
+    ws_need = lib.logo_workspace_bytes(p.c, 0, 0)
+    assert lib.logo_select(p.c, FAKE, 2, 0.0, 0.0, FAKE, 150, FAKE, None, None, FAKE, ws_need,
+                           None) == ERR_NULL
