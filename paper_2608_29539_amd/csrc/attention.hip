@@ -27,6 +27,7 @@
 // visible (no predicate), beyond its last row (skipped) or on the diagonal /
 // window edge (real-position mask on each score).
 #include "logo_internal.h"
+#include "plan.h"
 
 #include <type_traits>
 
@@ -767,8 +768,25 @@ void attn_kernel(const AttnArgs a) {
             }
         }
     } else {
-        const int hg = blockIdx.x % a.n_hg;
-        const int rest = blockIdx.x / a.n_hg;
+        int bid = blockIdx.x;
+        if constexpr (MODE == kModeLocal && EPI == kEpiFused) {
+            // The fused layer's local launch: workgroup 0 builds the global
+            // branch's work table (its LDS holds the table), the rest attend.
+            if (a.plan_wg) {
+                if (bid == 0) {
+                    constexpr int E = D == 128 ? 512 : 256;
+                    static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D>),
+                                  "plan table must fit in the K/V staging buffers");
+                    build_plan<waves_of(MODE) * 64, E>(
+                        a.cu_seqlens, a.num_seqs, a.plan,
+                        *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
+                    return;
+                }
+                bid -= 1;
+            }
+        }
+        const int hg = bid % a.n_hg;
+        const int rest = bid / a.n_hg;
         const int b = rest % a.num_seqs;
         int jt = rest / a.num_seqs;
         if (MODE == kModeDense)

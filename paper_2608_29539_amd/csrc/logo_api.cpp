@@ -205,16 +205,15 @@ logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel
     return LOGO_OK;
 }
 
-// plan != NULL: the selection launch(es) also build the global tile plan.
 logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
                        float threshold, double ratio, int32_t *sel_idx, int32_t cap,
                        int32_t *cu_sel, int32_t *tok2sel, float *thr_out, char *ws,
-                       hipStream_t s, const PlanArgs *plan = nullptr) {
+                       hipStream_t s) {
     const SelectWs w = select_ws(p);
     float *thr = thr_out ? thr_out : (float *)(ws + w.thr);
-    return hip_status(launch_select(p->cu_seqlens, p->num_seqs, p->total_tokens, gate,
-                                    (int)mode, threshold, ratio, sel_idx, cap, cu_sel, tok2sel,
-                                    thr, (int32_t *)(ws + w.counts), plan, s),
+    return hip_status(launch_select(p->cu_seqlens, p->num_seqs, p->max_seqlen, gate, (int)mode,
+                                    threshold, ratio, sel_idx, cap, cu_sel, tok2sel, thr,
+                                    (int32_t *)(ws + w.counts), s),
                       s);
 }
 
@@ -266,10 +265,12 @@ void set_fused(AttnArgs &a, const FusedEpi *f, const float *gain) {
     a.out_bf16 = f->out;
 }
 
-// o: raw fp32 O^L (f == NULL) or the fused epilogue (f != NULL).
+// o: raw fp32 O^L (f == NULL) or the fused epilogue (f != NULL).  plan:
+// with the fused epilogue, one extra workgroup of the launch builds the
+// global branch's work table.
 logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                       const logo_bf16 *v, float *o, const FusedEpi *f, const float *gain,
-                      hipStream_t s) {
+                      hipStream_t s, const PlanArgs *plan = nullptr) {
     if (p->total_tokens == 0)
         return LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
@@ -280,7 +281,11 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
     a.out = o;
     if (f)
         set_fused(a, f, gain);
-    const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max;
+    if (f && plan) {
+        a.plan_wg = 1;
+        a.plan = *plan;
+    }
+    const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max + a.plan_wg;
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
     return hip_status(
@@ -370,20 +375,20 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
 
     if ((st = mark(0)) != LOGO_OK)
         return st;
-    // The selection launch also builds the global branch's tile plan.
+    // Selection, then the local branch with the fused epilogue: Norm^L(O^L)
+    // straight to `out` for unselected tokens, (1-p) Norm^L(O^L) to the
+    // compact buffer for selected ones; one extra workgroup of that launch
+    // builds the global branch's tile plan.  Then the global branch finishes
+    // the selected rows.
     PlanArgs plan;
     int grid_g = 0;
     const bool with_plan = p->total_tokens > 0 && cap > 0;
     if (with_plan && (st = global_plan(p, sel, cus, cap, base + w.glob_ws, plan, grid_g)) != LOGO_OK)
         return st;
-    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s,
-                    with_plan ? &plan : nullptr);
+    st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);
     if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
         return st;
-    // Local branch with the fused epilogue: Norm^L(O^L) straight to `out`
-    // for unselected tokens, (1-p) Norm^L(O^L) to the compact buffer for
-    // selected ones.  Then the global branch finishes the selected rows.
-    st = run_local(p, q, k, v, nullptr, &fe, gain_local, s);
+    st = run_local(p, q, k, v, nullptr, &fe, gain_local, s, with_plan ? &plan : nullptr);
     if (st != LOGO_OK || (st = mark(2)) != LOGO_OK)
         return st;
     st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, nullptr, &fe,

@@ -49,7 +49,7 @@ inline TilePlan make_tile_plan(int hq, int hkv, int mode) {
 // long tile is split into nsplit entries over consecutive KV ranges; each
 // writes a partial (O, m, l) and the one that finishes last merges them in
 // split order (attention.hip).
-struct SparseTile {
+struct alignas(16) SparseTile {
     int32_t first;     // index of the tile's first row in sel_idx
     int32_t nrows;     // rows in the tile (1..tpw)
     int32_t seq;       // sequence b
@@ -91,6 +91,16 @@ inline int split_slots(int max_tiles, int n_hg) {
 //               ones; the global kernel then writes bf16 lc + p Norm^G(O^G).
 enum AttnEpi { kEpiRaw = 0, kEpiFused = 1 };
 
+// Tile plan of the global branch (device-built work table).  tmp and out each
+// hold max_tiles + split_slots entries; scratch holds 2 * stride ints with
+// stride >= max(B, max_tiles) + 1; split_cnt holds split_slots * n_hg ints.
+struct PlanArgs {
+    const int32_t *cu_sel;     // [B+1] compacted sequence offsets
+    const int32_t *sel_idx;    // [cap] selected token indices
+    int32_t tpw, cap, max_seqlen, n_hg, grid_wgs, split_slots, stride;
+    SparseTile *tmp, *out;
+    int32_t *scratch, *queue, *split_cnt;
+};
 struct AttnArgs {
     const uint16_t *q;
     const uint16_t *k;
@@ -115,6 +125,10 @@ struct AttnArgs {
     float eps;
     float *lc;                 // [capacity][Hq][d] fp32: (1-p) Norm^L of selected rows
     uint16_t *out_bf16;        // [N][Hq][d]
+    // fused local launch only: plan_wg = 1 makes workgroup 0 build the global
+    // branch's work table (`plan`) while the others attend
+    int32_t plan_wg;
+    PlanArgs plan;
 };
 
 // Launchers (return hipSuccess or the launch error).
@@ -122,28 +136,16 @@ hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, 
                             hipStream_t s);
 int attention_blocks_per_cu(int mode, int head_dim);
 
-// Tile plan of the global branch (device-built work table).  tmp and out each
-// hold max_tiles + split_slots entries; scratch holds 2 * stride ints with
-// stride >= max(B, max_tiles) + 1; split_cnt holds split_slots * n_hg ints.
-struct PlanArgs {
-    const int32_t *cu_sel;     // [B+1] compacted sequence offsets
-    const int32_t *sel_idx;    // [cap] selected token indices
-    int32_t tpw, cap, max_seqlen, n_hg, grid_wgs, split_slots, stride;
-    SparseTile *tmp, *out;
-    int32_t *scratch, *queue, *split_cnt;
-};
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
                               hipStream_t s);
 
 // Selection: thresholds, ranks and compaction.  seq_counts holds num_seqs
-// ints (per-sequence selected counts when num_seqs > 1).  With a non-null
-// plan the global tile plan is built too (inside the selection launch for
-// one sequence, as a separate launch otherwise).
-hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int n_tokens,
+// ints (per-sequence selected counts when num_seqs > 1).  max_seqlen sizes
+// the parts of a sequence that separate workgroups compact.
+hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *seq_counts,
-                         const PlanArgs *plan, hipStream_t s);
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s);
 
 // One budget-controller step on the device (b_th += gamma sign(F - rho)).
 hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,
