@@ -13,8 +13,10 @@ Reported (one JSON line on stdout):
                  (causally valid (query, key) pairs only, realized selection)
   speedup_vs_dense   t_dense / t_step, t_dense = best in-repo dense causal kernel
   roofline       the query-sparse global kernel (the dominant one) against the
-                 dense bf16 MFMA peak, its duration taken from HIP events
-                 recorded on its own stream inside the timed steps
+                 dense bf16 MFMA peak, its duration taken from HIP events that
+                 the profiled entry point records on the layer's stream, in a
+                 second timed run of the same steps (the headline steps run
+                 the plain entry point, with no events inside a step)
   cpu_baseline   the fp64 oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -223,28 +225,43 @@ def main(argv=None):
             e.record()                      # materialise the HIP events
     torch.cuda.synchronize()
 
-    def step(i):
+    def step(i=None):
+        # i: index of the event row the profiled entry point records stage
+        # boundaries into; None runs the plain entry point
         pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=w.ratio,
                          out=out, sel_capacity=cap, sel_idx=sel_idx, cu_sel=cu_sel,
-                         tok2sel=tok2sel, thr_out=thr, ws=ws, events=evs[i])
+                         tok2sel=tok2sel, thr_out=thr, ws=ws,
+                         events=None if i is None else evs[i])
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Timed region 1: the layer as a caller runs it (no events inside a step).
     t_wall = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = start.elapsed_time(end) / args.steps
+    # Timed region 2: the same steps through the profiled entry point, which
+    # records HIP events on the layer's stream at the stage boundaries
+    # (select | local + tile plan | - | global); the roofline's kernel
+    # duration comes from here.
     start.record()
     for i in range(args.warmup, n_ev):
         step(i)
     end.record()
     torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_step = start.elapsed_time(end) / args.steps
+    ms_step_profiled = start.elapsed_time(end) / args.steps
     stage_names = ("select", "local", "plan", "global")
     stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1])
                                   for i in range(args.warmup, n_ev)]))
                 for j, n in enumerate(stage_names)}
-    log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); stages "
+    log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); with stage "
+        f"events {ms_step_profiled:.3f} ms/step; stages "
         + " ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
 
     sel_np = sel_idx[: int(cu_sel[-1])].cpu().numpy()
@@ -363,6 +380,7 @@ def main(argv=None):
         "speedup_vs_dense": round(dense["t_dense_ms"] / ms_step, 3) if dense else None,
         "ideal_speedup_pairs": round(ideal, 3),
         "ideal_speedup_paper": round(1.0 / (w.ratio + w.window / w.max_seqlen), 3),
+        "ms_per_step_with_stage_events": round(ms_step_profiled, 4),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "local_tflops": round(local_tflops, 2),
         "global_tflops": round(global_tflops, 2),
@@ -371,7 +389,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "select_hbm": select_hbm,
         "threshold_mode": thr_mode,
-        "gpu": gpu_info(torch, busy=lambda: [step(0) for _ in range(600)])
+        "gpu": gpu_info(torch, busy=lambda: [step() for _ in range(600)])
                if not args.no_extra else None,
     }
     print(json.dumps(rec), flush=True)

@@ -44,6 +44,9 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr float kNegInf = -__builtin_inff();
 
+// Real-position masks of a KV tile (bit set).
+constexpr int kMaskNone = 0, kMaskCausal = 1, kMaskWindow = 2;
+
 // LDS tiles, both [key][d].  K rows are padded by 16 B so that the 16-byte
 // fragment reads of 8 consecutive rows hit distinct banks.  V rows are not
 // padded; instead the 64-byte segments of a row are permuted (segment j of
@@ -511,9 +514,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     // Softmax of tile kb (s -> pw); with do_pv, each 16-key slice's exps are
     // preceded by that slice's PV MFMAs of tile kb-1 (V(kb-1)), which read
     // the old pw before the exps overwrite it.  masked: the real-position
-    // mask (diagonal / window-edge tiles only).
+    // mask of the tile -- kMaskCausal (key <= pos, diagonal tiles),
+    // kMaskWindow (key > pos - w, the local window's left edge) or both.
     auto op_sm = [&](int kb_, auto do_pv, auto masked) {
-        if constexpr (decltype(masked)::value) {
+        constexpr int mk = decltype(masked)::value;
+        if constexpr (mk != kMaskNone) {
             const int k0 = kb_ * kBlockN;
 #pragma unroll
             for (int rg = 0; rg < RG; rg++)
@@ -522,8 +527,10 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
 #pragma unroll
                     for (int i = 0; i < 16; i++) {
                         const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
-                        bool ok = key <= pos[rg];
-                        if (MODE == kModeLocal)
+                        bool ok = true;
+                        if constexpr ((mk & kMaskCausal) != 0)
+                            ok = key <= pos[rg];
+                        if constexpr (MODE == kModeLocal && (mk & kMaskWindow) != 0)
                             ok = ok && (key > pos[rg] - w);
                         if (!ok)
                             s[rg][sb][i] = kNegInf;
@@ -579,6 +586,10 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
 
     using T_ = std::true_type;
     using F_ = std::false_type;
+    using MNone = std::integral_constant<int, kMaskNone>;
+    using MCausal = std::integral_constant<int, kMaskCausal>;
+    using MWindow = std::integral_constant<int, kMaskWindow>;
+    using MBoth = std::integral_constant<int, kMaskCausal | kMaskWindow>;
     // One step: S(kb) + softmax(kb) [x PV(kb-1)], or PV(kb-1) alone.
     auto step = [&](int kb_, auto do_s, auto do_pv, auto masked) {
         stage(kb_);
@@ -592,46 +603,59 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         }
         dma_wait_barrier();
     };
-    // Tiles needing the real-position mask: the diagonal tail (some key past
-    // the wave's first row) and, for the local branch, the window's left edge.
-    int kb_um_lo = kb_first, kb_um_hi = min(kb_last, (wpmin + 1) / kBlockN - 1);
+    // Tiles needing the real-position mask: the causal diagonal (some key past
+    // the wave's first row: kb > kb_c) and, for the local branch, the
+    // window's left edge (some key at or before the last row's pos - w:
+    // kb < kb_w).  The first is a suffix of the wave's tiles, the second a
+    // prefix.
+    const int kb_c = (wpmin + 1) / kBlockN - 1;
+    int kb_w = kb_first;
     if (MODE == kModeLocal) {
         const int edge = wpmax - w + 1;            // keys below this are out for the last row
         if (edge > 0)
-            kb_um_lo = max(kb_um_lo, (edge + kBlockN - 1) / kBlockN);
+            kb_w = max(kb_w, (edge + kBlockN - 1) / kBlockN);
     }
-    auto unmasked = [&](int kb_) { return kb_ >= kb_um_lo && kb_ <= kb_um_hi; };
 
     // Every wave walks all tiles of the workgroup's range (they share the
     // staging and the barriers) but computes only its own sub-range
-    // kb_first..kb_last, in loops of a single kind each -- masked window
-    // edge, unmasked middle, masked diagonal -- so that no loop body switches
-    // between instantiations.
+    // kb_first..kb_last, in loops of a single mask kind each -- window edge,
+    // unmasked middle (or both masks where edge and diagonal overlap),
+    // diagonal -- so that no loop body switches between instantiations.
     int kb = kb_lo;
     bool pending = false;
     for (; kb < kb_first && kb <= kb_hi; kb++)
-        step(kb, F_{}, F_{}, F_{});
+        step(kb, F_{}, F_{}, MNone{});
     if (kb_first <= kb_last) {
-        if (unmasked(kb))
-            step(kb, T_{}, F_{}, F_{});
+        // the first tile computed has no PV of a previous tile
+        const bool need_c = kb > kb_c, need_w = kb < kb_w;
+        if (need_c && need_w)
+            step(kb, T_{}, F_{}, MBoth{});
+        else if (need_c)
+            step(kb, T_{}, F_{}, MCausal{});
+        else if (need_w)
+            step(kb, T_{}, F_{}, MWindow{});
         else
-            step(kb, T_{}, F_{}, T_{});
+            step(kb, T_{}, F_{}, MNone{});
         kb++;
-        for (const int e = min(kb_last, kb_um_lo - 1); kb <= e; kb++)
-            step(kb, T_{}, T_{}, T_{});
-        for (const int e = min(kb_last, kb_um_hi); kb <= e; kb++)
-            step(kb, T_{}, T_{}, F_{});
+        if (MODE == kModeLocal) {
+            for (const int e = min(kb_last, min(kb_w - 1, kb_c)); kb <= e; kb++)
+                step(kb, T_{}, T_{}, MWindow{});
+            for (const int e = min(kb_last, kb_w - 1); kb <= e; kb++)
+                step(kb, T_{}, T_{}, MBoth{});
+        }
+        for (const int e = min(kb_last, kb_c); kb <= e; kb++)
+            step(kb, T_{}, T_{}, MNone{});
         for (; kb <= kb_last; kb++)
-            step(kb, T_{}, T_{}, T_{});
+            step(kb, T_{}, T_{}, MCausal{});
         pending = true;
     }
     if (pending && kb <= kb_hi) {
-        step(kb, F_{}, T_{}, F_{});
+        step(kb, F_{}, T_{}, MNone{});
         pending = false;
         kb++;
     }
     for (; kb <= kb_hi; kb++)
-        step(kb, F_{}, F_{}, F_{});
+        step(kb, F_{}, F_{}, MNone{});
     if (pending) {
         apply_rescale();
         pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step

@@ -3,27 +3,26 @@
 // original positions and compacted sequence offsets), plus the tile plan
 // of the query-sparse global branch.
 //
-//   select_seq_kernel one 1024-thread workgroup per sequence.  Threshold:
-//                     ratio mode takes k = floor(ratio*T) in IEEE double and
-//                     the (k+1)-th largest gate, found by a three-pass radix
-//                     select (12 + 12 + 8 bits) over order-preserving uint32
-//                     keys with LDS histograms; threshold mode takes the given
+//   select_kernel     up to 16 workgroups of 1024 threads per sequence, each
+//                     compacting one part of it.  Threshold: ratio mode takes
+//                     k = floor(ratio*T) in IEEE double and the (k+1)-th
+//                     largest gate, found by every part with radix passes of
+//                     at most 12 bits over order-preserving uint32 keys (LDS
+//                     histograms), starting below the bits that all keys of
+//                     the sequence share; threshold mode takes the given
 //                     value.  Then z_t = gate[t] > thr (strict, fp32, done on
-//                     the keys) is counted and, with the sequence's offset
-//                     known, compacted: ranks from wave ballots, mbcnt and a
-//                     workgroup scan; writes sel_idx, tok2sel and cu_sel.  One
-//                     sequence: a single launch does all of it.  Several: a
-//                     first launch finds the thresholds and counts, a second
-//                     one compacts with offset = sum of the earlier counts.
+//                     the keys) and the part's ranks follow from the selected
+//                     count before it plus one workgroup scan; writes sel_idx,
+//                     tok2sel and cu_sel.  One sequence: a single launch.
+//                     Several: a first launch finds the thresholds and
+//                     counts, a second one compacts with offset = sum of the
+//                     earlier counts.
 //   budget_kernel     one step of the global-budget controller (Sec. 3.2, Eq.
 //                     threshold-update) from the realized ratio cu_sel[B] / N.
 //   sparse_plan_kernel
-//                     cuts each sequence's selected rows into tiles of tpw
-//                     rows, splits the longest tiles into KV ranges so that no
-//                     work entry exceeds a fraction of one persistent
-//                     workgroup's mean load, orders the entries longest-first
-//                     (bucketed by KV length), then resets the work queues and
-//                     the split counters.
+//                     the global branch's work table (plan.h) for the
+//                     standalone query-sparse entry point; the fused layer
+//                     builds it inside its local-branch launch instead.
 #include "logo_internal.h"
 #include "plan.h"
 
