@@ -12,6 +12,7 @@ from .oracle import (  # noqa: F401
     budget_update,
     build,
     contextnorm,
+    decode,
     fuse,
     library_path,
     logo_fwd,

@@ -28,6 +28,10 @@
  *   - budget controller b_th <- b_th + gamma sign(F - rho) and the P-mask
  *     starting threshold                                  (Sec. 3.2, Eq. threshold-update
  *                                                          and the P-mask paragraph)
+ *   - one autoregressive decoding step: the new token's local and (when
+ *     selected) global attention over the KV cache, fused as above
+ *                                                         (Sec. 3.3 and App. B,
+ *                                                          Autoregressive Decoding)
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *   - positions are 0-based: key j is visible to query i iff j <= i (global)
@@ -374,6 +378,125 @@ int64_t oracle_logo_fwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
         oracle_contextnorm(ng, n_sel, Hq, d, gain_global, eps);
     }
     oracle_fuse(nl, ng, gate, tok2sel, N, Hq, d, out);
+    free(nl);
+    free(ng);
+    return n_sel;
+}
+
+/*
+ * One autoregressive decoding step of the layer (Sec. 3.3, Autoregressive
+ * Decoding; App. B, Autoregressive Decoding).
+ *
+ * Sequence b's cache holds L_b = cu[b+1] - cu[b] >= 1 tokens (rows cu[b] ..
+ * cu[b+1]-1 of k/v and k_g/v_g); the last of them is the new token itself,
+ * at position L_b - 1, its key and value already appended.  Its query
+ * q_new[b] attends over the local context (the last min(L_b, w) cached keys,
+ * itself included).  Its gate value gate_new[b] decides the global branch
+ * (z = [p > threshold], strict, as in Eq. gate-routing); a selected token's
+ * global query q_g_new[b] attends over all L_b cached global keys.  Both
+ * outputs are ContextNorm-ed and fused as in Eqs. contextnorm and
+ * output-fusion; an unselected token's output is Norm^L of its local output.
+ *
+ * Inputs as in oracle_logo_fwd; q_new, q_g_new are [B][Hq][d] (q_g_new,
+ * k_g, v_g may be NULL: the local tensors).  Outputs: o_local[B][Hq][d] and
+ * o_global[B][Hq][d] (raw branch outputs; rows of unselected tokens are
+ * zero), out[B][Hq][d], z_out[B].  Returns the number of selected tokens.
+ */
+int64_t oracle_decode(const uint16_t *q_new, const uint16_t *q_g_new, const uint16_t *k,
+                      const uint16_t *v, const uint16_t *k_g, const uint16_t *v_g,
+                      const float *gate_new, const int32_t *cu, int B, int Hq, int Hkv, int d,
+                      int window, double scale, float threshold, const float *gain_local,
+                      const float *gain_global, double eps, double *o_local, double *o_global,
+                      double *out, int32_t *z_out)
+{
+    const int G = Hq / Hkv;
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    if (!q_g_new)
+        q_g_new = q_new;
+    if (!k_g)
+        k_g = k;
+    if (!v_g)
+        v_g = v;
+    int64_t max_L = 1;
+    int64_t n_sel = 0;
+    for (int b = 0; b < B; b++) {
+        if ((int64_t)cu[b + 1] - cu[b] > max_L)
+            max_L = (int64_t)cu[b + 1] - cu[b];
+        z_out[b] = gate_new[b] > threshold ? 1 : 0;
+        n_sel += z_out[b];
+    }
+
+#pragma omp parallel
+    {
+        double *score = (double *)malloc((size_t)max_L * sizeof(double));
+        double *qd = (double *)malloc((size_t)d * sizeof(double));
+        double *acc = (double *)malloc((size_t)d * sizeof(double));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t job = 0; job < (int64_t)B * Hq * 2; job++) {
+            const int branch = (int)(job % 2); /* 0 local, 1 global */
+            const int h = (int)((job / 2) % Hq);
+            const int b = (int)(job / 2 / Hq);
+            const int kvh = h / G;
+            const int64_t base = cu[b];
+            const int64_t L = (int64_t)cu[b + 1] - base;
+            double *o = (branch == 0 ? o_local : o_global) + ((int64_t)b * Hq + h) * d;
+            if (branch == 1 && !z_out[b]) {
+                for (int c = 0; c < d; c++)
+                    o[c] = 0.0;
+                continue;
+            }
+            const uint16_t *qq = (branch == 0 ? q_new : q_g_new) + ((int64_t)b * Hq + h) * d;
+            const uint16_t *kk = branch == 0 ? k : k_g;
+            const uint16_t *vv = branch == 0 ? v : v_g;
+            /* context: keys lo .. L-1 of the cache */
+            const int64_t lo = (branch == 0 && L > window) ? L - window : 0;
+            const int64_t nk = L - lo;
+            for (int c = 0; c < d; c++)
+                qd[c] = bf16_to_double(qq[c]);
+            double m = -INFINITY;
+            for (int64_t j = 0; j < nk; j++) {
+                const uint16_t *kr = kk + ((base + lo + j) * Hkv + kvh) * (int64_t)d;
+                double dot = 0.0;
+                for (int c = 0; c < d; c++)
+                    dot += qd[c] * bf16_to_double(kr[c]);
+                score[j] = scale * dot;
+                if (score[j] > m)
+                    m = score[j];
+            }
+            double wsum = 0.0;
+            for (int c = 0; c < d; c++)
+                acc[c] = 0.0;
+            for (int64_t j = 0; j < nk; j++) {
+                const double e = exp(score[j] - m);
+                const uint16_t *vr = vv + ((base + lo + j) * Hkv + kvh) * (int64_t)d;
+                wsum += e;
+                for (int c = 0; c < d; c++)
+                    acc[c] += e * bf16_to_double(vr[c]);
+            }
+            for (int c = 0; c < d; c++)
+                o[c] = acc[c] / wsum;
+        }
+        free(score);
+        free(qd);
+        free(acc);
+    }
+
+    /* ContextNorm of both branches, then the fusion */
+    const int64_t row = (int64_t)Hq * d;
+    double *nl = (double *)malloc((size_t)B * row * sizeof(double));
+    double *ng = (double *)malloc((size_t)B * row * sizeof(double));
+    memcpy(nl, o_local, (size_t)B * row * sizeof(double));
+    memcpy(ng, o_global, (size_t)B * row * sizeof(double));
+    oracle_contextnorm(nl, B, Hq, d, gain_local, eps);
+    oracle_contextnorm(ng, B, Hq, d, gain_global, eps);
+    for (int b = 0; b < B; b++) {
+        const double p = (double)gate_new[b];
+        for (int64_t e = 0; e < row; e++) {
+            const double l = nl[b * row + e];
+            out[b * row + e] = z_out[b] ? (1.0 - p) * l + p * ng[b * row + e] : l;
+        }
+    }
     free(nl);
     free(ng);
     return n_sel;

@@ -67,6 +67,9 @@ def _load():
     lib.oracle_budget_update.restype = f32
     lib.oracle_pmask_initial_threshold.argtypes = [f32, i64]
     lib.oracle_pmask_initial_threshold.restype = f32
+    lib.oracle_decode.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, f32,
+                                  P, P, f64, P, P, P, P]
+    lib.oracle_decode.restype = i64
     _lib = lib
     return lib
 
@@ -218,3 +221,26 @@ def logo_rows(x: Dict[str, np.ndarray], window: int, rows, *, ratio: Optional[fl
     out = fuse(nl, ng, x["gate"][rows], sub_t2s)
     return dict(out=out, o_local=ol, o_global=og, selected_rows=selected_rows, thr=thr,
                 sel_idx=sel_idx, cu_sel=cu_sel, tok2sel=tok2sel)
+
+
+def decode(q_new, k, v, gate_new, cu_cache, window: int, threshold: float, *, q_g_new=None,
+           k_g=None, v_g=None, gain_local=None, gain_global=None, eps: float = 1e-6,
+           scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """One decoding step in fp64 (Sec. 3.3, Autoregressive Decoding): q_new is
+    [B, Hq, d] (the new tokens), k/v the packed caches [cu_cache[B], Hkv, d]
+    whose last row per sequence is the new token's own key/value."""
+    q_new, k, v = _c(q_new, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    q_g_new, k_g, v_g = _c(q_g_new, np.uint16), _c(k_g, np.uint16), _c(v_g, np.uint16)
+    gate_new, cu = _c(gate_new, np.float32), _c(cu_cache, np.int32)
+    B, Hq, d = q_new.shape
+    Hkv = k.shape[1]
+    ol = np.empty((B, Hq, d), dtype=np.float64)
+    og = np.empty((B, Hq, d), dtype=np.float64)
+    out = np.empty((B, Hq, d), dtype=np.float64)
+    z = np.empty(B, dtype=np.int32)
+    n = _load().oracle_decode(
+        _ptr(q_new), _ptr(q_g_new), _ptr(k), _ptr(v), _ptr(k_g), _ptr(v_g), _ptr(gate_new),
+        _ptr(cu), B, Hq, Hkv, d, int(window), float(scale), float(threshold),
+        _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)), float(eps),
+        _ptr(ol), _ptr(og), _ptr(out), _ptr(z))
+    return dict(out=out, o_local=ol, o_global=og, z=z.astype(bool), n_sel=int(n))

@@ -47,6 +47,19 @@ MUTATIONS = {
     "realized_ratio_inverted": ("(double)n_selected / (double)n_valid", "(double)n_valid / (double)n_selected"),
     "pmask_start_sign": ("(float)(0.5 - (double)gamma * (double)pmask_steps)",
                          "(float)(0.5 + (double)gamma * (double)pmask_steps)"),
+    "decode_window_w_plus_1_keys": ("(branch == 0 && L > window) ? L - window : 0",
+                                    "(branch == 0 && L > window) ? L - window - 1 : 0"),
+    "decode_gate_ge_instead_of_gt": ("z_out[b] = gate_new[b] > threshold ? 1 : 0;",
+                                     "z_out[b] = gate_new[b] >= threshold ? 1 : 0;"),
+    "decode_global_reads_local_query": ("(branch == 0 ? q_new : q_g_new)", "q_new"),
+    "decode_global_windowed": ("(branch == 0 && L > window)", "(L > window)"),
+    "decode_gqa_modulo_mapping": ("const int kvh = h / G;", "const int kvh = h % Hkv;"),
+    "decode_fusion_weights_swapped": ("? (1.0 - p) * l + p * ng[b * row + e] : l",
+                                      "? p * l + (1.0 - p) * ng[b * row + e] : l"),
+    "decode_unselected_fused": ("z_out[b] ? (1.0 - p) * l + p * ng[b * row + e] : l",
+                                "(1.0 - p) * l + p * ng[b * row + e]"),
+    "decode_cache_offset_dropped": ("const int64_t base = cu[b];\n            const int64_t L",
+                                    "const int64_t base = 0;\n            const int64_t L"),
 }
 
 

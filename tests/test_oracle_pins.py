@@ -427,3 +427,97 @@ def test_controller_settles_at_target_quantile(oracle_lib):
     thr = oracle_lib.thresholds(gate, cu, oracle_lib.SEL_THRESHOLD, threshold=b)
     _, cu_sel, _ = oracle_lib.select(gate, cu, thr)
     assert abs(int(cu_sel[-1]) / N - rho) <= gamma
+
+
+# ---------------------------------------------------------------------------
+# One decoding step (Sec. 3.3 and App. B, Autoregressive Decoding): the new
+# token is the last row of its sequence's cache.
+# ---------------------------------------------------------------------------
+DECODE_CASES = [
+    # seqlens (cache lengths), Hq, Hkv, d, window, threshold, distinct global, gains
+    ((5, 1, 9, 16), 4, 2, 8, 4, 0.5, False, False),
+    ((12, 3, 7), 2, 2, 4, 16, 0.3, True, True),
+    ((1, 2, 6, 11, 4), 8, 2, 8, 1, 0.6, True, False),
+    ((16,), 4, 1, 4, 5, -1.0, False, True),
+]
+
+
+def _decode_inputs(case, seed):
+    seqlens, Hq, Hkv, d, window, thr, distinct, gains = case
+    rng = np.random.default_rng(seed)
+    N = int(sum(seqlens))
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    x = dict(q=mk(N, Hq, d), k=mk(N, Hkv, d), v=mk(N, Hkv, d),
+             gate=rng.uniform(0, 1, N).astype(np.float32),
+             cu_seqlens=np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32))
+    if distinct:
+        x.update(q_g=mk(N, Hq, d), k_g=mk(N, Hkv, d), v_g=mk(N, Hkv, d))
+    gl = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if gains else None
+    gg = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if gains else None
+    last = x["cu_seqlens"][1:] - 1
+    return x, last, window, thr, gl, gg
+
+
+@pytest.mark.parametrize("ci", range(len(DECODE_CASES)))
+def test_decode_equals_layer_last_rows(oracle_lib, ci):
+    """The decoding step reproduces the layer's output at each sequence's last
+    position (threshold mode): same local window, same strict gate, same
+    global context, same ContextNorm and fusion."""
+    x, last, window, thr, gl, gg = _decode_inputs(DECODE_CASES[ci], 700 + ci)
+    ref = oracle_lib.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], window,
+                              threshold=thr, q_g=x.get("q_g"), k_g=x.get("k_g"),
+                              v_g=x.get("v_g"), gain_local=gl, gain_global=gg)
+    dq_g = x["q_g"][last] if "q_g" in x else None
+    r = oracle_lib.decode(x["q"][last], x["k"], x["v"], x["gate"][last], x["cu_seqlens"], window,
+                          thr, q_g_new=dq_g, k_g=x.get("k_g"), v_g=x.get("v_g"),
+                          gain_local=gl, gain_global=gg)
+    np.testing.assert_array_equal(r["z"], ref["tok2sel"][last] >= 0)
+    np.testing.assert_allclose(r["o_local"], ref["o_local"][last], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(r["out"], ref["out"][last], rtol=0, atol=1e-13)
+    sel = np.nonzero(r["z"])[0]
+    np.testing.assert_allclose(r["o_global"][sel], ref["o_global"][ref["tok2sel"][last[sel]]],
+                               rtol=0, atol=1e-13)
+    assert not r["o_global"][~r["z"]].any()
+
+
+@pytest.mark.parametrize("ci", range(len(DECODE_CASES)))
+def test_decode_bruteforce(oracle_lib, ci):
+    """Independent numpy: the last query row against the cache, explicit masks."""
+    x, last, window, thr, gl, gg = _decode_inputs(DECODE_CASES[ci], 800 + ci)
+    seqlens = np.diff(x["cu_seqlens"])
+    b = brute_layer(x["q"], x["k"], x["v"], x["gate"], seqlens, window, threshold=thr,
+                    q_g=x.get("q_g"), k_g=x.get("k_g"), v_g=x.get("v_g"), gain_l=gl, gain_g=gg)
+    dq_g = x["q_g"][last] if "q_g" in x else None
+    r = oracle_lib.decode(x["q"][last], x["k"], x["v"], x["gate"][last], x["cu_seqlens"], window,
+                          thr, q_g_new=dq_g, k_g=x.get("k_g"), v_g=x.get("v_g"),
+                          gain_local=gl, gain_global=gg)
+    np.testing.assert_array_equal(r["z"], b["selected"][last])
+    np.testing.assert_allclose(r["out"], b["out"][last], rtol=0, atol=1e-12)
+
+
+def test_decode_zero_query_closed_form(oracle_lib):
+    """q = 0 gives uniform weights: the local output is the mean of the last w
+    cached values, the global one the mean of all of them; an unselected
+    token's output is Norm^L of the former, a selected one's the fusion."""
+    rng = np.random.default_rng(5)
+    seqlens, Hq, Hkv, d, w = (9, 3), 2, 1, 4, 4
+    N = sum(seqlens)
+    v = bf16(np.round(rng.standard_normal((N, Hkv, d)) * 4) / 4)
+    k = bf16(np.round(rng.standard_normal((N, Hkv, d)) * 4) / 4)
+    q = np.zeros((2, Hq, d), np.uint16)
+    cu = np.array([0, 9, 12], np.int32)
+    gate = np.array([0.25, 0.75], np.float32)
+    r = oracle_lib.decode(q, k, v, gate, cu, w, 0.5, eps=0.0)
+    # strict '>': a gate equal to the threshold stays local
+    tie = oracle_lib.decode(q, k, v, np.array([0.5, 0.5], np.float32), cu, w, 0.5, eps=0.0)
+    assert tie["z"].tolist() == [False, False] and tie["n_sel"] == 0
+    vf = wide(v)[:, 0, :]
+    loc = [vf[5:9].mean(0), vf[9:12].mean(0)]
+    glo = vf[9:12].mean(0)
+    rms = lambda a: a / np.sqrt((a ** 2).mean())  # noqa: E731
+    np.testing.assert_allclose(r["o_local"][0, 0], loc[0], atol=1e-15)
+    np.testing.assert_allclose(r["o_local"][1, 1], loc[1], atol=1e-15)
+    np.testing.assert_allclose(r["o_global"][1, 0], glo, atol=1e-15)
+    assert r["z"].tolist() == [False, True]
+    np.testing.assert_allclose(r["out"][0, 0], rms(loc[0]), atol=1e-14)
+    np.testing.assert_allclose(r["out"][1, 0], 0.25 * rms(loc[1]) + 0.75 * rms(glo), atol=1e-14)
