@@ -68,7 +68,8 @@ typedef enum {
     LOGO_ENTRY_GLOBAL = 2,
     LOGO_ENTRY_COMBINE = 3,
     LOGO_ENTRY_FWD = 4,
-    LOGO_ENTRY_DENSE = 5
+    LOGO_ENTRY_DENSE = 5,
+    LOGO_ENTRY_DECODE = 6
 } logo_entry;
 
 /* Problem description (a host struct; only cu_seqlens is a device pointer). */
@@ -232,6 +233,48 @@ logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
                                    logo_stream stream);
+
+/*
+ * logo_decode -- one autoregressive decoding step of the layer (Sec. 3.3 and
+ * App. B, Autoregressive Decoding): each of the B sequences appends one
+ * token.  Its query attends to the last min(L_b, w) cached keys (local
+ * branch); when its gate passes the threshold (z = p > b_th, strict, fp32,
+ * Eq. gate-routing) its global query also attends to all L_b cached global
+ * keys; the outputs are ContextNorm-ed and fused as in logo_attn_fwd (Eqs.
+ * contextnorm, output-fusion).  Only selected tokens get global work: the
+ * selected sequences are compacted first, so an unselected token reads one
+ * window of its cache.
+ *   p          cu_seqlens = the caches: sequence b's cache is rows
+ *              cu[b] .. cu[b+1]-1 of k / v, L_b = cu[b+1] - cu[b] >= 1, and
+ *              its last row is the new token's own key and value (appended
+ *              by the caller).  num_seqs = B; total_tokens = cu[B];
+ *              max_seqlen >= every L_b; heads, head_dim, window, scale as in
+ *              the layer.  With cu_seqlens_host given, L_b = 0 is rejected
+ *              (LOGO_ERR_SHAPE); without it such a sequence outputs zeros.
+ *   q          device [B][Hq][d] bf16: the new tokens' queries.
+ *   k, v       device [N][Hkv][d] bf16: the caches (the prefill layout).
+ *   q_g, k_g, v_g  the global branch's tensors, same shapes (NULL = the
+ *              local ones, the identity branch transform).
+ *   gate       device [B] fp32: p of the new tokens (NaN is never selected).
+ *   mode       LOGO_SEL_THRESHOLD: b_th = threshold (NaN rejected);
+ *              LOGO_SEL_THRESHOLD_DEVICE: b_th = thr_dev[0] read on the
+ *              device (thr_dev must not be NULL); LOGO_SEL_RATIO is rejected
+ *              (LOGO_ERR_ARG): decoding routes with the layer's threshold.
+ *   gain_local, gain_global, eps   ContextNorm, as in logo_combine.
+ *   out        device [B][Hq][d] bf16.
+ *   active     device [B] int32 or NULL: the selected sequences, ascending,
+ *              in its first n_active entries.
+ *   n_active   device int32 or NULL: the number of selected sequences.
+ *   ws         >= logo_workspace_bytes(p, LOGO_ENTRY_DECODE, 0) bytes,
+ *              256-byte aligned (partial results of the key chunks).
+ * Asynchronous on `stream`; nothing is enqueued on error.
+ */
+logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                        const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                        const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                        float threshold, const float *thr_dev, const float *gain_local,
+                        const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
+                        int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream);
 
 /*
  * logo_budget_update -- one step of the global-budget controller

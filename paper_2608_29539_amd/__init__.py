@@ -9,6 +9,7 @@ the library; the first call does, and raises if it is missing (build it with
 """
 from .binding import (  # noqa: F401
     LOGO_ENTRY_COMBINE,
+    LOGO_ENTRY_DECODE,
     LOGO_ENTRY_DENSE,
     LOGO_ENTRY_FWD,
     LOGO_ENTRY_GLOBAL,
@@ -25,6 +26,7 @@ from .binding import (  # noqa: F401
     logo_attn_fwd,
     logo_budget_update,
     logo_combine,
+    logo_decode,
     logo_dense_causal_attn,
     logo_global_attn_sparse_q,
     logo_local_attn,

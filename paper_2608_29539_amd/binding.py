@@ -24,13 +24,14 @@ LOGO_ENTRY_GLOBAL = 2
 LOGO_ENTRY_COMBINE = 3
 LOGO_ENTRY_FWD = 4
 LOGO_ENTRY_DENSE = 5
+LOGO_ENTRY_DECODE = 6
 
 #: every symbol include/logo.h declares
 EXPORTS = (
     "logo_select", "logo_local_attn", "logo_global_attn_sparse_q", "logo_combine",
     "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
     "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
-    "logo_pmask_initial_threshold",
+    "logo_pmask_initial_threshold", "logo_decode",
 )
 
 _lib = None
@@ -85,6 +86,7 @@ def library():
                                    P, P, P, P, sz, P, P],
         "logo_dense_causal_attn": [PP, P, P, P, P, P],
         "logo_budget_update": [PP, P, f64, f32, P, P, P],
+        "logo_decode": [PP, P, P, P, P, P, P, P, i32, f32, P, P, P, f32, P, P, P, P, sz, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -398,3 +400,48 @@ def logo_budget_update(prob: Problem, cu_sel, rho: float, gamma: float, b_th, re
 def logo_pmask_initial_threshold(gamma: float, pmask_steps: int) -> float:
     """Starting threshold of the P-mask schedule (host value)."""
     return float(library().logo_pmask_initial_threshold(float(gamma), int(pmask_steps)))
+
+
+def logo_decode(prob: Problem, q, k, v, gate, *, threshold: Optional[float] = None,
+                threshold_device=None, q_g=None, k_g=None, v_g=None, gain_local=None,
+                gain_global=None, eps: float = 1e-6, out=None, active=None, n_active=None,
+                ws=None):
+    """One decoding step: ``prob.cu_seqlens`` bounds the KV caches (each
+    sequence's last cached row is its new token), ``q`` [B, Hq, d] the new
+    tokens' queries, ``gate`` [B].  Exactly one of ``threshold`` (host value)
+    and ``threshold_device`` (device fp32, element 0) gives b_th.  Returns
+    (out, active, n_active)."""
+    import torch
+    N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
+                        prob.num_seqs)
+    if (threshold is None) == (threshold_device is None):
+        raise ValueError("give exactly one of threshold / threshold_device")
+    if threshold_device is not None:
+        if (threshold_device.dtype != torch.float32 or not threshold_device.is_cuda
+                or threshold_device.numel() < 1):
+            raise ValueError("threshold_device: device float32 tensor")
+        mode = LOGO_SEL_THRESHOLD_DEVICE
+    else:
+        mode = LOGO_SEL_THRESHOLD
+    dev = q.device
+    _check(q, torch.bfloat16, (B, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    for t, nm, shp in ((q_g, "q_g", (B, Hq, d)), (k_g, "k_g", (N, Hkv, d)),
+                       (v_g, "v_g", (N, Hkv, d))):
+        if t is not None:
+            _check(t, torch.bfloat16, shp, nm)
+    _check(gate, torch.float32, (B,), "gate")
+    if out is None:
+        out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device=dev)
+    _check(out, torch.bfloat16, (B, Hq, d), "out")
+    if active is None:
+        active = torch.empty(B, dtype=torch.int32, device=dev)
+    if n_active is None:
+        n_active = torch.empty(1, dtype=torch.int32, device=dev)
+    ws, nbytes = _ws(prob, LOGO_ENTRY_DECODE, 0, ws)
+    _call("logo_decode", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g),
+          _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
+          _ptr(threshold_device), _ptr(gain_local), _ptr(gain_global), float(eps), _ptr(out),
+          _ptr(active), _ptr(n_active), _ptr(ws), nbytes, _stream())
+    return out, active, n_active

@@ -1,0 +1,376 @@
+// decode.hip -- one autoregressive decoding step of the layer (Sec. 3.3 and
+// App. B, Autoregressive Decoding).  Each of B sequences appends one token
+// whose key and value are already the last row of its cache.  The token's
+// query attends to the last min(L, w) cached keys (local branch); when its
+// gate passes the threshold it also attends to the whole cache (global
+// branch), and the two outputs are ContextNorm-ed and fused as in the layer.
+//
+// Rows are compacted as in the prefill: decode_select_kernel lists the
+// sequences whose token is selected, and only those get global work items,
+// so an unselected token costs one window of the cache (the paper's batched
+// decoding instead launches the dense kernel for every row and masks).
+//
+//   decode_select_kernel  z_b = gate[b] > thr (fp32, strict); compacted list
+//                         of selected sequences, each sequence's rank, count.
+//   decode_attn_kernel    split-KV attention, one workgroup per (sequence or
+//                         selected row, KV head, head group, chunk of keys):
+//                         the GH query heads of one KV head share every K/V
+//                         row read, eight lanes cover one 2d-byte row, and 32
+//                         rows are in flight per workgroup step.  Writes the
+//                         chunk's unnormalised (O, m, l) per head.
+//   decode_combine_kernel merges the chunks of each (sequence, head) in chunk
+//                         order, applies ContextNorm to each branch and the
+//                         fusion, and rounds once to bf16.
+//
+// The cache is read once per branch (HBM-bound); the arithmetic is fp32
+// (bf16 dot products accumulate in fp32 with v_dot2), so no MFMA is needed.
+#include "logo_internal.h"
+
+namespace logo {
+namespace {
+
+constexpr int kDecThreads = 256;
+constexpr int kStreams = kDecThreads / 8;   // keys in flight per workgroup step
+constexpr float kNegInfD = -__builtin_inff();
+constexpr float kLazyD = 8.f;               // exp2-domain headroom of the running max
+
+typedef uint32_t u32x4d __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2d __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+__global__ __launch_bounds__(1024) void decode_select_kernel(int B, const float *gate, int mode,
+                                                              float thr_host, const float *thr_dev,
+                                                              int32_t *act, int32_t *rank_of,
+                                                              int32_t *n_act) {
+    __shared__ int s_wave[16];
+    __shared__ int s_carry;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float thr = mode == 2 ? thr_dev[0] : thr_host;
+    if (tid == 0)
+        s_carry = 0;
+    __syncthreads();
+    for (int c0 = 0; c0 < B; c0 += 1024) {
+        const int b = c0 + tid;
+        const bool z = b < B && gate[b] > thr;      // NaN gate or threshold: false
+        const uint64_t m = __ballot(z);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+        if (lane == 0)
+            s_wave[wave] = (int)__popcll(m);
+        __syncthreads();
+        int before = s_carry;
+        for (int i = 0; i < wave; i++)
+            before += s_wave[i];
+        if (b < B) {
+            const int r = before + below;
+            rank_of[b] = z ? r : -1;
+            if (z)
+                act[r] = b;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int t = 0;
+            for (int i = 0; i < 16; i++)
+                t += s_wave[i];
+            s_carry += t;
+        }
+        __syncthreads();
+    }
+    if (tid == 0)
+        n_act[0] = s_carry;
+}
+
+// (m, l, acc) of stream b merged into stream a (exp2 domain).
+__device__ __forceinline__ void merge_into(float &ma, float &la, float &mb, float &lb, float *aa,
+                                           const float *ab, int n) {
+    const float M = fmaxf(ma, mb);
+    const float Mc = M == kNegInfD ? 0.f : M;
+    const float fa = __builtin_amdgcn_exp2f(ma - Mc), fb = __builtin_amdgcn_exp2f(mb - Mc);
+    la = la * fa + lb * fb;
+    for (int i = 0; i < n; i++)
+        aa[i] = aa[i] * fa + ab[i] * fb;
+    ma = M;
+}
+
+template <int D, int GH>
+__global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeArgs a) {
+    constexpr int DE = D / 8;            // d values per lane
+    constexpr int DW = DE / 2;           // 32-bit words per lane (2 bf16 each)
+    constexpr int NV = DE / 8;           // 16-byte loads per lane per row
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int e = lane & 7, sid = wave * 8 + (lane >> 3);
+
+    // work item -> (branch, row, kv head, head group, chunk)
+    const int per_row = a.hkv * a.nhg;
+    int item = blockIdx.x;
+    const bool global = item >= a.n_local_items;
+    if (global)
+        item -= a.n_local_items;
+    const int nch = global ? a.chunks_global : a.chunks_local;
+    const int c = item % nch;
+    const int rest = item / nch;
+    const int hgi = rest % a.nhg;
+    const int kvh = (rest / a.nhg) % a.hkv;
+    const int row = rest / per_row;              // sequence (local) or rank (global)
+    int b = row;
+    if (global) {
+        if (row >= a.n_act[0])
+            return;
+        b = a.act[row];
+    }
+    const int64_t base = a.cu[b];
+    const int L = a.cu[b + 1] - (int)base;
+    const int lo = global ? 0 : max(0, L - a.window);
+    const int k0 = lo + c * a.kc;
+    const int k1 = min(L, k0 + a.kc);
+    if (k0 >= k1)
+        return;                                  // a chunk past this sequence's keys
+    // this item's partials: [item][GH][m, l, acc[D]]
+    float *out_part = (global ? a.part_global : a.part_local) + (int64_t)item * GH * (D + 2);
+    const uint16_t *kc_ = global ? a.k_g : a.k;
+    const uint16_t *vc_ = global ? a.v_g : a.v;
+    const uint16_t *qv = global ? a.q_g : a.q;
+    const int h0 = kvh * a.group + hgi * GH;     // first query head of the group
+
+    // Query slices (bf16 pairs) of the GH heads.
+    uint32_t q2[GH][DW];
+#pragma unroll
+    for (int hh = 0; hh < GH; hh++) {
+        const uint32_t *qp = (const uint32_t *)(qv + ((int64_t)b * a.hq + h0 + hh) * D + e * DE);
+#pragma unroll
+        for (int i = 0; i < DW; i++)
+            q2[hh][i] = qp[i];
+    }
+    float m[GH], l[GH], acc[GH][DE];
+#pragma unroll
+    for (int hh = 0; hh < GH; hh++) {
+        m[hh] = kNegInfD;
+        l[hh] = 0.f;
+#pragma unroll
+        for (int i = 0; i < DE; i++)
+            acc[hh][i] = 0.f;
+    }
+
+    const int64_t row_stride = (int64_t)a.hkv * D;    // elements between cached tokens
+    const uint16_t *kbase = kc_ + (base * a.hkv + kvh) * (int64_t)D + e * DE;
+    const uint16_t *vbase = vc_ + (base * a.hkv + kvh) * (int64_t)D + e * DE;
+    auto load_row = [&](const uint16_t *p, int j, u32x4d (&r)[NV]) {
+#pragma unroll
+        for (int i = 0; i < NV; i++)
+            r[i] = *(const u32x4d *)(p + (int64_t)j * row_stride + i * 8);
+    };
+
+    // Each stream (8 lanes) walks keys k0 + sid, k0 + sid + 32, ...
+    int j = k0 + sid;
+    u32x4d kr[NV], vr[NV];
+    if (j < k1) {
+        load_row(kbase, j, kr);
+        load_row(vbase, j, vr);
+    }
+    for (; j < k1; j += kStreams) {
+        u32x4d kn[NV], vn[NV];
+        const int jn = j + kStreams;
+        if (jn < k1) {
+            load_row(kbase, jn, kn);
+            load_row(vbase, jn, vn);
+        }
+        // scores of the GH heads for key j (reduced over the 8 lanes)
+        float s[GH];
+#pragma unroll
+        for (int hh = 0; hh < GH; hh++) {
+            float d0 = 0.f;
+#pragma unroll
+            for (int i = 0; i < DW; i++) {
+                const uint32_t kw = kr[i / 4][i % 4];
+                d0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2d, q2[hh][i]),
+                                                    __builtin_bit_cast(bf16x2d, kw), d0, false);
+            }
+            d0 += __shfl_xor(d0, 1, 64);
+            d0 += __shfl_xor(d0, 2, 64);
+            d0 += __shfl_xor(d0, 4, 64);
+            s[hh] = d0 * a.scale_log2;
+        }
+        float vf[DE];
+#pragma unroll
+        for (int i = 0; i < DW; i++) {
+            const uint32_t vw = vr[i / 4][i % 4];
+            vf[2 * i] = bf16_lo(vw);
+            vf[2 * i + 1] = bf16_hi(vw);
+        }
+#pragma unroll
+        for (int hh = 0; hh < GH; hh++) {
+            if (s[hh] > m[hh] + kLazyD) {
+                // the running max moves (always on the first key)
+                const float alpha = __builtin_amdgcn_exp2f(m[hh] - s[hh]);
+                l[hh] *= alpha;
+#pragma unroll
+                for (int i = 0; i < DE; i++)
+                    acc[hh][i] *= alpha;
+                m[hh] = s[hh];
+            }
+            const float p = __builtin_amdgcn_exp2f(s[hh] - m[hh]);
+            l[hh] += p;
+#pragma unroll
+            for (int i = 0; i < DE; i++)
+                acc[hh][i] = fmaf(p, vf[i], acc[hh][i]);
+        }
+#pragma unroll
+        for (int i = 0; i < NV; i++) {
+            kr[i] = kn[i];
+            vr[i] = vn[i];
+        }
+    }
+
+    // Merge the 8 streams of the wave (lanes with the same e), then the waves.
+#pragma unroll
+    for (int hh = 0; hh < GH; hh++) {
+#pragma unroll
+        for (int sh = 8; sh < 64; sh <<= 1) {
+            float mo = __shfl_xor(m[hh], sh, 64), lo_ = __shfl_xor(l[hh], sh, 64);
+            float ao[DE];
+#pragma unroll
+            for (int i = 0; i < DE; i++)
+                ao[i] = __shfl_xor(acc[hh][i], sh, 64);
+            merge_into(m[hh], l[hh], mo, lo_, acc[hh], ao, DE);
+        }
+    }
+    __shared__ float s_m[4][GH], s_l[4][GH];
+    __shared__ float s_acc[4][GH][D];
+    if (lane < 8) {
+#pragma unroll
+        for (int hh = 0; hh < GH; hh++) {
+            if (lane == 0) {
+                s_m[wave][hh] = m[hh];
+                s_l[wave][hh] = l[hh];
+            }
+#pragma unroll
+            for (int i = 0; i < DE; i++)
+                s_acc[wave][hh][e * DE + i] = acc[hh][i];
+        }
+    }
+    __syncthreads();
+    // thread t < GH * D: head t / D, element t % D
+    for (int t = tid; t < GH * D; t += kDecThreads) {
+        const int hh = t / D, x = t % D;
+        float M = s_m[0][hh], Lw = s_l[0][hh], A = s_acc[0][hh][x];
+        for (int w2 = 1; w2 < 4; w2++) {
+            float mb = s_m[w2][hh], lb = s_l[w2][hh];
+            const float ab = s_acc[w2][hh][x];
+            merge_into(M, Lw, mb, lb, &A, &ab, 1);
+        }
+        float *op = out_part + hh * (D + 2);
+        op[2 + x] = A;
+        if (x == 0) {
+            op[0] = M;
+            op[1] = Lw;
+        }
+    }
+}
+
+// One workgroup per sequence; wave w takes heads w, w+4, ...; each lane D/64
+// elements.
+template <int D>
+__global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a) {
+    constexpr int PE = D / 64;
+    const int b = blockIdx.x;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int L = a.cu[b + 1] - a.cu[b];
+    // chunks of this sequence (clamped to the planned slots: max_seqlen bounds L)
+    const int n_loc = min((min(L, a.window) + a.kc - 1) / a.kc, a.chunks_local);
+    const int n_glb = min((L + a.kc - 1) / a.kc, a.chunks_global);
+    const int r = a.rank_of[b];
+    const float p = a.gate[b];
+    // merged (O / l) of one branch for head h, this lane's elements
+    auto branch = [&](const float *parts, int row, int nch, int h, int chunks_stride, float (&o)[PE]) {
+        const int kvh = h / a.group, hg = (h % a.group) / a.gh, hh = (h % a.group) % a.gh;
+        float M = kNegInfD, Lw = 0.f;
+        float A[PE];
+#pragma unroll
+        for (int i = 0; i < PE; i++)
+            A[i] = 0.f;
+        for (int c = 0; c < nch; c++) {
+            const int64_t item = (((int64_t)row * a.hkv + kvh) * a.nhg + hg) * chunks_stride + c;
+            const float *pp = parts + (item * a.gh + hh) * (D + 2);
+            float mb = pp[0], lb = pp[1];
+            float ab[PE];
+#pragma unroll
+            for (int i = 0; i < PE; i++)
+                ab[i] = pp[2 + lane * PE + i];
+            merge_into(M, Lw, mb, lb, A, ab, PE);
+        }
+        const float inv = Lw > 0.f ? 1.f / Lw : 0.f;
+#pragma unroll
+        for (int i = 0; i < PE; i++)
+            o[i] = A[i] * inv;
+    };
+    auto norm = [&](float (&o)[PE], const float *gain, int h) {
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < PE; i++)
+            ss = fmaf(o[i], o[i], ss);
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1)
+            ss += __shfl_xor(ss, sh, 64);
+        const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
+#pragma unroll
+        for (int i = 0; i < PE; i++)
+            o[i] = o[i] * rn * (gain ? gain[h * D + lane * PE + i] : 1.f);
+    };
+    for (int h = wave; h < a.hq; h += 4) {
+        float ol[PE];
+        branch(a.part_local, b, n_loc, h, a.chunks_local, ol);
+        norm(ol, a.gain_local, h);
+        if (r >= 0) {
+            float og[PE];
+            branch(a.part_global, r, n_glb, h, a.chunks_global, og);
+            norm(og, a.gain_global, h);
+#pragma unroll
+            for (int i = 0; i < PE; i++)
+                ol[i] = (1.f - p) * ol[i] + p * og[i];
+        }
+        uint16_t *op = a.out + ((int64_t)b * a.hq + h) * D + lane * PE;
+#pragma unroll
+        for (int i = 0; i < PE; i++)
+            op[i] = __builtin_bit_cast(uint16_t, (__bf16)ol[i]);
+    }
+}
+
+template <int D, int GH>
+hipError_t launch_attn_gh(const DecodeArgs &a, hipStream_t s) {
+    const int grid = a.n_local_items + a.n_global_items;
+    if (grid > 0)
+        hipLaunchKernelGGL((decode_attn_kernel<D, GH>), dim3(grid), dim3(kDecThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_attn_d(const DecodeArgs &a, hipStream_t s) {
+    if (a.gh == 4)
+        return launch_attn_gh<D, 4>(a, s);
+    if (a.gh == 2)
+        return launch_attn_gh<D, 2>(a, s);
+    return launch_attn_gh<D, 1>(a, s);
+}
+
+}  // namespace
+
+hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const float *thr_dev,
+                         hipStream_t s) {
+    hipLaunchKernelGGL(decode_select_kernel, dim3(1), dim3(1024), 0, s, a.num_seqs, a.gate, mode,
+                       thr_host, thr_dev, a.act, a.rank_of, a.n_act);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    e = a.head_dim == 128 ? launch_attn_d<128>(a, s) : launch_attn_d<64>(a, s);
+    if (e != hipSuccess)
+        return e;
+    if (a.head_dim == 128)
+        hipLaunchKernelGGL((decode_combine_kernel<128>), dim3(a.num_seqs), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL((decode_combine_kernel<64>), dim3(a.num_seqs), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace logo

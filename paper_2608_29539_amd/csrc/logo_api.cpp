@@ -159,6 +159,45 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
     return w;
 }
 
+// Decoding: keys per chunk (a multiple of 32, at least 256, at most 128
+// chunks per cache), query heads per work item (the largest of 4, 2, 1
+// dividing the group), and the workspace of the partial results.
+struct DecodePlan {
+    int kc, gh, nhg, chunks_local, chunks_global;
+    long long n_local_items, n_global_items;
+    size_t act, rank_of, n_act, part_local, part_global, total;
+};
+DecodePlan decode_plan(const logo_problem *p) {
+    DecodePlan d;
+    const long long maxL = p->max_seqlen > 0 ? p->max_seqlen : 1;
+    long long kc = (maxL + 127) / 128;
+    kc = ((kc + 31) / 32) * 32;
+    d.kc = (int)(kc < 256 ? 256 : kc);
+    const int g = p->num_q_heads / p->num_kv_heads;
+    d.gh = g % 4 == 0 ? 4 : (g % 2 == 0 ? 2 : 1);
+    d.nhg = g / d.gh;
+    const long long wl = maxL < p->window ? maxL : p->window;
+    d.chunks_local = (int)((wl + d.kc - 1) / d.kc);
+    d.chunks_global = (int)((maxL + d.kc - 1) / d.kc);
+    const long long per_row = (long long)p->num_kv_heads * d.nhg;
+    d.n_local_items = (long long)p->num_seqs * per_row * d.chunks_local;
+    d.n_global_items = (long long)p->num_seqs * per_row * d.chunks_global;
+    const size_t slot = sizeof(float) * (size_t)d.gh * (p->head_dim + 2);
+    size_t off = 0;
+    d.act = off;
+    off += align_up(sizeof(int32_t) * (size_t)p->num_seqs);
+    d.rank_of = off;
+    off += align_up(sizeof(int32_t) * (size_t)p->num_seqs);
+    d.n_act = off;
+    off += align_up(sizeof(int32_t));
+    d.part_local = off;
+    off += align_up(slot * (size_t)d.n_local_items);
+    d.part_global = off;
+    off += align_up(slot * (size_t)d.n_global_items);
+    d.total = off;
+    return d;
+}
+
 logo_status check_ws(void *ws, size_t ws_bytes, size_t need) {
     if (need == 0)
         return LOGO_OK;
@@ -453,6 +492,7 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_SELECT: return select_ws(p).total;
     case LOGO_ENTRY_GLOBAL: return global_ws(p, cap).total;
     case LOGO_ENTRY_FWD: return fwd_ws(p, cap).total;
+    case LOGO_ENTRY_DECODE: return decode_plan(p).total;
     case LOGO_ENTRY_LOCAL:
     case LOGO_ENTRY_COMBINE:
     case LOGO_ENTRY_DENSE: return 0;
@@ -582,6 +622,78 @@ logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
         return LOGO_ERR_UNSUPPORTED;
     hipStream_t s = (hipStream_t)stream;
     return hip_status(launch_attention(kModeDense, kEpiRaw, p->head_dim, a, (int)grid, s), s);
+}
+
+logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                        const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                        const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                        float threshold, const float *thr_dev, const float *gain_local,
+                        const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
+                        int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (!q || !k || !v || !gate || !out)
+        return LOGO_ERR_NULL;
+    if (mode == LOGO_SEL_THRESHOLD) {
+        if (std::isnan(threshold))
+            return LOGO_ERR_ARG;
+    } else if (mode == LOGO_SEL_THRESHOLD_DEVICE) {
+        if (!thr_dev)
+            return LOGO_ERR_NULL;
+    } else {
+        return LOGO_ERR_ARG;
+    }
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    if (p->cu_seqlens_host)
+        for (int b = 0; b < p->num_seqs; b++)
+            if (p->cu_seqlens_host[b + 1] - p->cu_seqlens_host[b] < 1)
+                return LOGO_ERR_SHAPE;
+    if ((long long)p->num_seqs * p->num_q_heads >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    const DecodePlan d = decode_plan(p);
+    if (d.n_local_items + d.n_global_items >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    st = check_ws(ws, ws_bytes, d.total);
+    if (st != LOGO_OK)
+        return st;
+    char *base = (char *)ws;
+    DecodeArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.q_g = q_g ? q_g : q;
+    a.k_g = k_g ? k_g : k;
+    a.v_g = v_g ? v_g : v;
+    a.cu = p->cu_seqlens;
+    a.gate = gate;
+    a.gain_local = gain_local;
+    a.gain_global = gain_global;
+    a.eps = eps;
+    a.scale_log2 = scale_log2(p);
+    a.num_seqs = p->num_seqs;
+    a.hq = p->num_q_heads;
+    a.hkv = p->num_kv_heads;
+    a.group = p->num_q_heads / p->num_kv_heads;
+    a.head_dim = p->head_dim;
+    a.window = p->window;
+    a.gh = d.gh;
+    a.nhg = d.nhg;
+    a.kc = d.kc;
+    a.chunks_local = d.chunks_local;
+    a.chunks_global = d.chunks_global;
+    a.n_local_items = (int32_t)d.n_local_items;
+    a.n_global_items = (int32_t)d.n_global_items;
+    a.act = active ? active : (int32_t *)(base + d.act);
+    a.rank_of = (int32_t *)(base + d.rank_of);
+    a.n_act = n_active ? n_active : (int32_t *)(base + d.n_act);
+    a.part_local = (float *)(base + d.part_local);
+    a.part_global = (float *)(base + d.part_global);
+    a.out = out;
+    hipStream_t s = (hipStream_t)stream;
+    return hip_status(launch_decode(a, (int)mode, threshold, thr_dev, s), s);
 }
 
 }  // extern "C"

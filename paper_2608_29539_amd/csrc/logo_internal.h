@@ -147,6 +147,28 @@ hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
                          int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s);
 
+// One decoding step (decode.hip).  Work items: local (sequence, KV head,
+// head group, chunk) then global (selected rank, KV head, head group,
+// chunk); partials [item][gh][m, l, acc[d]].
+struct DecodeArgs {
+    const uint16_t *q, *k, *v;       // q: [B][Hq][d] new tokens; k, v: caches [N][Hkv][d]
+    const uint16_t *q_g, *k_g, *v_g; // global-branch tensors (aliases when not given)
+    const int32_t *cu;               // [B+1] cache boundaries
+    const float *gate;               // [B] gate of the new tokens
+    const float *gain_local, *gain_global;
+    float eps, scale_log2;
+    int32_t num_seqs, hq, hkv, group, head_dim, window;
+    int32_t gh, nhg;                 // query heads per item, head groups per KV head
+    int32_t kc;                      // keys per chunk
+    int32_t chunks_local, chunks_global;
+    int32_t n_local_items, n_global_items;
+    int32_t *act, *rank_of, *n_act;  // selected sequences (compacted), rank or -1, count
+    float *part_local, *part_global;
+    uint16_t *out;                   // [B][Hq][d] bf16
+};
+hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const float *thr_dev,
+                         hipStream_t s);
+
 // One budget-controller step on the device (b_th += gamma sign(F - rho)).
 hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,
                                 float gamma, float *b_th, float *realized, hipStream_t s);

@@ -7,10 +7,12 @@ of the method's arithmetic: it only draws random numbers and encodes them
 fp32).  Everything it returns is a plain numpy array.
 """
 from .logo_inputs import (  # noqa: F401
+    DECODE_WORKLOADS,
     WORKLOADS,
     Workload,
     bf16_bits_from_f32,
     f32_from_bf16_bits,
+    make_decode_inputs,
     make_gate_only,
     make_inputs,
     small_workload,

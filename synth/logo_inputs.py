@@ -117,6 +117,14 @@ WORKLOADS: Dict[str, Workload] = {
 for _w in _ratio_sweep():
     WORKLOADS[_w.name] = _w
 
+#: Decoding workloads: `seqlens` are the KV-cache lengths (each sequence's
+#: last cached row is its new token), `ratio` the expected selected fraction
+#: of the new tokens (gates U(0,1), threshold 1 - ratio).
+DECODE_WORKLOADS: Dict[str, Workload] = {
+    "decode-B16-32k-gqa": Workload("decode-B16-32k-gqa", (32768,) * 16, 32, 8, 128, 1024,
+                                   1.0 / 8, 2001, note="16 caches of 32K tokens"),
+}
+
 
 def _normal_bf16(rng: np.random.Generator, shape, scale: Optional[float]) -> np.ndarray:
     x = rng.standard_normal(size=int(np.prod(shape)), dtype=np.float32)
@@ -193,3 +201,26 @@ def small_workload(seqlens: Sequence[int], hq: int, hkv: int, d: int, window: in
 def expected_selected(seqlens: Sequence[int], ratio: float) -> int:
     """Number of tokens a ratio-mode selection keeps when gate values are distinct."""
     return int(sum(min(T, math.floor(ratio * T)) for T in seqlens))
+
+
+def make_decode_inputs(w: Workload, *, distinct_global: bool = False) -> Dict[str, np.ndarray]:
+    """Inputs of one decoding step: the caches ``k``/``v`` [N,Hkv,d] (N = sum
+    of the cache lengths), the new tokens' queries ``q`` [B,Hq,d] and gates
+    ``gate`` [B] (float32), and ``cu_seqlens`` [B+1] of the caches.  Same
+    seeded streams as ``make_inputs``; with ``distinct_global`` also
+    ``q_g``/``k_g``/``v_g``."""
+    ss = np.random.SeedSequence(w.seed).spawn(4)
+    rq, rk, rv, rg = (np.random.Generator(np.random.PCG64(s)) for s in ss)
+    N, B = w.total_tokens, len(w.seqlens)
+    k = _normal_bf16(rk, (N, w.num_kv_heads, w.head_dim), w.qkv_scale)
+    v = _normal_bf16(rv, (N, w.num_kv_heads, w.head_dim), w.qkv_scale)
+    q = _normal_bf16(rq, (B, w.num_q_heads, w.head_dim), w.qkv_scale)
+    gate = make_gate(rg, (B,), w.gate)
+    cu = np.zeros(B + 1, dtype=np.int32)
+    cu[1:] = np.cumsum(np.asarray(w.seqlens, dtype=np.int64)).astype(np.int32)
+    out = dict(q=q, k=k, v=v, gate=gate, cu_seqlens=cu)
+    if distinct_global:
+        out["q_g"] = _normal_bf16(rq, q.shape, w.qkv_scale)
+        out["k_g"] = _normal_bf16(rk, k.shape, w.qkv_scale)
+        out["v_g"] = _normal_bf16(rv, v.shape, w.qkv_scale)
+    return out

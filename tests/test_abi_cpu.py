@@ -192,3 +192,39 @@ def test_device_threshold_mode_needs_thr_out(lib):
     ws_need = lib.logo_workspace_bytes(p.c, 0, 0)
     assert lib.logo_select(p.c, FAKE, 2, 0.0, 0.0, FAKE, 150, FAKE, None, None, FAKE, ws_need,
                            None) == ERR_NULL
+
+
+def test_decode_validation(lib):
+    """logo_decode rejects bad arguments before any launch."""
+    p = Prob(seqlens=(100, 50), hq=8, hkv=2, d=128, window=16)
+    need = lib.logo_workspace_bytes(p.c, 6, 0)
+    assert need > 0 and need % 256 == 0
+    f = lib.logo_decode
+    args = [p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 0, 0.5, None, None, None, 1e-6, FAKE,
+            None, None, FAKE, need, None]
+
+    def call(**kw):
+        a = list(args)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return f(*a)
+
+    assert call(a1=None) == ERR_NULL                 # q
+    assert call(a7=None) == ERR_NULL                 # gate
+    assert call(a14=None) == ERR_NULL                # out
+    assert call(a9=float("nan")) == ERR_ARG          # NaN threshold
+    assert call(a8=1) == ERR_ARG                     # ratio mode
+    assert call(a8=2) == ERR_NULL                    # device threshold without thr_dev
+    assert call(a13=-1.0) == ERR_ARG                 # eps
+    assert call(a18=need - 1) == ERR_WORKSPACE
+    assert call(a17=None) == ERR_WORKSPACE
+    empty = Prob(seqlens=(10, 0, 5), hq=8, hkv=2, d=128, window=16)
+    need_e = lib.logo_workspace_bytes(empty.c, 6, 0)
+    a = list(args)
+    a[0], a[18] = empty.c, need_e
+    assert f(*a) == ERR_SHAPE                        # a sequence with an empty cache
+    assert f(Prob(d=96).c, *args[1:]) == ERR_UNSUPPORTED
+    # the partial-result slots grow with the cache (chunks of >= 256 keys)
+    big = Prob(seqlens=(32768,) * 4, hq=32, hkv=8, d=128, window=1024)
+    nb = lib.logo_workspace_bytes(big.c, 6, 0)
+    assert 4 * 32 * (128 + 4) * 4 * 4 <= nb < 64 << 20
