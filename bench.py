@@ -152,6 +152,66 @@ def cpu_baseline(x, w, stride: int, log_fn=log):
                        f"selection over the full sequence; {dt:.1f}s fp64")}
 
 
+def bench_decode(pk, torch, name: str, steps: int, warmup: int):
+    """One decoding step (logo_decode) on a decoding workload, timed with HIP
+    events on the current stream.  Algorithmic bytes: each new token's local
+    window of the cache, the whole cache for a selected token (with aliased
+    global tensors the window is part of it), the queries, gates and the bf16
+    output.  Also timed: the paper's conservative batched policy (any selected
+    row launches the global branch for every row, i.e. threshold -inf)."""
+    import synth
+    w = synth.DECODE_WORKLOADS[name]
+    x = synth.make_decode_inputs(w)
+    dev = {}
+    for k_, v_ in x.items():
+        t = torch.from_numpy(np.ascontiguousarray(v_.view(np.int16) if v_.dtype == np.uint16
+                                                  else v_)).cuda()
+        dev[k_] = t.view(torch.bfloat16) if v_.dtype == np.uint16 else t
+    prob = pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
+                      cu_seqlens_host=x["cu_seqlens"])
+    B, Hq, Hkv, d = len(w.seqlens), w.num_q_heads, w.num_kv_heads, w.head_dim
+    thr = 1.0 - w.ratio
+    out = torch.empty((B, Hq, d), dtype=torch.bfloat16, device="cuda")
+    act = torch.empty(B, dtype=torch.int32, device="cuda")
+    n_act = torch.empty(1, dtype=torch.int32, device="cuda")
+    ws = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_DECODE), dtype=torch.uint8,
+                     device="cuda")
+
+    def timed(threshold):
+        def call():
+            pk.logo_decode(prob, dev["q"], dev["k"], dev["v"], dev["gate"], threshold=threshold,
+                           out=out, active=act, n_active=n_act, ws=ws)
+        for _ in range(warmup):
+            call()
+        torch.cuda.synchronize()
+        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s0.record()
+        for _ in range(steps):
+            call()
+        s1.record()
+        torch.cuda.synchronize()
+        return s0.elapsed_time(s1) / steps, int(n_act.cpu()[0])
+
+    t_all, n_all = timed(-float("inf"))
+    t_logo, n_sel = timed(thr)
+    L = np.diff(x["cu_seqlens"]).astype(np.int64)
+    z = x["gate"] > np.float32(thr)
+    rows = np.where(z, L, np.minimum(L, w.window)).sum()
+    row_bytes = 2 * Hkv * d * 2                       # one cached token's K and V
+    alg = float(rows * row_bytes + B * Hq * d * 2 * 2 + B * 4)
+    gbs = alg / (t_logo * 1e-3) / 1e9
+    log(f"decode {name}: {t_logo * 1e3:.1f} us/step ({n_sel}/{B} selected), "
+        f"{gbs:.0f} GB/s algorithmic; every row global {t_all * 1e3:.1f} us")
+    return {"workload": name, "batch": B, "cache_lens": sorted(set(int(t) for t in L)),
+            "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "window": w.window,
+            "threshold": thr, "n_selected": n_sel, "us_per_step": round(t_logo * 1e3, 2),
+            "algorithmic_bytes": alg,
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4)},
+            "conservative_policy_us": round(t_all * 1e3, 2),
+            "speedup_vs_conservative": round(t_all / t_logo, 3)}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -167,6 +227,8 @@ def main(argv=None):
     ap.add_argument("--no-dense", action="store_true", help="skip the dense baseline")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the threshold-mode run and the clock query")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decoding-step measurement")
+    ap.add_argument("--decode-workload", default="decode-B16-32k-gqa")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of MIB MiB "
                          "(the reference kernel for scaling FETCH_SIZE / WRITE_SIZE)")
@@ -350,6 +412,10 @@ def main(argv=None):
                 "flops_per_launch": fl * p_global,
                 "duration_ms": round(stage_ms["global"], 4)}
 
+    decode = None
+    if not args.no_decode:
+        decode = bench_decode(pk, torch, args.decode_workload, steps=50, warmup=20)
+
     cpu = None
     if not args.no_cpu:
         stride = args.cpu_stride
@@ -389,6 +455,7 @@ def main(argv=None):
         "cpu_baseline": cpu,
         "select_hbm": select_hbm,
         "threshold_mode": thr_mode,
+        "decode": decode,
         "gpu": gpu_info(torch, busy=lambda: [step() for _ in range(600)])
                if not args.no_extra else None,
     }

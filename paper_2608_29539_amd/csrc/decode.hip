@@ -269,43 +269,80 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
     }
 }
 
-// One workgroup per sequence; wave w takes heads w, w+4, ...; each lane D/64
-// elements.
+// One wave per (sequence, query head), four per workgroup.  A branch's
+// chunks are merged in one pass: the largest chunk maximum first (lane c
+// holds chunk c), then every chunk's weight 2^(m_c - M) independently, so
+// the weighted sum over chunks has all its loads in flight.  Each lane owns
+// D/64 output elements.  The chunk count of a branch is at most 128.
+constexpr int kMaxChunks = 128;
+
 template <int D>
 __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a) {
     constexpr int PE = D / 64;
-    const int b = blockIdx.x;
+    __shared__ float s_w[4][kMaxChunks];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int job = blockIdx.x * 4 + wave;
+    if (job >= a.num_seqs * a.hq)
+        return;                                   // whole wave: no barrier below
+    const int b = job / a.hq, h = job % a.hq;
     const int L = a.cu[b + 1] - a.cu[b];
     // chunks of this sequence (clamped to the planned slots: max_seqlen bounds L)
     const int n_loc = min((min(L, a.window) + a.kc - 1) / a.kc, a.chunks_local);
     const int n_glb = min((L + a.kc - 1) / a.kc, a.chunks_global);
     const int r = a.rank_of[b];
     const float p = a.gate[b];
-    // merged (O / l) of one branch for head h, this lane's elements
-    auto branch = [&](const float *parts, int row, int nch, int h, int chunks_stride, float (&o)[PE]) {
-        const int kvh = h / a.group, hg = (h % a.group) / a.gh, hh = (h % a.group) % a.gh;
-        float M = kNegInfD, Lw = 0.f;
+    const int kvh = h / a.group, hg = (h % a.group) / a.gh, hh = (h % a.group) % a.gh;
+    float *w = s_w[wave];
+    // O / l of one branch (row = sequence or selected rank) for this lane's elements
+    auto branch = [&](const float *parts, int row, int nch, int chunks_stride, float (&o)[PE]) {
+        const int64_t item0 = (((int64_t)row * a.hkv + kvh) * a.nhg + hg) * chunks_stride;
+        auto slot = [&](int c) { return parts + ((item0 + c) * a.gh + hh) * (D + 2); };
+        float mc[2], lc[2];
+        float M = kNegInfD;
+#pragma unroll
+        for (int i = 0; i < 2; i++) {
+            const int c = lane + 64 * i;
+            mc[i] = c < nch ? slot(c)[0] : kNegInfD;
+            lc[i] = c < nch ? slot(c)[1] : 0.f;
+            M = fmaxf(M, mc[i]);
+        }
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1)
+            M = fmaxf(M, __shfl_xor(M, sh, 64));
+        const float Mc = M == kNegInfD ? 0.f : M;
+        float lsum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 2; i++) {
+            const int c = lane + 64 * i;
+            const float wc = c < nch ? __builtin_amdgcn_exp2f(mc[i] - Mc) : 0.f;
+            if (c < nch)
+                w[c] = wc;
+            lsum = fmaf(wc, lc[i], lsum);
+        }
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1)
+            lsum += __shfl_xor(lsum, sh, 64);
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
         float A[PE];
 #pragma unroll
         for (int i = 0; i < PE; i++)
             A[i] = 0.f;
+#pragma unroll 4
         for (int c = 0; c < nch; c++) {
-            const int64_t item = (((int64_t)row * a.hkv + kvh) * a.nhg + hg) * chunks_stride + c;
-            const float *pp = parts + (item * a.gh + hh) * (D + 2);
-            float mb = pp[0], lb = pp[1];
-            float ab[PE];
+            const float wc = w[c];
+            const float *pp = slot(c) + 2 + lane * PE;
 #pragma unroll
             for (int i = 0; i < PE; i++)
-                ab[i] = pp[2 + lane * PE + i];
-            merge_into(M, Lw, mb, lb, A, ab, PE);
+                A[i] = fmaf(wc, pp[i], A[i]);
         }
-        const float inv = Lw > 0.f ? 1.f / Lw : 0.f;
+        __builtin_amdgcn_wave_barrier();
+        const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
 #pragma unroll
         for (int i = 0; i < PE; i++)
             o[i] = A[i] * inv;
     };
-    auto norm = [&](float (&o)[PE], const float *gain, int h) {
+    auto norm = [&](float (&o)[PE], const float *gain) {
         float ss = 0.f;
 #pragma unroll
         for (int i = 0; i < PE; i++)
@@ -318,23 +355,21 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
         for (int i = 0; i < PE; i++)
             o[i] = o[i] * rn * (gain ? gain[h * D + lane * PE + i] : 1.f);
     };
-    for (int h = wave; h < a.hq; h += 4) {
-        float ol[PE];
-        branch(a.part_local, b, n_loc, h, a.chunks_local, ol);
-        norm(ol, a.gain_local, h);
-        if (r >= 0) {
-            float og[PE];
-            branch(a.part_global, r, n_glb, h, a.chunks_global, og);
-            norm(og, a.gain_global, h);
-#pragma unroll
-            for (int i = 0; i < PE; i++)
-                ol[i] = (1.f - p) * ol[i] + p * og[i];
-        }
-        uint16_t *op = a.out + ((int64_t)b * a.hq + h) * D + lane * PE;
+    float ol[PE];
+    branch(a.part_local, b, n_loc, a.chunks_local, ol);
+    norm(ol, a.gain_local);
+    if (r >= 0) {
+        float og[PE];
+        branch(a.part_global, r, n_glb, a.chunks_global, og);
+        norm(og, a.gain_global);
 #pragma unroll
         for (int i = 0; i < PE; i++)
-            op[i] = __builtin_bit_cast(uint16_t, (__bf16)ol[i]);
+            ol[i] = (1.f - p) * ol[i] + p * og[i];
     }
+    uint16_t *op = a.out + ((int64_t)b * a.hq + h) * D + lane * PE;
+#pragma unroll
+    for (int i = 0; i < PE; i++)
+        op[i] = __builtin_bit_cast(uint16_t, (__bf16)ol[i]);
 }
 
 template <int D, int GH>
@@ -366,10 +401,11 @@ hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const fl
     e = a.head_dim == 128 ? launch_attn_d<128>(a, s) : launch_attn_d<64>(a, s);
     if (e != hipSuccess)
         return e;
+    const int grid = (a.num_seqs * a.hq + 3) / 4;
     if (a.head_dim == 128)
-        hipLaunchKernelGGL((decode_combine_kernel<128>), dim3(a.num_seqs), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((decode_combine_kernel<128>), dim3(grid), dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL((decode_combine_kernel<64>), dim3(a.num_seqs), dim3(256), 0, s, a);
+        hipLaunchKernelGGL((decode_combine_kernel<64>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
