@@ -6,14 +6,18 @@ with it.  The arithmetic lives in ``logo_oracle.c`` (plain C, fp64, OpenMP);
 this module only builds that file with gcc and marshals numpy arrays.
 """
 from .oracle import (  # noqa: F401
+    LP,
     SEL_RATIO,
+    SO,
     SEL_THRESHOLD,
     attn_rows,
+    branch_transform,
     budget_update,
     build,
     contextnorm,
     decode,
     fuse,
+    gate_proj,
     library_path,
     logo_fwd,
     logo_rows,

@@ -32,6 +32,8 @@
  *     selected) global attention over the KV cache, fused as above
  *                                                         (Sec. 3.3 and App. B,
  *                                                          Autoregressive Decoding)
+ *   - the gate projection p = sigmoid(x . w_g)            (Sec. 3.2, Eq. gate-routing)
+ *   - the branch transforms LP (U A) and SO (U * s + b)   (Sec. 3.2, Eq. branch-transform)
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *   - positions are 0-based: key j is visible to query i iff j <= i (global)
@@ -500,4 +502,53 @@ int64_t oracle_decode(const uint16_t *q_new, const uint16_t *q_g_new, const uint
     free(nl);
     free(ng);
     return n_sel;
+}
+
+/*
+ * Gate projection (Sec. 3.2, Eq. gate-routing): p_t = sigmoid(x_t . w_g) for
+ * every token, x [N][dm] and w_g [dm] bf16, the dot product and the sigmoid
+ * in double, p rounded once to fp32.
+ */
+void oracle_gate_proj(const uint16_t *x, const uint16_t *w_g, int64_t N, int dm, float *p_out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < N; t++) {
+        double dot = 0.0;
+        for (int c = 0; c < dm; c++)
+            dot += bf16_to_double(x[t * dm + c]) * bf16_to_double(w_g[c]);
+        p_out[t] = (float)(1.0 / (1.0 + exp(-dot)));
+    }
+}
+
+/*
+ * Branch transform phi_{U,h} from local to global representations (Sec.
+ * 3.2, Eq. branch-transform), per head h of u [N][H][d] (bf16):
+ *   kind 0 (LP): out[t][h][j] = sum_c u[t][h][c] * A[h][c][j]   (A bf16 [H][d][d])
+ *   kind 1 (SO): out[t][h][j] = u[t][h][j] * s[h][j] + b[h][j] (s, b fp32 [H][d])
+ * for the token rows listed in rows[0..n_rows) (all N tokens when rows is
+ * NULL, n_rows = N).  out is [n_rows][H][d] in double (not rounded).
+ */
+void oracle_branch_transform(const uint16_t *u, int H, int d, int kind, const uint16_t *A,
+                             const float *s, const float *b, const int32_t *rows,
+                             int64_t n_rows, double *out)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < n_rows; r++) {
+        const int64_t t = rows ? rows[r] : r;
+        for (int h = 0; h < H; h++) {
+            const uint16_t *ur = u + (t * H + h) * (int64_t)d;
+            double *o = out + (r * H + h) * (int64_t)d;
+            for (int j = 0; j < d; j++) {
+                if (kind == 0) {
+                    double acc = 0.0;
+                    for (int c = 0; c < d; c++)
+                        acc += bf16_to_double(ur[c]) *
+                               bf16_to_double(A[((int64_t)h * d + c) * d + j]);
+                    o[j] = acc;
+                } else {
+                    o[j] = bf16_to_double(ur[j]) * (double)s[h * d + j] + (double)b[h * d + j];
+                }
+            }
+        }
+    }
 }

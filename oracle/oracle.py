@@ -70,6 +70,8 @@ def _load():
     lib.oracle_decode.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, f32,
                                   P, P, f64, P, P, P, P]
     lib.oracle_decode.restype = i64
+    lib.oracle_gate_proj.argtypes = [P, P, i64, i32, P]
+    lib.oracle_branch_transform.argtypes = [P, i32, i32, i32, P, P, P, P, i64, P]
     _lib = lib
     return lib
 
@@ -244,3 +246,31 @@ def decode(q_new, k, v, gate_new, cu_cache, window: int, threshold: float, *, q_
         _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)), float(eps),
         _ptr(ol), _ptr(og), _ptr(out), _ptr(z))
     return dict(out=out, o_local=ol, o_global=og, z=z.astype(bool), n_sel=int(n))
+
+
+def gate_proj(x, w_g) -> np.ndarray:
+    """p = sigmoid(x . w_g) per token (Eq. gate-routing), fp32: x [N, dm] and
+    w_g [dm] are bf16 bits."""
+    x, w_g = _c(x, np.uint16), _c(w_g, np.uint16)
+    N, dm = x.shape
+    p = np.empty(N, dtype=np.float32)
+    _load().oracle_gate_proj(_ptr(x), _ptr(w_g), N, dm, _ptr(p))
+    return p
+
+
+LP, SO = 0, 1
+
+
+def branch_transform(u, kind: int, *, A=None, s=None, b=None, rows=None) -> np.ndarray:
+    """Eq. branch-transform for the rows ``rows`` (all when None): LP with
+    A [H, d, d] (bf16 bits) or SO with s, b [H, d] (fp32); fp64 result
+    [len(rows), H, d]."""
+    u = _c(u, np.uint16)
+    N, H, d = u.shape
+    rows = _c(rows, np.int32)
+    n = N if rows is None else rows.size
+    out = np.empty((n, H, d), dtype=np.float64)
+    _load().oracle_branch_transform(_ptr(u), H, d, int(kind), _ptr(_c(A, np.uint16)),
+                                    _ptr(_c(s, np.float32)), _ptr(_c(b, np.float32)),
+                                    _ptr(rows), n, _ptr(out))
+    return out

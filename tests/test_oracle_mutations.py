@@ -60,6 +60,13 @@ MUTATIONS = {
                                 "(1.0 - p) * l + p * ng[b * row + e]"),
     "decode_cache_offset_dropped": ("const int64_t base = cu[b];\n            const int64_t L",
                                     "const int64_t base = 0;\n            const int64_t L"),
+    "gate_sigmoid_sign": ("p_out[t] = (float)(1.0 / (1.0 + exp(-dot)));",
+                          "p_out[t] = (float)(1.0 / (1.0 + exp(dot)));"),
+    "gate_weight_index": ("* bf16_to_double(w_g[c]);", "* bf16_to_double(w_g[0]);"),
+    "lp_matrix_transposed": ("A[((int64_t)h * d + c) * d + j]", "A[((int64_t)h * d + j) * d + c]"),
+    "lp_matrix_ignores_head": ("A[((int64_t)h * d + c) * d + j]", "A[((int64_t)0 * d + c) * d + j]"),
+    "so_offset_sign": ("+ (double)b[h * d + j];", "- (double)b[h * d + j];"),
+    "transform_rows_ignored": ("const int64_t t = rows ? rows[r] : r;", "const int64_t t = r;"),
 }
 
 

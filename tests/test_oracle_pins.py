@@ -521,3 +521,69 @@ def test_decode_zero_query_closed_form(oracle_lib):
     assert r["z"].tolist() == [False, True]
     np.testing.assert_allclose(r["out"][0, 0], rms(loc[0]), atol=1e-14)
     np.testing.assert_allclose(r["out"][1, 0], 0.25 * rms(loc[1]) + 0.75 * rms(glo), atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Gate projection (Eq. gate-routing) and branch transforms (Eq.
+# branch-transform).
+# ---------------------------------------------------------------------------
+def test_gate_proj_hand_and_init(oracle_lib):
+    """Hand values: x.w = 0 gives exactly 1/2; x.w = 1 gives 1/(1+e^-1); a zero
+    gate vector (the near-zero initialisation) centres every p at 1/2."""
+    x = bf16(np.array([[1.0, 2.0], [2.0, 0.0], [-3.0, 4.0]], np.float32))
+    w = bf16(np.array([0.5, -0.25], np.float32))
+    p = oracle_lib.gate_proj(x, w)
+    assert p.dtype == np.float32
+    assert p[0] == np.float32(0.5)
+    assert p[1] == np.float32(0.7310585786300049)
+    assert p[2] == np.float32(1.0 / (1.0 + math.exp(2.5)))
+    z = oracle_lib.gate_proj(x, bf16(np.zeros(2, np.float32)))
+    assert (z == np.float32(0.5)).all()
+
+
+def test_gate_proj_bruteforce(oracle_lib):
+    rng = np.random.default_rng(11)
+    x = bf16(np.round(rng.standard_normal((37, 96)) * 16) / 16)
+    w = bf16(np.round(rng.standard_normal(96) * 16) / 64)
+    ref = (1.0 / (1.0 + np.exp(-(wide(x) @ wide(w))))).astype(np.float32)
+    np.testing.assert_array_equal(oracle_lib.gate_proj(x, w), ref)
+
+
+def test_branch_transform_identity_and_permutation(oracle_lib):
+    """Both transforms start as identities (Sec. 3.2): LP with A = I and SO with
+    s = 1, b = 0 return U; a permutation matrix permutes the channels."""
+    rng = np.random.default_rng(12)
+    N, H, d = 9, 3, 8
+    u = bf16(np.round(rng.standard_normal((N, H, d)) * 8) / 8)
+    eye = bf16(np.broadcast_to(np.eye(d, dtype=np.float32), (H, d, d)).copy())
+    np.testing.assert_array_equal(oracle_lib.branch_transform(u, oracle_lib.LP, A=eye), wide(u))
+    ones, zeros = np.ones((H, d), np.float32), np.zeros((H, d), np.float32)
+    np.testing.assert_array_equal(oracle_lib.branch_transform(u, oracle_lib.SO, s=ones, b=zeros),
+                                  wide(u))
+    perm = [rng.permutation(d) for _ in range(H)]
+    P = np.zeros((H, d, d), np.float32)
+    for h in range(H):
+        P[h, perm[h], np.arange(d)] = 1.0          # out[:, j] = u[:, perm[j]]
+    out = oracle_lib.branch_transform(u, oracle_lib.LP, A=bf16(P))
+    for h in range(H):
+        np.testing.assert_array_equal(out[:, h, :], wide(u)[:, h, perm[h]])
+
+
+def test_branch_transform_bruteforce_and_rows(oracle_lib):
+    rng = np.random.default_rng(13)
+    N, H, d = 11, 4, 16
+    u = bf16(np.round(rng.standard_normal((N, H, d)) * 8) / 8)
+    A = bf16(np.round(rng.standard_normal((H, d, d)) * 8) / 64)
+    s = rng.uniform(0.5, 2.0, (H, d)).astype(np.float32)
+    b = rng.standard_normal((H, d)).astype(np.float32)
+    lp = np.stack([wide(u)[:, h, :] @ wide(A)[h] for h in range(H)], axis=1)
+    so = wide(u) * s.astype(np.float64)[None] + b.astype(np.float64)[None]
+    np.testing.assert_allclose(oracle_lib.branch_transform(u, oracle_lib.LP, A=A), lp,
+                               rtol=0, atol=1e-12)
+    np.testing.assert_allclose(oracle_lib.branch_transform(u, oracle_lib.SO, s=s, b=b), so,
+                               rtol=0, atol=1e-12)
+    rows = np.array([10, 0, 7, 7], np.int32)
+    np.testing.assert_allclose(oracle_lib.branch_transform(u, oracle_lib.LP, A=A, rows=rows),
+                               lp[rows], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(oracle_lib.branch_transform(u, oracle_lib.SO, s=s, b=b, rows=rows),
+                               so[rows], rtol=0, atol=1e-12)
