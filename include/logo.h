@@ -277,6 +277,52 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
                         int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream);
 
 /*
+ * logo_gate_proj -- the gate of Eq. gate-routing (Sec. 3.2):
+ * gate_out[t] = sigmoid(x[t] . w_g) for t < n_tokens, in fp32 (bf16 products
+ * accumulated in fp32).  The result is the `gate` input of logo_select /
+ * logo_attn_fwd / logo_decode (both the routing preference and the fusion
+ * weight).
+ *   x          device [n_tokens][d_model] bf16, 16-byte aligned.
+ *   w_g        device [d_model] bf16, 16-byte aligned.
+ *   d_model    a multiple of 8 (LOGO_ERR_UNSUPPORTED otherwise), >= 8.
+ *   gate_out   device [n_tokens] fp32.
+ * Asynchronous on `stream`; nothing is enqueued on error.
+ */
+logo_status logo_gate_proj(int64_t n_tokens, int32_t d_model, const logo_bf16 *x,
+                           const logo_bf16 *w_g, float *gate_out, logo_stream stream);
+
+/* Branch transform kinds of Eq. branch-transform. */
+typedef enum {
+    LOGO_PHI_LP = 0,   /* linear projection U A_h, A_h a d x d matrix per head */
+    LOGO_PHI_SO = 1    /* scale and offset U * s_h + b_h                       */
+} logo_phi_kind;
+
+/*
+ * logo_branch_transform -- the global branch's representation from the local
+ * one, per head (Sec. 3.2, Eq. branch-transform): u_g[t][h] = u[t][h] A[h]
+ * (LP) or u[t][h] * s[h] + b[h] (SO), fp32 arithmetic, one bf16 rounding.
+ * Identity parameters (A = I; s = 1, b = 0) reproduce u exactly.
+ *   n_tokens, num_heads, head_dim   u and u_g are [n_tokens][H][d] bf16,
+ *              d in {64, 128}, 16-byte aligned; u_g must not overlap u.
+ *   kind       LOGO_PHI_LP (A: device [H][d][d] bf16, row c of A[h] maps
+ *              channel c to the output channels) or LOGO_PHI_SO (s, b:
+ *              device [H][d] fp32).
+ *   rows       device [n_rows] int32 token indices (each < n_tokens) or NULL
+ *              for every token (then n_rows must be n_tokens); only the
+ *              listed rows of u_g are written -- e.g. the selected queries
+ *              (sel_idx) of the query-sparse global branch.
+ *   n_rows_dev device int32 or NULL: the number of valid entries of rows when
+ *              it is known only on the device (e.g. &cu_sel[B]); at most
+ *              n_rows are used.
+ * Asynchronous on `stream`; nothing is enqueued on error.
+ */
+logo_status logo_branch_transform(int64_t n_tokens, int32_t num_heads, int32_t head_dim,
+                                  logo_phi_kind kind, const logo_bf16 *u, const logo_bf16 *A,
+                                  const float *s, const float *b, const int32_t *rows,
+                                  int64_t n_rows, const int32_t *n_rows_dev, logo_bf16 *u_g,
+                                  logo_stream stream);
+
+/*
  * logo_budget_update -- one step of the global-budget controller
  * (Sec. 3.2, Eq. threshold-update) on the device, without a host sync:
  *   F    = cu_sel[B] / N, the realized global ratio of the last selection

@@ -15,6 +15,8 @@ from .binding import (  # noqa: F401
     LOGO_ENTRY_GLOBAL,
     LOGO_ENTRY_LOCAL,
     LOGO_ENTRY_SELECT,
+    LOGO_PHI_LP,
+    LOGO_PHI_SO,
     LOGO_SEL_RATIO,
     LOGO_SEL_THRESHOLD,
     LOGO_SEL_THRESHOLD_DEVICE,
@@ -24,10 +26,12 @@ from .binding import (  # noqa: F401
     library,
     library_path,
     logo_attn_fwd,
+    logo_branch_transform,
     logo_budget_update,
     logo_combine,
     logo_decode,
     logo_dense_causal_attn,
+    logo_gate_proj,
     logo_global_attn_sparse_q,
     logo_local_attn,
     logo_pmask_initial_threshold,

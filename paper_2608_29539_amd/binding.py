@@ -25,13 +25,15 @@ LOGO_ENTRY_COMBINE = 3
 LOGO_ENTRY_FWD = 4
 LOGO_ENTRY_DENSE = 5
 LOGO_ENTRY_DECODE = 6
+LOGO_PHI_LP = 0
+LOGO_PHI_SO = 1
 
 #: every symbol include/logo.h declares
 EXPORTS = (
     "logo_select", "logo_local_attn", "logo_global_attn_sparse_q", "logo_combine",
     "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
     "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
-    "logo_pmask_initial_threshold", "logo_decode",
+    "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
 )
 
 _lib = None
@@ -87,6 +89,8 @@ def library():
         "logo_dense_causal_attn": [PP, P, P, P, P, P],
         "logo_budget_update": [PP, P, f64, f32, P, P, P],
         "logo_decode": [PP, P, P, P, P, P, P, P, i32, f32, P, P, P, f32, P, P, P, P, sz, P],
+        "logo_gate_proj": [i64, i32, P, P, P, P],
+        "logo_branch_transform": [i64, i32, i32, ctypes.c_int, P, P, P, P, P, i64, P, P, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -445,3 +449,47 @@ def logo_decode(prob: Problem, q, k, v, gate, *, threshold: Optional[float] = No
           _ptr(threshold_device), _ptr(gain_local), _ptr(gain_global), float(eps), _ptr(out),
           _ptr(active), _ptr(n_active), _ptr(ws), nbytes, _stream())
     return out, active, n_active
+
+
+def logo_gate_proj(x, w_g, out=None):
+    """p = sigmoid(x . w_g) per token (fp32): x [N, d_model] and w_g [d_model]
+    bf16 device tensors, d_model a multiple of 8."""
+    import torch
+    if x.dim() != 2:
+        raise ValueError("x: [N, d_model]")
+    N, dm = x.shape
+    _check(x, torch.bfloat16, (N, dm), "x")
+    _check(w_g, torch.bfloat16, (dm,), "w_g")
+    if out is None:
+        out = torch.empty(N, dtype=torch.float32, device=x.device)
+    _check(out, torch.float32, (N,), "out")
+    _call("logo_gate_proj", int(N), int(dm), _ptr(x), _ptr(w_g), _ptr(out), _stream())
+    return out
+
+
+def logo_branch_transform(u, kind: int, *, A=None, s=None, b=None, rows=None, n_rows=None,
+                          n_rows_dev=None, out=None):
+    """Eq. branch-transform per head: LP (``A`` [H, d, d] bf16) or SO (``s``,
+    ``b`` [H, d] fp32) of ``u`` [N, H, d] bf16 into ``out`` (same shape; only
+    the rows listed in ``rows`` -- int32 token indices -- when given)."""
+    import torch
+    N, H, d = u.shape
+    _check(u, torch.bfloat16, (N, H, d), "u")
+    if kind == LOGO_PHI_LP:
+        _check(A, torch.bfloat16, (H, d, d), "A")
+    else:
+        _check(s, torch.float32, (H, d), "s")
+        _check(b, torch.float32, (H, d), "b")
+    if rows is not None:
+        _check(rows, torch.int32, None, "rows")
+        n_rows = rows.numel() if n_rows is None else n_rows
+    else:
+        n_rows = N
+    if n_rows_dev is not None:
+        _check(n_rows_dev, torch.int32, None, "n_rows_dev")
+    if out is None:
+        out = torch.empty_like(u)
+    _check(out, torch.bfloat16, (N, H, d), "out")
+    _call("logo_branch_transform", int(N), int(H), int(d), int(kind), _ptr(u), _ptr(A), _ptr(s),
+          _ptr(b), _ptr(rows), int(n_rows), _ptr(n_rows_dev), _ptr(out), _stream())
+    return out

@@ -696,4 +696,50 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
     return hip_status(launch_decode(a, (int)mode, threshold, thr_dev, s), s);
 }
 
+logo_status logo_gate_proj(int64_t n_tokens, int32_t d_model, const logo_bf16 *x,
+                           const logo_bf16 *w_g, float *gate_out, logo_stream stream) {
+    if (n_tokens < 0 || d_model < 1)
+        return LOGO_ERR_SHAPE;
+    if (d_model % 8 != 0)
+        return LOGO_ERR_UNSUPPORTED;
+    if (n_tokens == 0)
+        return LOGO_OK;
+    if (!x || !w_g || !gate_out)
+        return LOGO_ERR_NULL;
+    if ((uintptr_t)x % 16 != 0 || (uintptr_t)w_g % 16 != 0)
+        return LOGO_ERR_ARG;
+    if (n_tokens / 4 >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    hipStream_t s = (hipStream_t)stream;
+    return hip_status(launch_gate_proj(n_tokens, d_model, x, w_g, gate_out, s), s);
+}
+
+logo_status logo_branch_transform(int64_t n_tokens, int32_t num_heads, int32_t head_dim,
+                                  logo_phi_kind kind, const logo_bf16 *u, const logo_bf16 *A,
+                                  const float *s, const float *b, const int32_t *rows,
+                                  int64_t n_rows, const int32_t *n_rows_dev, logo_bf16 *u_g,
+                                  logo_stream stream) {
+    if (n_tokens < 0 || num_heads < 1 || n_rows < 0)
+        return LOGO_ERR_SHAPE;
+    if (head_dim != 64 && head_dim != 128)
+        return LOGO_ERR_UNSUPPORTED;
+    if (kind != LOGO_PHI_LP && kind != LOGO_PHI_SO)
+        return LOGO_ERR_ARG;
+    if (!rows && n_rows != n_tokens)
+        return LOGO_ERR_SHAPE;
+    if (n_rows == 0 || n_tokens == 0)
+        return LOGO_OK;
+    if (!u || !u_g || (kind == LOGO_PHI_LP && !A) || (kind == LOGO_PHI_SO && (!s || !b)))
+        return LOGO_ERR_NULL;
+    if ((uintptr_t)u % 16 != 0 || (uintptr_t)u_g % 16 != 0 || (A && (uintptr_t)A % 16 != 0))
+        return LOGO_ERR_ARG;
+    if (n_rows * num_heads * head_dim / 8 / 256 >= (1LL << 31) ||
+        (n_rows + 255) / 256 >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    hipStream_t st = (hipStream_t)stream;
+    return hip_status(launch_branch_transform((int)kind, n_rows, num_heads, head_dim, u, A, s, b,
+                                              rows, n_rows_dev, u_g, st),
+                      st);
+}
+
 }  // extern "C"

@@ -169,6 +169,16 @@ struct DecodeArgs {
 hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const float *thr_dev,
                          hipStream_t s);
 
+// Gate projection and branch transforms (transform.hip).  kind 0 = LP
+// (A [H][d][d] bf16), 1 = SO (s, b [H][d] fp32); rows = token list or NULL,
+// n_rows_dev = device row count (NULL: n_rows).
+hipError_t launch_gate_proj(int64_t n, int dm, const uint16_t *x, const uint16_t *w, float *p,
+                            hipStream_t s);
+hipError_t launch_branch_transform(int kind, int64_t n_rows, int H, int d, const uint16_t *u,
+                                   const uint16_t *A, const float *sc, const float *bi,
+                                   const int32_t *rows, const int32_t *n_rows_dev, uint16_t *out,
+                                   hipStream_t s);
+
 // One budget-controller step on the device (b_th += gamma sign(F - rho)).
 hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,
                                 float gamma, float *b_th, float *realized, hipStream_t s);

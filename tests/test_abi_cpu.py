@@ -228,3 +228,20 @@ def test_decode_validation(lib):
     big = Prob(seqlens=(32768,) * 4, hq=32, hkv=8, d=128, window=1024)
     nb = lib.logo_workspace_bytes(big.c, 6, 0)
     assert 4 * 32 * (128 + 4) * 4 * 4 <= nb < 64 << 20
+
+
+def test_gate_and_transform_validation(lib):
+    g = lib.logo_gate_proj
+    assert g(-1, 64, FAKE, FAKE, FAKE, None) == ERR_SHAPE
+    assert g(10, 60, FAKE, FAKE, FAKE, None) == ERR_UNSUPPORTED      # d_model % 8
+    assert g(10, 64, None, FAKE, FAKE, None) == ERR_NULL
+    assert g(10, 64, ctypes.c_void_p(0x1008), FAKE, FAKE, None) == ERR_ARG   # misaligned x
+    assert g(0, 64, None, None, None, None) == OK                    # nothing to do
+    t = lib.logo_branch_transform
+    assert t(10, 4, 96, 0, FAKE, FAKE, None, None, None, 10, None, FAKE, None) == ERR_UNSUPPORTED
+    assert t(10, 4, 128, 2, FAKE, FAKE, None, None, None, 10, None, FAKE, None) == ERR_ARG
+    assert t(10, 4, 128, 0, FAKE, None, None, None, None, 10, None, FAKE, None) == ERR_NULL
+    assert t(10, 4, 128, 1, FAKE, None, FAKE, None, None, 10, None, FAKE, None) == ERR_NULL
+    assert t(10, 4, 128, 0, FAKE, FAKE, None, None, None, 9, None, FAKE, None) == ERR_SHAPE
+    assert t(10, 0, 128, 0, FAKE, FAKE, None, None, None, 10, None, FAKE, None) == ERR_SHAPE
+    assert t(10, 4, 128, 0, FAKE, FAKE, None, None, None, 10, None, None, None) == ERR_NULL

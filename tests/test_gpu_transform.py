@@ -1,0 +1,164 @@
+"""GPU parity of the gate projection (Eq. gate-routing) and the LP / SO branch
+transforms (Eq. branch-transform), through the C ABI, against the oracle.
+
+Bars (derived from the arithmetic):
+  * gate: p in fp32 from a dot product accumulated in fp32; per token
+    |p - p_oracle| <= 0.25 * d_model * 2^-24 * sum|x_i w_i| + 4e-7 (the
+    sigmoid's slope is at most 1/4; 4e-7 covers its own fp32 rounding);
+  * transforms: one bf16 rounding of an fp32 result; per element
+    |u_g - oracle| <= 2^-8 |oracle| + 2 d 2^-24 sum_c |u_c A_cj| (LP) or
+    2^-8 |oracle| + 2^-22 (|u s| + |b|) (SO); identity parameters exact;
+  * the layer fed with transformed tensors: the layer bar (max-abs 2e-2,
+    mean-abs 2e-3) against the oracle layer fed with the oracle's transforms.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _support import err_stats, to_device, torch_bf16_to_f64
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def pk():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible: the gpu tests need an MI355X")
+    import paper_2608_29539_amd as pk
+    pk.library()
+    oracle.build(force=False)
+    return pk
+
+
+def bf16_dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def rand_bf16(rng, shape, scale=1.0):
+    return synth.bf16_bits_from_f32(
+        (rng.standard_normal(int(np.prod(shape))) * scale).astype(np.float32)).reshape(shape)
+
+
+def wide(b):
+    return synth.f32_from_bf16_bits(b).reshape(b.shape).astype(np.float64)
+
+
+@pytest.mark.parametrize("N,dm", [(1, 64), (5, 512), (1000, 2048), (33333, 1024), (77, 4104)])
+def test_gate_proj(pk, N, dm):
+    import torch
+    rng = np.random.default_rng(N + dm)
+    x = rand_bf16(rng, (N, dm))
+    w = rand_bf16(rng, (dm,), 1.0 / np.sqrt(dm))
+    p = pk.logo_gate_proj(bf16_dev(x), bf16_dev(w))
+    torch.cuda.synchronize()
+    ref = oracle.gate_proj(x, w).astype(np.float64)
+    got = p.cpu().numpy().astype(np.float64)
+    tol = 0.25 * dm * 2.0 ** -24 * (np.abs(wide(x)) @ np.abs(wide(w))) + 4e-7
+    err = np.abs(got - ref)
+    print(f"[gate N={N} dm={dm}] max_err={err.max():.3g} max_tol_ratio={(err / tol).max():.3g}")
+    assert (err <= tol).all()
+    z = pk.logo_gate_proj(bf16_dev(x), torch.zeros(dm, dtype=torch.bfloat16, device="cuda"))
+    torch.cuda.synchronize()
+    assert (z.cpu().numpy() == np.float32(0.5)).all()     # near-zero init centres p at 1/2
+
+
+def transform_tol(kind, u, A=None, s=None, b=None, ref=None, rows=None):
+    uw = wide(u) if rows is None else wide(u)[rows]
+    if kind == oracle.LP:
+        acc = np.einsum("nhc,hcj->nhj", np.abs(uw), np.abs(wide(A)))
+        return 2.0 ** -8 * np.abs(ref) + 2 * u.shape[-1] * 2.0 ** -24 * acc
+    return 2.0 ** -8 * np.abs(ref) + 2.0 ** -22 * (np.abs(uw * s[None]) + np.abs(b[None]))
+
+
+@pytest.mark.parametrize("d", [64, 128])
+@pytest.mark.parametrize("kind", ["LP", "SO"])
+def test_branch_transform(pk, kind, d):
+    import torch
+    rng = np.random.default_rng(d + (0 if kind == "LP" else 1))
+    N, H = 3001, 8
+    u = rand_bf16(rng, (N, H, d))
+    k = oracle.LP if kind == "LP" else oracle.SO
+    A = rand_bf16(rng, (H, d, d), 1.0 / np.sqrt(d)) if kind == "LP" else None
+    s = rng.uniform(0.5, 2.0, (H, d)).astype(np.float32) if kind == "SO" else None
+    b = rng.standard_normal((H, d)).astype(np.float32) if kind == "SO" else None
+    out = pk.logo_branch_transform(
+        bf16_dev(u), k, A=bf16_dev(A) if A is not None else None,
+        s=torch.from_numpy(s).cuda() if s is not None else None,
+        b=torch.from_numpy(b).cuda() if b is not None else None)
+    torch.cuda.synchronize()
+    ref = oracle.branch_transform(u, k, A=A, s=s, b=b)
+    err = np.abs(torch_bf16_to_f64(out) - ref)
+    tol = transform_tol(k, u, A, s, b, ref)
+    print(f"[{kind} d={d}] max_err={err.max():.3g} max_tol_ratio={(err / tol).max():.3g}")
+    assert (err <= tol).all()
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_branch_transform_identity_and_rows(pk, d):
+    """Identity parameters return u bit for bit; a row list writes only its rows
+    (others keep their previous contents), and a device count limits it."""
+    import torch
+    rng = np.random.default_rng(40 + d)
+    N, H = 700, 4
+    u = rand_bf16(rng, (N, H, d))
+    du = bf16_dev(u)
+    eye = np.broadcast_to(np.eye(d, dtype=np.float32), (H, d, d)).copy()
+    out = pk.logo_branch_transform(du, pk.LOGO_PHI_LP, A=bf16_dev(synth.bf16_bits_from_f32(eye)
+                                                                 .reshape(H, d, d)))
+    so = pk.logo_branch_transform(du, pk.LOGO_PHI_SO, s=torch.ones(H, d, device="cuda"),
+                                  b=torch.zeros(H, d, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), du.view(torch.int16))
+    assert torch.equal(so.view(torch.int16), du.view(torch.int16))
+    A = rand_bf16(rng, (H, d, d), 1.0 / np.sqrt(d))
+    rows = np.array([699, 0, 313, 5, 6, 7, 400], np.int32)
+    sentinel = torch.full((N, H, d), 3.0, dtype=torch.bfloat16, device="cuda")
+    n_dev = torch.tensor([5], dtype=torch.int32, device="cuda")
+    pk.logo_branch_transform(du, pk.LOGO_PHI_LP, A=bf16_dev(A),
+                             rows=torch.from_numpy(rows).cuda(), n_rows_dev=n_dev, out=sentinel)
+    torch.cuda.synchronize()
+    got = torch_bf16_to_f64(sentinel)
+    ref = oracle.branch_transform(u, oracle.LP, A=A, rows=rows[:5])
+    tol = transform_tol(oracle.LP, u, A, ref=ref, rows=rows[:5])
+    assert (np.abs(got[rows[:5]] - ref) <= tol).all()
+    untouched = np.setdiff1d(np.arange(N), rows[:5])
+    assert (got[untouched] == 3.0).all()
+
+
+def test_layer_with_lp_transforms(pk):
+    """The layer fed with GPU LP transforms (K^G, V^G for every token, Q^G for
+    the selected rows only) against the oracle layer fed with the oracle's
+    transforms rounded to bf16."""
+    import torch
+    w = synth.small_workload((2000, 777, 3000), 8, 2, 128, 256, 0.25, seed=4100)
+    x = synth.make_inputs(w)
+    rng = np.random.default_rng(4100)
+    H, Hkv, d = 8, 2, 128
+    AQ = rand_bf16(rng, (H, d, d), 1.0 / np.sqrt(d))
+    AK = rand_bf16(rng, (Hkv, d, d), 1.0 / np.sqrt(d))
+    AV = rand_bf16(rng, (Hkv, d, d), 1.0 / np.sqrt(d))
+    dev = to_device(x)
+    prob = pk.Problem(dev["cu_seqlens"], H, Hkv, d, w.window, cu_seqlens_host=x["cu_seqlens"])
+    cap = pk.logo_ratio_capacity(prob, w.ratio)
+    sel_idx, cu_sel, _, _ = pk.logo_select(prob, dev["gate"], ratio=w.ratio, sel_capacity=cap)
+    kg = pk.logo_branch_transform(dev["k"], pk.LOGO_PHI_LP, A=bf16_dev(AK))
+    vg = pk.logo_branch_transform(dev["v"], pk.LOGO_PHI_LP, A=bf16_dev(AV))
+    qg = torch.zeros_like(dev["q"])
+    pk.logo_branch_transform(dev["q"], pk.LOGO_PHI_LP, A=bf16_dev(AQ), rows=sel_idx,
+                             n_rows=cap, n_rows_dev=cu_sel[-1:], out=qg)
+    out, _, _, _, _ = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                       ratio=w.ratio, q_g=qg, k_g=kg, v_g=vg)
+    torch.cuda.synchronize()
+
+    def rnd(a):
+        return synth.bf16_bits_from_f32(a.astype(np.float32)).reshape(a.shape)
+    ref = oracle.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w.window,
+                          ratio=w.ratio, q_g=rnd(oracle.branch_transform(x["q"], oracle.LP, A=AQ)),
+                          k_g=rnd(oracle.branch_transform(x["k"], oracle.LP, A=AK)),
+                          v_g=rnd(oracle.branch_transform(x["v"], oracle.LP, A=AV)))
+    st = err_stats(torch_bf16_to_f64(out), ref["out"])
+    print("[layer+LP] " + " ".join(f"{k}={v:.3g}" for k, v in st.items()))
+    assert st["max_abs"] <= 2e-2 and st["mean_abs"] <= 2e-3
