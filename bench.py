@@ -212,6 +212,60 @@ def bench_decode(pk, torch, name: str, steps: int, warmup: int):
             "speedup_vs_conservative": round(t_all / t_logo, 3)}
 
 
+def bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, steps: int = 20):
+    """The steps on either side of the attention at the workload's shape: the
+    gate projection p = sigmoid(x . w_g) with d_model = Hq d, and the LP / SO
+    branch transforms of K and V (every token) and of Q (selected rows only).
+    HBM-bound: algorithmic bytes = inputs read once + outputs written once."""
+    N, Hq, Hkv, d = w.total_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
+    dm = Hq * d
+    g = torch.Generator(device="cuda").manual_seed(7)
+    x = torch.randn((N, dm), generator=g, device="cuda").to(torch.bfloat16)
+    wg = (torch.randn(dm, generator=g, device="cuda") / dm ** 0.5).to(torch.bfloat16)
+    A_kv = (torch.randn((Hkv, d, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    A_q = (torch.randn((Hq, d, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    s_kv = torch.rand((Hkv, d), generator=g, device="cuda") + 0.5
+    b_kv = torch.randn((Hkv, d), generator=g, device="cuda")
+    p_out = torch.empty(N, dtype=torch.float32, device="cuda")
+    kg = torch.empty_like(dev["k"])
+    qg = torch.empty_like(dev["q"])
+    n_sel = int(cu_sel[-1])
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    rows = {}
+    t = timed(lambda: pk.logo_gate_proj(x, wg, out=p_out))
+    rows["gate_proj"] = (t, N * dm * 2 + dm * 2 + N * 4, 2.0 * N * dm)
+    t = timed(lambda: pk.logo_branch_transform(dev["k"], pk.LOGO_PHI_LP, A=A_kv, out=kg))
+    rows["lp_k"] = (t, 2 * N * Hkv * d * 2 + Hkv * d * d * 2, 2.0 * N * Hkv * d * d)
+    t = timed(lambda: pk.logo_branch_transform(dev["k"], pk.LOGO_PHI_SO, s=s_kv, b=b_kv, out=kg))
+    rows["so_k"] = (t, 2 * N * Hkv * d * 2 + 2 * Hkv * d * 4, 2.0 * N * Hkv * d)
+    t = timed(lambda: pk.logo_branch_transform(dev["q"], pk.LOGO_PHI_LP, A=A_q, rows=sel_idx,
+                                               n_rows=cap, n_rows_dev=cu_sel[-1:], out=qg))
+    rows["lp_q_selected"] = (t, 2 * n_sel * Hq * d * 2 + Hq * d * d * 2 + n_sel * 4,
+                             2.0 * n_sel * Hq * d * d)
+    out = {}
+    for k_, (ms, nbytes, flops) in rows.items():
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out[k_] = {"us": round(ms * 1e3, 2), "bytes": float(nbytes), "GB_s": round(gbs, 1),
+                   "frac_hbm": round(gbs / PEAK_HBM_GBS, 4),
+                   "TFLOP_s": round(flops / (ms * 1e-3) / 1e12, 1)}
+        log(f"transform {k_}: {ms * 1e3:.1f} us, {gbs:.0f} GB/s")
+    out["shape"] = {"tokens": N, "d_model": dm, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                    "selected_rows": n_sel}
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,6 +282,8 @@ def main(argv=None):
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the threshold-mode run and the clock query")
     ap.add_argument("--no-decode", action="store_true", help="skip the decoding-step measurement")
+    ap.add_argument("--no-transforms", action="store_true",
+                    help="skip the gate-projection / branch-transform measurement")
     ap.add_argument("--decode-workload", default="decode-B16-32k-gqa")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of MIB MiB "
@@ -412,6 +468,10 @@ def main(argv=None):
                 "flops_per_launch": fl * p_global,
                 "duration_ms": round(stage_ms["global"], 4)}
 
+    transforms = None
+    if not args.no_transforms:
+        transforms = bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap)
+
     decode = None
     if not args.no_decode:
         decode = bench_decode(pk, torch, args.decode_workload, steps=50, warmup=20)
@@ -456,6 +516,7 @@ def main(argv=None):
         "select_hbm": select_hbm,
         "threshold_mode": thr_mode,
         "decode": decode,
+        "transforms": transforms,
         "gpu": gpu_info(torch, busy=lambda: [step() for _ in range(600)])
                if not args.no_extra else None,
     }

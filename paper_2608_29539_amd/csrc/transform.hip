@@ -90,8 +90,10 @@ __global__ __launch_bounds__(256) void so_transform_kernel(int64_t n_rows, int H
 }
 
 // LP: workgroup = (head h, block of kLpRows rows); 4 waves, each 32 rows at
-// a time.  LDS holds A_h^T [d][d + 8] (bf16, rows padded by 16 bytes).
-constexpr int kLpRows = 256;
+// a time with the next 32 rows' operands prefetched.  LDS holds A_h^T
+// [d][d + 8] (bf16, rows padded by 16 bytes), filled with coalesced reads of
+// eight rows of A_h per thread and one 16-byte write.
+constexpr int kLpRows = 512;
 
 template <int D>
 __global__ __launch_bounds__(256) void lp_transform_kernel(int64_t n_rows, int H, const uint16_t *u,
@@ -99,7 +101,7 @@ __global__ __launch_bounds__(256) void lp_transform_kernel(int64_t n_rows, int H
                                                            const int32_t *n_rows_dev,
                                                            uint16_t *out) {
     constexpr int KP = D + 8;
-    __shared__ uint16_t at[D][KP];                  // at[j][c] = A_h[c][j]
+    __shared__ __attribute__((aligned(16))) uint16_t at[D][KP];   // at[j][c] = A_h[c][j]
     const int h = blockIdx.y;
     const int64_t r0 = (int64_t)blockIdx.x * kLpRows;
     const int64_t nr = n_rows_dev ? min((int64_t)n_rows_dev[0], n_rows) : n_rows;
@@ -107,49 +109,67 @@ __global__ __launch_bounds__(256) void lp_transform_kernel(int64_t n_rows, int H
         return;                                     // whole workgroup
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m = lane & 31, g = lane >> 5;
-    // stage A_h transposed: thread reads 8 consecutive j of one row c
+    // stage A_h transposed: task (c-block of 8, column j) reads A_h[c0..c0+7][j]
+    // (lanes take consecutive j: coalesced) and writes at[j][c0..c0+7]
     const uint16_t *Ah = A + (int64_t)h * D * D;
     for (int idx = tid; idx < D * D / 8; idx += 256) {
-        const int c = idx / (D / 8), j0 = (idx % (D / 8)) * 8;
-        const u32x4t v = *(const u32x4t *)(Ah + c * D + j0);
+        const int j = idx % D, c0 = (idx / D) * 8;
+        uint32_t w4[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            at[j0 + 2 * i][c] = (uint16_t)(v[i] & 0xFFFFu);
-            at[j0 + 2 * i + 1][c] = (uint16_t)(v[i] >> 16);
-        }
+        for (int i = 0; i < 4; i++)
+            w4[i] = (uint32_t)Ah[(c0 + 2 * i) * D + j] | ((uint32_t)Ah[(c0 + 2 * i + 1) * D + j] << 16);
+        *(u32x4t *)&at[j][c0] = u32x4t{w4[0], w4[1], w4[2], w4[3]};
     }
     __syncthreads();
-    for (int64_t rb = r0 + wave * 32; rb < min(r0 + kLpRows, nr); rb += 4 * 32) {
-        // this lane's token row (rows past the end repeat the last one, not stored)
+    const int64_t r_end = min(r0 + kLpRows, nr);
+    // this lane's operand row of the block starting at rb (rows past the end
+    // repeat the last one and are not stored)
+    auto load_block = [&](int64_t rb, bf16x8t (&uf)[D / 16], int64_t &t) {
         const int64_t r = min(rb + m, nr - 1);
-        const int64_t t = rows ? rows[r] : r;
+        t = rows ? rows[r] : r;
         const uint16_t *ur = u + (t * H + h) * (int64_t)D + g * 8;
-        bf16x8t uf[D / 16];
 #pragma unroll
         for (int cb = 0; cb < D / 16; cb++)
             uf[cb] = *(const bf16x8t *)(ur + cb * 16);
-        f32x16t acc[D / 32];
+    };
+    int64_t rb = r0 + wave * 32;
+    if (rb >= r_end)
+        return;
+    bf16x8t uf[D / 16];
+    int64_t t;
+    load_block(rb, uf, t);
+    for (; rb < r_end; rb += 4 * 32) {
+        bf16x8t un[D / 16];
+        int64_t tn = t;
+        const bool more = rb + 4 * 32 < r_end;
+        if (more)
+            load_block(rb + 4 * 32, un, tn);
+        uint16_t *op = out + (t * H + h) * (int64_t)D + g * 4;
+        const bool store = rb + m < r_end;
 #pragma unroll
         for (int jb = 0; jb < D / 32; jb++) {
-            acc[jb] = f32x16t{};
+            f32x16t acc = f32x16t{};
 #pragma unroll
             for (int cb = 0; cb < D / 16; cb++) {
                 const bf16x8t af = *(const bf16x8t *)&at[jb * 32 + m][cb * 16 + g * 8];
-                acc[jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, uf[cb], acc[jb], 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, uf[cb], acc, 0, 0, 0);
             }
-        }
-        if (rb + m < nr) {
-            // lane holds out[t][h][j] for j = 32 jb + 8 (i/4) + 4 g + i%4
-            uint16_t *op = out + (t * H + h) * (int64_t)D + g * 4;
-#pragma unroll
-            for (int jb = 0; jb < D / 32; jb++)
+            // lane holds out[t][h][j] for j = 32 jb + 8 q + 4 g + (0..3)
+            if (store) {
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
                     u32x2t o;
-                    o.x = pack2(acc[jb][q * 4 + 0], acc[jb][q * 4 + 1]);
-                    o.y = pack2(acc[jb][q * 4 + 2], acc[jb][q * 4 + 3]);
+                    o.x = pack2(acc[q * 4 + 0], acc[q * 4 + 1]);
+                    o.y = pack2(acc[q * 4 + 2], acc[q * 4 + 3]);
                     *(u32x2t *)(op + jb * 32 + q * 8) = o;
                 }
+            }
+        }
+        if (more) {
+#pragma unroll
+            for (int cb = 0; cb < D / 16; cb++)
+                uf[cb] = un[cb];
+            t = tn;
         }
     }
 }
