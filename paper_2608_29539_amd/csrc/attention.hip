@@ -675,56 +675,53 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     for (int rg = 0; rg < RG; rg++) {
         const float inv = 1.f / l_tot[rg];
         if (EPI == kEpiFused && MODE != kModeDense) {
-            // ContextNorm over the row's d values: this lane holds d/2 of
-            // them, its partner l^32 the other half.
+            // ContextNorm over the row's d values (this lane holds d/2 of them,
+            // its partner l^32 the other half), the softmax's 1/l, the fusion
+            // weight and the gain folded into one scale per element:
+            // Norm(o) = acc * (1/l) / sqrt(mean((acc/l)^2) + eps).
             float ss = 0.f;
 #pragma unroll
             for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
-                for (int i = 0; i < 16; i++) {
-                    const float o = acc[rg][cb][i] * inv;
-                    acc[rg][cb][i] = o;
-                    ss = fmaf(o, o, ss);
-                }
+                for (int i = 0; i < 16; i++)
+                    ss = fmaf(acc[rg][cb][i], acc[rg][cb][i], ss);
             ss = pair_sum(ss);
             if (!(wave_valid && row_valid[rg]))
                 continue;
-            const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
+            const float rn = 1.f / sqrtf(ss * inv * inv / (float)D + a.eps);
             const int64_t tok = qtok[rg];
             const float p = ep_gate[rg];
             const int r = ep_rank[rg];
             const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
-            uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
-            if (MODE == kModeLocal && r >= 0) {
-                // selected token: keep (1-p) Norm^L in fp32 for the global kernel
+            // selected token in the local branch: keep (1-p) Norm^L in fp32
+            const bool keep = MODE == kModeLocal && r >= 0;
+            const float wgt = (MODE == kModeGlobal) ? p : (keep ? 1.f - p : 1.f);
+            const float scale = inv * rn * wgt;
+            auto scaled = [&](int cb, int qd) {
+                f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
+                           acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
+                v *= scale;
+                if (gp)
+                    v *= *(const f32x4 *)(gp + cb * 32 + qd * 8);
+                return v;
+            };
+            if (keep) {
                 float *lp = a.lc + ((int64_t)r * a.hq + head) * D + g * 4;
-                const float wgt = (1.f - p) * rn;
 #pragma unroll
                 for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
-                    for (int qd = 0; qd < 4; qd++) {
-                        f32x4 gn = {1.f, 1.f, 1.f, 1.f};
-                        if (gp)
-                            gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
-                        f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
-                                   acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
-                        *(f32x4 *)(lp + cb * 32 + qd * 8) = v * gn * wgt;
-                    }
+                    for (int qd = 0; qd < 4; qd++)
+                        *(f32x4 *)(lp + cb * 32 + qd * 8) = scaled(cb, qd);
                 continue;
             }
             const float *lp = (MODE == kModeGlobal)
                                   ? a.lc + ((int64_t)r * a.hq + head) * D + g * 4 : nullptr;
-            const float wgt = (MODE == kModeGlobal) ? p * rn : rn;
+            uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
             for (int cb = 0; cb < D / 32; cb++)
 #pragma unroll
                 for (int qd = 0; qd < 4; qd++) {
-                    f32x4 gn = {1.f, 1.f, 1.f, 1.f};
-                    if (gp)
-                        gn = *(const f32x4 *)(gp + cb * 32 + qd * 8);
-                    f32x4 v = {acc[rg][cb][qd * 4 + 0], acc[rg][cb][qd * 4 + 1],
-                               acc[rg][cb][qd * 4 + 2], acc[rg][cb][qd * 4 + 3]};
-                    v = v * gn * wgt;
+                    f32x4 v = scaled(cb, qd);
                     if (MODE == kModeGlobal)
                         v += *(const f32x4 *)(lp + cb * 32 + qd * 8);
                     u32x2 o;
