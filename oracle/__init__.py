@@ -19,6 +19,7 @@ from .oracle import (  # noqa: F401
     fuse,
     gate_proj,
     library_path,
+    logo_bwd,
     logo_fwd,
     logo_rows,
     num_threads,

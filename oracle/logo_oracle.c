@@ -33,6 +33,9 @@
  *                                                         (Sec. 3.3 and App. B,
  *                                                          Autoregressive Decoding)
  *   - the gate projection p = sigmoid(x . w_g)            (Sec. 3.2, Eq. gate-routing)
+ *   - the backward pass: gradients of the layer's inputs given dL/d out,
+ *     the selection held fixed                            (Sec. 3.3 and App. B, the
+ *                                                          row-sparse backward)
  *   - the branch transforms LP (U A) and SO (U * s + b)   (Sec. 3.2, Eq. branch-transform)
  *
  * Readings where the paper is silent (each also listed in the design notes):
@@ -551,4 +554,191 @@ void oracle_branch_transform(const uint16_t *u, int H, int d, int kind, const ui
             }
         }
     }
+}
+
+/*
+ * Backward pass of the layer for training (Sec. 3.3 and App. B: the backward
+ * keeps the forward's row-sparse structure; query gradients exist only for
+ * the rows a branch computes).  The selection is the forward's (threshold /
+ * ratio as in oracle_logo_fwd) and is held fixed: z is a hard decision with
+ * no gradient.  Given dout = dL/d out [N][Hq][d] (double), the chain rule is
+ * written out per (row, head), in double:
+ *   fusion (Eq. output-fusion):  d~oL = (z ? 1-p : 1) dout,  d~oG = p dout,
+ *                                dL/dp = z * sum_{h,c} dout (~oG - ~oL)
+ *   ContextNorm (Eq. contextnorm), y = o g / r, r = sqrt(mean o^2 + eps):
+ *                                dg_c += dy_c o_c / r,
+ *                                do_c = g_c dy_c / r - o_c (sum_k g_k dy_k o_k) / (d r^3)
+ *   attention (Eq. attention):   P = softmax(scale q.k_j) over the context,
+ *                                dv_j += P_j do,  dP_j = do . v_j,
+ *                                dS_j = P_j (dP_j - sum_k P_k dP_k),
+ *                                dq += scale sum_j dS_j k_j,  dk_j += scale dS_j q
+ * Outputs (caller-allocated, overwritten): dq, dk, dv for the local-branch
+ * tensors and dq_g, dk_g, dv_g for the global-branch ones (with aliased
+ * global tensors the caller adds each pair), dgate [N], dgain_l and dgain_g
+ * [Hq][d].  Returns n_sel.
+ */
+int64_t oracle_logo_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                        const uint16_t *q_g, const uint16_t *k_g, const uint16_t *v_g,
+                        const float *gate, const int32_t *cu, int B, int Hq, int Hkv, int d,
+                        int window, double scale, int mode, float threshold, double ratio,
+                        const float *gain_local, const float *gain_global, double eps,
+                        const double *dout, double *dq, double *dk, double *dv, double *dq_g,
+                        double *dk_g, double *dv_g, double *dgate, double *dgain_l,
+                        double *dgain_g)
+{
+    const int64_t N = cu[B];
+    const int G = Hq / Hkv;
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    if (!q_g)
+        q_g = q;
+    if (!k_g)
+        k_g = k;
+    if (!v_g)
+        v_g = v;
+    float *thr = (float *)malloc((size_t)B * sizeof(float));
+    int32_t *sel = (int32_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int32_t));
+    int32_t *cu_sel = (int32_t *)malloc((size_t)(B + 1) * sizeof(int32_t));
+    int32_t *t2s = (int32_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int32_t));
+    oracle_thresholds(gate, cu, B, mode, threshold, ratio, thr);
+    const int64_t n_sel = oracle_select(gate, cu, B, thr, sel, cu_sel, t2s);
+
+    const int64_t row = (int64_t)Hq * d;
+    memset(dq, 0, (size_t)N * row * sizeof(double));
+    memset(dq_g, 0, (size_t)N * row * sizeof(double));
+    memset(dk, 0, (size_t)N * Hkv * d * sizeof(double));
+    memset(dv, 0, (size_t)N * Hkv * d * sizeof(double));
+    memset(dk_g, 0, (size_t)N * Hkv * d * sizeof(double));
+    memset(dv_g, 0, (size_t)N * Hkv * d * sizeof(double));
+    memset(dgain_l, 0, (size_t)row * sizeof(double));
+    memset(dgain_g, 0, (size_t)row * sizeof(double));
+    /* normalised branch outputs ~oL (all rows) and ~oG (selected rows, by token) */
+    double *yl = (double *)calloc((size_t)(N > 0 ? N : 1) * row, sizeof(double));
+    double *yg = (double *)calloc((size_t)(N > 0 ? N : 1) * row, sizeof(double));
+    int64_t max_T = 1;
+    for (int b = 0; b < B; b++)
+        if ((int64_t)cu[b + 1] - cu[b] > max_T)
+            max_T = (int64_t)cu[b + 1] - cu[b];
+
+    /* one job per (branch, KV head): the rows of its G query heads, so the
+       dk / dv / gain accumulations of a job touch only its own heads */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int job = 0; job < 2 * Hkv; job++) {
+        const int branch = job / Hkv; /* 0 local, 1 global */
+        const int hk = job % Hkv;
+        const uint16_t *Q = branch ? q_g : q, *K = branch ? k_g : k, *V = branch ? v_g : v;
+        double *dQ = branch ? dq_g : dq, *dK = branch ? dk_g : dk, *dV = branch ? dv_g : dv;
+        double *dG = branch ? dgain_g : dgain_l, *Y = branch ? yg : yl;
+        const float *gain = branch ? gain_global : gain_local;
+        double *P = (double *)malloc((size_t)max_T * sizeof(double));
+        double *dP = (double *)malloc((size_t)max_T * sizeof(double));
+        double *qd = (double *)malloc((size_t)d * sizeof(double));
+        double *o = (double *)malloc((size_t)d * sizeof(double));
+        double *dy = (double *)malloc((size_t)d * sizeof(double));
+        double *dO = (double *)malloc((size_t)d * sizeof(double));
+        for (int b = 0; b < B; b++) {
+            const int64_t base = cu[b], T = (int64_t)cu[b + 1] - base;
+            for (int64_t i = 0; i < T; i++) {
+                const int64_t t = base + i;
+                const int z = t2s[t] >= 0;
+                if (branch == 1 && !z)
+                    continue;
+                const int64_t lo = (branch == 0 && i - window + 1 > 0) ? i - window + 1 : 0;
+                const int64_t nk = i - lo + 1;
+                const double p = (double)gate[t];
+                for (int h = hk * G; h < (hk + 1) * G; h++) {
+                    for (int c = 0; c < d; c++)
+                        qd[c] = bf16_to_double(Q[(t * Hq + h) * (int64_t)d + c]);
+                    /* forward recomputation: P, o, r, y */
+                    double m = -INFINITY;
+                    for (int64_t j = 0; j < nk; j++) {
+                        const uint16_t *kr = K + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        double dot = 0.0;
+                        for (int c = 0; c < d; c++)
+                            dot += qd[c] * bf16_to_double(kr[c]);
+                        P[j] = scale * dot;
+                        if (P[j] > m)
+                            m = P[j];
+                    }
+                    double den = 0.0;
+                    for (int64_t j = 0; j < nk; j++) {
+                        P[j] = exp(P[j] - m);
+                        den += P[j];
+                    }
+                    for (int c = 0; c < d; c++)
+                        o[c] = 0.0;
+                    for (int64_t j = 0; j < nk; j++) {
+                        P[j] /= den;
+                        const uint16_t *vr = V + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        for (int c = 0; c < d; c++)
+                            o[c] += P[j] * bf16_to_double(vr[c]);
+                    }
+                    double ms = 0.0;
+                    for (int c = 0; c < d; c++)
+                        ms += o[c] * o[c];
+                    const double r = sqrt(ms / (double)d + eps);
+                    double *yr = Y + (t * Hq + h) * (int64_t)d;
+                    const double *dr = dout + (t * Hq + h) * (int64_t)d;
+                    const double wgt = branch ? p : (z ? 1.0 - p : 1.0);
+                    const float *gh = gain ? gain + (int64_t)h * d : NULL;
+                    double gdo = 0.0;
+                    for (int c = 0; c < d; c++) {
+                        const double gc = gh ? (double)gh[c] : 1.0;
+                        yr[c] = o[c] / r * gc;
+                        dy[c] = wgt * dr[c];
+                        dG[h * d + c] += dy[c] * o[c] / r;
+                        gdo += gc * dy[c] * o[c];
+                    }
+                    /* ContextNorm backward */
+                    for (int c = 0; c < d; c++) {
+                        const double gc = gh ? (double)gh[c] : 1.0;
+                        dO[c] = gc * dy[c] / r - o[c] * gdo / ((double)d * r * r * r);
+                    }
+                    /* softmax attention backward */
+                    double delta = 0.0;
+                    for (int64_t j = 0; j < nk; j++) {
+                        const uint16_t *vr = V + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        double s = 0.0;
+                        for (int c = 0; c < d; c++)
+                            s += dO[c] * bf16_to_double(vr[c]);
+                        dP[j] = s;
+                        delta += P[j] * s;
+                    }
+                    double *dqr = dQ + (t * Hq + h) * (int64_t)d;
+                    for (int64_t j = 0; j < nk; j++) {
+                        const double ds = P[j] * (dP[j] - delta);
+                        const uint16_t *kr = K + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        double *dkr = dK + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        double *dvr = dV + ((base + lo + j) * Hkv + hk) * (int64_t)d;
+                        for (int c = 0; c < d; c++) {
+                            dqr[c] += scale * ds * bf16_to_double(kr[c]);
+                            dkr[c] += scale * ds * qd[c];
+                            dvr[c] += P[j] * dO[c];
+                        }
+                    }
+                }
+            }
+        }
+        free(P);
+        free(dP);
+        free(qd);
+        free(o);
+        free(dy);
+        free(dO);
+    }
+    /* gate gradient through the fusion weight */
+    for (int64_t t = 0; t < N; t++) {
+        double acc = 0.0;
+        if (t2s[t] >= 0)
+            for (int64_t e = 0; e < row; e++)
+                acc += dout[t * row + e] * (yg[t * row + e] - yl[t * row + e]);
+        dgate[t] = acc;
+    }
+    free(yl);
+    free(yg);
+    free(thr);
+    free(sel);
+    free(cu_sel);
+    free(t2s);
+    return n_sel;
 }

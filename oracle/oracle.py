@@ -71,6 +71,9 @@ def _load():
                                   P, P, f64, P, P, P, P]
     lib.oracle_decode.restype = i64
     lib.oracle_gate_proj.argtypes = [P, P, i64, i32, P]
+    lib.oracle_logo_bwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, i32,
+                                    f32, f64, P, P, f64, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_logo_bwd.restype = i64
     lib.oracle_branch_transform.argtypes = [P, i32, i32, i32, P, P, P, P, i64, P]
     _lib = lib
     return lib
@@ -274,3 +277,42 @@ def branch_transform(u, kind: int, *, A=None, s=None, b=None, rows=None) -> np.n
                                     _ptr(_c(s, np.float32)), _ptr(_c(b, np.float32)),
                                     _ptr(rows), n, _ptr(out))
     return out
+
+
+def logo_bwd(q, k, v, gate, cu_seqlens, window: int, dout, *, ratio: Optional[float] = None,
+             threshold: Optional[float] = None, q_g=None, k_g=None, v_g=None, gain_local=None,
+             gain_global=None, eps: float = 1e-6, scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """Gradients of the layer (fp64) given dout = dL/d out [N, Hq, d], the
+    selection held fixed.  With aliased global tensors (q_g etc. None) the
+    returned dq / dk / dv include both branches; otherwise the global-branch
+    gradients are dq_g / dk_g / dv_g."""
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    alias = q_g is None and k_g is None and v_g is None
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    q_g, k_g, v_g = _c(q_g, np.uint16), _c(k_g, np.uint16), _c(v_g, np.uint16)
+    gate, cu = _c(gate, np.float32), _c(cu_seqlens, np.int32)
+    dout = _c(dout, np.float64)
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    B = cu.size - 1
+    mode = SEL_RATIO if ratio is not None else SEL_THRESHOLD
+    n1 = max(N, 1)
+    dq, dq_g = np.empty((n1, Hq, d)), np.empty((n1, Hq, d))
+    dk, dv, dk_g, dv_g = (np.empty((n1, Hkv, d)) for _ in range(4))
+    dgate = np.empty(n1)
+    dgl, dgg = np.empty((Hq, d)), np.empty((Hq, d))
+    n = _load().oracle_logo_bwd(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g), _ptr(gate), _ptr(cu), B,
+        Hq, Hkv, d, int(window), float(scale), mode,
+        float(threshold if threshold is not None else 0.0),
+        float(ratio if ratio is not None else 0.0),
+        _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)), float(eps),
+        _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dq_g), _ptr(dk_g), _ptr(dv_g),
+        _ptr(dgate), _ptr(dgl), _ptr(dgg))
+    r = dict(dgate=dgate[:N], dgain_local=dgl, dgain_global=dgg, n_sel=int(n))
+    if alias:
+        r.update(dq=(dq + dq_g)[:N], dk=(dk + dk_g)[:N], dv=(dv + dv_g)[:N])
+    else:
+        r.update(dq=dq[:N], dk=dk[:N], dv=dv[:N], dq_g=dq_g[:N], dk_g=dk_g[:N], dv_g=dv_g[:N])
+    return r

@@ -67,6 +67,19 @@ MUTATIONS = {
     "lp_matrix_ignores_head": ("A[((int64_t)h * d + c) * d + j]", "A[((int64_t)0 * d + c) * d + j]"),
     "so_offset_sign": ("+ (double)b[h * d + j];", "- (double)b[h * d + j];"),
     "transform_rows_ignored": ("const int64_t t = rows ? rows[r] : r;", "const int64_t t = r;"),
+    "bwd_norm_missing_cubic_term": (
+        "dO[c] = gc * dy[c] / r - o[c] * gdo / ((double)d * r * r * r);", "dO[c] = gc * dy[c] / r;"),
+    "bwd_softmax_delta_dropped": ("const double ds = P[j] * (dP[j] - delta);",
+                                  "const double ds = P[j] * dP[j];"),
+    "bwd_dk_missing_scale": ("dkr[c] += scale * ds * qd[c];", "dkr[c] += ds * qd[c];"),
+    "bwd_dv_before_norm": ("dvr[c] += P[j] * dO[c];", "dvr[c] += P[j] * dy[c];"),
+    "bwd_local_weight_ignores_gate": ("const double wgt = branch ? p : (z ? 1.0 - p : 1.0);",
+                                      "const double wgt = branch ? p : 1.0;"),
+    "bwd_dgate_sign": ("(yg[t * row + e] - yl[t * row + e])", "(yl[t * row + e] - yg[t * row + e])"),
+    "bwd_gain_grad_unnormalised": ("dG[h * d + c] += dy[c] * o[c] / r;",
+                                   "dG[h * d + c] += dy[c] * o[c];"),
+    "bwd_window_w_plus_1_keys": ("(branch == 0 && i - window + 1 > 0) ? i - window + 1 : 0",
+                                 "(branch == 0 && i - window > 0) ? i - window : 0"),
 }
 
 

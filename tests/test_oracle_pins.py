@@ -587,3 +587,120 @@ def test_branch_transform_bruteforce_and_rows(oracle_lib):
                                lp[rows], rtol=0, atol=1e-12)
     np.testing.assert_allclose(oracle_lib.branch_transform(u, oracle_lib.SO, s=s, b=b, rows=rows),
                                so[rows], rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Backward pass (training; Sec. 3.3 / App. B): the oracle's analytic
+# gradients against central finite differences of an independent fp64 numpy
+# forward, with the selection held fixed.
+# ---------------------------------------------------------------------------
+def np_layer_f64(qf, kf, vf, qgf, kgf, vgf, p, seqlens, window, z, gl, gg, eps, scale):
+    """The layer in fp64 from float inputs (explicit masks, full score matrix)."""
+    N, Hq, d = qf.shape
+    G = Hq // kf.shape[1]
+    out = np.zeros((N, Hq, d))
+    start = 0
+    for T in seqlens:
+        sl = slice(start, start + T)
+        start += T
+        if T == 0:
+            continue
+        i = np.arange(T)[:, None]
+        j = np.arange(T)[None, :]
+        causal = j <= i
+        local = causal & (j > i - window)
+        for h in range(Hq):
+            ys = []
+            for (Q, K, V, mask, g) in ((qf, kf, vf, local, gl), (qgf, kgf, vgf, causal, gg)):
+                S = scale * (Q[sl, h, :] @ K[sl, h // G, :].T)
+                S = np.where(mask, S, -np.inf)
+                W = np.exp(S - S.max(axis=1, keepdims=True))
+                O = (W / W.sum(axis=1, keepdims=True)) @ V[sl, h // G, :]
+                r = np.sqrt((O ** 2).mean(axis=1, keepdims=True) + eps)
+                ys.append(O / r * (1.0 if g is None else g[h][None, :]))
+            pw = p[sl][:, None]
+            out[sl, h, :] = np.where(z[sl][:, None], (1 - pw) * ys[0] + pw * ys[1], ys[0])
+    return out
+
+
+BWD_CASES = [
+    # seqlens, Hq, Hkv, d, window, distinct global tensors, gains, eps
+    ((5, 7), 2, 1, 4, 3, False, False, 1e-6),
+    ((9,), 4, 2, 8, 4, True, True, 1e-3),
+    ((3, 0, 6), 2, 2, 4, 16, False, True, 0.0),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(BWD_CASES)))
+def test_backward_finite_differences(oracle_lib, ci):
+    seqlens, Hq, Hkv, d, window, distinct, gains, eps = BWD_CASES[ci]
+    rng = np.random.default_rng(900 + ci)
+    N = sum(seqlens)
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    q, k, v = mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)
+    qg, kg, vg = (mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)) if distinct else (None,) * 3
+    # gates kept away from the threshold so no finite step changes the selection
+    gate = rng.choice([0.15, 0.3, 0.7, 0.85], N).astype(np.float32)
+    gl = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if gains else None
+    gg = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32) if gains else None
+    cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+    dout = rng.standard_normal((N, Hq, d))
+    scale = 1.0 / math.sqrt(d)
+    r = oracle_lib.logo_bwd(q, k, v, gate, cu, window, dout, threshold=0.5, q_g=qg, k_g=kg,
+                            v_g=vg, gain_local=gl, gain_global=gg, eps=eps)
+    z = gate > np.float32(0.5)
+    base = dict(qf=wide(q), kf=wide(k), vf=wide(v),
+                qgf=wide(qg) if distinct else wide(q), kgf=wide(kg) if distinct else wide(k),
+                vgf=wide(vg) if distinct else wide(v), p=gate.astype(np.float64),
+                gl=None if gl is None else gl.astype(np.float64),
+                gg=None if gg is None else gg.astype(np.float64))
+
+    def loss(**over):
+        a = dict(base)
+        a.update(over)
+        if not distinct:       # aliased global tensors move with the local ones
+            for lk, gk in (("qf", "qgf"), ("kf", "kgf"), ("vf", "vgf")):
+                if lk in over:
+                    a[gk] = a[lk]
+        o = np_layer_f64(a["qf"], a["kf"], a["vf"], a["qgf"], a["kgf"], a["vgf"], a["p"],
+                         seqlens, window, z, a["gl"], a["gg"], eps, scale)
+        return float((dout * o).sum())
+
+    targets = [("qf", "dq"), ("kf", "dk"), ("vf", "dv"), ("p", "dgate")]
+    if distinct:
+        targets += [("qgf", "dq_g"), ("kgf", "dk_g"), ("vgf", "dv_g")]
+    if gains:
+        targets += [("gl", "dgain_local"), ("gg", "dgain_global")]
+    h = 1e-6
+    for name, gname in targets:
+        for _ in range(2):
+            U = rng.standard_normal(base[name].shape)
+            fd = (loss(**{name: base[name] + h * U}) - loss(**{name: base[name] - h * U})) / (2 * h)
+            an = float((r[gname] * U).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_backward_invariants(oracle_lib):
+    """Softmax shift invariance makes each branch's key gradients sum to zero
+    over a sequence's keys (per KV head); with eps = 0, ContextNorm removes any
+    positive scale of v, so <dv, v> = 0."""
+    rng = np.random.default_rng(950)
+    seqlens, Hq, Hkv, d, w = (12, 7), 4, 2, 8, 5
+    N = sum(seqlens)
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    q, k, v = mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)
+    qg, kg, vg = mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)
+    gate = rng.uniform(0, 1, N).astype(np.float32)
+    cu = np.array([0, 12, 19], np.int32)
+    dout = rng.standard_normal((N, Hq, d))
+    r = oracle_lib.logo_bwd(q, k, v, gate, cu, w, dout, ratio=0.4, q_g=qg, k_g=kg, v_g=vg, eps=0.0)
+    for key in ("dk", "dk_g"):
+        for b in range(2):
+            np.testing.assert_allclose(r[key][cu[b]:cu[b + 1]].sum(axis=0), 0.0, atol=1e-10)
+    assert abs(float((r["dv"] * wide(v)).sum())) < 1e-9
+    assert abs(float((r["dv_g"] * wide(vg)).sum())) < 1e-9
+    # unselected tokens get no gradient through the fusion weight or the global query
+    sel = r["n_sel"]
+    assert 0 < sel < N
+    t2s = oracle_lib.logo_fwd(q, k, v, gate, cu, w, ratio=0.4)["tok2sel"]
+    assert not r["dgate"][t2s < 0].any() and not r["dq_g"][t2s < 0].any()
