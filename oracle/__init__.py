@@ -17,6 +17,7 @@ from .oracle import (  # noqa: F401
     contextnorm,
     decode,
     fuse,
+    fusion_bwd,
     gate_proj,
     library_path,
     logo_bwd,

@@ -742,3 +742,68 @@ int64_t oracle_logo_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v,
     free(t2s);
     return n_sel;
 }
+
+/*
+ * Backward of ContextNorm and the fusion alone (Eqs. contextnorm and
+ * output-fusion), per (token, head), given the raw branch outputs:
+ *   ol [N][Hq][d] (every token), og [N][Hq][d] (rows of selected tokens,
+ *   indexed by token; others unused), gate p [N], z [N] (1 = selected),
+ *   gains (NULL = 1), eps, dout [N][Hq][d].
+ * Writes dol = dL/d oL, dog = dL/d oG (zero for unselected tokens), the
+ * row sums delta_l[t][h] = sum_c dol * ol and delta_g[t][h] = sum_c dog * og,
+ * dgate [N] and the gain gradients dgain_l, dgain_g [Hq][d].  The same chain
+ * rule as in oracle_logo_bwd, in double.
+ */
+void oracle_fusion_bwd(const double *ol, const double *og, const float *gate, const int32_t *z,
+                       int64_t N, int Hq, int d, const float *gain_local,
+                       const float *gain_global, double eps, const double *dout, double *dol,
+                       double *dog, double *delta_l, double *delta_g, double *dgate,
+                       double *dgain_l, double *dgain_g)
+{
+    memset(dgain_l, 0, (size_t)Hq * d * sizeof(double));
+    memset(dgain_g, 0, (size_t)Hq * d * sizeof(double));
+    for (int64_t t = 0; t < N; t++) {
+        const double p = (double)gate[t];
+        double dp = 0.0;
+        for (int h = 0; h < Hq; h++) {
+            const int64_t off = (t * Hq + h) * (int64_t)d;
+            const double *dr = dout + off;
+            for (int branch = 0; branch < 2; branch++) {
+                const double *o = (branch ? og : ol) + off;
+                double *dO = (branch ? dog : dol) + off;
+                double *delta = branch ? delta_g : delta_l;
+                double *dgn = branch ? dgain_g : dgain_l;
+                const float *gn = branch ? gain_global : gain_local;
+                if (branch == 1 && !z[t]) {
+                    for (int c = 0; c < d; c++)
+                        dO[c] = 0.0;
+                    delta[t * Hq + h] = 0.0;
+                    continue;
+                }
+                const double wgt = branch ? p : (z[t] ? 1.0 - p : 1.0);
+                double sq = 0.0;
+                for (int c = 0; c < d; c++)
+                    sq += o[c] * o[c];
+                const double rr = sqrt(sq / (double)d + eps);
+                double proj = 0.0, side = 0.0;
+                for (int c = 0; c < d; c++) {
+                    const double gc = gn ? (double)gn[(int64_t)h * d + c] : 1.0;
+                    const double y = o[c] / rr * gc;
+                    proj += gc * wgt * dr[c] * o[c];
+                    dgn[(int64_t)h * d + c] += wgt * dr[c] * o[c] / rr;
+                    side += (branch ? 1.0 : -1.0) * dr[c] * y;
+                }
+                if (z[t])
+                    dp += side;
+                double dl = 0.0;
+                for (int c = 0; c < d; c++) {
+                    const double gc = gn ? (double)gn[(int64_t)h * d + c] : 1.0;
+                    dO[c] = gc * wgt * dr[c] / rr - o[c] * proj / ((double)d * rr * rr * rr);
+                    dl += dO[c] * o[c];
+                }
+                delta[t * Hq + h] = dl;
+            }
+        }
+        dgate[t] = dp;
+    }
+}

@@ -74,6 +74,8 @@ def _load():
     lib.oracle_logo_bwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, i32,
                                     f32, f64, P, P, f64, P, P, P, P, P, P, P, P, P, P]
     lib.oracle_logo_bwd.restype = i64
+    lib.oracle_fusion_bwd.argtypes = [P, P, P, P, i64, i32, i32, P, P, f64, P, P, P, P, P, P, P,
+                                      P]
     lib.oracle_branch_transform.argtypes = [P, i32, i32, i32, P, P, P, P, i64, P]
     _lib = lib
     return lib
@@ -316,3 +318,24 @@ def logo_bwd(q, k, v, gate, cu_seqlens, window: int, dout, *, ratio: Optional[fl
     else:
         r.update(dq=dq[:N], dk=dk[:N], dv=dv[:N], dq_g=dq_g[:N], dk_g=dk_g[:N], dv_g=dv_g[:N])
     return r
+
+
+def fusion_bwd(o_local, o_global_by_token, gate, z, dout, *, gain_local=None, gain_global=None,
+               eps: float = 1e-6) -> Dict[str, np.ndarray]:
+    """Backward of ContextNorm + fusion only: raw branch outputs [N, Hq, d]
+    (the global one indexed by token, used where z), gate [N], z [N] bool,
+    dout [N, Hq, d] -> dol, dog, delta_l, delta_g, dgate, dgain_local/global."""
+    ol, og = _c(o_local, np.float64), _c(o_global_by_token, np.float64)
+    gate, zz = _c(gate, np.float32), _c(np.asarray(z).astype(np.int32), np.int32)
+    dout = _c(dout, np.float64)
+    N, Hq, d = ol.shape
+    dol, dog = np.empty_like(ol), np.empty_like(ol)
+    dl, dg = np.empty((N, Hq)), np.empty((N, Hq))
+    dgate = np.empty(N)
+    gl, gg = np.empty((Hq, d)), np.empty((Hq, d))
+    _load().oracle_fusion_bwd(_ptr(ol), _ptr(og), _ptr(gate), _ptr(zz), N, Hq, d,
+                              _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)),
+                              float(eps), _ptr(dout), _ptr(dol), _ptr(dog), _ptr(dl), _ptr(dg),
+                              _ptr(dgate), _ptr(gl), _ptr(gg))
+    return dict(dol=dol, dog=dog, delta_l=dl, delta_g=dg, dgate=dgate, dgain_local=gl,
+                dgain_global=gg)

@@ -80,6 +80,11 @@ MUTATIONS = {
                                    "dG[h * d + c] += dy[c] * o[c];"),
     "bwd_window_w_plus_1_keys": ("(branch == 0 && i - window + 1 > 0) ? i - window + 1 : 0",
                                  "(branch == 0 && i - window > 0) ? i - window : 0"),
+    "fusion_bwd_projection_ignores_weight": ("proj += gc * wgt * dr[c] * o[c];",
+                                             "proj += gc * dr[c] * o[c];"),
+    "fusion_bwd_dgate_sign": ("side += (branch ? 1.0 : -1.0) * dr[c] * y;",
+                              "side += (branch ? -1.0 : 1.0) * dr[c] * y;"),
+    "fusion_bwd_delta_uses_dout": ("dl += dO[c] * o[c];", "dl += dr[c] * o[c];"),
 }
 
 

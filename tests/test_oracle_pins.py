@@ -704,3 +704,38 @@ def test_backward_invariants(oracle_lib):
     assert 0 < sel < N
     t2s = oracle_lib.logo_fwd(q, k, v, gate, cu, w, ratio=0.4)["tok2sel"]
     assert not r["dgate"][t2s < 0].any() and not r["dq_g"][t2s < 0].any()
+
+
+def test_fusion_bwd_finite_differences(oracle_lib):
+    """ContextNorm + fusion backward against central differences of a numpy
+    fp64 forward of Eqs. contextnorm / output-fusion."""
+    rng = np.random.default_rng(960)
+    N, Hq, d, eps = 7, 3, 8, 1e-3
+    ol, og = rng.standard_normal((N, Hq, d)), rng.standard_normal((N, Hq, d))
+    gate = rng.uniform(0.1, 0.9, N).astype(np.float32)
+    z = np.array([1, 0, 1, 1, 0, 0, 1], bool)
+    gl = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32)
+    gg = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32)
+    dout = rng.standard_normal((N, Hq, d))
+    r = oracle_lib.fusion_bwd(ol, og, gate, z, dout, gain_local=gl, gain_global=gg, eps=eps)
+
+    def fwd(ol_, og_, p_, gl_, gg_):
+        nl = ol_ / np.sqrt((ol_ ** 2).mean(-1, keepdims=True) + eps) * gl_[None]
+        ng = og_ / np.sqrt((og_ ** 2).mean(-1, keepdims=True) + eps) * gg_[None]
+        pw = p_[:, None, None]
+        return np.where(z[:, None, None], (1 - pw) * nl + pw * ng, nl)
+
+    base = [ol, og, gate.astype(np.float64), gl.astype(np.float64), gg.astype(np.float64)]
+    names = ["dol", "dog", "dgate", "dgain_local", "dgain_global"]
+    h = 1e-6
+    for idx, name in enumerate(names):
+        U = rng.standard_normal(base[idx].shape)
+        plus, minus = list(base), list(base)
+        plus[idx] = base[idx] + h * U
+        minus[idx] = base[idx] - h * U
+        fd = ((dout * fwd(*plus)).sum() - (dout * fwd(*minus)).sum()) / (2 * h)
+        an = float((r[name] * U).sum())
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+    np.testing.assert_allclose(r["delta_l"], (r["dol"] * ol).sum(-1), atol=1e-12)
+    np.testing.assert_allclose(r["delta_g"], (r["dog"] * og).sum(-1), atol=1e-12)
+    assert not r["dog"][~z].any() and not r["dgate"][~z].any()
