@@ -69,7 +69,9 @@ typedef enum {
     LOGO_ENTRY_COMBINE = 3,
     LOGO_ENTRY_FWD = 4,
     LOGO_ENTRY_DENSE = 5,
-    LOGO_ENTRY_DECODE = 6
+    LOGO_ENTRY_DECODE = 6,
+    LOGO_ENTRY_FWD_TRAIN = 7,
+    LOGO_ENTRY_BWD = 8
 } logo_entry;
 
 /* Problem description (a host struct; only cu_seqlens is a device pointer). */
@@ -223,6 +225,74 @@ logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
                                    int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
                                    int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
                                    logo_stream stream, void *const *events);
+
+/*
+ * logo_attn_fwd_train -- the layer forward for training: the same output as
+ * logo_attn_fwd, computed through the unfused path (select, raw local
+ * branch, raw global branch, logo_combine), keeping what logo_attn_bwd
+ * needs.  The selection outputs are required here (they are the saved
+ * routing decision of Sec. 3.3, held fixed by the backward pass).
+ *   sel_idx [sel_capacity], cu_sel [B+1], tok2sel [N]: as for logo_select
+ *   (sel_idx may be NULL only when sel_capacity is 0); thr_out [B] or NULL.
+ *   o_local  [N][Hq][d] fp32: raw O^L (Eq. branch-attention, local context).
+ *   lse_local [Hq][N] fp32: per (head, token) the base-2 log-sum-exp of the
+ *            scaled scores, log2 sum_j 2^(c s_j) with c = softmax_scale *
+ *            log2(e) over the keys of the row's window.
+ *   o_global [sel_capacity][Hq][d] fp32, lse_global [Hq][sel_capacity]:
+ *            the same for the selected rows of the global branch (Eq.
+ *            query-sparse-global), compact in rank order.
+ *   Everything else as for logo_attn_fwd.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD_TRAIN, sel_capacity) bytes,
+ *   256-byte aligned.
+ */
+logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                                const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                float threshold, double ratio, const float *gain_local,
+                                const float *gain_global, float eps, logo_bf16 *out,
+                                int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                                int32_t *tok2sel, float *thr_out, float *o_local,
+                                float *lse_local, float *o_global, float *lse_global, void *ws,
+                                size_t ws_bytes, logo_stream stream);
+
+/*
+ * logo_attn_bwd -- gradients of the layer given dL/d out, with the routing
+ * decision z held fixed (it is a hard threshold, Eq. gate-routing; the
+ * gate receives its gradient through the fusion weight p_t of Eq.
+ * output-fusion).  The chain rule runs through Eq. output-fusion, Eq.
+ * contextnorm and the two attentions (Eq. branch-attention with the local
+ * window; Eq. query-sparse-global, whose backward visits the selected rows
+ * only: App. B, backward traversal).
+ *   Inputs: the forward's tensors and gains, and the saved outputs of
+ *   logo_attn_fwd_train (sel_idx, sel_capacity, cu_sel, tok2sel, o_local,
+ *   lse_local, o_global, lse_global); dout [N][Hq][d] bf16 = dL/d out.
+ *   Outputs (fp32, row-major like the inputs, overwritten):
+ *     dq [N][Hq][d], dk, dv [N][Hkv][d]: gradients of the local-branch
+ *       tensors.  Where a global-branch tensor is NULL (it aliases the local
+ *       one), its gradient is added in here and its d*_g must be NULL.
+ *     dq_g, dk_g, dv_g: gradients of q_g, k_g, v_g when those are given
+ *       (each must be non-NULL exactly when its tensor is); rows of dq_g of
+ *       unselected tokens are zero.
+ *     dgate [N] or NULL: dL/dp_t (zero for unselected tokens).
+ *     dgain_local, dgain_global [Hq][d] or NULL: gain gradients (the gains
+ *       themselves may be NULL, meaning 1).
+ *   Numerics: P and dS are recomputed from lse and rounded to bf16 for the
+ *   matrix products (fp32 accumulation); dO of each branch is rounded to
+ *   bf16 once.
+ *   Limits: Hq * d / 8 must be <= 256 or 512 or 1024 (Hq * d <= 8192).
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_BWD, sel_capacity) bytes,
+ *   256-byte aligned.
+ */
+logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                          const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                          const logo_bf16 *v_g, const float *gate, const float *gain_local,
+                          const float *gain_global, float eps, const int32_t *sel_idx,
+                          int32_t sel_capacity, const int32_t *cu_sel, const int32_t *tok2sel,
+                          const float *o_local, const float *lse_local, const float *o_global,
+                          const float *lse_global, const logo_bf16 *dout, float *dq, float *dk,
+                          float *dv, float *dq_g, float *dk_g, float *dv_g, float *dgate,
+                          float *dgain_local, float *dgain_global, void *ws, size_t ws_bytes,
+                          logo_stream stream);
 
 /*
  * logo_dense_causal_attn -- dense causal softmax attention for every token

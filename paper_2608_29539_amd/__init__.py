@@ -8,10 +8,12 @@ the library; the first call does, and raises if it is missing (build it with
 ``paper_2608_29539_amd.build.build_library()``).
 """
 from .binding import (  # noqa: F401
+    LOGO_ENTRY_BWD,
     LOGO_ENTRY_COMBINE,
     LOGO_ENTRY_DECODE,
     LOGO_ENTRY_DENSE,
     LOGO_ENTRY_FWD,
+    LOGO_ENTRY_FWD_TRAIN,
     LOGO_ENTRY_GLOBAL,
     LOGO_ENTRY_LOCAL,
     LOGO_ENTRY_SELECT,
@@ -25,7 +27,9 @@ from .binding import (  # noqa: F401
     exported_symbols,
     library,
     library_path,
+    logo_attn_bwd,
     logo_attn_fwd,
+    logo_attn_fwd_train,
     logo_branch_transform,
     logo_budget_update,
     logo_combine,

@@ -25,6 +25,8 @@ LOGO_ENTRY_COMBINE = 3
 LOGO_ENTRY_FWD = 4
 LOGO_ENTRY_DENSE = 5
 LOGO_ENTRY_DECODE = 6
+LOGO_ENTRY_FWD_TRAIN = 7
+LOGO_ENTRY_BWD = 8
 LOGO_PHI_LP = 0
 LOGO_PHI_SO = 1
 
@@ -34,6 +36,7 @@ EXPORTS = (
     "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
     "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
     "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
+    "logo_attn_fwd_train", "logo_attn_bwd",
 )
 
 _lib = None
@@ -91,6 +94,10 @@ def library():
         "logo_decode": [PP, P, P, P, P, P, P, P, i32, f32, P, P, P, f32, P, P, P, P, sz, P],
         "logo_gate_proj": [i64, i32, P, P, P, P],
         "logo_branch_transform": [i64, i32, i32, ctypes.c_int, P, P, P, P, P, i64, P, P, P],
+        "logo_attn_fwd_train": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P,
+                                P, P, P, P, P, P, P, sz, P],
+        "logo_attn_bwd": [PP, P, P, P, P, P, P, P, P, P, f32, P, i32, P, P, P, P, P, P, P, P, P,
+                          P, P, P, P, P, P, P, P, sz, P],
     }
     for name, args in sigs.items():
         fn = getattr(lib, name)
@@ -371,6 +378,85 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
         handles = (ctypes.c_void_p * 5)(*[ctypes.c_void_p(e.cuda_event) for e in events])
         _call("logo_attn_fwd_profiled", *args, handles)
     return out, sel_idx, cu_sel, tok2sel, thr_out
+
+
+def logo_attn_fwd_train(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None,
+                        threshold: Optional[float] = None, threshold_device=None, q_g=None,
+                        k_g=None, v_g=None, gain_local=None, gain_global=None,
+                        eps: float = 1e-6, sel_capacity: Optional[int] = None, ws=None) -> dict:
+    """Training forward of the layer.  Returns a dict with ``out`` and the
+    saved state the backward needs: sel_idx, cu_sel, tok2sel, thr_out,
+    o_local, lse_local, o_global, lse_global, sel_capacity."""
+    import torch
+    N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
+                        prob.num_seqs)
+    mode, thr_dev = _sel_mode(ratio, threshold, threshold_device, B)
+    dev = q.device
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    for t, nm, shp in ((q_g, "q_g", (N, Hq, d)), (k_g, "k_g", (N, Hkv, d)),
+                       (v_g, "v_g", (N, Hkv, d))):
+        if t is not None:
+            _check(t, torch.bfloat16, shp, nm)
+    _check(gate, torch.float32, (N,), "gate")
+    if sel_capacity is None:
+        sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
+    cap = max(int(sel_capacity), 1)
+    f32 = dict(dtype=torch.float32, device=dev)
+    st = dict(
+        out=torch.empty((N, Hq, d), dtype=torch.bfloat16, device=dev),
+        sel_idx=torch.empty(cap, dtype=torch.int32, device=dev),
+        cu_sel=torch.empty(B + 1, dtype=torch.int32, device=dev),
+        tok2sel=torch.empty(max(N, 1), dtype=torch.int32, device=dev),
+        thr_out=thr_dev if thr_dev is not None else torch.empty(B, **f32),
+        o_local=torch.empty((max(N, 1), Hq, d), **f32),
+        lse_local=torch.empty((Hq, max(N, 1)), **f32),
+        o_global=torch.empty((cap, Hq, d), **f32),
+        lse_global=torch.empty((Hq, cap), **f32),
+        sel_capacity=cap)
+    ws, nbytes = _ws(prob, LOGO_ENTRY_FWD_TRAIN, cap, ws)
+    _call("logo_attn_fwd_train", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g),
+          _ptr(v_g), _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
+          float(ratio if ratio is not None else 0.0), _ptr(gain_local), _ptr(gain_global),
+          float(eps), _ptr(st["out"]), _ptr(st["sel_idx"]), cap, _ptr(st["cu_sel"]),
+          _ptr(st["tok2sel"]), _ptr(st["thr_out"]), _ptr(st["o_local"]), _ptr(st["lse_local"]),
+          _ptr(st["o_global"]), _ptr(st["lse_global"]), _ptr(ws), nbytes, _stream())
+    return st
+
+
+def logo_attn_bwd(prob: Problem, q, k, v, gate, saved: dict, dout, *, q_g=None, k_g=None,
+                  v_g=None, gain_local=None, gain_global=None, eps: float = 1e-6,
+                  dgain: bool = True, ws=None) -> dict:
+    """Gradients of the layer given dout = dL/d out (bf16 [N, Hq, d]) and the
+    ``saved`` dict of ``logo_attn_fwd_train``.  Returns fp32 dq, dk, dv (the
+    global branch's share added in where its tensor is not given), dq_g /
+    dk_g / dv_g for the given global tensors, dgate and (with ``dgain``)
+    dgain_local / dgain_global."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    dev = q.device
+    _check(dout, torch.bfloat16, (N, Hq, d), "dout")
+    f32 = dict(dtype=torch.float32, device=dev)
+    g = dict(dq=torch.empty((N, Hq, d), **f32), dk=torch.empty((N, Hkv, d), **f32),
+             dv=torch.empty((N, Hkv, d), **f32), dgate=torch.empty(max(N, 1), **f32))
+    for t, nm, shp in ((q_g, "dq_g", (N, Hq, d)), (k_g, "dk_g", (N, Hkv, d)),
+                       (v_g, "dv_g", (N, Hkv, d))):
+        g[nm] = torch.empty(shp, **f32) if t is not None else None
+    if dgain:
+        g["dgain_local"] = torch.empty((Hq, d), **f32)
+        g["dgain_global"] = torch.empty((Hq, d), **f32)
+    cap = int(saved["sel_capacity"])
+    ws, nbytes = _ws(prob, LOGO_ENTRY_BWD, cap, ws)
+    _call("logo_attn_bwd", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g), _ptr(v_g),
+          _ptr(gate), _ptr(gain_local), _ptr(gain_global), float(eps), _ptr(saved["sel_idx"]),
+          cap, _ptr(saved["cu_sel"]), _ptr(saved["tok2sel"]), _ptr(saved["o_local"]),
+          _ptr(saved["lse_local"]), _ptr(saved["o_global"]), _ptr(saved["lse_global"]),
+          _ptr(dout), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(g["dq_g"]),
+          _ptr(g["dk_g"]), _ptr(g["dv_g"]), _ptr(g["dgate"]), _ptr(g.get("dgain_local")),
+          _ptr(g.get("dgain_global")), _ptr(ws), nbytes, _stream())
+    g["dgate"] = g["dgate"][:N]
+    return {kk: vv for kk, vv in g.items() if vv is not None}
 
 
 def logo_dense_causal_attn(prob: Problem, q, k, v, out=None):

@@ -28,21 +28,12 @@
 // window edge (real-position mask on each score).
 #include "logo_internal.h"
 #include "plan.h"
+#include "attn_common.h"
 
 #include <type_traits>
 
 namespace logo {
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-constexpr float kNegInf = -__builtin_inff();
 
 // Real-position masks of a KV tile (bit set).
 constexpr int kMaskNone = 0, kMaskCausal = 1, kMaskWindow = 2;
@@ -64,19 +55,6 @@ __device__ __forceinline__ constexpr int vswz(int r) {
     // rows per 256-byte bank window: 128 / D; segments per row: D / 32
     return (r / (128 / D)) % (D / 32);
 }
-
-// Value of the partner lane (l ^ 32) and own value, combined.
-__device__ __forceinline__ float pair_max(float x) {
-    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair_sum(float x) {
-    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// Buffer resource word 3 for raw (untyped, stride 0) buffer loads.
-constexpr int kRawBufferFlags = 0x00020000;
 
 // K/V tiles go global -> LDS directly (buffer_load_dwordx4 ... lds): each
 // wave-instruction writes 64 consecutive 16-byte LDS slots (lane i at
@@ -120,34 +98,7 @@ __device__ __forceinline__ void dma_plan(Dma<D, W> &d, int wave, int lane, int r
 // flags.
 __device__ __forceinline__ u32x4 tile_rsrc(const uint16_t *kv, int T, int k0, int row_bytes) {
     const int rows = min(kBlockN, T - k0);
-    const int nbytes = rows > 0 ? rows * row_bytes : 0;
-    const uint64_t p = (uint64_t)((const char *)kv + (long long)k0 * row_bytes);
-    u32x4 r;
-    r[0] = __builtin_amdgcn_readfirstlane((uint32_t)p);
-    r[1] = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) & 0xFFFFu;
-    r[2] = __builtin_amdgcn_readfirstlane(nbytes);
-    r[3] = kRawBufferFlags;
-    return r;
-}
-
-// One 16-byte-per-lane global -> LDS load.  Issued as inline assembly so that
-// the compiler does not make every later LDS read wait for it: the tile it
-// fills is only read after the wait + barrier that ends the pipeline step,
-// while the reads in between go to the other buffer.  M0 (the LDS base of
-// the load) is saved and restored around it.
-__device__ __forceinline__ void lds_load16(u32x4 r, const void *lds, int voffset) {
-    const uint32_t lds_addr = __builtin_amdgcn_readfirstlane(
-        (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds);
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %1\n\t"
-        "s_nop 0\n\t"
-        "buffer_load_dwordx4 %2, %3, 0 offen lds\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "s"(lds_addr), "v"(voffset), "s"(r)
-        : "memory");
+    return raw_rsrc((const char *)kv + (long long)k0 * row_bytes, rows > 0 ? rows * row_bytes : 0);
 }
 
 template <int D, int W>
@@ -173,20 +124,6 @@ __device__ __forceinline__ void dma_v(uint16_t *dst, const Dma<D, W> &d, const u
     }
 }
 
-// s_waitcnt operand that waits for vmcnt = 0 only (lgkmcnt and expcnt at
-// their maximum).  Issued through the builtin so the compiler knows that no
-// vector-memory load is outstanding afterwards.
-constexpr int kWaitVmcnt0 = 0x0F70;
-
-// Completion of this wave's LDS-bound loads, then the workgroup barrier.
-__device__ __forceinline__ void dma_wait_barrier() {
-    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-    __syncthreads();
-}
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
 // V^T operand of the O^T MFMA straight from the row-major V tile with the
 // gfx950 LDS transpose read: within each 16-lane group, lane 4b+e receives
 // element e of the 4-element rows addressed by lanes b, b+4, b+8, b+12.
@@ -196,18 +133,7 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // (second read): the 8 keys of its MFMA k-slice, in the order the S^T
 // accumulator (and so P^T) holds them.
 __device__ __forceinline__ bf16x8 read_vt_frag(const uint16_t *vrow_lane, int row_stride) {
-    const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)vrow_lane);
-    const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)(vrow_lane + 8 * row_stride));
-    const s16x4 ab[2] = {a, b};
-    return __builtin_bit_cast(bf16x8, ab);
-}
-
-// Two fp32 -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
-__device__ __forceinline__ bf16x2 cvt_bf16x2(float a, float b) {
-    return __builtin_convertvector(f32x2{a, b}, bf16x2);
-}
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-    return __builtin_bit_cast(uint32_t, cvt_bf16x2(a, b));
+    return lds_tr_pair(vrow_lane, vrow_lane + 8 * row_stride);
 }
 
 // Attention for one work item: a tile of rows x the heads of one head group.
@@ -223,9 +149,6 @@ constexpr float kLazy = 8.f;
 // feeds one MFMA per row group.
 constexpr int RG = kRowsPerWave / 32;
 
-// Wave-uniform value, made explicit so the compiler keeps it in SGPRs.
-__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
 // Split-KV partials of the global branch.  Every entry of a split tile
 // stores its unnormalised O (relative to its reference m, exp2 domain), m
 // and l per lane, releases them, and counts itself done; the entry that
@@ -235,7 +158,7 @@ __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlan
 template <int D>
 __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile &t, int hg,
                                             int wave, int lane, f32x16 (&acc)[RG][D / 32],
-                                            const float (&m)[RG], float (&l)[RG]) {
+                                            float (&m)[RG], float (&l)[RG]) {
     __shared__ int s_last;
     constexpr int kLanes = kWavesGlobal * 64;
     constexpr int kAccFloats = kLanes * RG * (D / 2);
@@ -294,6 +217,7 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
             M = mn;
         }
         l[rg] = L;
+        m[rg] = M;
     }
     return true;
 }
@@ -745,6 +669,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
                     *(u32x2 *)(op + cb * 32 + qd * 8) = v;
                 }
         } else {
+            // training forward: the row's base-2 log-sum-exp of the scaled
+            // scores, log2(sum_j 2^(c s_j)) = m + log2(l)
+            if (a.lse && g == 0)
+                a.lse[(int64_t)head * a.lse_stride + orow[rg]] =
+                    (m_ref[rg] == kNegInf ? 0.f : m_ref[rg]) + log2f(l_tot[rg]);
             float *op = (float *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
             for (int cb = 0; cb < D / 32; cb++)

@@ -66,10 +66,12 @@ logo_status check_problem(const logo_problem *p) {
     return LOGO_OK;
 }
 
+double softmax_scale(const logo_problem *p) {
+    return p->softmax_scale > 0.f ? (double)p->softmax_scale : 1.0 / std::sqrt((double)p->head_dim);
+}
+
 float scale_log2(const logo_problem *p) {
-    const double s = p->softmax_scale > 0.f ? (double)p->softmax_scale
-                                            : 1.0 / std::sqrt((double)p->head_dim);
-    return (float)(s * 1.4426950408889634);   // log2(e)
+    return (float)(softmax_scale(p) * 1.4426950408889634);   // log2(e)
 }
 
 AttnArgs make_args(const logo_problem *p, const TilePlan &tp) {
@@ -162,6 +164,81 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
 // Decoding: keys per chunk (a multiple of 32, at least 256, at most 128
 // chunks per cache), query heads per work item (the largest of 4, 2, 1
 // dividing the group), and the workspace of the partial results.
+// logo_attn_fwd_train: selection scratch, the global branch's work table
+// and the thresholds when thr_out is NULL.
+struct TrainWs {
+    size_t sel_ws, glob_ws, thr, total;
+};
+TrainWs train_ws(const logo_problem *p, int32_t cap) {
+    TrainWs w;
+    size_t off = 0;
+    w.sel_ws = off;
+    off += align_up(select_ws(p).total);
+    w.glob_ws = off;
+    off += align_up(global_ws(p, cap).total);
+    w.thr = off;
+    off += align_up(sizeof(float) * (size_t)p->num_seqs);
+    w.total = off;
+    return w;
+}
+
+// logo_attn_bwd: dO^L / dO^G (bf16), the compact Q^G rows, the row sums
+// Delta, the per-row gate terms and the gain-gradient partials.
+constexpr int kFusionBwdMaxBlocks = 1024;
+struct BwdWs {
+    size_t dol, dog, qc, delta_l, delta_g, side, part_l, part_g, total;
+    int blocks, tokens_per_block, part_rows;
+};
+BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
+    const size_t N = (size_t)p->total_tokens, H = (size_t)p->num_q_heads, d = p->head_dim;
+    const int P = fusion_bwd_tokens_per_pass(p->num_q_heads, p->head_dim);
+    const long long passes = ((long long)N + P - 1) / P;
+    BwdWs w;
+    w.blocks = (int)(passes < kFusionBwdMaxBlocks ? passes : kFusionBwdMaxBlocks);
+    if (w.blocks < 1)
+        w.blocks = 1;
+    w.tokens_per_block = (int)((passes + w.blocks - 1) / w.blocks) * P;
+    w.part_rows = w.blocks * P;
+    size_t off = 0;
+    w.dol = off;
+    off += align_up(2 * N * H * d);
+    w.dog = off;
+    off += align_up(2 * (size_t)cap * H * d);
+    w.qc = off;
+    off += align_up(2 * (size_t)cap * H * d);
+    w.delta_l = off;
+    off += align_up(4 * H * N);
+    w.delta_g = off;
+    off += align_up(4 * H * (size_t)cap);
+    w.side = off;
+    off += align_up(4 * N * H);
+    w.part_l = off;
+    off += align_up(4 * (size_t)w.part_rows * H * d);
+    w.part_g = off;
+    off += align_up(4 * (size_t)w.part_rows * H * d);
+    w.total = off;
+    return w;
+}
+
+BwdArgs make_bwd_args(const logo_problem *p) {
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
+    BwdArgs a;
+    std::memset(&a, 0, sizeof a);
+    a.cu_seqlens = p->cu_seqlens;
+    a.num_seqs = p->num_seqs;
+    a.hq = p->num_q_heads;
+    a.hkv = p->num_kv_heads;
+    a.group = p->num_q_heads / p->num_kv_heads;
+    a.hpw = tp.hpw;
+    a.tpw = tp.tpw;
+    a.n_hg = tp.n_hg;
+    a.window = p->window;
+    a.ntile_max = (p->max_seqlen + tp.tpw - 1) / tp.tpw;
+    a.scale_log2 = scale_log2(p);
+    a.scale = (float)softmax_scale(p);
+    return a;
+}
+
 struct DecodePlan {
     int kc, gh, nhg, chunks_local, chunks_global;
     long long n_local_items, n_global_items;
@@ -309,7 +386,7 @@ void set_fused(AttnArgs &a, const FusedEpi *f, const float *gain) {
 // global branch's work table.
 logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                       const logo_bf16 *v, float *o, const FusedEpi *f, const float *gain,
-                      hipStream_t s, const PlanArgs *plan = nullptr) {
+                      hipStream_t s, const PlanArgs *plan = nullptr, float *lse = nullptr) {
     if (p->total_tokens == 0)
         return LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
@@ -318,6 +395,8 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
     a.k = k;
     a.v = v;
     a.out = o;
+    a.lse = lse;
+    a.lse_stride = p->total_tokens;
     if (f)
         set_fused(a, f, gain);
     if (f && plan) {
@@ -334,7 +413,8 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                        const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
                        int32_t cap, float *o, const FusedEpi *f, const float *gain, char *ws,
-                       hipStream_t s, hipEvent_t after_plan = nullptr, bool plan_done = false) {
+                       hipStream_t s, hipEvent_t after_plan = nullptr, bool plan_done = false,
+                       float *lse = nullptr) {
     if (p->total_tokens == 0 || cap == 0)
         return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
@@ -361,6 +441,8 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     a.queue = pa.queue;
     a.split_cnt = pa.split_cnt;
     a.partial = (float *)(ws + w.partial);
+    a.lse = lse;
+    a.lse_stride = cap;
     if (f)
         set_fused(a, f, gain);
     return hip_status(
@@ -493,6 +575,8 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_GLOBAL: return global_ws(p, cap).total;
     case LOGO_ENTRY_FWD: return fwd_ws(p, cap).total;
     case LOGO_ENTRY_DECODE: return decode_plan(p).total;
+    case LOGO_ENTRY_FWD_TRAIN: return train_ws(p, cap).total;
+    case LOGO_ENTRY_BWD: return bwd_ws(p, cap).total;
     case LOGO_ENTRY_LOCAL:
     case LOGO_ENTRY_COMBINE:
     case LOGO_ENTRY_DENSE: return 0;
@@ -740,6 +824,186 @@ logo_status logo_branch_transform(int64_t n_tokens, int32_t num_heads, int32_t h
     return hip_status(launch_branch_transform((int)kind, n_rows, num_heads, head_dim, u, A, s, b,
                                               rows, n_rows_dev, u_g, st),
                       st);
+}
+
+logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                                const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                float threshold, double ratio, const float *gain_local,
+                                const float *gain_global, float eps, logo_bf16 *out,
+                                int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                                int32_t *tok2sel, float *thr_out, float *o_local,
+                                float *lse_local, float *o_global, float *lse_global, void *ws,
+                                size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (!gate || !cu_sel)
+        return LOGO_ERR_NULL;
+    if (p->total_tokens > 0 &&
+        (!q || !k || !v || !out || !tok2sel || !o_local || !lse_local))
+        return LOGO_ERR_NULL;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    if (sel_capacity > 0 && (!sel_idx || !o_global || !lse_global))
+        return LOGO_ERR_NULL;
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    const int32_t cap = sel_capacity;
+    const TrainWs w = train_ws(p, cap);
+    st = check_ws(ws, ws_bytes, w.total);
+    if (st != LOGO_OK)
+        return st;
+    char *base = (char *)ws;
+    float *thr = thr_out ? thr_out : (float *)(base + w.thr);
+    st = check_select_args(p, gate, mode, threshold, ratio, sel_idx, cap, cu_sel, thr_out);
+    if (st != LOGO_OK)
+        return st;
+    hipStream_t s = (hipStream_t)stream;
+    st = run_select(p, gate, mode, threshold, ratio, sel_idx, cap, cu_sel, tok2sel, thr,
+                    base + w.sel_ws, s);
+    if (st != LOGO_OK)
+        return st;
+    st = run_local(p, q, k, v, o_local, nullptr, nullptr, s, nullptr, lse_local);
+    if (st != LOGO_OK)
+        return st;
+    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel_idx, cu_sel, cap,
+                    o_global, nullptr, nullptr, base + w.glob_ws, s, nullptr, false, lse_global);
+    if (st != LOGO_OK)
+        return st;
+    return hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, o_local,
+                                     cap > 0 ? o_global : nullptr, gate, tok2sel, gain_local,
+                                     gain_global, eps, 1, out, s),
+                      s);
+}
+
+logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                          const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                          const logo_bf16 *v_g, const float *gate, const float *gain_local,
+                          const float *gain_global, float eps, const int32_t *sel_idx,
+                          int32_t sel_capacity, const int32_t *cu_sel, const int32_t *tok2sel,
+                          const float *o_local, const float *lse_local, const float *o_global,
+                          const float *lse_global, const logo_bf16 *dout, float *dq, float *dk,
+                          float *dv, float *dq_g, float *dk_g, float *dv_g, float *dgate,
+                          float *dgain_local, float *dgain_global, void *ws, size_t ws_bytes,
+                          logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (!cu_sel)
+        return LOGO_ERR_NULL;
+    if ((q_g == nullptr) != (dq_g == nullptr) || (k_g == nullptr) != (dk_g == nullptr) ||
+        (v_g == nullptr) != (dv_g == nullptr))
+        return LOGO_ERR_ARG;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    const int32_t N = p->total_tokens;
+    if (N > 0 && (!q || !k || !v || !gate || !tok2sel || !o_local || !lse_local || !dout ||
+                  !dq || !dk || !dv))
+        return LOGO_ERR_NULL;
+    if (N > 0 && sel_capacity > 0 && (!sel_idx || !o_global || !lse_global))
+        return LOGO_ERR_NULL;
+    if (!(eps >= 0.f) || std::isinf(eps))
+        return LOGO_ERR_ARG;
+    if (!fusion_bwd_supported(p->num_q_heads, p->head_dim))
+        return LOGO_ERR_UNSUPPORTED;
+    const int32_t cap = sel_capacity;
+    const BwdWs w = bwd_ws(p, cap);
+    st = check_ws(ws, ws_bytes, w.total);
+    if (st != LOGO_OK)
+        return st;
+    if (N == 0)
+        return LOGO_OK;
+    char *base = (char *)ws;
+    hipStream_t s = (hipStream_t)stream;
+    const int H = p->num_q_heads, d = p->head_dim;
+    const logo_bf16 *qg = q_g ? q_g : q;
+
+    // 1. ContextNorm + fusion backward (and the compact Q^G rows)
+    FusionBwdArgs f;
+    std::memset(&f, 0, sizeof f);
+    f.ol = o_local;
+    f.og = o_global;
+    f.dout = dout;
+    f.q_g = qg;
+    f.gate = gate;
+    f.tok2sel = tok2sel;
+    f.gain_l = gain_local;
+    f.gain_g = gain_global;
+    f.eps = eps;
+    f.n = N;
+    f.hq = H;
+    f.cap = cap;
+    f.tokens_per_block = w.tokens_per_block;
+    f.dol = (uint16_t *)(base + w.dol);
+    f.dog = (uint16_t *)(base + w.dog);
+    f.qc = (uint16_t *)(base + w.qc);
+    f.delta_l = (float *)(base + w.delta_l);
+    f.delta_g = (float *)(base + w.delta_g);
+    f.side = (float *)(base + w.side);
+    f.part_l = dgain_local ? (float *)(base + w.part_l) : nullptr;
+    f.part_g = dgain_global ? (float *)(base + w.part_g) : nullptr;
+    st = hip_status(launch_fusion_bwd(f, w.blocks, d, s), s);
+    if (st == LOGO_OK && dgate)
+        st = hip_status(launch_gate_grad(N, H, f.side, dgate, s), s);
+    if (st == LOGO_OK && dgain_local)
+        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_l, dgain_local, s), s);
+    if (st == LOGO_OK && dgain_global)
+        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_g, dgain_global, s), s);
+    if (st != LOGO_OK)
+        return st;
+
+    // 2. local branch: dQ, dK, dV (overwrite)
+    BwdArgs a = make_bwd_args(p);
+    a.cap = cap;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.dout = f.dol;
+    a.lse = lse_local;
+    a.delta = f.delta_l;
+    a.row_stride = N;
+    a.sel_idx = sel_idx;
+    a.cu_sel = cu_sel;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    const long long grid_q = (long long)a.n_hg * p->num_seqs * a.ntile_max;
+    const int kpb = bwd_keys_per_block();
+    const long long grid_kv =
+        (long long)((p->max_seqlen + kpb - 1) / kpb) * p->num_seqs * p->num_kv_heads;
+    if (grid_q >= (1LL << 31) || grid_kv >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    st = hip_status(launch_bwd_dq(kModeLocal, d, a, (int)grid_q, s), s);
+    if (st == LOGO_OK)
+        st = hip_status(launch_bwd_dkv(kModeLocal, d, a, (int)grid_kv, s), s);
+    if (st != LOGO_OK)
+        return st;
+
+    // 3. global branch: selected rows (compact), dense K/V; added into the
+    //    local gradients where the branch shares the tensor
+    if (dq_g)
+        st = hip_status(launch_fill_zero((int64_t)N * H * d, dq_g, s), s);
+    if (st != LOGO_OK)
+        return st;
+    a.q = f.qc;
+    a.k = k_g ? k_g : k;
+    a.v = v_g ? v_g : v;
+    a.dout = f.dog;
+    a.lse = lse_global;
+    a.delta = f.delta_g;
+    a.row_stride = cap;
+    a.dq = dq_g ? dq_g : dq;
+    a.dk = dk_g ? dk_g : dk;
+    a.dv = dv_g ? dv_g : dv;
+    a.acc_q = dq_g ? 0 : 1;
+    a.acc_k = dk_g ? 0 : 1;
+    a.acc_v = dv_g ? 0 : 1;
+    if (cap > 0)
+        st = hip_status(launch_bwd_dq(kModeGlobal, d, a, (int)grid_q, s), s);
+    if (st == LOGO_OK)
+        st = hip_status(launch_bwd_dkv(kModeGlobal, d, a, (int)grid_kv, s), s);
+    return st;
 }
 
 }  // extern "C"

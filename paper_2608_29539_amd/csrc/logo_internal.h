@@ -129,6 +129,10 @@ struct AttnArgs {
     // branch's work table (`plan`) while the others attend
     int32_t plan_wg;
     PlanArgs plan;
+    // raw epilogue only: lse (or NULL) receives each row's base-2
+    // log-sum-exp of the scaled scores at [head * lse_stride + row]
+    float *lse;
+    int64_t lse_stride;
 };
 
 // Launchers (return hipSuccess or the launch error).
@@ -178,6 +182,44 @@ hipError_t launch_branch_transform(int kind, int64_t n_rows, int H, int d, const
                                    const uint16_t *A, const float *sc, const float *bi,
                                    const int32_t *rows, const int32_t *n_rows_dev, uint16_t *out,
                                    hipStream_t s);
+
+// Backward pass (bwd.hip).  Rows of a branch: local = tokens (row index =
+// token), global = selected rows in rank order (row index = rank, token =
+// sel_idx[rank]).  q / dout are the branch's row-major [rows][Hq][d] bf16
+// tensors (the global branch uses the compact copy of Q^G), lse / delta are
+// [Hq][row_stride] fp32.  acc_*: add into the output instead of overwriting.
+struct BwdArgs {
+    const uint16_t *q, *k, *v, *dout;
+    const float *lse, *delta;
+    const int32_t *cu_seqlens, *sel_idx, *cu_sel;
+    float *dq, *dk, *dv;
+    int32_t num_seqs, hq, hkv, group, hpw, tpw, n_hg, window, ntile_max, cap;
+    int32_t acc_q, acc_k, acc_v;
+    int64_t row_stride;
+    float scale_log2, scale;
+};
+struct FusionBwdArgs {
+    const float *ol, *og;              // raw O^L [N][Hq][d], O^G [cap][Hq][d] (compact)
+    const uint16_t *dout, *q_g;        // [N][Hq][d]
+    const float *gate;
+    const int32_t *tok2sel;
+    const float *gain_l, *gain_g;      // [Hq][d] or NULL
+    float eps;
+    int32_t n, hq, cap, tokens_per_block;
+    uint16_t *dol, *dog, *qc;          // [N][Hq][d], [cap][Hq][d], [cap][Hq][d]
+    float *delta_l, *delta_g;          // [Hq][N], [Hq][cap]
+    float *side;                       // [N][Hq]: row terms of dL/dp
+    float *part_l, *part_g;            // gain-gradient partials or NULL
+};
+int fusion_bwd_tokens_per_pass(int hq, int head_dim);
+bool fusion_bwd_supported(int hq, int head_dim);
+hipError_t launch_fusion_bwd(const FusionBwdArgs &a, int grid, int head_dim, hipStream_t s);
+hipError_t launch_gate_grad(int n, int hq, const float *side, float *dgate, hipStream_t s);
+hipError_t launch_gain_grad(int rows, int cols, const float *part, float *out, hipStream_t s);
+hipError_t launch_fill_zero(int64_t n, float *x, hipStream_t s);
+hipError_t launch_bwd_dq(int mode, int head_dim, const BwdArgs &a, int grid, hipStream_t s);
+hipError_t launch_bwd_dkv(int mode, int head_dim, const BwdArgs &a, int grid, hipStream_t s);
+int bwd_keys_per_block();
 
 // One budget-controller step on the device (b_th += gamma sign(F - rho)).
 hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_tokens, double rho,

@@ -13,6 +13,7 @@ from .logo_inputs import (  # noqa: F401
     bf16_bits_from_f32,
     f32_from_bf16_bits,
     make_decode_inputs,
+    make_dout,
     make_gate_only,
     make_inputs,
     small_workload,

@@ -177,6 +177,13 @@ def make_inputs(w: Workload, *, distinct_global: bool = False) -> Dict[str, np.n
     return out
 
 
+def make_dout(w: Workload, seed: int) -> np.ndarray:
+    """Upstream gradient dL/d out for a backward pass: bf16 bits [N, Hq, d]
+    of N(0,1) draws from its own seeded stream."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([w.seed, seed])))
+    return _normal_bf16(rng, (w.total_tokens, w.num_q_heads, w.head_dim), None)
+
+
 def make_gate_only(w: Workload) -> Dict[str, np.ndarray]:
     """The gate and cu_seqlens of a workload, without drawing Q/K/V.
 

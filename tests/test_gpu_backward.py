@@ -1,0 +1,121 @@
+"""GPU parity of the training forward and the backward pass of the layer
+(selection held fixed): logo_attn_fwd_train and logo_attn_bwd through the C
+ABI against the fp64 oracle's forward and backward.
+
+Bars.  Training forward: the bf16 output within the layer's bar (max-abs
+2e-2, mean-abs 2e-3, times max(gain) when gains are given).  Backward: for every gradient tensor G (dq, dk, dv, the
+global-branch ones, dgate, the gain gradients), against the oracle's G_ref:
+  relative L2 error  ||G - G_ref|| / ||G_ref||  <= 1e-2
+  max-abs error      max |G - G_ref|            <= 2e-2 max |G_ref|
+The kernels round dO, P and dS to bf16 (relative error <= 2^-9 each) for the
+matrix products and accumulate in fp32; a gradient element is a sum of
+products of two or three such rounded factors, so its per-term relative
+error is below 3 * 2^-9 = 0.6%, and sums of many terms with independent
+rounding errors sit well under that in L2.  The bars leave about a factor 2
+over the worst case measured here.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from _support import to_device, torch_bf16_to_f64, err_stats
+
+pytestmark = pytest.mark.gpu
+
+REL_L2, REL_MAX = 1e-2, 2e-2
+
+
+@pytest.fixture(scope="module")
+def pk():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible: the gpu tests need an MI355X")
+    import paper_2608_29539_amd as pk
+    pk.library()
+    oracle.build(force=False)
+    return pk
+
+
+def grad_err(got, ref):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    nref = np.linalg.norm(ref)
+    mref = np.abs(ref).max() if ref.size else 0.0
+    if nref == 0.0:
+        return dict(rel_l2=float(np.linalg.norm(got)), rel_max=float(np.abs(got).max()
+                                                                      if got.size else 0.0))
+    return dict(rel_l2=float(np.linalg.norm(got - ref) / nref),
+                rel_max=float(np.abs(got - ref).max() / mref))
+
+
+def run_case(pk, w, *, ratio=None, threshold=None, distinct=False, gains=False, tag=""):
+    import torch
+    x = synth.make_inputs(w, distinct_global=distinct)
+    dout = synth.make_dout(w, 1)
+    rng = np.random.default_rng(w.seed + 17)
+    gl = rng.uniform(0.5, 1.5, (w.num_q_heads, w.head_dim)).astype(np.float32) if gains else None
+    gg = rng.uniform(0.5, 1.5, (w.num_q_heads, w.head_dim)).astype(np.float32) if gains else None
+    dev = to_device(dict(x, dout=dout))
+    prob = pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
+                      cu_seqlens_host=x["cu_seqlens"])
+    tg = lambda a: torch.from_numpy(a).cuda() if a is not None else None  # noqa: E731
+    kw = dict(q_g=dev.get("q_g"), k_g=dev.get("k_g"), v_g=dev.get("v_g"), gain_local=tg(gl),
+              gain_global=tg(gg), eps=1e-6)
+    print(f"[bwd {tag}] seqlens={w.seqlens} H={w.num_q_heads}/{w.num_kv_heads} "
+          f"d={w.head_dim} w={w.window} ratio={ratio} thr={threshold}", flush=True)
+    saved = pk.logo_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=ratio,
+                                   threshold=threshold, **kw)
+    grads = pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved,
+                             dev["dout"], **kw)
+    torch.cuda.synchronize()
+
+    # forward output against the oracle
+    okw = dict(ratio=ratio, threshold=threshold, q_g=x.get("q_g"), k_g=x.get("k_g"),
+               v_g=x.get("v_g"), gain_local=gl, gain_global=gg, eps=1e-6)
+    fref = oracle.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w.window, **okw)
+    st = err_stats(torch_bf16_to_f64(saved["out"]), fref["out"])
+    # the layer's bar is stated for unit-RMS rows; gains scale the rows (and
+    # so the bf16 rounding of the output) by at most max(gain)
+    gmax = max(float(gl.max()), float(gg.max())) if gains else 1.0
+    assert st["max_abs"] <= 2e-2 * gmax and st["mean_abs"] <= 2e-3 * gmax, (tag, "fwd", st)
+    n_sel = int(saved["cu_sel"].cpu()[-1])
+    assert n_sel == fref["n_sel"], (tag, n_sel, fref["n_sel"])
+
+    dout64 = synth.f32_from_bf16_bits(dout).reshape(dout.shape).astype(np.float64)
+    ref = oracle.logo_bwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w.window, dout64,
+                          **okw)
+    names = ["dq", "dk", "dv", "dgate", "dgain_local", "dgain_global"]
+    if distinct:
+        names += ["dq_g", "dk_g", "dv_g"]
+    worst = {}
+    for nm in names:
+        e = grad_err(grads[nm].cpu().numpy(), ref[nm])
+        worst[nm] = e
+        print(f"[bwd {tag}] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}",
+              flush=True)
+    for nm, e in worst.items():
+        assert e["rel_l2"] <= REL_L2 and e["rel_max"] <= REL_MAX, (tag, nm, e)
+    return grads, ref
+
+
+BWD_CASES = [
+    # (seqlens, Hq, Hkv, d, window, ratio, threshold, distinct, gains)
+    ((300, 1000), 8, 2, 128, 257, 0.25, None, False, True),
+    ((64, 65, 700), 4, 4, 64, 64, None, 0.5, True, False),
+    ((2048,), 16, 2, 128, 1, 0.125, None, False, False),
+    ((129,), 4, 1, 128, 4096, 0.0, None, False, True),
+    ((513, 200), 4, 2, 64, 100, 1.0, None, True, True),
+    ((3000,), 6, 2, 64, 512, 0.5, None, False, False),
+    ((1024, 77), 32, 8, 128, 256, 0.125, None, False, True),
+    ((1, 2, 3, 190), 2, 2, 128, 3, None, -math.inf, False, False),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(BWD_CASES)))
+def test_backward_small(pk, ci):
+    lens, hq, hkv, d, win, ratio, thr, distinct, gains = BWD_CASES[ci]
+    w = synth.small_workload(lens, hq, hkv, d, win, ratio or 0.0, seed=5000 + ci)
+    run_case(pk, w, ratio=ratio, threshold=thr, distinct=distinct, gains=gains, tag=f"case{ci}")
