@@ -10,6 +10,7 @@ from .oracle import (  # noqa: F401
     SEL_RATIO,
     SO,
     SEL_THRESHOLD,
+    attn_bwd,
     attn_rows,
     branch_transform,
     budget_update,

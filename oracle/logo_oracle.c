@@ -807,3 +807,86 @@ void oracle_fusion_bwd(const double *ol, const double *og, const float *gate, co
         dgate[t] = dp;
     }
 }
+
+/*
+ * Backward of plain causal softmax attention (Eq. attention; with window >= 1
+ * the local context of Sec. 3.1, keys max(0, i-w+1)..i; window <= 0 = full
+ * causal): the dense baseline's training step.  Given dout = dL/do
+ * [N][Hq][d] (double) for o_i = sum_j P_ij v_j, P_i = softmax(scale q_i.k_j):
+ *   dv_j += P_ij dout_i,   dP_ij = dout_i . v_j,
+ *   dS_ij = P_ij (dP_ij - sum_k P_ik dP_ik),
+ *   dq_i += scale sum_j dS_ij k_j,   dk_j += scale dS_ij q_i
+ * Outputs dq [N][Hq][d], dk, dv [N][Hkv][d] (overwritten), in double.
+ */
+void oracle_attn_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, const int32_t *cu,
+                     int B, int Hq, int Hkv, int d, int window, double scale, const double *dout,
+                     double *dq, double *dk, double *dv)
+{
+    const int64_t N = cu[B];
+    const int G = Hq / Hkv;
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    memset(dq, 0, (size_t)N * Hq * d * sizeof(double));
+    memset(dk, 0, (size_t)N * Hkv * d * sizeof(double));
+    memset(dv, 0, (size_t)N * Hkv * d * sizeof(double));
+    int64_t max_T = 1;
+    for (int b = 0; b < B; b++)
+        if ((int64_t)cu[b + 1] - cu[b] > max_T)
+            max_T = (int64_t)cu[b + 1] - cu[b];
+    /* one job per KV head: the dk / dv rows it accumulates are its own */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int hk = 0; hk < Hkv; hk++) {
+        double *w_p = (double *)malloc((size_t)max_T * sizeof(double));
+        double *w_dp = (double *)malloc((size_t)max_T * sizeof(double));
+        double *qrow = (double *)malloc((size_t)d * sizeof(double));
+        for (int b = 0; b < B; b++) {
+            const int64_t base = cu[b], T = (int64_t)cu[b + 1] - base;
+            for (int64_t i = 0; i < T; i++) {
+                const int64_t first = (window >= 1 && i - window + 1 > 0) ? i - window + 1 : 0;
+                const int64_t cnt = i - first + 1;
+                for (int h = hk * G; h < (hk + 1) * G; h++) {
+                    const int64_t qo = ((base + i) * Hq + h) * (int64_t)d;
+                    for (int c = 0; c < d; c++)
+                        qrow[c] = bf16_to_double(q[qo + c]);
+                    double mx = -INFINITY;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        const int64_t ko = ((base + first + j) * Hkv + hk) * (int64_t)d;
+                        double acc = 0.0;
+                        for (int c = 0; c < d; c++)
+                            acc += qrow[c] * bf16_to_double(k[ko + c]);
+                        w_p[j] = scale * acc;
+                        mx = w_p[j] > mx ? w_p[j] : mx;
+                    }
+                    double sum = 0.0;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        w_p[j] = exp(w_p[j] - mx);
+                        sum += w_p[j];
+                    }
+                    const double *go = dout + qo;
+                    double rowdot = 0.0;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        w_p[j] /= sum;
+                        const int64_t vo = ((base + first + j) * Hkv + hk) * (int64_t)d;
+                        double acc = 0.0;
+                        for (int c = 0; c < d; c++)
+                            acc += go[c] * bf16_to_double(v[vo + c]);
+                        w_dp[j] = acc;
+                        rowdot += w_p[j] * acc;
+                    }
+                    for (int64_t j = 0; j < cnt; j++) {
+                        const int64_t ko = ((base + first + j) * Hkv + hk) * (int64_t)d;
+                        const double g_s = w_p[j] * (w_dp[j] - rowdot);
+                        for (int c = 0; c < d; c++) {
+                            dq[qo + c] += scale * g_s * bf16_to_double(k[ko + c]);
+                            dk[ko + c] += scale * g_s * qrow[c];
+                            dv[ko + c] += w_p[j] * go[c];
+                        }
+                    }
+                }
+            }
+        }
+        free(w_p);
+        free(w_dp);
+        free(qrow);
+    }
+}

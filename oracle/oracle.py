@@ -74,6 +74,8 @@ def _load():
     lib.oracle_logo_bwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, i32,
                                     f32, f64, P, P, f64, P, P, P, P, P, P, P, P, P, P]
     lib.oracle_logo_bwd.restype = i64
+    lib.oracle_attn_bwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, f64, P, P, P, P]
+    lib.oracle_attn_bwd.restype = None
     lib.oracle_fusion_bwd.argtypes = [P, P, P, P, i64, i32, i32, P, P, f64, P, P, P, P, P, P, P,
                                       P]
     lib.oracle_branch_transform.argtypes = [P, i32, i32, i32, P, P, P, P, i64, P]
@@ -339,3 +341,19 @@ def fusion_bwd(o_local, o_global_by_token, gate, z, dout, *, gain_local=None, ga
                               _ptr(dgate), _ptr(gl), _ptr(gg))
     return dict(dol=dol, dog=dog, delta_l=dl, delta_g=dg, dgate=dgate, dgain_local=gl,
                 dgain_global=gg)
+
+
+def attn_bwd(q, k, v, cu_seqlens, window: int, dout, *, scale: float = 0.0
+             ) -> Dict[str, np.ndarray]:
+    """Gradients of plain causal attention (window <= 0: full causal) given
+    dout = dL/do [N, Hq, d] -> dq [N, Hq, d], dk, dv [N, Hkv, d] (fp64)."""
+    q, k, v = _c(q, np.uint16), _c(k, np.uint16), _c(v, np.uint16)
+    cu = _c(cu_seqlens, np.int32)
+    dout = _c(dout, np.float64)
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    n1 = max(N, 1)
+    dq, dk, dv = np.empty((n1, Hq, d)), np.empty((n1, Hkv, d)), np.empty((n1, Hkv, d))
+    _load().oracle_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(cu), cu.size - 1, Hq, Hkv, d,
+                            int(window), float(scale), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv))
+    return dict(dq=dq[:N], dk=dk[:N], dv=dv[:N])

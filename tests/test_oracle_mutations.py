@@ -85,6 +85,11 @@ MUTATIONS = {
     "fusion_bwd_dgate_sign": ("side += (branch ? 1.0 : -1.0) * dr[c] * y;",
                               "side += (branch ? -1.0 : 1.0) * dr[c] * y;"),
     "fusion_bwd_delta_uses_dout": ("dl += dO[c] * o[c];", "dl += dr[c] * o[c];"),
+    "attn_bwd_rowdot_dropped": ("const double g_s = w_p[j] * (w_dp[j] - rowdot);",
+                                "const double g_s = w_p[j] * w_dp[j];"),
+    "attn_bwd_dv_unweighted": ("dv[ko + c] += w_p[j] * go[c];", "dv[ko + c] += go[c];"),
+    "attn_bwd_window_w_plus_1_keys": ("(window >= 1 && i - window + 1 > 0) ? i - window + 1 : 0",
+                                      "(window >= 1 && i - window > 0) ? i - window : 0"),
 }
 
 

@@ -739,3 +739,66 @@ def test_fusion_bwd_finite_differences(oracle_lib):
     np.testing.assert_allclose(r["delta_l"], (r["dol"] * ol).sum(-1), atol=1e-12)
     np.testing.assert_allclose(r["delta_g"], (r["dog"] * og).sum(-1), atol=1e-12)
     assert not r["dog"][~z].any() and not r["dgate"][~z].any()
+
+
+def np_attn_f64(qf, kf, vf, seqlens, window, scale):
+    """Plain causal attention in fp64 (window <= 0: full causal)."""
+    N, Hq, d = qf.shape
+    G = Hq // kf.shape[1]
+    out = np.zeros((N, Hq, d))
+    start = 0
+    for T in seqlens:
+        sl = slice(start, start + T)
+        start += T
+        if T == 0:
+            continue
+        i = np.arange(T)[:, None]
+        j = np.arange(T)[None, :]
+        mask = (j <= i) & ((j > i - window) if window >= 1 else True)
+        for h in range(Hq):
+            S = np.where(mask, scale * (qf[sl, h] @ kf[sl, h // G].T), -np.inf)
+            W = np.exp(S - S.max(axis=1, keepdims=True))
+            out[sl, h] = (W / W.sum(axis=1, keepdims=True)) @ vf[sl, h // G]
+    return out
+
+
+@pytest.mark.parametrize("window", [0, 3])
+def test_attn_bwd_finite_differences(oracle_lib, window):
+    """Plain attention backward (the dense baseline's) against central
+    differences of a numpy fp64 forward, GQA and two sequences."""
+    rng = np.random.default_rng(970 + window)
+    seqlens, Hq, Hkv, d = (6, 9), 4, 2, 8
+    N = sum(seqlens)
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    q, k, v = mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)
+    cu = np.array([0, 6, 15], np.int32)
+    dout = rng.standard_normal((N, Hq, d))
+    scale = 0.4
+    r = oracle_lib.attn_bwd(q, k, v, cu, window, dout, scale=scale)
+    base = dict(q=wide(q), k=wide(k), v=wide(v))
+
+    def loss(**over):
+        a = dict(base, **over)
+        return float((dout * np_attn_f64(a["q"], a["k"], a["v"], seqlens, window, scale)).sum())
+
+    h = 1e-6
+    for name in ("q", "k", "v"):
+        for _ in range(2):
+            U = rng.standard_normal(base[name].shape)
+            fd = (loss(**{name: base[name] + h * U}) - loss(**{name: base[name] - h * U})) / (2 * h)
+            an = float((r["d" + name] * U).sum())
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_attn_bwd_window_one(oracle_lib):
+    """With one key per row the softmax is constant: dq = dk = 0 and dv_j is
+    the sum of dout_j over the query heads of the KV head."""
+    rng = np.random.default_rng(975)
+    N, Hq, Hkv, d = 11, 6, 2, 4
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    q, k, v = mk(N, Hq, d), mk(N, Hkv, d), mk(N, Hkv, d)
+    dout = rng.standard_normal((N, Hq, d))
+    r = oracle_lib.attn_bwd(q, k, v, np.array([0, 4, 11], np.int32), 1, dout)
+    assert not r["dq"].any() and not r["dk"].any()
+    np.testing.assert_allclose(r["dv"], dout.reshape(N, Hkv, Hq // Hkv, d).sum(axis=2),
+                               atol=1e-12)
