@@ -266,6 +266,86 @@ def bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, steps: int = 20):
     return out
 
 
+def bench_train(pk, torch, w, dev, x, steps: int = 5, warmup: int = 2):
+    """Training step of the layer (logo_attn_fwd_train + logo_attn_bwd, the
+    selection held fixed) against the dense causal baseline's training step
+    (logo_dense_causal_attn_fwd_train + logo_dense_causal_attn_bwd), both with
+    an upstream gradient already in HBM.  Algorithmic FLOPs: forward 4 d Hq
+    per (query, key) pair, backward 8 d Hq (dV, dP, dQ, dK; the recomputed
+    scores are not counted)."""
+    import synth
+    N, Hq, Hkv, d = w.total_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
+    prob = pk.Problem(dev["cu_seqlens"], Hq, Hkv, d, w.window, cu_seqlens_host=x["cu_seqlens"])
+    dense_prob = pk.Problem(dev["cu_seqlens"], Hq, Hkv, d, w.max_seqlen,
+                            cu_seqlens_host=x["cu_seqlens"])
+    dout = synth.make_dout(w, 1)
+    dout_t = torch.from_numpy(dout.view(np.int16)).cuda().view(torch.bfloat16)
+    cap = max(pk.logo_ratio_capacity(prob, w.ratio), 1)
+    ws_f = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_FWD_TRAIN, cap),
+                       dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_BWD, cap), dtype=torch.uint8,
+                       device="cuda")
+    ws_d = torch.empty(pk.logo_workspace_bytes(dense_prob, pk.LOGO_ENTRY_DENSE_BWD, 0),
+                       dtype=torch.uint8, device="cuda")
+    saved = {}
+
+    def fwd():
+        saved.update(pk.logo_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                            ratio=w.ratio, sel_capacity=cap, ws=ws_f))
+
+    def bwd():
+        return pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved, dout_t,
+                                ws=ws_b)
+
+    dsaved = {}
+
+    def dfwd():
+        dsaved["out"], dsaved["lse"] = pk.logo_dense_causal_attn_fwd_train(
+            dense_prob, dev["q"], dev["k"], dev["v"])
+
+    def dbwd():
+        return pk.logo_dense_causal_attn_bwd(dense_prob, dev["q"], dev["k"], dev["v"],
+                                             dsaved["out"], dsaved["lse"], dout_t, ws=ws_d)
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    for _ in range(warmup):
+        fwd()
+        bwd()
+    torch.cuda.synchronize()
+    t_step = timed(lambda: (fwd(), bwd()), steps)
+    t_bwd = timed(bwd, steps)
+    for _ in range(warmup):
+        dfwd()
+        dbwd()
+    torch.cuda.synchronize()
+    t_dstep = timed(lambda: (dfwd(), dbwd()), steps)
+    t_dbwd = timed(dbwd, steps)
+    n_sel = int(saved["cu_sel"][-1])
+    sel_np = saved["sel_idx"][:n_sel].cpu().numpy()
+    p_local, p_global, p_dense = pair_counts(x["cu_seqlens"], w.window, sel_np)
+    fl = 4.0 * d * Hq
+    res = {"workload": w.name, "n_sel": n_sel,
+           "logo_fwd_bwd_ms": round(t_step, 4), "logo_bwd_ms": round(t_bwd, 4),
+           "dense_fwd_bwd_ms": round(t_dstep, 4), "dense_bwd_ms": round(t_dbwd, 4),
+           "speedup_fwd_bwd": round(t_dstep / t_step, 3),
+           "speedup_bwd": round(t_dbwd / t_bwd, 3),
+           "logo_bwd_tflops": round(2 * fl * (p_local + p_global) / (t_bwd * 1e-3) / 1e12, 2),
+           "dense_bwd_tflops": round(2 * fl * p_dense / (t_dbwd * 1e-3) / 1e12, 2),
+           "logo_fwd_bwd_tflops": round(3 * fl * (p_local + p_global) / (t_step * 1e-3) / 1e12,
+                                        2),
+           "dense_fwd_bwd_tflops": round(3 * fl * p_dense / (t_dstep * 1e-3) / 1e12, 2)}
+    log("train: " + " ".join(f"{k}={v}" for k, v in res.items()))
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -285,6 +365,8 @@ def main(argv=None):
     ap.add_argument("--no-transforms", action="store_true",
                     help="skip the gate-projection / branch-transform measurement")
     ap.add_argument("--decode-workload", default="decode-B16-32k-gqa")
+    ap.add_argument("--no-train", action="store_true",
+                    help="skip the training-step (forward + backward) measurement")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of MIB MiB "
                          "(the reference kernel for scaling FETCH_SIZE / WRITE_SIZE)")
@@ -472,6 +554,10 @@ def main(argv=None):
     if not args.no_transforms:
         transforms = bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap)
 
+    train = None
+    if not args.no_train:
+        train = bench_train(pk, torch, w, dev, x)
+
     decode = None
     if not args.no_decode:
         decode = bench_decode(pk, torch, args.decode_workload, steps=50, warmup=20)
@@ -517,6 +603,7 @@ def main(argv=None):
         "threshold_mode": thr_mode,
         "decode": decode,
         "transforms": transforms,
+        "train": train,
         "gpu": gpu_info(torch, busy=lambda: [step() for _ in range(600)])
                if not args.no_extra else None,
     }

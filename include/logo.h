@@ -71,7 +71,8 @@ typedef enum {
     LOGO_ENTRY_DENSE = 5,
     LOGO_ENTRY_DECODE = 6,
     LOGO_ENTRY_FWD_TRAIN = 7,
-    LOGO_ENTRY_BWD = 8
+    LOGO_ENTRY_BWD = 8,
+    LOGO_ENTRY_DENSE_BWD = 9
 } logo_entry;
 
 /* Problem description (a host struct; only cu_seqlens is a device pointer). */
@@ -303,6 +304,32 @@ logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
                                    logo_stream stream);
+
+/*
+ * logo_dense_causal_attn_fwd_train -- logo_dense_causal_attn that also keeps
+ * lse [Hq][N] fp32: per (head, token) the base-2 log-sum-exp of the scaled
+ * scores over keys 0..i, log2 sum_j 2^(c s_j), c = softmax_scale * log2(e).
+ * lse may be NULL (then this is logo_dense_causal_attn).  No workspace.
+ */
+logo_status logo_dense_causal_attn_fwd_train(const logo_problem *p, const logo_bf16 *q,
+                                             const logo_bf16 *k, const logo_bf16 *v,
+                                             logo_bf16 *out, float *lse, logo_stream stream);
+
+/*
+ * logo_dense_causal_attn_bwd -- gradients of dense causal softmax attention
+ * (Eq. attention with the global context): the dense baseline's backward.
+ *   out [N][Hq][d] bf16 and lse [Hq][N] from logo_dense_causal_attn_fwd_train,
+ *   dout [N][Hq][d] bf16 = dL/d out; dq [N][Hq][d], dk, dv [N][Hkv][d] fp32
+ *   (overwritten).  P and dS are recomputed from lse and rounded to bf16 for
+ *   the matrix products (fp32 accumulation), as in logo_attn_bwd.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_DENSE_BWD, 0) bytes (the row
+ *   sums dout . out), 256-byte aligned.
+ */
+logo_status logo_dense_causal_attn_bwd(const logo_problem *p, const logo_bf16 *q,
+                                       const logo_bf16 *k, const logo_bf16 *v,
+                                       const logo_bf16 *out, const float *lse,
+                                       const logo_bf16 *dout, float *dq, float *dk, float *dv,
+                                       void *ws, size_t ws_bytes, logo_stream stream);
 
 /*
  * logo_decode -- one autoregressive decoding step of the layer (Sec. 3.3 and

@@ -12,6 +12,7 @@ from .binding import (  # noqa: F401
     LOGO_ENTRY_COMBINE,
     LOGO_ENTRY_DECODE,
     LOGO_ENTRY_DENSE,
+    LOGO_ENTRY_DENSE_BWD,
     LOGO_ENTRY_FWD,
     LOGO_ENTRY_FWD_TRAIN,
     LOGO_ENTRY_GLOBAL,
@@ -35,6 +36,8 @@ from .binding import (  # noqa: F401
     logo_combine,
     logo_decode,
     logo_dense_causal_attn,
+    logo_dense_causal_attn_bwd,
+    logo_dense_causal_attn_fwd_train,
     logo_gate_proj,
     logo_global_attn_sparse_q,
     logo_local_attn,

@@ -27,6 +27,7 @@ LOGO_ENTRY_DENSE = 5
 LOGO_ENTRY_DECODE = 6
 LOGO_ENTRY_FWD_TRAIN = 7
 LOGO_ENTRY_BWD = 8
+LOGO_ENTRY_DENSE_BWD = 9
 LOGO_PHI_LP = 0
 LOGO_PHI_SO = 1
 
@@ -36,7 +37,8 @@ EXPORTS = (
     "logo_attn_fwd", "logo_attn_fwd_profiled", "logo_dense_causal_attn", "logo_workspace_bytes",
     "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
     "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
-    "logo_attn_fwd_train", "logo_attn_bwd",
+    "logo_attn_fwd_train", "logo_attn_bwd", "logo_dense_causal_attn_fwd_train",
+    "logo_dense_causal_attn_bwd",
 )
 
 _lib = None
@@ -96,6 +98,8 @@ def library():
         "logo_branch_transform": [i64, i32, i32, ctypes.c_int, P, P, P, P, P, i64, P, P, P],
         "logo_attn_fwd_train": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P,
                                 P, P, P, P, P, P, P, sz, P],
+        "logo_dense_causal_attn_fwd_train": [PP, P, P, P, P, P, P],
+        "logo_dense_causal_attn_bwd": [PP, P, P, P, P, P, P, P, P, P, P, sz, P],
         "logo_attn_bwd": [PP, P, P, P, P, P, P, P, P, P, f32, P, i32, P, P, P, P, P, P, P, P, P,
                           P, P, P, P, P, P, P, P, sz, P],
     }
@@ -471,6 +475,39 @@ def logo_dense_causal_attn(prob: Problem, q, k, v, out=None):
     _check(out, torch.bfloat16, (N, Hq, d), "out")
     _call("logo_dense_causal_attn", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream())
     return out
+
+
+def logo_dense_causal_attn_fwd_train(prob: Problem, q, k, v, out=None, lse=None):
+    """Dense causal attention keeping the base-2 LSE: (out bf16 [N, Hq, d],
+    lse fp32 [Hq, N])."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    if out is None:
+        out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=q.device)
+    if lse is None:
+        lse = torch.empty((Hq, max(N, 1)), dtype=torch.float32, device=q.device)
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    _call("logo_dense_causal_attn_fwd_train", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+          _ptr(lse), _stream())
+    return out, lse
+
+
+def logo_dense_causal_attn_bwd(prob: Problem, q, k, v, out, lse, dout, *, ws=None) -> dict:
+    """Gradients of dense causal attention: fp32 dq, dk, dv."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(dout, torch.bfloat16, (N, Hq, d), "dout")
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    f32 = dict(dtype=torch.float32, device=q.device)
+    g = dict(dq=torch.empty((N, Hq, d), **f32), dk=torch.empty((N, Hkv, d), **f32),
+             dv=torch.empty((N, Hkv, d), **f32))
+    ws, nbytes = _ws(prob, LOGO_ENTRY_DENSE_BWD, 0, ws)
+    _call("logo_dense_causal_attn_bwd", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+          _ptr(dout), _ptr(g["dq"]), _ptr(g["dk"]), _ptr(g["dv"]), _ptr(ws), nbytes, _stream())
+    return g
 
 
 def logo_budget_update(prob: Problem, cu_sel, rho: float, gamma: float, b_th, realized=None):

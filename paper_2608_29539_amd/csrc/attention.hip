@@ -657,6 +657,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         }
         if (!(wave_valid && row_valid[rg]))
             continue;
+        // training forward: the row's base-2 log-sum-exp of the scaled
+        // scores, log2(sum_j 2^(c s_j)) = m + log2(l)
+        if (a.lse && g == 0)
+            a.lse[(int64_t)head * a.lse_stride + orow[rg]] =
+                (m_ref[rg] == kNegInf ? 0.f : m_ref[rg]) + log2f(l_tot[rg]);
         if (MODE == kModeDense) {
             uint16_t *op = (uint16_t *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
@@ -669,11 +674,6 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
                     *(u32x2 *)(op + cb * 32 + qd * 8) = v;
                 }
         } else {
-            // training forward: the row's base-2 log-sum-exp of the scaled
-            // scores, log2(sum_j 2^(c s_j)) = m + log2(l)
-            if (a.lse && g == 0)
-                a.lse[(int64_t)head * a.lse_stride + orow[rg]] =
-                    (m_ref[rg] == kNegInf ? 0.f : m_ref[rg]) + log2f(l_tot[rg]);
             float *op = (float *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
 #pragma unroll
             for (int cb = 0; cb < D / 32; cb++)

@@ -687,6 +687,33 @@ __global__ __launch_bounds__(256) void gain_grad_kernel(int rows, int cols, cons
         out[col] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
 }
 
+// Delta = rowsum(dO * O) per (token, head) for plain attention (bf16 O and
+// dO), written [Hq][N]; one thread per 8 elements, d / 8 lanes per row.
+template <int D>
+__global__ __launch_bounds__(256) void attn_delta_kernel(int64_t n_rows, int hq, int64_t n,
+                                                         const uint16_t *o, const uint16_t *dout,
+                                                         float *delta) {
+    const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t row = g / (D / 8);
+    const bool ok = row < n_rows;
+    float acc = 0.f;
+    if (ok) {
+        const u32x4 a = *(const u32x4 *)(o + g * 8), b = *(const u32x4 *)(dout + g * 8);
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const uint32_t x = a[i], y = b[i];
+            acc = fmaf(__uint_as_float(x << 16), __uint_as_float(y << 16), acc);
+            acc = fmaf(__uint_as_float(x & 0xFFFF0000u), __uint_as_float(y & 0xFFFF0000u), acc);
+        }
+    }
+    acc = row_sum<D>(acc);
+    if (ok && (g % (D / 8)) == 0) {
+        const int64_t t = row / hq;
+        const int h = (int)(row % hq);
+        delta[(int64_t)h * n + t] = acc;
+    }
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(int64_t n, float *x) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < n)
@@ -736,6 +763,21 @@ hipError_t launch_gate_grad(int n, int hq, const float *side, float *dgate, hipS
 hipError_t launch_gain_grad(int rows, int cols, const float *part, float *out, hipStream_t s) {
     hipLaunchKernelGGL(gain_grad_kernel, dim3((cols + 63) / 64), dim3(256), 0, s, rows, cols, part,
                        out);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_delta(int64_t n, int hq, int head_dim, const uint16_t *o,
+                             const uint16_t *dout, float *delta, hipStream_t s) {
+    const int64_t threads = n * hq * (head_dim / 8);
+    if (threads <= 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+        hipLaunchKernelGGL((attn_delta_kernel<128>), grid, dim3(256), 0, s, n * hq, hq, n, o, dout,
+                           delta);
+    else
+        hipLaunchKernelGGL((attn_delta_kernel<64>), grid, dim3(256), 0, s, n * hq, hq, n, o, dout,
+                           delta);
     return hipGetLastError();
 }
 

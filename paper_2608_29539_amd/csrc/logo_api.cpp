@@ -220,6 +220,10 @@ BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
     return w;
 }
 
+size_t dense_bwd_ws(const logo_problem *p) {
+    return align_up(sizeof(float) * (size_t)p->num_q_heads * (size_t)p->total_tokens);
+}
+
 BwdArgs make_bwd_args(const logo_problem *p) {
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
     BwdArgs a;
@@ -577,6 +581,7 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_DECODE: return decode_plan(p).total;
     case LOGO_ENTRY_FWD_TRAIN: return train_ws(p, cap).total;
     case LOGO_ENTRY_BWD: return bwd_ws(p, cap).total;
+    case LOGO_ENTRY_DENSE_BWD: return dense_bwd_ws(p);
     case LOGO_ENTRY_LOCAL:
     case LOGO_ENTRY_COMBINE:
     case LOGO_ENTRY_DENSE: return 0;
@@ -688,6 +693,12 @@ logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
                                    logo_stream stream) {
+    return logo_dense_causal_attn_fwd_train(p, q, k, v, out, nullptr, stream);
+}
+
+logo_status logo_dense_causal_attn_fwd_train(const logo_problem *p, const logo_bf16 *q,
+                                             const logo_bf16 *k, const logo_bf16 *v,
+                                             logo_bf16 *out, float *lse, logo_stream stream) {
     logo_status st = check_problem(p);
     if (st != LOGO_OK)
         return st;
@@ -701,6 +712,8 @@ logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
     a.k = k;
     a.v = v;
     a.out = out;
+    a.lse = lse;
+    a.lse_stride = p->total_tokens;
     const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max;
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
@@ -1003,6 +1016,53 @@ logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_
         st = hip_status(launch_bwd_dq(kModeGlobal, d, a, (int)grid_q, s), s);
     if (st == LOGO_OK)
         st = hip_status(launch_bwd_dkv(kModeGlobal, d, a, (int)grid_kv, s), s);
+    return st;
+}
+
+logo_status logo_dense_causal_attn_bwd(const logo_problem *p, const logo_bf16 *q,
+                                       const logo_bf16 *k, const logo_bf16 *v,
+                                       const logo_bf16 *out, const float *lse,
+                                       const logo_bf16 *dout, float *dq, float *dk, float *dv,
+                                       void *ws, size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    const int32_t N = p->total_tokens;
+    if (N > 0 && (!q || !k || !v || !out || !lse || !dout || !dq || !dk || !dv))
+        return LOGO_ERR_NULL;
+    st = check_ws(ws, ws_bytes, dense_bwd_ws(p));
+    if (st != LOGO_OK)
+        return st;
+    if (N == 0)
+        return LOGO_OK;
+    hipStream_t s = (hipStream_t)stream;
+    float *delta = (float *)ws;
+    st = hip_status(launch_attn_delta(N, p->num_q_heads, p->head_dim, out, dout, delta, s), s);
+    if (st != LOGO_OK)
+        return st;
+    // plain causal attention is the local kernels' row set with a window that
+    // covers every sequence
+    BwdArgs a = make_bwd_args(p);
+    a.window = p->max_seqlen > 0 ? p->max_seqlen : 1;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.dout = dout;
+    a.lse = lse;
+    a.delta = delta;
+    a.row_stride = N;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    const long long grid_q = (long long)a.n_hg * p->num_seqs * a.ntile_max;
+    const int kpb = bwd_keys_per_block();
+    const long long grid_kv =
+        (long long)((p->max_seqlen + kpb - 1) / kpb) * p->num_seqs * p->num_kv_heads;
+    if (grid_q >= (1LL << 31) || grid_kv >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    st = hip_status(launch_bwd_dq(kModeLocal, p->head_dim, a, (int)grid_q, s), s);
+    if (st == LOGO_OK)
+        st = hip_status(launch_bwd_dkv(kModeLocal, p->head_dim, a, (int)grid_kv, s), s);
     return st;
 }
 

@@ -217,6 +217,8 @@ hipError_t launch_fusion_bwd(const FusionBwdArgs &a, int grid, int head_dim, hip
 hipError_t launch_gate_grad(int n, int hq, const float *side, float *dgate, hipStream_t s);
 hipError_t launch_gain_grad(int rows, int cols, const float *part, float *out, hipStream_t s);
 hipError_t launch_fill_zero(int64_t n, float *x, hipStream_t s);
+hipError_t launch_attn_delta(int64_t n, int hq, int head_dim, const uint16_t *o,
+                             const uint16_t *dout, float *delta, hipStream_t s);
 hipError_t launch_bwd_dq(int mode, int head_dim, const BwdArgs &a, int grid, hipStream_t s);
 hipError_t launch_bwd_dkv(int mode, int head_dim, const BwdArgs &a, int grid, hipStream_t s);
 int bwd_keys_per_block();

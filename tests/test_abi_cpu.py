@@ -245,3 +245,61 @@ def test_gate_and_transform_validation(lib):
     assert t(10, 4, 128, 0, FAKE, FAKE, None, None, None, 9, None, FAKE, None) == ERR_SHAPE
     assert t(10, 0, 128, 0, FAKE, FAKE, None, None, None, 10, None, FAKE, None) == ERR_SHAPE
     assert t(10, 4, 128, 0, FAKE, FAKE, None, None, None, 10, None, None, None) == ERR_NULL
+
+
+def _caller(f, args):
+    def call(**kw):
+        a = list(args)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return f(*a)
+    return call
+
+
+def test_train_and_backward_validation(lib):
+    """logo_attn_fwd_train, logo_attn_bwd and the dense training entry points
+    reject bad arguments before any launch."""
+    p = Prob(seqlens=(100, 50), hq=8, hkv=2, d=128, window=16)
+    need = lib.logo_workspace_bytes(p.c, 7, 150)
+    assert need > 0 and need % 256 == 0
+    call = _caller(lib.logo_attn_fwd_train,
+                   [p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 0, 0.5, 0.0, None, None, 1e-6,
+                    FAKE, FAKE, 150, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, FAKE, need, None])
+    for i in (1, 7, 14, 15, 17, 18, 20, 21, 22, 23):
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    assert call(a16=-1) == ERR_SHAPE
+    assert call(a13=-1.0) == ERR_ARG
+    assert call(a8=1, a10=2.0) == ERR_ARG
+    assert call(a9=float("nan")) == ERR_ARG
+    assert call(a25=need - 1) == ERR_WORKSPACE
+
+    need_b = lib.logo_workspace_bytes(p.c, 8, 150)
+    # the backward holds dO^L (bf16) and the row sums at least
+    assert need_b >= 150 * 8 * 128 * 2 + 8 * 150 * 4
+    args = [p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, None, None, 1e-6, FAKE, 150, FAKE,
+            FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, None, FAKE, None,
+            None, FAKE, need_b, None]
+    call = _caller(lib.logo_attn_bwd, args)
+    assert call(a4=FAKE) == ERR_ARG                  # q_g without dq_g
+    assert call(a23=FAKE) == ERR_ARG                 # dq_g without q_g
+    assert call(a6=FAKE) == ERR_ARG                  # v_g without dv_g
+    for i in (1, 7, 14, 15, 16, 19, 20, 21, 22, 13):
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    for i in (11, 17, 18):                           # needed when sel_capacity > 0
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    assert call(a12=-1) == ERR_SHAPE
+    assert call(a10=float("nan")) == ERR_ARG
+    assert call(a30=need_b - 1) == ERR_WORKSPACE
+    wide = Prob(seqlens=(100,), hq=48, hkv=8, d=128, window=16)   # Hq d / 8 = 768
+    a = list(args)
+    a[0], a[30] = wide.c, lib.logo_workspace_bytes(wide.c, 8, 150)
+    assert lib.logo_attn_bwd(*a) == ERR_UNSUPPORTED
+
+    need_d = lib.logo_workspace_bytes(p.c, 9, 0)
+    assert need_d == 8 * 150 * 4 + (-8 * 150 * 4) % 256
+    call = _caller(lib.logo_dense_causal_attn_bwd,
+                   [p.c, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, need_d, None])
+    for i in range(1, 10):
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    assert call(a11=need_d - 4) == ERR_WORKSPACE
+    assert lib.logo_dense_causal_attn_fwd_train(p.c, None, FAKE, FAKE, FAKE, None, None) == ERR_NULL

@@ -119,3 +119,35 @@ def test_backward_small(pk, ci):
     lens, hq, hkv, d, win, ratio, thr, distinct, gains = BWD_CASES[ci]
     w = synth.small_workload(lens, hq, hkv, d, win, ratio or 0.0, seed=5000 + ci)
     run_case(pk, w, ratio=ratio, threshold=thr, distinct=distinct, gains=gains, tag=f"case{ci}")
+
+
+DENSE_CASES = [
+    # (seqlens, Hq, Hkv, d)
+    ((300, 1000), 8, 2, 128),
+    ((64, 65, 700), 4, 4, 64),
+    ((2048,), 16, 2, 128),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(DENSE_CASES)))
+def test_dense_backward(pk, ci):
+    """The dense baseline's backward against the oracle's plain-attention
+    backward (same bars; dout . out is formed from the bf16 output)."""
+    import torch
+    lens, hq, hkv, d = DENSE_CASES[ci]
+    w = synth.small_workload(lens, hq, hkv, d, 1, 0.0, seed=5100 + ci)
+    x = synth.make_inputs(w)
+    dout = synth.make_dout(w, 2)
+    dev = to_device(dict(x, dout=dout))
+    prob = pk.Problem(dev["cu_seqlens"], hq, hkv, d, max(lens), cu_seqlens_host=x["cu_seqlens"])
+    print(f"[dense bwd case{ci}] seqlens={lens} H={hq}/{hkv} d={d}", flush=True)
+    out, lse = pk.logo_dense_causal_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"])
+    g = pk.logo_dense_causal_attn_bwd(prob, dev["q"], dev["k"], dev["v"], out, lse, dev["dout"])
+    torch.cuda.synchronize()
+    dout64 = synth.f32_from_bf16_bits(dout).reshape(dout.shape).astype(np.float64)
+    ref = oracle.attn_bwd(x["q"], x["k"], x["v"], x["cu_seqlens"], 0, dout64)
+    for nm in ("dq", "dk", "dv"):
+        e = grad_err(g[nm].cpu().numpy(), ref[nm])
+        print(f"[dense bwd case{ci}] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}",
+              flush=True)
+        assert e["rel_l2"] <= REL_L2 and e["rel_max"] <= REL_MAX, (ci, nm, e)
