@@ -132,7 +132,7 @@ __device__ __forceinline__ bf16x8 pack8(const bf16x2 (&w)[8], int half) {
 // dQ
 // ---------------------------------------------------------------------------
 template <int D, int MODE>
-__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(D == 128 ? 1 : 2)))
+__global__ __launch_bounds__(kBwdWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void bwd_dq_kernel(const BwdArgs a) {
     __shared__ __attribute__((aligned(16))) uint16_t sk[2][kTileRows * D];
     __shared__ __attribute__((aligned(16))) uint16_t sv[2][kTileRows * D];
@@ -217,9 +217,13 @@ void bwd_dq_kernel(const BwdArgs a) {
     for (int cb = 0; cb < D / 32; cb++)
         acc[cb] = f32x16{};
 
-    auto compute = [&](int kb_, int buf, auto masked) {
-        const char *kt = (const char *)sk[buf];
-        const char *vt = (const char *)sv[buf];
+    // bufc: the buffer as a compile-time constant, so that every fragment
+    // address is a per-lane offset plus an immediate.  masked: a compile-time
+    // flag (a runtime one is if-converted into selects on every tile).
+    auto compute = [&](int kb_, auto bufc, auto masked) {
+        constexpr int B = decltype(bufc)::value;
+        const char *kt = (const char *)sk[B];
+        const char *vt = (const char *)sv[B];
         const int k0 = kb_ * kTileRows;
 #pragma unroll
         for (int sb = 0; sb < 2; sb++) {
@@ -231,6 +235,16 @@ void bwd_dq_kernel(const BwdArgs a) {
                 dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     frag_at(vt + sb * 32 * D * 2, fo.row[ss]), dof[ss], dp, 0, 0, 0);
             }
+            // Schedule: two fragment reads ahead, then one MFMA per read, so
+            // only a few fragments are live at a time (the register budget
+            // of two waves per SIMD).
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);       // DS read
+#pragma unroll
+            for (int i = 0; i < D / 8 - 2; i++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
             // lane: query column; register i: key k0 + 32 sb + 8 (i/4) + 4 g + i%4
             bf16x2 dsw[8];
 #pragma unroll
@@ -258,24 +272,39 @@ void bwd_dq_kernel(const BwdArgs a) {
                     acc[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                         frag_tr<D>(kt, fo, sb * 32 + half * 16, cb), bf, acc[cb], 0, 0, 0);
             }
+            // one transposed fragment (two reads) ahead of each MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+            for (int i = 0; i < D / 16 - 1; i++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
     };
 
-    using T_ = std::true_type;
-    using F_ = std::false_type;
-    stage(kb_lo, 0);
-    dma_wait_barrier();
-    for (int kb = kb_lo; kb <= kb_hi; kb++) {
-        const int buf = (kb - kb_lo) & 1;
-        if (kb < kb_hi)
-            stage(kb + 1, buf ^ 1);
-        if (kb >= kb_first && kb <= kb_last) {
-            if (kb > kb_c || kb < kb_w)
-                compute(kb, buf, T_{});
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    // Step kb (buffer (kb - kb_lo) % 2): stage tile kb+1 into the other
+    // buffer, compute tile kb, then wait for the staged loads and barrier.
+    auto step = [&](int kb_, auto bufc) {
+        constexpr int B = decltype(bufc)::value;
+        if (kb_ < kb_hi)
+            stage(kb_ + 1, B ^ 1);
+        if (kb_ >= kb_first && kb_ <= kb_last) {
+            if (kb_ > kb_c || kb_ < kb_w)
+                compute(kb_, bufc, std::true_type{});
             else
-                compute(kb, buf, F_{});
+                compute(kb_, bufc, std::false_type{});
         }
         dma_wait_barrier();
+    };
+    stage(kb_lo, 0);
+    dma_wait_barrier();
+    for (int kb = kb_lo; kb <= kb_hi; kb += 2) {
+        step(kb, I0{});
+        if (kb + 1 <= kb_hi)
+            step(kb + 1, I1{});
     }
 
     if (!(wave_valid && valid))
@@ -408,7 +437,12 @@ void bwd_dkv_kernel(const BwdArgs a) {
     const int jmax = min(j0 + 31, T - 1);
 
     // One 64-row step: two halves of 32 query rows.
-    auto compute = [&](int buf, int r0, int nv, auto masked) {
+    // One MFMA path for masked and unmasked tiles (two instantiations would
+    // give the loop-carried dK / dV accumulators different registers on the
+    // two paths and copies where they merge); the mask is a uniform branch
+    // in the softmax part only.
+    auto compute = [&](auto bufc, int r0, int nv, bool masked) {
+        constexpr int buf = decltype(bufc)::value;
         const char *qt = (const char *)sq[buf];
         const char *dt = (const char *)sd[buf];
 #pragma unroll
@@ -443,7 +477,7 @@ void bwd_dkv_kernel(const BwdArgs a) {
 #pragma unroll
                 for (int e = 0; e < 2; e++) {
                     float p = __builtin_amdgcn_exp2f(fmaf(s[i + e], c, -lse[i + e]));
-                    if constexpr (decltype(masked)::value) {
+                    if (masked) {
                         const int qi = qh * 32 + ((i + e) >> 2) * 8 + g * 4 + ((i + e) & 3);
                         const int qpos = (MODE == kModeGlobal ? sp[buf][qi] : r0 + qi) - base;
                         bool ok = qi < nv && key <= qpos;
@@ -471,15 +505,10 @@ void bwd_dkv_kernel(const BwdArgs a) {
         }
     };
 
-    using T_ = std::true_type;
-    using F_ = std::false_type;
-    if (nsteps > 0) {
-        stage(0, 0);
-        commit(0);
-        dma_wait_barrier();
-    }
-    for (int st = 0; st < nsteps; st++) {
-        const int buf = st & 1;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    auto step = [&](int st, auto bufc) {
+        constexpr int buf = decltype(bufc)::value;
         const bool next = st + 1 < nsteps;
         if (next)
             stage(st + 1, buf ^ 1);
@@ -496,14 +525,21 @@ void bwd_dkv_kernel(const BwdArgs a) {
             bool full = nv == kTileRows && pmin >= j0 + 31 && j0 + 31 < T;
             if (MODE == kModeLocal)
                 full = full && pmax <= j0 + w - 1;
-            if (full)
-                compute(buf, r0, nv, F_{});
-            else
-                compute(buf, r0, nv, T_{});
+            compute(bufc, r0, nv, !full);
         }
         if (next)
             commit(buf ^ 1);
         dma_wait_barrier();
+    };
+    if (nsteps > 0) {
+        stage(0, 0);
+        commit(0);
+        dma_wait_barrier();
+    }
+    for (int st = 0; st < nsteps; st += 2) {
+        step(st, I0{});
+        if (st + 1 < nsteps)
+            step(st + 1, I1{});
     }
 
     if (key >= T)
