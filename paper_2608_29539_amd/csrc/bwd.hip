@@ -445,10 +445,11 @@ void bwd_dkv_kernel(const BwdArgs a) {
         constexpr int buf = decltype(bufc)::value;
         const char *qt = (const char *)sq[buf];
         const char *dt = (const char *)sd[buf];
+        // Both 32-row halves in one straight-line block (rows past nv are
+        // masked), so the scheduler can overlap one half's softmax with the
+        // other half's MFMAs.
 #pragma unroll
         for (int qh = 0; qh < 2; qh++) {
-            if (qh * 32 >= nv)
-                break;
             f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
             for (int ss = 0; ss < D / 16; ss++) {
@@ -457,8 +458,16 @@ void bwd_dkv_kernel(const BwdArgs a) {
                 dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
                     frag_at(dt + qh * 32 * D * 2, fo.row[ss]), vf[ss], dp, 0, 0, 0);
             }
+            // six fragment reads ahead, then one MFMA per read
+            __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+            for (int i = 0; i < D / 8 - 6; i++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
             // lane: key column; register i: row qh*32 + 8 (i/4) + 4 g + i%4
-            float lse[16], dl[16];
+            float p[16], dl[16];
 #pragma unroll
             for (int qd = 0; qd < 4; qd++) {
                 const int ro = qh * 32 + qd * 8 + g * 4;
@@ -466,30 +475,26 @@ void bwd_dkv_kernel(const BwdArgs a) {
                 const f32x4 d4 = *(const f32x4 *)&sdl[buf][ro];
 #pragma unroll
                 for (int e = 0; e < 4; e++) {
-                    lse[qd * 4 + e] = l4[e];
+                    p[qd * 4 + e] = __builtin_amdgcn_exp2f(fmaf(s[qd * 4 + e], c, -l4[e]));
                     dl[qd * 4 + e] = d4[e];
+                }
+            }
+            if (masked) {
+#pragma unroll
+                for (int i = 0; i < 16; i++) {
+                    const int qi = qh * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
+                    const int qpos = (MODE == kModeGlobal ? sp[buf][qi] : r0 + qi) - base;
+                    bool ok = qi < nv && key <= qpos;
+                    if (MODE == kModeLocal)
+                        ok = ok && qpos < key + w;
+                    p[i] = ok ? p[i] : 0.f;
                 }
             }
             bf16x2 pw[8], dsw[8];
 #pragma unroll
             for (int i = 0; i < 16; i += 2) {
-                float p2[2], d2[2];
-#pragma unroll
-                for (int e = 0; e < 2; e++) {
-                    float p = __builtin_amdgcn_exp2f(fmaf(s[i + e], c, -lse[i + e]));
-                    if (masked) {
-                        const int qi = qh * 32 + ((i + e) >> 2) * 8 + g * 4 + ((i + e) & 3);
-                        const int qpos = (MODE == kModeGlobal ? sp[buf][qi] : r0 + qi) - base;
-                        bool ok = qi < nv && key <= qpos;
-                        if (MODE == kModeLocal)
-                            ok = ok && qpos < key + w;
-                        p = ok ? p : 0.f;
-                    }
-                    p2[e] = p;
-                    d2[e] = p * (dp[i + e] - dl[i + e]);
-                }
-                pw[i >> 1] = cvt_bf16x2(p2[0], p2[1]);
-                dsw[i >> 1] = cvt_bf16x2(d2[0], d2[1]);
+                pw[i >> 1] = cvt_bf16x2(p[i], p[i + 1]);
+                dsw[i >> 1] = cvt_bf16x2(p[i] * (dp[i] - dl[i]), p[i + 1] * (dp[i + 1] - dl[i + 1]));
             }
 #pragma unroll
             for (int half = 0; half < 2; half++) {
@@ -502,6 +507,14 @@ void bwd_dkv_kernel(const BwdArgs a) {
                         frag_tr<D>(qt, fo, qh * 32 + half * 16, cb), db, dk[cb], 0, 0, 0);
                 }
             }
+            // two transposed fragments (four reads) ahead of the MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+            for (int i = 0; i < D / 8 - 4; i++) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
         }
     };
 
