@@ -719,21 +719,26 @@ __global__ __launch_bounds__(256) void gate_grad_kernel(int n, int hq, const flo
     dgate[t] = s;
 }
 
-// Column sums of [rows][cols] partials: 64 columns per workgroup, the 4
-// waves take every 4th row, then a fixed-order sum of the 4.
+// Column sums of [rows][cols] partials over row chunks of kGainChunk:
+// workgroup (x, y) sums rows y*kGainChunk .. +kGainChunk-1 of 64 columns
+// (the 4 waves take every 4th row, then a fixed-order sum of the 4) into
+// out[y][cols].  Two passes reduce any row count to one row.
+constexpr int kGainChunk = 64;
 __global__ __launch_bounds__(256) void gain_grad_kernel(int rows, int cols, const float *part,
                                                         float *out) {
     __shared__ float red[4][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = blockIdx.x * 64 + lane;
+    const int r0 = blockIdx.y * kGainChunk, r1 = min(rows, r0 + kGainChunk);
     float s = 0.f;
     if (col < cols)
-        for (int r = wave; r < rows; r += 4)
+        for (int r = r0 + wave; r < r1; r += 4)
             s += part[(int64_t)r * cols + col];
     red[wave][lane] = s;
     __syncthreads();
     if (wave == 0 && col < cols)
-        out[col] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+        out[(int64_t)blockIdx.y * cols + col] =
+            (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
 }
 
 // Delta = rowsum(dO * O) per (token, head) for plain attention (bf16 O and
@@ -809,9 +814,21 @@ hipError_t launch_gate_grad(int n, int hq, const float *side, float *dgate, hipS
     return hipGetLastError();
 }
 
-hipError_t launch_gain_grad(int rows, int cols, const float *part, float *out, hipStream_t s) {
-    hipLaunchKernelGGL(gain_grad_kernel, dim3((cols + 63) / 64), dim3(256), 0, s, rows, cols, part,
-                       out);
+int gain_grad_chunks(int rows) { return (rows + kGainChunk - 1) / kGainChunk; }
+
+hipError_t launch_gain_grad(int rows, int cols, const float *part, float *tmp, float *out,
+                            hipStream_t s) {
+    const int chunks = gain_grad_chunks(rows);
+    if (chunks > kGainChunk)
+        return hipErrorInvalidValue;               // two passes cover 4096 rows
+    const float *src = part;
+    if (chunks > 1) {
+        hipLaunchKernelGGL(gain_grad_kernel, dim3((cols + 63) / 64, chunks), dim3(256), 0, s, rows,
+                           cols, part, tmp);
+        src = tmp;
+    }
+    hipLaunchKernelGGL(gain_grad_kernel, dim3((cols + 63) / 64, 1), dim3(256), 0, s,
+                       chunks > 1 ? chunks : rows, cols, src, out);
     return hipGetLastError();
 }
 

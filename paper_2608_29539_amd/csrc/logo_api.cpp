@@ -7,6 +7,7 @@
 #include "../../include/logo.h"
 #include "logo_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -184,9 +185,9 @@ TrainWs train_ws(const logo_problem *p, int32_t cap) {
 
 // logo_attn_bwd: dO^L / dO^G (bf16), the compact Q^G rows, the row sums
 // Delta, the per-row gate terms and the gain-gradient partials.
-constexpr int kFusionBwdMaxBlocks = 1024;
+constexpr int kFusionBwdMaxBlocks = 2048;
 struct BwdWs {
-    size_t dol, dog, qc, delta_l, delta_g, side, part_l, part_g, total;
+    size_t dol, dog, qc, delta_l, delta_g, side, part_l, part_g, part_tmp, total;
     int blocks, tokens_per_block, part_rows;
 };
 BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
@@ -194,7 +195,9 @@ BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
     const int P = fusion_bwd_tokens_per_pass(p->num_q_heads, p->head_dim);
     const long long passes = ((long long)N + P - 1) / P;
     BwdWs w;
-    w.blocks = (int)(passes < kFusionBwdMaxBlocks ? passes : kFusionBwdMaxBlocks);
+    // at most 4096 partial rows (the two-pass column sum's reach)
+    const long long max_blocks = std::min<long long>(kFusionBwdMaxBlocks, 4096 / P);
+    w.blocks = (int)(passes < max_blocks ? passes : max_blocks);
     if (w.blocks < 1)
         w.blocks = 1;
     w.tokens_per_block = (int)((passes + w.blocks - 1) / w.blocks) * P;
@@ -216,6 +219,8 @@ BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
     off += align_up(4 * (size_t)w.part_rows * H * d);
     w.part_g = off;
     off += align_up(4 * (size_t)w.part_rows * H * d);
+    w.part_tmp = off;
+    off += align_up(4 * (size_t)gain_grad_chunks(w.part_rows) * H * d);
     w.total = off;
     return w;
 }
@@ -959,10 +964,11 @@ logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_
     st = hip_status(launch_fusion_bwd(f, w.blocks, d, s), s);
     if (st == LOGO_OK && dgate)
         st = hip_status(launch_gate_grad(N, H, f.side, dgate, s), s);
+    float *gtmp = (float *)(base + w.part_tmp);
     if (st == LOGO_OK && dgain_local)
-        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_l, dgain_local, s), s);
+        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_l, gtmp, dgain_local, s), s);
     if (st == LOGO_OK && dgain_global)
-        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_g, dgain_global, s), s);
+        st = hip_status(launch_gain_grad(w.part_rows, H * d, f.part_g, gtmp, dgain_global, s), s);
     if (st != LOGO_OK)
         return st;
 

@@ -215,7 +215,10 @@ int fusion_bwd_tokens_per_pass(int hq, int head_dim);
 bool fusion_bwd_supported(int hq, int head_dim);
 hipError_t launch_fusion_bwd(const FusionBwdArgs &a, int grid, int head_dim, hipStream_t s);
 hipError_t launch_gate_grad(int n, int hq, const float *side, float *dgate, hipStream_t s);
-hipError_t launch_gain_grad(int rows, int cols, const float *part, float *out, hipStream_t s);
+// gain-gradient column sums: tmp holds gain_grad_chunks(rows) x cols floats
+int gain_grad_chunks(int rows);
+hipError_t launch_gain_grad(int rows, int cols, const float *part, float *tmp, float *out,
+                            hipStream_t s);
 hipError_t launch_fill_zero(int64_t n, float *x, hipStream_t s);
 hipError_t launch_attn_delta(int64_t n, int hq, int head_dim, const uint16_t *o,
                              const uint16_t *dout, float *delta, hipStream_t s);
