@@ -346,6 +346,70 @@ def bench_train(pk, torch, w, dev, x, steps: int = 5, warmup: int = 2):
     return res
 
 
+def bench_sparse_operator(pk, torch, T: int = 65536, heads: int = 8, ratio: float = 0.5,
+                          steps: int = 3, warmup: int = 1):
+    """The paper's own benchmark shape (Sec. 4.3): the query-sparse global
+    attention alone, forward + backward, at B = 1, 8 heads, d = 128, budget
+    0.5, against dense causal attention forward + backward on the same
+    inputs (uniform gate, ratio-mode selection).  The paper reports 1.99x
+    (ideal 2x) at 64k for its Triton kernels on unnamed hardware."""
+    import synth
+    d = 128
+    w = synth.small_workload((T,), heads, heads, d, T, ratio, seed=1010)
+    x = synth.make_inputs(w)
+    dev = {}
+    for k_, v_ in x.items():
+        t = torch.from_numpy(np.ascontiguousarray(v_.view(np.int16) if v_.dtype == np.uint16
+                                                  else v_)).cuda()
+        dev[k_] = t.view(torch.bfloat16) if v_.dtype == np.uint16 else t
+    prob = pk.Problem(dev["cu_seqlens"], heads, heads, d, T, cu_seqlens_host=x["cu_seqlens"])
+    cap = max(pk.logo_ratio_capacity(prob, ratio), 1)
+    sel_idx, cu_sel, _, _ = pk.logo_select(prob, dev["gate"], ratio=ratio, sel_capacity=cap)
+    g = torch.Generator(device="cuda").manual_seed(11)
+    dout_c = torch.randn((cap, heads, d), generator=g, device="cuda").to(torch.bfloat16)
+    dout_d = torch.randn((T, heads, d), generator=g, device="cuda").to(torch.bfloat16)
+    ws_f = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_GLOBAL, cap),
+                       dtype=torch.uint8, device="cuda")
+    ws_b = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_GLOBAL_BWD, cap),
+                       dtype=torch.uint8, device="cuda")
+    ws_d = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_DENSE_BWD, 0),
+                       dtype=torch.uint8, device="cuda")
+    st = {}
+
+    def sparse():
+        st["o"], st["lse"] = pk.logo_global_attn_sparse_q_fwd_train(
+            prob, dev["q"], dev["k"], dev["v"], sel_idx, cu_sel, cap, ws=ws_f)
+        pk.logo_global_attn_sparse_q_bwd(prob, dev["q"], dev["k"], dev["v"], sel_idx, cu_sel, cap,
+                                         st["o"], st["lse"], dout_c, ws=ws_b)
+
+    def dense():
+        o, lse = pk.logo_dense_causal_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"])
+        pk.logo_dense_causal_attn_bwd(prob, dev["q"], dev["k"], dev["v"], o, lse, dout_d,
+                                      ws=ws_d)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    t_s, t_d = timed(sparse), timed(dense)
+    n_sel = int(cu_sel[-1])
+    res = {"shape": {"batch": 1, "tokens": T, "heads": heads, "head_dim": d, "budget": ratio,
+                     "n_sel": n_sel},
+           "sparse_fwd_bwd_ms": round(t_s, 3), "dense_fwd_bwd_ms": round(t_d, 3),
+           "speedup": round(t_d / t_s, 3), "ideal": round(1.0 / ratio, 3),
+           "paper_speedup": 1.99}
+    log("paper-shape sparse operator: " + " ".join(f"{k}={v}" for k, v in res.items()))
+    return res
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -367,6 +431,8 @@ def main(argv=None):
     ap.add_argument("--decode-workload", default="decode-B16-32k-gqa")
     ap.add_argument("--no-train", action="store_true",
                     help="skip the training-step (forward + backward) measurement")
+    ap.add_argument("--no-paper-shape", action="store_true",
+                    help="skip the query-sparse operator at the paper's benchmark shape")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="before timing, run one plain device-to-device copy of MIB MiB "
                          "(the reference kernel for scaling FETCH_SIZE / WRITE_SIZE)")
@@ -557,6 +623,8 @@ def main(argv=None):
     train = None
     if not args.no_train:
         train = bench_train(pk, torch, w, dev, x)
+        if not args.no_paper_shape:
+            train["paper_shape_sparse_operator"] = bench_sparse_operator(pk, torch)
 
     decode = None
     if not args.no_decode:

@@ -72,7 +72,8 @@ typedef enum {
     LOGO_ENTRY_DECODE = 6,
     LOGO_ENTRY_FWD_TRAIN = 7,
     LOGO_ENTRY_BWD = 8,
-    LOGO_ENTRY_DENSE_BWD = 9
+    LOGO_ENTRY_DENSE_BWD = 9,
+    LOGO_ENTRY_GLOBAL_BWD = 10
 } logo_entry;
 
 /* Problem description (a host struct; only cu_seqlens is a device pointer). */
@@ -304,6 +305,42 @@ logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_
 logo_status logo_dense_causal_attn(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v, logo_bf16 *out,
                                    logo_stream stream);
+
+/*
+ * logo_global_attn_sparse_q_fwd_train -- logo_global_attn_sparse_q that also
+ * keeps lse_global [Hq][sel_capacity] fp32: per (head, selected rank) the
+ * base-2 log-sum-exp of the scaled scores over keys 0..pos (Eq.
+ * query-sparse-global).  Arguments and workspace otherwise as for
+ * logo_global_attn_sparse_q (LOGO_ENTRY_GLOBAL).
+ */
+logo_status logo_global_attn_sparse_q_fwd_train(const logo_problem *p, const logo_bf16 *q,
+                                                const logo_bf16 *k, const logo_bf16 *v,
+                                                const int32_t *sel_idx, const int32_t *cu_sel,
+                                                int32_t sel_capacity, float *o_global,
+                                                float *lse_global, void *ws, size_t ws_bytes,
+                                                logo_stream stream);
+
+/*
+ * logo_global_attn_sparse_q_bwd -- gradients of the query-sparse global
+ * attention alone (Eq. query-sparse-global; App. B, backward traversal):
+ * the loss depends on the selected rows' outputs only.
+ *   sel_idx, cu_sel, sel_capacity: as for logo_global_attn_sparse_q;
+ *   o_global [sel_capacity][Hq][d] fp32 and lse_global [Hq][sel_capacity]
+ *   from logo_global_attn_sparse_q_fwd_train; dout [sel_capacity][Hq][d]
+ *   bf16 = dL/d o_global (compact, rank order; rows at or past n_sel are
+ *   not read).
+ *   dq [N][Hq][d] fp32: rows of selected tokens, zero elsewhere; dk, dv
+ *   [N][Hkv][d] fp32 (every key).  All overwritten.
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_GLOBAL_BWD, sel_capacity) bytes
+ *   (compact Q rows and the row sums dout . o), 256-byte aligned.
+ */
+logo_status logo_global_attn_sparse_q_bwd(const logo_problem *p, const logo_bf16 *q,
+                                          const logo_bf16 *k, const logo_bf16 *v,
+                                          const int32_t *sel_idx, const int32_t *cu_sel,
+                                          int32_t sel_capacity, const float *o_global,
+                                          const float *lse_global, const logo_bf16 *dout,
+                                          float *dq, float *dk, float *dv, void *ws,
+                                          size_t ws_bytes, logo_stream stream);
 
 /*
  * logo_dense_causal_attn_fwd_train -- logo_dense_causal_attn that also keeps

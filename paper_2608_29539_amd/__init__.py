@@ -16,6 +16,7 @@ from .binding import (  # noqa: F401
     LOGO_ENTRY_FWD,
     LOGO_ENTRY_FWD_TRAIN,
     LOGO_ENTRY_GLOBAL,
+    LOGO_ENTRY_GLOBAL_BWD,
     LOGO_ENTRY_LOCAL,
     LOGO_ENTRY_SELECT,
     LOGO_PHI_LP,
@@ -40,6 +41,8 @@ from .binding import (  # noqa: F401
     logo_dense_causal_attn_fwd_train,
     logo_gate_proj,
     logo_global_attn_sparse_q,
+    logo_global_attn_sparse_q_bwd,
+    logo_global_attn_sparse_q_fwd_train,
     logo_local_attn,
     logo_pmask_initial_threshold,
     logo_ratio_capacity,

@@ -28,6 +28,7 @@ LOGO_ENTRY_DECODE = 6
 LOGO_ENTRY_FWD_TRAIN = 7
 LOGO_ENTRY_BWD = 8
 LOGO_ENTRY_DENSE_BWD = 9
+LOGO_ENTRY_GLOBAL_BWD = 10
 LOGO_PHI_LP = 0
 LOGO_PHI_SO = 1
 
@@ -38,7 +39,8 @@ EXPORTS = (
     "logo_ratio_capacity", "logo_status_str", "logo_version", "logo_budget_update",
     "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
     "logo_attn_fwd_train", "logo_attn_bwd", "logo_dense_causal_attn_fwd_train",
-    "logo_dense_causal_attn_bwd",
+    "logo_dense_causal_attn_bwd", "logo_global_attn_sparse_q_fwd_train",
+    "logo_global_attn_sparse_q_bwd",
 )
 
 _lib = None
@@ -99,6 +101,8 @@ def library():
         "logo_attn_fwd_train": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P,
                                 P, P, P, P, P, P, P, sz, P],
         "logo_dense_causal_attn_fwd_train": [PP, P, P, P, P, P, P],
+        "logo_global_attn_sparse_q_fwd_train": [PP, P, P, P, P, P, i32, P, P, P, sz, P],
+        "logo_global_attn_sparse_q_bwd": [PP, P, P, P, P, P, i32, P, P, P, P, P, P, P, sz, P],
         "logo_dense_causal_attn_bwd": [PP, P, P, P, P, P, P, P, P, P, P, sz, P],
         "logo_attn_bwd": [PP, P, P, P, P, P, P, P, P, P, f32, P, i32, P, P, P, P, P, P, P, P, P,
                           P, P, P, P, P, P, P, P, sz, P],
@@ -475,6 +479,47 @@ def logo_dense_causal_attn(prob: Problem, q, k, v, out=None):
     _check(out, torch.bfloat16, (N, Hq, d), "out")
     _call("logo_dense_causal_attn", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream())
     return out
+
+
+def logo_global_attn_sparse_q_fwd_train(prob: Problem, q, k, v, sel_idx, cu_sel,
+                                        sel_capacity: int, o_global=None, lse_global=None,
+                                        ws=None):
+    """Query-sparse global attention keeping the base-2 LSE: (o_global fp32
+    [cap, Hq, d], lse_global fp32 [Hq, cap]), compact in rank order."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    cap = int(sel_capacity)
+    if o_global is None:
+        o_global = torch.empty((max(cap, 1), Hq, d), dtype=torch.float32, device=q.device)
+    if lse_global is None:
+        lse_global = torch.empty((Hq, max(cap, 1)), dtype=torch.float32, device=q.device)
+    ws, nbytes = _ws(prob, LOGO_ENTRY_GLOBAL, max(cap, 1), ws)
+    _call("logo_global_attn_sparse_q_fwd_train", prob.c, _ptr(q), _ptr(k), _ptr(v),
+          _ptr(sel_idx), _ptr(cu_sel), cap, _ptr(o_global), _ptr(lse_global), _ptr(ws), nbytes,
+          _stream())
+    return o_global, lse_global
+
+
+def logo_global_attn_sparse_q_bwd(prob: Problem, q, k, v, sel_idx, cu_sel, sel_capacity: int,
+                                  o_global, lse_global, dout, *, ws=None) -> dict:
+    """Gradients of the query-sparse global attention alone given dout =
+    dL/d o_global (bf16 [cap, Hq, d], compact): fp32 dq (zero rows for
+    unselected tokens), dk, dv."""
+    import torch
+    N, Hq, Hkv, d = prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim
+    cap = int(sel_capacity)
+    _check(dout, torch.bfloat16, (max(cap, 1), Hq, d), "dout")
+    f32 = dict(dtype=torch.float32, device=q.device)
+    g = dict(dq=torch.empty((N, Hq, d), **f32), dk=torch.empty((N, Hkv, d), **f32),
+             dv=torch.empty((N, Hkv, d), **f32))
+    ws, nbytes = _ws(prob, LOGO_ENTRY_GLOBAL_BWD, max(cap, 1), ws)
+    _call("logo_global_attn_sparse_q_bwd", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(sel_idx),
+          _ptr(cu_sel), cap, _ptr(o_global), _ptr(lse_global), _ptr(dout), _ptr(g["dq"]),
+          _ptr(g["dk"]), _ptr(g["dv"]), _ptr(ws), nbytes, _stream())
+    return g
 
 
 def logo_dense_causal_attn_fwd_train(prob: Problem, q, k, v, out=None, lse=None):

@@ -768,6 +768,44 @@ __global__ __launch_bounds__(256) void attn_delta_kernel(int64_t n_rows, int hq,
     }
 }
 
+// Inputs of the standalone query-sparse backward: per (selected rank < the
+// device count, head) row, the compact copy of the row of Q and Delta = dO . O (O fp32,
+// dO bf16, both compact), written [Hq][cap].  d / 8 lanes per row.
+template <int D>
+__global__ __launch_bounds__(256) void sparse_prep_kernel(int64_t n_rows, int hq, int64_t cap,
+                                                          const int32_t *n_sel_dev,
+                                                          const int32_t *sel_idx,
+                                                          const uint16_t *q, const float *o,
+                                                          const uint16_t *dout, uint16_t *qc,
+                                                          float *delta) {
+    const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t row = g / (D / 8);
+    // rows of ranks at or past the selected count (read on the device) are
+    // skipped: their sel_idx entries are not written by the selection
+    const int64_t live = min((int64_t)n_sel_dev[0], cap) * hq;
+    const bool ok = row < n_rows && row < live;
+    float acc = 0.f;
+    if (ok) {
+        const int64_t r = row / hq;
+        const int h = (int)(row % hq);
+        const int c0 = (int)(g % (D / 8)) * 8;
+        const u32x4 b = *(const u32x4 *)(dout + g * 8);
+        const f32x4 o0 = *(const f32x4 *)(o + g * 8), o1 = *(const f32x4 *)(o + g * 8 + 4);
+        const float of[8] = {o0[0], o0[1], o0[2], o0[3], o1[0], o1[1], o1[2], o1[3]};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const uint32_t y = b[i];
+            acc = fmaf(of[2 * i], __uint_as_float(y << 16), acc);
+            acc = fmaf(of[2 * i + 1], __uint_as_float(y & 0xFFFF0000u), acc);
+        }
+        const int64_t tok = sel_idx[r];
+        *(u32x4 *)(qc + g * 8) = *(const u32x4 *)(q + (tok * hq + h) * D + c0);
+    }
+    acc = row_sum<D>(acc);
+    if (ok && (g % (D / 8)) == 0)
+        delta[(int64_t)(row % hq) * cap + row / hq] = acc;
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(int64_t n, float *x) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i < n)
@@ -844,6 +882,22 @@ hipError_t launch_attn_delta(int64_t n, int hq, int head_dim, const uint16_t *o,
     else
         hipLaunchKernelGGL((attn_delta_kernel<64>), grid, dim3(256), 0, s, n * hq, hq, n, o, dout,
                            delta);
+    return hipGetLastError();
+}
+
+hipError_t launch_sparse_prep(int64_t cap, int hq, int head_dim, const int32_t *n_sel_dev,
+                              const int32_t *sel_idx, const uint16_t *q, const float *o,
+                              const uint16_t *dout, uint16_t *qc, float *delta, hipStream_t s) {
+    const int64_t threads = cap * hq * (head_dim / 8);
+    if (threads <= 0)
+        return hipSuccess;
+    const dim3 grid((unsigned)((threads + 255) / 256));
+    if (head_dim == 128)
+        hipLaunchKernelGGL((sparse_prep_kernel<128>), grid, dim3(256), 0, s, cap * hq, hq, cap,
+                           n_sel_dev, sel_idx, q, o, dout, qc, delta);
+    else
+        hipLaunchKernelGGL((sparse_prep_kernel<64>), grid, dim3(256), 0, s, cap * hq, hq, cap,
+                           n_sel_dev, sel_idx, q, o, dout, qc, delta);
     return hipGetLastError();
 }
 

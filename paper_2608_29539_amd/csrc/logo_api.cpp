@@ -225,6 +225,19 @@ BwdWs bwd_ws(const logo_problem *p, int32_t cap) {
     return w;
 }
 
+// standalone query-sparse backward: compact Q rows and Delta
+struct GlobalBwdWs {
+    size_t qc, delta, total;
+};
+GlobalBwdWs global_bwd_ws(const logo_problem *p, int32_t cap) {
+    GlobalBwdWs w;
+    const size_t H = (size_t)p->num_q_heads, d = p->head_dim;
+    w.qc = 0;
+    w.delta = align_up(2 * (size_t)cap * H * d);
+    w.total = w.delta + align_up(4 * H * (size_t)cap);
+    return w;
+}
+
 size_t dense_bwd_ws(const logo_problem *p) {
     return align_up(sizeof(float) * (size_t)p->num_q_heads * (size_t)p->total_tokens);
 }
@@ -587,6 +600,7 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_FWD_TRAIN: return train_ws(p, cap).total;
     case LOGO_ENTRY_BWD: return bwd_ws(p, cap).total;
     case LOGO_ENTRY_DENSE_BWD: return dense_bwd_ws(p);
+    case LOGO_ENTRY_GLOBAL_BWD: return global_bwd_ws(p, cap).total;
     case LOGO_ENTRY_LOCAL:
     case LOGO_ENTRY_COMBINE:
     case LOGO_ENTRY_DENSE: return 0;
@@ -1069,6 +1083,95 @@ logo_status logo_dense_causal_attn_bwd(const logo_problem *p, const logo_bf16 *q
     st = hip_status(launch_bwd_dq(kModeLocal, p->head_dim, a, (int)grid_q, s), s);
     if (st == LOGO_OK)
         st = hip_status(launch_bwd_dkv(kModeLocal, p->head_dim, a, (int)grid_kv, s), s);
+    return st;
+}
+
+logo_status logo_global_attn_sparse_q_fwd_train(const logo_problem *p, const logo_bf16 *q,
+                                                const logo_bf16 *k, const logo_bf16 *v,
+                                                const int32_t *sel_idx, const int32_t *cu_sel,
+                                                int32_t sel_capacity, float *o_global,
+                                                float *lse_global, void *ws, size_t ws_bytes,
+                                                logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    if (!cu_sel)
+        return LOGO_ERR_NULL;
+    if (sel_capacity > 0 && p->total_tokens > 0 &&
+        (!q || !k || !v || !sel_idx || !o_global || !lse_global))
+        return LOGO_ERR_NULL;
+    if (sel_capacity > 0 && p->total_tokens > 0) {
+        st = check_ws(ws, ws_bytes, global_ws(p, sel_capacity).total);
+        if (st != LOGO_OK)
+            return st;
+    }
+    return run_global(p, q, k, v, sel_idx, cu_sel, sel_capacity, o_global, nullptr, nullptr,
+                      (char *)ws, (hipStream_t)stream, nullptr, false, lse_global);
+}
+
+logo_status logo_global_attn_sparse_q_bwd(const logo_problem *p, const logo_bf16 *q,
+                                          const logo_bf16 *k, const logo_bf16 *v,
+                                          const int32_t *sel_idx, const int32_t *cu_sel,
+                                          int32_t sel_capacity, const float *o_global,
+                                          const float *lse_global, const logo_bf16 *dout,
+                                          float *dq, float *dk, float *dv, void *ws,
+                                          size_t ws_bytes, logo_stream stream) {
+    logo_status st = check_problem(p);
+    if (st != LOGO_OK)
+        return st;
+    if (sel_capacity < 0)
+        return LOGO_ERR_SHAPE;
+    const int32_t N = p->total_tokens, cap = sel_capacity;
+    if (!cu_sel)
+        return LOGO_ERR_NULL;
+    if (N > 0 && (!q || !k || !v || !dq || !dk || !dv))
+        return LOGO_ERR_NULL;
+    if (N > 0 && cap > 0 && (!sel_idx || !o_global || !lse_global || !dout))
+        return LOGO_ERR_NULL;
+    const GlobalBwdWs w = global_bwd_ws(p, cap);
+    st = check_ws(ws, ws_bytes, w.total);
+    if (st != LOGO_OK)
+        return st;
+    if (N == 0)
+        return LOGO_OK;
+    hipStream_t s = (hipStream_t)stream;
+    const int H = p->num_q_heads, d = p->head_dim;
+    char *base = (char *)ws;
+    uint16_t *qc = (uint16_t *)(base + w.qc);
+    float *delta = (float *)(base + w.delta);
+    st = hip_status(launch_fill_zero((int64_t)N * H * d, dq, s), s);
+    if (st == LOGO_OK && cap > 0)
+        st = hip_status(launch_sparse_prep(cap, H, d, cu_sel + p->num_seqs, sel_idx, q, o_global,
+                                           dout, qc, delta, s),
+                        s);
+    if (st != LOGO_OK)
+        return st;
+    BwdArgs a = make_bwd_args(p);
+    a.cap = cap;
+    a.q = qc;
+    a.k = k;
+    a.v = v;
+    a.dout = dout;
+    a.lse = lse_global;
+    a.delta = delta;
+    a.row_stride = cap;
+    a.sel_idx = sel_idx;
+    a.cu_sel = cu_sel;
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+    const long long grid_q = (long long)a.n_hg * p->num_seqs * a.ntile_max;
+    const int kpb = bwd_keys_per_block();
+    const long long grid_kv =
+        (long long)((p->max_seqlen + kpb - 1) / kpb) * p->num_seqs * p->num_kv_heads;
+    if (grid_q >= (1LL << 31) || grid_kv >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    if (cap > 0)
+        st = hip_status(launch_bwd_dq(kModeGlobal, d, a, (int)grid_q, s), s);
+    if (st == LOGO_OK)
+        st = hip_status(launch_bwd_dkv(kModeGlobal, d, a, (int)grid_kv, s), s);
     return st;
 }
 

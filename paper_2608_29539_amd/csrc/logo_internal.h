@@ -220,6 +220,11 @@ int gain_grad_chunks(int rows);
 hipError_t launch_gain_grad(int rows, int cols, const float *part, float *tmp, float *out,
                             hipStream_t s);
 hipError_t launch_fill_zero(int64_t n, float *x, hipStream_t s);
+// Compact Q rows + Delta for the standalone query-sparse backward: ranks
+// below min(n_sel_dev[0], cap) (the selected count, read on the device).
+hipError_t launch_sparse_prep(int64_t cap, int hq, int head_dim, const int32_t *n_sel_dev,
+                              const int32_t *sel_idx, const uint16_t *q, const float *o,
+                              const uint16_t *dout, uint16_t *qc, float *delta, hipStream_t s);
 hipError_t launch_attn_delta(int64_t n, int hq, int head_dim, const uint16_t *o,
                              const uint16_t *dout, float *delta, hipStream_t s);
 hipError_t launch_bwd_dq(int mode, int head_dim, const BwdArgs &a, int grid, hipStream_t s);

@@ -151,3 +151,70 @@ def test_dense_backward(pk, ci):
         print(f"[dense bwd case{ci}] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}",
               flush=True)
         assert e["rel_l2"] <= REL_L2 and e["rel_max"] <= REL_MAX, (ci, nm, e)
+
+
+SPARSE_CASES = [
+    # (seqlens, Hq, Hkv, d, ratio)
+    ((300, 1000), 8, 2, 128, 0.25),
+    ((64, 700, 33), 4, 4, 64, 0.5),
+    ((2048,), 8, 8, 128, 0.5),
+    ((129, 5), 4, 1, 128, 0.0),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(SPARSE_CASES)))
+def test_sparse_global_backward(pk, ci):
+    """The query-sparse global attention alone (training forward + backward)
+    against the oracle's attention backward with dout zero on unselected
+    rows (the operator's loss sees only the selected rows)."""
+    import torch
+    lens, hq, hkv, d, ratio = SPARSE_CASES[ci]
+    w = synth.small_workload(lens, hq, hkv, d, 1, ratio, seed=5200 + ci)
+    x = synth.make_inputs(w)
+    dout = synth.make_dout(w, 3)
+    thr = oracle.thresholds(x["gate"], x["cu_seqlens"], oracle.SEL_RATIO, ratio=ratio)
+    sel = oracle.select(x["gate"], x["cu_seqlens"], thr)[0]
+    n = sel.size
+    dev = to_device(x)
+    prob = pk.Problem(dev["cu_seqlens"], hq, hkv, d, max(lens), cu_seqlens_host=x["cu_seqlens"])
+    cap = max(pk.logo_ratio_capacity(prob, ratio), 1)
+    print(f"[sparse bwd case{ci}] seqlens={lens} H={hq}/{hkv} d={d} n_sel={n}", flush=True)
+    sel_idx, cu_sel, _, _ = pk.logo_select(prob, dev["gate"], ratio=ratio, sel_capacity=cap)
+    assert sel_idx[:n].cpu().numpy().tolist() == sel.tolist()
+    o, lse = pk.logo_global_attn_sparse_q_fwd_train(prob, dev["q"], dev["k"], dev["v"], sel_idx,
+                                                    cu_sel, cap)
+    dc = np.zeros((cap,) + dout.shape[1:], np.uint16)
+    dc[:n] = dout[sel]
+    g = pk.logo_global_attn_sparse_q_bwd(prob, dev["q"], dev["k"], dev["v"], sel_idx, cu_sel,
+                                         cap, o, lse, to_device(dict(d=dc))["d"])
+    torch.cuda.synchronize()
+    full = np.zeros(dout.shape)
+    full[sel] = synth.f32_from_bf16_bits(dout[sel]).reshape((n,) + dout.shape[1:])
+    ref = oracle.attn_bwd(x["q"], x["k"], x["v"], x["cu_seqlens"], 0, full)
+    for nm in ("dq", "dk", "dv"):
+        got = g[nm].cpu().numpy()
+        if n == 0:
+            assert not got.any(), (ci, nm)
+            continue
+        e = grad_err(got, ref[nm])
+        print(f"[sparse bwd case{ci}] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}",
+              flush=True)
+        assert e["rel_l2"] <= REL_L2 and e["rel_max"] <= REL_MAX, (ci, nm, e)
+    unsel = np.setdiff1d(np.arange(w.total_tokens), sel)
+    assert not g["dq"].cpu().numpy()[unsel].any()
+
+
+def test_backward_deterministic(pk):
+    """Two backward passes on the same inputs are bit-identical (no float
+    atomics; fixed-order reductions)."""
+    import torch
+    w = synth.small_workload((700, 1500), 8, 2, 128, 200, 0.25, seed=5300)
+    x = synth.make_inputs(w)
+    dev = to_device(dict(x, dout=synth.make_dout(w, 4)))
+    prob = pk.Problem(dev["cu_seqlens"], 8, 2, 128, 200, cu_seqlens_host=x["cu_seqlens"])
+    saved = pk.logo_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=0.25)
+    g1 = pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved, dev["dout"])
+    g2 = pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved, dev["dout"])
+    torch.cuda.synchronize()
+    for nm in g1:
+        assert torch.equal(g1[nm], g2[nm]), nm
