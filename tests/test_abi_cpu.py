@@ -303,3 +303,26 @@ def test_train_and_backward_validation(lib):
         assert call(**{f"a{i}": None}) == ERR_NULL, i
     assert call(a11=need_d - 4) == ERR_WORKSPACE
     assert lib.logo_dense_causal_attn_fwd_train(p.c, None, FAKE, FAKE, FAKE, None, None) == ERR_NULL
+
+
+def test_sparse_operator_training_validation(lib):
+    """The standalone query-sparse training entry points reject bad
+    arguments before any launch."""
+    p = Prob(seqlens=(100, 50), hq=8, hkv=2, d=128, window=16)
+    need_f = lib.logo_workspace_bytes(p.c, 2, 40)
+    call = _caller(lib.logo_global_attn_sparse_q_fwd_train,
+                   [p.c, FAKE, FAKE, FAKE, FAKE, FAKE, 40, FAKE, FAKE, FAKE, need_f, None])
+    for i in (1, 2, 3, 4, 5, 7, 8):
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    assert call(a6=-1) == ERR_SHAPE
+    assert call(a10=need_f - 1) == ERR_WORKSPACE
+    need_b = lib.logo_workspace_bytes(p.c, 10, 40)
+    assert need_b >= 40 * 8 * 128 * 2 + 8 * 40 * 4
+    call = _caller(lib.logo_global_attn_sparse_q_bwd,
+                   [p.c, FAKE, FAKE, FAKE, FAKE, FAKE, 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                    FAKE, need_b, None])
+    for i in (1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 12):
+        assert call(**{f"a{i}": None}) == ERR_NULL, i
+    assert call(a6=-1) == ERR_SHAPE
+    assert call(a14=need_b - 1) == ERR_WORKSPACE
+    assert call(a13=ctypes.c_void_p(0x1010)) == ERR_WORKSPACE      # misaligned
