@@ -22,6 +22,7 @@ from .oracle import (  # noqa: F401
     gate_proj,
     library_path,
     logo_bwd,
+    logo_bwd_sample,
     logo_fwd,
     logo_rows,
     num_threads,

@@ -890,3 +890,188 @@ void oracle_attn_bwd(const uint16_t *q, const uint16_t *k, const uint16_t *v, co
         free(qrow);
     }
 }
+
+/*
+ * The layer backward (as oracle_logo_bwd, same chain rule, fp64) evaluated
+ * only where a test samples it: dq and dq_g of the query tokens qrows[], dgate
+ * of those tokens, and dk, dv, dk_g, dv_g of the key tokens keys[].  The
+ * selection is given (tok2sel [N], rank or -1).  A key's gradient sums over
+ * every row that sees it: rows j..j+w-1 of its sequence for the local branch,
+ * every selected row at or after it for the global branch; those rows are
+ * recomputed in full (forward, ContextNorm backward, softmax backward).
+ * Outputs: dq_s, dqg_s [n_q][Hq][d], dgate_s [n_q], dk_s, dv_s, dkg_s, dvg_s
+ * [n_k][Hkv][d] (overwritten; the global ones are the global-branch tensors'
+ * gradients; a caller with aliased tensors adds the pairs).
+ */
+void oracle_logo_bwd_sample(const uint16_t *q, const uint16_t *k, const uint16_t *v,
+                            const uint16_t *q_g, const uint16_t *k_g, const uint16_t *v_g,
+                            const float *gate, const int32_t *cu, int B, int Hq, int Hkv, int d,
+                            int window, double scale, const int32_t *tok2sel,
+                            const float *gain_local, const float *gain_global, double eps,
+                            const double *dout, int64_t n_q, const int32_t *qrows, int64_t n_k,
+                            const int32_t *keys, double *dq_s, double *dqg_s, double *dgate_s,
+                            double *dk_s, double *dv_s, double *dkg_s, double *dvg_s)
+{
+    const int64_t N = cu[B];
+    const int G = Hq / Hkv;
+    if (scale <= 0.0)
+        scale = 1.0 / sqrt((double)d);
+    if (!q_g)
+        q_g = q;
+    if (!k_g)
+        k_g = k;
+    if (!v_g)
+        v_g = v;
+    const int64_t row = (int64_t)Hq * d;
+    /* sample index of each token as a query / as a key, or -1 */
+    int64_t *qpos = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    int64_t *kpos = (int64_t *)malloc((size_t)(N > 0 ? N : 1) * sizeof(int64_t));
+    for (int64_t t = 0; t < N; t++)
+        qpos[t] = kpos[t] = -1;
+    for (int64_t a = 0; a < n_q; a++)
+        qpos[qrows[a]] = a;
+    for (int64_t a = 0; a < n_k; a++)
+        kpos[keys[a]] = a;
+    memset(dq_s, 0, (size_t)n_q * row * sizeof(double));
+    memset(dqg_s, 0, (size_t)n_q * row * sizeof(double));
+    memset(dgate_s, 0, (size_t)n_q * sizeof(double));
+    memset(dk_s, 0, (size_t)n_k * Hkv * d * sizeof(double));
+    memset(dv_s, 0, (size_t)n_k * Hkv * d * sizeof(double));
+    memset(dkg_s, 0, (size_t)n_k * Hkv * d * sizeof(double));
+    memset(dvg_s, 0, (size_t)n_k * Hkv * d * sizeof(double));
+    /* rows to recompute, per branch: the sampled queries and every row that
+       sees a sampled key */
+    char *need = (char *)calloc((size_t)(N > 0 ? N : 1) * 2, 1);
+    for (int b = 0; b < B; b++) {
+        const int64_t base = cu[b], T = (int64_t)cu[b + 1] - base;
+        for (int64_t i = 0; i < T; i++) {
+            const int64_t t = base + i;
+            if (qpos[t] >= 0) {
+                need[2 * t] = 1;
+                need[2 * t + 1] = tok2sel[t] >= 0;
+            }
+            if (kpos[t] >= 0) {
+                const int64_t hi = (window >= 1 && i + window < T) ? i + window : T;
+                for (int64_t r = i; r < hi; r++)
+                    need[2 * (base + r)] = 1;
+                for (int64_t r = i; r < T; r++)
+                    if (tok2sel[base + r] >= 0)
+                        need[2 * (base + r) + 1] = 1;
+            }
+        }
+    }
+    int64_t max_T = 1;
+    for (int b = 0; b < B; b++)
+        if ((int64_t)cu[b + 1] - cu[b] > max_T)
+            max_T = (int64_t)cu[b + 1] - cu[b];
+    /* one job per (branch, KV head): its keys' and its heads' outputs only */
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int job = 0; job < 2 * Hkv; job++) {
+        const int br = job / Hkv, hk = job % Hkv;
+        const uint16_t *Qm = br ? q_g : q, *Km = br ? k_g : k, *Vm = br ? v_g : v;
+        const float *gmat = br ? gain_global : gain_local;
+        double *wts = (double *)malloc((size_t)max_T * sizeof(double));
+        double *gsc = (double *)malloc((size_t)max_T * sizeof(double));
+        double *qv = (double *)malloc((size_t)d * sizeof(double));
+        double *ov = (double *)malloc((size_t)d * sizeof(double));
+        double *go = (double *)malloc((size_t)d * sizeof(double));
+        for (int b = 0; b < B; b++) {
+            const int64_t base = cu[b], T = (int64_t)cu[b + 1] - base;
+            for (int64_t i = 0; i < T; i++) {
+                const int64_t t = base + i;
+                if (!need[2 * t + br])
+                    continue;
+                const int64_t j0 = (br == 0 && window >= 1 && i - window + 1 > 0) ? i - window + 1 : 0;
+                const int64_t cnt = i - j0 + 1;
+                const double pg = (double)gate[t];
+                const int sel = tok2sel[t] >= 0;
+                const double wb = br ? pg : (sel ? 1.0 - pg : 1.0);
+                for (int h = hk * G; h < (hk + 1) * G; h++) {
+                    const int64_t qo = (t * Hq + h) * (int64_t)d;
+                    for (int c = 0; c < d; c++)
+                        qv[c] = bf16_to_double(Qm[qo + c]);
+                    double mx = -INFINITY;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        const int64_t ko = ((base + j0 + j) * Hkv + hk) * (int64_t)d;
+                        double acc = 0.0;
+                        for (int c = 0; c < d; c++)
+                            acc += qv[c] * bf16_to_double(Km[ko + c]);
+                        wts[j] = scale * acc;
+                        mx = wts[j] > mx ? wts[j] : mx;
+                    }
+                    double z = 0.0;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        wts[j] = exp(wts[j] - mx);
+                        z += wts[j];
+                    }
+                    for (int c = 0; c < d; c++)
+                        ov[c] = 0.0;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        wts[j] /= z;
+                        const int64_t vo = ((base + j0 + j) * Hkv + hk) * (int64_t)d;
+                        for (int c = 0; c < d; c++)
+                            ov[c] += wts[j] * bf16_to_double(Vm[vo + c]);
+                    }
+                    double msq = 0.0;
+                    for (int c = 0; c < d; c++)
+                        msq += ov[c] * ov[c];
+                    const double rms = sqrt(msq / (double)d + eps);
+                    const double *gr = dout + qo;
+                    double gsum = 0.0, yside = 0.0;
+                    for (int c = 0; c < d; c++) {
+                        const double gc = gmat ? (double)gmat[(int64_t)h * d + c] : 1.0;
+                        gsum += gc * wb * gr[c] * ov[c];
+                        yside += gr[c] * ov[c] / rms * gc;
+                    }
+                    if (br == 0 && qpos[t] >= 0 && sel) {
+#pragma omp atomic
+                        dgate_s[qpos[t]] -= yside;
+                    }
+                    if (br == 1 && qpos[t] >= 0) {
+#pragma omp atomic
+                        dgate_s[qpos[t]] += yside;
+                    }
+                    for (int c = 0; c < d; c++) {
+                        const double gc = gmat ? (double)gmat[(int64_t)h * d + c] : 1.0;
+                        go[c] = gc * wb * gr[c] / rms - ov[c] * gsum / ((double)d * rms * rms * rms);
+                    }
+                    double rdot = 0.0;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        const int64_t vo = ((base + j0 + j) * Hkv + hk) * (int64_t)d;
+                        double acc = 0.0;
+                        for (int c = 0; c < d; c++)
+                            acc += go[c] * bf16_to_double(Vm[vo + c]);
+                        gsc[j] = acc;
+                        rdot += wts[j] * acc;
+                    }
+                    double *dqr = qpos[t] >= 0 ? (br ? dqg_s : dq_s) + (qpos[t] * Hq + h) * (int64_t)d
+                                               : NULL;
+                    for (int64_t j = 0; j < cnt; j++) {
+                        const double g_s = wts[j] * (gsc[j] - rdot);
+                        const int64_t kt = base + j0 + j;
+                        const int64_t ko = (kt * Hkv + hk) * (int64_t)d;
+                        if (dqr)
+                            for (int c = 0; c < d; c++)
+                                dqr[c] += scale * g_s * bf16_to_double(Km[ko + c]);
+                        if (kpos[kt] >= 0) {
+                            double *dkr = (br ? dkg_s : dk_s) + (kpos[kt] * Hkv + hk) * (int64_t)d;
+                            double *dvr = (br ? dvg_s : dv_s) + (kpos[kt] * Hkv + hk) * (int64_t)d;
+                            for (int c = 0; c < d; c++) {
+                                dkr[c] += scale * g_s * qv[c];
+                                dvr[c] += wts[j] * go[c];
+                            }
+                        }
+                    }
+                }
+            }
+        }
+        free(wts);
+        free(gsc);
+        free(qv);
+        free(ov);
+        free(go);
+    }
+    free(qpos);
+    free(kpos);
+    free(need);
+}

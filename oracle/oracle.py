@@ -74,6 +74,10 @@ def _load():
     lib.oracle_logo_bwd.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64, i32,
                                     f32, f64, P, P, f64, P, P, P, P, P, P, P, P, P, P]
     lib.oracle_logo_bwd.restype = i64
+    lib.oracle_logo_bwd_sample.argtypes = [P, P, P, P, P, P, P, P, i32, i32, i32, i32, i32, f64,
+                                           P, P, P, f64, P, i64, P, i64, P, P, P, P, P, P, P,
+                                           P]
+    lib.oracle_logo_bwd_sample.restype = None
     lib.oracle_attn_bwd.argtypes = [P, P, P, P, i32, i32, i32, i32, i32, f64, P, P, P, P]
     lib.oracle_attn_bwd.restype = None
     lib.oracle_fusion_bwd.argtypes = [P, P, P, P, i64, i32, i32, P, P, f64, P, P, P, P, P, P, P,
@@ -357,3 +361,47 @@ def attn_bwd(q, k, v, cu_seqlens, window: int, dout, *, scale: float = 0.0
     _load().oracle_attn_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(cu), cu.size - 1, Hq, Hkv, d,
                             int(window), float(scale), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv))
     return dict(dq=dq[:N], dk=dk[:N], dv=dv[:N])
+
+
+def logo_bwd_sample(x: Dict[str, np.ndarray], window: int, dout, qrows, keys, *,
+                    ratio: Optional[float] = None, threshold: Optional[float] = None,
+                    gain_local=None, gain_global=None, eps: float = 1e-6,
+                    scale: float = 0.0) -> Dict[str, np.ndarray]:
+    """The layer backward (fp64) at sampled places only: dq / dq_g / dgate of
+    the query tokens ``qrows`` and dk / dv / dk_g / dv_g of the key tokens
+    ``keys`` (selection over the whole sequences, as the layer does).  With
+    aliased global tensors (no q_g / k_g / v_g in ``x``) dq, dk, dv include
+    both branches.  The cost grows with the rows that see a sampled key:
+    sample global-branch keys near the end of their sequence."""
+    if (ratio is None) == (threshold is None):
+        raise ValueError("give exactly one of ratio / threshold")
+    mode = SEL_RATIO if ratio is not None else SEL_THRESHOLD
+    thr = thresholds(x["gate"], x["cu_seqlens"], mode,
+                     threshold=threshold if threshold is not None else 0.0,
+                     ratio=ratio if ratio is not None else 0.0)
+    _, _, tok2sel = select(x["gate"], x["cu_seqlens"], thr)
+    alias = "q_g" not in x and "k_g" not in x and "v_g" not in x
+    q, k, v = _c(x["q"], np.uint16), _c(x["k"], np.uint16), _c(x["v"], np.uint16)
+    qg, kg, vg = (_c(x.get(n), np.uint16) for n in ("q_g", "k_g", "v_g"))
+    gate, cu = _c(x["gate"], np.float32), _c(x["cu_seqlens"], np.int32)
+    qrows, keys = _c(np.asarray(qrows), np.int32), _c(np.asarray(keys), np.int32)
+    dout = _c(dout, np.float64)
+    N, Hq, d = q.shape
+    Hkv = k.shape[1]
+    nq, nk = qrows.size, keys.size
+    dq, dqg = np.empty((max(nq, 1), Hq, d)), np.empty((max(nq, 1), Hq, d))
+    dgate = np.empty(max(nq, 1))
+    dk, dv, dkg, dvg = (np.empty((max(nk, 1), Hkv, d)) for _ in range(4))
+    _load().oracle_logo_bwd_sample(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(qg), _ptr(kg), _ptr(vg), _ptr(gate), _ptr(cu),
+        cu.size - 1, Hq, Hkv, d, int(window), float(scale), _ptr(_c(tok2sel, np.int32)),
+        _ptr(_c(gain_local, np.float32)), _ptr(_c(gain_global, np.float32)), float(eps),
+        _ptr(dout), nq, _ptr(qrows), nk, _ptr(keys), _ptr(dq), _ptr(dqg), _ptr(dgate), _ptr(dk),
+        _ptr(dv), _ptr(dkg), _ptr(dvg))
+    r = dict(dgate=dgate[:nq], tok2sel=tok2sel)
+    if alias:
+        r.update(dq=(dq + dqg)[:nq], dk=(dk + dkg)[:nk], dv=(dv + dvg)[:nk])
+    else:
+        r.update(dq=dq[:nq], dk=dk[:nk], dv=dv[:nk], dq_g=dqg[:nq], dk_g=dkg[:nk],
+                 dv_g=dvg[:nk])
+    return r

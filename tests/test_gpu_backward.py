@@ -218,3 +218,48 @@ def test_backward_deterministic(pk):
     torch.cuda.synchronize()
     for nm in g1:
         assert torch.equal(g1[nm], g2[nm]), nm
+
+
+def test_backward_full_size_sampled(pk):
+    """T32k-gqa (32768 tokens, 32/8 heads, d 128, w 1024, ratio 1/8, bursty
+    gate) in the launch configuration the benchmark times, checked against
+    the oracle at sampled places: dq and dgate of 48 query rows (selected and
+    unselected, sequence edges, the latest selected rows) and dk / dv of 8
+    keys near the sequence end (their gradient sums over every row that sees
+    them), plus the key-gradient sum over all 32768 keys, which softmax shift
+    invariance makes zero for each KV head."""
+    import torch
+    w = synth.WORKLOADS["T32k-gqa"]
+    x = synth.make_inputs(w)
+    dout = synth.make_dout(w, 1)
+    dev = to_device(dict(x, dout=dout))
+    prob = pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
+                      cu_seqlens_host=x["cu_seqlens"])
+    print("[bwd full] T32k-gqa", flush=True)
+    saved = pk.logo_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                   ratio=w.ratio)
+    g = pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved, dev["dout"])
+    torch.cuda.synchronize()
+    N = w.total_tokens
+    t2s = saved["tok2sel"].cpu().numpy()
+    sel = np.nonzero(t2s >= 0)[0]
+    uns = np.nonzero(t2s < 0)[0]
+    rng = np.random.default_rng(77)
+    qrows = np.unique(np.concatenate([
+        [0, 1, 1023, 1024, N - 1], sel[:3], sel[-6:], rng.choice(sel, 14, replace=False),
+        rng.choice(uns, 20, replace=False)]))
+    keys = np.unique(np.concatenate([[N - 1, N - 2, N - 64, N - 65, N - 300],
+                                     rng.integers(N - 600, N, 3)]))
+    d64 = synth.f32_from_bf16_bits(dout).reshape(dout.shape).astype(np.float64)
+    ref = oracle.logo_bwd_sample(x, w.window, d64, qrows, keys, ratio=w.ratio)
+    assert np.array_equal(ref["tok2sel"], t2s)
+    for nm, idx in (("dq", qrows), ("dgate", qrows), ("dk", keys), ("dv", keys)):
+        e = grad_err(g[nm].cpu().numpy()[idx], ref[nm])
+        print(f"[bwd full] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}", flush=True)
+        assert e["rel_l2"] <= REL_L2 and e["rel_max"] <= REL_MAX, (nm, e)
+    dk = g["dk"].double()
+    rms = dk.pow(2).mean(dim=0).sqrt()                      # [Hkv, d]
+    zero_sum = dk.sum(dim=0).abs() / (rms * math.sqrt(N))
+    print(f"[bwd full] key-gradient sum / (sqrt(N) rms): max {float(zero_sum.max()):.3g}",
+          flush=True)
+    assert float(zero_sum.max()) <= 0.05

@@ -88,6 +88,10 @@ MUTATIONS = {
     "attn_bwd_rowdot_dropped": ("const double g_s = w_p[j] * (w_dp[j] - rowdot);",
                                 "const double g_s = w_p[j] * w_dp[j];"),
     "attn_bwd_dv_unweighted": ("dv[ko + c] += w_p[j] * go[c];", "dv[ko + c] += go[c];"),
+    "bwd_sample_key_rows_short": ("(window >= 1 && i + window < T) ? i + window : T",
+                                  "(window >= 1 && i + window - 1 < T) ? i + window - 1 : T"),
+    "bwd_sample_global_rows_unselected": ("                    if (tok2sel[base + r] >= 0)\n                        need[2 * (base + r) + 1] = 1;",
+                                          "                    need[2 * (base + r) + 1] = 0;"),
     "attn_bwd_window_w_plus_1_keys": ("(window >= 1 && i - window + 1 > 0) ? i - window + 1 : 0",
                                       "(window >= 1 && i - window > 0) ? i - window : 0"),
 }

@@ -802,3 +802,32 @@ def test_attn_bwd_window_one(oracle_lib):
     assert not r["dq"].any() and not r["dk"].any()
     np.testing.assert_allclose(r["dv"], dout.reshape(N, Hkv, Hq // Hkv, d).sum(axis=2),
                                atol=1e-12)
+
+
+@pytest.mark.parametrize("distinct", [False, True])
+def test_backward_sample_matches_full(oracle_lib, distinct):
+    """The sampled backward equals the full backward (itself pinned by finite
+    differences above) at the sampled queries and keys."""
+    rng = np.random.default_rng(990 + distinct)
+    seqlens, Hq, Hkv, d, w = (40, 1, 57), 4, 2, 8, 7
+    N = sum(seqlens)
+    mk = lambda *s: bf16(np.round(rng.standard_normal(s) * 8) / 8)  # noqa: E731
+    x = dict(q=mk(N, Hq, d), k=mk(N, Hkv, d), v=mk(N, Hkv, d),
+             gate=rng.uniform(0, 1, N).astype(np.float32),
+             cu_seqlens=np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32))
+    if distinct:
+        x.update(q_g=mk(N, Hq, d), k_g=mk(N, Hkv, d), v_g=mk(N, Hkv, d))
+    gl = rng.uniform(0.5, 1.5, (Hq, d)).astype(np.float32)
+    dout = rng.standard_normal((N, Hq, d))
+    full = oracle_lib.logo_bwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w, dout,
+                               ratio=0.3, q_g=x.get("q_g"), k_g=x.get("k_g"), v_g=x.get("v_g"),
+                               gain_local=gl, eps=1e-4)
+    qrows = np.array([0, 5, 39, 40, 41, 60, 97])
+    keys = np.array([0, 3, 39, 40, 44, 80, 97])
+    smp = oracle_lib.logo_bwd_sample(x, w, dout, qrows, keys, ratio=0.3, gain_local=gl,
+                                     eps=1e-4)
+    names = [("dq", qrows), ("dgate", qrows), ("dk", keys), ("dv", keys)]
+    if distinct:
+        names += [("dq_g", qrows), ("dk_g", keys), ("dv_g", keys)]
+    for nm, idx in names:
+        np.testing.assert_allclose(smp[nm], full[nm][idx], rtol=1e-11, atol=1e-12, err_msg=nm)
