@@ -60,7 +60,8 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_global_T32k-gqa_traffic.md")
 # Sources whose change invalidates the committed counter figures: the global
 # kernel, its tiling constants and the tile plan that orders its work.
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_29539_amd", "csrc", f)
-               for f in ("attention.hip", "logo_internal.h", "plan.h", "select.hip")]
+               for f in ("attention.hip", "attn_common.h", "logo_internal.h", "plan.h",
+                         "select.hip")]
 
 
 def kernel_source_hash() -> str:
