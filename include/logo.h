@@ -229,10 +229,9 @@ logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
                                    logo_stream stream, void *const *events);
 
 /*
- * logo_attn_fwd_train -- the layer forward for training: the same output as
- * logo_attn_fwd, computed through the unfused path (select, raw local
- * branch, raw global branch, logo_combine), keeping what logo_attn_bwd
- * needs.  The selection outputs are required here (they are the saved
+ * logo_attn_fwd_train -- the layer forward for training: logo_attn_fwd (the
+ * same launches and output) whose attention epilogues also keep what
+ * logo_attn_bwd needs.  The selection outputs are required here (they are the saved
  * routing decision of Sec. 3.3, held fixed by the backward pass).
  *   sel_idx [sel_capacity], cu_sel [B+1], tok2sel [N]: as for logo_select
  *   (sel_idx may be NULL only when sel_capacity is 0); thr_out [B] or NULL.

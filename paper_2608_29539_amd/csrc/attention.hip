@@ -288,7 +288,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     for (int rg = 0; rg < RG; rg++) {
         ep_gate[rg] = 0.f;
         ep_rank[rg] = -1;
-        if (EPI == kEpiFused && MODE != kModeDense) {
+        if (EPI != kEpiRaw && MODE != kModeDense) {
             ep_gate[rg] = a.gate[qtok[rg]];
             ep_rank[rg] = (MODE == kModeGlobal) ? (int)orow[rg] : a.tok2sel[qtok[rg]];
         }
@@ -598,7 +598,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
 #pragma unroll
     for (int rg = 0; rg < RG; rg++) {
         const float inv = 1.f / l_tot[rg];
-        if (EPI == kEpiFused && MODE != kModeDense) {
+        if (EPI != kEpiRaw && MODE != kModeDense) {
             // ContextNorm over the row's d values (this lane holds d/2 of them,
             // its partner l^32 the other half), the softmax's 1/l, the fusion
             // weight and the gain folded into one scale per element:
@@ -612,6 +612,23 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
             ss = pair_sum(ss);
             if (!(wave_valid && row_valid[rg]))
                 continue;
+            if constexpr (EPI == kEpiFusedTrain) {
+                // training forward: also the raw branch output (fp32, token
+                // rows for the local branch, rank rows for the global one) and
+                // the row's base-2 log-sum-exp of the scaled scores
+                if (g == 0)
+                    a.lse[(int64_t)head * a.lse_stride + orow[rg]] =
+                        (m_ref[rg] == kNegInf ? 0.f : m_ref[rg]) + log2f(l_tot[rg]);
+                float *rp = (float *)a.out + (orow[rg] * a.hq + head) * (int64_t)D + g * 4;
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+                    for (int qd = 0; qd < 4; qd++) {
+                        const f32x4 v = {acc[rg][cb][qd * 4 + 0] * inv, acc[rg][cb][qd * 4 + 1] * inv,
+                                         acc[rg][cb][qd * 4 + 2] * inv, acc[rg][cb][qd * 4 + 3] * inv};
+                        *(f32x4 *)(rp + cb * 32 + qd * 8) = v;
+                    }
+            }
             const float rn = 1.f / sqrtf(ss * inv * inv / (float)D + a.eps);
             const int64_t tok = qtok[rg];
             const float p = ep_gate[rg];
@@ -719,7 +736,7 @@ void attn_kernel(const AttnArgs a) {
         }
     } else {
         int bid = blockIdx.x;
-        if constexpr (MODE == kModeLocal && EPI == kEpiFused) {
+        if constexpr (MODE == kModeLocal && EPI != kEpiRaw) {
             // The fused layer's local launch: workgroup 0 builds the global
             // branch's work table (its LDS holds the table), the rest attend.
             if (a.plan_wg) {
@@ -767,11 +784,13 @@ int blocks_per_cu_one() {
 template <int D>
 hipError_t launch_d(int mode, int epi, const AttnArgs &a, int grid, hipStream_t s) {
     if (mode == kModeLocal)
-        return epi == kEpiFused ? launch_one<D, kModeLocal, kEpiFused>(a, grid, s)
-                                : launch_one<D, kModeLocal, kEpiRaw>(a, grid, s);
+        return epi == kEpiFused      ? launch_one<D, kModeLocal, kEpiFused>(a, grid, s)
+               : epi == kEpiFusedTrain ? launch_one<D, kModeLocal, kEpiFusedTrain>(a, grid, s)
+                                       : launch_one<D, kModeLocal, kEpiRaw>(a, grid, s);
     if (mode == kModeGlobal)
-        return epi == kEpiFused ? launch_one<D, kModeGlobal, kEpiFused>(a, grid, s)
-                                : launch_one<D, kModeGlobal, kEpiRaw>(a, grid, s);
+        return epi == kEpiFused      ? launch_one<D, kModeGlobal, kEpiFused>(a, grid, s)
+               : epi == kEpiFusedTrain ? launch_one<D, kModeGlobal, kEpiFusedTrain>(a, grid, s)
+                                       : launch_one<D, kModeGlobal, kEpiRaw>(a, grid, s);
     return launch_one<D, kModeDense, kEpiRaw>(a, grid, s);
 }
 

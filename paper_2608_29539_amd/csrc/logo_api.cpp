@@ -165,24 +165,6 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
 // Decoding: keys per chunk (a multiple of 32, at least 256, at most 128
 // chunks per cache), query heads per work item (the largest of 4, 2, 1
 // dividing the group), and the workspace of the partial results.
-// logo_attn_fwd_train: selection scratch, the global branch's work table
-// and the thresholds when thr_out is NULL.
-struct TrainWs {
-    size_t sel_ws, glob_ws, thr, total;
-};
-TrainWs train_ws(const logo_problem *p, int32_t cap) {
-    TrainWs w;
-    size_t off = 0;
-    w.sel_ws = off;
-    off += align_up(select_ws(p).total);
-    w.glob_ws = off;
-    off += align_up(global_ws(p, cap).total);
-    w.thr = off;
-    off += align_up(sizeof(float) * (size_t)p->num_seqs);
-    w.total = off;
-    return w;
-}
-
 // logo_attn_bwd: dO^L / dO^G (bf16), the compact Q^G rows, the row sums
 // Delta, the per-row gate terms and the gain-gradient partials.
 constexpr int kFusionBwdMaxBlocks = 2048;
@@ -429,7 +411,9 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
     return hip_status(
-        launch_attention(kModeLocal, f ? kEpiFused : kEpiRaw, p->head_dim, a, (int)grid, s), s);
+        launch_attention(kModeLocal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw, p->head_dim,
+                         a, (int)grid, s),
+        s);
 }
 
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
@@ -468,7 +452,9 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     if (f)
         set_fused(a, f, gain);
     return hip_status(
-        launch_attention(kModeGlobal, f ? kEpiFused : kEpiRaw, p->head_dim, a, grid, s), s);
+        launch_attention(kModeGlobal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw, p->head_dim,
+                         a, grid, s),
+        s);
 }
 
 logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
@@ -597,7 +583,7 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_GLOBAL: return global_ws(p, cap).total;
     case LOGO_ENTRY_FWD: return fwd_ws(p, cap).total;
     case LOGO_ENTRY_DECODE: return decode_plan(p).total;
-    case LOGO_ENTRY_FWD_TRAIN: return train_ws(p, cap).total;
+    case LOGO_ENTRY_FWD_TRAIN: return fwd_ws(p, cap).total;
     case LOGO_ENTRY_BWD: return bwd_ws(p, cap).total;
     case LOGO_ENTRY_DENSE_BWD: return dense_bwd_ws(p);
     case LOGO_ENTRY_GLOBAL_BWD: return global_bwd_ws(p, cap).total;
@@ -882,7 +868,7 @@ logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const
     if (!(eps >= 0.f) || std::isinf(eps))
         return LOGO_ERR_ARG;
     const int32_t cap = sel_capacity;
-    const TrainWs w = train_ws(p, cap);
+    const FwdWs w = fwd_ws(p, cap);
     st = check_ws(ws, ws_bytes, w.total);
     if (st != LOGO_OK)
         return st;
@@ -892,21 +878,27 @@ logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const
     if (st != LOGO_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
+    // The inference path's launches (selection; local branch whose extra
+    // workgroup builds the global branch's tile plan; global branch), with
+    // epilogues that also keep the raw branch outputs and their LSEs.
+    const FusedEpi fe{tok2sel, gate, nullptr, eps, (float *)(base + w.lc), out};
+    PlanArgs plan;
+    int grid_g = 0;
+    const bool with_plan = p->total_tokens > 0 && cap > 0;
+    if (with_plan &&
+        (st = global_plan(p, sel_idx, cu_sel, cap, base + w.glob_ws, plan, grid_g)) != LOGO_OK)
+        return st;
     st = run_select(p, gate, mode, threshold, ratio, sel_idx, cap, cu_sel, tok2sel, thr,
                     base + w.sel_ws, s);
     if (st != LOGO_OK)
         return st;
-    st = run_local(p, q, k, v, o_local, nullptr, nullptr, s, nullptr, lse_local);
+    st = run_local(p, q, k, v, o_local, &fe, gain_local, s, with_plan ? &plan : nullptr,
+                   lse_local);
     if (st != LOGO_OK)
         return st;
-    st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel_idx, cu_sel, cap,
-                    o_global, nullptr, nullptr, base + w.glob_ws, s, nullptr, false, lse_global);
-    if (st != LOGO_OK)
-        return st;
-    return hip_status(launch_combine(p->total_tokens, p->num_q_heads, p->head_dim, o_local,
-                                     cap > 0 ? o_global : nullptr, gate, tok2sel, gain_local,
-                                     gain_global, eps, 1, out, s),
-                      s);
+    return run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel_idx, cu_sel, cap,
+                      o_global, &fe, gain_global, base + w.glob_ws, s, nullptr,
+                      /*plan_done=*/true, lse_global);
 }
 
 logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,

@@ -89,7 +89,10 @@ inline int split_slots(int max_tiles, int n_hg) {
 //               kernel writes bf16 Norm^L(O^L) to `out` for unselected tokens and
 //               (1-p) Norm^L(O^L) (fp32) to the compact buffer `lc` for selected
 //               ones; the global kernel then writes bf16 lc + p Norm^G(O^G).
-enum AttnEpi { kEpiRaw = 0, kEpiFused = 1 };
+//   kEpiFusedTrain : kEpiFused, and also the raw branch output O (fp32, to
+//               `out`) and the base-2 LSE of each row (to `lse`) -- the
+//               training forward, which keeps them for the backward pass.
+enum AttnEpi { kEpiRaw = 0, kEpiFused = 1, kEpiFusedTrain = 2 };
 
 // Tile plan of the global branch (device-built work table).  tmp and out each
 // hold max_tiles + split_slots entries; scratch holds 2 * stride ints with
