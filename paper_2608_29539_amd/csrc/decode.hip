@@ -271,16 +271,20 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
 
 // One wave per (sequence, query head), four per workgroup.  A branch's
 // chunks are merged in one pass: the largest chunk maximum first (lane c
-// holds chunk c), then every chunk's weight 2^(m_c - M) independently, so
-// the weighted sum over chunks has all its loads in flight.  Each lane owns
-// D/64 output elements.  The chunk count of a branch is at most 128.
+// holds chunk c), then every chunk's weight 2^(m_c - M), then the weighted
+// sum, in which the wave's lanes are 4 chunk groups x 16 element groups
+// (lane = 16 cg + eg: chunks cg, cg+4, ..., elements D/16 eg ..), so each
+// lane's dependent chain is a quarter of the chunks; two shuffle steps add
+// the chunk groups.  Lanes 0..15 then hold the row (D/16 elements each) for
+// ContextNorm, the fusion and the store.  At most 128 chunks per branch.
 constexpr int kMaxChunks = 128;
 
 template <int D>
 __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a) {
-    constexpr int PE = D / 64;
+    constexpr int EL = D / 16;                    // elements per lane
     __shared__ float s_w[4][kMaxChunks];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int cg = lane >> 4, eg = lane & 15;
     const int job = blockIdx.x * 4 + wave;
     if (job >= a.num_seqs * a.hq)
         return;                                   // whole wave: no barrier below
@@ -293,8 +297,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
     const float p = a.gate[b];
     const int kvh = h / a.group, hg = (h % a.group) / a.gh, hh = (h % a.group) % a.gh;
     float *w = s_w[wave];
-    // O / l of one branch (row = sequence or selected rank) for this lane's elements
-    auto branch = [&](const float *parts, int row, int nch, int chunks_stride, float (&o)[PE]) {
+    // O / l of one branch (row = sequence or selected rank); lane eg's elements
+    auto branch = [&](const float *parts, int row, int nch, int chunks_stride, float (&o)[EL]) {
         const int64_t item0 = (((int64_t)row * a.hkv + kvh) * a.nhg + hg) * chunks_stride;
         auto slot = [&](int c) { return parts + ((item0 + c) * a.gh + hh) * (D + 2); };
         float mc[2], lc[2];
@@ -324,51 +328,58 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
             lsum += __shfl_xor(lsum, sh, 64);
         __builtin_amdgcn_wave_barrier();
         __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-        float A[PE];
+        float A[EL];
 #pragma unroll
-        for (int i = 0; i < PE; i++)
+        for (int i = 0; i < EL; i++)
             A[i] = 0.f;
-#pragma unroll 4
-        for (int c = 0; c < nch; c++) {
+#pragma unroll 2
+        for (int c = cg; c < nch; c += 4) {
             const float wc = w[c];
-            const float *pp = slot(c) + 2 + lane * PE;
+            const float *pp = slot(c) + 2 + eg * EL;
 #pragma unroll
-            for (int i = 0; i < PE; i++)
+            for (int i = 0; i < EL; i++)
                 A[i] = fmaf(wc, pp[i], A[i]);
+        }
+#pragma unroll
+        for (int i = 0; i < EL; i++) {
+            A[i] += __shfl_xor(A[i], 16, 64);
+            A[i] += __shfl_xor(A[i], 32, 64);
         }
         __builtin_amdgcn_wave_barrier();
         const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
 #pragma unroll
-        for (int i = 0; i < PE; i++)
+        for (int i = 0; i < EL; i++)
             o[i] = A[i] * inv;
     };
-    auto norm = [&](float (&o)[PE], const float *gain) {
+    auto norm = [&](float (&o)[EL], const float *gain) {
         float ss = 0.f;
 #pragma unroll
-        for (int i = 0; i < PE; i++)
+        for (int i = 0; i < EL; i++)
             ss = fmaf(o[i], o[i], ss);
 #pragma unroll
-        for (int sh = 1; sh < 64; sh <<= 1)
+        for (int sh = 1; sh < 16; sh <<= 1)
             ss += __shfl_xor(ss, sh, 64);
         const float rn = 1.f / sqrtf(ss / (float)D + a.eps);
 #pragma unroll
-        for (int i = 0; i < PE; i++)
-            o[i] = o[i] * rn * (gain ? gain[h * D + lane * PE + i] : 1.f);
+        for (int i = 0; i < EL; i++)
+            o[i] = o[i] * rn * (gain ? gain[h * D + eg * EL + i] : 1.f);
     };
-    float ol[PE];
+    float ol[EL];
     branch(a.part_local, b, n_loc, a.chunks_local, ol);
     norm(ol, a.gain_local);
     if (r >= 0) {
-        float og[PE];
+        float og[EL];
         branch(a.part_global, r, n_glb, a.chunks_global, og);
         norm(og, a.gain_global);
 #pragma unroll
-        for (int i = 0; i < PE; i++)
+        for (int i = 0; i < EL; i++)
             ol[i] = (1.f - p) * ol[i] + p * og[i];
     }
-    uint16_t *op = a.out + ((int64_t)b * a.hq + h) * D + lane * PE;
+    if (cg != 0)
+        return;
+    uint16_t *op = a.out + ((int64_t)b * a.hq + h) * D + eg * EL;
 #pragma unroll
-    for (int i = 0; i < PE; i++)
+    for (int i = 0; i < EL; i++)
         op[i] = __builtin_bit_cast(uint16_t, (__bf16)ol[i]);
 }
 
