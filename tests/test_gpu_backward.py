@@ -111,6 +111,7 @@ BWD_CASES = [
     ((3000,), 6, 2, 64, 512, 0.5, None, False, False),
     ((1024, 77), 32, 8, 128, 256, 0.125, None, False, True),
     ((1, 2, 3, 190), 2, 2, 128, 3, None, -math.inf, False, False),
+    ((1, 0, 37, 2, 0, 65), 4, 2, 64, 16, None, 0.5, True, True),
 ]
 
 
