@@ -126,11 +126,19 @@ DECODE_WORKLOADS: Dict[str, Workload] = {
 }
 
 
-def _normal_bf16(rng: np.random.Generator, shape, scale: Optional[float]) -> np.ndarray:
-    x = rng.standard_normal(size=int(np.prod(shape)), dtype=np.float32)
-    if scale is not None:
-        x *= np.float32(scale)
-    return bf16_bits_from_f32(x).reshape(shape)
+def _normal_bf16(rng: np.random.Generator, shape, scale: Optional[float],
+                 chunk: int = 1 << 20) -> np.ndarray:
+    """N(0, scale^2) draws rounded to bf16 bits.  Drawn in cache-sized chunks:
+    the generator's state carries over between calls, so the bytes equal one
+    draw of the whole array, without its multi-GB float32 temporaries."""
+    n = int(np.prod(shape))
+    out = np.empty(n, dtype=np.uint16)
+    for s in range(0, n, chunk):
+        x = rng.standard_normal(size=min(chunk, n - s), dtype=np.float32)
+        if scale is not None:
+            x *= np.float32(scale)
+        out[s:s + x.size] = bf16_bits_from_f32(x)
+    return out.reshape(shape)
 
 
 def make_gate(rng: np.random.Generator, seqlens: Sequence[int], kind: str) -> np.ndarray:

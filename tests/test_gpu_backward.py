@@ -221,22 +221,25 @@ def test_backward_deterministic(pk):
         assert torch.equal(g1[nm], g2[nm]), nm
 
 
-def test_backward_full_size_sampled(pk):
-    """T32k-gqa (32768 tokens, 32/8 heads, d 128, w 1024, ratio 1/8, bursty
-    gate) in the launch configuration the benchmark times, checked against
-    the oracle at sampled places: dq and dgate of 48 query rows (selected and
-    unselected, sequence edges, the latest selected rows) and dk / dv of 8
-    keys near the sequence end (their gradient sums over every row that sees
-    them), plus the key-gradient sum over all 32768 keys, which softmax shift
-    invariance makes zero for each KV head."""
+@pytest.mark.parametrize("name, n_sel_rows, n_uns_rows, n_keys",
+                         [("T32k-gqa", 14, 20, 3), ("T128k-gqa", 4, 4, 0)])
+def test_backward_full_size_sampled(pk, name, n_sel_rows, n_uns_rows, n_keys):
+    """A full-size workload (T32k-gqa: 32768 tokens, 32/8 heads, d 128, w 1024,
+    ratio 1/8, bursty gate; T128k-gqa: 131072 tokens, w 4096, ratio 1/16) in
+    the launch configuration the benchmark times, checked against the oracle
+    at sampled places: dq and dgate of query rows (selected and unselected,
+    sequence edges, the latest selected rows) and dk / dv of keys near the
+    sequence end (their gradient sums over every row that sees them), plus
+    the key-gradient sum over all keys, which softmax shift invariance makes
+    zero for each KV head."""
     import torch
-    w = synth.WORKLOADS["T32k-gqa"]
+    w = synth.WORKLOADS[name]
     x = synth.make_inputs(w)
     dout = synth.make_dout(w, 1)
     dev = to_device(dict(x, dout=dout))
     prob = pk.Problem(dev["cu_seqlens"], w.num_q_heads, w.num_kv_heads, w.head_dim, w.window,
                       cu_seqlens_host=x["cu_seqlens"])
-    print("[bwd full] T32k-gqa", flush=True)
+    print(f"[bwd full] {name}", flush=True)
     saved = pk.logo_attn_fwd_train(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
                                    ratio=w.ratio)
     g = pk.logo_attn_bwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], saved, dev["dout"])
@@ -247,10 +250,10 @@ def test_backward_full_size_sampled(pk):
     uns = np.nonzero(t2s < 0)[0]
     rng = np.random.default_rng(77)
     qrows = np.unique(np.concatenate([
-        [0, 1, 1023, 1024, N - 1], sel[:3], sel[-6:], rng.choice(sel, 14, replace=False),
-        rng.choice(uns, 20, replace=False)]))
-    keys = np.unique(np.concatenate([[N - 1, N - 2, N - 64, N - 65, N - 300],
-                                     rng.integers(N - 600, N, 3)]))
+        [0, 1, w.window - 1, w.window, N - 1], sel[:3], sel[-6:],
+        rng.choice(sel, n_sel_rows, replace=False), rng.choice(uns, n_uns_rows, replace=False)]))
+    keys = np.unique(np.concatenate([[N - 1, N - 2, N - 64, N - 65, N - 300][:2 + n_keys],
+                                     rng.integers(N - 600, N, n_keys)]))
     d64 = synth.f32_from_bf16_bits(dout).reshape(dout.shape).astype(np.float64)
     ref = oracle.logo_bwd_sample(x, w.window, d64, qrows, keys, ratio=w.ratio)
     assert np.array_equal(ref["tok2sel"], t2s)
