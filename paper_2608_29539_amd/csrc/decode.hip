@@ -15,9 +15,10 @@
 //   decode_attn_kernel    split-KV attention, one workgroup per (sequence or
 //                         selected row, KV head, head group, chunk of keys):
 //                         the GH query heads of one KV head share every K/V
-//                         row read, eight lanes cover one 2d-byte row, and 32
-//                         rows are in flight per workgroup step.  Writes the
-//                         chunk's unnormalised (O, m, l) per head.
+//                         row read, sixteen lanes (one DPP row) cover one
+//                         2d-byte row, and each of the 16 streams keeps two
+//                         rows in flight.  Writes the chunk's unnormalised
+//                         (O, m, l) per head.
 //   decode_combine_kernel merges the chunks of each (sequence, head) in chunk
 //                         order, applies ContextNorm to each branch and the
 //                         fusion, and rounds once to bf16.
@@ -30,7 +31,9 @@ namespace logo {
 namespace {
 
 constexpr int kDecThreads = 256;
-constexpr int kStreams = kDecThreads / 8;   // keys in flight per workgroup step
+constexpr int kLanesPerRow = 16;            // lanes that share one cached K / V row
+constexpr int kStreams = kDecThreads / kLanesPerRow;   // keys per workgroup step
+constexpr int kPrefetch = 2;                // rows in flight per stream
 constexpr float kNegInfD = -__builtin_inff();
 constexpr float kLazyD = 8.f;               // exp2-domain headroom of the running max
 
@@ -39,6 +42,28 @@ typedef __bf16 bf16x2d __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// One lane's slice of a cached row: N 32-bit words (one 16- or 8-byte load).
+// A struct rather than a dependent-size ext_vector_type: element reads of
+// such a vector passed by value into a lambda compiled to element 0.
+template <int N>
+struct alignas(4 * N) Words {
+    uint32_t w[N];
+};
+
+// Sum over the 16 lanes of a DPP row, returned in every lane: rotations by 8
+// and 4 within the row, then the two quad swaps.
+template <int Ctrl>
+__device__ __forceinline__ float dpp_f(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), Ctrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f<0x128>(x);   // row_ror:8
+    x += dpp_f<0x124>(x);   // row_ror:4
+    x += dpp_f<0x4E>(x);    // quad_perm [2,3,0,1]
+    x += dpp_f<0xB1>(x);    // quad_perm [1,0,3,2]
+    return x;
+}
 
 __global__ __launch_bounds__(1024) void decode_select_kernel(int B, const float *gate, int mode,
                                                               float thr_host, const float *thr_dev,
@@ -96,11 +121,11 @@ __device__ __forceinline__ void merge_into(float &ma, float &la, float &mb, floa
 
 template <int D, int GH>
 __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeArgs a) {
-    constexpr int DE = D / 8;            // d values per lane
-    constexpr int DW = DE / 2;           // 32-bit words per lane (2 bf16 each)
-    constexpr int NV = DE / 8;           // 16-byte loads per lane per row
+    constexpr int DE = D / kLanesPerRow;  // d values per lane
+    constexpr int DW = DE / 2;            // 32-bit words per lane (2 bf16 each)
+    typedef Words<DW> frag_t;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int e = lane & 7, sid = wave * 8 + (lane >> 3);
+    const int e = lane % kLanesPerRow, sid = tid / kLanesPerRow;
 
     // work item -> (branch, row, kv head, head group, chunk)
     const int per_row = a.hkv * a.nhg;
@@ -156,48 +181,26 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
     const int64_t row_stride = (int64_t)a.hkv * D;    // elements between cached tokens
     const uint16_t *kbase = kc_ + (base * a.hkv + kvh) * (int64_t)D + e * DE;
     const uint16_t *vbase = vc_ + (base * a.hkv + kvh) * (int64_t)D + e * DE;
-    auto load_row = [&](const uint16_t *p, int j, u32x4d (&r)[NV]) {
-#pragma unroll
-        for (int i = 0; i < NV; i++)
-            r[i] = *(const u32x4d *)(p + (int64_t)j * row_stride + i * 8);
+    auto load_row = [&](const uint16_t *p, int j) {
+        return *(const frag_t *)(p + (int64_t)j * row_stride);
     };
-
-    // Each stream (8 lanes) walks keys k0 + sid, k0 + sid + 32, ...
-    int j = k0 + sid;
-    u32x4d kr[NV], vr[NV];
-    if (j < k1) {
-        load_row(kbase, j, kr);
-        load_row(vbase, j, vr);
-    }
-    for (; j < k1; j += kStreams) {
-        u32x4d kn[NV], vn[NV];
-        const int jn = j + kStreams;
-        if (jn < k1) {
-            load_row(kbase, jn, kn);
-            load_row(vbase, jn, vn);
-        }
-        // scores of the GH heads for key j (reduced over the 8 lanes)
+    // Online softmax update with key row (kw, vw).
+    auto consume = [&](const frag_t kw, const frag_t vw) {
         float s[GH];
 #pragma unroll
         for (int hh = 0; hh < GH; hh++) {
             float d0 = 0.f;
 #pragma unroll
-            for (int i = 0; i < DW; i++) {
-                const uint32_t kw = kr[i / 4][i % 4];
+            for (int i = 0; i < DW; i++)
                 d0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2d, q2[hh][i]),
-                                                    __builtin_bit_cast(bf16x2d, kw), d0, false);
-            }
-            d0 += __shfl_xor(d0, 1, 64);
-            d0 += __shfl_xor(d0, 2, 64);
-            d0 += __shfl_xor(d0, 4, 64);
-            s[hh] = d0 * a.scale_log2;
+                                                    __builtin_bit_cast(bf16x2d, kw.w[i]), d0, false);
+            s[hh] = row16_sum(d0) * a.scale_log2;
         }
         float vf[DE];
 #pragma unroll
         for (int i = 0; i < DW; i++) {
-            const uint32_t vw = vr[i / 4][i % 4];
-            vf[2 * i] = bf16_lo(vw);
-            vf[2 * i + 1] = bf16_hi(vw);
+            vf[2 * i] = bf16_lo(vw.w[i]);
+            vf[2 * i + 1] = bf16_hi(vw.w[i]);
         }
 #pragma unroll
         for (int hh = 0; hh < GH; hh++) {
@@ -216,18 +219,42 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
             for (int i = 0; i < DE; i++)
                 acc[hh][i] = fmaf(p, vf[i], acc[hh][i]);
         }
+    };
+
+    // Each stream (16 lanes) walks keys k0 + sid, k0 + sid + kStreams, ...,
+    // with kPrefetch rows in flight in a ring of registers (the ring index is
+    // a compile-time constant: the loop body covers kPrefetch keys).
+    int j = k0 + sid;
+    frag_t kr[kPrefetch], vr[kPrefetch];
 #pragma unroll
-        for (int i = 0; i < NV; i++) {
-            kr[i] = kn[i];
-            vr[i] = vn[i];
+    for (int p = 0; p < kPrefetch; p++) {
+        const int jp = j + p * kStreams;
+        if (jp < k1) {
+            kr[p] = load_row(kbase, jp);
+            vr[p] = load_row(vbase, jp);
+        }
+    }
+    for (; j < k1; j += kPrefetch * kStreams) {
+#pragma unroll
+        for (int p = 0; p < kPrefetch; p++) {
+            const int jc = j + p * kStreams;
+            if (jc < k1) {
+                const frag_t kw = kr[p], vw = vr[p];
+                const int jn = jc + kPrefetch * kStreams;
+                if (jn < k1) {
+                    kr[p] = load_row(kbase, jn);
+                    vr[p] = load_row(vbase, jn);
+                }
+                consume(kw, vw);
+            }
         }
     }
 
-    // Merge the 8 streams of the wave (lanes with the same e), then the waves.
+    // Merge the streams of the wave (lanes with the same e), then the waves.
 #pragma unroll
     for (int hh = 0; hh < GH; hh++) {
 #pragma unroll
-        for (int sh = 8; sh < 64; sh <<= 1) {
+        for (int sh = kLanesPerRow; sh < 64; sh <<= 1) {
             float mo = __shfl_xor(m[hh], sh, 64), lo_ = __shfl_xor(l[hh], sh, 64);
             float ao[DE];
 #pragma unroll
@@ -238,7 +265,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
     }
     __shared__ float s_m[4][GH], s_l[4][GH];
     __shared__ float s_acc[4][GH][D];
-    if (lane < 8) {
+    if (lane < kLanesPerRow) {
 #pragma unroll
         for (int hh = 0; hh < GH; hh++) {
             if (lane == 0) {

@@ -251,9 +251,13 @@ struct DecodePlan {
 DecodePlan decode_plan(const logo_problem *p) {
     DecodePlan d;
     const long long maxL = p->max_seqlen > 0 ? p->max_seqlen : 1;
+    // Keys per chunk: at least 512 (a workgroup's fixed cost -- query loads,
+    // stream and wave merges, the partial's store -- is then small next to
+    // its 256 KiB of K / V per KV head at d = 128), at most 128 chunks per
+    // cache, a multiple of 32.
     long long kc = (maxL + 127) / 128;
     kc = ((kc + 31) / 32) * 32;
-    d.kc = (int)(kc < 256 ? 256 : kc);
+    d.kc = (int)(kc < 512 ? 512 : kc);
     const int g = p->num_q_heads / p->num_kv_heads;
     d.gh = g % 4 == 0 ? 4 : (g % 2 == 0 ? 2 : 1);
     d.nhg = g / d.gh;
