@@ -586,12 +586,23 @@ void bwd_dkv_kernel(const BwdArgs a) {
 // workgroup handles slots (t + 256 k) % S of token t0 + (t + 256 k) / S for
 // k < KS, so with S <= 256 a pass covers 256 / S tokens and with S > 256 a
 // token takes KS = S / 256 slot sets.  A (token, head) row is d / 8
-// consecutive lanes; its sums are lane shuffles within them.
+// consecutive lanes; its sums are DPP lane exchanges within them.
+template <int Ctrl>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), Ctrl, 0xF, 0xF, false));
+}
 template <int D>
 __device__ __forceinline__ float row_sum(float x) {
-#pragma unroll
-    for (int sh = 1; sh < D / 8; sh <<= 1)
-        x += __shfl_xor(x, sh, 64);
+    // DPP within each group of D / 8 lanes (16 or 8, aligned): the two quad
+    // swaps, then the half-row mirror (lane i <- 7 - i of its 8) and, for 16
+    // lanes, the row mirror (i <- 15 - i), each pairing the partial sums of
+    // disjoint lane sets.
+    static_assert(D / 8 == 16 || D / 8 == 8, "row of 8 or 16 lanes");
+    x += dpp_mov<0xB1>(x);        // quad_perm [1,0,3,2]
+    x += dpp_mov<0x4E>(x);        // quad_perm [2,3,0,1]
+    x += dpp_mov<0x141>(x);       // row_half_mirror
+    if constexpr (D / 8 == 16)
+        x += dpp_mov<0x140>(x);   // row_mirror
     return x;
 }
 
