@@ -70,6 +70,10 @@ DECODE_CASES = [
     ((700, 1, 40000), 8, 8, 128, 512, 0.4, True, False),
     ((1000, 2000, 255, 256, 257), 8, 2, 128, 128, -math.inf, False, False),
     ((1000, 2000), 8, 2, 128, 128, math.inf, False, False),
+    # group sizes 2 and 4 at d 64 and group size 2 at d 128 (GH = 2, 4, 2)
+    ((333, 1500, 70), 8, 4, 64, 200, 0.4, False, True),
+    ((2049, 5), 4, 1, 64, 1024, 0.1, True, False),
+    ((800, 4000), 4, 2, 128, 300, 0.05, False, False),
 ]
 
 
