@@ -21,6 +21,9 @@
  *     iff j <= i (global) or i-w < j <= i (local: exactly min(i+1, w) keys,
  *     the query included; the paper's 1-based context {max(1,t-w+1)..t}).
  *   - GQA: query head h reads key/value head h / (Hq/Hkv).
+ *   - A per-token array ([N] or [N][...]) may be NULL when N = 0 (every
+ *     sequence empty); per-sequence arrays ([B+1], [B]) are still required
+ *     and are written (cu_sel all zeros).
  *   - The caller owns every buffer.  The library never allocates or frees
  *     device memory, keeps no pointer after a call returns, and never
  *     synchronises: every call only enqueues work on `stream` (NULL = the

@@ -306,7 +306,7 @@ int64_t ratio_capacity(const logo_problem *p, double ratio) {
 logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel_mode mode,
                               float threshold, double ratio, const int32_t *sel_idx,
                               int32_t cap, const int32_t *cu_sel, const float *thr_out) {
-    if (!gate || !cu_sel)
+    if ((!gate && p->total_tokens > 0) || !cu_sel)
         return LOGO_ERR_NULL;
     if (cap < 0)
         return LOGO_ERR_SHAPE;
@@ -472,8 +472,6 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     if (st != LOGO_OK)
         return st;
     if (p->total_tokens > 0 && (!q || !k || !v || !gate || !out))
-        return LOGO_ERR_NULL;
-    if (!gate)
         return LOGO_ERR_NULL;
     if (sel_capacity < 0)
         return LOGO_ERR_SHAPE;
@@ -860,7 +858,7 @@ logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const
     logo_status st = check_problem(p);
     if (st != LOGO_OK)
         return st;
-    if (!gate || !cu_sel)
+    if ((!gate && p->total_tokens > 0) || !cu_sel)
         return LOGO_ERR_NULL;
     if (p->total_tokens > 0 &&
         (!q || !k || !v || !out || !tok2sel || !o_local || !lse_local))

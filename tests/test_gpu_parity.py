@@ -330,6 +330,31 @@ def test_layer_distinct_global_tensors(pk):
     _layer(pk, w, x=x, full=True)
 
 
+def test_layer_all_sequences_empty(pk):
+    """A batch whose every sequence is empty (N = 0): the layer and its
+    training forward / backward return OK, cu_sel is all zeros, ratio mode's
+    threshold is -inf (k = T = 0) and threshold mode's is the given value."""
+    import torch
+    cu_host = np.zeros(4, np.int32)
+    prob = pk.Problem(torch.zeros(4, dtype=torch.int32, device="cuda"), 8, 2, 64, 16,
+                      cu_seqlens_host=cu_host)
+    e = lambda h: torch.empty(0, h, 64, dtype=torch.bfloat16, device="cuda")
+    q, k, v = e(8), e(2), e(2)
+    gate = torch.empty(0, dtype=torch.float32, device="cuda")
+    for kw, thr_ref in ((dict(ratio=0.5), -math.inf), (dict(threshold=0.2), np.float32(0.2))):
+        out, sel_idx, cu_sel, tok2sel, thr = pk.logo_attn_fwd(prob, q, k, v, gate, **kw)
+        torch.cuda.synchronize()
+        assert out.shape == (0, 8, 64)
+        assert cu_sel.cpu().tolist() == [0, 0, 0, 0], kw
+        assert thr.cpu().tolist() == [thr_ref] * 3, kw
+    saved = pk.logo_attn_fwd_train(prob, q, k, v, gate, ratio=0.5)
+    g = pk.logo_attn_bwd(prob, q, k, v, gate, saved, e(8))
+    torch.cuda.synchronize()
+    assert saved["cu_sel"].cpu().tolist() == [0, 0, 0, 0]
+    assert g["dq"].shape == (0, 8, 64) and g["dk"].shape == (0, 2, 64)
+    assert g["dgate"].shape == (0,)
+
+
 def test_single_selected_at_position_zero(pk):
     import torch
     w = synth.small_workload((300,), 4, 2, 128, 32, 0.0, seed=1700)
