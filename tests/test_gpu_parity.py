@@ -353,6 +353,15 @@ def test_layer_all_sequences_empty(pk):
     assert saved["cu_sel"].cpu().tolist() == [0, 0, 0, 0]
     assert g["dq"].shape == (0, 8, 64) and g["dk"].shape == (0, 2, 64)
     assert g["dgate"].shape == (0,)
+    # the standalone steps and the dense baseline
+    sel_idx, cu_sel, tok2sel, thr = pk.logo_select(prob, gate, ratio=0.25)
+    o_l = pk.logo_local_attn(prob, q, k, v)
+    o_g = pk.logo_global_attn_sparse_q(prob, q, k, v, sel_idx, cu_sel, 0)
+    o = pk.logo_combine(prob, o_l, o_g, gate, tok2sel)
+    dense = pk.logo_dense_causal_attn(prob, q, k, v)
+    torch.cuda.synchronize()
+    assert cu_sel.cpu().tolist() == [0, 0, 0, 0]
+    assert o_l.shape == (0, 8, 64) and o.shape == (0, 8, 64) and dense.shape == (0, 8, 64)
 
 
 def test_single_selected_at_position_zero(pk):
