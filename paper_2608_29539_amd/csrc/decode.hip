@@ -5,20 +5,21 @@
 // gate passes the threshold it also attends to the whole cache (global
 // branch), and the two outputs are ContextNorm-ed and fused as in the layer.
 //
-// Rows are compacted as in the prefill: decode_select_kernel lists the
-// sequences whose token is selected, and only those get global work items,
-// so an unselected token costs one window of the cache (the paper's batched
-// decoding instead launches the dense kernel for every row and masks).
+// Only selected tokens do global work: every global work item tests its
+// sequence's routing decision z_b = gate[b] > thr (fp32, strict) and an
+// unselected one exits at once, so an unselected token costs one window of
+// the cache (the paper's batched decoding instead launches the dense kernel
+// for every row and masks).
 //
-//   decode_select_kernel  z_b = gate[b] > thr (fp32, strict); compacted list
-//                         of selected sequences, each sequence's rank, count.
-//   decode_attn_kernel    split-KV attention, one workgroup per (sequence or
-//                         selected row, KV head, head group, chunk of keys):
+//   decode_attn_kernel    split-KV attention, one workgroup per (branch,
+//                         sequence, KV head, head group, chunk of keys):
 //                         the GH query heads of one KV head share every K/V
 //                         row read, sixteen lanes (one DPP row) cover one
 //                         2d-byte row, and each of the 16 streams keeps two
 //                         rows in flight.  Writes the chunk's unnormalised
-//                         (O, m, l) per head.
+//                         (O, m, l) per head.  One extra workgroup writes
+//                         the compacted list of selected sequences, each
+//                         sequence's rank and the count.
 //   decode_combine_kernel merges the chunks of each (sequence, head) in chunk
 //                         order, applies ContextNorm to each branch and the
 //                         fusion, and rounds once to bf16.
@@ -65,46 +66,47 @@ __device__ __forceinline__ float row16_sum(float x) {
     return x;
 }
 
-__global__ __launch_bounds__(1024) void decode_select_kernel(int B, const float *gate, int mode,
-                                                              float thr_host, const float *thr_dev,
-                                                              int32_t *act, int32_t *rank_of,
-                                                              int32_t *n_act) {
-    __shared__ int s_wave[16];
-    __shared__ int s_carry;
+// The token's routing decision z_b = gate[b] > thr (fp32, strict: a NaN
+// gate or threshold selects nothing), taken identically by every workgroup
+// that needs it.
+__device__ __forceinline__ float decode_threshold(const DecodeArgs &a) {
+    return a.sel_mode == 2 ? a.thr_dev[0] : a.thr_host;
+}
+
+// The compacted list of selected sequences (ascending), each sequence's rank
+// (-1 if unselected) and the count: one workgroup, ballot + mbcnt ranks and
+// a carry over chunks of kDecThreads sequences.
+__device__ void build_active_list(const DecodeArgs &a) {
+    __shared__ int s_cnt[kDecThreads / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const float thr = mode == 2 ? thr_dev[0] : thr_host;
-    if (tid == 0)
-        s_carry = 0;
-    __syncthreads();
-    for (int c0 = 0; c0 < B; c0 += 1024) {
+    const float thr = decode_threshold(a);
+    int carry = 0;
+    for (int c0 = 0; c0 < a.num_seqs; c0 += kDecThreads) {
         const int b = c0 + tid;
-        const bool z = b < B && gate[b] > thr;      // NaN gate or threshold: false
+        const bool z = b < a.num_seqs && a.gate[b] > thr;
         const uint64_t m = __ballot(z);
         const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
         if (lane == 0)
-            s_wave[wave] = (int)__popcll(m);
+            s_cnt[wave] = (int)__popcll(m);
         __syncthreads();
-        int before = s_carry;
-        for (int i = 0; i < wave; i++)
-            before += s_wave[i];
-        if (b < B) {
+        int before = carry, total = 0;
+        for (int i = 0; i < kDecThreads / 64; i++) {
+            if (i < wave)
+                before += s_cnt[i];
+            total += s_cnt[i];
+        }
+        if (b < a.num_seqs) {
             const int r = before + below;
-            rank_of[b] = z ? r : -1;
+            a.rank_of[b] = z ? r : -1;
             if (z)
-                act[r] = b;
+                a.act[r] = b;
         }
-        __syncthreads();
-        if (tid == 0) {
-            int t = 0;
-            for (int i = 0; i < 16; i++)
-                t += s_wave[i];
-            s_carry += t;
-        }
-        __syncthreads();
+        carry += total;
+        __syncthreads();                         // s_cnt is rewritten by the next chunk
     }
     if (tid == 0)
-        n_act[0] = s_carry;
+        a.n_act[0] = carry;
 }
 
 // (m, l, acc) of stream b merged into stream a (exp2 domain).
@@ -127,9 +129,14 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int e = lane % kLanesPerRow, sid = tid / kLanesPerRow;
 
-    // work item -> (branch, row, kv head, head group, chunk)
+    // work item -> (branch, sequence, kv head, head group, chunk); the last
+    // workgroup builds the list of selected sequences instead
     const int per_row = a.hkv * a.nhg;
     int item = blockIdx.x;
+    if (item == a.n_local_items + a.n_global_items) {
+        build_active_list(a);
+        return;
+    }
     const bool global = item >= a.n_local_items;
     if (global)
         item -= a.n_local_items;
@@ -138,13 +145,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_attn_kernel(const DecodeAr
     const int rest = item / nch;
     const int hgi = rest % a.nhg;
     const int kvh = (rest / a.nhg) % a.hkv;
-    const int row = rest / per_row;              // sequence (local) or rank (global)
-    int b = row;
-    if (global) {
-        if (row >= a.n_act[0])
-            return;
-        b = a.act[row];
-    }
+    const int b = rest / per_row;                // sequence
+    if (global && !(a.gate[b] > decode_threshold(a)))
+        return;                                  // an unselected token: window only
     const int64_t base = a.cu[b];
     const int L = a.cu[b + 1] - (int)base;
     const int lo = global ? 0 : max(0, L - a.window);
@@ -324,7 +327,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
     const float p = a.gate[b];
     const int kvh = h / a.group, hg = (h % a.group) / a.gh, hh = (h % a.group) % a.gh;
     float *w = s_w[wave];
-    // O / l of one branch (row = sequence or selected rank); lane eg's elements
+    // O / l of one branch of sequence `row`; lane eg's elements
     auto branch = [&](const float *parts, int row, int nch, int chunks_stride, float (&o)[EL]) {
         const int64_t item0 = (((int64_t)row * a.hkv + kvh) * a.nhg + hg) * chunks_stride;
         auto slot = [&](int c) { return parts + ((item0 + c) * a.gh + hh) * (D + 2); };
@@ -396,7 +399,7 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
     norm(ol, a.gain_local);
     if (r >= 0) {
         float og[EL];
-        branch(a.part_global, r, n_glb, a.chunks_global, og);
+        branch(a.part_global, b, n_glb, a.chunks_global, og);
         norm(og, a.gain_global);
 #pragma unroll
         for (int i = 0; i < EL; i++)
@@ -412,9 +415,8 @@ __global__ __launch_bounds__(256) void decode_combine_kernel(const DecodeArgs a)
 
 template <int D, int GH>
 hipError_t launch_attn_gh(const DecodeArgs &a, hipStream_t s) {
-    const int grid = a.n_local_items + a.n_global_items;
-    if (grid > 0)
-        hipLaunchKernelGGL((decode_attn_kernel<D, GH>), dim3(grid), dim3(kDecThreads), 0, s, a);
+    const int grid = a.n_local_items + a.n_global_items + 1;   // + the list builder
+    hipLaunchKernelGGL((decode_attn_kernel<D, GH>), dim3(grid), dim3(kDecThreads), 0, s, a);
     return hipGetLastError();
 }
 
@@ -429,14 +431,8 @@ hipError_t launch_attn_d(const DecodeArgs &a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const float *thr_dev,
-                         hipStream_t s) {
-    hipLaunchKernelGGL(decode_select_kernel, dim3(1), dim3(1024), 0, s, a.num_seqs, a.gate, mode,
-                       thr_host, thr_dev, a.act, a.rank_of, a.n_act);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess)
-        return e;
-    e = a.head_dim == 128 ? launch_attn_d<128>(a, s) : launch_attn_d<64>(a, s);
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t s) {
+    hipError_t e = a.head_dim == 128 ? launch_attn_d<128>(a, s) : launch_attn_d<64>(a, s);
     if (e != hipSuccess)
         return e;
     const int grid = (a.num_seqs * a.hq + 3) / 4;

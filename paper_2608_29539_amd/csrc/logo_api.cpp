@@ -796,8 +796,11 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
     a.part_local = (float *)(base + d.part_local);
     a.part_global = (float *)(base + d.part_global);
     a.out = out;
+    a.sel_mode = (int32_t)mode;
+    a.thr_host = threshold;
+    a.thr_dev = thr_dev;
     hipStream_t s = (hipStream_t)stream;
-    return hip_status(launch_decode(a, (int)mode, threshold, thr_dev, s), s);
+    return hip_status(launch_decode(a, s), s);
 }
 
 logo_status logo_gate_proj(int64_t n_tokens, int32_t d_model, const logo_bf16 *x,

@@ -170,11 +170,13 @@ struct DecodeArgs {
     int32_t chunks_local, chunks_global;
     int32_t n_local_items, n_global_items;
     int32_t *act, *rank_of, *n_act;  // selected sequences (compacted), rank or -1, count
+    int32_t sel_mode;                // 0: threshold thr_host, 2: device threshold thr_dev[0]
+    float thr_host;
+    const float *thr_dev;
     float *part_local, *part_global;
     uint16_t *out;                   // [B][Hq][d] bf16
 };
-hipError_t launch_decode(const DecodeArgs &a, int mode, float thr_host, const float *thr_dev,
-                         hipStream_t s);
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t s);
 
 // Gate projection and branch transforms (transform.hip).  kind 0 = LP
 // (A [H][d][d] bf16), 1 = SO (s, b [H][d] fp32); rows = token list or NULL,
