@@ -213,11 +213,15 @@ def bench_decode(pk, torch, name: str, steps: int, warmup: int):
             "speedup_vs_conservative": round(t_all / t_logo, 3)}
 
 
-def bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, steps: int = 20):
+def bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, prob=None, tok2sel=None,
+                     steps: int = 20):
     """The steps on either side of the attention at the workload's shape: the
     gate projection p = sigmoid(x . w_g) with d_model = Hq d, and the LP / SO
-    branch transforms of K and V (every token) and of Q (selected rows only).
-    HBM-bound: algorithmic bytes = inputs read once + outputs written once."""
+    branch transforms of K and V (every token) and of Q (selected rows only),
+    and the standalone ContextNorm + fusion (`logo_combine`; the layer fuses
+    it into the attention epilogues) on fp32 branch outputs with the layer's
+    selection.  HBM-bound: algorithmic bytes = inputs read once + outputs
+    written once."""
     N, Hq, Hkv, d = w.total_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
     dm = Hq * d
     g = torch.Generator(device="cuda").manual_seed(7)
@@ -255,6 +259,14 @@ def bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, steps: int = 20):
                                                n_rows=cap, n_rows_dev=cu_sel[-1:], out=qg))
     rows["lp_q_selected"] = (t, 2 * n_sel * Hq * d * 2 + Hq * d * d * 2 + n_sel * 4,
                              2.0 * n_sel * Hq * d * d)
+    if prob is not None and tok2sel is not None:
+        ol = torch.randn((N, Hq, d), generator=g, device="cuda")
+        og = torch.randn((max(cap, 1), Hq, d), generator=g, device="cuda")
+        oc = torch.empty((N, Hq, d), dtype=torch.bfloat16, device="cuda")
+        t = timed(lambda: pk.logo_combine(prob, ol, og, dev["gate"], tok2sel, out=oc))
+        # O^L fp32 + bf16 out per token, O^G fp32 per selected row, gate + tok2sel
+        rows["combine"] = (t, N * Hq * d * (4 + 2) + n_sel * Hq * d * 4 + N * 8,
+                           10.0 * (N + n_sel) * Hq * d)
     out = {}
     for k_, (ms, nbytes, flops) in rows.items():
         gbs = nbytes / (ms * 1e-3) / 1e9
@@ -619,7 +631,8 @@ def main(argv=None):
 
     transforms = None
     if not args.no_transforms:
-        transforms = bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap)
+        transforms = bench_transforms(pk, torch, w, dev, sel_idx, cu_sel, cap, prob=prob,
+                                      tok2sel=tok2sel)
 
     train = None
     if not args.no_train:
