@@ -91,8 +91,9 @@ __global__ __launch_bounds__(256) void so_transform_kernel(int64_t n_rows, int H
 
 // LP: workgroup = (head h, block of kLpRows rows); 4 waves, each 32 rows at
 // a time with the next 32 rows' operands prefetched.  LDS holds A_h^T
-// [d][d + 8] (bf16, rows padded by 16 bytes), filled with coalesced reads of
-// eight rows of A_h per thread and one 16-byte write.
+// [d][d + 8] (bf16, rows padded by 16 bytes), filled by 8 x 8 blocks: eight
+// coalesced 16-byte row reads per thread, a transpose in registers, eight
+// 16-byte writes.
 constexpr int kLpRows = 512;
 
 template <int D>
@@ -109,16 +110,30 @@ __global__ __launch_bounds__(256) void lp_transform_kernel(int64_t n_rows, int H
         return;                                     // whole workgroup
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int m = lane & 31, g = lane >> 5;
-    // stage A_h transposed: task (c-block of 8, column j) reads A_h[c0..c0+7][j]
-    // (lanes take consecutive j: coalesced) and writes at[j][c0..c0+7]
+    // stage A_h transposed: a thread takes one 8 x 8 block (rows c0..c0+7,
+    // columns j0..j0+7) of A_h with eight 16-byte row reads (lanes take
+    // consecutive column blocks: coalesced), transposes it in registers and
+    // writes at[j0 + e][c0..c0+7] with one 16-byte store per column e
     const uint16_t *Ah = A + (int64_t)h * D * D;
-    for (int idx = tid; idx < D * D / 8; idx += 256) {
-        const int j = idx % D, c0 = (idx / D) * 8;
-        uint32_t w4[4];
+    constexpr int NB = D / 8;                       // 8 x 8 blocks per row
+    for (int idx = tid; idx < NB * NB; idx += 256) {
+        const int j0 = (idx % NB) * 8, c0 = (idx / NB) * 8;
+        u32x4t r[8];
 #pragma unroll
-        for (int i = 0; i < 4; i++)
-            w4[i] = (uint32_t)Ah[(c0 + 2 * i) * D + j] | ((uint32_t)Ah[(c0 + 2 * i + 1) * D + j] << 16);
-        *(u32x4t *)&at[j][c0] = u32x4t{w4[0], w4[1], w4[2], w4[3]};
+        for (int i = 0; i < 8; i++)
+            r[i] = *(const u32x4t *)(Ah + (int64_t)(c0 + i) * D + j0);
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            // element e of rows 2 i2 and 2 i2 + 1 -> the low / high half of word i2
+            uint32_t w[4];
+#pragma unroll
+            for (int i2 = 0; i2 < 4; i2++) {
+                const uint32_t a0 = r[2 * i2][e >> 1], a1 = r[2 * i2 + 1][e >> 1];
+                w[i2] = (e & 1) ? ((a0 >> 16) | (a1 & 0xFFFF0000u))
+                                : ((a0 & 0xFFFFu) | (a1 << 16));
+            }
+            *(u32x4t *)&at[j0 + e][c0] = u32x4t{w[0], w[1], w[2], w[3]};
+        }
     }
     __syncthreads();
     const int64_t r_end = min(r0 + kLpRows, nr);
