@@ -753,11 +753,27 @@ void attn_kernel(const AttnArgs a) {
             }
         }
         const int hg = bid % a.n_hg;
-        const int rest = bid / a.n_hg;
-        const int b = rest % a.num_seqs;
-        int jt = rest / a.num_seqs;
-        if (MODE == kModeDense)
-            jt = a.ntile_max - 1 - jt;       // longest rows first
+        int rest = bid / a.n_hg;
+        int b, jt;
+        if (MODE == kModeLocal) {
+            // the sequences' tiles back to back (a jt-major grid over the
+            // longest sequence left most workgroups of a ragged batch idle)
+            b = 0;
+            for (; b < a.num_seqs; b++) {
+                const int nt = (a.cu_seqlens[b + 1] - a.cu_seqlens[b] + a.tpw - 1) / a.tpw;
+                if (rest < nt)
+                    break;
+                rest -= nt;
+            }
+            if (b >= a.num_seqs)
+                return;
+            jt = rest;
+        } else {
+            b = rest % a.num_seqs;
+            jt = rest / a.num_seqs;
+            if (MODE == kModeDense)
+                jt = a.ntile_max - 1 - jt;       // longest rows first
+        }
         const int T = a.cu_seqlens[b + 1] - a.cu_seqlens[b];
         if (jt * a.tpw >= T)
             return;

@@ -411,7 +411,9 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
         a.plan_wg = 1;
         a.plan = *plan;
     }
-    const long long grid = (long long)tp.n_hg * p->num_seqs * a.ntile_max + a.plan_wg;
+    // the sequences' tiles back to back: sum_b ceil(T_b / tpw) <= ceil(N / tpw) + B - 1
+    const long long grid =
+        (long long)tp.n_hg * ((p->total_tokens + tp.tpw - 1) / tp.tpw + p->num_seqs) + a.plan_wg;
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
     return hip_status(
