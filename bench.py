@@ -5,13 +5,17 @@ A step is one ``logo_attn_fwd`` call (selection, local branch, query-sparse
 global branch, ContextNorm + fusion) over one batch of synthetic inputs that
 are already resident in HBM.  The default workload is "T32k-gqa" (B=1,
 T=32768, 32 query heads / 8 KV heads, d=128, window 1024, ratio 1/8, bursty
-gate).
+gate).  Untimed layer steps run for --settle-ms (the shader clock ramps up
+under load) before the W warm-up steps, then exactly K steps are timed.
 
 Reported (one JSON line on stdout):
   value          effective TFLOP/s = 4 d Hq (P_local + P_global) / t_step,
                  P_local = sum_i min(pos_i+1, w), P_global = sum_{i selected} (pos_i+1)
                  (causally valid (query, key) pairs only, realized selection)
-  speedup_vs_dense   t_dense / t_step, t_dense = best in-repo dense causal kernel
+  speedup_vs_dense   t_dense / t_layer, t_dense = best in-repo dense causal
+                 kernel; both from --rounds rounds that alternate a block of
+                 K layer steps with blocks of dense steps (medians), so the
+                 two are timed under the same clock state
   roofline       the query-sparse global kernel (the dominant one) against the
                  dense bf16 MFMA peak, its duration taken from HIP events that
                  the profiled entry point records on the layer's stream, in a
@@ -57,6 +61,7 @@ def pair_counts(cu: np.ndarray, window: int, sel_idx: np.ndarray):
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_global_T32k-gqa_traffic.md")
+TRACE_FILE = os.path.join(ROOT, "profiles", "logo_layer_T32k-gqa_kernel_stats.md")
 # Sources whose change invalidates the committed counter figures: the global
 # kernel, its tiling constants and the tile plan that orders its work.
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_29539_amd", "csrc", f)
@@ -72,46 +77,63 @@ def kernel_source_hash() -> str:
     return h.hexdigest()
 
 
-def committed_traffic(workload: str):
-    """HBM bytes per launch of the global kernel from the committed counter
-    summary, or None when the summary is missing, is for another workload, or
-    was taken on a different kernel source than the one built now."""
-    if not os.path.exists(TRAFFIC_FILE):
+def committed_fields(path: str, workload: str):
+    """The machine-readable "- key: `value`" lines of a committed profile
+    summary, or None when the file is missing, is for another workload, or was
+    taken on a different kernel source than the one built now."""
+    if not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if ":" in line and line.startswith("- "):
             k, v = line[2:].split(":", 1)
             fields[k.strip()] = v.strip().strip("`")
-    src_hash = kernel_source_hash()
-    if fields.get("workload") != workload or fields.get("kernel_source_sha256") != src_hash:
+    if fields.get("workload") != workload or fields.get("kernel_source_sha256") != kernel_source_hash():
         return None
+    return fields
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per launch of the global kernel (two counter passes)."""
+    f = committed_fields(TRAFFIC_FILE, workload)
     try:
-        return float(fields["traffic_bytes_per_launch"])
+        return float(f["traffic_bytes_per_launch"]) if f else None
     except (KeyError, ValueError):
         return None
 
 
-def gpu_info(torch, busy=None):
-    """Device name and the clock the peaks assume; the shader clock rocm-smi
-    reports while `busy` (a callable that enqueues about a second of layer
-    steps) keeps the GPU loaded, when the tool is available (best effort)."""
-    import subprocess
+def committed_trace_avg_us(workload: str):
+    """Average duration of the global kernel over the K timed calls of the
+    committed kernel-trace run (same sources), or None."""
+    f = committed_fields(TRACE_FILE, workload)
+    try:
+        return float(f["global_kernel_avg_us_timed"]) if f else None
+    except (KeyError, ValueError):
+        return None
+
+
+def current_sclk_mhz():
+    """The shader clock the driver reports right now (the level marked '*' in
+    sysfs pp_dpm_sclk), read in-process; None when no such file is readable."""
+    import glob
+    for f in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            for line in open(f):
+                if line.rstrip().endswith("*"):
+                    return int(line.split(":", 1)[1].strip().split("M")[0])
+        except (OSError, ValueError, IndexError):
+            continue
+    return None
+
+
+def gpu_info(torch, sclk_samples):
+    """Device name, the clock the peaks assume and the shader clock sampled
+    around the timed regions (no child process is started)."""
     props = torch.cuda.get_device_properties(0)
     info = {"name": props.name, "arch": getattr(props, "gcnArchName", None),
             "compute_units": props.multi_processor_count, "peak_sclk_mhz_assumed": 2400}
-    if busy is not None:
-        busy()
-    try:
-        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
-                           timeout=20)
-        for line in r.stdout.splitlines():
-            if "sclk" in line:
-                info["sclk_reported"] = line.split(":", 1)[-1].strip()
-                break
-    except Exception:                       # the tool is optional
-        pass
-    torch.cuda.synchronize()
+    vals = [v for v in sclk_samples if v is not None]
+    info["sclk_mhz_sampled"] = vals if vals else None
     return info
 
 
@@ -427,9 +449,12 @@ def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    # The shader clock ramps up over the first ~100 ms of load; 50 untimed
-    # steps (~90 ms) reach the steady clock the dense baseline also runs at.
-    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-ms", type=float, default=400.0,
+                    help="untimed layer steps for this long before the warm-up steps, so the "
+                         "shader clock has ramped up before any timed region")
+    ap.add_argument("--rounds", type=int, default=3,
+                    help="alternating layer / dense timing rounds for the speedup")
     ap.add_argument("--workload", default="T32k-gqa")
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-stride", type=int, default=0,
@@ -497,7 +522,7 @@ def main(argv=None):
         log(f"copy calibration: {nbytes} bytes copied")
         del src, dst
 
-    n_ev = args.steps + args.warmup
+    n_ev = args.steps
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(n_ev)]
     for row in evs:
         for e in row:
@@ -512,11 +537,34 @@ def main(argv=None):
                          tok2sel=tok2sel, thr_out=thr, ws=ws,
                          events=None if i is None else evs[i])
 
-    for i in range(args.warmup):
-        step(i)
+    def timed_block(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    sclk = []
+    # Clock settling: the shader clock ramps up over the first ~100 ms of
+    # load, so layer steps run untimed for --settle-ms before the W warm-up
+    # steps; every timed region below then starts at the steady clock.
+    t_settle = time.perf_counter()
+    n_settle = 0
+    while (time.perf_counter() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
+        n_settle += 10
+    for _ in range(args.warmup):
+        step()
     torch.cuda.synchronize()
+    sclk.append(current_sclk_mhz())
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    # Timed region 1: the layer as a caller runs it (no events inside a step).
+    # Timed region 1 (the headline): exactly K steps of the layer as a caller
+    # runs it (no events inside a step).
     t_wall = time.perf_counter()
     start.record()
     for _ in range(args.steps):
@@ -525,21 +573,22 @@ def main(argv=None):
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     ms_step = start.elapsed_time(end) / args.steps
+    sclk.append(current_sclk_mhz())
     # Timed region 2: the same steps through the profiled entry point, which
     # records HIP events on the layer's stream at the stage boundaries
     # (select | local + tile plan | - | global); the roofline's kernel
-    # duration comes from here.
+    # duration is the global stage's mean over these K steps.
     start.record()
-    for i in range(args.warmup, n_ev):
+    for i in range(n_ev):
         step(i)
     end.record()
     torch.cuda.synchronize()
     ms_step_profiled = start.elapsed_time(end) / args.steps
     stage_names = ("select", "local", "plan", "global")
-    stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1])
-                                  for i in range(args.warmup, n_ev)]))
+    stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(n_ev)]))
                 for j, n in enumerate(stage_names)}
-    log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}); with stage "
+    log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}, after "
+        f"{n_settle} settling + {args.warmup} warm-up steps); with stage "
         f"events {ms_step_profiled:.3f} ms/step; stages "
         + " ".join(f"{k}={v:.3f}" for k, v in stage_ms.items()))
 
@@ -551,39 +600,55 @@ def main(argv=None):
     global_tflops = fl * p_global / (stage_ms["global"] * 1e-3) / 1e12 if p_global else 0.0
     local_tflops = fl * p_local / (stage_ms["local"] * 1e-3) / 1e12
 
-    # dense causal baseline: the DENSE kernel and the query-sparse kernel with every row selected
+    # Dense causal baseline (the DENSE kernel, and the query-sparse kernel
+    # with every row selected; the faster is t_dense), timed under the same
+    # clock state as the layer: after one untimed call of each, --rounds
+    # rounds each time a block of K layer steps, then a block of dense steps
+    # of each kind; the speedup is the ratio of the medians over the rounds.
     dense = {}
+    fair = None
     if not args.no_dense:
         o2 = torch.empty((N, Hq, d), dtype=torch.bfloat16, device="cuda")
-        s0, s1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"], out=o2)
-        torch.cuda.synchronize()
-        s0.record()
-        for _ in range(args.dense_steps):
-            pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"], out=o2)
-        s1.record()
-        torch.cuda.synchronize()
-        dense["dense_kernel_ms"] = s0.elapsed_time(s1) / args.dense_steps
         all_idx = torch.arange(N, dtype=torch.int32, device="cuda")
         og = torch.empty((N, Hq, d), dtype=torch.float32, device="cuda")
         gws = torch.empty(pk.logo_workspace_bytes(prob, pk.LOGO_ENTRY_GLOBAL, N),
                           dtype=torch.uint8, device="cuda")
         cu_all = dev["cu_seqlens"].clone()
-        pk.logo_global_attn_sparse_q(prob, dev["q"], dev["k"], dev["v"], all_idx, cu_all, N,
-                                     o_global=og, ws=gws)
-        torch.cuda.synchronize()
-        s0.record()
-        for _ in range(args.dense_steps):
+
+        def dense_kernel():
+            pk.logo_dense_causal_attn(prob, dev["q"], dev["k"], dev["v"], out=o2)
+
+        def sparse_all_rows():
             pk.logo_global_attn_sparse_q(prob, dev["q"], dev["k"], dev["v"], all_idx, cu_all, N,
                                          o_global=og, ws=gws)
-        s1.record()
+        dense_kernel()
+        sparse_all_rows()
         torch.cuda.synchronize()
-        dense["sparse_q_all_rows_ms"] = s0.elapsed_time(s1) / args.dense_steps
-        del o2, og, gws
-        t_dense = min(dense.values())
+        rounds = {"layer": [], "dense_kernel": [], "sparse_q_all_rows": []}
+        for _ in range(args.rounds):
+            rounds["layer"].append(timed_block(step, args.steps))
+            rounds["dense_kernel"].append(timed_block(dense_kernel, args.dense_steps))
+            rounds["sparse_q_all_rows"].append(timed_block(sparse_all_rows, args.dense_steps))
+            sclk.append(current_sclk_mhz())
+        med = {k: float(np.median(v)) for k, v in rounds.items()}
+        dense["dense_kernel_ms"] = med["dense_kernel"]
+        dense["sparse_q_all_rows_ms"] = med["sparse_q_all_rows"]
+        t_dense = min(med["dense_kernel"], med["sparse_q_all_rows"])
         dense["t_dense_ms"] = t_dense
         dense["dense_tflops"] = fl * p_dense / (t_dense * 1e-3) / 1e12
+        sp = [min(dk, sq) / lay for lay, dk, sq in zip(rounds["layer"], rounds["dense_kernel"],
+                                                       rounds["sparse_q_all_rows"])]
+        fair = {"rounds": args.rounds, "layer_ms_median": round(med["layer"], 4),
+                "t_dense_ms_median": round(t_dense, 4),
+                "speedup_median": round(t_dense / med["layer"], 3),
+                "speedup_per_round": [round(v, 3) for v in sp],
+                "layer_ms_per_round": [round(v, 4) for v in rounds["layer"]],
+                "dense_kernel_ms_per_round": [round(v, 4) for v in rounds["dense_kernel"]],
+                "sparse_q_all_rows_ms_per_round": [round(v, 4)
+                                                   for v in rounds["sparse_q_all_rows"]]}
+        del o2, og, gws
         log("dense: " + " ".join(f"{k}={v:.3f}" for k, v in dense.items()))
+        log(f"interleaved rounds: {fair}")
 
     # Threshold mode on the same inputs (the Markov "on" set itself, b_th = 0.5)
     thr_mode = None
@@ -627,7 +692,15 @@ def main(argv=None):
                 "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4),
                 "traffic": committed_traffic(w.name),
                 "flops_per_launch": fl * p_global,
-                "duration_ms": round(stage_ms["global"], 4)}
+                "duration_ms": round(stage_ms["global"], 4),
+                "duration_source": "mean of the global stage's HIP events over the K profiled "
+                                   "steps"}
+    trace_us = committed_trace_avg_us(w.name)
+    if trace_us:
+        # the committed rocprofv3 kernel trace of the same sources and workload
+        roofline["trace_avg_us_timed_calls"] = trace_us
+        roofline["trace_frac"] = round(fl * p_global / (trace_us * 1e-6) / 1e12
+                                       / PEAK_BF16_TFLOPS, 4)
 
     transforms = None
     if not args.no_transforms:
@@ -671,7 +744,8 @@ def main(argv=None):
                    "q_heads": Hq, "kv_heads": w.num_kv_heads, "head_dim": d,
                    "window": w.window, "ratio": w.ratio, "gate": w.gate,
                    "n_sel": int(sel_np.size)},
-        "speedup_vs_dense": round(dense["t_dense_ms"] / ms_step, 3) if dense else None,
+        "speedup_vs_dense": fair["speedup_median"] if fair else None,
+        "speedup_timing": fair,
         "ideal_speedup_pairs": round(ideal, 3),
         "ideal_speedup_paper": round(1.0 / (w.ratio + w.window / w.max_seqlen), 3),
         "ms_per_step_with_stage_events": round(ms_step_profiled, 4),
@@ -686,8 +760,7 @@ def main(argv=None):
         "decode": decode,
         "transforms": transforms,
         "train": train,
-        "gpu": gpu_info(torch, busy=lambda: [step() for _ in range(600)])
-               if not args.no_extra else None,
+        "gpu": gpu_info(torch, sclk),
     }
     print(json.dumps(rec), flush=True)
     return 0

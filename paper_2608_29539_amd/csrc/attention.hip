@@ -8,11 +8,13 @@
 //   kModeDense  : every token, keys 0..i                   (dense causal
 //                 baseline, Eq. attention with the global context)
 //
-// Work decomposition.  A workgroup has 4 waves; each wave owns 32 query rows
-// of one query head, and all 4 waves read the same key/value head, so a
-// staged K/V tile in LDS serves 128 rows.  With GQA group size G the waves
-// take gcd(G,4) heads of one KV group, which keeps the tile's token span --
-// and so its causal-diagonal band -- short.
+// Work decomposition.  A workgroup has W waves (4 in the local mode, two
+// workgroups per CU; 8 in the global and dense modes, one per CU); each wave
+// owns 32 query rows of one query head, and all W waves read the same
+// key/value head, so a staged K/V tile in LDS serves 32 W rows (128 local,
+// 256 global / dense).  With GQA group size G the waves take gcd(G,4) heads
+// of one KV group, which keeps the tile's token span -- and so its
+// causal-diagonal band -- short.
 //
 // MFMA formulation (v_mfma_f32_32x32x16_bf16, lane l: column l%32, rows
 // 8*(i/4) + 4*(l/32) + i%4 of the 32x32 accumulator).  The kernel computes
@@ -713,26 +715,57 @@ void attn_kernel(const AttnArgs a) {
         // of their XCD (workgroups are dispatched round-robin over the 8
         // XCDs): queue x holds items x, x+8, x+16, ...  Items are in
         // longest-first order, and items that share a KV head tend to share
-        // an XCD and its L2.  Every workgroup exits after all 8 queues have
-        // returned an index past the end.
+        // an XCD and its L2.  Once its own queue is empty a workgroup takes
+        // what is left in the other queues (in XCD order), so no XCD idles
+        // while another has work.  Wave 0 reads the 8 queue counters at once
+        // and takes an item from the first queue that still has one; an
+        // index past the end means that queue has just emptied, and the
+        // counters only grow, so each retry closes a queue: a workgroup
+        // exits after at most 8 empty takes (the loop allows 17), and at
+        // once when there is no entry at all.
         __shared__ int s_item;
         const int x0 = blockIdx.x % kQueues;
-        const int n_items = a.queue[0] * a.n_hg;
-        // Own XCD's queue first; once it is empty, take what is left in the
-        // other queues (in XCD order), so no XCD idles while another has work.
-        for (int qi = 0; qi < kQueues; qi++) {
-            const int x = (x0 + qi) % kQueues;
-            for (;;) {
-                if (threadIdx.x == 0)
-                    s_item = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
-                __syncthreads();
-                const int item = __builtin_amdgcn_readfirstlane(s_item);
-                __syncthreads();
-                if (item >= n_items)
-                    break;
-                const SparseTile t = a.tiles[item / a.n_hg];
-                attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
+        const int n_entries = a.queue[0];
+        if (n_entries == 0)
+            return;
+        const int n_items = n_entries * a.n_hg;
+        const int lane = threadIdx.x & 63;
+        // this lane's queue (lanes 0..7) and its length
+        const int xl = (x0 + lane) % kQueues;
+        const int len_l = (n_items - xl + kQueues - 1) / kQueues;
+        for (;;) {
+            if (threadIdx.x < 64) {
+                int item = -1;
+                for (int tries = 0; tries <= 2 * kQueues; tries++) {
+                    const int c = lane < kQueues
+                                      ? __hip_atomic_load(&a.queue[1 + xl], __ATOMIC_RELAXED,
+                                                          __HIP_MEMORY_SCOPE_AGENT)
+                                      : 0;
+                    const uint64_t open =
+                        __builtin_amdgcn_ballot_w64(lane < kQueues && c < len_l);
+                    if (open == 0)
+                        break;
+                    const int f = __builtin_ctzll(open);
+                    const int x = (x0 + f) % kQueues;
+                    int got = 0;
+                    if (lane == f)
+                        got = x + kQueues * atomicAdd(&a.queue[1 + x], 1);
+                    got = __builtin_amdgcn_readlane(got, f);
+                    if (got < n_items) {
+                        item = got;
+                        break;
+                    }
+                }
+                if (lane == 0)
+                    s_item = item;
             }
+            __syncthreads();
+            const int item = __builtin_amdgcn_readfirstlane(s_item);
+            __syncthreads();
+            if (item < 0)
+                break;
+            const SparseTile t = a.tiles[item / a.n_hg];
+            attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
         }
     } else {
         int bid = blockIdx.x;

@@ -11,6 +11,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 
 using namespace logo;
 
@@ -341,18 +342,49 @@ logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode m
                       s);
 }
 
-// Persistent grid of the global kernel and the arguments of its tile plan
-// (work table in the global workspace `ws`).
+// Persistent grid of the global kernel on the current device: its CUs times
+// the kernel's resident workgroups per CU, rounded up to a multiple of the
+// work queues.  The CU count is queried once per device and the occupancy
+// once per head dim (std::call_once); a call only asks which device is
+// current.
+constexpr int kMaxDevices = 64;
+struct DeviceCache {
+    std::once_flag once;
+    int cus = 0;
+};
+DeviceCache g_devices[kMaxDevices];
+std::once_flag g_occ_once[2];
+int g_occ[2] = {0, 0};
+
+logo_status global_grid(int head_dim, int &grid) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return LOGO_ERR_HIP;
+    DeviceCache &c = g_devices[dev];
+    std::call_once(c.once, [&] {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+            c.cus = n;
+    });
+    if (c.cus <= 0)
+        return LOGO_ERR_HIP;
+    const int di = head_dim == 128 ? 1 : 0;
+    std::call_once(g_occ_once[di],
+                   [&] { g_occ[di] = attention_blocks_per_cu(kModeGlobal, head_dim); });
+    grid = c.cus * g_occ[di];
+    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    return LOGO_OK;
+}
+
+// The arguments of the global branch's tile plan (work table in the global
+// workspace `ws`) and the persistent grid that consumes it.
 logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int32_t *cu_sel,
                         int32_t cap, char *ws, PlanArgs &pa, int &grid) {
     const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
     const GlobalWs w = global_ws(p, cap);
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return LOGO_ERR_HIP;
-    grid = cus * attention_blocks_per_cu(kModeGlobal, p->head_dim);
-    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    const logo_status st = global_grid(p->head_dim, grid);
+    if (st != LOGO_OK)
+        return st;
     pa.cu_sel = cu_sel;
     pa.sel_idx = sel_idx;
     pa.tpw = tp.tpw;
@@ -422,10 +454,14 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
         s);
 }
 
+// built: the plan of a fused launch whose extra workgroup has already
+// written the work table (its arguments and grid from global_plan); NULL
+// builds the table with a launch of its own first.
 logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                        const logo_bf16 *v, const int32_t *sel_idx, const int32_t *cu_sel,
                        int32_t cap, float *o, const FusedEpi *f, const float *gain, char *ws,
-                       hipStream_t s, hipEvent_t after_plan = nullptr, bool plan_done = false,
+                       hipStream_t s, hipEvent_t after_plan = nullptr,
+                       const PlanArgs *built = nullptr, int built_grid = 0,
                        float *lse = nullptr) {
     if (p->total_tokens == 0 || cap == 0)
         return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
@@ -433,10 +469,13 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     const GlobalWs w = global_ws(p, cap);
     PlanArgs pa;
     int grid = 0;
-    logo_status st = global_plan(p, sel_idx, cu_sel, cap, ws, pa, grid);
-    if (st != LOGO_OK)
-        return st;
-    if (!plan_done) {
+    logo_status st;
+    if (built) {
+        pa = *built;
+        grid = built_grid;
+    } else {
+        if ((st = global_plan(p, sel_idx, cu_sel, cap, ws, pa, grid)) != LOGO_OK)
+            return st;
         st = hip_status(launch_sparse_plan(p->cu_seqlens, p->num_seqs, pa, s), s);
         if (st != LOGO_OK)
             return st;
@@ -526,7 +565,7 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
         return st;
     st = run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, nullptr, &fe,
                     gain_global, base + w.glob_ws, s, events ? (hipEvent_t)events[3] : nullptr,
-                    /*plan_done=*/true);
+                    &plan, grid_g);
     if (st != LOGO_OK)
         return st;
     return mark(4);
@@ -904,8 +943,8 @@ logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const
     if (st != LOGO_OK)
         return st;
     return run_global(p, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel_idx, cu_sel, cap,
-                      o_global, &fe, gain_global, base + w.glob_ws, s, nullptr,
-                      /*plan_done=*/true, lse_global);
+                      o_global, &fe, gain_global, base + w.glob_ws, s, nullptr, &plan, grid_g,
+                      lse_global);
 }
 
 logo_status logo_attn_bwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
@@ -1107,7 +1146,7 @@ logo_status logo_global_attn_sparse_q_fwd_train(const logo_problem *p, const log
             return st;
     }
     return run_global(p, q, k, v, sel_idx, cu_sel, sel_capacity, o_global, nullptr, nullptr,
-                      (char *)ws, (hipStream_t)stream, nullptr, false, lse_global);
+                      (char *)ws, (hipStream_t)stream, nullptr, nullptr, 0, lse_global);
 }
 
 logo_status logo_global_attn_sparse_q_bwd(const logo_problem *p, const logo_bf16 *q,

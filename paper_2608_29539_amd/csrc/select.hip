@@ -3,17 +3,19 @@
 // original positions and compacted sequence offsets), plus the tile plan
 // of the query-sparse global branch.
 //
-//   select_kernel     up to 16 workgroups of 1024 threads per sequence, each
-//                     compacting one part of it.  Threshold: ratio mode takes
+//   select_kernel     up to 16 workgroups of 1024 threads per sequence (more
+//                     for sequences over 512K tokens), each compacting one
+//                     part of it.  Threshold: ratio mode takes
 //                     k = floor(ratio*T) in IEEE double and the (k+1)-th
 //                     largest gate, found by every part with radix passes of
 //                     at most 12 bits over order-preserving uint32 keys (LDS
 //                     histograms), starting below the bits that all keys of
 //                     the sequence share; threshold mode takes the given
 //                     value.  Then z_t = gate[t] > thr (strict, fp32, done on
-//                     the keys) and the part's ranks follow from the selected
-//                     count before it plus one workgroup scan; writes sel_idx,
-//                     tok2sel and cu_sel.  One sequence: a single launch.
+//                     the keys held in registers) and the part's ranks follow
+//                     from wave ballots, one scan of per-block counts and the
+//                     lane prefix (mbcnt); writes sel_idx, tok2sel and
+//                     cu_sel.  One sequence: a single launch.
 //                     Several: a first launch finds the thresholds and
 //                     counts, a second one compacts with offset = sum of the
 //                     earlier counts.
@@ -33,8 +35,8 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kKeysPerThread = 32;                      // gate keys per thread per chunk
 constexpr int kSelChunk = kKeysPerThread * kSelThreads;  // tokens per chunk (32768)
-constexpr int kRoundTokens = 4 * kSelThreads;           // tokens per compaction round
-constexpr int kMaxParts = 16;                           // workgroups per sequence at most
+constexpr int kPartUnit = 4 * kSelThreads;              // smallest part (4096 tokens)
+constexpr int kMaxParts = 16;                           // parts per sequence while parts fit a chunk
 // Word 3 of a raw (untyped, stride 0) buffer descriptor.
 constexpr int kRawBufferWord3 = 0x00020000;
 
@@ -106,8 +108,10 @@ __device__ __forceinline__ void block_min_max(uint32_t &mn, uint32_t &mx, uint32
 }
 
 // Selection, one 1024-thread workgroup per (part, sequence): blockIdx.y is
-// the sequence, blockIdx.x the part, and part p compacts the tokens
-// [p * part_tokens, (p + 1) * part_tokens) of the sequence.
+// the sequence, blockIdx.x the part, and part p writes the tokens
+// [p * part_tokens, (p + 1) * part_tokens) of the sequence.  part_tokens is
+// 4096 times a power of two up to kSelChunk, or a multiple of kSelChunk, so
+// a part never straddles two chunks.
 //
 // kThreshold: find thr[b] (ratio mode, every part of the sequence finds the
 // same value) or take the given one, and part 0 writes thr[b]; otherwise read
@@ -121,17 +125,25 @@ __device__ __forceinline__ void block_min_max(uint32_t &mn, uint32_t &mx, uint32
 // keys share (the common prefix of the smallest and the largest key), so
 // that gates spread over a narrow range still spread over the histogram bins.
 // A pass whose chosen bin holds a single key ends the search.
+//
+// Compaction works on the keys in registers: key slot j of thread tid holds
+// token c0 + 1024 j + tid, so the lanes of wave w hold the 64 consecutive
+// tokens of block 16 j + w of the chunk.  One ballot per slot gives each
+// block's selected count (kept in LDS), one scan of the 512 block counts
+// gives each block's first rank, and a token's rank adds the selected lanes
+// below it (mbcnt).
 template <bool kThreshold, bool kWrite>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int32_t *__restrict__ cu, int B, const float *__restrict__ gate, int mode, float fixed,
     double ratio, float *__restrict__ thr, int32_t *__restrict__ cnt, int32_t *__restrict__ sel_idx,
     int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel, int part_tokens) {
-    __shared__ int hist[4096];
+    __shared__ int hist[4096];                // radix histogram, then the block counts
     __shared__ int s_wave[kSelWaves];
     __shared__ uint32_t s_u[2 * kSelWaves];
     __shared__ uint32_t s_bin;
-    __shared__ int s_rank, s_bincnt, s_total;
+    __shared__ int s_rank, s_bincnt;
     const int b = blockIdx.y, part = blockIdx.x, tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
     const int64_t base = cu[b];
     const int T = cu[b + 1] - (int)base;
     const int p0 = part * part_tokens;
@@ -143,11 +155,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     // Keys of one chunk of kSelChunk tokens (token c0 + j * 1024 + tid in
     // key[j]); a sequence that fits in one chunk is loaded once.
     const bool resident = T <= kSelChunk;
-    // The chunk is read through a buffer descriptor that covers exactly its
-    // tokens, so every load's address is this thread's offset plus a uniform
-    // constant, and the loads are unconditional (all in flight at once):
-    // slots past the sequence end read 0 and every use below tests t < T.
     uint32_t key[kKeysPerThread];
+    // The chunk is read through a buffer descriptor that covers exactly its
+    // tokens, with each load's whole offset in the bounds-checked VGPR
+    // offset: slots past the sequence end read 0 (and are never used, see
+    // in_seq), so the loads need no condition and are all in flight at once.
     auto load_chunk = [&](int c0) {
         const int n = min(T - c0, kSelChunk);
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
@@ -155,9 +167,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 #pragma unroll
         for (int j = 0; j < kKeysPerThread; j++)
             key[j] = float_key(__builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(r, tid * 4, j * kSelThreads * 4, 0)));
+                float, __builtin_amdgcn_raw_buffer_load_b32(r, (j * kSelThreads + tid) * 4, 0, 0)));
     };
-    if (resident && (radix || !kWrite || part > 0))
+    // slot j of the chunk at c0 holds a token of the sequence
+    auto in_seq = [&](int c0, int j) { return j * kSelThreads < T - c0 - tid; };
+    if (resident)
         load_chunk(0);
 
     uint32_t thr_key;
@@ -177,7 +191,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                     load_chunk(c0);
 #pragma unroll
                 for (int j = 0; j < kKeysPerThread; j++)
-                    if (c0 + j * kSelThreads + tid < T) {
+                    if (in_seq(c0, j)) {
                         mn = min(mn, key[j]);
                         mx = max(mx, key[j]);
                     }
@@ -198,25 +212,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                     for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                         if (!resident)
                             load_chunk(c0);
-                        // Runs of equal digits are counted in a register and
-                        // added in one atomic.
-                        int cur = -1, run_len = 0;
+                        // Consecutive slots of a thread are 1024 tokens apart,
+                        // so their digits are unrelated: one atomic per key.
 #pragma unroll
-                        for (int j = 0; j < kKeysPerThread; j++) {
-                            const int t = c0 + j * kSelThreads + tid;
-                            if (t < T && (key[j] & pmask) == prefix) {
-                                const int d = (int)((key[j] >> sh) & (uint32_t)(nb - 1));
-                                if (d != cur) {
-                                    if (run_len > 0)
-                                        atomicAdd(&hist[cur], run_len);
-                                    cur = d;
-                                    run_len = 0;
-                                }
-                                run_len++;
-                            }
-                        }
-                        if (run_len > 0)
-                            atomicAdd(&hist[cur], run_len);
+                        for (int j = 0; j < kKeysPerThread; j++)
+                            if (in_seq(c0, j) && (key[j] & pmask) == prefix)
+                                atomicAdd(&hist[(key[j] >> sh) & (uint32_t)(nb - 1)], 1);
                     }
                     __syncthreads();
                     // Each thread owns 4 consecutive bins.
@@ -249,11 +250,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                     if (hi >= 0 && unique && resident) {
                         // one key left in the bin: it is the threshold
 #pragma unroll
-                        for (int j = 0; j < kKeysPerThread; j++) {
-                            const int t = j * kSelThreads + tid;
-                            if (t < T && (key[j] & pmask) == prefix)
+                        for (int j = 0; j < kKeysPerThread; j++)
+                            if (in_seq(0, j) && (key[j] & pmask) == prefix)
                                 s_bin = key[j];
-                        }
                         __syncthreads();
                         prefix = s_bin;
                         break;
@@ -270,24 +269,36 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     }
     // z = gate > thr on the keys: -0 and +0 share a key, and NaN gates (keys
     // above +inf, or below -inf) never pass.
-    auto pass_z = [&](uint32_t kj) { return kj > thr_key && kj <= kPosInfKey; };
-    // selected tokens of the sequence before token `end`
-    auto count_before = [&](int end) {
-        int mine = 0;
-        for (int c0 = 0; c0 < end; c0 += kSelChunk) {
-            if (!resident)
-                load_chunk(c0);
+    auto pass_z = [&](int c0, int j) {
+        return in_seq(c0, j) && key[j] > thr_key && key[j] <= kPosInfKey;
+    };
+    // selected tokens of the chunk in registers (per wave, then the sum)
+    auto chunk_count = [&](int c0) {
+        int n = 0;
 #pragma unroll
-            for (int j = 0; j < kKeysPerThread; j++) {
-                const int t = c0 + j * kSelThreads + tid;
-                mine += (t < end && pass_z(key[j])) ? 1 : 0;
-            }
-        }
-        return block_sum(mine, s_wave);
+        for (int j = 0; j < kKeysPerThread; j++)
+            n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(pass_z(c0, j)));
+        return n;                              // wave-uniform
+    };
+    auto block_total = [&](int per_wave) {
+        if (lane == 0)
+            s_wave[wave] = per_wave;
+        __syncthreads();
+        int sum = 0;
+        for (int i = 0; i < kSelWaves; i++)
+            sum += s_wave[i];
+        __syncthreads();
+        return sum;
     };
 
     if constexpr (!kWrite) {
-        const int total = count_before(T);
+        int mine = 0;
+        for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+            if (!resident)
+                load_chunk(c0);
+            mine += chunk_count(c0);
+        }
+        const int total = block_total(mine);
         if (tid == 0)
             cnt[b] = total;
     } else {
@@ -300,44 +311,79 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         }
         if (part == 0 && tid == 0)
             cu_sel[b] = offset;
-        int running = offset + (part > 0 ? count_before(p0) : 0);
-        // Compaction of [p0, p1): each thread takes 4 consecutive tokens per
-        // round; ranks from one workgroup scan of the per-thread counts.  The
-        // last part runs to the end of the sequence.
         const int p1 = part == (int)gridDim.x - 1 ? T : min(T, p0 + part_tokens);
-        for (int c = p0; c < p1; c += kRoundTokens) {
-            const int t0 = c + tid * 4;
-            uint32_t zm = 0;
-#pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const int t = t0 + e;
-                if (t < p1 && pass_z(float_key(gate[base + t])))
-                    zm |= 1u << e;
+        int end_count = offset;               // selected tokens before p1 (with the offset)
+        if (p0 < p1) {
+            // the chunk that holds the part, and the selected tokens before it
+            const int cs = (p0 / kSelChunk) * kSelChunk;
+            int before = 0;
+            for (int c0 = 0; c0 < cs; c0 += kSelChunk) {
+                load_chunk(c0);
+                before += chunk_count(c0);
             }
-            const int n = __popc(zm);
-            const int incl = block_inclusive_scan(n, s_wave);
-            if (tid == kSelThreads - 1)
-                s_total = incl;
-            int r = running + incl - n;
+            before = offset + (cs > 0 ? block_total(before) : 0);
+            if (!resident)
+                load_chunk(cs);
+            // selected count of each 64-token block of the chunk
 #pragma unroll
-            for (int e = 0; e < 4; e++) {
-                const int t = t0 + e;
-                if (t < p1) {
-                    const bool z = (zm >> e) & 1u;
-                    if (z && r < cap)
+            for (int j = 0; j < kKeysPerThread; j++) {
+                const int n = __builtin_popcountll(__builtin_amdgcn_ballot_w64(pass_z(cs, j)));
+                if (lane == 0)
+                    hist[j * kSelWaves + wave] = n;
+            }
+            __syncthreads();
+            // exclusive scan of the 512 block counts (the first 8 waves)
+            constexpr int kBlocks = kKeysPerThread * kSelWaves;
+            int v = 0, incl = 0;
+            if (tid < kBlocks) {
+                v = hist[tid];
+                incl = v;
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const int t = __shfl_up(incl, d, 64);
+                    if (lane >= d)
+                        incl += t;
+                }
+                if (lane == 63)
+                    s_wave[wave] = incl;
+            }
+            __syncthreads();
+            if (tid < kBlocks) {
+                int pre = 0;
+                for (int i = 0; i < wave; i++)
+                    pre += s_wave[i];
+                hist[tid] = pre + incl - v;
+            }
+            int chunk_total = 0;
+            for (int i = 0; i < kBlocks / 64; i++)
+                chunk_total += s_wave[i];
+            __syncthreads();
+            // ranks and writes of the part's tokens
+#pragma unroll
+            for (int j = 0; j < kKeysPerThread; j++) {
+                const int j0 = cs + j * kSelThreads;      // first token of slot j
+                if (j0 + kSelThreads <= p0 || j0 >= p1)
+                    continue;                             // (wave-uniform)
+                const bool z = pass_z(cs, j);
+                const uint64_t bal = __builtin_amdgcn_ballot_w64(z);
+                const int r = before + hist[j * kSelWaves + wave] +
+                              (int)__builtin_amdgcn_mbcnt_hi(
+                                  (uint32_t)(bal >> 32),
+                                  __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+                const int t = j0 + tid;
+                if (t >= p0 && t < p1) {
+                    const bool keep = z && r < cap;
+                    if (keep)
                         sel_idx[r] = (int32_t)(base + t);
                     if (tok2sel)
-                        tok2sel[base + t] = (z && r < cap) ? r : -1;
-                    r += z ? 1 : 0;
+                        tok2sel[base + t] = keep ? r : -1;
                 }
             }
-            __syncthreads();
-            running += s_total;
-            __syncthreads();
+            end_count = before + chunk_total;
         }
         // the part holding the last token of the last sequence closes cu_sel
         if (b == B - 1 && p1 == T && tid == 0)
-            cu_sel[B] = running;
+            cu_sel[B] = end_count;
     }
 }
 
@@ -377,10 +423,13 @@ hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
                          int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s) {
-    // parts of whole compaction rounds, at most kMaxParts per sequence
-    const int rounds = max(1, (max_seqlen + kRoundTokens - 1) / kRoundTokens);
-    const int part_tokens = ((rounds + kMaxParts - 1) / kMaxParts) * kRoundTokens;
-    const int parts = max(1, (max_seqlen + part_tokens - 1) / part_tokens);
+    // parts of 4096 * 2^i tokens, at most kMaxParts per sequence unless a
+    // part would exceed one chunk (then one part per chunk)
+    int part_tokens = kPartUnit;
+    while (part_tokens < kSelChunk &&
+           ((long long)max_seqlen + part_tokens - 1) / part_tokens > kMaxParts)
+        part_tokens *= 2;
+    const int parts = (int)std::max(1LL, ((long long)max_seqlen + part_tokens - 1) / part_tokens);
     if (num_seqs == 1) {
         hipLaunchKernelGGL((select_kernel<true, true>), dim3(parts, 1), dim3(kSelThreads), 0, s,
                            cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,

@@ -185,6 +185,8 @@ def test_budget_controller_validation(lib):
     g = lib.logo_pmask_initial_threshold
     assert g(2.0 ** -10, 1024) == -0.5
     assert g(0.25, 0) == 0.5
+    # the value App. C prints for gamma = 0.0005 and S = 5000 steps
+    assert g(0.0005, 5000) == -2.0
 
 
 def test_device_threshold_mode_needs_thr_out(lib):

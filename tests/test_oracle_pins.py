@@ -411,6 +411,16 @@ def test_pmask_reaches_gate_centre(oracle_lib):
     assert step >= 511
 
 
+def test_pmask_start_printed_in_paper(oracle_lib):
+    # App. C (training details of the 1.5B comparison): gamma = 0.0005 and a
+    # P-mask of S = 5000 steps (20% of 100B tokens at 4M tokens per step)
+    # give the printed starting threshold b_th,0 = 0.5 - gamma S = -2.0.
+    # gamma is an fp32 argument: 0.0005 in fp32 is 0.00050000002374...,
+    # so 0.5 - gamma S = -2.0000001187 in double, 1.187e-7 from -2, less
+    # than half an fp32 ulp at 2 (1.192e-7): the fp32 result is exactly -2.
+    assert oracle_lib.pmask_initial_threshold(0.0005, 5000) == -2.0
+
+
 def test_controller_settles_at_target_quantile(oracle_lib):
     # gates on the grid (i + 0.5)/N: the fraction above t is 1 - t, so with
     # rho = 1/4 the controller must settle within gamma of t = 0.75 and then
