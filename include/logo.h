@@ -55,7 +55,9 @@ typedef enum {
     LOGO_ERR_UNSUPPORTED = 3, /* a valid but unimplemented case (head_dim)         */
     LOGO_ERR_ARG = 4,         /* an argument out of its domain (ratio, window...)  */
     LOGO_ERR_WORKSPACE = 5,   /* workspace missing, misaligned or too small        */
-    LOGO_ERR_HIP = 6          /* the HIP runtime refused a launch                  */
+    LOGO_ERR_HIP = 6,         /* the HIP runtime refused a launch                  */
+    LOGO_ERR_SCRATCH_LIMIT = 7 /* logo_decode_noalloc: the step needs more scratch
+                                  than LOGO_NOALLOC_SCRATCH_BYTES                  */
 } logo_status;
 
 typedef enum {
@@ -411,6 +413,33 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
                         float threshold, const float *thr_dev, const float *gain_local,
                         const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
                         int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream);
+
+/*
+ * logo_decode_noalloc -- logo_decode for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same decoding step with the same arguments and
+ * results, minus the workspace.  Its scratch memory (the partial results of
+ * the key chunks, and the selected list and count when active / n_active
+ * are NULL) is a fixed device array of LOGO_NOALLOC_SCRATCH_BYTES inside the
+ * library, which every GPU the library runs on holds from the module's load
+ * until the process ends.  The call allocates and frees nothing; the first
+ * call on a device looks up the array's address there once.
+ *   Errors: those of logo_decode, and LOGO_ERR_SCRATCH_LIMIT (nothing
+ *   enqueued) when logo_workspace_bytes(p, LOGO_ENTRY_DECODE, 0) exceeds
+ *   LOGO_NOALLOC_SCRATCH_BYTES (64 MiB; 32 caches of 32K tokens with 32
+ *   query heads and 8 KV heads of d = 128 need 35 MB).
+ *   Concurrency: every call on one GPU shares that GPU's array, which keeps
+ *   the last call's contents (nothing in it must start at zero).  Calls that
+ *   overlap on one GPU -- on different streams, or from different threads
+ *   without ordering -- race on it; order them on one stream.
+ */
+#define LOGO_NOALLOC_SCRATCH_BYTES (64u << 20)
+logo_status logo_decode_noalloc(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                                const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                float threshold, const float *thr_dev, const float *gain_local,
+                                const float *gain_global, float eps, logo_bf16 *out,
+                                int32_t *active, int32_t *n_active, logo_stream stream);
 
 /*
  * logo_gate_proj -- the gate of Eq. gate-routing (Sec. 3.2):

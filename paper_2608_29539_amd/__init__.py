@@ -36,6 +36,7 @@ from .binding import (  # noqa: F401
     logo_budget_update,
     logo_combine,
     logo_decode,
+    logo_decode_noalloc,
     logo_dense_causal_attn,
     logo_dense_causal_attn_bwd,
     logo_dense_causal_attn_fwd_train,

@@ -40,7 +40,7 @@ EXPORTS = (
     "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
     "logo_attn_fwd_train", "logo_attn_bwd", "logo_dense_causal_attn_fwd_train",
     "logo_dense_causal_attn_bwd", "logo_global_attn_sparse_q_fwd_train",
-    "logo_global_attn_sparse_q_bwd",
+    "logo_global_attn_sparse_q_bwd", "logo_decode_noalloc",
 )
 
 _lib = None
@@ -96,6 +96,7 @@ def library():
         "logo_dense_causal_attn": [PP, P, P, P, P, P],
         "logo_budget_update": [PP, P, f64, f32, P, P, P],
         "logo_decode": [PP, P, P, P, P, P, P, P, i32, f32, P, P, P, f32, P, P, P, P, sz, P],
+        "logo_decode_noalloc": [PP, P, P, P, P, P, P, P, i32, f32, P, P, P, f32, P, P, P, P],
         "logo_gate_proj": [i64, i32, P, P, P, P],
         "logo_branch_transform": [i64, i32, i32, ctypes.c_int, P, P, P, P, P, i64, P, P, P],
         "logo_attn_fwd_train": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P,
@@ -616,6 +617,46 @@ def logo_decode(prob: Problem, q, k, v, gate, *, threshold: Optional[float] = No
           _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
           _ptr(threshold_device), _ptr(gain_local), _ptr(gain_global), float(eps), _ptr(out),
           _ptr(active), _ptr(n_active), _ptr(ws), nbytes, _stream())
+    return out, active, n_active
+
+
+def logo_decode_noalloc(prob: Problem, q, k, v, gate, out, *, threshold: Optional[float] = None,
+                        threshold_device=None, q_g=None, k_g=None, v_g=None, gain_local=None,
+                        gain_global=None, eps: float = 1e-6, active=None, n_active=None):
+    """``logo_decode`` without a workspace: the library's fixed device scratch
+    array holds the partial results (and the selected list and count when
+    ``active`` / ``n_active`` are None).  ``out`` [B, Hq, d] bf16 must be
+    given; nothing is allocated.  Returns (out, active, n_active), the last
+    two None when not given."""
+    import torch
+    N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
+                        prob.num_seqs)
+    if (threshold is None) == (threshold_device is None):
+        raise ValueError("give exactly one of threshold / threshold_device")
+    if threshold_device is not None:
+        if (threshold_device.dtype != torch.float32 or not threshold_device.is_cuda
+                or threshold_device.numel() < 1):
+            raise ValueError("threshold_device: device float32 tensor")
+        mode = LOGO_SEL_THRESHOLD_DEVICE
+    else:
+        mode = LOGO_SEL_THRESHOLD
+    _check(q, torch.bfloat16, (B, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    for t, nm, shp in ((q_g, "q_g", (B, Hq, d)), (k_g, "k_g", (N, Hkv, d)),
+                       (v_g, "v_g", (N, Hkv, d))):
+        if t is not None:
+            _check(t, torch.bfloat16, shp, nm)
+    _check(gate, torch.float32, (B,), "gate")
+    _check(out, torch.bfloat16, (B, Hq, d), "out")
+    if active is not None:
+        _check(active, torch.int32, (B,), "active")
+    if n_active is not None:
+        _check(n_active, torch.int32, (1,), "n_active")
+    _call("logo_decode_noalloc", prob.c, _ptr(q), _ptr(k), _ptr(v), _ptr(q_g), _ptr(k_g),
+          _ptr(v_g), _ptr(gate), mode, float(threshold if threshold is not None else 0.0),
+          _ptr(threshold_device), _ptr(gain_local), _ptr(gain_global), float(eps), _ptr(out),
+          _ptr(active), _ptr(n_active), _stream())
     return out, active, n_active
 
 

@@ -356,6 +356,36 @@ DeviceCache g_devices[kMaxDevices];
 std::once_flag g_occ_once[2];
 int g_occ[2] = {0, 0};
 
+// Scratch memory of logo_decode_noalloc: a fixed device array instead of a
+// caller workspace (see that entry point).  Every GPU the library runs on
+// holds its own copy from the module's load until the process ends.  In host
+// code the array's name is only a host-side stand-in; its address on each
+// device is looked up once, with that device current, and only that address
+// is passed to kernels.
+static __device__ __align__(256) unsigned char scratch[LOGO_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchSlot {
+    std::once_flag once;
+    void *ptr = nullptr;
+};
+ScratchSlot g_scratch[kMaxDevices];
+
+logo_status device_scratch(void **ptr) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return LOGO_ERR_HIP;
+    ScratchSlot &sl = g_scratch[dev];
+    std::call_once(sl.once, [&] {
+        void *a = nullptr;
+        if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) == hipSuccess)
+            sl.ptr = a;
+    });
+    if (!sl.ptr)
+        return LOGO_ERR_HIP;
+    *ptr = sl.ptr;
+    return LOGO_OK;
+}
+
 logo_status global_grid(int head_dim, int &grid) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
@@ -584,6 +614,7 @@ const char *logo_status_str(logo_status s) {
     case LOGO_ERR_ARG: return "LOGO_ERR_ARG";
     case LOGO_ERR_WORKSPACE: return "LOGO_ERR_WORKSPACE";
     case LOGO_ERR_HIP: return "LOGO_ERR_HIP";
+    case LOGO_ERR_SCRATCH_LIMIT: return "LOGO_ERR_SCRATCH_LIMIT";
     }
     return "LOGO_ERR_UNKNOWN";
 }
@@ -769,12 +800,19 @@ logo_status logo_dense_causal_attn_fwd_train(const logo_problem *p, const logo_b
     return hip_status(launch_attention(kModeDense, kEpiRaw, p->head_dim, a, (int)grid, s), s);
 }
 
-logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
-                        const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
-                        const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
-                        float threshold, const float *thr_dev, const float *gain_local,
-                        const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
-                        int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream) {
+}  // extern "C"
+
+namespace {
+
+// One decoding step.  noalloc: the scratch is the library's fixed device
+// array (ws and ws_bytes are ignored), after the same argument checks.
+logo_status decode_run(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                       const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                       const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                       float threshold, const float *thr_dev, const float *gain_local,
+                       const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
+                       int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream,
+                       bool noalloc) {
     logo_status st = check_problem(p);
     if (st != LOGO_OK)
         return st;
@@ -800,6 +838,13 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
     const DecodePlan d = decode_plan(p);
     if (d.n_local_items + d.n_global_items >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
+    if (noalloc) {
+        if (d.total > (size_t)LOGO_NOALLOC_SCRATCH_BYTES)
+            return LOGO_ERR_SCRATCH_LIMIT;
+        if ((st = device_scratch(&ws)) != LOGO_OK)
+            return st;
+        ws_bytes = (size_t)LOGO_NOALLOC_SCRATCH_BYTES;
+    }
     st = check_ws(ws, ws_bytes, d.total);
     if (st != LOGO_OK)
         return st;
@@ -842,6 +887,30 @@ logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf
     a.thr_dev = thr_dev;
     hipStream_t s = (hipStream_t)stream;
     return hip_status(launch_decode(a, s), s);
+}
+
+}  // namespace
+
+extern "C" {
+
+logo_status logo_decode(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                        const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                        const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                        float threshold, const float *thr_dev, const float *gain_local,
+                        const float *gain_global, float eps, logo_bf16 *out, int32_t *active,
+                        int32_t *n_active, void *ws, size_t ws_bytes, logo_stream stream) {
+    return decode_run(p, q, k, v, q_g, k_g, v_g, gate, mode, threshold, thr_dev, gain_local,
+                      gain_global, eps, out, active, n_active, ws, ws_bytes, stream, false);
+}
+
+logo_status logo_decode_noalloc(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                                const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
+                                const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                                float threshold, const float *thr_dev, const float *gain_local,
+                                const float *gain_global, float eps, logo_bf16 *out,
+                                int32_t *active, int32_t *n_active, logo_stream stream) {
+    return decode_run(p, q, k, v, q_g, k_g, v_g, gate, mode, threshold, thr_dev, gain_local,
+                      gain_global, eps, out, active, n_active, nullptr, 0, stream, true);
 }
 
 logo_status logo_gate_proj(int64_t n_tokens, int32_t d_model, const logo_bf16 *x,

@@ -11,7 +11,8 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "logo.h")
 
-OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_ARG, ERR_WORKSPACE, ERR_HIP = range(7)
+OK, ERR_NULL, ERR_SHAPE, ERR_UNSUPPORTED, ERR_ARG, ERR_WORKSPACE, ERR_HIP, ERR_SCRATCH_LIMIT = \
+    range(8)
 
 
 @pytest.fixture(scope="module")
@@ -40,6 +41,7 @@ def test_status_strings_and_version(lib):
     import paper_2608_29539_amd as pk
     assert pk.logo_status_str(0) == "LOGO_OK"
     assert pk.logo_status_str(5) == "LOGO_ERR_WORKSPACE"
+    assert pk.logo_status_str(7) == "LOGO_ERR_SCRATCH_LIMIT"
     assert pk.logo_version().count(".") == 2
 
 
@@ -194,6 +196,24 @@ def test_device_threshold_mode_needs_thr_out(lib):
     ws_need = lib.logo_workspace_bytes(p.c, 0, 0)
     assert lib.logo_select(p.c, FAKE, 2, 0.0, 0.0, FAKE, 150, FAKE, None, None, FAKE, ws_need,
                            None) == ERR_NULL
+
+
+def test_decode_noalloc_validation(lib):
+    """logo_decode_noalloc checks its arguments as logo_decode does, and
+    refuses a step whose scratch exceeds the fixed array, before any HIP
+    call (64 caches of 32K tokens, 32 / 8 heads of d = 128: ~70 MB)."""
+    f = lib.logo_decode_noalloc
+    p = Prob(seqlens=(100, 50), hq=8, hkv=2, d=128, window=16)
+    assert f(p.c, None, FAKE, FAKE, None, None, None, FAKE, 0, 0.5, None, None, None, 1e-6,
+             FAKE, None, None, None) == ERR_NULL
+    assert f(p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 0, float("nan"), None, None, None,
+             1e-6, FAKE, None, None, None) == ERR_ARG
+    assert f(p.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 1, 0.5, None, None, None, 1e-6,
+             FAKE, None, None, None) == ERR_ARG          # ratio mode: not for decoding
+    big = Prob(seqlens=(32768,) * 64, hq=32, hkv=8, d=128, window=1024)
+    assert lib.logo_workspace_bytes(big.c, 6, 0) > (64 << 20)
+    assert f(big.c, FAKE, FAKE, FAKE, None, None, None, FAKE, 0, 0.5, None, None, None, 1e-6,
+             FAKE, None, None, None) == ERR_SCRATCH_LIMIT
 
 
 def test_decode_validation(lib):
