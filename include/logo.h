@@ -78,7 +78,8 @@ typedef enum {
     LOGO_ENTRY_FWD_TRAIN = 7,
     LOGO_ENTRY_BWD = 8,
     LOGO_ENTRY_DENSE_BWD = 9,
-    LOGO_ENTRY_GLOBAL_BWD = 10
+    LOGO_ENTRY_GLOBAL_BWD = 10,
+    LOGO_ENTRY_FWD_QPHI = 11
 } logo_entry;
 
 /* Problem description (a host struct; only cu_seqlens is a device pointer). */
@@ -486,6 +487,37 @@ logo_status logo_branch_transform(int64_t n_tokens, int32_t num_heads, int32_t h
                                   const float *s, const float *b, const int32_t *rows,
                                   int64_t n_rows, const int32_t *n_rows_dev, logo_bf16 *u_g,
                                   logo_stream stream);
+
+/*
+ * logo_attn_fwd_qphi -- logo_attn_fwd whose global-branch queries are the
+ * lightweight branch transform of the local ones (Sec. 3.2, Eq.
+ * branch-transform), applied by the query-sparse attention kernel to the
+ * selected rows only, as it loads them: q^G = q A_h (LP: bf16 products
+ * accumulated in fp32) or q * s_h + b_h (SO: fp32), one bf16 rounding -- the
+ * values logo_branch_transform writes (up to the fp32 summation order of
+ * LP).  No Q^G tensor is written or read.
+ *   q_phi      LOGO_PHI_LP (A: device [Hq][d][d] bf16, row c of A[h] maps
+ *              channel c to the output channels; s, b ignored) or
+ *              LOGO_PHI_SO (s, b: device [Hq][d] fp32; A ignored); anything
+ *              else is LOGO_ERR_ARG, a missing operand LOGO_ERR_NULL.
+ *   k_g, v_g   the global branch's keys / values (e.g. from
+ *              logo_branch_transform, which runs once per token for them), or
+ *              NULL for k / v.
+ *   Everything else as for logo_attn_fwd (there is no q_g argument).
+ *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD_QPHI, sel_capacity) bytes,
+ *   256-byte aligned: LOGO_ENTRY_FWD's workspace plus, for LP, a permuted
+ *   copy of A (2 Hq d^2 bytes) that the local-branch launch writes for the
+ *   global one.
+ */
+logo_status logo_attn_fwd_qphi(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                               const logo_bf16 *v, logo_phi_kind q_phi, const logo_bf16 *A,
+                               const float *s, const float *b, const logo_bf16 *k_g,
+                               const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                               float threshold, double ratio, const float *gain_local,
+                               const float *gain_global, float eps, logo_bf16 *out,
+                               int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                               int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                               logo_stream stream);
 
 /*
  * logo_budget_update -- one step of the global-budget controller

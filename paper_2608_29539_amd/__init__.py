@@ -14,6 +14,7 @@ from .binding import (  # noqa: F401
     LOGO_ENTRY_DENSE,
     LOGO_ENTRY_DENSE_BWD,
     LOGO_ENTRY_FWD,
+    LOGO_ENTRY_FWD_QPHI,
     LOGO_ENTRY_FWD_TRAIN,
     LOGO_ENTRY_GLOBAL,
     LOGO_ENTRY_GLOBAL_BWD,
@@ -31,6 +32,7 @@ from .binding import (  # noqa: F401
     library_path,
     logo_attn_bwd,
     logo_attn_fwd,
+    logo_attn_fwd_qphi,
     logo_attn_fwd_train,
     logo_branch_transform,
     logo_budget_update,

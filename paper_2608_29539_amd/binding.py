@@ -29,6 +29,7 @@ LOGO_ENTRY_FWD_TRAIN = 7
 LOGO_ENTRY_BWD = 8
 LOGO_ENTRY_DENSE_BWD = 9
 LOGO_ENTRY_GLOBAL_BWD = 10
+LOGO_ENTRY_FWD_QPHI = 11
 LOGO_PHI_LP = 0
 LOGO_PHI_SO = 1
 
@@ -40,7 +41,7 @@ EXPORTS = (
     "logo_pmask_initial_threshold", "logo_decode", "logo_gate_proj", "logo_branch_transform",
     "logo_attn_fwd_train", "logo_attn_bwd", "logo_dense_causal_attn_fwd_train",
     "logo_dense_causal_attn_bwd", "logo_global_attn_sparse_q_fwd_train",
-    "logo_global_attn_sparse_q_bwd", "logo_decode_noalloc",
+    "logo_global_attn_sparse_q_bwd", "logo_decode_noalloc", "logo_attn_fwd_qphi",
 )
 
 _lib = None
@@ -89,6 +90,8 @@ def library():
         "logo_local_attn": [PP, P, P, P, P, P],
         "logo_global_attn_sparse_q": [PP, P, P, P, P, P, i32, P, P, sz, P],
         "logo_combine": [PP, P, P, P, P, P, P, f32, ctypes.c_int, P, P],
+        "logo_attn_fwd_qphi": [PP, P, P, P, i32, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P,
+                               P, i32, P, P, P, P, sz, P],
         "logo_attn_fwd": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32, P, P,
                           P, P, sz, P],
         "logo_attn_fwd_profiled": [PP, P, P, P, P, P, P, P, i32, f32, f64, P, P, f32, P, P, i32,
@@ -386,6 +389,60 @@ def logo_attn_fwd(prob: Problem, q, k, v, gate, *, ratio: Optional[float] = None
             raise ValueError("events: five torch.cuda.Event objects")
         handles = (ctypes.c_void_p * 5)(*[ctypes.c_void_p(e.cuda_event) for e in events])
         _call("logo_attn_fwd_profiled", *args, handles)
+    return out, sel_idx, cu_sel, tok2sel, thr_out
+
+
+def logo_attn_fwd_qphi(prob: Problem, q, k, v, gate, q_phi: int, *, A=None, s=None, b=None,
+                       ratio: Optional[float] = None, threshold: Optional[float] = None,
+                       threshold_device=None, k_g=None, v_g=None, gain_local=None,
+                       gain_global=None, eps: float = 1e-6, out=None,
+                       sel_capacity: Optional[int] = None, sel_idx=None, cu_sel=None,
+                       tok2sel=None, thr_out=None, ws=None):
+    """The layer with the global branch's queries transformed inside the
+    query-sparse kernel: ``q_phi`` LOGO_PHI_LP with ``A`` [Hq, d, d] bf16, or
+    LOGO_PHI_SO with ``s``, ``b`` [Hq, d] float32.  Returns (out, sel_idx,
+    cu_sel, tok2sel, thr_out)."""
+    import torch
+    N, Hq, Hkv, d, B = (prob.total_tokens, prob.num_q_heads, prob.num_kv_heads, prob.head_dim,
+                        prob.num_seqs)
+    mode, thr_dev = _sel_mode(ratio, threshold, threshold_device, B)
+    if thr_dev is not None:
+        thr_out = thr_dev
+    dev = q.device
+    _check(q, torch.bfloat16, (N, Hq, d), "q")
+    _check(k, torch.bfloat16, (N, Hkv, d), "k")
+    _check(v, torch.bfloat16, (N, Hkv, d), "v")
+    for t, nm in ((k_g, "k_g"), (v_g, "v_g")):
+        if t is not None:
+            _check(t, torch.bfloat16, (N, Hkv, d), nm)
+    if q_phi == LOGO_PHI_LP:
+        _check(A, torch.bfloat16, (Hq, d, d), "A")
+    elif q_phi == LOGO_PHI_SO:
+        _check(s, torch.float32, (Hq, d), "s")
+        _check(b, torch.float32, (Hq, d), "b")
+    else:
+        raise ValueError("q_phi: LOGO_PHI_LP or LOGO_PHI_SO")
+    _check(gate, torch.float32, (N,), "gate")
+    if sel_capacity is None:
+        sel_capacity = logo_ratio_capacity(prob, ratio) if ratio is not None else N
+    if sel_idx is None:
+        sel_idx = torch.empty(max(sel_capacity, 1), dtype=torch.int32, device=dev)
+    if cu_sel is None:
+        cu_sel = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    if tok2sel is None:
+        tok2sel = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    if thr_out is None:
+        thr_out = torch.empty(B, dtype=torch.float32, device=dev)
+    if out is None:
+        out = torch.empty((N, Hq, d), dtype=torch.bfloat16, device=dev)
+    _check(out, torch.bfloat16, (N, Hq, d), "out")
+    ws, nbytes = _ws(prob, LOGO_ENTRY_FWD_QPHI, max(sel_capacity, 1), ws)
+    _call("logo_attn_fwd_qphi", prob.c, _ptr(q), _ptr(k), _ptr(v), int(q_phi), _ptr(A), _ptr(s),
+          _ptr(b), _ptr(k_g), _ptr(v_g), _ptr(gate), mode,
+          float(threshold if threshold is not None else 0.0),
+          float(ratio if ratio is not None else 0.0), _ptr(gain_local), _ptr(gain_global),
+          float(eps), _ptr(out), _ptr(sel_idx), int(max(sel_capacity, 1)), _ptr(cu_sel),
+          _ptr(tok2sel), _ptr(thr_out), _ptr(ws), nbytes, _stream())
     return out, sel_idx, cu_sel, tok2sel, thr_out
 
 

@@ -224,19 +224,129 @@ __device__ __forceinline__ bool merge_split(const AttnArgs &a, const SparseTile 
     return true;
 }
 
+// Wave-uniform state of one work item.
+struct ItemU {
+    int b, hg, T, nvalid, wg_pmin, wg_pmax, head, kvh;
+    int64_t base;
+    int kb_lo, kb_hi, kb_first, kb_last, wpmin, wpmax;
+    bool wave_valid;
+    SparseTile tile;
+};
+// This lane's query rows of one item (one per row group) and the inputs of
+// the fused epilogue; rows past the tile end repeat the last row and are
+// never stored.
+struct ItemL {
+    int pos[RG];
+    int64_t orow[RG], qtok[RG];
+    bool row_valid[RG];
+    float ep_gate[RG];
+    int ep_rank[RG];
+};
+
+// Column of the LP matrix that row r of its permuted copy holds: bits 2 and 3
+// of r (within its 32-row block) swapped.  With A'[h][r][k] = A[h][k][perm(r)]
+// as the A operand of the 32x32x16 MFMA and a lane's Q fragments as the B
+// operand, accumulator element 8 j + e of lane (g, m) is output channel
+// 16 j + 8 g + e of its 32-channel block for query row m -- the layout of the
+// B operand of the next product, so the rounded result replaces the
+// fragments directly.
+__device__ __forceinline__ int lp_perm(int r) { return (r & ~0xC) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+// Q^G = phi(Q) on the selected rows as the global kernel loads them (Eq.
+// branch-transform): LP q A_h (bf16 MFMA, fp32 accumulation) or SO
+// q * s_h + b_h (fp32), one bf16 rounding each.
+template <int D>
+__device__ __forceinline__ void apply_qphi(const AttnArgs &a, int head,
+                                           bf16x8 (&qf)[RG][D / 16]) {
+    const int lane = threadIdx.x & 63, g = lane >> 5, m = lane & 31;
+    if (a.qphi == 1) {
+        const uint16_t *ap = a.aperm + (int64_t)head * D * D;
+        bf16x8 qn[RG][D / 16];
+#pragma unroll
+        for (int cb = 0; cb < D / 32; cb++) {
+            f32x16 c[RG];
+#pragma unroll
+            for (int rg = 0; rg < RG; rg++)
+                c[rg] = f32x16{};
+#pragma unroll
+            for (int ks = 0; ks < D / 16; ks++) {
+                const bf16x8 af = *(const bf16x8 *)(ap + (cb * 32 + m) * D + ks * 16 + g * 8);
+#pragma unroll
+                for (int rg = 0; rg < RG; rg++)
+                    c[rg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, qf[rg][ks], c[rg], 0, 0, 0);
+            }
+#pragma unroll
+            for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                for (int h = 0; h < 2; h++)
+#pragma unroll
+                    for (int e = 0; e < 8; e += 2) {
+                        const bf16x2 v = cvt_bf16x2(c[rg][8 * h + e], c[rg][8 * h + e + 1]);
+                        qn[rg][2 * cb + h][e] = v[0];
+                        qn[rg][2 * cb + h][e + 1] = v[1];
+                    }
+        }
+#pragma unroll
+        for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+            for (int ks = 0; ks < D / 16; ks++)
+                qf[rg][ks] = qn[rg][ks];
+    } else if (a.qphi == 2) {
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ks++) {
+            const int c0 = head * D + ks * 16 + g * 8;
+            const f32x4 s0 = *(const f32x4 *)(a.qphi_s + c0), s1 = *(const f32x4 *)(a.qphi_s + c0 + 4);
+            const f32x4 b0 = *(const f32x4 *)(a.qphi_b + c0), b1 = *(const f32x4 *)(a.qphi_b + c0 + 4);
+            const float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+            const float bv[8] = {b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]};
+#pragma unroll
+            for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    const bf16x2 v = cvt_bf16x2(fmaf((float)qf[rg][ks][e], sv[e], bv[e]),
+                                                fmaf((float)qf[rg][ks][e + 1], sv[e + 1], bv[e + 1]));
+                    qf[rg][ks][e] = v[0];
+                    qf[rg][ks][e + 1] = v[1];
+                }
+        }
+    }
+}
+
+// The permuted copy of one head's LP matrix (see lp_perm), 16 bytes per
+// thread and step: A'[r][k0 .. k0+7] gathers column lp_perm(r) of rows
+// k0 .. k0+7 of A.
+template <int D, int NT>
+__device__ __forceinline__ void permute_lp_head(const uint16_t *A, uint16_t *Ap, int head) {
+    const uint16_t *src = A + (int64_t)head * D * D;
+    uint16_t *dst = Ap + (int64_t)head * D * D;
+    for (int c = threadIdx.x; c < D * D / 8; c += NT) {
+        const int r = c / (D / 8), k0 = (c % (D / 8)) * 8;
+        const uint16_t *sc = src + k0 * D + lp_perm(r);
+        auto pair = [&](int e) { return (uint32_t)sc[e * D] | ((uint32_t)sc[(e + 1) * D] << 16); };
+        *(u32x4 *)(dst + r * D + k0) = u32x4{pair(0), pair(2), pair(4), pair(6)};
+    }
+}
+
+// An item's indices and rows, and the loads of its Q fragments and fused-
+// epilogue inputs (issued here; waited for with the item's first K tile).
+//   Local / dense: tile jt of sequence b, rows = tokens jt*tpw ...
+//   Global: rows = sel_idx[first .. first+nrows), all in sequence b.
 template <int D, int MODE, int EPI>
-__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int b, int hg,
-                                            int jt, SparseTile tile) {
+__device__ __forceinline__ void item_begin(const AttnArgs &a, int b, int hg, int jt,
+                                           SparseTile tile, ItemU &u, ItemL &l,
+                                           bf16x8 (&qf)[RG][D / 16]) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);
     const int g = lane >> 5, m = lane & 31;
-    b = uni(b);
-    hg = uni(hg);
+    u.b = b = uni(b);
+    u.hg = hg = uni(hg);
     const int64_t base = uni(a.cu_seqlens[b]);
     const int T = uni(a.cu_seqlens[b + 1] - (int)base);
+    u.base = base;
+    u.T = T;
     const int hw = wave % a.hpw, tb = wave / a.hpw;
-    const int head = hg * a.hpw + hw;
-    const int kvh = (hg * a.hpw) / a.group;
+    u.head = hg * a.hpw + hw;
+    u.kvh = (hg * a.hpw) / a.group;
 
     int nvalid, wg_pmin, wg_pmax;
     if (MODE == kModeGlobal) {
@@ -250,51 +360,107 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         wg_pmin = p0;
         wg_pmax = p0 + nvalid - 1;
     }
-    // This lane's query rows (one per row group); rows past the tile end
-    // repeat the last row and are never stored.
-    int pos[RG];
-    int64_t orow[RG], qtok[RG];
-    bool row_valid[RG];
+    u.tile = tile;
+    u.nvalid = nvalid;
+    u.wg_pmin = wg_pmin;
+    u.wg_pmax = wg_pmax;
 #pragma unroll
     for (int rg = 0; rg < RG; rg++) {
         const int ri = tb * kRowsPerWave + rg * 32 + m;
-        row_valid[rg] = ri < nvalid;
-        const int ric = row_valid[rg] ? ri : nvalid - 1;
+        l.row_valid[rg] = ri < nvalid;
+        const int ric = l.row_valid[rg] ? ri : nvalid - 1;
         if (MODE == kModeGlobal) {
             const int rank = tile.first + ric;
-            pos[rg] = a.sel_idx[rank] - (int)base;
-            orow[rg] = rank;
+            l.pos[rg] = a.sel_idx[rank] - (int)base;
+            l.orow[rg] = rank;
         } else {
-            pos[rg] = wg_pmin + ric;
-            orow[rg] = base + pos[rg];
+            l.pos[rg] = wg_pmin + ric;
+            l.orow[rg] = base + l.pos[rg];
         }
-        qtok[rg] = base + pos[rg];
+        l.qtok[rg] = base + l.pos[rg];
     }
-    const bool wave_valid = tb * kRowsPerWave < nvalid;
-    const int wpmin = __builtin_amdgcn_readfirstlane(pos[0]);
-    const int wpmax = __builtin_amdgcn_readlane(pos[RG - 1], 31);
+    u.wave_valid = tb * kRowsPerWave < nvalid;
+    u.wpmin = __builtin_amdgcn_readfirstlane(l.pos[0]);
+    u.wpmax = __builtin_amdgcn_readlane(l.pos[RG - 1], 31);
 
-    bf16x8 qf[RG][D / 16];
 #pragma unroll
     for (int rg = 0; rg < RG; rg++) {
-        const uint16_t *qp = a.q + (qtok[rg] * a.hq + head) * (int64_t)D + g * 8;
+        const uint16_t *qp = a.q + (l.qtok[rg] * a.hq + u.head) * (int64_t)D + g * 8;
 #pragma unroll
         for (int s = 0; s < D / 16; s++)
             qf[rg][s] = *(const bf16x8 *)(qp + s * 16);
     }
+    if constexpr (MODE == kModeGlobal && EPI != kEpiRaw)
+        if (a.qphi != 0)
+            apply_qphi<D>(a, u.head, qf);
     // Inputs of the fused epilogue, fetched now so that their latency overlaps
     // the KV loop.
-    float ep_gate[RG];
-    int ep_rank[RG];
 #pragma unroll
     for (int rg = 0; rg < RG; rg++) {
-        ep_gate[rg] = 0.f;
-        ep_rank[rg] = -1;
+        l.ep_gate[rg] = 0.f;
+        l.ep_rank[rg] = -1;
         if (EPI != kEpiRaw && MODE != kModeDense) {
-            ep_gate[rg] = a.gate[qtok[rg]];
-            ep_rank[rg] = (MODE == kModeGlobal) ? (int)orow[rg] : a.tok2sel[qtok[rg]];
+            l.ep_gate[rg] = a.gate[l.qtok[rg]];
+            l.ep_rank[rg] = (MODE == kModeGlobal) ? (int)l.orow[rg] : a.tok2sel[l.qtok[rg]];
         }
     }
+
+    const int w = a.window;
+    const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
+    // KV blocks of this item: a global entry covers its own KV range
+    u.kb_lo = (MODE == kModeGlobal) ? uni(tile.kb_begin) : lo / kBlockN;
+    u.kb_hi = (MODE == kModeGlobal) ? uni(tile.kb_end) : wg_pmax / kBlockN;
+    // Tiles this wave computes: a contiguous, wave-uniform sub-range.
+    u.kb_first = u.kb_lo;
+    u.kb_last = min(u.wpmax / kBlockN, u.kb_hi);
+    if (MODE == kModeLocal)
+        u.kb_first = max(u.kb_lo, max(0, u.wpmin - w + 1) / kBlockN);
+    if (!u.wave_valid) {
+        u.kb_first = u.kb_hi + 1;
+        u.kb_last = u.kb_hi;
+    }
+}
+
+// The first K tile of an item into K buffer 0 (the K/V pipeline of attend_item
+// starts from it); every earlier read of K buffer 0 must have ended at a
+// barrier before this.
+template <int D, int W>
+__device__ __forceinline__ void item_first_k(const AttnArgs &a, Smem<D> &sm, const ItemU &u) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uni(tid >> 6);
+    const int row_bytes = a.hkv * D * 2;
+    Dma<D, W> dma;
+    dma_plan<D, W>(dma, wave, lane, row_bytes);
+    const uint16_t *kv_k = a.k + (u.base * a.hkv + u.kvh) * (int64_t)D;
+    dma_k<D, W>(&sm.k[0][0][0], dma, kv_k, u.T, u.kb_lo * kBlockN, row_bytes, wave);
+}
+
+// Attention for one work item whose item_begin loads and first K tile are in
+// flight.  prefetch() runs once every wave has passed the barrier after the
+// item's last K / V tile step -- the K buffers and qf are then free -- and
+// before the item's last PV product and epilogue, so the next item's loads
+// overlap them.
+template <int D, int MODE, int EPI, int W, class Prefetch>
+__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, const ItemU &u,
+                                            const ItemL &l, bf16x8 (&qf)[RG][D / 16],
+                                            Prefetch &&prefetch) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uni(tid >> 6);
+    const int g = lane >> 5, m = lane & 31;
+    const int64_t base = u.base;
+    const int T = u.T;
+    const int head = u.head, kvh = u.kvh;
+    const SparseTile &tile = u.tile;
+    const int wpmin = u.wpmin, wpmax = u.wpmax;
+    const bool wave_valid = u.wave_valid;
+    const int kb_lo = u.kb_lo, kb_hi = u.kb_hi;
+    const int kb_first = u.kb_first, kb_last = u.kb_last;
+    const int(&pos)[RG] = l.pos;
+    const int64_t(&orow)[RG] = l.orow;
+    const int64_t(&qtok)[RG] = l.qtok;
+    const bool(&row_valid)[RG] = l.row_valid;
+    const float(&ep_gate)[RG] = l.ep_gate;
+    const int(&ep_rank)[RG] = l.ep_rank;
 
     // Lane's row / column inside a V tile for the transpose reads.
     const int vt_row = 4 * g + ((lane & 15) >> 2);
@@ -307,18 +473,6 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
         vt_scol[cb] = (cb ^ vswz<D>(vt_row)) * 32 + vt_col;
 
     const int w = a.window;
-    const int lo = (MODE == kModeLocal) ? max(0, wg_pmin - w + 1) : 0;
-    // KV blocks of this item: a global entry covers its own KV range
-    const int kb_lo = (MODE == kModeGlobal) ? uni(tile.kb_begin) : lo / kBlockN;
-    const int kb_hi = (MODE == kModeGlobal) ? uni(tile.kb_end) : wg_pmax / kBlockN;
-    // Tiles this wave computes: a contiguous, wave-uniform sub-range.
-    int kb_first = kb_lo, kb_last = min(wpmax / kBlockN, kb_hi);
-    if (MODE == kModeLocal)
-        kb_first = max(kb_lo, max(0, wpmin - w + 1) / kBlockN);
-    if (!wave_valid) {
-        kb_first = kb_hi + 1;
-        kb_last = kb_hi;
-    }
     const float c = a.scale_log2;
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
@@ -327,7 +481,6 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     const int row_bytes = a.hkv * D * 2;
     const uint16_t *kv_k = a.k + (base * a.hkv + kvh) * (int64_t)D;
     const uint16_t *kv_v = a.v + (base * a.hkv + kvh) * (int64_t)D;
-    constexpr int W = waves_of(MODE);
     Dma<D, W> dma;
     dma_plan<D, W>(dma, wave, lane, row_bytes);
 
@@ -353,11 +506,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     f32x16 s[RG][2];                          // S of the tile being softmax-ed
     auto kidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
     auto vidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
-    __syncthreads();                         // the previous item's last tile is consumed
-    dma_k<D, W>(&sm.k[0][0][0], dma, kv_k, T, kb_lo * kBlockN, row_bytes, wave);
-    // This wait also covers the Q (and epilogue input) loads: inside the loop
-    // the only vector-memory loads in flight are the K/V tile loads, which
-    // the compiler does not track.
+    // The item's first K tile (buffer 0) and its Q and epilogue-input loads
+    // are in flight; this wait covers all of them: inside the loop the only
+    // vector-memory loads in flight are the K/V tile loads, which the
+    // compiler does not track.  The barrier also ends every wave's reads of
+    // the previous item's last V tile before this item's first V load.
     dma_wait_barrier();
 
     // Loads of step kb: K(kb+1) and V(kb).
@@ -582,6 +735,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     }
     for (; kb <= kb_hi; kb++)
         step(kb, F_{}, F_{}, MNone{});
+    prefetch();
     if (pending) {
         apply_rescale();
         pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step
@@ -594,7 +748,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     if constexpr (MODE == kModeGlobal) {
         // a split entry: publish the partial, and the last of the tile's
         // entries to finish merges all of them and runs the epilogue
-        if (uni(tile.nsplit) > 1 && !merge_split<D>(a, tile, hg, wave, lane, acc, m_ref, l_tot))
+        if (uni(tile.nsplit) > 1 && !merge_split<D>(a, tile, u.hg, wave, lane, acc, m_ref, l_tot))
             return;
     }
 #pragma unroll
@@ -706,10 +860,11 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, int 
     }
 }
 
-template <int D, int MODE, int EPI>
-__global__ __launch_bounds__(waves_of(MODE) * 64) __attribute__((amdgpu_waves_per_eu(2)))
+template <int D, int MODE, int EPI, int W>
+__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
     __shared__ Smem<D> sm;
+    auto no_prefetch = [] {};
     if (MODE == kModeGlobal) {
         // Persistent workgroups pull (tile, head group) items from the queue
         // of their XCD (workgroups are dispatched round-robin over the 8
@@ -759,109 +914,163 @@ void attn_kernel(const AttnArgs a) {
                 if (lane == 0)
                     s_item = item;
             }
+            // (these barriers also end every read of the previous item's
+            // K / V tiles before the next item's first K tile load)
             __syncthreads();
             const int item = __builtin_amdgcn_readfirstlane(s_item);
             __syncthreads();
             if (item < 0)
                 break;
             const SparseTile t = a.tiles[item / a.n_hg];
-            attend_item<D, MODE, EPI>(a, sm, t.seq, item % a.n_hg, 0, t);
+            ItemU u;
+            ItemL l;
+            bf16x8 qf[RG][D / 16];
+            item_begin<D, MODE, EPI>(a, t.seq, item % a.n_hg, 0, t, u, l, qf);
+            item_first_k<D, W>(a, sm, u);
+            attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, no_prefetch);
         }
-    } else {
-        int bid = blockIdx.x;
-        if constexpr (MODE == kModeLocal && EPI != kEpiRaw) {
+    } else if (MODE == kModeLocal) {
+        int wid = blockIdx.x;
+        if constexpr (EPI != kEpiRaw) {
             // The fused layer's local launch: workgroup 0 builds the global
             // branch's work table (its LDS holds the table), the rest attend.
             if (a.plan_wg) {
-                if (bid == 0) {
+                if (wid == 0) {
                     constexpr int E = D == 128 ? 512 : 256;
                     static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D>),
                                   "plan table must fit in the K/V staging buffers");
-                    build_plan<waves_of(MODE) * 64, E>(
-                        a.cu_seqlens, a.num_seqs, a.plan,
-                        *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
+                    build_plan<W * 64, E>(a.cu_seqlens, a.num_seqs, a.plan,
+                                          *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
                     return;
                 }
-                bid -= 1;
+                wid -= 1;
             }
+            // then, for a global branch with an LP query transform, one
+            // workgroup per head writes the permuted copy of its matrix
+            if (wid < a.prep_wgs) {
+                permute_lp_head<D, W * 64>(a.prep_a, a.aperm, wid);
+                return;
+            }
+            wid -= a.prep_wgs;
         }
-        const int hg = bid % a.n_hg;
-        int rest = bid / a.n_hg;
-        int b, jt;
-        if (MODE == kModeLocal) {
-            // the sequences' tiles back to back (a jt-major grid over the
-            // longest sequence left most workgroups of a ragged batch idle)
-            b = 0;
-            for (; b < a.num_seqs; b++) {
+        // Persistent workgroups: items wid, wid + stride, ...  Item i is head
+        // group i % n_hg of token tile i / n_hg, the sequences' tiles back to
+        // back (so no workgroup of a ragged batch idles); the valid items are
+        // a prefix, so the first invalid one ends the loop.
+        auto decode = [&](int item, int &b, int &hg, int &jt) {
+            if (item >= a.n_items)
+                return false;
+            hg = item % a.n_hg;
+            int rest = item / a.n_hg;
+            for (b = 0; b < a.num_seqs; b++) {
                 const int nt = (a.cu_seqlens[b + 1] - a.cu_seqlens[b] + a.tpw - 1) / a.tpw;
                 if (rest < nt)
                     break;
                 rest -= nt;
             }
-            if (b >= a.num_seqs)
-                return;
             jt = rest;
-        } else {
-            b = rest % a.num_seqs;
-            jt = rest / a.num_seqs;
-            if (MODE == kModeDense)
-                jt = a.ntile_max - 1 - jt;       // longest rows first
+            return b < a.num_seqs;
+        };
+        int item = wid, b = 0, hg = 0, jt = 0;
+        if (!decode(item, b, hg, jt))
+            return;
+        ItemU u;
+        ItemL l;
+        bf16x8 qf[RG][D / 16];
+        item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
+        item_first_k<D, W>(a, sm, u);
+        for (;;) {
+            // The next item's Q, epilogue inputs and first K tile are loaded
+            // while this item finishes its last PV product and epilogue.
+            const int next = item + a.item_stride;
+            int nb = 0, nhg = 0, njt = 0;
+            const bool has_next = decode(next, nb, nhg, njt);
+            ItemU nu;
+            ItemL nl;
+            attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, [&] {
+                if (has_next) {
+                    item_begin<D, MODE, EPI>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
+                    item_first_k<D, W>(a, sm, nu);
+                }
+            });
+            if (!has_next)
+                break;
+            u = nu;
+            l = nl;
+            item = next;
         }
+    } else {
+        const int bid = blockIdx.x;
+        const int hg = bid % a.n_hg;
+        const int rest = bid / a.n_hg;
+        const int b = rest % a.num_seqs;
+        const int jt = a.ntile_max - 1 - rest / a.num_seqs;       // longest rows first
         const int T = a.cu_seqlens[b + 1] - a.cu_seqlens[b];
         if (jt * a.tpw >= T)
             return;
-        attend_item<D, MODE, EPI>(a, sm, b, hg, jt, SparseTile{0, 0, 0, 0});
+        ItemU u;
+        ItemL l;
+        bf16x8 qf[RG][D / 16];
+        item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
+        item_first_k<D, W>(a, sm, u);
+        attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, no_prefetch);
     }
 }
 
-template <int D, int MODE, int EPI>
+template <int D, int MODE, int EPI, int W>
 hipError_t launch_one(const AttnArgs &a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((attn_kernel<D, MODE, EPI>), dim3(grid), dim3(waves_of(MODE) * 64), 0, s, a);
+    hipLaunchKernelGGL((attn_kernel<D, MODE, EPI, W>), dim3(grid), dim3(W * 64), 0, s, a);
     return hipGetLastError();
 }
 
-template <int D, int MODE>
+template <int D, int MODE, int W>
 int blocks_per_cu_one() {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE, kEpiRaw>,
-                                                     waves_of(MODE) * 64,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, attn_kernel<D, MODE, kEpiRaw, W>, W * 64,
                                                      0) != hipSuccess)
         return 1;
     return n > 0 ? n : 1;
 }
 
+template <int D, int MODE, int W>
+hipError_t launch_epi(int epi, const AttnArgs &a, int grid, hipStream_t s) {
+    return epi == kEpiFused        ? launch_one<D, MODE, kEpiFused, W>(a, grid, s)
+           : epi == kEpiFusedTrain ? launch_one<D, MODE, kEpiFusedTrain, W>(a, grid, s)
+                                   : launch_one<D, MODE, kEpiRaw, W>(a, grid, s);
+}
+
 template <int D>
-hipError_t launch_d(int mode, int epi, const AttnArgs &a, int grid, hipStream_t s) {
+hipError_t launch_d(int mode, int epi, int waves, const AttnArgs &a, int grid, hipStream_t s) {
     if (mode == kModeLocal)
-        return epi == kEpiFused      ? launch_one<D, kModeLocal, kEpiFused>(a, grid, s)
-               : epi == kEpiFusedTrain ? launch_one<D, kModeLocal, kEpiFusedTrain>(a, grid, s)
-                                       : launch_one<D, kModeLocal, kEpiRaw>(a, grid, s);
+        return waves == 8 ? launch_epi<D, kModeLocal, 8>(epi, a, grid, s)
+                          : launch_epi<D, kModeLocal, kWavesLocal>(epi, a, grid, s);
     if (mode == kModeGlobal)
-        return epi == kEpiFused      ? launch_one<D, kModeGlobal, kEpiFused>(a, grid, s)
-               : epi == kEpiFusedTrain ? launch_one<D, kModeGlobal, kEpiFusedTrain>(a, grid, s)
-                                       : launch_one<D, kModeGlobal, kEpiRaw>(a, grid, s);
-    return launch_one<D, kModeDense, kEpiRaw>(a, grid, s);
+        return launch_epi<D, kModeGlobal, kWavesGlobal>(epi, a, grid, s);
+    return launch_one<D, kModeDense, kEpiRaw, kWavesGlobal>(a, grid, s);
+}
+
+template <int D>
+int blocks_per_cu_d(int mode, int waves) {
+    if (mode == kModeLocal)
+        return waves == 8 ? blocks_per_cu_one<D, kModeLocal, 8>()
+                          : blocks_per_cu_one<D, kModeLocal, kWavesLocal>();
+    if (mode == kModeGlobal)
+        return blocks_per_cu_one<D, kModeGlobal, kWavesGlobal>();
+    return blocks_per_cu_one<D, kModeDense, kWavesGlobal>();
 }
 
 }  // namespace
 
-hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, int grid,
-                            hipStream_t s) {
+hipError_t launch_attention(int mode, int epi, int head_dim, int waves, const AttnArgs &a,
+                            int grid, hipStream_t s) {
     if (grid <= 0)
         return hipSuccess;
-    return head_dim == 128 ? launch_d<128>(mode, epi, a, grid, s)
-                           : launch_d<64>(mode, epi, a, grid, s);
+    return head_dim == 128 ? launch_d<128>(mode, epi, waves, a, grid, s)
+                           : launch_d<64>(mode, epi, waves, a, grid, s);
 }
 
-int attention_blocks_per_cu(int mode, int head_dim) {
-    if (head_dim == 128) {
-        if (mode == kModeLocal) return blocks_per_cu_one<128, kModeLocal>();
-        if (mode == kModeGlobal) return blocks_per_cu_one<128, kModeGlobal>();
-        return blocks_per_cu_one<128, kModeDense>();
-    }
-    if (mode == kModeLocal) return blocks_per_cu_one<64, kModeLocal>();
-    if (mode == kModeGlobal) return blocks_per_cu_one<64, kModeGlobal>();
-    return blocks_per_cu_one<64, kModeDense>();
+int attention_blocks_per_cu(int mode, int head_dim, int waves) {
+    return head_dim == 128 ? blocks_per_cu_d<128>(mode, waves) : blocks_per_cu_d<64>(mode, waves);
 }
 
 }  // namespace logo

@@ -113,7 +113,7 @@ struct GlobalWs {
     int max_tiles, slots, stride;
 };
 GlobalWs global_ws(const logo_problem *p, int32_t cap) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
     GlobalWs w;
     w.max_tiles = (int)((cap + tp.tpw - 1) / tp.tpw + p->num_seqs);
     w.slots = split_slots(w.max_tiles, tp.n_hg);
@@ -139,9 +139,11 @@ GlobalWs global_ws(const logo_problem *p, int32_t cap) {
 // logo_attn_fwd runs the fused epilogues, so its only large buffer is the
 // compact fp32 (1-p) Norm^L of the selected rows.
 struct FwdWs {
-    size_t sel_ws, glob_ws, lc, sel_idx, cu_sel, tok2sel, thr, total;
+    size_t sel_ws, glob_ws, lc, sel_idx, cu_sel, tok2sel, thr, aperm, total;
 };
-FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
+// aperm: room for the permuted copy of the LP query transform's matrices
+// (logo_attn_fwd_qphi with LOGO_PHI_LP).
+FwdWs fwd_ws(const logo_problem *p, int32_t cap, bool aperm = false) {
     const size_t row = (size_t)p->num_q_heads * p->head_dim * sizeof(float);
     FwdWs w;
     size_t off = 0;
@@ -159,6 +161,9 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap) {
     off += align_up(sizeof(int32_t) * (size_t)p->total_tokens);
     w.thr = off;
     off += align_up(sizeof(float) * (size_t)p->num_seqs);
+    w.aperm = off;
+    if (aperm)
+        off += align_up(2 * (size_t)p->num_q_heads * p->head_dim * p->head_dim);
     w.total = off;
     return w;
 }
@@ -226,7 +231,7 @@ size_t dense_bwd_ws(const logo_problem *p) {
 }
 
 BwdArgs make_bwd_args(const logo_problem *p) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesLocal);
     BwdArgs a;
     std::memset(&a, 0, sizeof a);
     a.cu_seqlens = p->cu_seqlens;
@@ -353,8 +358,6 @@ struct DeviceCache {
     int cus = 0;
 };
 DeviceCache g_devices[kMaxDevices];
-std::once_flag g_occ_once[2];
-int g_occ[2] = {0, 0};
 
 // Scratch memory of logo_decode_noalloc: a fixed device array instead of a
 // caller workspace (see that entry point).  Every GPU the library runs on
@@ -386,7 +389,7 @@ logo_status device_scratch(void **ptr) {
     return LOGO_OK;
 }
 
-logo_status global_grid(int head_dim, int &grid) {
+logo_status device_cus(int &cus) {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
         return LOGO_ERR_HIP;
@@ -396,12 +399,28 @@ logo_status global_grid(int head_dim, int &grid) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
             c.cus = n;
     });
-    if (c.cus <= 0)
-        return LOGO_ERR_HIP;
-    const int di = head_dim == 128 ? 1 : 0;
-    std::call_once(g_occ_once[di],
-                   [&] { g_occ[di] = attention_blocks_per_cu(kModeGlobal, head_dim); });
-    grid = c.cus * g_occ[di];
+    cus = c.cus;
+    return cus > 0 ? LOGO_OK : LOGO_ERR_HIP;
+}
+
+// Resident workgroups per CU of an attention kernel (mode x head dim x
+// waves), queried once each.
+std::once_flag g_occ_once[3][2][2];
+int g_occ[3][2][2];
+
+int blocks_per_cu(int mode, int head_dim, int waves) {
+    const int di = head_dim == 128 ? 1 : 0, wi = waves == 8 ? 1 : 0;
+    std::call_once(g_occ_once[mode][di][wi],
+                   [&] { g_occ[mode][di][wi] = attention_blocks_per_cu(mode, head_dim, waves); });
+    return g_occ[mode][di][wi];
+}
+
+logo_status global_grid(int head_dim, int &grid) {
+    int cus = 0;
+    const logo_status st = device_cus(cus);
+    if (st != LOGO_OK)
+        return st;
+    grid = cus * blocks_per_cu(kModeGlobal, head_dim, kWavesGlobal);
     grid = ((grid + kQueues - 1) / kQueues) * kQueues;
     return LOGO_OK;
 }
@@ -410,7 +429,7 @@ logo_status global_grid(int head_dim, int &grid) {
 // workspace `ws`) and the persistent grid that consumes it.
 logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int32_t *cu_sel,
                         int32_t cap, char *ws, PlanArgs &pa, int &grid) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
     const GlobalWs w = global_ws(p, cap);
     const logo_status st = global_grid(p->head_dim, grid);
     if (st != LOGO_OK)
@@ -433,6 +452,9 @@ logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int
 }
 
 // Fused-epilogue inputs (logo_attn_fwd only).
+// qphi: the global branch's query transform applied by the global kernel as
+// it loads the selected rows (0 none, 1 LP from the permuted copy aperm of
+// lp_a, which the local launch writes, 2 SO with qs / qb).
 struct FusedEpi {
     const int32_t *tok2sel;
     const float *gate;
@@ -440,6 +462,10 @@ struct FusedEpi {
     float eps;
     float *lc;
     logo_bf16 *out;
+    int qphi;
+    const logo_bf16 *lp_a;
+    uint16_t *aperm;
+    const float *qs, *qb;
 };
 
 void set_fused(AttnArgs &a, const FusedEpi *f, const float *gain) {
@@ -459,7 +485,8 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
                       hipStream_t s, const PlanArgs *plan = nullptr, float *lse = nullptr) {
     if (p->total_tokens == 0)
         return LOGO_OK;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeLocal);
+    const int waves = local_waves(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, waves);
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;
@@ -473,15 +500,32 @@ logo_status run_local(const logo_problem *p, const logo_bf16 *q, const logo_bf16
         a.plan_wg = 1;
         a.plan = *plan;
     }
-    // the sequences' tiles back to back: sum_b ceil(T_b / tpw) <= ceil(N / tpw) + B - 1
-    const long long grid =
-        (long long)tp.n_hg * ((p->total_tokens + tp.tpw - 1) / tp.tpw + p->num_seqs) + a.plan_wg;
-    if (grid >= (1LL << 31))
+    if (f && f->qphi == 1) {
+        a.prep_wgs = p->num_q_heads;
+        a.prep_a = f->lp_a;
+        a.aperm = f->aperm;
+    }
+    // items: head groups x the sequences' tiles back to back (sum_b
+    // ceil(T_b / tpw) <= ceil(N / tpw) + B - 1); persistent workgroups, a
+    // multiple of the 8 XCDs, take every item_stride-th item
+    const long long items =
+        (long long)tp.n_hg * ((p->total_tokens + tp.tpw - 1) / tp.tpw + p->num_seqs);
+    if (items >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
-    return hip_status(
-        launch_attention(kModeLocal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw, p->head_dim,
-                         a, (int)grid, s),
-        s);
+    int cus = 0;
+    logo_status st = device_cus(cus);
+    if (st != LOGO_OK)
+        return st;
+    long long wgs = (long long)cus * blocks_per_cu(kModeLocal, p->head_dim, waves);
+    wgs = ((wgs + kQueues - 1) / kQueues) * kQueues;
+    if (wgs > items)
+        wgs = items;
+    a.n_items = (int32_t)items;
+    a.item_stride = (int32_t)wgs;
+    return hip_status(launch_attention(kModeLocal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw,
+                                       p->head_dim, waves, a,
+                                       (int)wgs + a.plan_wg + a.prep_wgs, s),
+                      s);
 }
 
 // built: the plan of a fused launch whose extra workgroup has already
@@ -495,7 +539,7 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
                        float *lse = nullptr) {
     if (p->total_tokens == 0 || cap == 0)
         return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeGlobal);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
     const GlobalWs w = global_ws(p, cap);
     PlanArgs pa;
     int grid = 0;
@@ -524,11 +568,16 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     a.partial = (float *)(ws + w.partial);
     a.lse = lse;
     a.lse_stride = cap;
-    if (f)
+    if (f) {
         set_fused(a, f, gain);
+        a.qphi = f->qphi;
+        a.aperm = f->aperm;
+        a.qphi_s = f->qs;
+        a.qphi_b = f->qb;
+    }
     return hip_status(
         launch_attention(kModeGlobal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw, p->head_dim,
-                         a, grid, s),
+                         kWavesGlobal, a, grid, s),
         s);
 }
 
@@ -538,11 +587,15 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
                      double ratio, const float *gain_local, const float *gain_global, float eps,
                      logo_bf16 *out, int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
                      int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
-                     logo_stream stream, void *const *events) {
+                     logo_stream stream, void *const *events, int qphi = 0,
+                     const logo_bf16 *lp_a = nullptr, const float *so_s = nullptr,
+                     const float *so_b = nullptr) {
     logo_status st = check_problem(p);
     if (st != LOGO_OK)
         return st;
     if (p->total_tokens > 0 && (!q || !k || !v || !gate || !out))
+        return LOGO_ERR_NULL;
+    if ((qphi == 1 && !lp_a) || (qphi == 2 && (!so_s || !so_b)))
         return LOGO_ERR_NULL;
     if (sel_capacity < 0)
         return LOGO_ERR_SHAPE;
@@ -555,7 +608,7 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
                   : p->total_tokens;
     if (!(eps >= 0.f) || std::isinf(eps))
         return LOGO_ERR_ARG;
-    const FwdWs w = fwd_ws(p, cap);
+    const FwdWs w = fwd_ws(p, cap, qphi == 1);
     st = check_ws(ws, ws_bytes, w.total);
     if (st != LOGO_OK)
         return st;
@@ -568,7 +621,8 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     if (st != LOGO_OK)
         return st;
     hipStream_t s = (hipStream_t)stream;
-    const FusedEpi fe{t2s, gate, nullptr, eps, (float *)(base + w.lc), out};
+    const FusedEpi fe{t2s, gate, nullptr, eps, (float *)(base + w.lc), out,
+                      qphi, lp_a, (uint16_t *)(base + w.aperm), so_s, so_b};
     auto mark = [&](int i) -> logo_status {
         if (events && hipEventRecord((hipEvent_t)events[i], s) != hipSuccess)
             return LOGO_ERR_HIP;
@@ -656,6 +710,7 @@ size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capaci
     case LOGO_ENTRY_SELECT: return select_ws(p).total;
     case LOGO_ENTRY_GLOBAL: return global_ws(p, cap).total;
     case LOGO_ENTRY_FWD: return fwd_ws(p, cap).total;
+    case LOGO_ENTRY_FWD_QPHI: return fwd_ws(p, cap, true).total;
     case LOGO_ENTRY_DECODE: return decode_plan(p).total;
     case LOGO_ENTRY_FWD_TRAIN: return fwd_ws(p, cap).total;
     case LOGO_ENTRY_BWD: return bwd_ws(p, cap).total;
@@ -750,6 +805,22 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
                     ws_bytes, stream, nullptr);
 }
 
+logo_status logo_attn_fwd_qphi(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                               const logo_bf16 *v, logo_phi_kind q_phi, const logo_bf16 *A,
+                               const float *s, const float *b, const logo_bf16 *k_g,
+                               const logo_bf16 *v_g, const float *gate, logo_sel_mode mode,
+                               float threshold, double ratio, const float *gain_local,
+                               const float *gain_global, float eps, logo_bf16 *out,
+                               int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
+                               int32_t *tok2sel, float *thr_out, void *ws, size_t ws_bytes,
+                               logo_stream stream) {
+    if (q_phi != LOGO_PHI_LP && q_phi != LOGO_PHI_SO)
+        return LOGO_ERR_ARG;
+    return fwd_impl(p, q, k, v, nullptr, k_g, v_g, gate, mode, threshold, ratio, gain_local,
+                    gain_global, eps, out, sel_idx, sel_capacity, cu_sel, tok2sel, thr_out, ws,
+                    ws_bytes, stream, nullptr, q_phi == LOGO_PHI_LP ? 1 : 2, A, s, b);
+}
+
 logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v,
                                    const logo_bf16 *q_g, const logo_bf16 *k_g,
@@ -785,7 +856,7 @@ logo_status logo_dense_causal_attn_fwd_train(const logo_problem *p, const logo_b
         return LOGO_OK;
     if (!q || !k || !v || !out)
         return LOGO_ERR_NULL;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kModeDense);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;
@@ -797,7 +868,7 @@ logo_status logo_dense_causal_attn_fwd_train(const logo_problem *p, const logo_b
     if (grid >= (1LL << 31))
         return LOGO_ERR_UNSUPPORTED;
     hipStream_t s = (hipStream_t)stream;
-    return hip_status(launch_attention(kModeDense, kEpiRaw, p->head_dim, a, (int)grid, s), s);
+    return hip_status(launch_attention(kModeDense, kEpiRaw, p->head_dim, kWavesGlobal, a, (int)grid, s), s);
 }
 
 }  // extern "C"
@@ -996,7 +1067,8 @@ logo_status logo_attn_fwd_train(const logo_problem *p, const logo_bf16 *q, const
     // The inference path's launches (selection; local branch whose extra
     // workgroup builds the global branch's tile plan; global branch), with
     // epilogues that also keep the raw branch outputs and their LSEs.
-    const FusedEpi fe{tok2sel, gate, nullptr, eps, (float *)(base + w.lc), out};
+    const FusedEpi fe{tok2sel, gate, nullptr, eps, (float *)(base + w.lc), out,
+                      0, nullptr, nullptr, nullptr, nullptr};
     PlanArgs plan;
     int grid_g = 0;
     const bool with_plan = p->total_tokens > 0 && cap > 0;

@@ -12,10 +12,13 @@ namespace logo {
 // query rows of one query head, and all W waves read the same key/value head,
 // so a K/V tile staged in LDS serves 32 W rows.  With GQA group size G the
 // waves cover HPW = gcd(G, 4) heads x (W / HPW) blocks of 32 tokens: a tile
-// is TPW = 32 W / HPW tokens x HPW heads.  The local branch uses W = 4 (two
-// workgroups per CU: its items are short, and a second workgroup hides one's
-// start and end); the global and dense modes use W = 8 (one workgroup per CU:
-// each staged tile serves twice the rows).
+// is TPW = 32 W / HPW tokens x HPW heads.  The global and dense modes use
+// W = 8 (one workgroup per CU: each staged tile serves 256 rows).  The local
+// branch uses W = 8 when HPW = 4 (64 tokens: with 64-key tiles both 32-token
+// blocks need the same KV tiles of a window that is a multiple of 64) and
+// W = 4 otherwise (two workgroups per CU; a wider token span would leave
+// waves idle at the window's ends); its workgroups are persistent and
+// prefetch the next item while they finish the current one.
 // ---------------------------------------------------------------------------
 constexpr int kRowsPerWave = 32;
 constexpr int kBlockN = 64;   // keys per K/V tile
@@ -25,9 +28,8 @@ constexpr int kWavesGlobal = 8;
 
 enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
 
-__host__ __device__ constexpr int waves_of(int mode) {
-    return mode == kModeLocal ? kWavesLocal : kWavesGlobal;
-}
+// Waves of a local-branch workgroup for Hq / Hkv query / KV heads.
+inline int local_waves(int hq, int hkv) { return (hq / hkv) % 4 == 0 ? 8 : kWavesLocal; }
 
 struct TilePlan {
     int hpw;      // heads per workgroup (1, 2 or 4)
@@ -35,11 +37,11 @@ struct TilePlan {
     int n_hg;     // head groups = Hq / hpw
 };
 
-inline TilePlan make_tile_plan(int hq, int hkv, int mode) {
+inline TilePlan make_tile_plan(int hq, int hkv, int waves) {
     const int g = hq / hkv;
     TilePlan t;
     t.hpw = (g % 4 == 0) ? 4 : (g % 2 == 0) ? 2 : 1;
-    t.tpw = kRowsPerWave * (waves_of(mode) / t.hpw);
+    t.tpw = kRowsPerWave * (waves / t.hpw);
     t.n_hg = hq / t.hpw;
     return t;
 }
@@ -131,6 +133,21 @@ struct AttnArgs {
     // fused local launch only: plan_wg = 1 makes workgroup 0 build the global
     // branch's work table (`plan`) while the others attend
     int32_t plan_wg;
+    // local mode: the persistent workgroups (after the plan workgroup) take
+    // items w, w + item_stride, ... below n_items (head group fastest, then
+    // the sequences' token tiles back to back)
+    int32_t n_items, item_stride;
+    // fused local launch only: prep_wgs workgroups (after the plan workgroup)
+    // write the permuted copy aperm of the LP matrices A [Hq][d][d] that the
+    // global launch reads (one head each)
+    int32_t prep_wgs;
+    const uint16_t *prep_a;
+    uint16_t *aperm;
+    // fused global mode only: the branch transform of the selected queries,
+    // applied as they are loaded (0 none, 1 LP with aperm, 2 SO with qphi_s /
+    // qphi_b [Hq][d])
+    int32_t qphi;
+    const float *qphi_s, *qphi_b;
     PlanArgs plan;
     // raw epilogue only: lse (or NULL) receives each row's base-2
     // log-sum-exp of the scaled scores at [head * lse_stride + row]
@@ -139,9 +156,11 @@ struct AttnArgs {
 };
 
 // Launchers (return hipSuccess or the launch error).
-hipError_t launch_attention(int mode, int epi, int head_dim, const AttnArgs &a, int grid,
-                            hipStream_t s);
-int attention_blocks_per_cu(int mode, int head_dim);
+// waves: the workgroup's waves (8 for the global and dense modes; local_waves
+// for the local mode).
+hipError_t launch_attention(int mode, int epi, int head_dim, int waves, const AttnArgs &a,
+                            int grid, hipStream_t s);
+int attention_blocks_per_cu(int mode, int head_dim, int waves);
 
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
                               hipStream_t s);

@@ -162,3 +162,67 @@ def test_layer_with_lp_transforms(pk):
     st = err_stats(torch_bf16_to_f64(out), ref["out"])
     print("[layer+LP] " + " ".join(f"{k}={v:.3g}" for k, v in st.items()))
     assert st["max_abs"] <= 2e-2 and st["mean_abs"] <= 2e-3
+
+
+QPHI_CASES = [
+    # (seqlens, Hq, Hkv, d, window, ratio, kind, distinct k_g / v_g)
+    ((2000, 777, 3000), 8, 2, 128, 256, 0.25, "lp", True),
+    ((4100,), 8, 2, 128, 1024, 0.125, "so", False),
+    ((1500, 300), 8, 8, 64, 100, 0.3, "lp", False),
+    ((2049, 1), 4, 2, 128, 64, 0.5, "so", True),
+    ((3000,), 16, 4, 64, 512, 0.2, "lp", False),
+]
+
+
+@pytest.mark.parametrize("ci", range(len(QPHI_CASES)))
+def test_layer_fused_query_transform(pk, ci):
+    """logo_attn_fwd_qphi: the global kernel applies LP / SO to the selected
+    queries as it loads them (Eq. branch-transform).  Against the oracle
+    layer fed with the oracle's transform of Q rounded to bf16 (the layer
+    bar), and bit for bit against the two-pass path (logo_branch_transform of
+    the selected rows, then logo_attn_fwd with that Q^G): both round the same
+    fp32 values once."""
+    import torch
+    seqlens, H, Hkv, d, win, ratio, kind, distinct = QPHI_CASES[ci]
+    w = synth.small_workload(seqlens, H, Hkv, d, win, ratio, seed=4200 + ci)
+    x = synth.make_inputs(w, distinct_global=distinct)
+    rng = np.random.default_rng(4200 + ci)
+    dev = to_device(x)
+    prob = pk.Problem(dev["cu_seqlens"], H, Hkv, d, win, cu_seqlens_host=x["cu_seqlens"])
+    kw = {}
+    okw = {}
+    if kind == "lp":
+        AQ = rand_bf16(rng, (H, d, d), 1.0 / np.sqrt(d))
+        kw = dict(A=bf16_dev(AQ))
+        okw = dict(A=AQ)
+        phi, ophi = pk.LOGO_PHI_LP, oracle.LP
+    else:
+        s_ = rng.uniform(0.5, 1.5, (H, d)).astype(np.float32)
+        b_ = rng.normal(0.0, 0.5, (H, d)).astype(np.float32)
+        kw = dict(s=torch.from_numpy(s_).cuda(), b=torch.from_numpy(b_).cuda())
+        okw = dict(s=s_, b=b_)
+        phi, ophi = pk.LOGO_PHI_SO, oracle.SO
+    # distinct global keys / values: seeded inputs of their own (the query
+    # transform is what this test is about)
+    kg, vg = dev.get("k_g"), dev.get("v_g")
+    out, sel_idx, cu_sel, _, _ = pk.logo_attn_fwd_qphi(prob, dev["q"], dev["k"], dev["v"],
+                                                       dev["gate"], phi, ratio=ratio, k_g=kg,
+                                                       v_g=vg, **kw)
+    cap = pk.logo_ratio_capacity(prob, ratio)
+    qg = torch.zeros_like(dev["q"])
+    pk.logo_branch_transform(dev["q"], phi, rows=sel_idx, n_rows=cap, n_rows_dev=cu_sel[-1:],
+                             out=qg, **kw)
+    out2 = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=ratio, q_g=qg,
+                            k_g=kg, v_g=vg)[0]
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), ci
+
+    def rnd(a):
+        return synth.bf16_bits_from_f32(a.astype(np.float32)).reshape(a.shape)
+    ref = oracle.logo_fwd(
+        x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], win, ratio=ratio,
+        q_g=rnd(oracle.branch_transform(x["q"], ophi, **okw)), k_g=x.get("k_g"), v_g=x.get("v_g"))
+    st = err_stats(torch_bf16_to_f64(out), ref["out"])
+    print(f"[layer+qphi {kind} {ci}] " + " ".join(f"{k}={v:.3g}" for k, v in st.items()),
+          flush=True)
+    assert st["max_abs"] <= 2e-2 and st["mean_abs"] <= 2e-3
