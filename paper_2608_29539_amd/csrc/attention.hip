@@ -1045,7 +1045,8 @@ hipError_t launch_d(int mode, int epi, int waves, const AttnArgs &a, int grid, h
         return waves == 8 ? launch_epi<D, kModeLocal, 8>(epi, a, grid, s)
                           : launch_epi<D, kModeLocal, kWavesLocal>(epi, a, grid, s);
     if (mode == kModeGlobal)
-        return launch_epi<D, kModeGlobal, kWavesGlobal>(epi, a, grid, s);
+        return waves == 8 ? launch_epi<D, kModeGlobal, kWavesGlobal>(epi, a, grid, s)
+                          : launch_epi<D, kModeGlobal, kWavesLocal>(epi, a, grid, s);
     return launch_one<D, kModeDense, kEpiRaw, kWavesGlobal>(a, grid, s);
 }
 
@@ -1055,7 +1056,8 @@ int blocks_per_cu_d(int mode, int waves) {
         return waves == 8 ? blocks_per_cu_one<D, kModeLocal, 8>()
                           : blocks_per_cu_one<D, kModeLocal, kWavesLocal>();
     if (mode == kModeGlobal)
-        return blocks_per_cu_one<D, kModeGlobal, kWavesGlobal>();
+        return waves == 8 ? blocks_per_cu_one<D, kModeGlobal, kWavesGlobal>()
+                          : blocks_per_cu_one<D, kModeGlobal, kWavesLocal>();
     return blocks_per_cu_one<D, kModeDense, kWavesGlobal>();
 }
 

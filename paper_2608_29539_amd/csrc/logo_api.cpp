@@ -113,7 +113,8 @@ struct GlobalWs {
     int max_tiles, slots, stride;
 };
 GlobalWs global_ws(const logo_problem *p, int32_t cap) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads,
+                                       global_waves(p->num_q_heads, p->num_kv_heads));
     GlobalWs w;
     w.max_tiles = (int)((cap + tp.tpw - 1) / tp.tpw + p->num_seqs);
     w.slots = split_slots(w.max_tiles, tp.n_hg);
@@ -415,12 +416,12 @@ int blocks_per_cu(int mode, int head_dim, int waves) {
     return g_occ[mode][di][wi];
 }
 
-logo_status global_grid(int head_dim, int &grid) {
+logo_status global_grid(int head_dim, int waves, int &grid) {
     int cus = 0;
     const logo_status st = device_cus(cus);
     if (st != LOGO_OK)
         return st;
-    grid = cus * blocks_per_cu(kModeGlobal, head_dim, kWavesGlobal);
+    grid = cus * blocks_per_cu(kModeGlobal, head_dim, waves);
     grid = ((grid + kQueues - 1) / kQueues) * kQueues;
     return LOGO_OK;
 }
@@ -429,11 +430,18 @@ logo_status global_grid(int head_dim, int &grid) {
 // workspace `ws`) and the persistent grid that consumes it.
 logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int32_t *cu_sel,
                         int32_t cap, char *ws, PlanArgs &pa, int &grid) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
+    const int waves = global_waves(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, waves);
     const GlobalWs w = global_ws(p, cap);
-    const logo_status st = global_grid(p->head_dim, grid);
+    const logo_status st = global_grid(p->head_dim, waves, grid);
     if (st != LOGO_OK)
         return st;
+    // no more persistent workgroups than the plan can make items (tiles,
+    // each split at most kMaxSplit ways, times head groups): a small
+    // selection does not pay for draining the queues of a full grid
+    const long long most = (long long)w.max_tiles * kMaxSplit * tp.n_hg;
+    if (most < grid)
+        grid = (int)(((most + kQueues - 1) / kQueues) * kQueues);
     pa.cu_sel = cu_sel;
     pa.sel_idx = sel_idx;
     pa.tpw = tp.tpw;
@@ -539,7 +547,8 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
                        float *lse = nullptr) {
     if (p->total_tokens == 0 || cap == 0)
         return after_plan ? hip_status(hipEventRecord(after_plan, s), s) : LOGO_OK;
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, kWavesGlobal);
+    const int waves = global_waves(p->num_q_heads, p->num_kv_heads);
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, waves);
     const GlobalWs w = global_ws(p, cap);
     PlanArgs pa;
     int grid = 0;
@@ -577,7 +586,7 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
     }
     return hip_status(
         launch_attention(kModeGlobal, f ? (o ? kEpiFusedTrain : kEpiFused) : kEpiRaw, p->head_dim,
-                         kWavesGlobal, a, grid, s),
+                         waves, a, grid, s),
         s);
 }
 

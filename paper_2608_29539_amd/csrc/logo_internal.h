@@ -30,6 +30,11 @@ enum AttnMode { kModeLocal = 0, kModeGlobal = 1, kModeDense = 2 };
 
 // Waves of a local-branch workgroup for Hq / Hkv query / KV heads.
 inline int local_waves(int hq, int hkv) { return (hq / hkv) % 4 == 0 ? 8 : kWavesLocal; }
+// Waves of a global-branch workgroup: 4 (two workgroups per CU, 128 rows
+// of one head per tile) when every KV head has a single query head, else 8.
+// A 256-row tile of selected rows spans ~256 / ratio positions, so its causal
+// band is long, and with one head per group there are few such tiles.
+inline int global_waves(int hq, int hkv) { return hq == hkv ? kWavesLocal : kWavesGlobal; }
 
 struct TilePlan {
     int hpw;      // heads per workgroup (1, 2 or 4)
