@@ -47,11 +47,18 @@ constexpr int kMaskNone = 0, kMaskCausal = 1, kMaskWindow = 2;
 // one 64-byte segment from each of 4 consecutive rows per half-wave, hit 4
 // distinct 64-byte bank groups of the 256-byte bank window.
 constexpr int kKPad = 8;
-template <int D>
+// Output staging of the 8-wave local kernel: each wave's 32 bf16 output rows
+// (padded by 16 B) pass through LDS so that every store instruction writes
+// whole rows (see attend_item).
+constexpr int kStagePad = 8;
+template <int D, int STG = 0>
 struct alignas(16) Smem {
     uint16_t k[2][kBlockN][D + kKPad];
     uint16_t v[2][kBlockN][D];
+    uint16_t ostage[STG > 0 ? STG : 1][kRowsPerWave][STG > 0 ? D + kStagePad : 1];
 };
+template <int MODE, int W>
+constexpr int stage_waves() { return MODE == kModeLocal && W == 8 ? W : 0; }
 template <int D>
 __device__ __forceinline__ constexpr int vswz(int r) {
     // rows per 256-byte bank window: 128 / D; segments per row: D / 32
@@ -424,8 +431,8 @@ __device__ __forceinline__ void item_begin(const AttnArgs &a, int b, int hg, int
 // The first K tile of an item into K buffer 0 (the K/V pipeline of attend_item
 // starts from it); every earlier read of K buffer 0 must have ended at a
 // barrier before this.
-template <int D, int W>
-__device__ __forceinline__ void item_first_k(const AttnArgs &a, Smem<D> &sm, const ItemU &u) {
+template <int D, int W, int STG>
+__device__ __forceinline__ void item_first_k(const AttnArgs &a, Smem<D, STG> &sm, const ItemU &u) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);
     const int row_bytes = a.hkv * D * 2;
@@ -435,15 +442,19 @@ __device__ __forceinline__ void item_first_k(const AttnArgs &a, Smem<D> &sm, con
     dma_k<D, W>(&sm.k[0][0][0], dma, kv_k, u.T, u.kb_lo * kBlockN, row_bytes, wave);
 }
 
-// Attention for one work item whose item_begin loads and first K tile are in
-// flight.  prefetch() runs once every wave has passed the barrier after the
-// item's last K / V tile step -- the K buffers and qf are then free -- and
-// before the item's last PV product and epilogue, so the next item's loads
-// overlap them.
-template <int D, int MODE, int EPI, int W, class Prefetch>
-__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, const ItemU &u,
+// Attention for one work item.  Its item_begin loads and first K tile are
+// in flight (waited: false), or every wave has already waited for its own
+// share of them (waited: true; then the first step needs only the barrier).
+// prefetch() runs once every wave has passed the barrier after the item's
+// last K / V tile step -- the K buffers and qf are then free -- and before
+// the item's last PV product and epilogue, so the next item's loads overlap
+// them; it returns whether it issued loads, and then each wave waits for
+// them before its first output store.  So the next item starts without
+// waiting for this item's stores, which drain during its first step.
+template <int D, int MODE, int EPI, int W, int STG, class Prefetch>
+__device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm, const ItemU &u,
                                             const ItemL &l, bf16x8 (&qf)[RG][D / 16],
-                                            Prefetch &&prefetch) {
+                                            bool waited, Prefetch &&prefetch) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);
     const int g = lane >> 5, m = lane & 31;
@@ -506,12 +517,18 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, cons
     f32x16 s[RG][2];                          // S of the tile being softmax-ed
     auto kidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
     auto vidx = [&](int kb_) { return (kb_ - kb_lo) & 1; };
-    // The item's first K tile (buffer 0) and its Q and epilogue-input loads
-    // are in flight; this wait covers all of them: inside the loop the only
-    // vector-memory loads in flight are the K/V tile loads, which the
-    // compiler does not track.  The barrier also ends every wave's reads of
-    // the previous item's last V tile before this item's first V load.
-    dma_wait_barrier();
+    // The item's first K tile (buffer 0) and its Q and epilogue-input loads:
+    // this wait covers all of them (inside the loop the only vector-memory
+    // loads in flight are the K/V tile loads, which the compiler does not
+    // track).  The barrier also ends every wave's reads of the previous
+    // item's last V tile before this item's first V load.  When each wave has
+    // waited for its loads already, a bare barrier (no memory fence, which
+    // would wait for the previous item's output stores) suffices: the K tile
+    // is in LDS once every wave's share has arrived.
+    if (waited)
+        __builtin_amdgcn_s_barrier();
+    else
+        dma_wait_barrier();
 
     // Loads of step kb: K(kb+1) and V(kb).
     auto stage = [&](int kb_) {
@@ -735,7 +752,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, cons
     }
     for (; kb <= kb_hi; kb++)
         step(kb, F_{}, F_{}, MNone{});
-    prefetch();
+    const bool prefetched = prefetch();
     if (pending) {
         apply_rescale();
         pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step
@@ -766,6 +783,10 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, cons
                 for (int i = 0; i < 16; i++)
                     ss = fmaf(acc[rg][cb][i], acc[rg][cb][i], ss);
             ss = pair_sum(ss);
+            // the next item's loads have arrived before this item's stores
+            // are issued (see above)
+            if (rg == 0 && prefetched)
+                __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
             if (!(wave_valid && row_valid[rg]))
                 continue;
             if constexpr (EPI == kEpiFusedTrain) {
@@ -824,7 +845,10 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, cons
                     u32x2 o;
                     o.x = pack_bf16x2(v.x, v.y);
                     o.y = pack_bf16x2(v.z, v.w);
-                    *(u32x2 *)(op + cb * 32 + qd * 8) = o;
+                    if constexpr (STG > 0)
+                        *(u32x2 *)&sm.ostage[wave][m][cb * 32 + qd * 8 + g * 4] = o;
+                    else
+                        *(u32x2 *)(op + cb * 32 + qd * 8) = o;
                 }
             continue;
         }
@@ -858,13 +882,36 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D> &sm, cons
                 }
         }
     }
+    if constexpr (STG > 0 && EPI != kEpiRaw) {
+        // The wave's unselected rows, staged in LDS above (row m at
+        // ostage[wave][m]), go out as 16-byte chunks in row order: every
+        // store instruction writes 64 lanes x 16 B = whole head slices of
+        // 128 / D rows, instead of 16 B in each of 32 rows.  Rows are
+        // consecutive tokens (local mode); selected and invalid rows were
+        // written elsewhere or not at all and are skipped.
+        static_assert(RG == 1, "one row group per wave");
+        const bool staged = wave_valid && row_valid[0] && ep_rank[0] < 0;
+        const uint32_t smask = (uint32_t)__builtin_amdgcn_ballot_w64(staged && g == 0);
+        constexpr int kChunksPerRow = D / 8;
+        const int64_t tok0 = base + wpmin;
+#pragma unroll
+        for (int i = 0; i < kRowsPerWave * kChunksPerRow / 64; i++) {
+            const int c = i * 64 + lane;
+            const int r = c / kChunksPerRow, c8 = (c % kChunksPerRow) * 8;
+            if ((smask >> r) & 1u) {
+                const u32x4 v = *(const u32x4 *)&sm.ostage[wave][r][c8];
+                *(u32x4 *)(a.out_bf16 + ((tok0 + r) * a.hq + head) * (int64_t)D + c8) = v;
+            }
+        }
+    }
 }
 
 template <int D, int MODE, int EPI, int W>
 __global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_kernel(const AttnArgs a) {
-    __shared__ Smem<D> sm;
-    auto no_prefetch = [] {};
+    constexpr int STG = stage_waves<MODE, W>();
+    __shared__ Smem<D, STG> sm;
+    auto no_prefetch = [] { return false; };
     if (MODE == kModeGlobal) {
         // Persistent workgroups pull (tile, head group) items from the queue
         // of their XCD (workgroups are dispatched round-robin over the 8
@@ -926,8 +973,8 @@ void attn_kernel(const AttnArgs a) {
             ItemL l;
             bf16x8 qf[RG][D / 16];
             item_begin<D, MODE, EPI>(a, t.seq, item % a.n_hg, 0, t, u, l, qf);
-            item_first_k<D, W>(a, sm, u);
-            attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, no_prefetch);
+            item_first_k<D, W, STG>(a, sm, u);
+            attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, false, no_prefetch);
         }
     } else if (MODE == kModeLocal) {
         int wid = blockIdx.x;
@@ -937,7 +984,7 @@ void attn_kernel(const AttnArgs a) {
             if (a.plan_wg) {
                 if (wid == 0) {
                     constexpr int E = D == 128 ? 512 : 256;
-                    static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D>),
+                    static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D, STG>),
                                   "plan table must fit in the K/V staging buffers");
                     build_plan<W * 64, E>(a.cu_seqlens, a.num_seqs, a.plan,
                                           *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
@@ -978,7 +1025,8 @@ void attn_kernel(const AttnArgs a) {
         ItemL l;
         bf16x8 qf[RG][D / 16];
         item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
-        item_first_k<D, W>(a, sm, u);
+        item_first_k<D, W, STG>(a, sm, u);
+        bool waited = false;
         for (;;) {
             // The next item's Q, epilogue inputs and first K tile are loaded
             // while this item finishes its last PV product and epilogue.
@@ -987,14 +1035,16 @@ void attn_kernel(const AttnArgs a) {
             const bool has_next = decode(next, nb, nhg, njt);
             ItemU nu;
             ItemL nl;
-            attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, [&] {
+            attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, waited, [&] {
                 if (has_next) {
                     item_begin<D, MODE, EPI>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
-                    item_first_k<D, W>(a, sm, nu);
+                    item_first_k<D, W, STG>(a, sm, nu);
                 }
+                return has_next;
             });
             if (!has_next)
                 break;
+            waited = true;
             u = nu;
             l = nl;
             item = next;
@@ -1012,8 +1062,8 @@ void attn_kernel(const AttnArgs a) {
         ItemL l;
         bf16x8 qf[RG][D / 16];
         item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
-        item_first_k<D, W>(a, sm, u);
-        attend_item<D, MODE, EPI, W>(a, sm, u, l, qf, no_prefetch);
+        item_first_k<D, W, STG>(a, sm, u);
+        attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, false, no_prefetch);
     }
 }
 
