@@ -7,11 +7,12 @@
 //                     for sequences over 512K tokens), each compacting one
 //                     part of it.  Threshold: ratio mode takes
 //                     k = floor(ratio*T) in IEEE double and the (k+1)-th
-//                     largest gate, found by every part with radix passes of
-//                     at most 12 bits over order-preserving uint32 keys (LDS
-//                     histograms), starting below the bits that all keys of
-//                     the sequence share; threshold mode takes the given
-//                     value.  Then z_t = gate[t] > thr (strict, fp32, done on
+//                     largest gate, found by every part: an LDS histogram
+//                     of 4096 equal-width probability bins, then the keys of
+//                     the bin that holds it are gathered and ranked among
+//                     themselves (radix passes of at most 12 bits over
+//                     order-preserving uint32 keys when that bin is too
+//                     full); threshold mode takes the given value.  Then z_t = gate[t] > thr (strict, fp32, done on
 //                     the keys held in registers) and the part's ranks follow
 //                     from wave ballots, one scan of per-block counts and the
 //                     lane prefix (mbcnt); writes sel_idx, tok2sel and
@@ -53,6 +54,19 @@ __device__ __forceinline__ float key_float(uint32_t k) {
 }
 // Keys above this one are positive NaNs, which never compare greater.
 constexpr uint32_t kPosInfKey = 0xFF800000u;
+
+// First-pass bins of the ratio-mode search: kProbBins equal-width bins over
+// the probability range [0, 1].  prob_bin is non-decreasing in the key:
+// values below 0 and negative NaN keys go to bin 0, values from 1 up,
+// +inf and positive NaN keys to the last bin.
+constexpr int kProbBins = 4096;
+constexpr int kMaxCand = 1024;          // keys of one bin ranked directly
+__device__ __forceinline__ int prob_bin(uint32_t key) {
+    if (key > kPosInfKey)
+        return kProbBins - 1;
+    const float v = fminf(fmaxf(key_float(key), 0.f), 1.f);
+    return min((int)(v * (float)kProbBins), kProbBins - 1);
+}
 
 // Block-wide inclusive scan of one int per thread (blockDim.x <= 1024).
 __device__ __forceinline__ int block_inclusive_scan(int v, int *s_wave) {
@@ -120,11 +134,14 @@ __device__ __forceinline__ void block_min_max(uint32_t &mn, uint32_t &mx, uint32
 // part); otherwise (one part per sequence) write the sequence's count to
 // cnt[b].
 //
-// Ratio mode: the threshold is the key of ascending rank T-k-1, found by radix
-// passes of at most 12 bits that start below the bits all of the sequence's
-// keys share (the common prefix of the smallest and the largest key), so
-// that gates spread over a narrow range still spread over the histogram bins.
-// A pass whose chosen bin holds a single key ends the search.
+// Ratio mode: the threshold is the key of ascending rank T-k-1.  A histogram
+// over kProbBins probability bins finds the bin that holds it; when that bin
+// holds at most kMaxCand keys they are gathered into LDS and the threshold is
+// the one with the right number of smaller keys.  Otherwise radix passes of
+// at most 12 bits start below the bits all of the sequence's keys share (the
+// common prefix of the smallest and the largest key), so that gates spread
+// over a narrow range still spread over the histogram bins; a pass whose
+// chosen bin holds a single key ends the search.
 //
 // Compaction works on the keys in registers: key slot j of thread tid holds
 // token c0 + 1024 j + tid, so the lanes of wave w hold the 64 consecutive
@@ -141,7 +158,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     __shared__ int s_wave[kSelWaves];
     __shared__ uint32_t s_u[2 * kSelWaves];
     __shared__ uint32_t s_bin;
-    __shared__ int s_rank, s_bincnt;
+    __shared__ int s_rank, s_bincnt, s_ncand;
+    __shared__ uint32_t cand[kMaxCand];       // keys of the threshold's probability bin
     const int b = blockIdx.y, part = blockIdx.x, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t base = cu[b];
@@ -184,82 +202,152 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         } else if (!radix) {
             thr_key = float_key(-__builtin_inff());
         } else {
-            int rank = (int)(T - k - 1);      // ascending rank of the threshold value
-            uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+            const int rank0 = (int)(T - k - 1);   // ascending rank of the threshold value
+            // The bin that holds the key of ascending rank `rank`, of nb
+            // counted bins (4 per thread): s_bin, the rank within it
+            // (s_rank) and its count (s_bincnt).
+            auto pick_bin = [&](int nb, int rank) {
+                int own = 0;
+                int c4[4];
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    const int bin = tid * 4 + j;
+                    c4[j] = bin < nb ? hist[bin] : 0;
+                    own += c4[j];
+                }
+                const int incl = block_inclusive_scan(own, s_wave);
+                int run = incl - own;
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    if (c4[j] > 0 && rank >= run && rank < run + c4[j]) {
+                        s_bin = (uint32_t)(tid * 4 + j);
+                        s_rank = rank - run;
+                        s_bincnt = c4[j];
+                    }
+                    run += c4[j];
+                }
+                __syncthreads();
+            };
+            // First pass: kProbBins bins of equal width over the probability
+            // range [0, 1] (values outside it, infinities and NaN keys go to
+            // the end bins, in key order).  Gates are probabilities, so the
+            // bins split them finely; the keys in the threshold's bin are
+            // gathered and ranked among themselves.
+            for (int i = tid; i < kProbBins; i += kSelThreads)
+                hist[i] = 0;
+            if (tid == 0)
+                s_ncand = 0;
+            __syncthreads();
             for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                 if (!resident)
                     load_chunk(c0);
 #pragma unroll
                 for (int j = 0; j < kKeysPerThread; j++)
-                    if (in_seq(c0, j)) {
-                        mn = min(mn, key[j]);
-                        mx = max(mx, key[j]);
-                    }
+                    if (in_seq(c0, j))
+                        atomicAdd(&hist[prob_bin(key[j])], 1);
             }
-            block_min_max(mn, mx, s_u);
-            uint32_t prefix = mn;
-            if (mn != mx) {
-                int hi = 31 - __clz(mn ^ mx);           // highest bit that differs
-                uint32_t pmask = ~((2u << hi) - 1u);    // bits every key shares
-                prefix = mn & pmask;
-                while (hi >= 0) {
-                    const int nbits = min(12, hi + 1);
-                    const int sh = hi + 1 - nbits;
-                    const int nb = 1 << nbits;
-                    for (int i = tid; i < nb; i += kSelThreads)
-                        hist[i] = 0;
-                    __syncthreads();
-                    for (int c0 = 0; c0 < T; c0 += kSelChunk) {
-                        if (!resident)
-                            load_chunk(c0);
-                        // Consecutive slots of a thread are 1024 tokens apart,
-                        // so their digits are unrelated: one atomic per key.
+            __syncthreads();
+            pick_bin(kProbBins, rank0);
+            const int pbin = (int)s_bin, prank = s_rank, pcnt = s_bincnt;
+            if (pcnt <= kMaxCand) {
+                // gather the bin's keys (one LDS atomic per wave and slot)
+                for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+                    if (!resident)
+                        load_chunk(c0);
 #pragma unroll
-                        for (int j = 0; j < kKeysPerThread; j++)
-                            if (in_seq(c0, j) && (key[j] & pmask) == prefix)
-                                atomicAdd(&hist[(key[j] >> sh) & (uint32_t)(nb - 1)], 1);
-                    }
-                    __syncthreads();
-                    // Each thread owns 4 consecutive bins.
-                    int own = 0;
-                    int c4[4];
-#pragma unroll
-                    for (int j = 0; j < 4; j++) {
-                        const int bin = tid * 4 + j;
-                        c4[j] = bin < nb ? hist[bin] : 0;
-                        own += c4[j];
-                    }
-                    const int incl = block_inclusive_scan(own, s_wave);
-                    int run = incl - own;
-#pragma unroll
-                    for (int j = 0; j < 4; j++) {
-                        if (c4[j] > 0 && rank >= run && rank < run + c4[j]) {
-                            s_bin = (uint32_t)(tid * 4 + j);
-                            s_rank = rank - run;
-                            s_bincnt = c4[j];
-                        }
-                        run += c4[j];
-                    }
-                    __syncthreads();
-                    prefix |= s_bin << sh;
-                    pmask |= (uint32_t)(nb - 1) << sh;
-                    rank = s_rank;
-                    const bool unique = s_bincnt == 1;
-                    __syncthreads();
-                    hi = sh - 1;
-                    if (hi >= 0 && unique && resident) {
-                        // one key left in the bin: it is the threshold
-#pragma unroll
-                        for (int j = 0; j < kKeysPerThread; j++)
-                            if (in_seq(0, j) && (key[j] & pmask) == prefix)
-                                s_bin = key[j];
-                        __syncthreads();
-                        prefix = s_bin;
-                        break;
+                    for (int j = 0; j < kKeysPerThread; j++) {
+                        const bool m = in_seq(c0, j) && prob_bin(key[j]) == pbin;
+                        const uint64_t bal = __builtin_amdgcn_ballot_w64(m);
+                        if (bal == 0)
+                            continue;                     // (wave-uniform)
+                        const int leader = __builtin_ctzll(bal);
+                        int at = 0;
+                        if (lane == leader)
+                            at = atomicAdd(&s_ncand, __builtin_popcountll(bal));
+                        at = __builtin_amdgcn_readlane(at, leader);
+                        if (m)
+                            cand[at + (int)__builtin_amdgcn_mbcnt_hi(
+                                          (uint32_t)(bal >> 32),
+                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] = key[j];
                     }
                 }
+                __syncthreads();
+                // the candidate with prank candidates below it (ties: the
+                // one whose run of equal keys covers prank)
+                if (tid < pcnt) {
+                    const uint32_t x = cand[tid];
+                    int lt = 0, le = 0;
+                    for (int i = 0; i < pcnt; i++) {
+                        const uint32_t y = cand[i];
+                        lt += y < x;
+                        le += y <= x;
+                    }
+                    if (lt <= prank && prank < le)
+                        s_bin = x;
+                }
+                __syncthreads();
+                thr_key = s_bin;
+            } else {
+                // A bin too full to rank directly (gates outside [0, 1], or
+                // many close or equal values): radix passes over all keys.
+                int rank = rank0;
+                uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+                for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+                    if (!resident)
+                        load_chunk(c0);
+#pragma unroll
+                    for (int j = 0; j < kKeysPerThread; j++)
+                        if (in_seq(c0, j)) {
+                            mn = min(mn, key[j]);
+                            mx = max(mx, key[j]);
+                        }
+                }
+                block_min_max(mn, mx, s_u);
+                uint32_t prefix = mn;
+                if (mn != mx) {
+                    int hi = 31 - __clz(mn ^ mx);           // highest bit that differs
+                    uint32_t pmask = ~((2u << hi) - 1u);    // bits every key shares
+                    prefix = mn & pmask;
+                    while (hi >= 0) {
+                        const int nbits = min(12, hi + 1);
+                        const int sh = hi + 1 - nbits;
+                        const int nb = 1 << nbits;
+                        for (int i = tid; i < nb; i += kSelThreads)
+                            hist[i] = 0;
+                        __syncthreads();
+                        for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+                            if (!resident)
+                                load_chunk(c0);
+                            // Consecutive slots of a thread are 1024 tokens
+                            // apart, so their digits are unrelated: one
+                            // atomic per key.
+#pragma unroll
+                            for (int j = 0; j < kKeysPerThread; j++)
+                                if (in_seq(c0, j) && (key[j] & pmask) == prefix)
+                                    atomicAdd(&hist[(key[j] >> sh) & (uint32_t)(nb - 1)], 1);
+                        }
+                        __syncthreads();
+                        pick_bin(nb, rank);
+                        prefix |= s_bin << sh;
+                        pmask |= (uint32_t)(nb - 1) << sh;
+                        rank = s_rank;
+                        const bool unique = s_bincnt == 1;
+                        __syncthreads();
+                        hi = sh - 1;
+                        if (hi >= 0 && unique && resident) {
+                            // one key left in the bin: it is the threshold
+#pragma unroll
+                            for (int j = 0; j < kKeysPerThread; j++)
+                                if (in_seq(0, j) && (key[j] & pmask) == prefix)
+                                    s_bin = key[j];
+                            __syncthreads();
+                            prefix = s_bin;
+                            break;
+                        }
+                    }
+                }
+                thr_key = prefix;
             }
-            thr_key = prefix;
         }
         if (part == 0 && tid == 0)
             thr[b] = mode == 1 ? key_float(thr_key) : fixed;
