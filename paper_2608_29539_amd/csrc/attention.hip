@@ -39,6 +39,11 @@ namespace {
 
 // Real-position masks of a KV tile (bit set).
 constexpr int kMaskNone = 0, kMaskCausal = 1, kMaskWindow = 2;
+// Which 32-key halves of a 64-key tile a step computes: both, only the upper
+// one (the lower half lies left of every row's window), only the lower one,
+// or the lower one and the upper one unless no row reaches it (decided at run
+// time: the causal diagonal tiles).
+constexpr int kHalfBoth = 0, kHalfUpper = 1, kHalfLower = 2, kHalfDiag = 3;
 
 // LDS tiles, both [key][d].  K rows are padded by 16 B so that the 16-byte
 // fragment reads of 8 consecutive rows hit distinct banks.  V rows are not
@@ -537,16 +542,20 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
                         wave);
         dma_v<D, W>(&sm.v[vidx(kb_)][0][0], dma, kv_v, T, kb_ * kBlockN, row_bytes, wave);
     };
-    // S(kb) = K(kb) Q^T into s.
-    auto op_s = [&](int kb_) {
+    // S(kb) = K(kb) Q^T into s (the 32-key halves sb0 <= sb < sb1).
+    auto op_s = [&](int kb_, auto half) {
+        constexpr int hf = decltype(half)::value;
+        constexpr int sb0 = hf == kHalfUpper ? 1 : 0, sb1 = hf == kHalfLower ? 1 : 2;
         const uint16_t(*kt)[D + kKPad] = sm.k[kidx(kb_)];
 #pragma unroll
         for (int rg = 0; rg < RG; rg++)
-            s[rg][0] = s[rg][1] = f32x16{};
+#pragma unroll
+            for (int sb = sb0; sb < sb1; sb++)
+                s[rg][sb] = f32x16{};
 #pragma unroll
         for (int ss = 0; ss < D / 16; ss++)
 #pragma unroll
-            for (int sb = 0; sb < 2; sb++) {
+            for (int sb = sb0; sb < sb1; sb++) {
                 const bf16x8 kf = *(const bf16x8 *)&kt[sb * 32 + m][ss * 16 + g * 8];
 #pragma unroll
                 for (int rg = 0; rg < RG; rg++)
@@ -557,7 +566,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
         // per read, so LDS latency hides behind the MFMAs of the S blocks.
         __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);      // DS reads
 #pragma unroll
-        for (int i = 0; i < D / 8 - 4; i++) {
+        for (int i = 0; i < (D / 16) * (sb1 - sb0) - 4; i++) {
             __builtin_amdgcn_sched_group_barrier(0x008, RG, 0); // MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
         }
@@ -612,14 +621,16 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
     // the old pw before the exps overwrite it.  masked: the real-position
     // mask of the tile -- kMaskCausal (key <= pos, diagonal tiles),
     // kMaskWindow (key > pos - w, the local window's left edge) or both.
-    auto op_sm = [&](int kb_, auto do_pv, auto masked) {
+    auto op_sm = [&](int kb_, auto do_pv, auto masked, auto half) {
         constexpr int mk = decltype(masked)::value;
+        constexpr int hf = decltype(half)::value;
+        constexpr int sb0 = hf == kHalfUpper ? 1 : 0, sb1 = hf == kHalfLower ? 1 : 2;
         if constexpr (mk != kMaskNone) {
             const int k0 = kb_ * kBlockN;
 #pragma unroll
             for (int rg = 0; rg < RG; rg++)
 #pragma unroll
-                for (int sb = 0; sb < 2; sb++)
+                for (int sb = sb0; sb < sb1; sb++)
 #pragma unroll
                     for (int i = 0; i < 16; i++) {
                         const int key = k0 + sb * 32 + (i >> 2) * 8 + g * 4 + (i & 3);
@@ -638,7 +649,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
         for (int rg = 0; rg < RG; rg++) {
             float mx = kNegInf;
 #pragma unroll
-            for (int sb = 0; sb < 2; sb++)
+            for (int sb = sb0; sb < sb1; sb++)
 #pragma unroll
                 for (int i = 0; i < 16; i++)
                     mx = fmaxf(mx, s[rg][sb][i]);
@@ -661,6 +672,17 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
             if constexpr (decltype(do_pv)::value)
                 pv_slice(vprev, q);
             const int sb = q >> 1, i0 = (q & 1) * 8;
+            if (sb < sb0 || sb >= sb1) {
+                // a half no row sees: P = 0 (read by the next step's PV
+                // product only when it is the lower half)
+                if (hf == kHalfUpper)
+#pragma unroll
+                    for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                        for (int i = i0; i < i0 + 8; i += 2)
+                            pw[rg][sb][i >> 1] = bf16x2{};
+                continue;
+            }
 #pragma unroll
             for (int rg = 0; rg < RG; rg++)
 #pragma unroll
@@ -686,16 +708,56 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
     using MCausal = std::integral_constant<int, kMaskCausal>;
     using MWindow = std::integral_constant<int, kMaskWindow>;
     using MBoth = std::integral_constant<int, kMaskCausal | kMaskWindow>;
+    using HBoth = std::integral_constant<int, kHalfBoth>;
+    using HUpper = std::integral_constant<int, kHalfUpper>;
+    using HLower = std::integral_constant<int, kHalfLower>;
+    using HDiag = std::integral_constant<int, kHalfDiag>;
+    // 32-key halves no row of the wave sees: the lower half of the first
+    // computed tile lies left of every row's window (local branch; then that
+    // tile is a window-edge tile), the upper half of the last one right of
+    // every row's position (then it is a diagonal tile).  Their score MFMAs
+    // (and, for the lower half, exps) are skipped, and the upper half's PV
+    // product too.
+    const bool lo_out = MODE == kModeLocal && kb_first * kBlockN + 31 <= wpmin - w;
+    const bool hi_out = kb_last * kBlockN + 32 > wpmax;
+    // The last computed tile's upper half was skipped: its PV product covers
+    // the lower half only.
+    bool last_lower = false;
+    auto pv_last = [&](int vi) {
+        if (last_lower) {
+            pv_slice(vi, 0);
+            pv_slice(vi, 1);
+        } else {
+            pv(vi);
+        }
+    };
     // One step: S(kb) + softmax(kb) [x PV(kb-1)], or PV(kb-1) alone.
-    auto step = [&](int kb_, auto do_s, auto do_pv, auto masked) {
+    auto step = [&](int kb_, auto do_s, auto do_pv, auto masked, auto half) {
         stage(kb_);
         if constexpr (decltype(do_pv)::value)
             apply_rescale();
         if constexpr (decltype(do_s)::value) {
-            op_s(kb_);
-            op_sm(kb_, do_pv, masked);
+            if constexpr (decltype(half)::value == kHalfDiag) {
+                // the last tile's upper half is skipped when every row
+                // lies below it; its scores are then -inf (P = 0)
+                op_s(kb_, HLower{});
+                if (hi_out && kb_ == kb_last) {
+#pragma unroll
+                    for (int rg = 0; rg < RG; rg++)
+#pragma unroll
+                        for (int i = 0; i < 16; i++)
+                            s[rg][1][i] = kNegInf;
+                    last_lower = true;
+                } else {
+                    op_s(kb_, HUpper{});
+                }
+                op_sm(kb_, do_pv, masked, HBoth{});
+            } else {
+                op_s(kb_, half);
+                op_sm(kb_, do_pv, masked, half);
+            }
         } else if constexpr (decltype(do_pv)::value) {
-            pv(vidx(kb_ - 1));
+            pv_last(vidx(kb_ - 1));
         }
         dma_wait_barrier();
     };
@@ -720,42 +782,49 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
     int kb = kb_lo;
     bool pending = false;
     for (; kb < kb_first && kb <= kb_hi; kb++)
-        step(kb, F_{}, F_{}, MNone{});
+        step(kb, F_{}, F_{}, MNone{}, HBoth{});
     if (kb_first <= kb_last) {
         // the first tile computed has no PV of a previous tile
         const bool need_c = kb > kb_c, need_w = kb < kb_w;
-        if (need_c && need_w)
-            step(kb, T_{}, F_{}, MBoth{});
-        else if (need_c)
-            step(kb, T_{}, F_{}, MCausal{});
-        else if (need_w)
-            step(kb, T_{}, F_{}, MWindow{});
-        else
-            step(kb, T_{}, F_{}, MNone{});
+        if (need_c && need_w) {
+            if (MODE == kModeLocal && lo_out)
+                step(kb, T_{}, F_{}, MBoth{}, HUpper{});
+            else
+                step(kb, T_{}, F_{}, MBoth{}, HBoth{});
+        } else if (need_c) {
+            step(kb, T_{}, F_{}, MCausal{}, HBoth{});
+        } else if (need_w) {
+            if (MODE == kModeLocal && lo_out)
+                step(kb, T_{}, F_{}, MWindow{}, HUpper{});
+            else
+                step(kb, T_{}, F_{}, MWindow{}, HBoth{});
+        } else {
+            step(kb, T_{}, F_{}, MNone{}, HBoth{});
+        }
         kb++;
         if (MODE == kModeLocal) {
             for (const int e = min(kb_last, min(kb_w - 1, kb_c)); kb <= e; kb++)
-                step(kb, T_{}, T_{}, MWindow{});
+                step(kb, T_{}, T_{}, MWindow{}, HBoth{});
             for (const int e = min(kb_last, kb_w - 1); kb <= e; kb++)
-                step(kb, T_{}, T_{}, MBoth{});
+                step(kb, T_{}, T_{}, MBoth{}, HBoth{});
         }
         for (const int e = min(kb_last, kb_c); kb <= e; kb++)
-            step(kb, T_{}, T_{}, MNone{});
+            step(kb, T_{}, T_{}, MNone{}, HBoth{});
         for (; kb <= kb_last; kb++)
-            step(kb, T_{}, T_{}, MCausal{});
+            step(kb, T_{}, T_{}, MCausal{}, HDiag{});
         pending = true;
     }
     if (pending && kb <= kb_hi) {
-        step(kb, F_{}, T_{}, MNone{});
+        step(kb, F_{}, T_{}, MNone{}, HBoth{});
         pending = false;
         kb++;
     }
     for (; kb <= kb_hi; kb++)
-        step(kb, F_{}, F_{}, MNone{});
+        step(kb, F_{}, F_{}, MNone{}, HBoth{});
     const bool prefetched = prefetch();
     if (pending) {
         apply_rescale();
-        pv(vidx(kb_hi));                     // V(kb_hi) was staged by the last step
+        pv_last(vidx(kb_hi));                // V(kb_hi) was staged by the last step
     }
 
     float l_tot[RG];
