@@ -52,57 +52,54 @@ __device__ __forceinline__ float key_float(uint32_t k) {
     const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
     return __uint_as_float(u);
 }
-// Keys above this one are positive NaNs, which never compare greater.
-constexpr uint32_t kPosInfKey = 0xFF800000u;
-
 // First-pass bins of the ratio-mode search: kProbBins equal-width bins over
-// the probability range [0, 1].  prob_bin is non-decreasing in the key:
-// values below 0 and negative NaN keys go to bin 0, values from 1 up,
-// +inf and positive NaN keys to the last bin.
+// the probability range [0, 1].  prob_bin is non-decreasing in the value:
+// values below 0 (and -inf) go to bin 0, values from 1 up (and +inf) to the
+// last bin; a NaN lands in bin 0 (ratio mode requires finite gates, so this
+// only keeps the index in range).
 constexpr int kProbBins = 4096;
-constexpr int kMaxCand = 1024;          // keys of one bin ranked directly
-__device__ __forceinline__ int prob_bin(uint32_t key) {
-    if (key > kPosInfKey)
-        return kProbBins - 1;
-    const float v = fminf(fmaxf(key_float(key), 0.f), 1.f);
-    return min((int)(v * (float)kProbBins), kProbBins - 1);
+constexpr int kMaxCand = 1024;          // values of one bin ranked directly
+__device__ __forceinline__ int prob_bin(float v) {
+    return (int)fminf(fmaxf(v * (float)kProbBins, 0.f), (float)(kProbBins - 1));
 }
 
-// Block-wide inclusive scan of one int per thread (blockDim.x <= 1024).
-__device__ __forceinline__ int block_inclusive_scan(int v, int *s_wave) {
+// Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and
+// row broadcasts (lanes that a step does not write add zero).
+__device__ __forceinline__ int wave_incl_scan(int x) {
+    int s = x + __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);   // row_shr:1
+    s += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);          // row_shr:2
+    s += __builtin_amdgcn_update_dpp(0, x, 0x113, 0xf, 0xf, true);          // row_shr:3
+    s += __builtin_amdgcn_update_dpp(0, s, 0x114, 0xf, 0xe, false);         // row_shr:4
+    s += __builtin_amdgcn_update_dpp(0, s, 0x118, 0xf, 0xc, false);         // row_shr:8
+    s += __builtin_amdgcn_update_dpp(0, s, 0x142, 0xa, 0xf, false);         // row_bcast:15
+    s += __builtin_amdgcn_update_dpp(0, s, 0x143, 0xc, 0xf, false);         // row_bcast:31
+    return s;
+}
+
+// Block-wide exclusive prefix sum of one int per thread, and the block total
+// (blockDim.x = kSelThreads).  s_wave: kSelWaves ints of LDS.
+__device__ __forceinline__ int block_excl_scan(int v, int *s_wave, int &total) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int t = __shfl_up(v, d, 64);
-        if (lane >= d)
-            v += t;
-    }
+    const int incl = wave_incl_scan(v);
     if (lane == 63)
-        s_wave[wave] = v;
+        s_wave[wave] = incl;
     __syncthreads();
-    int before = 0;
-    for (int i = 0; i < wave; i++)
-        before += s_wave[i];
+    const int wt = wave_incl_scan(lane < kSelWaves ? s_wave[lane] : 0);
+    total = __builtin_amdgcn_readlane(wt, kSelWaves - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(wave);
+    const int before = wv > 0 ? __builtin_amdgcn_readlane(wt, wv - 1) : 0;
     __syncthreads();
-    return v + before;
+    return before + incl - v;
 }
 
 // Block-wide sum (every thread gets it).
 __device__ __forceinline__ int block_sum(int v, int *s_wave) {
-#pragma unroll
-    for (int d = 32; d > 0; d >>= 1)
-        v += __shfl_xor(v, d, 64);
-    if ((threadIdx.x & 63) == 0)
-        s_wave[threadIdx.x >> 6] = v;
-    __syncthreads();
-    int sum = 0;
-    for (int i = 0; i < (int)(blockDim.x >> 6); i++)
-        sum += s_wave[i];
-    __syncthreads();
-    return sum;
+    int total;
+    block_excl_scan(v, s_wave, total);
+    return total;
 }
 
-// Block-wide minimum and maximum (every thread gets both).
+// Block-wide minimum and maximum of the keys (every thread gets both).
 __device__ __forceinline__ void block_min_max(uint32_t &mn, uint32_t &mx, uint32_t *s_u) {
 #pragma unroll
     for (int d = 32; d > 0; d >>= 1) {
@@ -134,32 +131,38 @@ __device__ __forceinline__ void block_min_max(uint32_t &mn, uint32_t &mx, uint32
 // part); otherwise (one part per sequence) write the sequence's count to
 // cnt[b].
 //
-// Ratio mode: the threshold is the key of ascending rank T-k-1.  A histogram
-// over kProbBins probability bins finds the bin that holds it; when that bin
-// holds at most kMaxCand keys they are gathered into LDS and the threshold is
-// the one with the right number of smaller keys.  Otherwise radix passes of
-// at most 12 bits start below the bits all of the sequence's keys share (the
-// common prefix of the smallest and the largest key), so that gates spread
-// over a narrow range still spread over the histogram bins; a pass whose
-// chosen bin holds a single key ends the search.
+// The gates of one chunk of kSelChunk tokens stay in registers: slot j of
+// thread tid holds token c0 + 1024 j + tid, so the lanes of wave w hold the
+// 64 consecutive tokens of block 16 j + w of the chunk.  Slots past the
+// chunk's end hold -inf, which is never selected (gate > thr is false for
+// every thr), and a wave skips the slots none of its lanes holds a token in.
 //
-// Compaction works on the keys in registers: key slot j of thread tid holds
-// token c0 + 1024 j + tid, so the lanes of wave w hold the 64 consecutive
-// tokens of block 16 j + w of the chunk.  One ballot per slot gives each
-// block's selected count (kept in LDS), one scan of the 512 block counts
-// gives each block's first rank, and a token's rank adds the selected lanes
-// below it (mbcnt).
+// Ratio mode: the threshold is the gate of ascending rank T-k-1.  A histogram
+// over kProbBins probability bins finds the bin that holds it (the -inf
+// fillers of the visited slots rank first, so the rank is shifted by their
+// count); when that bin holds at most kMaxCand values they are gathered into
+// LDS and the threshold is the one with the right number of smaller values.
+// Otherwise radix passes of at most 12 bits over order-preserving uint32 keys
+// start below the bits all of the sequence's keys share (the common prefix of
+// the smallest and the largest key), so that gates spread over a narrow range
+// still spread over the histogram bins; a pass whose chosen bin holds a
+// single key ends the search.
+//
+// Compaction: z = gate > thr in fp32 (NaN never passes, -0 equals +0).  One
+// ballot per slot gives each block's selected count (kept in LDS), one scan
+// of the 512 block counts gives each block's first rank, and a token's rank
+// adds the selected lanes below it (mbcnt).
 template <bool kThreshold, bool kWrite>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int32_t *__restrict__ cu, int B, const float *__restrict__ gate, int mode, float fixed,
     double ratio, float *__restrict__ thr, int32_t *__restrict__ cnt, int32_t *__restrict__ sel_idx,
     int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel, int part_tokens) {
-    __shared__ int hist[4096];                // radix histogram, then the block counts
+    __shared__ int hist[kProbBins];           // histogram, then the block counts
     __shared__ int s_wave[kSelWaves];
     __shared__ uint32_t s_u[2 * kSelWaves];
-    __shared__ uint32_t s_bin;
-    __shared__ int s_rank, s_bincnt, s_ncand;
-    __shared__ uint32_t cand[kMaxCand];       // keys of the threshold's probability bin
+    __shared__ int s_bin, s_rank, s_bincnt, s_ncand;
+    __shared__ float s_thr;
+    __shared__ float cand[kMaxCand];          // values of the threshold's probability bin
     const int b = blockIdx.y, part = blockIdx.x, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
     const int64_t base = cu[b];
@@ -170,40 +173,51 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 
     const long long k = (kThreshold && mode == 1) ? (long long)floor(ratio * (double)T) : 0;
     const bool radix = kThreshold && mode == 1 && k < T;
-    // Keys of one chunk of kSelChunk tokens (token c0 + j * 1024 + tid in
-    // key[j]); a sequence that fits in one chunk is loaded once.
+    // Gates of one chunk (token c0 + j * 1024 + tid in g[j]); a sequence
+    // that fits in one chunk is loaded once.
     const bool resident = T <= kSelChunk;
-    uint32_t key[kKeysPerThread];
+    float g[kKeysPerThread];
     // The chunk is read through a buffer descriptor that covers exactly its
     // tokens, with each load's whole offset in the bounds-checked VGPR
-    // offset: slots past the sequence end read 0 (and are never used, see
-    // in_seq), so the loads need no condition and are all in flight at once.
+    // offset, so the loads need no condition and are all in flight at once.
     auto load_chunk = [&](int c0) {
         const int n = min(T - c0, kSelChunk);
         const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
             (void *)(gate + base + c0), (short)0, n * 4, kRawBufferWord3);
 #pragma unroll
-        for (int j = 0; j < kKeysPerThread; j++)
-            key[j] = float_key(__builtin_bit_cast(
-                float, __builtin_amdgcn_raw_buffer_load_b32(r, (j * kSelThreads + tid) * 4, 0, 0)));
+        for (int j = 0; j < kKeysPerThread; j++) {
+            const float v = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(r, (j * kSelThreads + tid) * 4, 0, 0));
+            g[j] = j * kSelThreads < n - tid ? v : -__builtin_inff();
+        }
     };
-    // slot j of the chunk at c0 holds a token of the sequence
-    auto in_seq = [&](int c0, int j) { return j * kSelThreads < T - c0 - tid; };
+    // Slots of the chunk at c0 in which some lane of wave w holds a token.
+    auto wave_slots = [&](int c0, int w) {
+        const int n = min(T - c0, kSelChunk) - w * 64;
+        return n > 0 ? min(kKeysPerThread, (n + kSelThreads - 1) / kSelThreads) : 0;
+    };
     if (resident)
         load_chunk(0);
 
-    uint32_t thr_key;
+    float thr_v;
     if constexpr (kThreshold) {
         if (mode == 2)
             fixed = thr[0];                   // the device-held threshold
         if (mode != 1) {
-            // a NaN threshold (device mode) selects nothing, as gate > NaN
-            thr_key = fixed == fixed ? float_key(fixed) : 0xFFFFFFFFu;
+            thr_v = fixed;                    // a NaN threshold selects nothing
         } else if (!radix) {
-            thr_key = float_key(-__builtin_inff());
+            thr_v = -__builtin_inff();
         } else {
-            const int rank0 = (int)(T - k - 1);   // ascending rank of the threshold value
-            // The bin that holds the key of ascending rank `rank`, of nb
+            // ascending rank of the threshold among the visited values:
+            // T - k - 1 among the gates, after the -inf fillers
+            int rank0 = (int)(T - k - 1);
+            for (int c0 = 0; c0 < T; c0 += kSelChunk) {
+                int visited = 0;
+                for (int w = 0; w < kSelWaves; w++)
+                    visited += wave_slots(c0, w) * 64;
+                rank0 += visited - min(T - c0, kSelChunk);
+            }
+            // The bin that holds the value of ascending rank `rank`, of nb
             // counted bins (4 per thread): s_bin, the rank within it
             // (s_rank) and its count (s_bincnt).
             auto pick_bin = [&](int nb, int rank) {
@@ -215,12 +229,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                     c4[j] = bin < nb ? hist[bin] : 0;
                     own += c4[j];
                 }
-                const int incl = block_inclusive_scan(own, s_wave);
-                int run = incl - own;
+                int total;
+                int run = block_excl_scan(own, s_wave, total);
 #pragma unroll
                 for (int j = 0; j < 4; j++) {
                     if (c4[j] > 0 && rank >= run && rank < run + c4[j]) {
-                        s_bin = (uint32_t)(tid * 4 + j);
+                        s_bin = tid * 4 + j;
                         s_rank = rank - run;
                         s_bincnt = c4[j];
                     }
@@ -229,77 +243,72 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 __syncthreads();
             };
             // First pass: kProbBins bins of equal width over the probability
-            // range [0, 1] (values outside it, infinities and NaN keys go to
-            // the end bins, in key order).  Gates are probabilities, so the
-            // bins split them finely; the keys in the threshold's bin are
-            // gathered and ranked among themselves.
+            // range [0, 1].  Gates are probabilities, so the bins split them
+            // finely; the values in the threshold's bin are gathered and
+            // ranked among themselves.
             for (int i = tid; i < kProbBins; i += kSelThreads)
                 hist[i] = 0;
-            if (tid == 0)
+            if (tid == 0) {
                 s_ncand = 0;
+                s_thr = -__builtin_inff();
+            }
             __syncthreads();
             for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                 if (!resident)
                     load_chunk(c0);
+                const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
 #pragma unroll
                 for (int j = 0; j < kKeysPerThread; j++)
-                    if (in_seq(c0, j))
-                        atomicAdd(&hist[prob_bin(key[j])], 1);
+                    if (j < ns)
+                        atomicAdd(&hist[prob_bin(g[j])], 1);
             }
             __syncthreads();
             pick_bin(kProbBins, rank0);
-            const int pbin = (int)s_bin, prank = s_rank, pcnt = s_bincnt;
+            const int pbin = s_bin, prank = s_rank, pcnt = s_bincnt;
             if (pcnt <= kMaxCand) {
-                // gather the bin's keys (one LDS atomic per wave and slot)
+                // gather the bin's values
                 for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                     if (!resident)
                         load_chunk(c0);
+                    const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
 #pragma unroll
-                    for (int j = 0; j < kKeysPerThread; j++) {
-                        const bool m = in_seq(c0, j) && prob_bin(key[j]) == pbin;
-                        const uint64_t bal = __builtin_amdgcn_ballot_w64(m);
-                        if (bal == 0)
-                            continue;                     // (wave-uniform)
-                        const int leader = __builtin_ctzll(bal);
-                        int at = 0;
-                        if (lane == leader)
-                            at = atomicAdd(&s_ncand, __builtin_popcountll(bal));
-                        at = __builtin_amdgcn_readlane(at, leader);
-                        if (m)
-                            cand[at + (int)__builtin_amdgcn_mbcnt_hi(
-                                          (uint32_t)(bal >> 32),
-                                          __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u))] = key[j];
-                    }
+                    for (int j = 0; j < kKeysPerThread; j++)
+                        if (j < ns && prob_bin(g[j]) == pbin) {
+                            const int at = atomicAdd(&s_ncand, 1);
+                            if (at < kMaxCand)
+                                cand[at] = g[j];
+                        }
                 }
                 __syncthreads();
-                // the candidate with prank candidates below it (ties: the
-                // one whose run of equal keys covers prank)
+                // the value with prank values below it (ties: the one whose
+                // run of equal values covers prank); -0 is reported as +0
                 if (tid < pcnt) {
-                    const uint32_t x = cand[tid];
+                    const float x = cand[tid];
                     int lt = 0, le = 0;
                     for (int i = 0; i < pcnt; i++) {
-                        const uint32_t y = cand[i];
+                        const float y = cand[i];
                         lt += y < x;
                         le += y <= x;
                     }
                     if (lt <= prank && prank < le)
-                        s_bin = x;
+                        s_thr = x + 0.f;
                 }
                 __syncthreads();
-                thr_key = s_bin;
+                thr_v = s_thr;
             } else {
                 // A bin too full to rank directly (gates outside [0, 1], or
-                // many close or equal values): radix passes over all keys.
+                // many close or equal values): radix passes over the keys.
                 int rank = rank0;
                 uint32_t mn = 0xFFFFFFFFu, mx = 0u;
                 for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                     if (!resident)
                         load_chunk(c0);
+                    const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
 #pragma unroll
                     for (int j = 0; j < kKeysPerThread; j++)
-                        if (in_seq(c0, j)) {
-                            mn = min(mn, key[j]);
-                            mx = max(mx, key[j]);
+                        if (j < ns) {
+                            mn = min(mn, float_key(g[j]));
+                            mx = max(mx, float_key(g[j]));
                         }
                 }
                 block_min_max(mn, mx, s_u);
@@ -318,17 +327,20 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                         for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                             if (!resident)
                                 load_chunk(c0);
+                            const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
                             // Consecutive slots of a thread are 1024 tokens
                             // apart, so their digits are unrelated: one
                             // atomic per key.
 #pragma unroll
-                            for (int j = 0; j < kKeysPerThread; j++)
-                                if (in_seq(c0, j) && (key[j] & pmask) == prefix)
-                                    atomicAdd(&hist[(key[j] >> sh) & (uint32_t)(nb - 1)], 1);
+                            for (int j = 0; j < kKeysPerThread; j++) {
+                                const uint32_t key = float_key(g[j]);
+                                if (j < ns && (key & pmask) == prefix)
+                                    atomicAdd(&hist[(key >> sh) & (uint32_t)(nb - 1)], 1);
+                            }
                         }
                         __syncthreads();
                         pick_bin(nb, rank);
-                        prefix |= s_bin << sh;
+                        prefix |= (uint32_t)s_bin << sh;
                         pmask |= (uint32_t)(nb - 1) << sh;
                         rank = s_rank;
                         const bool unique = s_bincnt == 1;
@@ -336,47 +348,34 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                         hi = sh - 1;
                         if (hi >= 0 && unique && resident) {
                             // one key left in the bin: it is the threshold
+                            const int ns = __builtin_amdgcn_readfirstlane(wave_slots(0, wave));
 #pragma unroll
                             for (int j = 0; j < kKeysPerThread; j++)
-                                if (in_seq(0, j) && (key[j] & pmask) == prefix)
-                                    s_bin = key[j];
+                                if (j < ns && (float_key(g[j]) & pmask) == prefix)
+                                    s_u[0] = float_key(g[j]);
                             __syncthreads();
-                            prefix = s_bin;
+                            prefix = s_u[0];
                             break;
                         }
                     }
                 }
-                thr_key = prefix;
+                thr_v = key_float(prefix);
             }
         }
         if (part == 0 && tid == 0)
-            thr[b] = mode == 1 ? key_float(thr_key) : fixed;
+            thr[b] = thr_v;
     } else {
-        const float v = thr[b];
-        thr_key = v == v ? float_key(v) : 0xFFFFFFFFu;   // NaN: nothing passes
+        thr_v = thr[b];
     }
-    // z = gate > thr on the keys: -0 and +0 share a key, and NaN gates (keys
-    // above +inf, or below -inf) never pass.
-    auto pass_z = [&](int c0, int j) {
-        return in_seq(c0, j) && key[j] > thr_key && key[j] <= kPosInfKey;
-    };
-    // selected tokens of the chunk in registers (per wave, then the sum)
+    // selected tokens of the chunk in registers (per wave)
     auto chunk_count = [&](int c0) {
+        const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
         int n = 0;
 #pragma unroll
         for (int j = 0; j < kKeysPerThread; j++)
-            n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(pass_z(c0, j)));
+            if (j < ns)
+                n += __builtin_popcountll(__builtin_amdgcn_ballot_w64(g[j] > thr_v));
         return n;                              // wave-uniform
-    };
-    auto block_total = [&](int per_wave) {
-        if (lane == 0)
-            s_wave[wave] = per_wave;
-        __syncthreads();
-        int sum = 0;
-        for (int i = 0; i < kSelWaves; i++)
-            sum += s_wave[i];
-        __syncthreads();
-        return sum;
     };
 
     if constexpr (!kWrite) {
@@ -386,7 +385,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 load_chunk(c0);
             mine += chunk_count(c0);
         }
-        const int total = block_total(mine);
+        const int total = block_sum(lane == 0 ? mine : 0, s_wave);
         if (tid == 0)
             cnt[b] = total;
     } else {
@@ -409,50 +408,38 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 load_chunk(c0);
                 before += chunk_count(c0);
             }
-            before = offset + (cs > 0 ? block_total(before) : 0);
+            before = offset + (cs > 0 ? block_sum(lane == 0 ? before : 0, s_wave) : 0);
             if (!resident)
                 load_chunk(cs);
-            // selected count of each 64-token block of the chunk
+            // selected count of each 64-token block of the chunk: lane j of
+            // the wave collects slot j's count, one LDS write per wave
+            const int ns = __builtin_amdgcn_readfirstlane(wave_slots(cs, wave));
+            int bc = 0;
 #pragma unroll
-            for (int j = 0; j < kKeysPerThread; j++) {
-                const int n = __builtin_popcountll(__builtin_amdgcn_ballot_w64(pass_z(cs, j)));
-                if (lane == 0)
-                    hist[j * kSelWaves + wave] = n;
-            }
-            __syncthreads();
-            // exclusive scan of the 512 block counts (the first 8 waves)
-            constexpr int kBlocks = kKeysPerThread * kSelWaves;
-            int v = 0, incl = 0;
-            if (tid < kBlocks) {
-                v = hist[tid];
-                incl = v;
-#pragma unroll
-                for (int d = 1; d < 64; d <<= 1) {
-                    const int t = __shfl_up(incl, d, 64);
-                    if (lane >= d)
-                        incl += t;
+            for (int j = 0; j < kKeysPerThread; j++)
+                if (j < ns) {
+                    const int nj = __builtin_popcountll(__builtin_amdgcn_ballot_w64(g[j] > thr_v));
+                    bc = lane == j ? nj : bc;
                 }
-                if (lane == 63)
-                    s_wave[wave] = incl;
-            }
+            if (lane < kKeysPerThread)
+                hist[lane * kSelWaves + wave] = bc;
             __syncthreads();
-            if (tid < kBlocks) {
-                int pre = 0;
-                for (int i = 0; i < wave; i++)
-                    pre += s_wave[i];
-                hist[tid] = pre + incl - v;
-            }
-            int chunk_total = 0;
-            for (int i = 0; i < kBlocks / 64; i++)
-                chunk_total += s_wave[i];
+            // exclusive scan of the 512 block counts in token order (block
+            // 16 j + w at hist[16 j + w])
+            constexpr int kBlocks = kKeysPerThread * kSelWaves;
+            int chunk_total;
+            const int v = tid < kBlocks ? hist[tid] : 0;
+            const int ex = block_excl_scan(v, s_wave, chunk_total);
+            if (tid < kBlocks)
+                hist[tid] = ex;
             __syncthreads();
             // ranks and writes of the part's tokens
 #pragma unroll
             for (int j = 0; j < kKeysPerThread; j++) {
                 const int j0 = cs + j * kSelThreads;      // first token of slot j
-                if (j0 + kSelThreads <= p0 || j0 >= p1)
+                if (j0 + kSelThreads <= p0 || j0 >= p1 || j >= ns)
                     continue;                             // (wave-uniform)
-                const bool z = pass_z(cs, j);
+                const bool z = g[j] > thr_v;
                 const uint64_t bal = __builtin_amdgcn_ballot_w64(z);
                 const int r = before + hist[j * kSelWaves + wave] +
                               (int)__builtin_amdgcn_mbcnt_hi(
