@@ -54,13 +54,15 @@ __device__ __forceinline__ float key_float(uint32_t k) {
 }
 // First-pass bins of the ratio-mode search: kProbBins equal-width bins over
 // the probability range [0, 1].  prob_bin is non-decreasing in the value:
-// values below 0 (and -inf) go to bin 0, values from 1 up (and +inf) to the
-// last bin; a NaN lands in bin 0 (ratio mode requires finite gates, so this
-// only keeps the index in range).
+// values below 1/4096 (and -inf) go to bin 0, values from 4095/4096 up (and
+// +inf) to the last bin; a NaN lands in the last bin (ratio mode requires
+// finite gates, so this only keeps the index in range).  v * 4096 is exact,
+// so bin b holds exactly the values in [b/4096, (b+1)/4096) (open-ended for
+// the end bins), which is how the gather pass tests membership.
 constexpr int kProbBins = 4096;
 constexpr int kMaxCand = 1024;          // values of one bin ranked directly
 __device__ __forceinline__ int prob_bin(float v) {
-    return (int)fminf(fmaxf(v * (float)kProbBins, 0.f), (float)(kProbBins - 1));
+    return (int)fmaxf(fminf(v * (float)kProbBins, (float)(kProbBins - 1)), 0.f);
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave with DPP row shifts and
@@ -266,14 +268,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             pick_bin(kProbBins, rank0);
             const int pbin = s_bin, prank = s_rank, pcnt = s_bincnt;
             if (pcnt <= kMaxCand) {
-                // gather the bin's values
+                // gather the bin's values: min(v, 1) in [lo, hi) is the same
+                // test as prob_bin(v) == pbin (NaN: min gives 1, last bin)
+                const float lo = pbin == 0 ? -__builtin_inff() : (float)pbin * (1.f / kProbBins);
+                const float hi = pbin == kProbBins - 1 ? 2.f : (float)(pbin + 1) * (1.f / kProbBins);
                 for (int c0 = 0; c0 < T; c0 += kSelChunk) {
                     if (!resident)
                         load_chunk(c0);
                     const int ns = __builtin_amdgcn_readfirstlane(wave_slots(c0, wave));
 #pragma unroll
                     for (int j = 0; j < kKeysPerThread; j++)
-                        if (j < ns && prob_bin(g[j]) == pbin) {
+                        if (j < ns && fminf(g[j], 1.f) >= lo && fminf(g[j], 1.f) < hi) {
                             const int at = atomicAdd(&s_ncand, 1);
                             if (at < kMaxCand)
                                 cand[at] = g[j];
