@@ -453,7 +453,7 @@ def main(argv=None):
     ap.add_argument("--settle-ms", type=float, default=400.0,
                     help="untimed layer steps for this long before the warm-up steps, so the "
                          "shader clock has ramped up before any timed region")
-    ap.add_argument("--rounds", type=int, default=3,
+    ap.add_argument("--rounds", type=int, default=5,
                     help="alternating layer / dense timing rounds for the speedup")
     ap.add_argument("--workload", default="T32k-gqa")
     ap.add_argument("--dense-steps", type=int, default=5)
@@ -662,10 +662,14 @@ def main(argv=None):
             pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], threshold=0.5,
                              out=out, sel_capacity=cap_t, sel_idx=sel_t, cu_sel=cu_sel,
                              tok2sel=tok2sel, thr_out=thr, ws=ws_t)
-        for _ in range(2):
-            step_t()
-        torch.cuda.synchronize()
-        n_t = 10
+        # the same settled clock as the headline region: untimed steps for
+        # --settle-ms, then K timed steps
+        t_settle_t = time.perf_counter()
+        while (time.perf_counter() - t_settle_t) * 1e3 < args.settle_ms:
+            for _ in range(10):
+                step_t()
+            torch.cuda.synchronize()
+        n_t = args.steps
         start.record()
         for _ in range(n_t):
             step_t()
