@@ -115,6 +115,37 @@ def test_select_ties_and_nan(pk):
         _select_and_compare(pk, g3, cu, "ratio", r, f"signed-{r}")
 
 
+def test_select_probability_bin_paths(pk):
+    """Ratio mode through each path of the threshold search: the threshold's
+    probability bin (width 1/4096) holding a few values, exactly 1024 (the
+    most ranked directly), 1025 (radix passes instead) and thousands of equal
+    values; gates in [0, 1] throughout."""
+    rng = np.random.default_rng(21)
+    T = 20000
+    base = rng.random(T, dtype=np.float32)
+    cases = []
+    for n_in_bin in (7, 1024, 1025, 6000):
+        g = base.copy()
+        idx = rng.choice(T, n_in_bin, replace=False)
+        # n_in_bin distinct or equal values inside one bin [0.75, 0.75 + 1/4096)
+        if n_in_bin == 6000:
+            g[idx] = np.float32(0.75)
+        else:
+            g[idx] = (np.float32(0.75) + rng.random(n_in_bin, dtype=np.float32)
+                      * np.float32(1.0 / 4096 * 0.999)).astype(np.float32)
+        # keep every other value out of that bin
+        other = np.setdiff1d(np.arange(T), idx)
+        inb = (g[other] >= np.float32(0.75)) & (g[other] < np.float32(0.75 + 1.0 / 4096))
+        g[other[inb]] = np.float32(0.5)
+        cases.append((n_in_bin, g))
+    cu = np.array([0, T], np.int32)
+    for n_in_bin, g in cases:
+        n_above = int((g >= np.float32(0.75 + 1.0 / 4096)).sum())
+        # a ratio whose threshold rank falls inside the bin
+        k = n_above + n_in_bin // 2
+        _select_and_compare(pk, g, cu, "ratio", (k + 0.5) / T, f"bin-{n_in_bin}")
+
+
 @pytest.mark.parametrize("name", ["T1k-tiny", "T8k-b2", "T32k-gqa", "T128k-gqa",
                                   "varlen-4seq-r0", "varlen-4seq-r0.03125", "varlen-4seq-r0.125",
                                   "varlen-4seq-r0.5", "varlen-4seq-r1"])
