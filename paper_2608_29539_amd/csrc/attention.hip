@@ -8,13 +8,16 @@
 //   kModeDense  : every token, keys 0..i                   (dense causal
 //                 baseline, Eq. attention with the global context)
 //
-// Work decomposition.  A workgroup has W waves (4 in the local mode, two
-// workgroups per CU; 8 in the global and dense modes, one per CU); each wave
-// owns 32 query rows of one query head, and all W waves read the same
-// key/value head, so a staged K/V tile in LDS serves 32 W rows (128 local,
-// 256 global / dense).  With GQA group size G the waves take gcd(G,4) heads
+// Work decomposition.  A workgroup has W waves: 8 (one workgroup per CU) in
+// the local mode when G = Hq/Hkv is a multiple of 4, else 4 (two per CU); 8
+// in the global mode, except 4 when G = 1; 8 in the dense mode (see
+// local_waves / global_waves).  Each wave owns 32 query rows of one query
+// head, and all W waves read the same key/value head, so a staged K/V tile in
+// LDS serves 32 W rows.  With GQA group size G the waves take gcd(G,4) heads
 // of one KV group, which keeps the tile's token span -- and so its
-// causal-diagonal band -- short.
+// causal-diagonal band -- short.  The local and global modes run persistent
+// workgroups (static item striding with a prefetch of the next item, and
+// per-XCD work queues, respectively).
 //
 // MFMA formulation (v_mfma_f32_32x32x16_bf16, lane l: column l%32, rows
 // 8*(i/4) + 4*(l/32) + i%4 of the 32x32 accumulator).  The kernel computes
@@ -27,7 +30,8 @@
 //
 // Causal handling (App. B): per KV tile a wave classifies itself as fully
 // visible (no predicate), beyond its last row (skipped) or on the diagonal /
-// window edge (real-position mask on each score).
+// window edge (real-position mask on each score); a 32-key half of its first
+// or last tile that none of its rows sees is not computed.
 #include "logo_internal.h"
 #include "plan.h"
 #include "attn_common.h"

@@ -13,7 +13,8 @@ namespace logo {
 // so a K/V tile staged in LDS serves 32 W rows.  With GQA group size G the
 // waves cover HPW = gcd(G, 4) heads x (W / HPW) blocks of 32 tokens: a tile
 // is TPW = 32 W / HPW tokens x HPW heads.  The global and dense modes use
-// W = 8 (one workgroup per CU: each staged tile serves 256 rows).  The local
+// W = 8 (one workgroup per CU: each staged tile serves 256 rows), the global
+// mode W = 4 when G = 1 (see global_waves).  The local
 // branch uses W = 8 when HPW = 4 (64 tokens: with 64-key tiles both 32-token
 // blocks need the same KV tiles of a window that is a multiple of 64) and
 // W = 4 otherwise (two workgroups per CU; a wider token span would leave

@@ -8,15 +8,16 @@
 //                     part of it.  Threshold: ratio mode takes
 //                     k = floor(ratio*T) in IEEE double and the (k+1)-th
 //                     largest gate, found by every part: an LDS histogram
-//                     of 4096 equal-width probability bins, then the keys of
-//                     the bin that holds it are gathered and ranked among
+//                     of 4096 equal-width probability bins, then the gates
+//                     of the bin that holds it are gathered and ranked among
 //                     themselves (radix passes of at most 12 bits over
 //                     order-preserving uint32 keys when that bin is too
-//                     full); threshold mode takes the given value.  Then z_t = gate[t] > thr (strict, fp32, done on
-//                     the keys held in registers) and the part's ranks follow
-//                     from wave ballots, one scan of per-block counts and the
-//                     lane prefix (mbcnt); writes sel_idx, tok2sel and
-//                     cu_sel.  One sequence: a single launch.
+//                     full); threshold mode takes the given value.  Then
+//                     z_t = gate[t] > thr (strict, fp32, on the gates held
+//                     in registers) and the part's ranks follow from wave
+//                     ballots, one scan of per-block counts and the lane
+//                     prefix (mbcnt); writes sel_idx, tok2sel and cu_sel.
+//                     One sequence: a single launch.
 //                     Several: a first launch finds the thresholds and
 //                     counts, a second one compacts with offset = sum of the
 //                     earlier counts.
@@ -34,14 +35,15 @@ namespace {
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
-constexpr int kKeysPerThread = 32;                      // gate keys per thread per chunk
+constexpr int kKeysPerThread = 32;                      // gates per thread per chunk
 constexpr int kSelChunk = kKeysPerThread * kSelThreads;  // tokens per chunk (32768)
 constexpr int kPartUnit = 4 * kSelThreads;              // smallest part (4096 tokens)
 constexpr int kMaxParts = 16;                           // parts per sequence while parts fit a chunk
 // Word 3 of a raw (untyped, stride 0) buffer descriptor.
 constexpr int kRawBufferWord3 = 0x00020000;
 
-// Order-preserving map from fp32 to uint32 (-0 is folded onto +0 first).
+// Order-preserving map from fp32 to uint32 (-0 is folded onto +0 first); the
+// radix passes of the threshold search work on these keys.
 __device__ __forceinline__ uint32_t float_key(float f) {
     uint32_t u = __float_as_uint(f);
     if (u == 0x80000000u)
@@ -174,7 +176,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         return;                               // an empty part (the whole workgroup)
 
     const long long k = (kThreshold && mode == 1) ? (long long)floor(ratio * (double)T) : 0;
-    const bool radix = kThreshold && mode == 1 && k < T;
+    const bool search = kThreshold && mode == 1 && k < T;   // ratio mode, k < T
     // Gates of one chunk (token c0 + j * 1024 + tid in g[j]); a sequence
     // that fits in one chunk is loaded once.
     const bool resident = T <= kSelChunk;
@@ -207,7 +209,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             fixed = thr[0];                   // the device-held threshold
         if (mode != 1) {
             thr_v = fixed;                    // a NaN threshold selects nothing
-        } else if (!radix) {
+        } else if (!search) {
             thr_v = -__builtin_inff();
         } else {
             // ascending rank of the threshold among the visited values:
