@@ -455,6 +455,8 @@ def main(argv=None):
                          "shader clock has ramped up before any timed region")
     ap.add_argument("--rounds", type=int, default=5,
                     help="alternating layer / dense timing rounds for the speedup")
+    ap.add_argument("--block-warmup", type=int, default=3,
+                    help="untimed calls before each timed block of the interleaved rounds")
     ap.add_argument("--workload", default="T32k-gqa")
     ap.add_argument("--dense-steps", type=int, default=5)
     ap.add_argument("--cpu-stride", type=int, default=0,
@@ -537,7 +539,11 @@ def main(argv=None):
                          tok2sel=tok2sel, thr_out=thr, ws=ws,
                          events=None if i is None else evs[i])
 
-    def timed_block(fn, n):
+    def timed_block(fn, n, warm=0):
+        # warm untimed calls of the same kernel first, so that no block is
+        # timed across the switch from another kernel
+        for _ in range(warm):
+            fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record()
@@ -604,7 +610,8 @@ def main(argv=None):
     # with every row selected; the faster is t_dense), timed under the same
     # clock state as the layer: after one untimed call of each, --rounds
     # rounds each time a block of K layer steps, then a block of dense steps
-    # of each kind; the speedup is the ratio of the medians over the rounds.
+    # of each kind, every block after --block-warmup untimed calls of its own
+    # kernel; the speedup is the median over the rounds.
     dense = {}
     fair = None
     if not args.no_dense:
@@ -626,9 +633,11 @@ def main(argv=None):
         torch.cuda.synchronize()
         rounds = {"layer": [], "dense_kernel": [], "sparse_q_all_rows": []}
         for _ in range(args.rounds):
-            rounds["layer"].append(timed_block(step, args.steps))
-            rounds["dense_kernel"].append(timed_block(dense_kernel, args.dense_steps))
-            rounds["sparse_q_all_rows"].append(timed_block(sparse_all_rows, args.dense_steps))
+            rounds["layer"].append(timed_block(step, args.steps, args.block_warmup))
+            rounds["dense_kernel"].append(timed_block(dense_kernel, args.dense_steps,
+                                                      args.block_warmup))
+            rounds["sparse_q_all_rows"].append(timed_block(sparse_all_rows, args.dense_steps,
+                                                           args.block_warmup))
             sclk.append(current_sclk_mhz())
         med = {k: float(np.median(v)) for k, v in rounds.items()}
         dense["dense_kernel_ms"] = med["dense_kernel"]
@@ -638,7 +647,8 @@ def main(argv=None):
         dense["dense_tflops"] = fl * p_dense / (t_dense * 1e-3) / 1e12
         sp = [min(dk, sq) / lay for lay, dk, sq in zip(rounds["layer"], rounds["dense_kernel"],
                                                        rounds["sparse_q_all_rows"])]
-        fair = {"rounds": args.rounds, "layer_ms_median": round(med["layer"], 4),
+        fair = {"rounds": args.rounds, "block_warmup": args.block_warmup,
+                "layer_ms_median": round(med["layer"], 4),
                 "t_dense_ms_median": round(t_dense, 4),
                 "speedup_median": round(t_dense / med["layer"], 3),
                 "speedup_per_round": [round(v, 3) for v in sp],
