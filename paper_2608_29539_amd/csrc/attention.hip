@@ -1050,28 +1050,32 @@ void attn_kernel(const AttnArgs a) {
             attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, false, no_prefetch);
         }
     } else if (MODE == kModeLocal) {
-        int wid = blockIdx.x;
+        const int wid = blockIdx.x;
         if constexpr (EPI != kEpiRaw) {
-            // The fused layer's local launch: workgroup 0 builds the global
-            // branch's work table (its LDS holds the table), the rest attend.
-            if (a.plan_wg) {
-                if (wid == 0) {
-                    constexpr int E = D == 128 ? 512 : 256;
-                    static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D, STG>),
-                                  "plan table must fit in the K/V staging buffers");
-                    build_plan<W * 64, E>(a.cu_seqlens, a.num_seqs, a.plan,
-                                          *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
-                    return;
+            // The fused layer's local launch: after the item_stride
+            // persistent workgroups come one that builds the global branch's
+            // work table (its LDS holds the table) and, for a global branch
+            // with an LP query transform, one per head that writes the
+            // permuted copy of its matrix.  Being last, they take CUs that
+            // the first workgroups to finish leave free, and no item
+            // workgroup waits for them.
+            if (wid >= a.item_stride) {
+                int x = wid - a.item_stride;
+                if (a.plan_wg) {
+                    if (x == 0) {
+                        constexpr int E = D == 128 ? 512 : 256;
+                        static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D, STG>),
+                                      "plan table must fit in the K/V staging buffers");
+                        build_plan<W * 64, E>(a.cu_seqlens, a.num_seqs, a.plan,
+                                              *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
+                        return;
+                    }
+                    x -= 1;
                 }
-                wid -= 1;
-            }
-            // then, for a global branch with an LP query transform, one
-            // workgroup per head writes the permuted copy of its matrix
-            if (wid < a.prep_wgs) {
-                permute_lp_head<D, W * 64>(a.prep_a, a.aperm, wid);
+                if (x < a.prep_wgs)
+                    permute_lp_head<D, W * 64>(a.prep_a, a.aperm, x);
                 return;
             }
-            wid -= a.prep_wgs;
         }
         // Persistent workgroups: items wid, wid + stride, ...  Item i is head
         // group i % n_hg of token tile i / n_hg, the sequences' tiles back to

@@ -136,14 +136,16 @@ struct AttnArgs {
     float eps;
     float *lc;                 // [capacity][Hq][d] fp32: (1-p) Norm^L of selected rows
     uint16_t *out_bf16;        // [N][Hq][d]
-    // fused local launch only: plan_wg = 1 makes workgroup 0 build the global
-    // branch's work table (`plan`) while the others attend
+    // fused local launch only: plan_wg = 1 makes the workgroup after the
+    // item_stride persistent ones build the global branch's work table
+    // (`plan`)
     int32_t plan_wg;
-    // local mode: the persistent workgroups (after the plan workgroup) take
-    // items w, w + item_stride, ... below n_items (head group fastest, then
-    // the sequences' token tiles back to back)
+    // local mode: the persistent workgroups w < item_stride take items w,
+    // w + item_stride, ... below n_items (head group fastest, then the
+    // sequences' token tiles back to back)
     int32_t n_items, item_stride;
-    // fused local launch only: prep_wgs workgroups (after the plan workgroup)
+    // fused local launch only: prep_wgs workgroups (after the plan workgroup,
+    // at the end of the grid)
     // write the permuted copy aperm of the LP matrices A [Hq][d][d] that the
     // global launch reads (one head each)
     int32_t prep_wgs;
