@@ -16,11 +16,13 @@ Reported (one JSON line on stdout):
                  kernel; both from --rounds rounds that alternate a block of
                  K layer steps with blocks of dense steps (medians), so the
                  two are timed under the same clock state
-  roofline       the query-sparse global kernel (the dominant one) against the
-                 dense bf16 MFMA peak, its duration taken from HIP events that
-                 the profiled entry point records on the layer's stream, in a
-                 second timed run of the same steps (the headline steps run
-                 the plain entry point, with no events inside a step)
+  roofline       the dominant kernel against the dense bf16 MFMA peak: the
+                 one-launch layer kernel (both branches; GQA groups that are a
+                 multiple of 4) or else the query-sparse global kernel, its
+                 duration taken from HIP events that the profiled entry point
+                 records on the layer's stream, in a second timed run of the
+                 same steps (the headline steps run the plain entry point,
+                 with no events inside a step)
   cpu_baseline   the fp64 oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
@@ -60,10 +62,11 @@ def pair_counts(cu: np.ndarray, window: int, sel_idx: np.ndarray):
     return p_local, p_global, p_dense
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_global_T32k-gqa_traffic.md")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_layer_T32k-gqa_traffic.md")
 TRACE_FILE = os.path.join(ROOT, "profiles", "logo_layer_T32k-gqa_kernel_stats.md")
-# Sources whose change invalidates the committed counter figures: the global
-# kernel, its tiling constants and the tile plan that orders its work.
+# Sources whose change invalidates the committed counter figures: the
+# attention kernels, their tiling constants, the tile plan that orders the
+# global work and the selection kernel that feeds both.
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2608_29539_amd", "csrc", f)
                for f in ("attention.hip", "attn_common.h", "logo_internal.h", "plan.h",
                          "select.hip")]
@@ -94,7 +97,7 @@ def committed_fields(path: str, workload: str):
 
 
 def committed_traffic(workload: str):
-    """HBM bytes per launch of the global kernel (two counter passes)."""
+    """HBM bytes per launch of the dominant kernel (two counter passes)."""
     f = committed_fields(TRAFFIC_FILE, workload)
     try:
         return float(f["traffic_bytes_per_launch"]) if f else None
@@ -103,11 +106,11 @@ def committed_traffic(workload: str):
 
 
 def committed_trace_avg_us(workload: str):
-    """Average duration of the global kernel over the K timed calls of the
+    """Average duration of the dominant kernel over the K timed calls of the
     committed kernel-trace run (same sources), or None."""
     f = committed_fields(TRACE_FILE, workload)
     try:
-        return float(f["global_kernel_avg_us_timed"]) if f else None
+        return float(f["dominant_kernel_avg_us_timed"]) if f else None
     except (KeyError, ValueError):
         return None
 
@@ -581,16 +584,20 @@ def main(argv=None):
     ms_step = start.elapsed_time(end) / args.steps
     sclk.append(current_sclk_mhz())
     # Timed region 2: the same steps through the profiled entry point, which
-    # records HIP events on the layer's stream at the stage boundaries
-    # (select | local + tile plan | - | global); the roofline's kernel
-    # duration is the global stage's mean over these K steps.
+    # records HIP events on the layer's stream at the stage boundaries:
+    # select | one-launch layer | - | selected-row sum when both branches run
+    # 8-wave workgroups (GQA group a multiple of 4, the library's choice),
+    # else select | local + tile plan | - | global; the roofline's kernel
+    # duration is the layer's (or the global stage's) mean over these K steps.
     start.record()
     for i in range(n_ev):
         step(i)
     end.record()
     torch.cuda.synchronize()
     ms_step_profiled = start.elapsed_time(end) / args.steps
-    stage_names = ("select", "local", "plan", "global")
+    one_launch = Hq != w.num_kv_heads and (Hq // w.num_kv_heads) % 4 == 0
+    stage_names = (("select", "layer", "none", "sel_sum") if one_launch
+                   else ("select", "local", "plan", "global"))
     stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(n_ev)]))
                 for j, n in enumerate(stage_names)}
     log(f"layer: {ms_step:.3f} ms/step (wall {1e3 * t_wall / args.steps:.3f}, after "
@@ -603,8 +610,19 @@ def main(argv=None):
     fl = 4.0 * d * Hq
     value = fl * (p_local + p_global) / (ms_step * 1e-3) / 1e12
     ideal = p_dense / (p_local + p_global)
-    global_tflops = fl * p_global / (stage_ms["global"] * 1e-3) / 1e12 if p_global else 0.0
-    local_tflops = fl * p_local / (stage_ms["local"] * 1e-3) / 1e12
+    if one_launch:
+        dom_flops = fl * (p_local + p_global)
+        dom_ms = stage_ms["layer"]
+        dom_name = f"layer_kernel<{d}> (local and query-sparse global branch in one launch)"
+        branch_tflops = {"layer_tflops": round(dom_flops / (dom_ms * 1e-3) / 1e12, 2)}
+    else:
+        dom_flops = fl * p_global
+        dom_ms = stage_ms["global"]
+        dom_name = f"attn_kernel<{d}, global> (query-sparse global branch)"
+        branch_tflops = {
+            "local_tflops": round(fl * p_local / (stage_ms["local"] * 1e-3) / 1e12, 2),
+            "global_tflops": round(fl * p_global / (dom_ms * 1e-3) / 1e12, 2) if p_global else 0.0}
+    dom_tflops = dom_flops / (dom_ms * 1e-3) / 1e12
 
     # Dense causal baseline (the DENSE kernel, and the query-sparse kernel
     # with every row selected; the faster is t_dense), timed under the same
@@ -701,19 +719,19 @@ def main(argv=None):
                   "GB_s": round(sel_bytes / (stage_ms["select"] * 1e-3) / 1e9, 1),
                   "peak_GB_s": PEAK_HBM_GBS}
 
-    roofline = {"bound": "mfma", "kernel": "attn_kernel<128, global> (query-sparse global branch)",
-                "achieved": round(global_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(global_tflops / PEAK_BF16_TFLOPS, 4),
+    roofline = {"bound": "mfma", "kernel": dom_name,
+                "achieved": round(dom_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(dom_tflops / PEAK_BF16_TFLOPS, 4),
                 "traffic": committed_traffic(w.name),
-                "flops_per_launch": fl * p_global,
-                "duration_ms": round(stage_ms["global"], 4),
-                "duration_source": "mean of the global stage's HIP events over the K profiled "
+                "flops_per_launch": dom_flops,
+                "duration_ms": round(dom_ms, 4),
+                "duration_source": "mean of the kernel's stage HIP events over the K profiled "
                                    "steps"}
     trace_us = committed_trace_avg_us(w.name)
     if trace_us:
         # the committed rocprofv3 kernel trace of the same sources and workload
         roofline["trace_avg_us_timed_calls"] = trace_us
-        roofline["trace_frac"] = round(fl * p_global / (trace_us * 1e-6) / 1e12
+        roofline["trace_frac"] = round(dom_flops / (trace_us * 1e-6) / 1e12
                                        / PEAK_BF16_TFLOPS, 4)
 
     transforms = None
@@ -764,8 +782,7 @@ def main(argv=None):
         "ideal_speedup_paper": round(1.0 / (w.ratio + w.window / w.max_seqlen), 3),
         "ms_per_step_with_stage_events": round(ms_step_profiled, 4),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
-        "local_tflops": round(local_tflops, 2),
-        "global_tflops": round(global_tflops, 2),
+        **branch_tflops,
         "dense": {k: round(v, 4) for k, v in dense.items()} if dense else None,
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -186,9 +186,13 @@ logo_status logo_combine(const logo_problem *p, const float *o_local, const floa
  * logo_attn_fwd -- the whole layer: select, local branch, query-sparse
  * global branch, ContextNorm and fusion, in one stream-ordered sequence with
  * no host synchronisation (Sec. 3.2-3.3).  ContextNorm and the fusion run in
- * the epilogues of the two attention kernels: the local kernel writes
+ * the epilogues of the attention kernels: the local branch writes
  * Norm^L(O^L) (bf16) for unselected tokens and keeps (1-p) Norm^L(O^L) (fp32,
- * workspace) for selected ones, which the global kernel completes.
+ * workspace) for selected ones.  When Hq / Hkv is a multiple of 4 both
+ * branches run in one persistent launch (global work first, local work
+ * filling in behind it) that keeps p Norm^G(O^G) (fp32, workspace) too, and a
+ * short pass sums the two into the selected rows of `out`; otherwise the
+ * global branch's kernel, launched after the local one, completes them.
  *   q_g/k_g/v_g: global-branch tensors of the same shapes as q/k/v, or NULL
  *   to use q/k/v (the identity branch transform of Eq. branch-transform).
  *   gain_local / gain_global [Hq][d] fp32 or NULL (= 1); eps >= 0.
@@ -201,7 +205,7 @@ logo_status logo_combine(const logo_problem *p, const float *o_local, const floa
  *   out [N][Hq][d] bf16.
  *   ws >= logo_workspace_bytes(p, LOGO_ENTRY_FWD, sel_capacity) bytes,
  *   256-byte aligned (selection scratch, tile table, queue counters and the
- *   compact fp32 buffer of the selected rows).
+ *   compact fp32 buffers of the selected rows).
  */
 logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                           const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
@@ -221,8 +225,10 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
  *   global branch, events[4] after the query-sparse attention kernel (which
  *   applies Norm^G and the fusion for the selected rows).  Elapsed times
  *   between consecutive events are the stage times (select, local, plan,
- *   global).  `events` must not be NULL; everything else is as for
- *   logo_attn_fwd.
+ *   global).  With the one-launch layer (Hq / Hkv a multiple of 4) events[2]
+ *   and events[3] both follow that launch and events[4] the selected rows'
+ *   sum: the stages are (select, layer, -, sum).  `events` must not be NULL;
+ *   everything else is as for logo_attn_fwd.
  */
 logo_status logo_attn_fwd_profiled(const logo_problem *p, const logo_bf16 *q,
                                    const logo_bf16 *k, const logo_bf16 *v,

@@ -905,6 +905,17 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
                         *(f32x4 *)(lp + cb * 32 + qd * 8) = scaled(cb, qd);
                 continue;
             }
+            if constexpr (EPI == kEpiLayer && MODE == kModeGlobal) {
+                // one-launch layer: p Norm^G to the compact buffer; the local
+                // branch's part may not exist yet, a later pass adds them
+                float *cp = a.gc + ((int64_t)r * a.hq + head) * D + g * 4;
+#pragma unroll
+                for (int cb = 0; cb < D / 32; cb++)
+#pragma unroll
+                    for (int qd = 0; qd < 4; qd++)
+                        *(f32x4 *)(cp + cb * 32 + qd * 8) = scaled(cb, qd);
+                continue;
+            }
             const float *lp = (MODE == kModeGlobal)
                                   ? a.lc + ((int64_t)r * a.hq + head) * D + g * 4 : nullptr;
             uint16_t *op = a.out_bf16 + (tok * a.hq + head) * (int64_t)D + g * 4;
@@ -955,7 +966,7 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
                 }
         }
     }
-    if constexpr (STG > 0 && EPI != kEpiRaw) {
+    if constexpr (STG > 0 && EPI != kEpiRaw && MODE == kModeLocal) {
         // The wave's unselected rows, staged in LDS above (row m at
         // ostage[wave][m]), go out as 16-byte chunks in row order: every
         // store instruction writes 64 lanes x 16 B = whole head slices of
@@ -965,15 +976,23 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
         static_assert(RG == 1, "one row group per wave");
         const bool staged = wave_valid && row_valid[0] && ep_rank[0] < 0;
         const uint32_t smask = (uint32_t)__builtin_amdgcn_ballot_w64(staged && g == 0);
-        constexpr int kChunksPerRow = D / 8;
-        const int64_t tok0 = base + wpmin;
+        constexpr int kChunksPerRow = D / 8, kRowsPerStore = 64 / kChunksPerRow;
+        // The lane's row and chunk of the first store come from an opaque
+        // copy of the lane index, so that the compiler keeps one pointer live
+        // instead of hoisting a row index and mask per store out of the
+        // persistent item loop (which made the kernel spill).
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const int r0 = ln / kChunksPerRow, c8 = (ln % kChunksPerRow) * 8;
+        const uint16_t *src = &sm.ostage[wave][r0][c8];
+        uint16_t *dst = a.out_bf16 + ((base + wpmin + r0) * a.hq + head) * (int64_t)D + c8;
+        const int64_t dstep = (int64_t)kRowsPerStore * a.hq * D;
+        const uint32_t lmask = smask >> r0;
 #pragma unroll
-        for (int i = 0; i < kRowsPerWave * kChunksPerRow / 64; i++) {
-            const int c = i * 64 + lane;
-            const int r = c / kChunksPerRow, c8 = (c % kChunksPerRow) * 8;
-            if ((smask >> r) & 1u) {
-                const u32x4 v = *(const u32x4 *)&sm.ostage[wave][r][c8];
-                *(u32x4 *)(a.out_bf16 + ((tok0 + r) * a.hq + head) * (int64_t)D + c8) = v;
+        for (int i = 0; i < kRowsPerWave / kRowsPerStore; i++) {
+            if ((lmask >> (i * kRowsPerStore)) & 1u) {
+                const u32x4 v = *(const u32x4 *)(src + i * kRowsPerStore * (D + kStagePad));
+                *(u32x4 *)(dst + i * dstep) = v;
             }
         }
     }
@@ -1144,6 +1163,277 @@ void attn_kernel(const AttnArgs a) {
     }
 }
 
+// One item from per-XCD queues: queue x holds items x, x + 8, ... below
+// n_items and ctr[x] counts the takes from it.  The caller's own queue x0
+// first, then the others in XCD order; an index past the end means that
+// queue has just emptied, and the counters only grow, so each retry closes a
+// queue.  Called by all lanes of one wave; returns the item (wave-uniform) or
+// -1 once every queue is empty.
+__device__ __forceinline__ int queue_take(int32_t *ctr, int n_items, int x0) {
+    const int lane = threadIdx.x & 63;
+    const int xl = (x0 + lane) % kQueues;
+    const int len_l = (n_items - xl + kQueues - 1) / kQueues;
+    for (int tries = 0; tries <= 2 * kQueues; tries++) {
+        const int c = lane < kQueues
+                          ? __hip_atomic_load(&ctr[xl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                          : 0;
+        const uint64_t open = __builtin_amdgcn_ballot_w64(lane < kQueues && c < len_l);
+        if (open == 0)
+            return -1;
+        const int f = __builtin_ctzll(open);
+        const int x = (x0 + f) % kQueues;
+        int got = 0;
+        if (lane == f)
+            got = x + kQueues * atomicAdd(&ctr[x], 1);
+        got = __builtin_amdgcn_readlane(got, f);
+        if (got < n_items)
+            return got;
+    }
+    return -1;
+}
+
+// A work-table entry written during the same launch by another workgroup:
+// device-scope loads, which read the entry where the writer's release put it
+// and not a stale cached copy.
+__device__ __forceinline__ SparseTile load_tile_coherent(const SparseTile *p) {
+    const int32_t *w = reinterpret_cast<const int32_t *>(p);
+    auto ld = [&](int i) {
+        return __hip_atomic_load(w + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    SparseTile t;
+    t.first = ld(0);
+    t.nrows = ld(1);
+    t.seq = ld(2);
+    t.pos_max = ld(3);
+    t.kb_begin = ld(4);
+    t.kb_end = ld(5);
+    t.split = ld(6);
+    t.nsplit = ld(7);
+    t.sid = ld(8);
+    t.pad[0] = t.pad[1] = t.pad[2] = 0;
+    return t;
+}
+
+// Items left in a local queue below which a workgroup takes its next item
+// only when it needs it (the 32 workgroups of an XCD share its queue).
+constexpr int kLateClaimItems = 32;
+// Bound of the wait for the work table (s_sleep 8 = 512 cycles per poll:
+// ~2 s), so that no workgroup can wait for ever.
+constexpr int kPlanSpinMax = 1 << 23;
+
+// The layer's two branches in one persistent launch (8-wave workgroups on
+// both, Hq / Hkv a multiple of 4).  The local branch's items are short and
+// many (every token tile x head group, ~17 KV steps at w = 1024), the global
+// branch's few and long (a tile's whole causal prefix), so running them one
+// launch after the other leaves the GPU partly idle at each launch's end
+// (the workgroups of the global launch end ~10% apart: its long items and the
+// XCDs' different speeds).  Here every workgroup takes global items first,
+// longest first, and then local items until none is left, so the short local
+// items fill in behind the long ones:
+//   A. workgroup 0 builds the global work table (and the permuted LP
+//      matrices of an LP query transform) and releases it with a flag; every
+//      other workgroup meanwhile runs one local item, then waits for the
+//      flag.
+//   B. global items from the per-XCD queues of the table (longest first,
+//      stealing once the own queue is empty), epilogue kEpiLayer: p Norm^G
+//      of each selected row to the compact buffer gc.
+//   C. local items from per-XCD queues (queue x: items x, x + 8, ..., i.e.
+//      the head groups of one XCD share KV heads), the next item's loads
+//      issued after the current item's last K / V step as in the local
+//      launch; the next item is claimed from the own queue when the current
+//      one starts (the atomic's reply has arrived by the prefetch), except
+//      near the queue's end, where it is taken at the prefetch so that no
+//      workgroup holds an item it cannot start yet while others run dry.
+// Selected rows get (1-p) Norm^L in lc from their local item and p Norm^G in
+// gc from their global item, in either order; launch_sel_sum then writes
+// their output rows.
+template <int D>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+void layer_kernel(const AttnArgs a) {
+    constexpr int W = 8;
+    constexpr int STG = stage_waves<kModeLocal, W>();
+    __shared__ Smem<D, STG> sm;
+    __shared__ int s_item, s_entries;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int x0 = blockIdx.x % kQueues;
+    int32_t *const lq = a.ctl + 1;
+    // the global branch's tensors
+    AttnArgs ag = a;
+    ag.q = a.qg;
+    ag.k = a.kg;
+    ag.v = a.vg;
+    ag.gain = a.gain_g;
+    auto no_prefetch = [] { return false; };
+    // Local item -> (sequence, head group, token tile); false past the last
+    // valid item (items are head group fastest, then the sequences' token
+    // tiles back to back; n_items may exceed the valid ones).
+    auto decode = [&](int item, int &b, int &hg, int &jt) {
+        if (item < 0 || item >= a.n_items)
+            return false;
+        hg = item % a.n_hg;
+        int rest = item / a.n_hg;
+        for (b = 0; b < a.num_seqs; b++) {
+            const int nt = (a.cu_seqlens[b + 1] - a.cu_seqlens[b] + a.tpw - 1) / a.tpw;
+            if (rest < nt)
+                break;
+            rest -= nt;
+        }
+        jt = rest;
+        return b < a.num_seqs;
+    };
+    // wave 0 takes an item, the workgroup learns it (the second barrier ends
+    // every wave's read before s_item is written again)
+    auto take_wg = [&](int32_t *ctr, int n) {
+        if (tid < 64) {
+            const int it = queue_take(ctr, n, x0);
+            if (lane == 0)
+                s_item = it;
+        }
+        __syncthreads();
+        const int it = __builtin_amdgcn_readfirstlane(s_item);
+        __syncthreads();
+        return it;
+    };
+    // the next valid local item (any queue), or -1
+    auto take_local = [&](int &b, int &hg, int &jt) {
+        int it;
+        do {
+            it = take_wg(lq, a.n_items);
+        } while (it >= 0 && !decode(it, b, hg, jt));
+        return it;
+    };
+
+    // A. the work table, or one local item while it is built
+    if (blockIdx.x == 0) {
+        constexpr int E = D == 128 ? 512 : 256;
+        static_assert(sizeof(plan_detail::PlanLds<E>) <= sizeof(Smem<D, STG>),
+                      "plan table must fit in the staging buffers");
+        build_plan<W * 64, E>(a.cu_seqlens, a.num_seqs, a.plan,
+                              *reinterpret_cast<plan_detail::PlanLds<E> *>(&sm));
+        for (int h = 0; h < a.prep_wgs; h++)
+            permute_lp_head<D, W * 64>(a.prep_a, a.aperm, h);
+        // every wave's stores written back to where other XCDs read them,
+        // then the flag
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __syncthreads();
+        if (tid == 0) {
+            __hip_atomic_store(&a.ctl[0], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            s_entries = __hip_atomic_load(&a.queue[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else {
+        int b = 0, hg = 0, jt = 0;
+        if (take_local(b, hg, jt) >= 0) {
+            ItemU u;
+            ItemL l;
+            bf16x8 qf[RG][D / 16];
+            item_begin<D, kModeLocal, kEpiLayer>(a, b, hg, jt, SparseTile{}, u, l, qf);
+            item_first_k<D, W, STG>(a, sm, u);
+            attend_item<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u, l, qf, false, no_prefetch);
+        }
+        if (tid == 0) {
+            // (no table after the bound: the global items are skipped)
+            bool ready = false;
+            for (int n = 0; n < kPlanSpinMax && !ready; n++) {
+                ready = __hip_atomic_load(&a.ctl[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+                if (!ready)
+                    __builtin_amdgcn_s_sleep(8);
+            }
+            s_entries = ready ? __hip_atomic_load(&a.queue[0], __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT)
+                              : 0;
+        }
+    }
+    __syncthreads();
+
+    // B. global items
+    const int n_entries = __builtin_amdgcn_readfirstlane(s_entries);
+    if (n_entries > 0) {
+        const int n_gitems = n_entries * a.n_hg;
+        for (;;) {
+            const int item = take_wg(a.queue + 1, n_gitems);
+            if (item < 0)
+                break;
+            const SparseTile t = load_tile_coherent(a.tiles + item / a.n_hg);
+            ItemU u;
+            ItemL l;
+            bf16x8 qf[RG][D / 16];
+            item_begin<D, kModeGlobal, kEpiLayer>(ag, t.seq, item % a.n_hg, 0, t, u, l, qf);
+            item_first_k<D, W, STG>(ag, sm, u);
+            attend_item<D, kModeGlobal, kEpiLayer, W, STG>(ag, sm, u, l, qf, false, no_prefetch);
+        }
+    }
+
+    // C. local items
+    int b = 0, hg = 0, jt = 0;
+    if (take_local(b, hg, jt) < 0)
+        return;
+    ItemU u;
+    ItemL l;
+    bf16x8 qf[RG][D / 16];
+    item_begin<D, kModeLocal, kEpiLayer>(a, b, hg, jt, SparseTile{}, u, l, qf);
+    item_first_k<D, W, STG>(a, sm, u);
+    bool waited = false;
+    // Claim of the next item from the own queue, issued when an item starts
+    // and resolved at its prefetch, so that the atomic's reply has arrived by
+    // then; once the own queue's remaining items are fewer than its
+    // workgroups, the next item is taken only at the prefetch instead, so
+    // that no workgroup holds an item it cannot start yet while the queues
+    // run dry.
+    bool early = true;
+    for (;;) {
+        int claim = 0;
+        if (early && tid == 0)
+            claim = atomicAdd(&lq[x0], 1);
+        ItemU nu;
+        ItemL nl;
+        int nxt = -1;
+        attend_item<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u, l, qf, waited, [&] {
+            if (tid < 64) {
+                int nb, nhg, njt;
+                int it = early ? x0 + kQueues * __builtin_amdgcn_readfirstlane(claim) : -1;
+                if (!decode(it, nb, nhg, njt)) {
+                    do {
+                        it = queue_take(lq, a.n_items, x0);
+                    } while (it >= 0 && !decode(it, nb, nhg, njt));
+                }
+                if (lane == 0)
+                    s_item = it;
+            }
+            // s_item is written again only at the next item's prefetch,
+            // after that item's barriers
+            __syncthreads();
+            nxt = __builtin_amdgcn_readfirstlane(s_item);
+            if (nxt < 0)
+                return false;
+            early = nxt + kQueues * kLateClaimItems < a.n_items;
+            int nb = 0, nhg = 0, njt = 0;
+            decode(nxt, nb, nhg, njt);
+            item_begin<D, kModeLocal, kEpiLayer>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
+            item_first_k<D, W, STG>(a, sm, nu);
+            return true;
+        });
+        if (nxt < 0)
+            break;
+        waited = true;
+        u = nu;
+        l = nl;
+    }
+}
+
+template <int D>
+hipError_t launch_layer_d(const AttnArgs &a, int grid, hipStream_t s) {
+    hipLaunchKernelGGL((layer_kernel<D>), dim3(grid), dim3(512), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int D>
+int layer_blocks_per_cu_d() {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, layer_kernel<D>, 512, 0) != hipSuccess)
+        return 1;
+    return n > 0 ? n : 1;
+}
+
 template <int D, int MODE, int EPI, int W>
 hipError_t launch_one(const AttnArgs &a, int grid, hipStream_t s) {
     hipLaunchKernelGGL((attn_kernel<D, MODE, EPI, W>), dim3(grid), dim3(W * 64), 0, s, a);
@@ -1200,6 +1490,16 @@ hipError_t launch_attention(int mode, int epi, int head_dim, int waves, const At
 
 int attention_blocks_per_cu(int mode, int head_dim, int waves) {
     return head_dim == 128 ? blocks_per_cu_d<128>(mode, waves) : blocks_per_cu_d<64>(mode, waves);
+}
+
+hipError_t launch_layer(int head_dim, const AttnArgs &a, int grid, hipStream_t s) {
+    if (grid <= 0)
+        return hipSuccess;
+    return head_dim == 128 ? launch_layer_d<128>(a, grid, s) : launch_layer_d<64>(a, grid, s);
+}
+
+int layer_blocks_per_cu(int head_dim) {
+    return head_dim == 128 ? layer_blocks_per_cu_d<128>() : layer_blocks_per_cu_d<64>();
 }
 
 }  // namespace logo

@@ -2,10 +2,14 @@
 // (Eq. contextnorm: head-wise RMSNorm of each branch; Eq. output-fusion:
 // (1-p) Norm^L + p Norm^G for selected tokens, Norm^L otherwise).
 //
-// HBM-bound streaming kernel: one (token, head) row of d fp32 values is
-// handled by d/4 lanes with 16-byte loads; the row's sum of squares is a
-// butterfly over those lanes.  Unselected rows never touch o_global.
+// HBM-bound streaming kernels.  combine_kernel (logo_combine): one (token,
+// head) row of d fp32 values is handled by d/4 lanes with 16-byte loads; the
+// row's sum of squares is a butterfly over those lanes, and unselected rows
+// never touch o_global.  sel_sum_kernel: the selected rows' output of the
+// one-launch layer, from its two weighted branch parts.
 #include "logo_internal.h"
+
+#include <algorithm>
 
 namespace logo {
 namespace {
@@ -74,7 +78,58 @@ __global__ __launch_bounds__(256) void combine_kernel(long long n_rows, int hq,
     }
 }
 
+// Output rows of the selected tokens from the two branch parts of the
+// one-launch layer (Eq. output-fusion): out[sel_idx[r]][h] = bf16(lc[r][h] +
+// gc[r][h]), lc = (1-p) Norm^L and gc = p Norm^G already weighted.  Eight
+// values per thread (two 16-byte loads of each part, one 16-byte store),
+// grid-stride over the selected count read on the device.
+template <int D>
+__global__ __launch_bounds__(256) void sel_sum_kernel(int32_t cap, int hq,
+                                                      const int32_t *__restrict__ cu_sel, int B,
+                                                      const int32_t *__restrict__ sel_idx,
+                                                      const float *__restrict__ lc,
+                                                      const float *__restrict__ gc,
+                                                      uint16_t *__restrict__ out) {
+    constexpr int kVecPerRow = D / 8;
+    const int n = min(cu_sel[B], cap);
+    const long long nvec = (long long)n * hq * kVecPerRow;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < nvec;
+         i += (long long)gridDim.x * 256) {
+        const long long rh = i / kVecPerRow;           // r * hq + h
+        const int c = (int)(i % kVecPerRow) * 8;
+        const long long r = rh / hq;
+        const int h = (int)(rh % hq);
+        const float *pl = lc + rh * D + c, *pg = gc + rh * D + c;
+        const f32x4 a0 = *(const f32x4 *)pl, a1 = *(const f32x4 *)(pl + 4);
+        const f32x4 b0 = *(const f32x4 *)pg, b1 = *(const f32x4 *)(pg + 4);
+        const f32x4 y0 = a0 + b0, y1 = a1 + b1;
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        u32x4v o;
+        o.x = pack_bf16x2(y0.x, y0.y);
+        o.y = pack_bf16x2(y0.z, y0.w);
+        o.z = pack_bf16x2(y1.x, y1.y);
+        o.w = pack_bf16x2(y1.z, y1.w);
+        *(u32x4v *)(out + ((long long)sel_idx[r] * hq + h) * D + c) = o;
+    }
+}
+
 }  // namespace
+
+hipError_t launch_sel_sum(int32_t cap, int hq, int head_dim, const int32_t *cu_sel, int num_seqs,
+                          const int32_t *sel_idx, const float *lc, const float *gc,
+                          uint16_t *out, hipStream_t s) {
+    const long long vecs = (long long)cap * hq * (head_dim / 8);
+    if (vecs == 0)
+        return hipSuccess;
+    const long long grid = std::min((vecs + 255) / 256, 8192LL);
+    if (head_dim == 128)
+        hipLaunchKernelGGL(sel_sum_kernel<128>, dim3((unsigned)grid), dim3(256), 0, s, cap, hq,
+                           cu_sel, num_seqs, sel_idx, lc, gc, out);
+    else
+        hipLaunchKernelGGL(sel_sum_kernel<64>, dim3((unsigned)grid), dim3(256), 0, s, cap, hq,
+                           cu_sel, num_seqs, sel_idx, lc, gc, out);
+    return hipGetLastError();
+}
 
 hipError_t launch_combine(int n_tokens, int hq, int head_dim, const float *o_local,
                           const float *o_global, const float *gate, const int32_t *tok2sel,

@@ -137,10 +137,10 @@ GlobalWs global_ws(const logo_problem *p, int32_t cap) {
     return w;
 }
 
-// logo_attn_fwd runs the fused epilogues, so its only large buffer is the
-// compact fp32 (1-p) Norm^L of the selected rows.
+// logo_attn_fwd runs the fused epilogues, so its only large buffers are the
+// compact fp32 (1-p) Norm^L and p Norm^G of the selected rows.
 struct FwdWs {
-    size_t sel_ws, glob_ws, lc, sel_idx, cu_sel, tok2sel, thr, aperm, total;
+    size_t sel_ws, glob_ws, lc, gc, ctl, sel_idx, cu_sel, tok2sel, thr, aperm, total;
 };
 // aperm: room for the permuted copy of the LP query transform's matrices
 // (logo_attn_fwd_qphi with LOGO_PHI_LP).
@@ -154,6 +154,11 @@ FwdWs fwd_ws(const logo_problem *p, int32_t cap, bool aperm = false) {
     off += align_up(global_ws(p, cap).total);
     w.lc = off;
     off += align_up(row * (size_t)cap);
+    // the one-launch layer: p Norm^G of the selected rows, control words
+    w.gc = off;
+    off += align_up(row * (size_t)cap);
+    w.ctl = off;
+    off += align_up(sizeof(int32_t) * kLayerCtlWords);
     w.sel_idx = off;
     off += align_up(sizeof(int32_t) * (size_t)cap);
     w.cu_sel = off;
@@ -339,12 +344,12 @@ logo_status check_select_args(const logo_problem *p, const float *gate, logo_sel
 logo_status run_select(const logo_problem *p, const float *gate, logo_sel_mode mode,
                        float threshold, double ratio, int32_t *sel_idx, int32_t cap,
                        int32_t *cu_sel, int32_t *tok2sel, float *thr_out, char *ws,
-                       hipStream_t s) {
+                       hipStream_t s, int32_t *zero_words = nullptr, int n_zero = 0) {
     const SelectWs w = select_ws(p);
     float *thr = thr_out ? thr_out : (float *)(ws + w.thr);
     return hip_status(launch_select(p->cu_seqlens, p->num_seqs, p->max_seqlen, gate, (int)mode,
                                     threshold, ratio, sel_idx, cap, cu_sel, tok2sel, thr,
-                                    (int32_t *)(ws + w.counts), s),
+                                    (int32_t *)(ws + w.counts), s, zero_words, n_zero),
                       s);
 }
 
@@ -416,6 +421,23 @@ int blocks_per_cu(int mode, int head_dim, int waves) {
     return g_occ[mode][di][wi];
 }
 
+// Persistent grid of the one-launch layer (occupancy queried once per head
+// dim), a multiple of the work queues.
+std::once_flag g_layer_occ_once[2];
+int g_layer_occ[2];
+
+logo_status layer_grid(int head_dim, int &grid) {
+    int cus = 0;
+    const logo_status st = device_cus(cus);
+    if (st != LOGO_OK)
+        return st;
+    const int di = head_dim == 128 ? 1 : 0;
+    std::call_once(g_layer_occ_once[di], [&] { g_layer_occ[di] = layer_blocks_per_cu(head_dim); });
+    grid = cus * g_layer_occ[di];
+    grid = ((grid + kQueues - 1) / kQueues) * kQueues;
+    return LOGO_OK;
+}
+
 logo_status global_grid(int head_dim, int waves, int &grid) {
     int cus = 0;
     const logo_status st = device_cus(cus);
@@ -451,6 +473,7 @@ logo_status global_plan(const logo_problem *p, const int32_t *sel_idx, const int
     pa.grid_wgs = grid;
     pa.split_slots = w.slots;
     pa.stride = w.stride;
+    pa.extra_blocks = 0;
     pa.tmp = (SparseTile *)(ws + w.tiles_tmp);
     pa.out = (SparseTile *)(ws + w.tiles);
     pa.scratch = (int32_t *)(ws + w.scratch);
@@ -590,6 +613,67 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
         s);
 }
 
+// The one-launch layer (both branches with 8-wave workgroups): the local
+// items and the global work table's items in one persistent grid, whose
+// first workgroup builds the table (layer_kernel).  gc / ctl: the compact
+// p Norm^G buffer and the launch's control words (cleared by the selection
+// kernel before it).  The selected rows' output is written afterwards by
+// launch_sel_sum.
+logo_status run_layer(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
+                      const logo_bf16 *v, const logo_bf16 *qg, const logo_bf16 *kg,
+                      const logo_bf16 *vg, const int32_t *sel_idx, const int32_t *cu_sel,
+                      int32_t cap, const FusedEpi *f, const float *gain_local,
+                      const float *gain_global, float *gc, int32_t *ctl, char *glob_ws,
+                      hipStream_t s) {
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, 8);
+    PlanArgs pa;
+    int grid_g = 0;
+    logo_status st = global_plan(p, sel_idx, cu_sel, cap, glob_ws, pa, grid_g);
+    if (st != LOGO_OK)
+        return st;
+    int grid = 0;
+    if ((st = layer_grid(p->head_dim, grid)) != LOGO_OK)
+        return st;
+    // local items: head groups x the sequences' token tiles back to back (an
+    // upper bound; the valid ones are a prefix), each ~(w + tpw) / 64 + 1 KV
+    // blocks, which the table's split threshold counts as the grid's other
+    // work
+    const long long tiles = (p->total_tokens + tp.tpw - 1) / tp.tpw;
+    const long long items = (long long)tp.n_hg * (tiles + p->num_seqs);
+    if (items >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    const long long span = std::min<long long>(p->window, p->max_seqlen) + tp.tpw;
+    pa.grid_wgs = grid;
+    pa.extra_blocks = (int64_t)tp.n_hg * tiles * ((span + kBlockN - 1) / kBlockN + 1);
+    AttnArgs a = make_args(p, tp);
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.qg = qg;
+    a.kg = kg;
+    a.vg = vg;
+    set_fused(a, f, gain_local);
+    a.gain_g = gain_global;
+    a.gc = gc;
+    a.ctl = ctl;
+    a.sel_idx = sel_idx;
+    a.plan = pa;
+    a.tiles = pa.out;
+    a.queue = pa.queue;
+    a.split_cnt = pa.split_cnt;
+    a.partial = (float *)(glob_ws + global_ws(p, cap).partial);
+    a.n_items = (int32_t)items;
+    a.qphi = f->qphi;
+    a.aperm = f->aperm;
+    a.qphi_s = f->qs;
+    a.qphi_b = f->qb;
+    if (f->qphi == 1) {
+        a.prep_wgs = p->num_q_heads;
+        a.prep_a = f->lp_a;
+    }
+    return hip_status(launch_layer(p->head_dim, a, grid, s), s);
+}
+
 logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
                      const logo_bf16 *v, const logo_bf16 *q_g, const logo_bf16 *k_g,
                      const logo_bf16 *v_g, const float *gate, logo_sel_mode mode, float threshold,
@@ -645,9 +729,29 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     // compact buffer for selected ones; one extra workgroup of that launch
     // builds the global branch's tile plan.  Then the global branch finishes
     // the selected rows.
+    const bool with_plan = p->total_tokens > 0 && cap > 0;
+    if (with_plan && local_waves(p->num_q_heads, p->num_kv_heads) == 8 &&
+        global_waves(p->num_q_heads, p->num_kv_heads) == 8) {
+        // both branches in one launch, then the selected rows' sums
+        int32_t *ctl = (int32_t *)(base + w.ctl);
+        float *lc = (float *)(base + w.lc), *gc = (float *)(base + w.gc);
+        st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws,
+                        s, ctl, kLayerCtlWords);
+        if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
+            return st;
+        st = run_layer(p, q, k, v, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, &fe,
+                       gain_local, gain_global, gc, ctl, base + w.glob_ws, s);
+        if (st != LOGO_OK || (st = mark(2)) != LOGO_OK || (st = mark(3)) != LOGO_OK)
+            return st;
+        st = hip_status(launch_sel_sum(cap, p->num_q_heads, p->head_dim, cus, p->num_seqs, sel, lc,
+                                       gc, out, s),
+                        s);
+        if (st != LOGO_OK)
+            return st;
+        return mark(4);
+    }
     PlanArgs plan;
     int grid_g = 0;
-    const bool with_plan = p->total_tokens > 0 && cap > 0;
     if (with_plan && (st = global_plan(p, sel, cus, cap, base + w.glob_ws, plan, grid_g)) != LOGO_OK)
         return st;
     st = run_select(p, gate, mode, threshold, ratio, sel, cap, cus, t2s, thr, base + w.sel_ws, s);

@@ -100,7 +100,11 @@ inline int split_slots(int max_tiles, int n_hg) {
 //   kEpiFusedTrain : kEpiFused, and also the raw branch output O (fp32, to
 //               `out`) and the base-2 LSE of each row (to `lse`) -- the
 //               training forward, which keeps them for the backward pass.
-enum AttnEpi { kEpiRaw = 0, kEpiFused = 1, kEpiFusedTrain = 2 };
+//   kEpiLayer : the one-launch layer (layer_kernel): the local items as in
+//               kEpiFused; the global items write p Norm^G(O^G) (fp32) to the
+//               compact buffer `gc` instead of finishing the rows, and a
+//               separate pass sums lc + gc into `out`.
+enum AttnEpi { kEpiRaw = 0, kEpiFused = 1, kEpiFusedTrain = 2, kEpiLayer = 3 };
 
 // Tile plan of the global branch (device-built work table).  tmp and out each
 // hold max_tiles + split_slots entries; scratch holds 2 * stride ints with
@@ -109,6 +113,9 @@ struct PlanArgs {
     const int32_t *cu_sel;     // [B+1] compacted sequence offsets
     const int32_t *sel_idx;    // [cap] selected token indices
     int32_t tpw, cap, max_seqlen, n_hg, grid_wgs, split_slots, stride;
+    // other work of the same persistent grid, in KV-block units (the local
+    // items of the one-launch layer), counted into the split threshold
+    int64_t extra_blocks;
     SparseTile *tmp, *out;
     int32_t *scratch, *queue, *split_cnt;
 };
@@ -161,7 +168,17 @@ struct AttnArgs {
     // log-sum-exp of the scaled scores at [head * lse_stride + row]
     float *lse;
     int64_t lse_stride;
+    // one-launch layer only: the global branch's Q / K / V (q, k, v are the
+    // local branch's), the compact buffer of p Norm^G, and the launch's
+    // control words (zeroed before the launch): [0] = the work table is
+    // built, [1 + x] = local queue x's counter
+    const uint16_t *qg, *kg, *vg;
+    const float *gain_g;       // the global branch's gain (gain: the local one's)
+    float *gc;
+    int32_t *ctl;
 };
+// Control words of the one-launch layer.
+constexpr int kLayerCtlWords = 1 + kQueues;
 
 // Launchers (return hipSuccess or the launch error).
 // waves: the workgroup's waves (8 for the global and dense modes; local_waves
@@ -173,13 +190,27 @@ int attention_blocks_per_cu(int mode, int head_dim, int waves);
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
                               hipStream_t s);
 
+// The one-launch layer (8-wave workgroups on both branches, i.e. Hq / Hkv a
+// multiple of 4): grid persistent workgroups; a.n_items local items, the
+// global items of the work table that workgroup 0 builds (a.plan).
+hipError_t launch_layer(int head_dim, const AttnArgs &a, int grid, hipStream_t s);
+int layer_blocks_per_cu(int head_dim);
+// out[sel_idx[r]] = bf16(lc[r] + gc[r]) for the selected ranks r below
+// min(cu_sel[B], cap) (read on the device).
+hipError_t launch_sel_sum(int32_t cap, int hq, int head_dim, const int32_t *cu_sel, int num_seqs,
+                          const int32_t *sel_idx, const float *lc, const float *gc,
+                          uint16_t *out, hipStream_t s);
+
 // Selection: thresholds, ranks and compaction.  seq_counts holds num_seqs
 // ints (per-sequence selected counts when num_seqs > 1).  max_seqlen sizes
 // the parts of a sequence that separate workgroups compact.
+// zero_words (or NULL): n_zero ints the selection kernel clears (the control
+// words of the layer launch that follows it).
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s);
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s,
+                         int32_t *zero_words = nullptr, int n_zero = 0);
 
 // One decoding step (decode.hip).  Work items: local (sequence, KV head,
 // head group, chunk) then global (selected rank, KV head, head group,

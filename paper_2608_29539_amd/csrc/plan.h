@@ -11,8 +11,9 @@
 //
 // The table is built in LDS when it fits (the caller passes the LDS block and
 // its entry capacity) and copied out once; otherwise it is built in the
-// global buffers of PlanArgs.  Used by the standalone plan launch and by one
-// extra workgroup of the local-branch launch of the fused layer forward.
+// global buffers of PlanArgs.  Used by the standalone plan launch, by one
+// extra workgroup of the local-branch launch of the fused layer forward and
+// by the first workgroup of the one-launch layer.
 #pragma once
 
 #include "logo_internal.h"
@@ -216,9 +217,11 @@ __device__ void build_plan(const int32_t *cu, int B, const PlanArgs &p,
     sort_desc<NT>(tmp, out, n_tiles, max_blocks, l.hist, l.wave_part);
 
     // 4. KV split: a tile longer than `target` blocks (a 1/kSplitDiv share of
-    //    the mean load of one persistent workgroup) becomes ns = ceil(blocks /
-    //    target) entries (at most kMaxSplit), while partial slots last.
-    const unsigned long long work = l.total_blocks * (unsigned long long)n_hg;
+    //    the mean load of one persistent workgroup, other work of the grid
+    //    included) becomes ns = ceil(blocks / target) entries (at most
+    //    kMaxSplit), while partial slots last.
+    const unsigned long long work = l.total_blocks * (unsigned long long)n_hg +
+                                    (unsigned long long)(p.extra_blocks > 0 ? p.extra_blocks : 0);
     const unsigned long long div = (unsigned long long)kSplitDiv * (unsigned long long)p.grid_wgs;
     long long target = (long long)((work + div - 1) / div);
     if (target < kMinSplitBlocks)

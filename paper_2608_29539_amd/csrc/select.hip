@@ -160,7 +160,8 @@ template <bool kThreshold, bool kWrite>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int32_t *__restrict__ cu, int B, const float *__restrict__ gate, int mode, float fixed,
     double ratio, float *__restrict__ thr, int32_t *__restrict__ cnt, int32_t *__restrict__ sel_idx,
-    int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel, int part_tokens) {
+    int32_t cap, int32_t *__restrict__ cu_sel, int32_t *__restrict__ tok2sel, int part_tokens,
+    int32_t *__restrict__ zero_words, int n_zero) {
     __shared__ int hist[kProbBins];           // histogram, then the block counts
     __shared__ int s_wave[kSelWaves];
     __shared__ uint32_t s_u[2 * kSelWaves];
@@ -169,6 +170,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     __shared__ float cand[kMaxCand];          // values of the threshold's probability bin
     const int b = blockIdx.y, part = blockIdx.x, tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
+    // the control words of the launch that follows (first workgroup)
+    if (kWrite && b == 0 && part == 0 && tid < n_zero)
+        zero_words[tid] = 0;
     const int64_t base = cu[b];
     const int T = cu[b + 1] - (int)base;
     const int p0 = part * part_tokens;
@@ -504,7 +508,8 @@ hipError_t launch_budget_update(const int32_t *cu_sel, int num_seqs, int n_token
 hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen,
                          const float *gate, int mode, float threshold, double ratio,
                          int32_t *sel_idx, int32_t sel_capacity, int32_t *cu_sel,
-                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s) {
+                         int32_t *tok2sel, float *thr, int32_t *seq_counts, hipStream_t s,
+                         int32_t *zero_words, int n_zero) {
     // parts of 4096 * 2^i tokens, at most kMaxParts per sequence unless a
     // part would exceed one chunk (then one part per chunk)
     int part_tokens = kPartUnit;
@@ -515,18 +520,18 @@ hipError_t launch_select(const int32_t *cu_seqlens, int num_seqs, int max_seqlen
     if (num_seqs == 1) {
         hipLaunchKernelGGL((select_kernel<true, true>), dim3(parts, 1), dim3(kSelThreads), 0, s,
                            cu_seqlens, 1, gate, mode, threshold, ratio, thr, seq_counts, sel_idx,
-                           sel_capacity, cu_sel, tok2sel, part_tokens);
+                           sel_capacity, cu_sel, tok2sel, part_tokens, zero_words, n_zero);
         return hipGetLastError();
     }
     hipLaunchKernelGGL((select_kernel<true, false>), dim3(1, num_seqs), dim3(kSelThreads), 0, s,
                        cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts,
-                       sel_idx, sel_capacity, cu_sel, tok2sel, part_tokens);
+                       sel_idx, sel_capacity, cu_sel, tok2sel, part_tokens, nullptr, 0);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL((select_kernel<false, true>), dim3(parts, num_seqs), dim3(kSelThreads), 0,
                        s, cu_seqlens, num_seqs, gate, mode, threshold, ratio, thr, seq_counts,
-                       sel_idx, sel_capacity, cu_sel, tok2sel, part_tokens);
+                       sel_idx, sel_capacity, cu_sel, tok2sel, part_tokens, zero_words, n_zero);
     return hipGetLastError();
 }
 

@@ -412,6 +412,47 @@ def test_single_selected_at_position_zero(pk):
     assert st["max_abs"] <= MAX_ABS and st["mean_abs"] <= MEAN_ABS
 
 
+@pytest.mark.parametrize("case", ["late-rows-split", "none-selected", "many-seqs"])
+def test_layer_one_launch_cases(pk, case):
+    """The one-launch layer (Hq / Hkv a multiple of 4), every output element
+    against the oracle: a long sequence whose few selected rows all sit near
+    its end (their global tiles are longer than the launch's mean load, so
+    the work table splits each over four KV ranges whose partials are merged
+    inside the launch), a threshold no gate passes (no global item: the
+    local items alone), and a batch of 40 short ragged sequences (empty ones
+    included)."""
+    import torch
+    if case == "late-rows-split":
+        w = synth.small_workload((20000,), 8, 2, 128, 256, 0.0, seed=2100)
+        x = synth.make_inputs(w)
+        x["gate"][:] = x["gate"] * 0.5
+        x["gate"][-100:] = 0.9
+        kw = dict(threshold=0.5)
+    elif case == "none-selected":
+        w = synth.small_workload((3000, 1000), 8, 2, 64, 128, 0.0, seed=2101)
+        x = synth.make_inputs(w)
+        kw = dict(threshold=2.0)
+    else:
+        lens = np.random.default_rng(2102).integers(0, 600, 40)
+        lens[[3, 17]] = 0
+        w = synth.small_workload(tuple(int(t) for t in lens), 16, 4, 64, 100, 0.3, seed=2102)
+        x = synth.make_inputs(w)
+        kw = dict(ratio=0.3)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    out, sel, cu_sel, t2s, _ = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"],
+                                                **kw)
+    torch.cuda.synchronize()
+    ref = oracle.logo_fwd(x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], w.window, **kw)
+    assert cu_sel.cpu().numpy().tolist() == ref["cu_sel"].tolist()
+    n = int(ref["cu_sel"][-1])
+    assert n == {"late-rows-split": 100, "none-selected": 0}.get(case, n)
+    assert sel.cpu().numpy()[:n].tolist() == ref["sel_idx"][:n].tolist()
+    st = err_stats(torch_bf16_to_f64(out), ref["out"])
+    report(f"one-launch {case} n_sel={n}", st)
+    assert st["max_abs"] <= MAX_ABS and st["mean_abs"] <= MEAN_ABS
+
+
 def test_determinism(pk):
     import torch
     w = synth.small_workload((3000, 1500), 8, 2, 128, 256, 0.25, seed=1800)
