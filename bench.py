@@ -17,8 +17,8 @@ Reported (one JSON line on stdout):
                  K layer steps with blocks of dense steps (medians), so the
                  two are timed under the same clock state
   roofline       the dominant kernel against the dense bf16 MFMA peak: the
-                 one-launch layer kernel (both branches; GQA groups that are a
-                 multiple of 4) or else the query-sparse global kernel, its
+                 one-launch layer kernel (both branches, where the library runs
+                 them in one launch) or else the query-sparse global kernel, its
                  duration taken from HIP events that the profiled entry point
                  records on the layer's stream, in a second timed run of the
                  same steps (the headline steps run the plain entry point,
@@ -585,9 +585,9 @@ def main(argv=None):
     sclk.append(current_sclk_mhz())
     # Timed region 2: the same steps through the profiled entry point, which
     # records HIP events on the layer's stream at the stage boundaries:
-    # select | one-launch layer | - | selected-row sum when both branches run
-    # 8-wave workgroups (GQA group a multiple of 4, the library's choice),
-    # else select | local + tile plan | - | global; the roofline's kernel
+    # select | one-launch layer | - | selected-row sum when the library runs
+    # both branches in one launch (logo_attn_fwd_launches), else select |
+    # local + tile plan | - | global; the roofline's kernel
     # duration is the layer's (or the global stage's) mean over these K steps.
     start.record()
     for i in range(n_ev):
@@ -595,7 +595,7 @@ def main(argv=None):
     end.record()
     torch.cuda.synchronize()
     ms_step_profiled = start.elapsed_time(end) / args.steps
-    one_launch = Hq != w.num_kv_heads and (Hq // w.num_kv_heads) % 4 == 0
+    one_launch = pk.logo_attn_fwd_launches(prob) == 1
     stage_names = (("select", "layer", "none", "sel_sum") if one_launch
                    else ("select", "local", "plan", "global"))
     stage_ms = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(n_ev)]))

@@ -188,8 +188,8 @@ logo_status logo_combine(const logo_problem *p, const float *o_local, const floa
  * no host synchronisation (Sec. 3.2-3.3).  ContextNorm and the fusion run in
  * the epilogues of the attention kernels: the local branch writes
  * Norm^L(O^L) (bf16) for unselected tokens and keeps (1-p) Norm^L(O^L) (fp32,
- * workspace) for selected ones.  When Hq / Hkv is a multiple of 4 both
- * branches run in one persistent launch (global work first, local work
+ * workspace) for selected ones.  When Hq / Hkv is a multiple of 4, or 1,
+ * both branches run in one persistent launch (global work first, local work
  * filling in behind it) that keeps p Norm^G(O^G) (fp32, workspace) too, and a
  * short pass sums the two into the selected rows of `out`; otherwise the
  * global branch's kernel, launched after the local one, completes them.
@@ -225,7 +225,7 @@ logo_status logo_attn_fwd(const logo_problem *p, const logo_bf16 *q, const logo_
  *   global branch, events[4] after the query-sparse attention kernel (which
  *   applies Norm^G and the fusion for the selected rows).  Elapsed times
  *   between consecutive events are the stage times (select, local, plan,
- *   global).  With the one-launch layer (Hq / Hkv a multiple of 4) events[2]
+ *   global).  With the one-launch layer (Hq / Hkv a multiple of 4, or 1) events[2]
  *   and events[3] both follow that launch and events[4] the selected rows'
  *   sum: the stages are (select, layer, -, sum).  `events` must not be NULL;
  *   everything else is as for logo_attn_fwd.
@@ -560,6 +560,19 @@ float logo_pmask_initial_threshold(float gamma, int64_t pmask_steps);
  * problem: N).  Returns 0 for an invalid problem.
  */
 size_t logo_workspace_bytes(const logo_problem *p, int entry, int32_t sel_capacity);
+
+/*
+ * logo_attn_fwd_launches -- how logo_attn_fwd (and logo_attn_fwd_qphi /
+ * _profiled) runs the two attention branches of problem p when the
+ * selection capacity is nonzero: 1 = one persistent launch for both
+ * (Hq / Hkv a multiple of 4, or 1, and enough local work per workgroup to
+ * cover building the global work table inside the launch), 2 = the local
+ * launch, then the global one.  Host-only (no GPU work; queries the current
+ * device's CU count once).  The environment variable LOGO_FWD_LAUNCHES=1 or 2
+ * forces one or the other where both are possible.  Returns -1 for an
+ * invalid problem or a HIP error.
+ */
+int logo_attn_fwd_launches(const logo_problem *p);
 
 /* Selection bound used by the ratio-mode capacity check: sum_b floor(ratio*T_b)
  * computed from cu_seqlens_host, or N when that is NULL.  -1 on bad input. */

@@ -48,6 +48,7 @@ from .binding import (  # noqa: F401
     logo_global_attn_sparse_q_fwd_train,
     logo_local_attn,
     logo_pmask_initial_threshold,
+    logo_attn_fwd_launches,
     logo_ratio_capacity,
     logo_select,
     logo_status_str,

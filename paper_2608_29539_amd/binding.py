@@ -42,6 +42,7 @@ EXPORTS = (
     "logo_attn_fwd_train", "logo_attn_bwd", "logo_dense_causal_attn_fwd_train",
     "logo_dense_causal_attn_bwd", "logo_global_attn_sparse_q_fwd_train",
     "logo_global_attn_sparse_q_bwd", "logo_decode_noalloc", "logo_attn_fwd_qphi",
+    "logo_attn_fwd_launches",
 )
 
 _lib = None
@@ -119,6 +120,8 @@ def library():
     lib.logo_workspace_bytes.restype = sz
     lib.logo_ratio_capacity.argtypes = [PP, f64]
     lib.logo_ratio_capacity.restype = i64
+    lib.logo_attn_fwd_launches.argtypes = [PP]
+    lib.logo_attn_fwd_launches.restype = ctypes.c_int
     lib.logo_status_str.argtypes = [ctypes.c_int]
     lib.logo_status_str.restype = ctypes.c_char_p
     lib.logo_version.restype = ctypes.c_char_p
@@ -230,6 +233,10 @@ def logo_workspace_bytes(prob: Problem, entry: int, sel_capacity: int = 0) -> in
 
 def logo_ratio_capacity(prob: Problem, ratio: float) -> int:
     return int(library().logo_ratio_capacity(prob.c, ratio))
+
+
+def logo_attn_fwd_launches(prob: Problem) -> int:
+    return int(library().logo_attn_fwd_launches(prob.c))
 
 
 def _sel_mode(ratio, threshold, threshold_device, B):

@@ -343,6 +343,14 @@ __device__ __forceinline__ void permute_lp_head(const uint16_t *A, uint16_t *Ap,
     }
 }
 
+// The tensors of an item's branch: the one-launch layer's global items read
+// the global branch's Q / K / V and gain (qg, kg, vg, gain_g); every other
+// item, the standalone global launch included, reads q, k, v and gain.
+template <int MODE, int EPI>
+__device__ __forceinline__ constexpr bool global_tensors() {
+    return MODE == kModeGlobal && EPI == kEpiLayer;
+}
+
 // An item's indices and rows, and the loads of its Q fragments and fused-
 // epilogue inputs (issued here; waited for with the item's first K tile).
 //   Local / dense: tile jt of sequence b, rows = tokens jt*tpw ...
@@ -401,7 +409,8 @@ __device__ __forceinline__ void item_begin(const AttnArgs &a, int b, int hg, int
 
 #pragma unroll
     for (int rg = 0; rg < RG; rg++) {
-        const uint16_t *qp = a.q + (l.qtok[rg] * a.hq + u.head) * (int64_t)D + g * 8;
+        const uint16_t *qp = (global_tensors<MODE, EPI>() ? a.qg : a.q) +
+                             (l.qtok[rg] * a.hq + u.head) * (int64_t)D + g * 8;
 #pragma unroll
         for (int s = 0; s < D / 16; s++)
             qf[rg][s] = *(const bf16x8 *)(qp + s * 16);
@@ -440,14 +449,15 @@ __device__ __forceinline__ void item_begin(const AttnArgs &a, int b, int hg, int
 // The first K tile of an item into K buffer 0 (the K/V pipeline of attend_item
 // starts from it); every earlier read of K buffer 0 must have ended at a
 // barrier before this.
-template <int D, int W, int STG>
+template <int D, int MODE, int EPI, int W, int STG>
 __device__ __forceinline__ void item_first_k(const AttnArgs &a, Smem<D, STG> &sm, const ItemU &u) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);
     const int row_bytes = a.hkv * D * 2;
     Dma<D, W> dma;
     dma_plan<D, W>(dma, wave, lane, row_bytes);
-    const uint16_t *kv_k = a.k + (u.base * a.hkv + u.kvh) * (int64_t)D;
+    const uint16_t *kv_k =
+        (global_tensors<MODE, EPI>() ? a.kg : a.k) + (u.base * a.hkv + u.kvh) * (int64_t)D;
     dma_k<D, W>(&sm.k[0][0][0], dma, kv_k, u.T, u.kb_lo * kBlockN, row_bytes, wave);
 }
 
@@ -499,8 +509,9 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
     // K/V base of this sequence and KV head, and this thread's fixed byte
     // offsets inside a tile.
     const int row_bytes = a.hkv * D * 2;
-    const uint16_t *kv_k = a.k + (base * a.hkv + kvh) * (int64_t)D;
-    const uint16_t *kv_v = a.v + (base * a.hkv + kvh) * (int64_t)D;
+    constexpr bool kGT = global_tensors<MODE, EPI>();
+    const uint16_t *kv_k = (kGT ? a.kg : a.k) + (base * a.hkv + kvh) * (int64_t)D;
+    const uint16_t *kv_v = (kGT ? a.vg : a.v) + (base * a.hkv + kvh) * (int64_t)D;
     Dma<D, W> dma;
     dma_plan<D, W>(dma, wave, lane, row_bytes);
 
@@ -883,7 +894,8 @@ __device__ __forceinline__ void attend_item(const AttnArgs &a, Smem<D, STG> &sm,
             const int64_t tok = qtok[rg];
             const float p = ep_gate[rg];
             const int r = ep_rank[rg];
-            const float *gp = a.gain ? a.gain + head * D + g * 4 : nullptr;
+            const float *gain = kGT ? a.gain_g : a.gain;
+            const float *gp = gain ? gain + head * D + g * 4 : nullptr;
             // selected token in the local branch: keep (1-p) Norm^L in fp32
             const bool keep = MODE == kModeLocal && r >= 0;
             const float wgt = (MODE == kModeGlobal) ? p : (keep ? 1.f - p : 1.f);
@@ -1065,7 +1077,7 @@ void attn_kernel(const AttnArgs a) {
             ItemL l;
             bf16x8 qf[RG][D / 16];
             item_begin<D, MODE, EPI>(a, t.seq, item % a.n_hg, 0, t, u, l, qf);
-            item_first_k<D, W, STG>(a, sm, u);
+            item_first_k<D, MODE, EPI, W, STG>(a, sm, u);
             attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, false, no_prefetch);
         }
     } else if (MODE == kModeLocal) {
@@ -1121,7 +1133,7 @@ void attn_kernel(const AttnArgs a) {
         ItemL l;
         bf16x8 qf[RG][D / 16];
         item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
-        item_first_k<D, W, STG>(a, sm, u);
+        item_first_k<D, MODE, EPI, W, STG>(a, sm, u);
         bool waited = false;
         for (;;) {
             // The next item's Q, epilogue inputs and first K tile are loaded
@@ -1134,7 +1146,7 @@ void attn_kernel(const AttnArgs a) {
             attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, waited, [&] {
                 if (has_next) {
                     item_begin<D, MODE, EPI>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
-                    item_first_k<D, W, STG>(a, sm, nu);
+                    item_first_k<D, MODE, EPI, W, STG>(a, sm, nu);
                 }
                 return has_next;
             });
@@ -1158,7 +1170,7 @@ void attn_kernel(const AttnArgs a) {
         ItemL l;
         bf16x8 qf[RG][D / 16];
         item_begin<D, MODE, EPI>(a, b, hg, jt, SparseTile{}, u, l, qf);
-        item_first_k<D, W, STG>(a, sm, u);
+        item_first_k<D, MODE, EPI, W, STG>(a, sm, u);
         attend_item<D, MODE, EPI, W, STG>(a, sm, u, l, qf, false, no_prefetch);
     }
 }
@@ -1215,14 +1227,16 @@ __device__ __forceinline__ SparseTile load_tile_coherent(const SparseTile *p) {
 }
 
 // Items left in a local queue below which a workgroup takes its next item
-// only when it needs it (the 32 workgroups of an XCD share its queue).
-constexpr int kLateClaimItems = 32;
+// only when it needs it (the 32 or 64 workgroups of an XCD share its queue;
+// switching three items per workgroup before the end measured best).
+constexpr int kLateClaimItems = 96;
 // Bound of the wait for the work table (s_sleep 8 = 512 cycles per poll:
 // ~2 s), so that no workgroup can wait for ever.
 constexpr int kPlanSpinMax = 1 << 23;
 
-// The layer's two branches in one persistent launch (8-wave workgroups on
-// both, Hq / Hkv a multiple of 4).  The local branch's items are short and
+// The layer's two branches in one persistent launch, when both use W-wave
+// workgroups with the same tiles: W = 8 (one per CU) for Hq / Hkv a multiple
+// of 4, W = 4 (two per CU) for one query head per KV head.  The local branch's items are short and
 // many (every token tile x head group, ~17 KV steps at w = 1024), the global
 // branch's few and long (a tile's whole causal prefix), so running them one
 // launch after the other leaves the GPU partly idle at each launch's end
@@ -1247,22 +1261,15 @@ constexpr int kPlanSpinMax = 1 << 23;
 // Selected rows get (1-p) Norm^L in lc from their local item and p Norm^G in
 // gc from their global item, in either order; launch_sel_sum then writes
 // their output rows.
-template <int D>
-__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(2)))
+template <int D, int W>
+__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void layer_kernel(const AttnArgs a) {
-    constexpr int W = 8;
     constexpr int STG = stage_waves<kModeLocal, W>();
     __shared__ Smem<D, STG> sm;
     __shared__ int s_item, s_entries;
     const int tid = threadIdx.x, lane = tid & 63;
     const int x0 = blockIdx.x % kQueues;
     int32_t *const lq = a.ctl + 1;
-    // the global branch's tensors
-    AttnArgs ag = a;
-    ag.q = a.qg;
-    ag.k = a.kg;
-    ag.v = a.vg;
-    ag.gain = a.gain_g;
     auto no_prefetch = [] { return false; };
     // Local item -> (sequence, head group, token tile); false past the last
     // valid item (items are head group fastest, then the sequences' token
@@ -1303,6 +1310,13 @@ void layer_kernel(const AttnArgs a) {
         return it;
     };
 
+    // With two workgroups per CU (W = 4) the second half of the grid starts
+    // with local items, so that a CU runs a (memory-bound) global item and a
+    // (compute-bound) local item side by side rather than two of one kind.
+    bool local_first = false;
+    if constexpr (W == 4)
+        local_first = blockIdx.x >= gridDim.x / 2;
+
     // A. the work table, or one local item while it is built
     if (blockIdx.x == 0) {
         constexpr int E = D == 128 ? 512 : 256;
@@ -1316,20 +1330,22 @@ void layer_kernel(const AttnArgs a) {
         // then the flag
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
         __syncthreads();
-        if (tid == 0) {
+        if (tid == 0)
             __hip_atomic_store(&a.ctl[0], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            s_entries = __hip_atomic_load(&a.queue[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-    } else {
+    } else if (!local_first) {
         int b = 0, hg = 0, jt = 0;
         if (take_local(b, hg, jt) >= 0) {
             ItemU u;
             ItemL l;
             bf16x8 qf[RG][D / 16];
             item_begin<D, kModeLocal, kEpiLayer>(a, b, hg, jt, SparseTile{}, u, l, qf);
-            item_first_k<D, W, STG>(a, sm, u);
+            item_first_k<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u);
             attend_item<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u, l, qf, false, no_prefetch);
         }
+    }
+
+    // B. global items, once the table is there
+    auto global_phase = [&] {
         if (tid == 0) {
             // (no table after the bound: the global items are skipped)
             bool ready = false;
@@ -1342,12 +1358,10 @@ void layer_kernel(const AttnArgs a) {
                                                   __HIP_MEMORY_SCOPE_AGENT)
                               : 0;
         }
-    }
-    __syncthreads();
-
-    // B. global items
-    const int n_entries = __builtin_amdgcn_readfirstlane(s_entries);
-    if (n_entries > 0) {
+        __syncthreads();
+        const int n_entries = __builtin_amdgcn_readfirstlane(s_entries);
+        if (n_entries <= 0)
+            return;
         const int n_gitems = n_entries * a.n_hg;
         for (;;) {
             const int item = take_wg(a.queue + 1, n_gitems);
@@ -1357,79 +1371,93 @@ void layer_kernel(const AttnArgs a) {
             ItemU u;
             ItemL l;
             bf16x8 qf[RG][D / 16];
-            item_begin<D, kModeGlobal, kEpiLayer>(ag, t.seq, item % a.n_hg, 0, t, u, l, qf);
-            item_first_k<D, W, STG>(ag, sm, u);
-            attend_item<D, kModeGlobal, kEpiLayer, W, STG>(ag, sm, u, l, qf, false, no_prefetch);
+            item_begin<D, kModeGlobal, kEpiLayer>(a, t.seq, item % a.n_hg, 0, t, u, l, qf);
+            item_first_k<D, kModeGlobal, kEpiLayer, W, STG>(a, sm, u);
+            attend_item<D, kModeGlobal, kEpiLayer, W, STG>(a, sm, u, l, qf, false, no_prefetch);
         }
-    }
-
+    };
     // C. local items
-    int b = 0, hg = 0, jt = 0;
-    if (take_local(b, hg, jt) < 0)
-        return;
-    ItemU u;
-    ItemL l;
-    bf16x8 qf[RG][D / 16];
-    item_begin<D, kModeLocal, kEpiLayer>(a, b, hg, jt, SparseTile{}, u, l, qf);
-    item_first_k<D, W, STG>(a, sm, u);
-    bool waited = false;
-    // Claim of the next item from the own queue, issued when an item starts
-    // and resolved at its prefetch, so that the atomic's reply has arrived by
-    // then; once the own queue's remaining items are fewer than its
-    // workgroups, the next item is taken only at the prefetch instead, so
-    // that no workgroup holds an item it cannot start yet while the queues
-    // run dry.
-    bool early = true;
-    for (;;) {
-        int claim = 0;
-        if (early && tid == 0)
-            claim = atomicAdd(&lq[x0], 1);
-        ItemU nu;
-        ItemL nl;
-        int nxt = -1;
-        attend_item<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u, l, qf, waited, [&] {
-            if (tid < 64) {
-                int nb, nhg, njt;
-                int it = early ? x0 + kQueues * __builtin_amdgcn_readfirstlane(claim) : -1;
-                if (!decode(it, nb, nhg, njt)) {
-                    do {
-                        it = queue_take(lq, a.n_items, x0);
-                    } while (it >= 0 && !decode(it, nb, nhg, njt));
+    auto local_phase = [&] {
+        int b = 0, hg = 0, jt = 0;
+        if (take_local(b, hg, jt) < 0)
+            return;
+        ItemU u;
+        ItemL l;
+        bf16x8 qf[RG][D / 16];
+        item_begin<D, kModeLocal, kEpiLayer>(a, b, hg, jt, SparseTile{}, u, l, qf);
+        item_first_k<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u);
+        bool waited = false;
+        // Claim of the next item from the own queue, issued when an item
+        // starts and resolved at its prefetch, so that the atomic's reply
+        // has arrived by then; once the own queue's remaining items are fewer
+        // than kLateClaimItems, the next item is taken only at the prefetch
+        // instead, so that no workgroup holds an item it cannot start yet
+        // while the queues run dry.
+        bool early = true;
+        for (;;) {
+            int claim = 0;
+            if (early && tid == 0)
+                claim = atomicAdd(&lq[x0], 1);
+            ItemU nu;
+            ItemL nl;
+            int nxt = -1;
+            attend_item<D, kModeLocal, kEpiLayer, W, STG>(a, sm, u, l, qf, waited, [&] {
+                if (tid < 64) {
+                    int nb, nhg, njt;
+                    int it = early ? x0 + kQueues * __builtin_amdgcn_readfirstlane(claim) : -1;
+                    if (!decode(it, nb, nhg, njt)) {
+                        do {
+                            it = queue_take(lq, a.n_items, x0);
+                        } while (it >= 0 && !decode(it, nb, nhg, njt));
+                    }
+                    if (lane == 0)
+                        s_item = it;
                 }
-                if (lane == 0)
-                    s_item = it;
-            }
-            // s_item is written again only at the next item's prefetch,
-            // after that item's barriers
-            __syncthreads();
-            nxt = __builtin_amdgcn_readfirstlane(s_item);
+                // s_item is written again only at the next item's prefetch,
+                // after that item's barriers, or by take_wg after a barrier
+                __syncthreads();
+                nxt = __builtin_amdgcn_readfirstlane(s_item);
+                if (nxt < 0)
+                    return false;
+                early = nxt + kQueues * kLateClaimItems < a.n_items;
+                int nb = 0, nhg = 0, njt = 0;
+                decode(nxt, nb, nhg, njt);
+                item_begin<D, kModeLocal, kEpiLayer>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
+                item_first_k<D, kModeLocal, kEpiLayer, W, STG>(a, sm, nu);
+                return true;
+            });
             if (nxt < 0)
-                return false;
-            early = nxt + kQueues * kLateClaimItems < a.n_items;
-            int nb = 0, nhg = 0, njt = 0;
-            decode(nxt, nb, nhg, njt);
-            item_begin<D, kModeLocal, kEpiLayer>(a, nb, nhg, njt, SparseTile{}, nu, nl, qf);
-            item_first_k<D, W, STG>(a, sm, nu);
-            return true;
-        });
-        if (nxt < 0)
-            break;
-        waited = true;
-        u = nu;
-        l = nl;
+                break;
+            waited = true;
+            u = nu;
+            l = nl;
+        }
+    };
+    if (local_first) {
+        local_phase();
+        global_phase();
+    } else {
+        global_phase();
+        local_phase();
     }
 }
 
 template <int D>
-hipError_t launch_layer_d(const AttnArgs &a, int grid, hipStream_t s) {
-    hipLaunchKernelGGL((layer_kernel<D>), dim3(grid), dim3(512), 0, s, a);
+hipError_t launch_layer_d(int waves, const AttnArgs &a, int grid, hipStream_t s) {
+    if (waves == 8)
+        hipLaunchKernelGGL((layer_kernel<D, 8>), dim3(grid), dim3(512), 0, s, a);
+    else
+        hipLaunchKernelGGL((layer_kernel<D, 4>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 template <int D>
-int layer_blocks_per_cu_d() {
+int layer_blocks_per_cu_d(int waves) {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, layer_kernel<D>, 512, 0) != hipSuccess)
+    const hipError_t e =
+        waves == 8 ? hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, layer_kernel<D, 8>, 512, 0)
+                   : hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, layer_kernel<D, 4>, 256, 0);
+    if (e != hipSuccess)
         return 1;
     return n > 0 ? n : 1;
 }
@@ -1492,14 +1520,15 @@ int attention_blocks_per_cu(int mode, int head_dim, int waves) {
     return head_dim == 128 ? blocks_per_cu_d<128>(mode, waves) : blocks_per_cu_d<64>(mode, waves);
 }
 
-hipError_t launch_layer(int head_dim, const AttnArgs &a, int grid, hipStream_t s) {
+hipError_t launch_layer(int head_dim, int waves, const AttnArgs &a, int grid, hipStream_t s) {
     if (grid <= 0)
         return hipSuccess;
-    return head_dim == 128 ? launch_layer_d<128>(a, grid, s) : launch_layer_d<64>(a, grid, s);
+    return head_dim == 128 ? launch_layer_d<128>(waves, a, grid, s)
+                           : launch_layer_d<64>(waves, a, grid, s);
 }
 
-int layer_blocks_per_cu(int head_dim) {
-    return head_dim == 128 ? layer_blocks_per_cu_d<128>() : layer_blocks_per_cu_d<64>();
+int layer_blocks_per_cu(int head_dim, int waves) {
+    return head_dim == 128 ? layer_blocks_per_cu_d<128>(waves) : layer_blocks_per_cu_d<64>(waves);
 }
 
 }  // namespace logo

@@ -422,18 +422,19 @@ int blocks_per_cu(int mode, int head_dim, int waves) {
 }
 
 // Persistent grid of the one-launch layer (occupancy queried once per head
-// dim), a multiple of the work queues.
-std::once_flag g_layer_occ_once[2];
-int g_layer_occ[2];
+// dim and workgroup size), a multiple of the work queues.
+std::once_flag g_layer_occ_once[2][2];
+int g_layer_occ[2][2];
 
-logo_status layer_grid(int head_dim, int &grid) {
+logo_status layer_grid(int head_dim, int waves, int &grid) {
     int cus = 0;
     const logo_status st = device_cus(cus);
     if (st != LOGO_OK)
         return st;
-    const int di = head_dim == 128 ? 1 : 0;
-    std::call_once(g_layer_occ_once[di], [&] { g_layer_occ[di] = layer_blocks_per_cu(head_dim); });
-    grid = cus * g_layer_occ[di];
+    const int di = head_dim == 128 ? 1 : 0, wi = waves == 8 ? 1 : 0;
+    std::call_once(g_layer_occ_once[di][wi],
+                   [&] { g_layer_occ[di][wi] = layer_blocks_per_cu(head_dim, waves); });
+    grid = cus * g_layer_occ[di][wi];
     grid = ((grid + kQueues - 1) / kQueues) * kQueues;
     return LOGO_OK;
 }
@@ -613,38 +614,73 @@ logo_status run_global(const logo_problem *p, const logo_bf16 *q, const logo_bf1
         s);
 }
 
-// The one-launch layer (both branches with 8-wave workgroups): the local
-// items and the global work table's items in one persistent grid, whose
-// first workgroup builds the table (layer_kernel).  gc / ctl: the compact
-// p Norm^G buffer and the launch's control words (cleared by the selection
-// kernel before it).  The selected rows' output is written afterwards by
-// launch_sel_sum.
-logo_status run_layer(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
-                      const logo_bf16 *v, const logo_bf16 *qg, const logo_bf16 *kg,
-                      const logo_bf16 *vg, const int32_t *sel_idx, const int32_t *cu_sel,
-                      int32_t cap, const FusedEpi *f, const float *gain_local,
-                      const float *gain_global, float *gc, int32_t *ctl, char *glob_ws,
-                      hipStream_t s) {
-    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, 8);
-    PlanArgs pa;
-    int grid_g = 0;
-    logo_status st = global_plan(p, sel_idx, cu_sel, cap, glob_ws, pa, grid_g);
+// logo_attn_fwd's launches: both branches in one launch (layer_kernel) when
+// their workgroups have the same waves and the local branch gives each
+// persistent workgroup at least kLayerMinLocalBlocks KV blocks of work --
+// enough to cover the work table, which the launch's first workgroup builds
+// (~15-20 us) while the others run local items; otherwise the local launch,
+// then the global one.  LOGO_FWD_LAUNCHES=1 or 2 picks one or the other where
+// both are possible (tests run both).
+constexpr long long kLayerMinLocalBlocks = 8;
+struct LayerPlan {
+    int waves = 0, grid = 0;
+    long long items = 0;          // local items (an upper bound; the valid ones a prefix)
+    long long extra_blocks = 0;   // their KV blocks, ~(w + tpw) / 64 + 1 each
+};
+
+logo_status layer_plan(const logo_problem *p, LayerPlan &lp) {
+    lp = LayerPlan{};
+    const int waves = layer_waves(p->num_q_heads, p->num_kv_heads);
+    if (waves == 0 || p->total_tokens == 0)
+        return LOGO_OK;
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, waves);
+    int grid = 0;
+    const logo_status st = layer_grid(p->head_dim, waves, grid);
     if (st != LOGO_OK)
         return st;
-    int grid = 0;
-    if ((st = layer_grid(p->head_dim, grid)) != LOGO_OK)
-        return st;
-    // local items: head groups x the sequences' token tiles back to back (an
-    // upper bound; the valid ones are a prefix), each ~(w + tpw) / 64 + 1 KV
-    // blocks, which the table's split threshold counts as the grid's other
-    // work
     const long long tiles = (p->total_tokens + tp.tpw - 1) / tp.tpw;
-    const long long items = (long long)tp.n_hg * (tiles + p->num_seqs);
-    if (items >= (1LL << 31))
-        return LOGO_ERR_UNSUPPORTED;
     const long long span = std::min<long long>(p->window, p->max_seqlen) + tp.tpw;
-    pa.grid_wgs = grid;
-    pa.extra_blocks = (int64_t)tp.n_hg * tiles * ((span + kBlockN - 1) / kBlockN + 1);
+    lp.waves = waves;
+    lp.grid = grid;
+    lp.items = (long long)tp.n_hg * (tiles + p->num_seqs);
+    lp.extra_blocks = (long long)tp.n_hg * tiles * ((span + kBlockN - 1) / kBlockN + 1);
+    return LOGO_OK;
+}
+
+bool use_one_launch(const LayerPlan &lp) {
+    if (lp.waves == 0)
+        return false;
+    const char *e = std::getenv("LOGO_FWD_LAUNCHES");
+    if (e && e[0] == '1')
+        return true;
+    if (e && e[0] == '2')
+        return false;
+    return lp.extra_blocks >= kLayerMinLocalBlocks * lp.grid;
+}
+
+// The one-launch layer: the local items and the global work table's items in
+// one persistent grid, whose first workgroup builds the table
+// (layer_kernel).  gc / ctl: the compact p Norm^G buffer and the launch's
+// control words (cleared by the selection kernel before it).  The selected
+// rows' output is written afterwards by launch_sel_sum.
+logo_status run_layer(const logo_problem *p, const LayerPlan &lp, const logo_bf16 *q,
+                      const logo_bf16 *k, const logo_bf16 *v, const logo_bf16 *qg,
+                      const logo_bf16 *kg, const logo_bf16 *vg, const int32_t *sel_idx,
+                      const int32_t *cu_sel, int32_t cap, const FusedEpi *f,
+                      const float *gain_local, const float *gain_global, float *gc, int32_t *ctl,
+                      char *glob_ws, hipStream_t s) {
+    const TilePlan tp = make_tile_plan(p->num_q_heads, p->num_kv_heads, lp.waves);
+    PlanArgs pa;
+    int grid_g = 0;
+    const logo_status st = global_plan(p, sel_idx, cu_sel, cap, glob_ws, pa, grid_g);
+    if (st != LOGO_OK)
+        return st;
+    if (lp.items >= (1LL << 31))
+        return LOGO_ERR_UNSUPPORTED;
+    // the local items count into the table's split threshold as the grid's
+    // other work
+    pa.grid_wgs = lp.grid;
+    pa.extra_blocks = (int64_t)lp.extra_blocks;
     AttnArgs a = make_args(p, tp);
     a.q = q;
     a.k = k;
@@ -662,7 +698,7 @@ logo_status run_layer(const logo_problem *p, const logo_bf16 *q, const logo_bf16
     a.queue = pa.queue;
     a.split_cnt = pa.split_cnt;
     a.partial = (float *)(glob_ws + global_ws(p, cap).partial);
-    a.n_items = (int32_t)items;
+    a.n_items = (int32_t)lp.items;
     a.qphi = f->qphi;
     a.aperm = f->aperm;
     a.qphi_s = f->qs;
@@ -671,7 +707,7 @@ logo_status run_layer(const logo_problem *p, const logo_bf16 *q, const logo_bf16
         a.prep_wgs = p->num_q_heads;
         a.prep_a = f->lp_a;
     }
-    return hip_status(launch_layer(p->head_dim, a, grid, s), s);
+    return hip_status(launch_layer(p->head_dim, lp.waves, a, lp.grid, s), s);
 }
 
 logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 *k,
@@ -730,8 +766,10 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
     // builds the global branch's tile plan.  Then the global branch finishes
     // the selected rows.
     const bool with_plan = p->total_tokens > 0 && cap > 0;
-    if (with_plan && local_waves(p->num_q_heads, p->num_kv_heads) == 8 &&
-        global_waves(p->num_q_heads, p->num_kv_heads) == 8) {
+    LayerPlan lp;
+    if (with_plan && (st = layer_plan(p, lp)) != LOGO_OK)
+        return st;
+    if (with_plan && use_one_launch(lp)) {
         // both branches in one launch, then the selected rows' sums
         int32_t *ctl = (int32_t *)(base + w.ctl);
         float *lc = (float *)(base + w.lc), *gc = (float *)(base + w.gc);
@@ -739,8 +777,8 @@ logo_status fwd_impl(const logo_problem *p, const logo_bf16 *q, const logo_bf16 
                         s, ctl, kLayerCtlWords);
         if (st != LOGO_OK || (st = mark(1)) != LOGO_OK)
             return st;
-        st = run_layer(p, q, k, v, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap, &fe,
-                       gain_local, gain_global, gc, ctl, base + w.glob_ws, s);
+        st = run_layer(p, lp, q, k, v, q_g ? q_g : q, k_g ? k_g : k, v_g ? v_g : v, sel, cus, cap,
+                       &fe, gain_local, gain_global, gc, ctl, base + w.glob_ws, s);
         if (st != LOGO_OK || (st = mark(2)) != LOGO_OK || (st = mark(3)) != LOGO_OK)
             return st;
         st = hip_status(launch_sel_sum(cap, p->num_q_heads, p->head_dim, cus, p->num_seqs, sel, lc,
@@ -787,6 +825,15 @@ const char *logo_status_str(logo_status s) {
 }
 
 const char *logo_version(void) { return "0.1.0"; }
+
+int logo_attn_fwd_launches(const logo_problem *p) {
+    if (check_problem(p) != LOGO_OK)
+        return -1;
+    LayerPlan lp;
+    if (layer_plan(p, lp) != LOGO_OK)
+        return -1;
+    return use_one_launch(lp) ? 1 : 2;
+}
 
 int64_t logo_ratio_capacity(const logo_problem *p, double ratio) {
     if (check_problem(p) != LOGO_OK || !(ratio >= 0.0 && ratio <= 1.0))

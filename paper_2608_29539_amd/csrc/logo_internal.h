@@ -190,11 +190,16 @@ int attention_blocks_per_cu(int mode, int head_dim, int waves);
 hipError_t launch_sparse_plan(const int32_t *cu_seqlens, int num_seqs, const PlanArgs &plan,
                               hipStream_t s);
 
-// The one-launch layer (8-wave workgroups on both branches, i.e. Hq / Hkv a
-// multiple of 4): grid persistent workgroups; a.n_items local items, the
-// global items of the work table that workgroup 0 builds (a.plan).
-hipError_t launch_layer(int head_dim, const AttnArgs &a, int grid, hipStream_t s);
-int layer_blocks_per_cu(int head_dim);
+// The one-launch layer, for problems whose two branches use workgroups of
+// the same waves (and so the same tiles): 8 when Hq / Hkv is a multiple of 4,
+// 4 when Hq = Hkv (layer_waves; 0 = not eligible).  grid persistent
+// workgroups; a.n_items local items, the global items of the work table that
+// workgroup 0 builds (a.plan).
+inline int layer_waves(int hq, int hkv) {
+    return local_waves(hq, hkv) == global_waves(hq, hkv) ? local_waves(hq, hkv) : 0;
+}
+hipError_t launch_layer(int head_dim, int waves, const AttnArgs &a, int grid, hipStream_t s);
+int layer_blocks_per_cu(int head_dim, int waves);
 // out[sel_idx[r]] = bf16(lc[r] + gc[r]) for the selected ranks r below
 // min(cu_sel[B], cap) (read on the device).
 hipError_t launch_sel_sum(int32_t cap, int hq, int head_dim, const int32_t *cu_sel, int num_seqs,

@@ -332,7 +332,7 @@ def _layer(pk, w: synth.Workload, x=None, n_sel_rows=96, n_other=96, full=False,
     return out
 
 
-def test_layer_tiny_full(pk):
+def test_layer_tiny_full(pk, fwd_launches):
     _layer(pk, synth.WORKLOADS["T1k-tiny"], full=True)
 
 
@@ -347,7 +347,7 @@ def test_layer_longest_sampled(pk):
 
 
 @pytest.mark.parametrize("ci", range(4))
-def test_layer_small_full(pk, ci):
+def test_layer_small_full(pk, ci, fwd_launches):
     cases = [((1000, 23, 1), 8, 2, 128, 100, 0.3), ((513,), 4, 4, 64, 1, 0.9),
              ((640, 0, 300), 8, 8, 128, 2000, 0.5), ((129, 257), 16, 2, 64, 64, 1.0)]
     seqlens, hq, hkv, d, win, r = cases[ci]
@@ -355,7 +355,7 @@ def test_layer_small_full(pk, ci):
     _layer(pk, w, full=True)
 
 
-def test_layer_distinct_global_tensors(pk):
+def test_layer_distinct_global_tensors(pk, fwd_launches):
     w = synth.small_workload((900, 400), 8, 2, 128, 96, 0.4, seed=1600)
     x = synth.make_inputs(w, distinct_global=True)
     _layer(pk, w, x=x, full=True)
@@ -395,7 +395,7 @@ def test_layer_all_sequences_empty(pk):
     assert o_l.shape == (0, 8, 64) and o.shape == (0, 8, 64) and dense.shape == (0, 8, 64)
 
 
-def test_single_selected_at_position_zero(pk):
+def test_single_selected_at_position_zero(pk, fwd_launches):
     import torch
     w = synth.small_workload((300,), 4, 2, 128, 32, 0.0, seed=1700)
     x = synth.make_inputs(w)
@@ -413,14 +413,14 @@ def test_single_selected_at_position_zero(pk):
 
 
 @pytest.mark.parametrize("case", ["late-rows-split", "none-selected", "many-seqs"])
-def test_layer_one_launch_cases(pk, case):
-    """The one-launch layer (Hq / Hkv a multiple of 4), every output element
-    against the oracle: a long sequence whose few selected rows all sit near
-    its end (their global tiles are longer than the launch's mean load, so
-    the work table splits each over four KV ranges whose partials are merged
-    inside the launch), a threshold no gate passes (no global item: the
-    local items alone), and a batch of 40 short ragged sequences (empty ones
-    included)."""
+def test_layer_launch_cases(pk, case, fwd_launches):
+    """Both launch plans of the layer (Hq / Hkv a multiple of 4), every output
+    element against the oracle: a long sequence whose few selected rows all
+    sit near its end (in one launch their global tiles are longer than the
+    launch's mean load, so the work table splits each over four KV ranges
+    whose partials are merged inside the launch), a threshold no gate passes
+    (no global item: the local items alone), and a batch of 40 short ragged
+    sequences (empty ones included)."""
     import torch
     if case == "late-rows-split":
         w = synth.small_workload((20000,), 8, 2, 128, 256, 0.0, seed=2100)
@@ -449,11 +449,35 @@ def test_layer_one_launch_cases(pk, case):
     assert n == {"late-rows-split": 100, "none-selected": 0}.get(case, n)
     assert sel.cpu().numpy()[:n].tolist() == ref["sel_idx"][:n].tolist()
     st = err_stats(torch_bf16_to_f64(out), ref["out"])
-    report(f"one-launch {case} n_sel={n}", st)
+    assert pk.logo_attn_fwd_launches(prob) == fwd_launches
+    report(f"launches={fwd_launches} {case} n_sel={n}", st)
     assert st["max_abs"] <= MAX_ABS and st["mean_abs"] <= MEAN_ABS
 
 
-def test_determinism(pk):
+def test_fwd_launch_plan(pk, monkeypatch):
+    """logo_attn_fwd_launches: one launch where both branches use the same
+    workgroups and the local work covers building the work table, two
+    otherwise; LOGO_FWD_LAUNCHES forces the choice only where both plans
+    apply."""
+    import torch
+    monkeypatch.delenv("LOGO_FWD_LAUNCHES", raising=False)
+
+    def plan(seqlens, hq, hkv, d, win):
+        cu = np.concatenate([[0], np.cumsum(seqlens)]).astype(np.int32)
+        prob = pk.Problem(torch.from_numpy(cu).cuda(), hq, hkv, d, win, cu_seqlens_host=cu)
+        return pk.logo_attn_fwd_launches(prob)
+    assert plan((32768,), 32, 8, 128, 1024) == 1          # T32k-gqa
+    assert plan((8192, 8192), 16, 16, 128, 512) == 1      # T8k-b2 (MHA)
+    assert plan((1024,), 4, 4, 64, 128) == 2              # T1k-tiny: too little local work
+    assert plan((32768,), 32, 16, 128, 1024) == 2         # G = 2: different workgroups
+    monkeypatch.setenv("LOGO_FWD_LAUNCHES", "1")
+    assert plan((1024,), 4, 4, 64, 128) == 1
+    assert plan((32768,), 32, 16, 128, 1024) == 2
+    monkeypatch.setenv("LOGO_FWD_LAUNCHES", "2")
+    assert plan((32768,), 32, 8, 128, 1024) == 2
+
+
+def test_determinism(pk, fwd_launches):
     import torch
     w = synth.small_workload((3000, 1500), 8, 2, 128, 256, 0.25, seed=1800)
     x = synth.make_inputs(w)
@@ -465,7 +489,7 @@ def test_determinism(pk):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
-def test_layer_gains_fused_epilogue(pk):
+def test_layer_gains_fused_epilogue(pk, fwd_launches):
     """Per-branch ContextNorm gains through the fused epilogues of logo_attn_fwd."""
     import torch
     w = synth.small_workload((1100, 333), 8, 2, 128, 160, 0.3, seed=1900)
@@ -491,7 +515,7 @@ def test_layer_gains_fused_epilogue(pk):
     assert st["max_abs"] <= MAX_ABS * gmax and st["mean_abs"] <= MEAN_ABS * gmax
 
 
-def test_layer_threshold_overflow(pk):
+def test_layer_threshold_overflow(pk, fwd_launches):
     """Threshold mode with a capacity below the number of passing tokens:
     the first sel_capacity selections are fused, the rest are treated as
     unselected, cu_sel still counts them all."""

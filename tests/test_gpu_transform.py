@@ -128,7 +128,7 @@ def test_branch_transform_identity_and_rows(pk, d):
     assert (got[untouched] == 3.0).all()
 
 
-def test_layer_with_lp_transforms(pk):
+def test_layer_with_lp_transforms(pk, fwd_launches):
     """The layer fed with GPU LP transforms (K^G, V^G for every token, Q^G for
     the selected rows only) against the oracle layer fed with the oracle's
     transforms rounded to bf16."""
@@ -175,7 +175,7 @@ QPHI_CASES = [
 
 
 @pytest.mark.parametrize("ci", range(len(QPHI_CASES)))
-def test_layer_fused_query_transform(pk, ci):
+def test_layer_fused_query_transform(pk, ci, fwd_launches):
     """logo_attn_fwd_qphi: the global kernel applies LP / SO to the selected
     queries as it loads them (Eq. branch-transform).  Against the oracle
     layer fed with the oracle's transform of Q rounded to bf16 (the layer
