@@ -71,7 +71,7 @@ struct alignas(16) SparseTile {
 };
 constexpr int kMaxSplit = 4;          // KV ranges per tile at most
 constexpr int kSplitDiv = 1;          // split tiles longer than 1/kSplitDiv of a workgroup's mean load
-constexpr int kMinSplitBlocks = 16;   // never split tiles of 16 KV blocks or fewer
+constexpr int kMinSplitBlocks = 4;    // never split tiles of 4 KV blocks or fewer
 constexpr int kSplitGridRef = 512;    // persistent workgroups the split slots are sized for
 
 // Partial result of one split entry for one head group, lane-major: the
