@@ -17,7 +17,9 @@
 // of one KV group, which keeps the tile's token span -- and so its
 // causal-diagonal band -- short.  The local and global modes run persistent
 // workgroups (static item striding with a prefetch of the next item, and
-// per-XCD work queues, respectively).
+// per-XCD work queues, respectively).  layer_kernel runs the items of both
+// branches in one persistent launch (global items longest first, local items
+// filling in behind them), where the two use workgroups of the same waves.
 //
 // MFMA formulation (v_mfma_f32_32x32x16_bf16, lane l: column l%32, rows
 // 8*(i/4) + 4*(l/32) + i%4 of the 32x32 accumulator).  The kernel computes
