@@ -94,6 +94,16 @@ def test_problem_validation(lib):
     assert lib.logo_local_attn(p.c, None, FAKE, FAKE, FAKE, None) == ERR_NULL
 
 
+def test_fwd_launches_rejects_invalid_problems(lib):
+    """logo_attn_fwd_launches validates the problem before any device query:
+    -1 for a NULL or invalid problem (the plan itself needs the GPU's CU
+    count and is checked in the GPU suite)."""
+    assert lib.logo_attn_fwd_launches(None) == -1
+    assert lib.logo_attn_fwd_launches(Prob(hq=6, hkv=4).c) == -1
+    assert lib.logo_attn_fwd_launches(Prob(d=96).c) == -1
+    assert lib.logo_attn_fwd_launches(Prob(window=0).c) == -1
+
+
 def test_select_validation(lib):
     p = Prob()
     ws_need = lib.logo_workspace_bytes(p.c, 0, 0)
