@@ -23,7 +23,10 @@ Reported (one JSON line on stdout):
                  records on the layer's stream, in a second timed run of the
                  same steps (the headline steps run the plain entry point,
                  with no events inside a step)
-  cpu_baseline   the fp64 oracle on a bounded sample of the same workload
+  global_kernel_alone  with the one-launch layer: the query-sparse global
+                 kernel by itself (the two-launch plan's last stage, the
+                 same selection), its TFLOP/s and fraction of that peak
+  cpu_baseline  the fp64 oracle on a bounded sample of the same workload
 """
 from __future__ import annotations
 
@@ -624,6 +627,41 @@ def main(argv=None):
             "global_tflops": round(fl * p_global / (dom_ms * 1e-3) / 1e12, 2) if p_global else 0.0}
     dom_tflops = dom_flops / (dom_ms * 1e-3) / 1e12
 
+    # The query-sparse global kernel on its own: where the layer runs both
+    # branches in one launch, the same K profiled steps again under the
+    # two-launch plan (LOGO_FWD_LAUNCHES=2), whose last stage is the global
+    # kernel alone, on the same selection.
+    global_alone = None
+    if one_launch and not args.no_extra and p_global:
+        prev = os.environ.get("LOGO_FWD_LAUNCHES")
+        os.environ["LOGO_FWD_LAUNCHES"] = "2"
+        try:
+            assert pk.logo_attn_fwd_launches(prob) == 2
+            for _ in range(args.block_warmup):
+                step()
+            torch.cuda.synchronize()
+            start.record()
+            for i in range(n_ev):
+                step(i)
+            end.record()
+            torch.cuda.synchronize()
+            ms2 = start.elapsed_time(end) / args.steps
+            st2 = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(n_ev)]))
+                   for j, n in enumerate(("select", "local", "plan", "global"))}
+        finally:
+            if prev is None:
+                os.environ.pop("LOGO_FWD_LAUNCHES", None)
+            else:
+                os.environ["LOGO_FWD_LAUNCHES"] = prev
+        g_tf = fl * p_global / (st2["global"] * 1e-3) / 1e12
+        global_alone = {"kernel": f"attn_kernel<{d}, global> (two-launch plan)",
+                        "ms_per_step_with_stage_events": round(ms2, 4),
+                        "stage_ms": {k: round(v, 4) for k, v in st2.items()},
+                        "global_tflops": round(g_tf, 2),
+                        "global_frac": round(g_tf / PEAK_BF16_TFLOPS, 4),
+                        "local_tflops": round(fl * p_local / (st2["local"] * 1e-3) / 1e12, 2)}
+        log(f"two-launch plan: {global_alone}")
+
     # Dense causal baseline (the DENSE kernel, and the query-sparse kernel
     # with every row selected; the faster is t_dense), timed under the same
     # clock state as the layer: after one untimed call of each, --rounds
@@ -783,6 +821,7 @@ def main(argv=None):
         "ms_per_step_with_stage_events": round(ms_step_profiled, 4),
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         **branch_tflops,
+        "global_kernel_alone": global_alone,
         "dense": {k: round(v, 4) for k, v in dense.items()} if dense else None,
         "roofline": roofline,
         "cpu_baseline": cpu,
