@@ -681,15 +681,24 @@ __global__ __launch_bounds__(256) void fusion_bwd_kernel(const FusionBwdArgs a) 
 #pragma unroll
                 for (int e = 0; e < 8; e++) {
                     dO[e] = gv[e] * wgt * dr[e] * ir - o[e] * k3;
-                    dl = fmaf(dO[e], o[e], dl);
                     gacc[e] = fmaf(wgt * dr[e] * ir, o[e], gacc[e]);
+                }
+                // The attention backward takes dO in bf16 (dP = dO V^T);
+                // Delta = dO . O takes the same rounded values, so that
+                // sum_j dS_j = sum_j P_j (dP_j - Delta) vanishes as it does
+                // in exact arithmetic (with one visible key, dS = 0).
+                const u32x4 dob = u32x4{pack_bf16x2(dO[0], dO[1]), pack_bf16x2(dO[2], dO[3]),
+                                        pack_bf16x2(dO[4], dO[5]), pack_bf16x2(dO[6], dO[7])};
+#pragma unroll
+                for (int i = 0; i < 4; i++) {
+                    dl = fmaf(__uint_as_float(dob[i] << 16), o[2 * i], dl);
+                    dl = fmaf(__uint_as_float(dob[i] & 0xFFFF0000u), o[2 * i + 1], dl);
                 }
                 dl = row_sum<D>(dl);
                 side += (br ? 1.f : -1.f) * sd * ir;
                 const int64_t row = br ? rank : tok;
                 uint16_t *dst = (br ? a.dog : a.dol) + (row * a.hq + h) * D + c0;
-                *(u32x4 *)dst = u32x4{pack_bf16x2(dO[0], dO[1]), pack_bf16x2(dO[2], dO[3]),
-                                      pack_bf16x2(dO[4], dO[5]), pack_bf16x2(dO[6], dO[7])};
+                *(u32x4 *)dst = dob;
                 if (lead)
                     (br ? a.delta_g : a.delta_l)[(int64_t)h * (br ? a.cap : a.n) + row] = dl;
                 if (br == 1)

@@ -93,6 +93,15 @@ def run_case(pk, w, *, ratio=None, threshold=None, distinct=False, gains=False, 
     worst = {}
     for nm in names:
         e = grad_err(grads[nm].cpu().numpy(), ref[nm])
+        if nm == "dgate" and n_sel and not np.any(ref[nm]):
+            # identical branches (window >= T, the same tensors, no gains):
+            # dL/dp_t = dout . (Norm^G - Norm^L) is 0 in exact arithmetic, and
+            # the GPU's value is the rounding difference of its two branch
+            # kernels; measured against the size of one term, sum |dout * out|
+            term = np.abs(dout64 * fref["out"]).sum(axis=(1, 2))
+            got = grads[nm].cpu().numpy().astype(np.float64)
+            e = dict(rel_l2=float(np.linalg.norm(got) / np.linalg.norm(term)),
+                     rel_max=float(np.abs(got).max() / term.max()))
         worst[nm] = e
         print(f"[bwd {tag}] {nm}: rel_l2={e['rel_l2']:.3g} rel_max={e['rel_max']:.3g}",
               flush=True)
@@ -120,6 +129,47 @@ def test_backward_small(pk, ci):
     lens, hq, hkv, d, win, ratio, thr, distinct, gains = BWD_CASES[ci]
     w = synth.small_workload(lens, hq, hkv, d, win, ratio or 0.0, seed=5000 + ci)
     run_case(pk, w, ratio=ratio, threshold=thr, distinct=distinct, gains=gains, tag=f"case{ci}")
+
+
+def _bwd_sweep_cases(n=16, seed=5151):
+    """Seeded random shapes for the training forward + backward: 1-3 ragged
+    sequences (empty, one token, tile edges, several tiles), each G in
+    {1, 2, 4, 8} with each d in {64, 128} twice, 1-4 KV heads, windows from 1
+    to beyond T, ratio or threshold mode, distinct global tensors and gains
+    drawn at random."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B = int(rng.integers(1, 4))
+        lens = [int(t) for t in rng.choice([0, 1, 63, 64, 65, 255, 700, 1500], size=B)]
+        if sum(lens) == 0:
+            lens[-1] = 200
+        hkv = int(rng.choice([1, 2, 4]))
+        G = (1, 2, 4, 8)[i % 4]
+        d = (64, 128)[(i // 4) % 2]
+        win = int(rng.choice([1, 16, 64, 65, 200, 1024, 5000]))
+        if rng.random() < 0.75:
+            ratio, thr = float(rng.choice([0.0, 0.02, 0.125, 0.3, 0.75, 1.0])), None
+        else:
+            ratio, thr = None, float(rng.choice([0.25, 0.5, 0.9]))
+        cases.append((tuple(lens), hkv * G, hkv, d, win, ratio, thr, bool(rng.random() < 0.5),
+                      bool(rng.random() < 0.5)))
+    return cases
+
+
+BWD_SWEEP = _bwd_sweep_cases()
+
+
+@pytest.mark.parametrize("ci", range(len(BWD_SWEEP)),
+                         ids=[f"T{'-'.join(map(str, c[0]))}_h{c[1]}-{c[2]}_d{c[3]}_w{c[4]}"
+                              f"_{'r' + str(c[5]) if c[6] is None else 'thr' + str(c[6])}"
+                              f"{'_distinct' if c[7] else ''}{'_gains' if c[8] else ''}"
+                              for c in BWD_SWEEP])
+def test_backward_random_sweep(pk, ci):
+    lens, hq, hkv, d, win, ratio, thr, distinct, gains = BWD_SWEEP[ci]
+    w = synth.small_workload(lens, hq, hkv, d, win, ratio or 0.0, seed=5200 + ci)
+    run_case(pk, w, ratio=ratio, threshold=thr, distinct=distinct, gains=gains,
+             tag=f"sweep{ci}")
 
 
 DENSE_CASES = [
