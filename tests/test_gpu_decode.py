@@ -84,6 +84,42 @@ def test_decode_small(pk, ci):
     run_case(pk, w, thr, distinct=distinct, gains=gains, tag=f"case{ci}")
 
 
+def _decode_sweep_cases(n=24, seed=6161):
+    """Seeded random decoding steps: 1-12 caches of 1 to 9000 tokens (tile
+    edges included), each G in {1, 2, 4, 8} with each d in {64, 128} three
+    times, 1-8 KV heads, windows from 1 to beyond the cache, thresholds from
+    -inf to +inf, distinct global tensors and gains drawn at random."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B = int(rng.integers(1, 13))
+        lens = tuple(int(t) for t in rng.choice([1, 2, 63, 64, 65, 255, 256, 257, 1000, 4097,
+                                                 9000], size=B))
+        hkv = int(rng.choice([1, 2, 4, 8]))
+        G = (1, 2, 4, 8)[i % 4]
+        if hkv * G > 32:
+            hkv = 32 // G
+        d = (64, 128)[(i // 4) % 2]
+        win = int(rng.choice([1, 16, 64, 257, 1024, 5000]))
+        thr = float(rng.choice([-math.inf, 0.1, 0.5, 0.9, math.inf]))
+        cases.append((lens, hkv * G, hkv, d, win, thr, bool(rng.random() < 0.5),
+                      bool(rng.random() < 0.5)))
+    return cases
+
+
+DECODE_SWEEP = _decode_sweep_cases()
+
+
+@pytest.mark.parametrize("ci", range(len(DECODE_SWEEP)),
+                         ids=[f"B{len(c[0])}_h{c[1]}-{c[2]}_d{c[3]}_w{c[4]}_thr{c[5]}"
+                              f"{'_distinct' if c[6] else ''}{'_gains' if c[7] else ''}"
+                              for c in DECODE_SWEEP])
+def test_decode_random_sweep(pk, ci):
+    lens, hq, hkv, d, win, thr, distinct, gains = DECODE_SWEEP[ci]
+    w = synth.small_workload(lens, hq, hkv, d, win, 0.0, seed=3300 + ci)
+    run_case(pk, w, thr, distinct=distinct, gains=gains, tag=f"sweep{ci}")
+
+
 def test_decode_gate_edges(pk):
     """NaN gates are never selected, a gate equal to the threshold stays local,
     and -0 / +0 compare equal."""
