@@ -57,6 +57,8 @@ def markov_burst_gate(rng: np.random.Generator, T: int, p_stay_on: float,
     """
     trans = rng.random(T)                  # float64 uniforms for the chain
     u = rng.random(T, dtype=np.float32)    # float32 uniforms for the value
+    if T == 0:
+        return np.zeros(0, dtype=np.float32)
     s = np.empty(T, dtype=np.bool_)
     state = bool(trans[0] < pi_on)
     for t in range(T):

@@ -155,6 +155,52 @@ def test_select_workloads(pk, name):
     _select_and_compare(pk, x["gate"], x["cu_seqlens"], "ratio", w.ratio, name)
 
 
+def _select_sweep_cases(n=40, seed=7171):
+    """Seeded random selections: 1-40 sequences whose lengths straddle the
+    kernel's part (4096) and chunk (32768) edges, gates uniform, logit-normal,
+    bursty, heavily tied (multiples of 1/64) or signed normal (outside
+    [0, 1]), ratio mode at a random ratio or threshold mode at a random value
+    (an exact gate value half the time, to exercise the strict comparison)."""
+    rng = np.random.default_rng(seed)
+    sizes = [0, 1, 2, 63, 64, 65, 1023, 1024, 1025, 4095, 4096, 4097, 5000, 32767, 32768,
+             32769, 70000]
+    cases = []
+    for i in range(n):
+        B = int(rng.choice([1, 1, 2, 3, 7, 40]))
+        lens = [int(t) for t in rng.choice(sizes, size=B)]
+        if B == 40:
+            lens = [min(t, 5000) for t in lens]
+        kind = ("uniform", "logit_normal", "markov_burst", "ties", "signed")[i % 5]
+        mode = "ratio" if rng.random() < 0.6 else "threshold"
+        cases.append((tuple(lens), kind, mode, float(rng.random()), int(rng.integers(1 << 30))))
+    return cases
+
+
+SELECT_SWEEP = _select_sweep_cases()
+
+
+@pytest.mark.parametrize("ci", range(len(SELECT_SWEEP)))
+def test_select_random_sweep(pk, ci):
+    lens, kind, mode, u, gseed = SELECT_SWEEP[ci]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    N = int(cu[-1])
+    rng = np.random.default_rng(gseed)
+    if kind in ("uniform", "logit_normal", "markov_burst"):
+        w = synth.small_workload(lens, 4, 4, 64, 16, 0.125, seed=gseed % 100000, gate=kind)
+        gate = synth.make_gate_only(w)["gate"]
+    elif kind == "ties":
+        gate = (rng.integers(0, 65, N) / 64.0).astype(np.float32)
+    else:
+        gate = (rng.standard_normal(N) * 2.0).astype(np.float32)
+    if mode == "ratio":
+        val = u
+    elif N and u < 0.5:
+        val = float(gate[int(u * 2 * N) % N])     # a gate value itself
+    else:
+        val = float(np.float32(u if kind != "signed" else 4.0 * u - 2.0))
+    _select_and_compare(pk, gate, cu, mode, val, f"sweep{ci}-{kind}-{mode}")
+
+
 def test_select_overflow_threshold_mode(pk):
     """Threshold mode with a small capacity: the first sel_capacity selections
     are kept, the rest are marked -1, and cu_sel still counts them all."""
