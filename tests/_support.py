@@ -82,3 +82,20 @@ def sample_rows(cu: np.ndarray, tok2sel: np.ndarray, n_sel_rows: int, n_other: i
             picks.append(np.array([cu[b], cu[b + 1] - 1, min(cu[b] + 63, cu[b + 1] - 1)]))
     r = np.unique(np.concatenate(picks)) if picks else np.zeros(0, np.int64)
     return r[(r >= 0) & (r < N)].astype(np.int32)
+
+
+def over_bar_elements(bits: np.ndarray, ref: np.ndarray, bar: float):
+    """Elements of a bf16 output (raw bits, the shape of ``ref``) more than
+    ``bar`` from the fp64 oracle, and how many of them are not a faithful
+    rounding, i.e. neither of the two bf16 values that bracket the oracle
+    value (bf16 is sign-magnitude: the fp32 value's top half truncates toward
+    zero, and the next code up is the next magnitude)."""
+    bits = np.asarray(bits, np.uint16).reshape(ref.shape)
+    got = synth.f32_from_bf16_bits(bits.reshape(-1)).reshape(ref.shape).astype(np.float64)
+    big = np.argwhere(np.abs(got - ref) > bar)
+    unfaithful = 0
+    for bi in big:
+        lo = np.uint16(np.float32(ref[tuple(bi)]).view(np.uint32) >> 16)
+        unfaithful += int(bits[tuple(bi)] not in (lo, np.uint16(lo + 1)))
+    return big, unfaithful
+

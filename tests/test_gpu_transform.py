@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 import synth
-from _support import err_stats, to_device, torch_bf16_to_f64
+from _support import err_stats, over_bar_elements, to_device, torch_bf16_to_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -174,23 +174,17 @@ QPHI_CASES = [
 ]
 
 
-@pytest.mark.parametrize("ci", range(len(QPHI_CASES)))
-def test_layer_fused_query_transform(pk, ci, fwd_launches):
-    """logo_attn_fwd_qphi: the global kernel applies LP / SO to the selected
-    queries as it loads them (Eq. branch-transform).  Against the oracle
-    layer fed with the oracle's transform of Q rounded to bf16 (the layer
-    bar), and bit for bit against the two-pass path (logo_branch_transform of
-    the selected rows, then logo_attn_fwd with that Q^G): both round the same
-    fp32 values once."""
+def _qphi_case(pk, case, seed, tag):
+    """One logo_attn_fwd_qphi call against the two-pass path (bit for bit)
+    and the oracle layer; returns the error statistics, the output's raw bits
+    and the oracle output."""
     import torch
-    seqlens, H, Hkv, d, win, ratio, kind, distinct = QPHI_CASES[ci]
-    w = synth.small_workload(seqlens, H, Hkv, d, win, ratio, seed=4200 + ci)
+    seqlens, H, Hkv, d, win, ratio, kind, distinct = case
+    w = synth.small_workload(seqlens, H, Hkv, d, win, ratio, seed=seed)
     x = synth.make_inputs(w, distinct_global=distinct)
-    rng = np.random.default_rng(4200 + ci)
+    rng = np.random.default_rng(seed)
     dev = to_device(x)
     prob = pk.Problem(dev["cu_seqlens"], H, Hkv, d, win, cu_seqlens_host=x["cu_seqlens"])
-    kw = {}
-    okw = {}
     if kind == "lp":
         AQ = rand_bf16(rng, (H, d, d), 1.0 / np.sqrt(d))
         kw = dict(A=bf16_dev(AQ))
@@ -205,6 +199,8 @@ def test_layer_fused_query_transform(pk, ci, fwd_launches):
     # distinct global keys / values: seeded inputs of their own (the query
     # transform is what this test is about)
     kg, vg = dev.get("k_g"), dev.get("v_g")
+    print(f"[layer+qphi {tag}] T={seqlens} Hq={H} Hkv={Hkv} d={d} w={win} ratio={ratio} "
+          f"{kind} distinct={distinct}", flush=True)
     out, sel_idx, cu_sel, _, _ = pk.logo_attn_fwd_qphi(prob, dev["q"], dev["k"], dev["v"],
                                                        dev["gate"], phi, ratio=ratio, k_g=kg,
                                                        v_g=vg, **kw)
@@ -215,7 +211,7 @@ def test_layer_fused_query_transform(pk, ci, fwd_launches):
     out2 = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=ratio, q_g=qg,
                             k_g=kg, v_g=vg)[0]
     torch.cuda.synchronize()
-    assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), ci
+    assert torch.equal(out.view(torch.int16), out2.view(torch.int16)), tag
 
     def rnd(a):
         return synth.bf16_bits_from_f32(a.astype(np.float32)).reshape(a.shape)
@@ -223,6 +219,62 @@ def test_layer_fused_query_transform(pk, ci, fwd_launches):
         x["q"], x["k"], x["v"], x["gate"], x["cu_seqlens"], win, ratio=ratio,
         q_g=rnd(oracle.branch_transform(x["q"], ophi, **okw)), k_g=x.get("k_g"), v_g=x.get("v_g"))
     st = err_stats(torch_bf16_to_f64(out), ref["out"])
-    print(f"[layer+qphi {kind} {ci}] " + " ".join(f"{k}={v:.3g}" for k, v in st.items()),
-          flush=True)
+    print(f"[layer+qphi {tag}] " + " ".join(f"{k}={v:.3g}" for k, v in st.items()), flush=True)
+    bits = out.view(torch.int16).cpu().numpy().view(np.uint16)[:w.total_tokens]
+    return st, bits, ref["out"]
+
+
+@pytest.mark.parametrize("ci", range(len(QPHI_CASES)))
+def test_layer_fused_query_transform(pk, ci, fwd_launches):
+    """logo_attn_fwd_qphi: the global kernel applies LP / SO to the selected
+    queries as it loads them (Eq. branch-transform).  Against the oracle
+    layer fed with the oracle's transform of Q rounded to bf16 (the layer
+    bar), and bit for bit against the two-pass path (logo_branch_transform of
+    the selected rows, then logo_attn_fwd with that Q^G): both round the same
+    fp32 values once."""
+    st, _, _ = _qphi_case(pk, QPHI_CASES[ci], 4200 + ci, f"{QPHI_CASES[ci][6]} {ci}")
     assert st["max_abs"] <= 2e-2 and st["mean_abs"] <= 2e-3
+
+
+def _qphi_sweep_cases(n=16, seed=8181):
+    """Seeded random shapes for the query transform on load: 1-3 ragged
+    sequences, each G in {1, 2, 4, 8} with each d in {64, 128} twice, LP and
+    SO alternating, windows 1-5000, ratios from 0 to 1, distinct global keys /
+    values drawn at random."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        B = int(rng.integers(1, 4))
+        lens = [int(t) for t in rng.choice([0, 1, 63, 64, 65, 255, 700, 1500, 2900], size=B)]
+        if sum(lens) == 0:
+            lens[-1] = 300
+        hkv = int(rng.choice([1, 2, 4]))
+        G = (1, 2, 4, 8)[i % 4]
+        d = (64, 128)[(i // 4) % 2]
+        win = int(rng.choice([1, 16, 64, 65, 200, 1024, 5000]))
+        r = float(rng.choice([0.0, 0.02, 0.125, 0.3, 0.75, 1.0]))
+        cases.append((tuple(lens), hkv * G, hkv, d, win, r, ("lp", "so")[i % 2],
+                      bool(rng.random() < 0.5)))
+    return cases
+
+
+QPHI_SWEEP = _qphi_sweep_cases()
+
+
+def test_layer_fused_query_transform_sweep(pk, fwd_launches):
+    """The query transform on load over the seeded sweep: bit for bit against
+    the two-pass path in every case; against the oracle, each case within the
+    mean bar, and an element above 2e-2 only as a faithful rounding of the
+    oracle value (the bf16 output spacing is 2^-5 at |out| >= 4), at most one
+    in 10^7 of the sweep's elements -- the criterion of the full-output
+    tests."""
+    total = over = 0
+    for ci, case in enumerate(QPHI_SWEEP):
+        st, bits, ref = _qphi_case(pk, case, 4400 + ci, f"sweep {ci}")
+        assert st["mean_abs"] <= 2e-3, (ci, st)
+        big, unfaithful = over_bar_elements(bits, ref, 2e-2)
+        assert unfaithful == 0, (ci, st)
+        total += ref.size
+        over += int(big.shape[0])
+    print(f"[layer+qphi sweep] {over} of {total} elements above 2e-2", flush=True)
+    assert over <= total * 1e-7
