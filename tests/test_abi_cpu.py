@@ -358,3 +358,26 @@ def test_sparse_operator_training_validation(lib):
     assert call(a6=-1) == ERR_SHAPE
     assert call(a14=need_b - 1) == ERR_WORKSPACE
     assert call(a13=ctypes.c_void_p(0x1010)) == ERR_WORKSPACE      # misaligned
+
+
+def test_header_is_c99_and_callable_from_c(lib, tmp_path):
+    """include/logo.h compiles as strict C99 (no C++ in the interface) and a
+    C program linked against liblogo.so gets the documented answers from its
+    host-side paths (tests/c/abi_from_c.c; nothing there reaches the GPU)."""
+    import shutil
+    import subprocess
+    import paper_2608_29539_amd as pk
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not found")
+    libdir = os.path.dirname(pk.library_path())
+    exe = str(tmp_path / "abi_from_c")
+    cmd = [gcc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic",
+           "-I", os.path.join(ROOT, "include"), os.path.join(ROOT, "tests", "c", "abi_from_c.c"),
+           "-L", libdir, "-llogo", f"-Wl,-rpath,{libdir}", "-o", exe]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    print(r.stdout)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "0 failure(s)" in r.stdout
