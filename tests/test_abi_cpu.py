@@ -166,6 +166,18 @@ def test_global_combine_fwd_validation(lib):
     bad = list(args)
     bad[13] = float("inf")
     assert f(*bad) == ERR_ARG
+    # the profiled entry: the five events are required, then the same checks
+    fp = lib.logo_attn_fwd_profiled
+    assert fp(*args, None) == ERR_NULL
+    ev = (ctypes.c_void_p * 5)(*([FAKE.value] * 4 + [None]))
+    assert fp(*args, ev) == ERR_NULL
+    ev = (ctypes.c_void_p * 5)(*([FAKE.value] * 5))
+    bad = list(args)
+    bad[1] = None
+    assert fp(*bad, ev) == ERR_NULL
+    bad = list(args)
+    bad[21] = need_f - 1
+    assert fp(*bad, ev) == ERR_WORKSPACE
     d = lib.logo_dense_causal_attn
     assert d(Prob(d=32).c, FAKE, FAKE, FAKE, FAKE, None) == ERR_UNSUPPORTED
     assert d(p.c, FAKE, None, FAKE, FAKE, None) == ERR_NULL

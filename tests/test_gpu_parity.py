@@ -474,6 +474,35 @@ def test_layer_random_sweep_full(pk, fwd_launches):
     assert over <= total * 1e-7
 
 
+def test_profiled_entry_matches_plain(pk, fwd_launches):
+    """logo_attn_fwd_profiled runs the same launches as logo_attn_fwd and
+    records five caller-created HIP events at the stage boundaries: the
+    output and the selection are bit-identical, every stage time is >= 0 and
+    the stage times add up to the first-to-last elapsed time."""
+    import torch
+    w = synth.small_workload((3000, 1200), 16, 4, 128, 256, 0.2, seed=1800)
+    x = synth.make_inputs(w)
+    dev = to_device(x)
+    prob = problem(pk, x, dev, w)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    for e in evs:
+        e.record()                      # creates the HIP event behind each object
+    torch.cuda.synchronize()
+    a = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=w.ratio)
+    b = pk.logo_attn_fwd(prob, dev["q"], dev["k"], dev["v"], dev["gate"], ratio=w.ratio,
+                         events=evs)
+    torch.cuda.synchronize()
+    n = int(a[2][-1])
+    assert torch.equal(a[0].view(torch.int16), b[0].view(torch.int16))
+    assert torch.equal(a[1][:n], b[1][:n]) and torch.equal(a[2], b[2])
+    assert torch.equal(a[3], b[3])
+    stages = [evs[j].elapsed_time(evs[j + 1]) for j in range(4)]
+    total = evs[0].elapsed_time(evs[4])
+    print(f"[profiled] stages ms {[round(t, 4) for t in stages]} total {total:.4f}", flush=True)
+    assert all(t >= 0.0 for t in stages)
+    assert abs(sum(stages) - total) <= 1e-3 + 1e-3 * total
+
+
 def test_layer_distinct_global_tensors(pk, fwd_launches):
     w = synth.small_workload((900, 400), 8, 2, 128, 96, 0.4, seed=1600)
     x = synth.make_inputs(w, distinct_global=True)
